@@ -1,0 +1,449 @@
+"""Pins of the CPU oracle against facts it does not compute itself.
+
+Each test fixes a part of the oracle with something outside it: published
+known-answer vectors, brute force on tiny inputs, closed forms, invariants
+the paper states, special cases that reduce to a library routine, or the
+distribution the paper's Eq. 2 demands.  No GPU is involved.
+"""
+import itertools
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _built():
+    O.build(force=False)
+
+
+# ------------------------------------------------------------- Philox ---
+
+def test_philox_known_answers():
+    """Philox4x32-10 against the published known-answer vectors."""
+    rows = [l.split() for l in open(os.path.join(GOLDEN, "philox4x32_10_kat.txt"))
+            if l.strip() and not l.startswith("#")]
+    assert len(rows) == 3
+    for r in rows:
+        v = [int(x, 16) for x in r]
+        got = O.philox4x32_10(v[0:4], v[4:6])
+        assert [int(x) for x in got] == v[6:10]
+
+
+def test_draw_uses_counter_and_key_layout():
+    """draw(seed, hop, v, j) is word 0 of Philox(ctr=(j, lo v, hi v, hop), key=(lo, hi seed))."""
+    seed = (0x12345678 << 32) | 0x9abcdef0
+    v = (7 << 32) | 3
+    got = O.draw(seed, 5, v, 11)
+    ref = O.philox4x32_10([11, 3, 7, 5], [0x9abcdef0, 0x12345678])[0]
+    assert got == int(ref)
+    # each component of the key changes the draw
+    assert O.draw(seed, 6, v, 11) != got
+    assert O.draw(seed, 5, v + 1, 11) != got
+    assert O.draw(seed, 5, v, 12) != got
+    assert O.draw(seed ^ 1, 5, v, 11) != got
+
+
+# -------------------------------------------------------- range map O4 ---
+
+@pytest.mark.parametrize("b", [1, 2, 3, 7, 10, 1000, 99991, 2**31 - 1, 2**32 - 1])
+def test_below_inverse_boundaries(b):
+    """floor(x*b/2^32): the first x mapping to t is ceil(t*2^32/b)."""
+    rng = np.random.default_rng(b)
+    ts = {0, b - 1} | set(int(t) for t in rng.integers(0, b, 50))
+    for t in ts:
+        x0 = -(-(t << 32) // b)          # ceil(t * 2^32 / b)
+        assert O.below(x0, b) == t
+        if x0 > 0:
+            assert O.below(x0 - 1, b) == t - 1
+    assert O.below(0xFFFFFFFF, b) == b - 1
+    assert O.below(0, b) == 0
+
+
+# ---------------------------------------------------------- CSR, O1 -------
+
+@pytest.mark.parametrize("seed", range(6))
+def test_csr_brute_force(seed):
+    n, u, v = W.random_graph(n=40, m=200, seed=seed)
+    csr = O.build_csr(n, u, v, symmetrize=True)
+    adj = [set() for _ in range(n)]
+    for a, b in zip(u.tolist(), v.tolist()):
+        if a != b:
+            adj[a].add(b)
+            adj[b].add(a)
+    assert csr.row_ptr[0] == 0
+    for x in range(n):
+        row = csr.col[csr.row_ptr[x]:csr.row_ptr[x + 1]].tolist()
+        assert row == sorted(adj[x])
+    assert csr.nnz % 2 == 0
+
+
+def test_csr_directed_and_edge_cases():
+    n, u, v = W.tiny_graph("isolated")
+    csr = O.build_csr(n, u, v, symmetrize=False)
+    expect = [set() for _ in range(n)]
+    for a, b in zip(u.tolist(), v.tolist()):
+        if a != b:
+            expect[a].add(b)
+    for x in range(n):
+        assert csr.col[csr.row_ptr[x]:csr.row_ptr[x + 1]].tolist() == sorted(expect[x])
+    e = O.build_csr(5, np.zeros(0, np.int32), np.zeros(0, np.int32))
+    assert e.nnz == 0 and e.row_ptr.tolist() == [0] * 6
+    with pytest.raises(ValueError):
+        O.build_csr(3, [0], [3])
+
+
+# -------------------------------------------------- degree ranking, O2 ---
+
+@pytest.mark.parametrize("r", [0.0, 0.05, 0.2, 0.5, 1.0, 1e-9, 0.999999])
+def test_rank_cache_brute_force(r):
+    n, u, v = W.random_graph(n=300, m=900, seed=3)
+    csr = O.build_csr(n, u, v)
+    deg = csr.degrees()
+    rank, slot, c = O.rank_cache(csr, r)
+    assert rank.tolist() == sorted(range(n), key=lambda x: (-int(deg[x]), x))
+    assert c == math.floor(r * n)
+    cached = [x for x in range(n) if slot[x] >= 0]
+    assert sorted(slot[cached].tolist()) == list(range(c))     # bijection onto [0, C)
+    for s in range(c):
+        assert slot[rank[s]] == s
+
+
+# ------------------------------------------------- Floyd sampler, O5 ------
+
+def _star(n):
+    _, u, v = W.tiny_graph("star") if n == 200 else (None, np.zeros(n - 1, np.int32),
+                                                       np.arange(1, n, dtype=np.int32))
+    return O.build_csr(n, u, v)
+
+
+def test_sample_node_properties():
+    n, u, v = W.random_graph(n=60, m=700, seed=9)
+    csr = O.build_csr(n, u, v)
+    for node in range(n):
+        row = csr.col[csr.row_ptr[node]:csr.row_ptr[node + 1]]
+        for k in [0, 1, 3, 5, 10, 100, -1]:
+            s = O.sample_node(csr, node, k, rng_seed=77, hop=1)
+            want = len(row) if k < 0 else min(len(row), k)
+            assert s.size == want
+            assert len(set(s.tolist())) == s.size            # distinct
+            assert set(s.tolist()) <= set(row.tolist())        # subset of the row
+            if k < 0 or len(row) <= k:
+                assert s.tolist() == row.tolist()              # whole row, CSR order
+
+
+def test_sample_subsets_uniform():
+    """Eq. 2 with fixed size: every k-subset of a deg-6 row equally likely."""
+    csr = _star(7)                     # hub 0 has neighbours 1..6
+    d, k, trials = 6, 3, 40000
+    subsets = {frozenset(c): 0 for c in itertools.combinations(range(1, d + 1), k)}
+    for t in range(trials):
+        s = O.sample_node(csr, 0, k, rng_seed=(123 << 32) | t, hop=0)
+        subsets[frozenset(s.tolist())] += 1
+    exp = trials / len(subsets)
+    chi2 = sum((c - exp) ** 2 / exp for c in subsets.values())
+    # 19 degrees of freedom: P(chi2 > 50) < 1e-4
+    assert chi2 < 50, chi2
+
+
+def test_sample_marginal_inclusion():
+    """Each neighbour of v is kept with probability k/deg (Eq. 2's indicator)."""
+    csr = _star(200)                   # hub degree 199
+    k, trials = 10, 6000
+    hits = np.zeros(200, np.int64)
+    for t in range(trials):
+        s = O.sample_node(csr, 0, k, rng_seed=t, hop=1)
+        hits[s] += 1
+    p = k / 199
+    frac = hits[1:] / trials
+    sd = math.sqrt(p * (1 - p) / trials)
+    assert np.all(np.abs(frac - p) < 5 * sd)
+    assert abs(frac.mean() - p) < 1e-12 + 5 * sd / math.sqrt(199)
+
+
+def test_sample_k1_uniform_single_draw():
+    csr = _star(9)                     # hub degree 8
+    counts = np.zeros(9, np.int64)
+    trials = 16000
+    for t in range(trials):
+        s = O.sample_node(csr, 0, 1, rng_seed=99, hop=t)
+        counts[s[0]] += 1
+    exp = trials / 8
+    chi2 = ((counts[1:] - exp) ** 2 / exp).sum()
+    assert chi2 < 30                   # 7 dof
+
+
+def test_sample_reproducible_per_node():
+    """S_h(v) depends only on (rng_seed, hop, v): same in any batch."""
+    n, u, v = W.random_graph(n=500, m=6000, seed=4)
+    csr = O.build_csr(n, u, v)
+    seed = W.rng_seed_for_batch(3)
+    b1 = O.sample_blocks(csr, [5, 17, 42], [4, 3], seed)
+    b2 = O.sample_blocks(csr, [42, 99, 5], [4, 3], seed)
+
+    def rows(b):
+        out = {}
+        for i in range(b.sizes[0]):
+            node = int(b.nodes[i])
+            out[node] = b.nbrs[0][b.indptr[0][i]:b.indptr[0][i + 1]].tolist()
+        return out
+    r1, r2 = rows(b1), rows(b2)
+    for node in (5, 42):
+        assert r1[node] == r2[node]
+        assert r1[node] == O.sample_node(csr, node, 4, seed, 0).tolist()
+
+
+# --------------------------------------------------- hop expansion, O6 ----
+
+def _check_blocks(csr, seeds, fanouts, rng_seed):
+    b = O.sample_blocks(csr, seeds, fanouts, rng_seed)
+    L = len(fanouts)
+    # F_0: seeds, first occurrences, independent dict-based build
+    f0 = list(dict.fromkeys(int(s) for s in seeds))
+    assert b.nodes[:b.sizes[0]].tolist() == f0
+    for h in range(1, L + 1):
+        n_prev, n_h = b.sizes[h - 1], b.sizes[h]
+        ip, nb, ix = b.indptr[h - 1], b.nbrs[h - 1], b.indices[h - 1]
+        assert ip.size == n_prev + 1 and ip[0] == 0
+        for i in range(n_prev):
+            node = int(b.nodes[i])
+            got = nb[ip[i]:ip[i + 1]].tolist()
+            assert got == O.sample_node(csr, node, fanouts[h - 1], rng_seed, h - 1).tolist()
+        # F_h = F_(h-1) + new ids in first-occurrence order
+        seen = dict.fromkeys(b.nodes[:n_prev].tolist())
+        for x in nb.tolist():
+            seen.setdefault(x, None)
+        assert b.nodes[:n_h].tolist() == list(seen)
+        # indices map N_h into F_h; bijection and prefix property
+        assert np.array_equal(b.nodes[ix], nb)
+        assert ix.size == 0 or (ix.min() >= 0 and ix.max() < n_h)
+        assert len(set(b.nodes[:n_h].tolist())) == n_h
+        # Eq. 12 bound (tau = 1, no overlap)
+        assert n_h <= n_prev * (1 + max(fanouts[h - 1], 0)) or fanouts[h - 1] < 0
+        assert ip[-1] <= n_prev * max(fanouts[h - 1], 0) or fanouts[h - 1] < 0
+    return b
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_blocks_random(seed):
+    n, u, v = W.random_graph(n=400, m=3000, seed=seed)
+    csr = O.build_csr(n, u, v)
+    rng = np.random.default_rng(seed)
+    seeds = rng.integers(0, n, 40).astype(np.int32)      # repeats allowed
+    _check_blocks(csr, seeds, [5, 3, 2], W.rng_seed_for_batch(seed))
+
+
+@pytest.mark.parametrize("kind", ["empty", "one_edge", "path", "star", "clique", "isolated", "deg_k"])
+def test_blocks_tiny_graphs(kind):
+    n, u, v = W.tiny_graph(kind)
+    csr = O.build_csr(n, u, v)
+    seeds = np.arange(n, dtype=np.int32)[::-1].copy()
+    _check_blocks(csr, seeds, [5, 5], 7)
+    _check_blocks(csr, seeds[:1], [1, 0, 2], 8)
+
+
+def test_blocks_full_neighbourhood_is_whole_csr():
+    """seeds = V in id order, k >= max degree: block 1 is the CSR itself."""
+    n, u, v = W.random_graph(n=150, m=700, seed=11)
+    csr = O.build_csr(n, u, v)
+    maxdeg = int(csr.degrees().max())
+    b = O.sample_blocks(csr, np.arange(n, dtype=np.int32), [maxdeg, maxdeg + 3], 1)
+    assert b.sizes == [n, n, n]
+    for h in range(2):
+        assert np.array_equal(b.indptr[h], csr.row_ptr.astype(np.int32))
+        assert np.array_equal(b.indices[h], csr.col)
+        assert np.array_equal(b.nbrs[h], csr.col)
+
+
+def test_blocks_bad_seed():
+    csr = O.build_csr(4, [0, 1], [1, 2])
+    with pytest.raises(ValueError):
+        O.sample_blocks(csr, [0, 4], [2], 1)
+
+
+# --------------------------------------------------------- gather, O7 -----
+
+def test_gather_rows_and_counts():
+    n, u, v = W.random_graph(n=200, m=1500, seed=2)
+    csr = O.build_csr(n, u, v)
+    feats = W.features(n, 7, "f32", seed=5)
+    _, slot, c = O.rank_cache(csr, 0.3)
+    ids = np.array([3, 3, 199, 0, 250, -1, 17], np.int32)
+    rows, counts = O.gather(feats, slot, ids)
+    for i, x in enumerate(ids.tolist()):
+        if 0 <= x < n:
+            assert rows[i].tobytes() == feats[x].tobytes()
+        else:
+            assert not rows[i].any()
+    valid = [x for x in ids.tolist() if 0 <= x < n]
+    assert counts.tolist() == [sum(slot[x] >= 0 for x in valid),
+                               sum(slot[x] < 0 for x in valid), 2]
+
+
+def test_gather_closed_form_hits():
+    """Seeds = V, k >= max degree: gathering N_1 hits sum of degrees of the top C."""
+    n, u, v = W.random_graph(n=300, m=2500, seed=6)
+    csr = O.build_csr(n, u, v)
+    deg = csr.degrees()
+    maxdeg = int(deg.max())
+    b = O.sample_blocks(csr, np.arange(n, dtype=np.int32), [maxdeg], 3)
+    feats = W.features(n, 4, "bf16", seed=1)
+    prev = -1
+    for r in [0.0, 0.1, 0.25, 0.5, 1.0]:
+        rank, slot, c = O.rank_cache(csr, r)
+        _, counts = O.gather(feats, slot, b.nbrs[0])
+        assert counts[0] == int(deg[rank[:c]].sum())
+        assert counts[0] + counts[1] == csr.nnz
+        assert counts[0] >= prev
+        prev = counts[0]
+    assert prev == csr.nnz
+
+
+# ------------------------------------------------------------ bf16 RNE ----
+
+def test_round_bf16_special_cases():
+    r = O.round_bf16
+    assert r(1.0) == 1.0
+    assert r(1.0 + 2**-8) == 1.0                       # tie, even below
+    assert r(1.0 + 3 * 2**-8) == 1.0 + 2**-6           # tie, even above
+    assert r(1.0 + 2**-8 + 2**-40) == 1.0 + 2**-7      # not a tie in double
+    assert r(-(1.0 + 3 * 2**-8)) == -(1.0 + 2**-6)
+    mx = (2 - 2**-7) * 2.0**127
+    assert r(mx) == mx
+    assert r(mx * (1 + 2**-9)) == mx
+    assert math.isinf(r((2 - 2**-8) * 2.0**127))       # overflow threshold
+    assert math.isinf(r(1e300)) and r(-1e300) < 0
+    assert r(2.0**-133) == 2.0**-133                   # smallest subnormal
+    assert r(2.0**-134) == 0.0                         # tie to even (zero)
+    assert r(3 * 2.0**-134) == 2.0**-132               # tie to even (2 ulps)
+    assert math.isnan(r(float("nan")))
+    assert r(0.0) == 0.0 and math.copysign(1, r(-0.0)) < 0
+
+
+def test_round_bf16_matches_library_cast():
+    """For every float32 exponent/mantissa-high pattern and every rounding
+    class of the low half, the oracle equals torch's float32 -> bfloat16."""
+    torch = pytest.importorskip("torch")
+    hi = np.arange(1 << 16, dtype=np.uint32) << 16
+    lows = np.array([0, 1, 0x3FFF, 0x7FFF, 0x8000, 0x8001, 0xC000, 0xFFFF], np.uint32)
+    bits = (hi[:, None] | lows[None, :]).ravel()
+    rng = np.random.default_rng(0)
+    bits = np.concatenate([bits, rng.integers(0, 1 << 32, 2_000_000, dtype=np.uint64).astype(np.uint32)])
+    f = bits.view(np.float32)
+    ours = O.round_bf16_array(f.astype(np.float64))
+    lib = torch.from_numpy(f.copy()).to(torch.bfloat16).to(torch.float64).numpy()
+    nan = np.isnan(f)
+    assert np.array_equal(np.isnan(ours), nan)
+    assert np.array_equal(ours[~nan], lib[~nan])
+
+
+# --------------------------------------------------- SAGE forward, O8 -----
+
+def _dense_layer(indptr, indices, X, Wt, relu):
+    """Dense brute force: A_mean (n_dst x n_src) @ X, then [X_dst | agg] @ W."""
+    n_dst = indptr.size - 1
+    A = np.zeros((n_dst, X.shape[0]))
+    for i in range(n_dst):
+        cnt = indptr[i + 1] - indptr[i]
+        for p in range(indptr[i], indptr[i + 1]):
+            A[i, indices[p]] += 1.0 / cnt
+    agg = A @ X
+    z = np.concatenate([X[:n_dst], agg], axis=1) @ Wt
+    return (np.maximum(z, 0) if relu else z), agg
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_sage_forward_dense_brute_force(seed):
+    n, u, v = W.random_graph(n=120, m=500, seed=seed)
+    csr = O.build_csr(n, u, v)
+    b = O.sample_blocks(csr, np.arange(0, n, 9, dtype=np.int32), [4, 3], 55 + seed)
+    dims = [5, 6, 3]
+    feats = W.features(n, dims[0], "f32", seed=seed)
+    H0 = O.to_f64(feats[b.nodes], "f32")
+    Ws = [O.to_f64(W.glorot(dims[l], dims[l + 1], "f32", seed + l), "f32") for l in range(2)]
+    got, trace = O.sage_forward(b, H0, Ws, keep=True)
+    X = H0
+    for l in range(1, 3):
+        hb = 2 - l + 1
+        X, agg = _dense_layer(b.indptr[hb - 1], b.indices[hb - 1], X, Ws[l - 1], relu=l < 2)
+        np.testing.assert_allclose(trace[l - 1][0], agg, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(got, X, rtol=1e-12, atol=1e-12)
+
+
+def test_sage_full_neighbourhood_is_DinvAX():
+    """Seeds = V and k >= max degree: aggregation is D^-1 A X (zero rows for isolated)."""
+    n, u, v = W.tiny_graph("isolated")
+    csr = O.build_csr(n, u, v)
+    b = O.sample_blocks(csr, np.arange(n, dtype=np.int32), [50], 1)
+    X = np.random.default_rng(1).standard_normal((n, 4))
+    Wt = np.concatenate([np.zeros((4, 4)), np.eye(4)])   # passes the aggregate
+    out = O.sage_layer(b.indptr[0], b.indices[0], X, Wt, relu=False, bf16=False, round_out=False)
+    A = np.zeros((n, n))
+    for x in range(n):
+        for y in csr.col[csr.row_ptr[x]:csr.row_ptr[x + 1]]:
+            A[x, y] = 1
+    deg = A.sum(1)
+    expect = np.divide(A @ X, deg[:, None], out=np.zeros_like(X), where=deg[:, None] > 0)
+    np.testing.assert_allclose(out, expect, rtol=1e-13, atol=0)
+    assert not out[10:].any()                          # isolated nodes -> zero rows
+
+
+def test_sage_combine_identities_and_linearity():
+    n, u, v = W.random_graph(n=50, m=300, seed=8)
+    csr = O.build_csr(n, u, v)
+    b = O.sample_blocks(csr, np.arange(0, n, 3, dtype=np.int32), [1], 9)
+    X = np.random.default_rng(2).standard_normal((b.sizes[1], 6))
+    ip, ix = b.indptr[0], b.indices[0]
+    I, Z = np.eye(6), np.zeros((6, 6))
+    self_pass = O.sage_layer(ip, ix, X, np.concatenate([I, Z]), False, False, False)
+    np.testing.assert_array_equal(self_pass, X[:ip.size - 1])
+    agg_pass = O.sage_layer(ip, ix, X, np.concatenate([Z, I]), False, False, False)
+    for i in range(ip.size - 1):                        # k = 1 copies one row exactly
+        if ip[i + 1] > ip[i]:
+            np.testing.assert_array_equal(agg_pass[i], X[ix[ip[i]]])
+        else:
+            assert not agg_pass[i].any()
+    W1 = np.random.default_rng(3).standard_normal((12, 4))
+    W2 = np.random.default_rng(4).standard_normal((12, 4))
+    a = O.sage_layer(ip, ix, X, W1, False, False, False)
+    c = O.sage_layer(ip, ix, X, W2, False, False, False)
+    s = O.sage_layer(ip, ix, X, 2 * W1 - W2, False, False, False)
+    np.testing.assert_allclose(s, 2 * a - c, rtol=1e-12, atol=1e-12)
+    r = O.sage_layer(ip, ix, X, W1, True, False, False)
+    np.testing.assert_array_equal(r, np.maximum(a, 0))
+
+
+def test_sage_bf16_rounding_points():
+    """bf16 mode rounds the aggregate and the hidden output, not the logits."""
+    n, u, v = W.random_graph(n=80, m=400, seed=12)
+    csr = O.build_csr(n, u, v)
+    b = O.sample_blocks(csr, np.arange(0, n, 4, dtype=np.int32), [3], 2)
+    X = O.to_f64(W.features(b.sizes[1], 8, "bf16", seed=3), "bf16")
+    Wt = O.to_f64(W.glorot(8, 5, "bf16", 1), "bf16")
+    ip, ix = b.indptr[0], b.indices[0]
+    z, agg = O.sage_layer(ip, ix, X, Wt, relu=True, bf16=True, round_out=True, want_agg=True)
+    np.testing.assert_array_equal(agg, O.round_bf16_array(agg))
+    np.testing.assert_array_equal(z, O.round_bf16_array(z))
+    z64, agg64 = O.sage_layer(ip, ix, X, Wt, relu=True, bf16=False, round_out=False, want_agg=True)
+    np.testing.assert_array_equal(agg, O.round_bf16_array(agg64))
+    logits = O.sage_layer(ip, ix, X, Wt, relu=False, bf16=True, round_out=False)
+    expect = np.concatenate([X[:ip.size - 1], agg], axis=1) @ Wt
+    np.testing.assert_allclose(logits, expect, rtol=1e-12, atol=1e-12)
+
+
+def test_sage_rows_subset_matches_full():
+    n, u, v = W.random_graph(n=100, m=600, seed=13)
+    csr = O.build_csr(n, u, v)
+    b = O.sample_blocks(csr, np.arange(0, n, 2, dtype=np.int32), [5], 4)
+    X = np.random.default_rng(5).standard_normal((b.sizes[1], 7))
+    Wt = np.random.default_rng(6).standard_normal((14, 3))
+    full = O.sage_layer(b.indptr[0], b.indices[0], X, Wt, True, False, False)
+    rows = np.array([0, 7, 3, 49], np.int64)
+    part = O.sage_layer(b.indptr[0], b.indices[0], X, Wt, True, False, False, rows=rows)
+    np.testing.assert_array_equal(part, full[rows])
