@@ -1,0 +1,225 @@
+"""Throughput of the sampled mini-batch step on one MI355X.
+
+A step is one mini-batch through the whole path: Eq. 2 fanout sampling with
+per-hop dedup/relabel, the cache gather of F_L's feature rows (hits from
+HBM, misses from the pinned host store), and the L-layer SAGE forward
+(mean aggregation + combine GEMM).  Seeds for every batch are staged in HBM
+before the timed region; graph, cache and weights are built once.
+
+Prints one JSON line: seeds/s over the timed steps, a roofline entry for
+the dominant device kernel (algorithmic bytes or flops per launch over its
+average HIP-event duration, measured inside the timed region), per-kernel
+figures, and the CPU oracle timed on a bounded sample of the same batches.
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "sampled seed nodes/sec through sample+gather+2-layer SAGE fwd; gather/SpMM GB/s"
+DEFAULT_WORKLOAD = "chunglu-233k-d602"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+HOST_LINK_PEAK_GBS = 64.0      # PCIe 5.0 x16, one direction
+MFMA_PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash(files) -> str:
+    h = hashlib.sha1()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2404_09544_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:12]
+
+
+KERNEL_SOURCES = {"aggregate_mean": ["spmm.hip", "common.hpp"],
+                  "gather_hit": ["gather.hip", "common.hpp", "scan.hpp"],
+                  "combine_gemm": ["gemm.hip", "common.hpp"]}
+
+
+def traffic_for(kernel: str, workload: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if still current."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_hash") != kernel_source_hash(KERNEL_SOURCES[kernel]):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--cache-fraction", type=float, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-batches", type=int, default=2)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the path is single-GPU: no sharding, no collectives)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import workloads as W
+    import paper_2404_09544_amd as G
+    from paper_2404_09544_amd.step import MiniBatchStep, to_device_weights
+
+    torch.cuda.set_device(0)
+    wl = W.Workload(args.workload)
+    r = wl.cfg["cache"] if args.cache_fraction is None else args.cache_fraction
+    t0 = time.perf_counter()
+    src, dst = wl.edges()
+    feats = wl.features()
+    log(f"inputs {wl.name}: n={wl.n} pairs={src.size} d={wl.d} {wl.dtype} ({time.perf_counter() - t0:.1f}s)")
+    t0 = time.perf_counter()
+    g = G.Graph(wl.n, src, dst, offsets_i64=wl.cfg["offsets_i64"])
+    c = G.Cache(g, feats, wl.dtype, r, store_on_device=wl.cfg["store_on_device"])
+    log(f"graph nnz={g.nnz} max_deg={g.max_degree}; cache C={c.n_cached} ld={c.ld} "
+        f"({time.perf_counter() - t0:.1f}s)")
+    ws = wl.weights()
+    step = MiniBatchStep(g, c, to_device_weights(ws, wl.dtype), wl.dims, wl.fanouts, wl.dtype)
+    n_b = args.warmup + args.steps
+    seeds_dev = [torch.from_numpy(wl.seeds(b)).cuda() for b in range(n_b)]
+    counts_hist = torch.zeros((n_b, 3), dtype=torch.int64, device="cuda")
+    sizes_hist = []
+    stream = torch.cuda.current_stream()
+
+    for b in range(args.warmup):
+        step.run(seeds_dev[b], wl.rng_seed(b), stream)
+        counts_hist[b].copy_(step.counts)
+    torch.cuda.synchronize()
+
+    G.profile_start()
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for b in range(args.warmup, n_b):
+        step.run(seeds_dev[b], wl.rng_seed(b), stream)
+        counts_hist[b].copy_(step.counts)
+        sizes_hist.append(list(step.sizes))
+    torch.cuda.synchronize()
+    t_end = time.perf_counter()
+    prof = G.profile_stop()
+    elapsed = t_end - t_start
+    ms_per_step = elapsed * 1e3 / args.steps
+    seeds_per_s = wl.batch * args.steps / elapsed
+    counts = counts_hist[args.warmup:].cpu().numpy()
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, {seeds_per_s:,.0f} seeds/s")
+
+    # ---- algorithmic work per timed batch, from the measured sizes -------
+    # Re-sampling a batch is deterministic, so the blocks of each timed batch
+    # are regenerated here (untimed) to count distinct source rows.
+    elt = 2 if wl.dtype == "bf16" else 4
+    L = wl.L
+    work = {"gather_hit": 0.0, "gather_miss": 0.0, "aggregate_mean": 0.0, "combine_gemm": 0.0,
+            "aggregate_mean_edge": 0.0}
+    probe = G.Blocks()
+    for i, b in enumerate(range(args.warmup, n_b)):
+        sz = sizes_hist[i]
+        hits, misses = int(counts[i][0]), int(counts[i][1])
+        work["gather_hit"] += hits * (2 * wl.d * elt + 8)
+        work["gather_miss"] += misses * wl.d * elt
+        G.sample(g, seeds_dev[b], wl.fanouts, wl.rng_seed(b), probe)
+        _, _, ip, _, ix = probe.to_host()
+        for l in range(1, L + 1):
+            hb = L - l + 1
+            n_dst, E = sz[hb - 1], int(ip[hb - 1][-1])
+            u = np.unique(ix[hb - 1]).size
+            din, dout = wl.dims[l - 1], wl.dims[l]
+            e_in = elt
+            e_out = elt
+            work["aggregate_mean"] += u * din * e_in + n_dst * din * e_out + 4 * (E + n_dst + 1)
+            work["aggregate_mean_edge"] += E * din * e_in + n_dst * din * e_out + 4 * (E + n_dst + 1)
+            work["combine_gemm"] += 2.0 * n_dst * (2 * din) * dout
+    probe.close()
+
+    kernels = {}
+    for name, (launches, ms) in prof.items():
+        kernels[name] = {"launches": launches, "total_ms": round(ms, 4),
+                         "avg_us": round(ms * 1e3 / max(launches, 1), 3)}
+    rows = []
+    for name, bound, peak, unit in [("gather_hit", "hbm", HBM_PEAK_GBS, "GB/s"),
+                                    ("aggregate_mean", "hbm", HBM_PEAK_GBS, "GB/s"),
+                                    ("combine_gemm", "mfma", MFMA_PEAK_TFLOPS[wl.dtype], "TFLOP/s"),
+                                    ("gather_miss", "host_link", HOST_LINK_PEAK_GBS, "GB/s")]:
+        if name not in prof:
+            continue
+        launches, ms = prof[name]
+        amount = work[name]
+        achieved = amount / (ms * 1e-3) / (1e12 if unit == "TFLOP/s" else 1e9)
+        ent = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+               "frac": round(achieved / peak, 4), "avg_us": kernels[name]["avg_us"],
+               "per_launch": amount / max(launches, 1)}
+        if name == "aggregate_mean":
+            ent["achieved_edge_effective"] = round(work["aggregate_mean_edge"] / (ms * 1e-3) / 1e9, 2)
+        kernels[name].update(ent)
+        rows.append((ms, name))
+    device_rows = [(ms, n) for ms, n in rows if kernels[n]["bound"] in ("hbm", "mfma")]
+    dom = max(device_rows)[1] if device_rows else None
+    roofline = None
+    if dom:
+        k = kernels[dom]
+        tr = traffic_for(dom, wl.name) if dom in KERNEL_SOURCES else None
+        roofline = {"kernel": dom, "bound": k["bound"], "achieved": k["achieved"], "peak": k["peak"],
+                    "unit": k["unit"], "frac": k["frac"], "traffic": tr}
+
+    # ---- CPU baseline: the oracle on a bounded sample of the same batches --
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle as O
+        t0 = time.perf_counter()
+        csr = O.build_csr(wl.n, src, dst)
+        _, slot, _ = O.rank_cache(csr, r)
+        wd = [O.to_f64(w, wl.dtype) for w in ws]
+        log(f"oracle set-up {time.perf_counter() - t0:.1f}s")
+        nb = max(1, args.cpu_batches)
+        t0 = time.perf_counter()
+        for b in range(args.warmup, args.warmup + nb):
+            ob = O.sample_blocks(csr, wl.seeds(b), wl.fanouts, wl.rng_seed(b))
+            h0, _ = O.gather(feats, slot, ob.nodes)
+            O.sage_forward(ob, O.to_f64(h0, wl.dtype), wd, bf16=wl.dtype == "bf16")
+        ct = time.perf_counter() - t0
+        cpu = {"value": round(wl.batch * nb / ct, 2), "unit": "seeds/s", "cores": 1, "kind": "oracle",
+               "sample": f"{nb} batch(es) of {wl.batch} seeds of {wl.name} (batches {args.warmup}.."
+                         f"{args.warmup + nb - 1}), single-threaded C oracle, {ct:.1f}s"}
+        log(f"oracle: {cpu['value']} seeds/s")
+
+    mean_sizes = np.mean(np.array(sizes_hist), axis=0).round(1).tolist()
+    hit_rate = float(counts[:, 0].sum() / max(counts[:, :2].sum(), 1))
+    out = {
+        "metric": METRIC, "value": round(seeds_per_s, 2), "unit": "seeds/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "n": wl.n, "nnz": g.nnz, "d": wl.d, "fanouts": wl.fanouts,
+                   "batch": wl.batch, "layers": wl.L, "dims": wl.dims, "cache_fraction": r,
+                   "store_on_device": wl.cfg["store_on_device"], "global_batch": wl.batch},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+        "batch_stats": {"mean_frontier_sizes": mean_sizes, "hit_rate": round(hit_rate, 4),
+                        "miss_bytes_per_batch": round(float(counts[:, 1].mean()) * wl.d * elt, 1)},
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,240 @@
+/* gnnav.h -- C ABI of the MI355X sampled mini-batch step for GraphSAGE-style
+ * training, as decomposed by GNNavigator (DAC'24, arXiv 2404.09544).
+ *
+ * One mini-batch (Algorithm 1, Section 2.1, forward part) is:
+ *   gnnav_sample        Eq. 2 node-wise fanout sampling plus the per-hop
+ *                       union (dedup/relabel) of the sampled frontier;
+ *   gnnav_gather        the device-cache step of Section 3.2 ("Transmission
+ *                       strategies"): cached rows read from HBM, the rest
+ *                       read from the host store over the host-device link;
+ *   gnnav_sage_forward  Eq. 1 per layer: mean Aggregate over sampled
+ *                       neighbours, then the SAGE Combine (one GEMM).
+ * gnnav_build_csr and gnnav_build_cache are one-time set-up.
+ *
+ * Conventions shared by every entry point:
+ *   - Status codes only; no C++ exception crosses this boundary.  A failing
+ *     call leaves a message readable through gnnav_last_error() (per thread,
+ *     valid until that thread's next gnnav_* call).
+ *   - `stream` is a hipStream_t passed as void*; NULL is the null stream.
+ *   - "device" pointers are HBM addresses on the current HIP device;
+ *     "host" pointers are ordinary process memory.  Row-major everywhere.
+ *   - `ld` arguments are row strides in elements.  Feature-row strides must
+ *     make every row start on a 16-byte boundary (ld * element size is a
+ *     multiple of 16 and the base pointer is 16-byte aligned).
+ *   - Handles are created by gnnav_build_* / gnnav_blocks_create and freed by
+ *     the matching *_free, which accepts NULL.  Handles copy their inputs;
+ *     callers keep ownership of every buffer they pass in.
+ */
+#ifndef GNNAV_H
+#define GNNAV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GNNAV_ABI_VERSION 1
+
+typedef enum gnnav_status {
+    GNNAV_OK = 0,
+    GNNAV_E_INVALID = 1,   /* bad argument: null pointer, bad size, bad stride */
+    GNNAV_E_RANGE = 2,     /* a node id outside [0, n) where ids must be valid */
+    GNNAV_E_NOMEM = 3,     /* host, pinned or device allocation failed */
+    GNNAV_E_CAPACITY = 4,  /* a size bound exceeds the 32-bit local-id range */
+    GNNAV_E_DEVICE = 5     /* a HIP runtime error (its text is in last_error) */
+} gnnav_status;
+
+typedef enum gnnav_dtype { GNNAV_F32 = 0, GNNAV_BF16 = 1 } gnnav_dtype;
+
+/* gnnav_build_csr flags */
+#define GNNAV_SYMMETRIZE 0x1u   /* add (v,u) for every input pair (u,v) */
+#define GNNAV_OFFSETS_I64 0x2u  /* keep row offsets as int64 on the device */
+/* gnnav_build_cache flags */
+#define GNNAV_STORE_ON_DEVICE 0x1u /* the full feature store lives in HBM */
+
+typedef struct gnnav_graph gnnav_graph;
+typedef struct gnnav_cache gnnav_cache;
+typedef struct gnnav_blocks gnnav_blocks;
+
+/* One sampled hop h (1-based): destinations F_(h-1), sources F_h. */
+typedef struct gnnav_block_view {
+    int64_t n_dst;            /* |F_(h-1)| */
+    int64_t n_src;            /* |F_h| */
+    int64_t nnz;              /* E_h, sampled edges of this hop */
+    const int32_t *indptr;    /* device, n_dst + 1: row i owns [indptr[i], indptr[i+1]) */
+    const int32_t *indices;   /* device, nnz: local ids in [0, n_src) */
+    const int32_t *neighbors; /* device, nnz: the same edges as global node ids */
+    const int32_t *src_ids;   /* device, n_src: global ids of F_h (prefix of the node list) */
+} gnnav_block_view;
+
+/* Message of this thread's last failing call ("" if none). */
+const char *gnnav_last_error(void);
+
+/* GNNAV_ABI_VERSION of the loaded library. */
+int32_t gnnav_abi_version(void);
+
+/* ---------------------------------------------------------------- graph ---
+ * Graph G(V, E) of Algorithm 1's input, as CSR in HBM.
+ * src, dst: host arrays of n_edges node ids in [0, n_nodes).  Self pairs are
+ * dropped, repeated pairs kept once, and with GNNAV_SYMMETRIZE each pair is
+ * stored in both directions.  Each row lists its neighbours in ascending id
+ * order.  Offsets are int32 unless GNNAV_OFFSETS_I64 is set or nnz needs
+ * more; column ids are int32.
+ * Errors: E_INVALID (null pointers with n_edges > 0, n_nodes < 0 or
+ * > INT32_MAX, out == NULL), E_RANGE (an endpoint outside [0, n_nodes)),
+ * E_NOMEM, E_DEVICE.  On error *out is left unchanged.                    */
+gnnav_status gnnav_build_csr(int64_t n_nodes, int64_t n_edges, const int32_t *src,
+                             const int32_t *dst, uint32_t flags, gnnav_graph **out);
+
+/* Sizes of a graph; any output pointer may be NULL. */
+gnnav_status gnnav_graph_info(const gnnav_graph *g, int64_t *n_nodes, int64_t *nnz,
+                              int64_t *max_degree, int32_t *offsets_i64);
+
+/* Host copies of the CSR: row_ptr (int64, n_nodes+1 entries) and col
+ * (int32, nnz entries), caller-allocated.  For tests and tooling.        */
+gnnav_status gnnav_graph_csr_host(const gnnav_graph *g, int64_t *row_ptr, int32_t *col);
+
+void gnnav_graph_free(gnnav_graph *g);
+
+/* ---------------------------------------------------------------- cache ---
+ * Static device feature cache in front of a pinned host feature store
+ * (Section 3.2, "Transmission strategies", with the cache-update policy
+ * disabled and a cache ratio, as in the PaGraph template of Section 3.2 and
+ * the static-cache baseline of Section 4.1).
+ * feats_host: n_nodes x d row-major (n_nodes of g), float32 or bfloat16 bit
+ * patterns.  The C = floor(cache_fraction * n_nodes) vertices of largest
+ * degree (ties: smaller id first) get cache slots 0..C-1 in that order and
+ * their rows are copied into HBM.  Every row is also copied into a pinned,
+ * device-mapped host store (or an HBM store with GNNAV_STORE_ON_DEVICE).
+ * Rows in both are padded with zeros to a 16-byte stride (see cache_info).
+ * Errors: E_INVALID (null pointers, d <= 0, cache_fraction outside [0, 1]
+ * or NaN, bad dtype), E_NOMEM, E_DEVICE.  On error *out is unchanged.     */
+gnnav_status gnnav_build_cache(const gnnav_graph *g, const void *feats_host, int64_t d,
+                               gnnav_dtype dt, double cache_fraction, uint32_t flags,
+                               gnnav_cache **out);
+
+/* Cache geometry; any output pointer may be NULL.  ld is the padded row
+ * stride in elements used by the cache and the store.                   */
+gnnav_status gnnav_cache_info(const gnnav_cache *c, int64_t *n_cached, int64_t *d, int64_t *ld,
+                              int32_t *dtype, int32_t *store_on_device);
+
+/* Host copy of the slot map (int32[n_nodes]: slot, or -1 if not cached). */
+gnnav_status gnnav_cache_slot_map_host(const gnnav_cache *c, int32_t *slot_map);
+
+void gnnav_cache_free(gnnav_cache *c);
+
+/* --------------------------------------------------------------- sample ---
+ * Blocks: device workspace that receives the sampled frontiers and hops.
+ * It grows on demand and is reused across calls (no per-batch allocation
+ * once it has reached the largest batch's size).                          */
+gnnav_status gnnav_blocks_create(gnnav_blocks **out);
+void gnnav_blocks_free(gnnav_blocks *b);
+
+/* Eq. 2 node-wise sampling for n_hops hops plus the union of each hop.
+ * seeds_dev: device int32[n_seeds], the target vertices B^0 (repeats are
+ * dropped, first occurrence kept).  fanouts: host int32[n_hops]; fanouts[0]
+ * applies to the seeds; k < 0 takes every neighbour.  For each node v of
+ * F_(h-1) (every node, including ones reached earlier): if deg(v) <= k the
+ * whole row, else k distinct neighbours by Floyd's selection whose draws
+ * are Philox4x32-10 word 0 with key (lo32, hi32 of rng_seed) and counter
+ * (slot j, lo32 v, hi32 v, h-1), each mapped to [0, m] as floor(x*(m+1)/2^32).
+ * F_h is F_(h-1) followed by the new ids in order of first occurrence.
+ * Results stay on the device in `blocks` (see gnnav_blocks_hop/_nodes);
+ * they are valid until the next gnnav_sample on the same blocks.  The call
+ * enqueues its kernels on `stream` and synchronises that stream once at the
+ * end to publish the per-hop sizes to the host.
+ * Errors: E_INVALID (null pointers, n_hops < 1 or > 16, n_seeds < 0),
+ * E_CAPACITY (an Eq. 12 bound exceeds INT32_MAX), E_RANGE (a seed outside
+ * [0, n); the blocks' contents are then unspecified but reusable),
+ * E_NOMEM, E_DEVICE.                                                      */
+gnnav_status gnnav_sample(const gnnav_graph *g, const int32_t *seeds_dev, int64_t n_seeds,
+                          const int32_t *fanouts, int32_t n_hops, uint64_t rng_seed,
+                          gnnav_blocks *blocks, void *stream);
+
+/* View of hop h (1..n_hops) of the last gnnav_sample. */
+gnnav_status gnnav_blocks_hop(const gnnav_blocks *b, int32_t hop, gnnav_block_view *out);
+
+/* All frontiers: *nodes_dev = device int32 list whose first n_per_hop[h]
+ * entries are F_h; n_per_hop receives n_hops+1 sizes (host int64 array,
+ * caller-allocated, may be NULL); *n_hops receives L (may be NULL).       */
+gnnav_status gnnav_blocks_nodes(const gnnav_blocks *b, const int32_t **nodes_dev,
+                                int64_t *n_per_hop, int32_t *n_hops);
+
+/* --------------------------------------------------------------- gather ---
+ * Section 3.2's cache step for n_ids requested vertices: out row i (device,
+ * stride ld_out elements of the cache dtype) becomes the feature row of
+ * ids_dev[i].  Cached vertices are copied from HBM; the rest are read from
+ * the host store by zero-copy loads over the host-device link, on a second
+ * stream that joins `stream` before the call's work completes.  Each row
+ * copies ceil(d * elt / 16) 16-byte units: the columns from d up to the
+ * next 16-byte boundary are written with zeros; later columns are untouched.
+ * An id outside [0, n) gives a zero row and counts as invalid.
+ * counts_dev: device int64[3] receiving {hits, misses, invalid}; overwritten.
+ * Asynchronous with respect to the host.
+ * Errors: E_INVALID (null pointers with n_ids > 0, ld_out < d, row stride
+ * not a multiple of 16 bytes or out_dev not 16-byte aligned), E_NOMEM,
+ * E_DEVICE.                                                               */
+gnnav_status gnnav_gather(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_ids,
+                          void *out_dev, int64_t ld_out, int64_t *counts_dev, void *stream);
+
+/* ------------------------------------------------------- SAGE, per layer ---
+ * Eq. 1 Aggregate, GraphSAGE mean: for each destination row i < n_dst,
+ * out[i] = (1/cnt_i) * sum over p in [indptr[i], indptr[i+1]) of
+ * x[indices[p]], or zeros when the row is empty.  fp32 accumulation in CSR
+ * order; bf16 inputs give bf16 outputs rounded to nearest-even.  x and out
+ * are device matrices with strides ld_x, ld_out (16-byte row alignment);
+ * columns from d up to the next 16-byte boundary of out are written with
+ * zeros.  indptr/indices are device int32 (a block of gnnav_sample or any
+ * CSR whose indices are valid rows of x).
+ * Errors: E_INVALID (null pointers with n_dst > 0, d <= 0, strides < d or
+ * misaligned), E_DEVICE.  Asynchronous.                                   */
+gnnav_status gnnav_aggregate_mean(const int32_t *indptr_dev, const int32_t *indices_dev,
+                                  int64_t n_dst, const void *x_dev, int64_t ld_x, int64_t d,
+                                  gnnav_dtype dt, void *out_dev, int64_t ld_out, void *stream);
+
+/* Eq. 1 Combine for SAGE: out = act(self * W[0:d_in] + agg * W[d_in:2*d_in])
+ * for m rows, with W row-major [2*d_in, d_out] (device), self and agg
+ * device [m x d_in] with strides ld_self, ld_agg.  act is ReLU when relu is
+ * nonzero.  dt = F32: fp32 operands, fp32 MFMA, fp32 output.  dt = BF16:
+ * bf16 operands, fp32 accumulation, output bf16 (nearest-even) when
+ * out_bf16 is nonzero, else fp32.  The concatenation [self | agg] is never
+ * formed.  Errors: E_INVALID (null pointers with m > 0, d_in or d_out <= 0,
+ * strides too small), E_DEVICE.  Asynchronous.                            */
+gnnav_status gnnav_combine(const void *self_dev, int64_t ld_self, const void *agg_dev,
+                           int64_t ld_agg, int64_t m, int64_t d_in, const void *w_dev,
+                           int64_t d_out, gnnav_dtype dt, int32_t relu, int32_t out_bf16,
+                           void *out_dev, int64_t ld_out, void *stream);
+
+/* ---------------------------------------------------------- SAGE forward ---
+ * Algorithm 1, lines 4-6 (forward only): n_layers = L of the last
+ * gnnav_sample on `b`.  Layer l (1-based) runs on hop b = L-l+1:
+ * destinations F_(b-1), sources F_b; it aggregates (mean) and combines with
+ * W_dev[l-1] (device, row-major [2*dims[l-1], dims[l]]), applies ReLU for
+ * l < L.  x_dev holds the n_L input rows of F_L (stride ld_x, dims[0]
+ * used), e.g. the output of gnnav_gather on F_L.  logits_dev receives the
+ * |F_0| x dims[L] fp32 result (stride ld_out).  dt = BF16 keeps features,
+ * weights, aggregates and hidden layers in bfloat16 (fp32 accumulation);
+ * the logits stay fp32.  Intermediate buffers live in `b` and are reused.
+ * Errors: E_INVALID (null pointers, n_layers differs from the sampled
+ * hops, dims <= 0, strides), E_NOMEM, E_DEVICE.  Asynchronous.            */
+gnnav_status gnnav_sage_forward(gnnav_blocks *b, const void *x_dev, int64_t ld_x,
+                                const void *const *W_dev, const int32_t *dims, int32_t n_layers,
+                                gnnav_dtype dt, float *logits_dev, int64_t ld_out, void *stream);
+
+/* ------------------------------------------------------------ profiling ---
+ * Per-kernel timing with HIP events recorded around every kernel launch on
+ * the stream it is launched on.  profile_start clears the table and turns
+ * recording on; profile_stop synchronises the device, resolves the events
+ * and turns recording off.  Entries are read by index.                    */
+gnnav_status gnnav_profile_start(void);
+gnnav_status gnnav_profile_stop(void);
+int32_t gnnav_profile_count(void);
+gnnav_status gnnav_profile_get(int32_t i, char *name, int32_t name_cap, int64_t *launches,
+                               double *total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GNNAV_H */

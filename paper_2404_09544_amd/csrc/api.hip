@@ -1,0 +1,700 @@
+// C ABI of the sampled mini-batch step (declarations and contracts in
+// include/gnnav.h): handles, argument checks, one-time set-up on the host
+// (CSR build, degree ranking, pinned store), and the per-batch
+// orchestration that enqueues the kernels of sample.hip, gather.hip,
+// spmm.hip and gemm.hip.
+#include <algorithm>
+#include <functional>
+#include <cmath>
+#include <cstring>
+#include <mutex>
+#include <thread>
+
+#include "common.hpp"
+#include "scan.hpp"
+
+using namespace gnnav;
+
+// ------------------------------------------------------------------ errors
+namespace gnnav {
+static thread_local std::string t_last_error;
+void set_last_error(const std::string &msg) { t_last_error = msg; }
+}  // namespace gnnav
+
+extern "C" const char *gnnav_last_error(void) { return t_last_error.c_str(); }
+extern "C" int32_t gnnav_abi_version(void) { return GNNAV_ABI_VERSION; }
+
+// ---------------------------------------------------------- device buffer
+void DevBuf::ensure(size_t need, hipStream_t stream) {
+    if (need <= bytes && p) return;
+    if (p) {
+        GNNAV_HIP(hipStreamSynchronize(stream));
+        GNNAV_HIP(hipFree(p));
+        p = nullptr;
+        bytes = 0;
+    }
+    size_t b = need < 256 ? 256 : need;
+    b += b / 8;  // headroom so slowly growing batches do not reallocate every time
+    if (hipMalloc(&p, b) != hipSuccess) {
+        (void)hipGetLastError();
+        p = nullptr;
+        fail(GNNAV_E_NOMEM, "device allocation of " + std::to_string(b) + " bytes failed");
+    }
+    bytes = b;
+}
+void DevBuf::release() {
+    if (p) (void)hipFree(p);
+    p = nullptr;
+    bytes = 0;
+}
+
+// -------------------------------------------------------------- profiling
+namespace {
+struct ProfEntry {
+    std::string name;
+    int64_t launches = 0;
+    double ms = 0;
+};
+struct Pending {
+    int slot;
+    hipEvent_t a, b;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<ProfEntry> g_prof;
+std::vector<Pending> g_pending;
+std::vector<hipEvent_t> g_event_pool;
+
+hipEvent_t take_event() {
+    if (!g_event_pool.empty()) {
+        hipEvent_t e = g_event_pool.back();
+        g_event_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e;
+    GNNAV_HIP(hipEventCreate(&e));
+    return e;
+}
+}  // namespace
+
+namespace gnnav {
+bool profiling_on() { return g_prof_on; }
+
+KernelTimer::KernelTimer(const char *name, hipStream_t s) : stream(s) {
+    if (!g_prof_on) return;
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    int idx = -1;
+    for (size_t i = 0; i < g_prof.size(); ++i)
+        if (g_prof[i].name == name) idx = (int)i;
+    if (idx < 0) {
+        g_prof.push_back(ProfEntry{name, 0, 0});
+        idx = (int)g_prof.size() - 1;
+    }
+    Pending p{idx, take_event(), take_event()};
+    GNNAV_HIP(hipEventRecord(p.a, s));
+    g_pending.push_back(p);
+    slot = (int)g_pending.size() - 1;
+}
+KernelTimer::~KernelTimer() {
+    if (slot < 0) return;
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    (void)hipEventRecord(g_pending[slot].b, stream);
+    g_prof[g_pending[slot].slot].launches++;
+}
+}  // namespace gnnav
+
+extern "C" gnnav_status gnnav_profile_start(void) {
+    return guarded([&] {
+        GNNAV_HIP(hipDeviceSynchronize());
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        for (auto &p : g_pending) {
+            g_event_pool.push_back(p.a);
+            g_event_pool.push_back(p.b);
+        }
+        g_pending.clear();
+        g_prof.clear();
+        g_prof_on = true;
+    });
+}
+
+extern "C" gnnav_status gnnav_profile_stop(void) {
+    return guarded([&] {
+        GNNAV_HIP(hipDeviceSynchronize());
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        g_prof_on = false;
+        for (auto &p : g_pending) {
+            float ms = 0;
+            GNNAV_HIP(hipEventElapsedTime(&ms, p.a, p.b));
+            g_prof[p.slot].ms += ms;
+            g_event_pool.push_back(p.a);
+            g_event_pool.push_back(p.b);
+        }
+        g_pending.clear();
+    });
+}
+
+extern "C" int32_t gnnav_profile_count(void) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    return (int32_t)g_prof.size();
+}
+
+extern "C" gnnav_status gnnav_profile_get(int32_t i, char *name, int32_t name_cap, int64_t *launches,
+                                          double *total_ms) {
+    return guarded([&] {
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        GNNAV_CHECK(i >= 0 && i < (int32_t)g_prof.size(), GNNAV_E_INVALID, "profile index out of range");
+        if (name && name_cap > 0) {
+            std::strncpy(name, g_prof[i].name.c_str(), (size_t)name_cap - 1);
+            name[name_cap - 1] = 0;
+        }
+        if (launches) *launches = g_prof[i].launches;
+        if (total_ms) *total_ms = g_prof[i].ms;
+    });
+}
+
+// ------------------------------------------------------------------ graph
+struct gnnav_graph {
+    int64_t n = 0, nnz = 0, max_deg = 0;
+    bool i64 = false;
+    std::vector<int64_t> row_ptr_host;
+    DevBuf row_ptr, col;
+};
+
+static void parallel_for(int64_t n, const std::function<void(int64_t, int64_t)> &fn) {
+    unsigned hw = std::thread::hardware_concurrency();
+    int64_t T = std::max<int64_t>(1, std::min<int64_t>(hw ? hw : 1, 16));
+    if (n < 100000) T = 1;
+    std::vector<std::thread> th;
+    for (int64_t t = 0; t < T; ++t) {
+        int64_t b = n * t / T, e = n * (t + 1) / T;
+        if (t == T - 1)
+            fn(b, e);
+        else
+            th.emplace_back(fn, b, e);
+    }
+    for (auto &x : th) x.join();
+}
+
+extern "C" gnnav_status gnnav_build_csr(int64_t n_nodes, int64_t n_edges, const int32_t *src,
+                                        const int32_t *dst, uint32_t flags, gnnav_graph **out) {
+    return guarded([&] {
+        GNNAV_CHECK(out, GNNAV_E_INVALID, "out is NULL");
+        GNNAV_CHECK(n_nodes >= 0 && n_nodes <= INT32_MAX, GNNAV_E_INVALID, "n_nodes outside [0, INT32_MAX]");
+        GNNAV_CHECK(n_edges >= 0, GNNAV_E_INVALID, "n_edges < 0");
+        GNNAV_CHECK(n_edges == 0 || (src && dst), GNNAV_E_INVALID, "src/dst NULL");
+        const bool sym = flags & GNNAV_SYMMETRIZE;
+        for (int64_t i = 0; i < n_edges; ++i)
+            GNNAV_CHECK(src[i] >= 0 && src[i] < n_nodes && dst[i] >= 0 && dst[i] < n_nodes, GNNAV_E_RANGE,
+                        "edge " + std::to_string(i) + " has an endpoint outside [0, n_nodes)");
+        // bucket the arcs by source row (counting sort), then sort + dedup each row
+        std::vector<int64_t> rp(n_nodes + 1, 0);
+        for (int64_t i = 0; i < n_edges; ++i) {
+            if (src[i] == dst[i]) continue;
+            rp[src[i] + 1]++;
+            if (sym) rp[dst[i] + 1]++;
+        }
+        for (int64_t v = 0; v < n_nodes; ++v) rp[v + 1] += rp[v];
+        std::vector<int32_t> col(std::max<int64_t>(rp[n_nodes], 1));
+        {
+            std::vector<int64_t> fill(rp.begin(), rp.end() - 1);
+            for (int64_t i = 0; i < n_edges; ++i) {
+                if (src[i] == dst[i]) continue;
+                col[fill[src[i]]++] = dst[i];
+                if (sym) col[fill[dst[i]]++] = src[i];
+            }
+        }
+        std::vector<int64_t> kept(n_nodes + 1, 0);
+        parallel_for(n_nodes, [&](int64_t b, int64_t e) {
+            for (int64_t v = b; v < e; ++v) {
+                int32_t *r0 = col.data() + rp[v], *r1 = col.data() + rp[v + 1];
+                std::sort(r0, r1);
+                kept[v + 1] = std::unique(r0, r1) - r0;
+            }
+        });
+        auto *g = new gnnav_graph();
+        try {
+            g->n = n_nodes;
+            g->row_ptr_host.assign(n_nodes + 1, 0);
+            for (int64_t v = 0; v < n_nodes; ++v) {
+                g->row_ptr_host[v + 1] = g->row_ptr_host[v] + kept[v + 1];
+                g->max_deg = std::max<int64_t>(g->max_deg, kept[v + 1]);
+            }
+            g->nnz = g->row_ptr_host[n_nodes];
+            for (int64_t v = 0, o = 0; v < n_nodes; ++v) {  // compact rows in place (o <= rp[v])
+                std::memmove(col.data() + o, col.data() + rp[v], (size_t)kept[v + 1] * sizeof(int32_t));
+                o += kept[v + 1];
+            }
+            g->i64 = (flags & GNNAV_OFFSETS_I64) || g->nnz > INT32_MAX;
+            hipStream_t s0 = nullptr;
+            if (g->i64) {
+                g->row_ptr.ensure((n_nodes + 1) * sizeof(int64_t), s0);
+                GNNAV_HIP(hipMemcpy(g->row_ptr.p, g->row_ptr_host.data(), (n_nodes + 1) * sizeof(int64_t),
+                                    hipMemcpyHostToDevice));
+            } else {
+                std::vector<int32_t> r32(g->row_ptr_host.begin(), g->row_ptr_host.end());
+                g->row_ptr.ensure((n_nodes + 1) * sizeof(int32_t), s0);
+                GNNAV_HIP(hipMemcpy(g->row_ptr.p, r32.data(), (n_nodes + 1) * sizeof(int32_t),
+                                    hipMemcpyHostToDevice));
+            }
+            g->col.ensure(std::max<int64_t>(g->nnz, 1) * sizeof(int32_t), s0);
+            if (g->nnz > 0)
+                GNNAV_HIP(hipMemcpy(g->col.p, col.data(), g->nnz * sizeof(int32_t), hipMemcpyHostToDevice));
+        } catch (...) {
+            g->row_ptr.release();
+            g->col.release();
+            delete g;
+            throw;
+        }
+        *out = g;
+    });
+}
+
+extern "C" gnnav_status gnnav_graph_info(const gnnav_graph *g, int64_t *n_nodes, int64_t *nnz,
+                                         int64_t *max_degree, int32_t *offsets_i64) {
+    return guarded([&] {
+        GNNAV_CHECK(g, GNNAV_E_INVALID, "graph is NULL");
+        if (n_nodes) *n_nodes = g->n;
+        if (nnz) *nnz = g->nnz;
+        if (max_degree) *max_degree = g->max_deg;
+        if (offsets_i64) *offsets_i64 = g->i64 ? 1 : 0;
+    });
+}
+
+extern "C" gnnav_status gnnav_graph_csr_host(const gnnav_graph *g, int64_t *row_ptr, int32_t *col) {
+    return guarded([&] {
+        GNNAV_CHECK(g && row_ptr && col, GNNAV_E_INVALID, "NULL argument");
+        std::memcpy(row_ptr, g->row_ptr_host.data(), (g->n + 1) * sizeof(int64_t));
+        if (g->nnz > 0) GNNAV_HIP(hipMemcpy(col, g->col.p, g->nnz * sizeof(int32_t), hipMemcpyDeviceToHost));
+    });
+}
+
+extern "C" void gnnav_graph_free(gnnav_graph *g) {
+    if (!g) return;
+    (void)hipDeviceSynchronize();
+    g->row_ptr.release();
+    g->col.release();
+    delete g;
+}
+
+// ------------------------------------------------------------------ cache
+struct gnnav_cache {
+    int64_t n = 0, c = 0, d = 0, ld = 0, elt = 4;
+    gnnav_dtype dt = GNNAV_F32;
+    bool store_on_device = false;
+    DevBuf slot_map, cache_rows, store_dev;
+    void *store_host = nullptr;       // pinned, device-mapped
+    void *store_ptr = nullptr;        // device-visible address of the store
+    std::vector<int32_t> slot_host;
+    hipStream_t side = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+    DevBuf hit_list, miss_list, part, dev_counts;
+};
+
+static void free_cache(gnnav_cache *c) {
+    if (!c) return;
+    (void)hipDeviceSynchronize();
+    c->slot_map.release();
+    c->cache_rows.release();
+    c->store_dev.release();
+    c->hit_list.release();
+    c->miss_list.release();
+    c->part.release();
+    c->dev_counts.release();
+    if (c->store_host) (void)hipHostFree(c->store_host);
+    if (c->side) (void)hipStreamDestroy(c->side);
+    if (c->fork) (void)hipEventDestroy(c->fork);
+    if (c->join) (void)hipEventDestroy(c->join);
+    delete c;
+}
+
+// Copy rows ids[0..count) (or rows 0..count) of the padded host image into
+// device memory through a pinned staging buffer.
+static void upload_rows(void *dst_dev, const uint8_t *feats, int64_t row_bytes, int64_t pitch,
+                        const int32_t *ids, int64_t count) {
+    if (count <= 0) return;
+    const int64_t chunk_rows = std::max<int64_t>(1, (64 << 20) / pitch);
+    void *stage = nullptr;
+    GNNAV_HIP(hipHostMalloc(&stage, (size_t)(chunk_rows * pitch), hipHostMallocDefault));
+    try {
+        for (int64_t r0 = 0; r0 < count; r0 += chunk_rows) {
+            const int64_t rn = std::min(chunk_rows, count - r0);
+            uint8_t *sp = (uint8_t *)stage;
+            std::memset(sp, 0, (size_t)(rn * pitch));
+            for (int64_t i = 0; i < rn; ++i) {
+                const int64_t v = ids ? ids[r0 + i] : r0 + i;
+                std::memcpy(sp + i * pitch, feats + v * row_bytes, (size_t)row_bytes);
+            }
+            GNNAV_HIP(hipMemcpy((uint8_t *)dst_dev + r0 * pitch, stage, (size_t)(rn * pitch),
+                                hipMemcpyHostToDevice));
+        }
+    } catch (...) {
+        (void)hipHostFree(stage);
+        throw;
+    }
+    GNNAV_HIP(hipHostFree(stage));
+}
+
+extern "C" gnnav_status gnnav_build_cache(const gnnav_graph *g, const void *feats_host, int64_t d, gnnav_dtype dt,
+                                          double cache_fraction, uint32_t flags, gnnav_cache **out) {
+    return guarded([&] {
+        GNNAV_CHECK(g && out, GNNAV_E_INVALID, "NULL graph or out");
+        GNNAV_CHECK(d > 0, GNNAV_E_INVALID, "d must be positive");
+        GNNAV_CHECK(dt == GNNAV_F32 || dt == GNNAV_BF16, GNNAV_E_INVALID, "dtype must be F32 or BF16");
+        GNNAV_CHECK(cache_fraction >= 0.0 && cache_fraction <= 1.0, GNNAV_E_INVALID,
+                    "cache_fraction outside [0, 1]");
+        GNNAV_CHECK(g->n == 0 || feats_host, GNNAV_E_INVALID, "feats_host is NULL");
+        auto *c = new gnnav_cache();
+        try {
+            c->n = g->n;
+            c->d = d;
+            c->dt = dt;
+            c->elt = dt == GNNAV_BF16 ? 2 : 4;
+            const int64_t row_bytes = d * c->elt;
+            const int64_t pitch = (row_bytes + 15) / 16 * 16;
+            c->ld = pitch / c->elt;
+            c->store_on_device = flags & GNNAV_STORE_ON_DEVICE;
+            // degree ranking: degree descending, id ascending (counting sort)
+            const int64_t n = g->n;
+            std::vector<int64_t> bucket(g->max_deg + 2, 0);
+            for (int64_t v = 0; v < n; ++v) bucket[g->max_deg - (g->row_ptr_host[v + 1] - g->row_ptr_host[v]) + 1]++;
+            for (size_t i = 1; i < bucket.size(); ++i) bucket[i] += bucket[i - 1];
+            std::vector<int32_t> rank(std::max<int64_t>(n, 1));
+            for (int64_t v = 0; v < n; ++v)
+                rank[bucket[g->max_deg - (g->row_ptr_host[v + 1] - g->row_ptr_host[v])]++] = (int32_t)v;
+            int64_t C = (int64_t)std::floor(cache_fraction * (double)n);
+            C = std::max<int64_t>(0, std::min<int64_t>(C, n));
+            c->c = C;
+            c->slot_host.assign(n, -1);
+            for (int64_t s = 0; s < C; ++s) c->slot_host[rank[s]] = (int32_t)s;
+            hipStream_t s0 = nullptr;
+            c->slot_map.ensure(std::max<int64_t>(n, 1) * sizeof(int32_t), s0);
+            if (n > 0)
+                GNNAV_HIP(hipMemcpy(c->slot_map.p, c->slot_host.data(), n * sizeof(int32_t), hipMemcpyHostToDevice));
+            const uint8_t *feats = (const uint8_t *)feats_host;
+            c->cache_rows.ensure(std::max<int64_t>(C, 1) * pitch, s0);
+            upload_rows(c->cache_rows.p, feats, row_bytes, pitch, rank.data(), C);
+            if (c->store_on_device) {
+                c->store_dev.ensure(std::max<int64_t>(n, 1) * pitch, s0);
+                upload_rows(c->store_dev.p, feats, row_bytes, pitch, nullptr, n);
+                c->store_ptr = c->store_dev.p;
+            } else {
+                const size_t bytes = (size_t)std::max<int64_t>(n, 1) * pitch;
+                if (hipHostMalloc(&c->store_host, bytes, hipHostMallocMapped) != hipSuccess) {
+                    (void)hipGetLastError();
+                    c->store_host = nullptr;
+                    fail(GNNAV_E_NOMEM, "pinned host store of " + std::to_string(bytes) + " bytes failed");
+                }
+                uint8_t *hp = (uint8_t *)c->store_host;
+                parallel_for(n, [&](int64_t b, int64_t e) {
+                    for (int64_t v = b; v < e; ++v) {
+                        std::memcpy(hp + v * pitch, feats + v * row_bytes, (size_t)row_bytes);
+                        std::memset(hp + v * pitch + row_bytes, 0, (size_t)(pitch - row_bytes));
+                    }
+                });
+                GNNAV_HIP(hipHostGetDevicePointer(&c->store_ptr, c->store_host, 0));
+            }
+            GNNAV_HIP(hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking));
+            GNNAV_HIP(hipEventCreateWithFlags(&c->fork, hipEventDisableTiming));
+            GNNAV_HIP(hipEventCreateWithFlags(&c->join, hipEventDisableTiming));
+            c->dev_counts.ensure(2 * sizeof(int32_t), s0);
+        } catch (...) {
+            free_cache(c);
+            throw;
+        }
+        *out = c;
+    });
+}
+
+extern "C" gnnav_status gnnav_cache_info(const gnnav_cache *c, int64_t *n_cached, int64_t *d, int64_t *ld,
+                                         int32_t *dtype, int32_t *store_on_device) {
+    return guarded([&] {
+        GNNAV_CHECK(c, GNNAV_E_INVALID, "cache is NULL");
+        if (n_cached) *n_cached = c->c;
+        if (d) *d = c->d;
+        if (ld) *ld = c->ld;
+        if (dtype) *dtype = (int32_t)c->dt;
+        if (store_on_device) *store_on_device = c->store_on_device ? 1 : 0;
+    });
+}
+
+extern "C" gnnav_status gnnav_cache_slot_map_host(const gnnav_cache *c, int32_t *slot_map) {
+    return guarded([&] {
+        GNNAV_CHECK(c && slot_map, GNNAV_E_INVALID, "NULL argument");
+        std::memcpy(slot_map, c->slot_host.data(), c->n * sizeof(int32_t));
+    });
+}
+
+extern "C" void gnnav_cache_free(gnnav_cache *c) { free_cache(c); }
+
+// ----------------------------------------------------------------- blocks
+namespace {
+constexpr int kMaxHops = 16;
+constexpr int kSizeN = 0;         // sizes[kSizeN + h] = |F_h|
+constexpr int kSizeE = 17;        // sizes[kSizeE + h] = E_h (h >= 1)
+constexpr int kSizeErr = 40;      // out-of-range seed count
+constexpr int kSizeSlots = 48;
+}  // namespace
+
+struct gnnav_blocks {
+    int32_t L = 0;
+    int64_t n_h[kMaxHops + 1] = {0};
+    int64_t e_h[kMaxHops + 1] = {0};
+    int64_t map_nodes = -1;
+    DevBuf map, sizes, nodes, part;
+    DevBuf indptr[kMaxHops], nbrs[kMaxHops], indices[kMaxHops];
+    int32_t *sizes_host = nullptr;  // pinned mirror of `sizes`
+    DevBuf agg, hid[2];             // forward workspace
+};
+
+extern "C" gnnav_status gnnav_blocks_create(gnnav_blocks **out) {
+    return guarded([&] {
+        GNNAV_CHECK(out, GNNAV_E_INVALID, "out is NULL");
+        auto *b = new gnnav_blocks();
+        if (hipHostMalloc((void **)&b->sizes_host, kSizeSlots * sizeof(int32_t), hipHostMallocDefault) !=
+            hipSuccess) {
+            (void)hipGetLastError();
+            delete b;
+            fail(GNNAV_E_NOMEM, "pinned size buffer");
+        }
+        *out = b;
+    });
+}
+
+extern "C" void gnnav_blocks_free(gnnav_blocks *b) {
+    if (!b) return;
+    (void)hipDeviceSynchronize();
+    b->map.release();
+    b->sizes.release();
+    b->nodes.release();
+    b->part.release();
+    for (int h = 0; h < kMaxHops; ++h) {
+        b->indptr[h].release();
+        b->nbrs[h].release();
+        b->indices[h].release();
+    }
+    b->agg.release();
+    b->hid[0].release();
+    b->hid[1].release();
+    if (b->sizes_host) (void)hipHostFree(b->sizes_host);
+    delete b;
+}
+
+extern "C" gnnav_status gnnav_sample(const gnnav_graph *g, const int32_t *seeds_dev, int64_t n_seeds,
+                                     const int32_t *fanouts, int32_t n_hops, uint64_t rng_seed,
+                                     gnnav_blocks *b, void *stream) {
+    return guarded([&] {
+        GNNAV_CHECK(g && b && fanouts, GNNAV_E_INVALID, "NULL graph, blocks or fanouts");
+        GNNAV_CHECK(n_hops >= 1 && n_hops <= kMaxHops, GNNAV_E_INVALID, "n_hops outside [1, 16]");
+        GNNAV_CHECK(n_seeds >= 0, GNNAV_E_INVALID, "n_seeds < 0");
+        GNNAV_CHECK(n_seeds == 0 || seeds_dev, GNNAV_E_INVALID, "seeds_dev is NULL");
+        GNNAV_CHECK(n_seeds <= INT32_MAX, GNNAV_E_CAPACITY, "n_seeds above INT32_MAX");
+        for (int h = 0; h < n_hops; ++h)
+            GNNAV_CHECK(fanouts[h] <= 1024, GNNAV_E_INVALID, "fanout above 1024");
+        hipStream_t s = (hipStream_t)stream;
+        // Eq. 12 capacity bounds (tau = 1, no overlap): E_h <= n_(h-1) * k_h,
+        // n_h <= min(n, n_(h-1) + E_h).
+        int64_t nb[kMaxHops + 1], eb[kMaxHops + 1];
+        nb[0] = std::min<int64_t>(n_seeds, g->n);
+        eb[0] = 0;
+        for (int h = 1; h <= n_hops; ++h) {
+            const int64_t k = fanouts[h - 1] < 0 ? g->max_deg : std::min<int64_t>(fanouts[h - 1], g->max_deg);
+            eb[h] = nb[h - 1] * k;
+            nb[h] = std::min<int64_t>(g->n, nb[h - 1] + eb[h]);
+            GNNAV_CHECK(eb[h] < INT32_MAX && nb[h] < INT32_MAX, GNNAV_E_CAPACITY,
+                        "hop " + std::to_string(h) + " bound exceeds the int32 range");
+        }
+        int64_t max_list = n_seeds;
+        for (int h = 1; h <= n_hops; ++h) max_list = std::max(max_list, std::max(eb[h], nb[h - 1] + 1));
+        // workspace
+        if (b->map_nodes < g->n) {
+            b->map.ensure(std::max<int64_t>(g->n, 1) * sizeof(int32_t), s);
+            launch_fill_i32(b->map.as<int32_t>(), INT_MAX, g->n, s);
+            b->map_nodes = g->n;
+        }
+        b->sizes.ensure(kSizeSlots * sizeof(int32_t), s);
+        b->nodes.ensure(std::max<int64_t>(nb[n_hops], 1) * sizeof(int32_t), s);
+        b->part.ensure(scan_parts(max_list) * sizeof(int64_t), s);
+        for (int h = 1; h <= n_hops; ++h) {
+            b->indptr[h - 1].ensure((nb[h - 1] + 1) * sizeof(int32_t), s);
+            b->nbrs[h - 1].ensure(std::max<int64_t>(eb[h], 1) * sizeof(int32_t), s);
+            b->indices[h - 1].ensure(std::max<int64_t>(eb[h], 1) * sizeof(int32_t), s);
+        }
+        int32_t *sz = b->sizes.as<int32_t>();
+        int32_t *map = b->map.as<int32_t>();
+        int32_t *nodes = b->nodes.as<int32_t>();
+        int32_t *part = b->part.as<int32_t>();
+        launch_fill_i32(sz, 0, kSizeSlots, s);
+        // F_0: seeds without repeats, first occurrence kept
+        DedupArgs d0{seeds_dev, n_seeds, nullptr, n_seeds, map, g->n, nodes, nullptr, sz + kSizeN, sz + kSizeErr,
+                     part};
+        launch_dedup(d0, s);
+        for (int h = 1; h <= n_hops; ++h) {
+            SampleHopArgs a{g->row_ptr.p, g->i64, g->col.as<int32_t>(), nodes, sz + kSizeN + h - 1,
+                            b->indptr[h - 1].as<int32_t>(), b->nbrs[h - 1].as<int32_t>(), sz + kSizeE + h,
+                            fanouts[h - 1], rng_seed, (uint32_t)(h - 1), nb[h - 1], part};
+            launch_count_scan(a, s);
+            launch_sample_hop(a, s);
+            DedupArgs dh{b->nbrs[h - 1].as<int32_t>(), 0, sz + kSizeE + h, eb[h], map, g->n, nodes,
+                         sz + kSizeN + h - 1, sz + kSizeN + h, nullptr, part};
+            launch_dedup(dh, s);
+            launch_relabel(b->nbrs[h - 1].as<int32_t>(), sz + kSizeE + h, eb[h], map,
+                           b->indices[h - 1].as<int32_t>(), s);
+        }
+        launch_reset_map(nodes, sz + kSizeN + n_hops, nb[n_hops], map, s);
+        GNNAV_HIP(hipMemcpyAsync(b->sizes_host, sz, kSizeSlots * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+        GNNAV_HIP(hipStreamSynchronize(s));
+        b->L = n_hops;
+        for (int h = 0; h <= n_hops; ++h) b->n_h[h] = b->sizes_host[kSizeN + h];
+        for (int h = 1; h <= n_hops; ++h) b->e_h[h] = b->sizes_host[kSizeE + h];
+        GNNAV_CHECK(b->sizes_host[kSizeErr] == 0, GNNAV_E_RANGE,
+                    std::to_string(b->sizes_host[kSizeErr]) + " seed(s) outside [0, n)");
+    });
+}
+
+extern "C" gnnav_status gnnav_blocks_hop(const gnnav_blocks *b, int32_t hop, gnnav_block_view *out) {
+    return guarded([&] {
+        GNNAV_CHECK(b && out, GNNAV_E_INVALID, "NULL argument");
+        GNNAV_CHECK(hop >= 1 && hop <= b->L, GNNAV_E_INVALID, "hop outside [1, L]");
+        out->n_dst = b->n_h[hop - 1];
+        out->n_src = b->n_h[hop];
+        out->nnz = b->e_h[hop];
+        out->indptr = b->indptr[hop - 1].as<int32_t>();
+        out->indices = b->indices[hop - 1].as<int32_t>();
+        out->neighbors = b->nbrs[hop - 1].as<int32_t>();
+        out->src_ids = b->nodes.as<int32_t>();
+    });
+}
+
+extern "C" gnnav_status gnnav_blocks_nodes(const gnnav_blocks *b, const int32_t **nodes_dev, int64_t *n_per_hop,
+                                           int32_t *n_hops) {
+    return guarded([&] {
+        GNNAV_CHECK(b, GNNAV_E_INVALID, "blocks is NULL");
+        if (nodes_dev) *nodes_dev = b->nodes.as<int32_t>();
+        if (n_per_hop)
+            for (int h = 0; h <= b->L; ++h) n_per_hop[h] = b->n_h[h];
+        if (n_hops) *n_hops = b->L;
+    });
+}
+
+// ----------------------------------------------------------------- gather
+static bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+extern "C" gnnav_status gnnav_gather(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_ids, void *out_dev,
+                                     int64_t ld_out, int64_t *counts_dev, void *stream) {
+    return guarded([&] {
+        GNNAV_CHECK(c && counts_dev, GNNAV_E_INVALID, "NULL cache or counts");
+        GNNAV_CHECK(n_ids >= 0 && n_ids < INT32_MAX, GNNAV_E_INVALID, "n_ids outside [0, INT32_MAX)");
+        GNNAV_CHECK(n_ids == 0 || (ids_dev && out_dev), GNNAV_E_INVALID, "NULL ids or out");
+        GNNAV_CHECK(ld_out >= c->d, GNNAV_E_INVALID, "ld_out < d");
+        GNNAV_CHECK((ld_out * c->elt) % 16 == 0 && aligned16(out_dev), GNNAV_E_INVALID,
+                    "out rows must be 16-byte aligned");
+        hipStream_t s = (hipStream_t)stream;
+        auto *cc = const_cast<gnnav_cache *>(c);
+        cc->hit_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
+        cc->miss_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
+        cc->part.ensure(scan_parts(n_ids) * sizeof(int64_t), s);
+        GatherArgs a{ids_dev, n_ids, c->slot_map.as<int32_t>(), c->n, c->cache_rows.p, c->store_ptr,
+                     c->ld * c->elt, out_dev, ld_out * c->elt, c->d * c->elt, counts_dev,
+                     cc->dev_counts.as<int32_t>(), cc->hit_list.as<int2>(), cc->miss_list.as<int2>(),
+                     cc->part.as<int32_t>()};
+        launch_classify(a, s);
+        if (n_ids == 0) return;
+        GNNAV_HIP(hipEventRecord(cc->fork, s));
+        GNNAV_HIP(hipStreamWaitEvent(cc->side, cc->fork, 0));
+        launch_gather_rows(a, /*hits=*/false, cc->side);
+        launch_gather_rows(a, /*hits=*/true, s);
+        GNNAV_HIP(hipEventRecord(cc->join, cc->side));
+        GNNAV_HIP(hipStreamWaitEvent(s, cc->join, 0));
+    });
+}
+
+// ------------------------------------------------------------------- SAGE
+static int64_t padded_ld(int64_t d, int64_t elt) { return (d * elt + 15) / 16 * 16 / elt; }
+
+extern "C" gnnav_status gnnav_aggregate_mean(const int32_t *indptr_dev, const int32_t *indices_dev, int64_t n_dst,
+                                             const void *x_dev, int64_t ld_x, int64_t d, gnnav_dtype dt,
+                                             void *out_dev, int64_t ld_out, void *stream) {
+    return guarded([&] {
+        GNNAV_CHECK(dt == GNNAV_F32 || dt == GNNAV_BF16, GNNAV_E_INVALID, "bad dtype");
+        GNNAV_CHECK(n_dst >= 0 && d > 0, GNNAV_E_INVALID, "n_dst < 0 or d <= 0");
+        GNNAV_CHECK(n_dst == 0 || (indptr_dev && indices_dev && x_dev && out_dev), GNNAV_E_INVALID,
+                    "NULL argument");
+        const int64_t elt = dt == GNNAV_BF16 ? 2 : 4;
+        GNNAV_CHECK(ld_x >= d && ld_out >= d, GNNAV_E_INVALID, "stride below d");
+        GNNAV_CHECK((ld_x * elt) % 16 == 0 && (ld_out * elt) % 16 == 0 && aligned16(x_dev) && aligned16(out_dev),
+                    GNNAV_E_INVALID, "rows must be 16-byte aligned");
+        launch_aggregate_mean(indptr_dev, indices_dev, n_dst, x_dev, ld_x, d, dt == GNNAV_BF16, out_dev, ld_out,
+                              (hipStream_t)stream);
+    });
+}
+
+extern "C" gnnav_status gnnav_combine(const void *self_dev, int64_t ld_self, const void *agg_dev, int64_t ld_agg,
+                                      int64_t m, int64_t d_in, const void *w_dev, int64_t d_out, gnnav_dtype dt,
+                                      int32_t relu, int32_t out_bf16, void *out_dev, int64_t ld_out,
+                                      void *stream) {
+    return guarded([&] {
+        GNNAV_CHECK(dt == GNNAV_F32 || dt == GNNAV_BF16, GNNAV_E_INVALID, "bad dtype");
+        GNNAV_CHECK(m >= 0 && d_in > 0 && d_out > 0, GNNAV_E_INVALID, "bad sizes");
+        GNNAV_CHECK(m == 0 || (self_dev && agg_dev && w_dev && out_dev), GNNAV_E_INVALID, "NULL argument");
+        GNNAV_CHECK(!(dt == GNNAV_F32 && out_bf16), GNNAV_E_INVALID, "bf16 output needs bf16 operands");
+        const int64_t elt = dt == GNNAV_BF16 ? 2 : 4;
+        GNNAV_CHECK(ld_self >= d_in && ld_agg >= d_in && ld_out >= d_out, GNNAV_E_INVALID, "stride too small");
+        GNNAV_CHECK((ld_self * elt) % 16 == 0 && (ld_agg * elt) % 16 == 0 && aligned16(self_dev) &&
+                        aligned16(agg_dev),
+                    GNNAV_E_INVALID, "operand rows must be 16-byte aligned");
+        launch_combine(self_dev, ld_self, agg_dev, ld_agg, m, d_in, w_dev, d_out, dt == GNNAV_BF16, relu != 0,
+                       out_bf16 != 0, out_dev, ld_out, (hipStream_t)stream);
+    });
+}
+
+extern "C" gnnav_status gnnav_sage_forward(gnnav_blocks *b, const void *x_dev, int64_t ld_x,
+                                           const void *const *W_dev, const int32_t *dims, int32_t n_layers,
+                                           gnnav_dtype dt, float *logits_dev, int64_t ld_out, void *stream) {
+    return guarded([&] {
+        GNNAV_CHECK(b && W_dev && dims && logits_dev, GNNAV_E_INVALID, "NULL argument");
+        GNNAV_CHECK(n_layers == b->L && n_layers >= 1, GNNAV_E_INVALID, "n_layers differs from the sampled hops");
+        GNNAV_CHECK(dt == GNNAV_F32 || dt == GNNAV_BF16, GNNAV_E_INVALID, "bad dtype");
+        const int L = n_layers;
+        for (int l = 0; l <= L; ++l) GNNAV_CHECK(dims[l] > 0, GNNAV_E_INVALID, "dims must be positive");
+        for (int l = 0; l < L; ++l) GNNAV_CHECK(W_dev[l], GNNAV_E_INVALID, "NULL weight");
+        GNNAV_CHECK(ld_out >= dims[L], GNNAV_E_INVALID, "ld_out < dims[L]");
+        const bool bf = dt == GNNAV_BF16;
+        const int64_t elt = bf ? 2 : 4;
+        GNNAV_CHECK(ld_x >= dims[0] && (ld_x * elt) % 16 == 0 && aligned16(x_dev), GNNAV_E_INVALID,
+                    "x rows must be 16-byte aligned with ld_x >= dims[0]");
+        hipStream_t s = (hipStream_t)stream;
+        // workspace: agg for the largest layer, two ping-pong hidden buffers
+        int64_t agg_bytes = 1, hid_bytes = 1;
+        for (int l = 1; l <= L; ++l) {
+            const int hb = L - l + 1;
+            const int64_t rows = b->n_h[hb - 1];
+            agg_bytes = std::max(agg_bytes, rows * padded_ld(dims[l - 1], elt) * elt);
+            if (l < L) hid_bytes = std::max(hid_bytes, rows * padded_ld(dims[l], elt) * elt);
+        }
+        b->agg.ensure(agg_bytes, s);
+        if (L > 1) {
+            b->hid[0].ensure(hid_bytes, s);
+            b->hid[1].ensure(hid_bytes, s);
+        }
+        const void *x = x_dev;
+        int64_t ldx = ld_x;
+        for (int l = 1; l <= L; ++l) {
+            const int hb = L - l + 1;
+            const int64_t rows = b->n_h[hb - 1];
+            const int64_t din = dims[l - 1], dout = dims[l];
+            const int64_t lda = padded_ld(din, elt);
+            launch_aggregate_mean(b->indptr[hb - 1].as<int32_t>(), b->indices[hb - 1].as<int32_t>(), rows, x, ldx,
+                                  din, bf, b->agg.p, lda, s);
+            if (l < L) {
+                void *h = b->hid[l & 1].p;
+                const int64_t ldh = padded_ld(dout, elt);
+                launch_combine(x, ldx, b->agg.p, lda, rows, din, W_dev[l - 1], dout, bf, true, bf, h, ldh, s);
+                x = h;
+                ldx = ldh;
+            } else {
+                launch_combine(x, ldx, b->agg.p, lda, rows, din, W_dev[l - 1], dout, bf, false, false, logits_dev,
+                               ld_out, s);
+            }
+        }
+    });
+}

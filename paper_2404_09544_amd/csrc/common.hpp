@@ -1,0 +1,204 @@
+// Internal declarations shared by the gnnav HIP sources (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "gnnav.h"
+
+namespace gnnav {
+
+// ------------------------------------------------------------------ errors
+struct Error {
+    gnnav_status status;
+    std::string msg;
+};
+
+[[noreturn]] inline void fail(gnnav_status st, const std::string &msg) { throw Error{st, msg}; }
+
+#define GNNAV_HIP(call)                                                                   \
+    do {                                                                                  \
+        hipError_t e_ = (call);                                                           \
+        if (e_ != hipSuccess)                                                             \
+            ::gnnav::fail(GNNAV_E_DEVICE, std::string(#call) + ": " + hipGetErrorString(e_)); \
+    } while (0)
+
+#define GNNAV_CHECK(cond, st, msg)                    \
+    do {                                              \
+        if (!(cond)) ::gnnav::fail((st), (msg));      \
+    } while (0)
+
+// Runs `body`, converting exceptions into a status and the thread's error text.
+void set_last_error(const std::string &msg);
+template <class F>
+gnnav_status guarded(F &&body) {
+    try {
+        set_last_error("");
+        body();
+        return GNNAV_OK;
+    } catch (const Error &e) {
+        set_last_error(e.msg);
+        return e.status;
+    } catch (const std::bad_alloc &) {
+        set_last_error("host allocation failed");
+        return GNNAV_E_NOMEM;
+    } catch (const std::exception &e) {
+        set_last_error(e.what());
+        return GNNAV_E_DEVICE;
+    }
+}
+
+// --------------------------------------------------- grow-only device buffer
+// Reallocation waits for `stream` so in-flight kernels never see a freed buffer.
+struct DevBuf {
+    void *p = nullptr;
+    size_t bytes = 0;
+    void ensure(size_t need, hipStream_t stream);
+    void release();
+    template <class T>
+    T *as() const { return static_cast<T *>(p); }
+};
+
+// -------------------------------------------------------------- profiling
+// When profiling is on, each Launch records a start/stop event pair around
+// the kernel on the stream the kernel is enqueued on.
+bool profiling_on();
+struct KernelTimer {
+    KernelTimer(const char *name, hipStream_t s);
+    ~KernelTimer();
+    int slot = -1;
+    hipStream_t stream;
+};
+
+inline unsigned grid_for(int64_t items, int64_t per_block, int64_t cap) {
+    int64_t g = (items + per_block - 1) / per_block;
+    if (g > cap) g = cap;
+    return (unsigned)(g < 1 ? 1 : g);
+}
+
+// ------------------------------------------------------ device primitives
+constexpr int kWave = 64;
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+// bf16 bit pattern of a float, round to nearest, ties to even; NaN stays NaN.
+__device__ __forceinline__ uint16_t bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+template <class V>
+__device__ __forceinline__ V wave_inclusive_sum(V x) {
+    const int lane = lane_id();
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        V y = __shfl_up(x, o, kWave);
+        if (lane >= o) x += y;
+    }
+    return x;
+}
+
+// Exclusive prefix sum over a block of NT threads; `scratch` holds NT/64
+// values in LDS.  Returns the thread's exclusive prefix; `total` gets the
+// block sum.  Must be called by every thread of the block.
+template <class V, int NT>
+__device__ __forceinline__ V block_exclusive_sum(V x, V *scratch, V &total) {
+    constexpr int NW = NT / kWave;
+    const int lane = lane_id(), wid = threadIdx.x / kWave;
+    V inc = wave_inclusive_sum(x);
+    if (lane == kWave - 1) scratch[wid] = inc;
+    __syncthreads();
+    if (wid == 0) {
+        V t = lane < NW ? scratch[lane] : V(0);
+        t = wave_inclusive_sum(t);
+        if (lane < NW) scratch[lane] = t;
+    }
+    __syncthreads();
+    V off = wid > 0 ? scratch[wid - 1] : V(0);
+    total = scratch[NW - 1];
+    __syncthreads();
+    return off + inc - x;
+}
+
+// ------------------------------------------------------------ launchers
+// Device-wide exclusive scan + emit in three launches (per-tile sums, one
+// block scanning the tile sums, per-tile scan and emit).  See scan.hpp.
+
+// sample.hip
+struct SampleHopArgs {
+    const void *row_ptr;
+    bool offsets_i64;
+    const int32_t *col;
+    const int32_t *nodes;
+    const int32_t *n_prev;   // device: |F_(h-1)|
+    int32_t *indptr;         // device: |F_(h-1)|+1
+    int32_t *nbrs;           // device: E_h
+    int32_t *e_out;          // device: E_h (written)
+    int32_t fanout;
+    uint64_t rng_seed;
+    uint32_t hop;            // 0-based
+    int64_t rows_bound;
+    int32_t *part;           // scan partials
+};
+void launch_count_scan(const SampleHopArgs &a, hipStream_t s);
+void launch_sample_hop(const SampleHopArgs &a, hipStream_t s);
+
+struct DedupArgs {
+    const int32_t *list;     // ids to union into the frontier
+    int64_t len_const;       // used when len_ptr == nullptr
+    const int32_t *len_ptr;  // device length
+    int64_t len_bound;
+    int32_t *map;            // int32[n_nodes]
+    int64_t n_nodes;
+    int32_t *nodes;
+    const int32_t *base_ptr; // device |F_(h-1)| (nullptr: 0)
+    int32_t *size_out;       // device |F_h|
+    int32_t *err;            // device count of out-of-range ids (nullable)
+    int32_t *part;
+};
+void launch_dedup(const DedupArgs &a, hipStream_t s);
+void launch_relabel(const int32_t *list, const int32_t *len_ptr, int64_t len_bound,
+                    const int32_t *map, int32_t *indices, hipStream_t s);
+void launch_reset_map(const int32_t *nodes, const int32_t *n_ptr, int64_t bound, int32_t *map,
+                      hipStream_t s);
+void launch_fill_i32(int32_t *p, int32_t v, int64_t n, hipStream_t s);
+
+// gather.hip
+struct GatherArgs {
+    const int32_t *ids;
+    int64_t n_ids;
+    const int32_t *slot_map;
+    int64_t n_nodes;
+    const void *cache;       // device [C x ld]
+    const void *store;       // device-visible store [n x ld] (host-mapped or HBM)
+    int64_t src_ld_bytes;
+    void *out;
+    int64_t out_ld_bytes;
+    int64_t row_bytes;       // d * elt
+    int64_t *counts;         // device int64[3]
+    int32_t *dev_counts;     // device int32[2]: hits, misses
+    int2 *hit_list;
+    int2 *miss_list;
+    int32_t *part;
+};
+void launch_classify(const GatherArgs &a, hipStream_t s);
+void launch_gather_rows(const GatherArgs &a, bool hits, hipStream_t s);
+
+// spmm.hip
+void launch_aggregate_mean(const int32_t *indptr, const int32_t *indices, int64_t n_dst,
+                           const void *x, int64_t ld_x, int64_t d, bool bf16, void *out,
+                           int64_t ld_out, hipStream_t s);
+
+// gemm.hip
+void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
+                    int64_t d_in, const void *w, int64_t d_out, bool bf16, bool relu,
+                    bool out_bf16, void *out, int64_t ld_out, hipStream_t s);
+
+}  // namespace gnnav

@@ -1,0 +1,122 @@
+// Feature gather through the static device cache (the cache step of the
+// paper's transmission abstraction: find the cached part of the batch, fetch
+// the rest from the host).
+//
+//   classify   slot lookup per requested id; an order-preserving scan
+//              splits the requests into a hit list (out row, cache slot)
+//              and a miss list (out row, node id) and writes the counts;
+//              out-of-range ids get a zero row right here
+//   rows       copies listed rows in 16-byte units; the hit launch reads
+//              the HBM cache, the miss launch reads the host store through
+//              its device mapping (zero-copy over the host link) and runs on
+//              a second stream so both proceed together
+#include "common.hpp"
+#include "scan.hpp"
+
+namespace gnnav {
+
+struct ClassifyOp {
+    const int32_t *ids;
+    int64_t n_ids;
+    const int32_t *slot_map;
+    int64_t n_nodes;
+    int2 *hit_list;
+    int2 *miss_list;
+    int64_t *counts;
+    int32_t *dev_counts;
+    uint4 *out;
+    int64_t out_ld16;
+    int64_t chunks;
+    // packed value: hits in the high 32 bits, misses in the low 32 bits
+    __device__ int64_t n() const { return n_ids; }
+    __device__ int64_t value(int64_t i) const {
+        const int32_t id = ids[i];
+        if (id < 0 || id >= n_nodes) return 0;
+        return slot_map[id] >= 0 ? (int64_t(1) << 32) : int64_t(1);
+    }
+    __device__ void emit(int64_t i, int64_t prefix, int64_t v) const {
+        const int32_t id = ids[i];
+        if (v == 0) {
+            uint4 *row = out + i * out_ld16;
+            for (int64_t c = 0; c < chunks; ++c) row[c] = make_uint4(0, 0, 0, 0);
+        } else if (v == 1) {
+            miss_list[(int32_t)(prefix & 0xffffffff)] = make_int2((int32_t)i, id);
+        } else {
+            hit_list[(int32_t)(prefix >> 32)] = make_int2((int32_t)i, slot_map[id]);
+        }
+    }
+    __device__ void total(int64_t t) const {
+        const int64_t hits = t >> 32, misses = t & 0xffffffff;
+        counts[0] = hits;
+        counts[1] = misses;
+        counts[2] = n_ids - hits - misses;
+        dev_counts[0] = (int32_t)hits;
+        dev_counts[1] = (int32_t)misses;
+    }
+};
+
+void launch_classify(const GatherArgs &a, hipStream_t s) {
+    ClassifyOp op{a.ids, a.n_ids, a.slot_map, a.n_nodes, a.hit_list, a.miss_list, a.counts,
+                  a.dev_counts, (uint4 *)a.out, a.out_ld_bytes / 16, (a.row_bytes + 15) / 16};
+    run_scan(op, a.n_ids, (int64_t *)a.part, "classify", s);
+}
+
+// G lanes per row (power of two), 64/G rows per wavefront pass.  Each lane
+// moves 16-byte units c = lane%G, lane%G + G, ... of its row.
+template <int G>
+__global__ void __launch_bounds__(256) k_gather_rows(const int2 *__restrict__ list,
+                                                     const int32_t *__restrict__ count_ptr,
+                                                     const uint4 *__restrict__ src, int64_t src_ld16,
+                                                     uint4 *__restrict__ out, int64_t out_ld16,
+                                                     int32_t chunks) {
+    constexpr int RPW = kWave / G;
+    const int lane = lane_id();
+    const int sub = lane / G, c0 = lane % G;
+    const int64_t count = *count_ptr;
+    const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
+    for (int64_t r = (((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave) * RPW + sub; r < count;
+         r += nwaves * RPW) {
+        const int2 e = list[r];
+        const uint4 *s = src + (int64_t)e.y * src_ld16;
+        uint4 *d = out + (int64_t)e.x * out_ld16;
+        int c = c0;
+        for (; c + 3 * G < chunks; c += 4 * G) {
+            const uint4 a = s[c], b = s[c + G], x = s[c + 2 * G], y = s[c + 3 * G];
+            d[c] = a;
+            d[c + G] = b;
+            d[c + 2 * G] = x;
+            d[c + 3 * G] = y;
+        }
+        for (; c < chunks; c += G) d[c] = s[c];
+    }
+}
+
+void launch_gather_rows(const GatherArgs &a, bool hits, hipStream_t s) {
+    const int32_t chunks = (int32_t)((a.row_bytes + 15) / 16);
+    int g = 1;
+    while (g < chunks && g < kWave) g <<= 1;
+    const int64_t rows_bound = a.n_ids;
+    if (rows_bound <= 0 || chunks <= 0) return;
+    const int rows_per_block = (256 / kWave) * (kWave / g);
+    // The miss path needs only enough waves to cover host-link latency.
+    const unsigned grid = grid_for(rows_bound, rows_per_block, hits ? 8192 : 1024);
+    const int2 *list = hits ? a.hit_list : a.miss_list;
+    const int32_t *cnt = a.dev_counts + (hits ? 0 : 1);
+    const uint4 *src = (const uint4 *)(hits ? a.cache : a.store);
+    const int64_t sld = a.src_ld_bytes / 16, old = a.out_ld_bytes / 16;
+    KernelTimer t(hits ? "gather_hit" : "gather_miss", s);
+    switch (g) {
+#define GNNAV_G(GV)                                                                                 \
+    case GV:                                                                                        \
+        hipLaunchKernelGGL(k_gather_rows<GV>, dim3(grid), dim3(256), 0, s, list, cnt, src, sld,     \
+                           (uint4 *)a.out, old, chunks);                                            \
+        break;
+        GNNAV_G(1) GNNAV_G(2) GNNAV_G(4) GNNAV_G(8) GNNAV_G(16) GNNAV_G(32) GNNAV_G(64)
+#undef GNNAV_G
+        default:
+            fail(GNNAV_E_INVALID, "bad row width");
+    }
+    GNNAV_HIP(hipGetLastError());
+}
+
+}  // namespace gnnav

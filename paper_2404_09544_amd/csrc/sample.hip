@@ -1,0 +1,299 @@
+// Eq. 2 node-wise fanout sampling and the per-hop frontier union.
+//
+// Per hop h:
+//   count scan   indptr_h = exclusive scan of min(deg(v), k) over F_(h-1)
+//   sample       one wavefront per destination row: copy the row when
+//                deg <= k, else Floyd's k-subset with Philox4x32-10 draws
+//   dedup        first position of each id in N_h (atomicMin on a dense
+//                per-node table), then an order-preserving scan appends the
+//                new ids to the node list and records their local ids
+//   relabel      indices_h[p] = local id of N_h[p]
+// The node table lives in HBM (int32 per graph node).  Entry encoding:
+// INT_MAX = unseen, p >= 0 = smallest position seen in the current list,
+// -(local+1) = already in the frontier with that local id.
+#include "common.hpp"
+#include "scan.hpp"
+
+namespace gnnav {
+
+// ---------------------------------------------------------------- Philox
+// Philox4x32-10 (Salmon et al., SC'11): ten rounds; each multiplies words 0
+// and 2 by the Philox multipliers and mixes the high halves with words 1, 3
+// and the round key; the key advances by the Weyl constants between rounds.
+// Only output word 0 is needed.
+__device__ __forceinline__ uint32_t philox_word0(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                                 uint32_t k0, uint32_t k1) {
+    constexpr uint32_t kMulA = 0xD2511F53u, kMulB = 0xCD9E8D57u;
+    constexpr uint32_t kWeylA = 0x9E3779B9u, kWeylB = 0xBB67AE85u;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint32_t lo_a = c0 * kMulA, hi_a = __umulhi(c0, kMulA);
+        const uint32_t lo_b = c2 * kMulB, hi_b = __umulhi(c2, kMulB);
+        const uint32_t x0 = hi_b ^ c1 ^ k0;
+        const uint32_t x2 = hi_a ^ c3 ^ k1;
+        c0 = x0;
+        c1 = lo_b;
+        c2 = x2;
+        c3 = lo_a;
+        k0 += kWeylA;
+        k1 += kWeylB;
+    }
+    return c0;
+}
+
+template <class OffT>
+__device__ __forceinline__ int64_t row_degree(const OffT *rp, int32_t v, int64_t &start) {
+    start = (int64_t)rp[v];
+    return (int64_t)rp[v + 1] - start;
+}
+
+// ------------------------------------------------------------ count scan
+template <class OffT>
+struct CountOp {
+    const OffT *row_ptr;
+    const int32_t *nodes;
+    const int32_t *n_ptr;
+    int32_t k;
+    int32_t *indptr;
+    int32_t *e_out;
+    __device__ int64_t n() const { return *n_ptr; }
+    __device__ int32_t value(int64_t i) const {
+        int64_t st;
+        int64_t deg = row_degree(row_ptr, nodes[i], st);
+        return (int32_t)((k < 0 || deg <= k) ? deg : k);
+    }
+    __device__ void emit(int64_t i, int32_t prefix, int32_t) const { indptr[i] = prefix; }
+    __device__ void total(int32_t t) const {
+        indptr[*n_ptr] = t;
+        *e_out = t;
+    }
+};
+
+void launch_count_scan(const SampleHopArgs &a, hipStream_t s) {
+    if (a.offsets_i64) {
+        CountOp<int64_t> op{(const int64_t *)a.row_ptr, a.nodes, a.n_prev, a.fanout, a.indptr, a.e_out};
+        run_scan(op, a.rows_bound, a.part, "count_scan", s);
+    } else {
+        CountOp<int32_t> op{(const int32_t *)a.row_ptr, a.nodes, a.n_prev, a.fanout, a.indptr, a.e_out};
+        run_scan(op, a.rows_bound, a.part, "count_scan", s);
+    }
+}
+
+// ---------------------------------------------------------- sample kernel
+// One wavefront per destination row, grid-stride over rows.  For k <= 64
+// lane j holds draw j: t_j = floor(x_j * (m_j + 1) / 2^32), m_j = deg-k+j.
+// Floyd's rule is sequential in j (slot j takes t_j unless an earlier slot
+// already holds it, then m_j), so the wave walks j in order and decides
+// each slot with one ballot against the slots already fixed.
+template <class OffT>
+__global__ void __launch_bounds__(256) k_sample_small(const OffT *__restrict__ row_ptr,
+                                                      const int32_t *__restrict__ col,
+                                                      const int32_t *__restrict__ nodes,
+                                                      const int32_t *__restrict__ n_prev,
+                                                      const int32_t *__restrict__ indptr,
+                                                      int32_t *__restrict__ out, int32_t k,
+                                                      uint32_t key0, uint32_t key1, uint32_t hop) {
+    const int lane = lane_id();
+    const int64_t n_rows = *n_prev;
+    const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
+    for (int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave; i < n_rows; i += nwaves) {
+        const int32_t v = nodes[i];
+        int64_t start;
+        const int64_t deg = row_degree(row_ptr, v, start);
+        int32_t *dst = out + indptr[i];
+        if (k < 0 || deg <= k) {
+            for (int64_t j = lane; j < deg; j += kWave) dst[j] = col[start + j];
+            continue;
+        }
+        uint32_t t = 0, m = 0;
+        if (lane < k) {
+            m = (uint32_t)(deg - k + lane);
+            const uint32_t x = philox_word0((uint32_t)lane, (uint32_t)v, 0u, hop, key0, key1);
+            t = __umulhi(x, m + 1u);
+        }
+        uint32_t pick = t;
+        for (int j = 1; j < k; ++j) {
+            const uint32_t tj = (uint32_t)__builtin_amdgcn_readlane((int)t, j);
+            const uint64_t clash = __ballot(lane < j && pick == tj);
+            if (lane == j && clash != 0) pick = m;
+        }
+        if (lane < k) dst[lane] = col[start + pick];
+    }
+}
+
+// 64 < k <= kMaxFanout: chosen offsets kept in LDS per wave; each slot j is
+// checked against all earlier slots with a wave-wide ballot per 64 slots.
+constexpr int kMaxFanout = 1024;
+
+template <class OffT>
+__global__ void __launch_bounds__(256) k_sample_big(const OffT *__restrict__ row_ptr,
+                                                    const int32_t *__restrict__ col,
+                                                    const int32_t *__restrict__ nodes,
+                                                    const int32_t *__restrict__ n_prev,
+                                                    const int32_t *__restrict__ indptr,
+                                                    int32_t *__restrict__ out, int32_t k,
+                                                    uint32_t key0, uint32_t key1, uint32_t hop) {
+    __shared__ uint32_t taken_all[256 / kWave][kMaxFanout];
+    uint32_t *taken = taken_all[threadIdx.x / kWave];
+    const int lane = lane_id();
+    const int64_t n_rows = *n_prev;
+    const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
+    for (int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave; i < n_rows; i += nwaves) {
+        const int32_t v = nodes[i];
+        int64_t start;
+        const int64_t deg = row_degree(row_ptr, v, start);
+        int32_t *dst = out + indptr[i];
+        if (deg <= k) {
+            for (int64_t j = lane; j < deg; j += kWave) dst[j] = col[start + j];
+            continue;
+        }
+        for (int jb = 0; jb < k; jb += kWave) {
+            const int jl = jb + lane;
+            uint32_t t = 0, m = 0;
+            if (jl < k) {
+                m = (uint32_t)(deg - k + jl);
+                const uint32_t x = philox_word0((uint32_t)jl, (uint32_t)v, 0u, hop, key0, key1);
+                t = __umulhi(x, m + 1u);
+            }
+            uint32_t pick = t;
+            const int jend = min(k, jb + kWave);
+            for (int j = jb; j < jend; ++j) {
+                const uint32_t tj = (uint32_t)__builtin_amdgcn_readlane((int)t, j - jb);
+                bool hit = lane < j - jb && pick == tj;
+                for (int q = lane; q < jb; q += kWave) hit = hit || taken[q] == tj;
+                const uint64_t clash = __ballot(hit);
+                if (lane == j - jb && clash != 0) pick = m;
+            }
+            if (jl < k) taken[jl] = pick;
+            __builtin_amdgcn_s_waitcnt(0);
+            __builtin_amdgcn_wave_barrier();
+        }
+        for (int q = lane; q < k; q += kWave) dst[q] = col[start + taken[q]];
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
+void launch_sample_hop(const SampleHopArgs &a, hipStream_t s) {
+    if (a.rows_bound <= 0) return;
+    GNNAV_CHECK(a.fanout <= kMaxFanout, GNNAV_E_INVALID, "fanout above 1024");
+    const uint32_t key0 = (uint32_t)(a.rng_seed & 0xffffffffu), key1 = (uint32_t)(a.rng_seed >> 32);
+    const unsigned grid = grid_for(a.rows_bound, 256 / kWave, 16384);
+    KernelTimer t("sample_hop", s);
+    const bool big = a.fanout > kWave;
+    if (a.offsets_i64) {
+        auto kern = big ? k_sample_big<int64_t> : k_sample_small<int64_t>;
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, (const int64_t *)a.row_ptr, a.col,
+                           a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop);
+    } else {
+        auto kern = big ? k_sample_big<int32_t> : k_sample_small<int32_t>;
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, (const int32_t *)a.row_ptr, a.col,
+                           a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop);
+    }
+    GNNAV_HIP(hipGetLastError());
+}
+
+// ------------------------------------------------------------------ dedup
+__device__ __forceinline__ int64_t list_len(int64_t c, const int32_t *p) { return p ? (int64_t)*p : c; }
+
+__global__ void __launch_bounds__(256) k_first_position(const int32_t *__restrict__ list, int64_t len_const,
+                                                        const int32_t *__restrict__ len_ptr,
+                                                        int32_t *__restrict__ map, int64_t n_nodes,
+                                                        int32_t *__restrict__ err) {
+    const int64_t len = list_len(len_const, len_ptr);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int32_t bad = 0;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < len; p += stride) {
+        const int32_t id = list[p];
+        if (id < 0 || id >= n_nodes) {
+            ++bad;
+            continue;
+        }
+        if (map[id] > (int32_t)p) atomicMin(&map[id], (int32_t)p);
+    }
+    if (bad && err) atomicAdd(err, bad);
+}
+
+struct DedupOp {
+    const int32_t *list;
+    int64_t len_const;
+    const int32_t *len_ptr;
+    int32_t *map;
+    int64_t n_nodes;
+    int32_t *nodes;
+    const int32_t *base_ptr;
+    int32_t *size_out;
+    __device__ int64_t n() const { return list_len(len_const, len_ptr); }
+    __device__ int32_t value(int64_t p) const {
+        const int32_t id = list[p];
+        if (id < 0 || id >= n_nodes) return 0;
+        return map[id] == (int32_t)p ? 1 : 0;
+    }
+    __device__ void emit(int64_t p, int32_t prefix, int32_t v) const {
+        if (!v) return;
+        const int32_t id = list[p];
+        const int32_t local = (base_ptr ? *base_ptr : 0) + prefix;
+        nodes[local] = id;
+        map[id] = -(local + 1);
+    }
+    __device__ void total(int32_t t) const { *size_out = (base_ptr ? *base_ptr : 0) + t; }
+};
+
+void launch_dedup(const DedupArgs &a, hipStream_t s) {
+    if (a.len_bound > 0) {
+        KernelTimer t("dedup_first", s);
+        hipLaunchKernelGGL(k_first_position, dim3(grid_for(a.len_bound, 256, 8192)), dim3(256), 0, s,
+                           a.list, a.len_const, a.len_ptr, a.map, a.n_nodes, a.err);
+        GNNAV_HIP(hipGetLastError());
+    }
+    DedupOp op{a.list, a.len_const, a.len_ptr, a.map, a.n_nodes, a.nodes, a.base_ptr, a.size_out};
+    run_scan(op, a.len_bound, a.part, "dedup_scan", s);
+}
+
+__global__ void __launch_bounds__(256) k_relabel(const int32_t *__restrict__ list,
+                                                 const int32_t *__restrict__ len_ptr,
+                                                 const int32_t *__restrict__ map,
+                                                 int32_t *__restrict__ indices) {
+    const int64_t len = *len_ptr;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < len; p += stride)
+        indices[p] = -map[list[p]] - 1;
+}
+
+void launch_relabel(const int32_t *list, const int32_t *len_ptr, int64_t len_bound, const int32_t *map,
+                    int32_t *indices, hipStream_t s) {
+    if (len_bound <= 0) return;
+    KernelTimer t("relabel", s);
+    hipLaunchKernelGGL(k_relabel, dim3(grid_for(len_bound, 256, 8192)), dim3(256), 0, s, list, len_ptr,
+                       map, indices);
+    GNNAV_HIP(hipGetLastError());
+}
+
+__global__ void __launch_bounds__(256) k_reset_map(const int32_t *__restrict__ nodes,
+                                                   const int32_t *__restrict__ n_ptr,
+                                                   int32_t *__restrict__ map) {
+    const int64_t n = *n_ptr;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        map[nodes[i]] = INT_MAX;
+}
+
+void launch_reset_map(const int32_t *nodes, const int32_t *n_ptr, int64_t bound, int32_t *map,
+                      hipStream_t s) {
+    if (bound <= 0) return;
+    KernelTimer t("reset_map", s);
+    hipLaunchKernelGGL(k_reset_map, dim3(grid_for(bound, 256, 8192)), dim3(256), 0, s, nodes, n_ptr, map);
+    GNNAV_HIP(hipGetLastError());
+}
+
+__global__ void __launch_bounds__(256) k_fill_i32(int32_t *__restrict__ p, int32_t v, int64_t n) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
+}
+
+void launch_fill_i32(int32_t *p, int32_t v, int64_t n, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_fill_i32, dim3(grid_for(n, 256, 8192)), dim3(256), 0, s, p, v, n);
+    GNNAV_HIP(hipGetLastError());
+}
+
+}  // namespace gnnav

@@ -1,0 +1,38 @@
+"""The C-ABI library loads and exports every symbol include/gnnav.h declares.
+
+No compute call is made, so this runs without a GPU.
+"""
+import ctypes
+import os
+import re
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gnnav.h")
+LIB = os.path.join(ROOT, "paper_2404_09544_amd", "libgnnav.so")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gnnav_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for must in ["gnnav_build_csr", "gnnav_build_cache", "gnnav_sample", "gnnav_gather",
+                 "gnnav_sage_forward"]:
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol():
+    assert os.path.exists(LIB), "build first: python -m paper_2404_09544_amd.build"
+    lib = ctypes.CDLL(LIB)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_binding_covers_every_export():
+    import paper_2404_09544_amd as g
+    assert sorted(g.EXPORTS) == declared_functions()
+    assert g.abi_version() == 1
+    assert g._lib.gnnav_last_error() == b""
