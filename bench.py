@@ -47,7 +47,7 @@ def kernel_source_hash(files) -> str:
 
 
 KERNEL_SOURCES = {"aggregate_mean": ["spmm.hip", "common.hpp"],
-                  "gather_hit": ["gather.hip", "common.hpp", "scan.hpp"],
+                  "gather_hit": ["gather.hip", "common.hpp"],
                   "combine_gemm": ["gemm.hip", "common.hpp"]}
 
 
@@ -58,7 +58,7 @@ def traffic_for(kernel: str, workload: str):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("source_hash") != kernel_source_hash(KERNEL_SOURCES[kernel]):
+    if rec.get("source_hash") != kernel_source_hash(KERNEL_SOURCES[kernel.split(".")[0]]):
         return None
     return rec.get("bytes_per_launch")
 
@@ -72,7 +72,19 @@ def main():
     ap.add_argument("--cache-fraction", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-batches", type=int, default=2)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy (scales rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        n = 256 * 1024 * 1024
+        x = torch.ones(n, dtype=torch.float32, device="cuda")
+        y = torch.empty_like(x)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4}), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the path is single-GPU: no sharding, no collectives)", file=sys.stderr)
@@ -129,8 +141,8 @@ def main():
     # are regenerated here (untimed) to count distinct source rows.
     elt = 2 if wl.dtype == "bf16" else 4
     L = wl.L
-    work = {"gather_hit": 0.0, "gather_miss": 0.0, "aggregate_mean": 0.0, "combine_gemm": 0.0,
-            "aggregate_mean_edge": 0.0}
+    work = {"gather_hit": 0.0, "gather_miss": 0.0}
+    edge = {}
     probe = G.Blocks()
     for i, b in enumerate(range(args.warmup, n_b)):
         sz = sizes_hist[i]
@@ -144,11 +156,11 @@ def main():
             n_dst, E = sz[hb - 1], int(ip[hb - 1][-1])
             u = np.unique(ix[hb - 1]).size
             din, dout = wl.dims[l - 1], wl.dims[l]
-            e_in = elt
-            e_out = elt
-            work["aggregate_mean"] += u * din * e_in + n_dst * din * e_out + 4 * (E + n_dst + 1)
-            work["aggregate_mean_edge"] += E * din * e_in + n_dst * din * e_out + 4 * (E + n_dst + 1)
-            work["combine_gemm"] += 2.0 * n_dst * (2 * din) * dout
+            ka, kg = f"aggregate_mean.l{l}", f"combine_gemm.l{l}"
+            # compulsory bytes: each distinct source row once, each output row once, the CSR
+            work[ka] = work.get(ka, 0.0) + u * din * elt + n_dst * din * elt + 4 * (E + n_dst + 1)
+            edge[ka] = edge.get(ka, 0.0) + E * din * elt + n_dst * din * elt + 4 * (E + n_dst + 1)
+            work[kg] = work.get(kg, 0.0) + 2.0 * n_dst * (2 * din) * dout
     probe.close()
 
     kernels = {}
@@ -156,20 +168,22 @@ def main():
         kernels[name] = {"launches": launches, "total_ms": round(ms, 4),
                          "avg_us": round(ms * 1e3 / max(launches, 1), 3)}
     rows = []
-    for name, bound, peak, unit in [("gather_hit", "hbm", HBM_PEAK_GBS, "GB/s"),
-                                    ("aggregate_mean", "hbm", HBM_PEAK_GBS, "GB/s"),
-                                    ("combine_gemm", "mfma", MFMA_PEAK_TFLOPS[wl.dtype], "TFLOP/s"),
-                                    ("gather_miss", "host_link", HOST_LINK_PEAK_GBS, "GB/s")]:
+    for name in work:
         if name not in prof:
             continue
+        if name == "gather_miss":
+            bound, peak, unit = "host_link", HOST_LINK_PEAK_GBS, "GB/s"
+        elif name.startswith("combine_gemm"):
+            bound, peak, unit = "mfma", MFMA_PEAK_TFLOPS[wl.dtype], "TFLOP/s"
+        else:
+            bound, peak, unit = "hbm", HBM_PEAK_GBS, "GB/s"
         launches, ms = prof[name]
         amount = work[name]
         achieved = amount / (ms * 1e-3) / (1e12 if unit == "TFLOP/s" else 1e9)
         ent = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-               "frac": round(achieved / peak, 4), "avg_us": kernels[name]["avg_us"],
-               "per_launch": amount / max(launches, 1)}
-        if name == "aggregate_mean":
-            ent["achieved_edge_effective"] = round(work["aggregate_mean_edge"] / (ms * 1e-3) / 1e9, 2)
+               "frac": round(achieved / peak, 4), "per_launch": round(amount / max(launches, 1), 1)}
+        if name in edge:
+            ent["achieved_edge_effective"] = round(edge[name] / (ms * 1e-3) / 1e9, 2)
         kernels[name].update(ent)
         rows.append((ms, name))
     device_rows = [(ms, n) for ms, n in rows if kernels[n]["bound"] in ("hbm", "mfma")]
@@ -177,9 +191,8 @@ def main():
     roofline = None
     if dom:
         k = kernels[dom]
-        tr = traffic_for(dom, wl.name) if dom in KERNEL_SOURCES else None
         roofline = {"kernel": dom, "bound": k["bound"], "achieved": k["achieved"], "peak": k["peak"],
-                    "unit": k["unit"], "frac": k["frac"], "traffic": tr}
+                    "unit": k["unit"], "frac": k["frac"], "traffic": traffic_for(dom, wl.name)}
 
     # ---- CPU baseline: the oracle on a bounded sample of the same batches --
     cpu = None

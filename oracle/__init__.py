@@ -265,3 +265,36 @@ def sage_forward(blocks: Blocks, H0: np.ndarray, Ws, bf16: bool = False, keep=Fa
         trace.append((agg, H))
         X = H
     return (X, trace) if keep else X
+
+
+def sage_forward_rows(blocks: Blocks, H0: np.ndarray, Ws, out_rows, bf16: bool = False):
+    """Logits of the destination rows ``out_rows`` of F_0 only.
+
+    Same arithmetic as ``sage_forward``, restricted to the receptive field
+    of the requested rows: layer l is evaluated only at the rows that layer
+    l+1 reads (its own destination rows and their sampled neighbours).
+    Rows outside the receptive field are never read, so they stay zero.
+    """
+    L = blocks.n_hops
+    need = [None] * (L + 1)          # need[l]: rows of H^l that must be computed
+    need[L] = np.unique(np.asarray(out_rows, dtype=np.int64))
+    for l in range(L, 1, -1):
+        b = L - l + 1                # layer l reads block b
+        ip, ix = blocks.indptr[b - 1], blocks.indices[b - 1]
+        rows = need[l]
+        nb = [ix[ip[i]:ip[i + 1]] for i in rows]
+        cat = np.concatenate([rows] + [x.astype(np.int64) for x in nb]) if len(rows) else rows
+        need[l - 1] = np.unique(cat)
+    X = np.asarray(H0, dtype=np.float64)
+    for l in range(1, L + 1):
+        b = L - l + 1
+        last = l == L
+        rows = need[l]
+        part = sage_layer(blocks.indptr[b - 1], blocks.indices[b - 1], X, Ws[l - 1],
+                          relu=not last, bf16=bf16, round_out=not last, rows=rows)
+        if last:
+            order = np.searchsorted(rows, np.asarray(out_rows, dtype=np.int64))
+            return part[order]
+        full = np.zeros((blocks.sizes[b - 1], Ws[l - 1].shape[1]), np.float64)
+        full[rows] = part
+        X = full

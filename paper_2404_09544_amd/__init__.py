@@ -136,7 +136,7 @@ class Graph:
         return rp, col[:self.nnz]
 
     def close(self):
-        if getattr(self, "_h", None):
+        if getattr(self, "_h", None) and _lib is not None:
             _lib.gnnav_graph_free(self._h)
             self._h = None
 
@@ -173,7 +173,7 @@ class Cache:
         return out[:self.n]
 
     def close(self):
-        if getattr(self, "_h", None):
+        if getattr(self, "_h", None) and _lib is not None:
             _lib.gnnav_cache_free(self._h)
             self._h = None
 
@@ -224,7 +224,7 @@ class Blocks:
         return nodes, sizes, ip, nb, ix
 
     def close(self):
-        if getattr(self, "_h", None):
+        if getattr(self, "_h", None) and _lib is not None:
             _lib.gnnav_blocks_free(self._h)
             self._h = None
 

@@ -676,24 +676,30 @@ extern "C" gnnav_status gnnav_sage_forward(gnnav_blocks *b, const void *x_dev, i
             b->hid[0].ensure(hid_bytes, s);
             b->hid[1].ensure(hid_bytes, s);
         }
+        static const char *kAggLabel[] = {"aggregate_mean.l1", "aggregate_mean.l2", "aggregate_mean.l3",
+                                          "aggregate_mean.l4+"};
+        static const char *kGemmLabel[] = {"combine_gemm.l1", "combine_gemm.l2", "combine_gemm.l3",
+                                           "combine_gemm.l4+"};
         const void *x = x_dev;
         int64_t ldx = ld_x;
         for (int l = 1; l <= L; ++l) {
+            const int tag = l < 4 ? l - 1 : 3;
             const int hb = L - l + 1;
             const int64_t rows = b->n_h[hb - 1];
             const int64_t din = dims[l - 1], dout = dims[l];
             const int64_t lda = padded_ld(din, elt);
             launch_aggregate_mean(b->indptr[hb - 1].as<int32_t>(), b->indices[hb - 1].as<int32_t>(), rows, x, ldx,
-                                  din, bf, b->agg.p, lda, s);
+                                  din, bf, b->agg.p, lda, s, kAggLabel[tag]);
             if (l < L) {
                 void *h = b->hid[l & 1].p;
                 const int64_t ldh = padded_ld(dout, elt);
-                launch_combine(x, ldx, b->agg.p, lda, rows, din, W_dev[l - 1], dout, bf, true, bf, h, ldh, s);
+                launch_combine(x, ldx, b->agg.p, lda, rows, din, W_dev[l - 1], dout, bf, true, bf, h, ldh, s,
+                               kGemmLabel[tag]);
                 x = h;
                 ldx = ldh;
             } else {
                 launch_combine(x, ldx, b->agg.p, lda, rows, din, W_dev[l - 1], dout, bf, false, false, logits_dev,
-                               ld_out, s);
+                               ld_out, s, kGemmLabel[tag]);
             }
         }
     });

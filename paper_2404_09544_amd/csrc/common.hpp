@@ -194,11 +194,12 @@ void launch_gather_rows(const GatherArgs &a, bool hits, hipStream_t s);
 // spmm.hip
 void launch_aggregate_mean(const int32_t *indptr, const int32_t *indices, int64_t n_dst,
                            const void *x, int64_t ld_x, int64_t d, bool bf16, void *out,
-                           int64_t ld_out, hipStream_t s);
+                           int64_t ld_out, hipStream_t s, const char *label = "aggregate_mean");
 
 // gemm.hip
 void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
                     int64_t d_in, const void *w, int64_t d_out, bool bf16, bool relu,
-                    bool out_bf16, void *out, int64_t ld_out, hipStream_t s);
+                    bool out_bf16, void *out, int64_t ld_out, hipStream_t s,
+                    const char *label = "combine_gemm");
 
 }  // namespace gnnav

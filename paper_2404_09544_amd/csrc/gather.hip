@@ -98,8 +98,10 @@ void launch_gather_rows(const GatherArgs &a, bool hits, hipStream_t s) {
     const int64_t rows_bound = a.n_ids;
     if (rows_bound <= 0 || chunks <= 0) return;
     const int rows_per_block = (256 / kWave) * (kWave / g);
-    // The miss path needs only enough waves to cover host-link latency.
-    const unsigned grid = grid_for(rows_bound, rows_per_block, hits ? 8192 : 1024);
+    // The miss path needs only enough waves to cover the host link's latency
+    // (64 workgroups keep it at ~53 GB/s); more of them queue slow host reads
+    // in the memory system and stall the concurrent HBM copy of the hits.
+    const unsigned grid = grid_for(rows_bound, rows_per_block, hits ? 8192 : 64);
     const int2 *list = hits ? a.hit_list : a.miss_list;
     const int32_t *cnt = a.dev_counts + (hits ? 0 : 1);
     const uint4 *src = (const uint4 *)(hits ? a.cache : a.store);

@@ -252,10 +252,10 @@ __global__ void __launch_bounds__(256) k_combine_bf16(const uint16_t *__restrict
 template <int BN>
 static void launch_combine_bn(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
                               int64_t d_in, const void *w, int64_t d_out, bool bf16, bool relu,
-                              bool out_bf16, void *out, int64_t ld_out, hipStream_t s) {
+                              bool out_bf16, void *out, int64_t ld_out, hipStream_t s, const char *label) {
     constexpr int BM = 64;
     const dim3 grid((unsigned)((m + BM - 1) / BM), (unsigned)((d_out + BN - 1) / BN));
-    KernelTimer t("combine_gemm", s);
+    KernelTimer t(label, s);
     if (!bf16) {
         if (out_bf16) fail(GNNAV_E_INVALID, "bf16 output needs bf16 operands");
         hipLaunchKernelGGL((k_combine_f32<BM, BN, float>), grid, dim3(256), 0, s, (const float *)self, ld_self,
@@ -275,13 +275,14 @@ static void launch_combine_bn(const void *self, int64_t ld_self, const void *agg
 
 void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m, int64_t d_in,
                     const void *w, int64_t d_out, bool bf16, bool relu, bool out_bf16, void *out,
-                    int64_t ld_out, hipStream_t s) {
+                    int64_t ld_out, hipStream_t s, const char *label) {
     if (m <= 0) return;
     if (d_out <= 64)
-        launch_combine_bn<64>(self, ld_self, agg, ld_agg, m, d_in, w, d_out, bf16, relu, out_bf16, out, ld_out, s);
+        launch_combine_bn<64>(self, ld_self, agg, ld_agg, m, d_in, w, d_out, bf16, relu, out_bf16, out, ld_out, s,
+                              label);
     else
         launch_combine_bn<128>(self, ld_self, agg, ld_agg, m, d_in, w, d_out, bf16, relu, out_bf16, out, ld_out,
-                               s);
+                               s, label);
 }
 
 }  // namespace gnnav

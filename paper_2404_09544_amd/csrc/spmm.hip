@@ -119,7 +119,8 @@ __global__ void __launch_bounds__(256) k_spmm_mean(const int32_t *__restrict__ i
 
 template <bool BF16>
 static void launch_spmm_t(const int32_t *indptr, const int32_t *indices, int64_t n_dst, const void *x,
-                          int64_t ld_x, int64_t d, void *out, int64_t ld_out, hipStream_t s) {
+                          int64_t ld_x, int64_t d, void *out, int64_t ld_out, hipStream_t s,
+                          const char *label) {
     constexpr int elt = BF16 ? 2 : 4;
     const int32_t chunks = (int32_t)((d * elt + 15) / 16);
     int g = 1;
@@ -131,7 +132,7 @@ static void launch_spmm_t(const int32_t *indptr, const int32_t *indices, int64_t
     const uint4 *xx = (const uint4 *)x;
     uint4 *oo = (uint4 *)out;
     const int64_t xl = ld_x * elt / 16, ol = ld_out * elt / 16;
-    KernelTimer t("aggregate_mean", s);
+    KernelTimer t(label, s);
 #define GNNAV_L(GV, QV)                                                                             \
     hipLaunchKernelGGL((k_spmm_mean<BF16, GV, QV>), dim3(grid), dim3(256), 0, s, indptr, indices,     \
                        n_dst, xx, xl, oo, ol, chunks, (int32_t)d)
@@ -158,12 +159,13 @@ static void launch_spmm_t(const int32_t *indptr, const int32_t *indices, int64_t
 }
 
 void launch_aggregate_mean(const int32_t *indptr, const int32_t *indices, int64_t n_dst, const void *x,
-                           int64_t ld_x, int64_t d, bool bf16, void *out, int64_t ld_out, hipStream_t s) {
+                           int64_t ld_x, int64_t d, bool bf16, void *out, int64_t ld_out, hipStream_t s,
+                           const char *label) {
     if (n_dst <= 0) return;
     if (bf16)
-        launch_spmm_t<true>(indptr, indices, n_dst, x, ld_x, d, out, ld_out, s);
+        launch_spmm_t<true>(indptr, indices, n_dst, x, ld_x, d, out, ld_out, s, label);
     else
-        launch_spmm_t<false>(indptr, indices, n_dst, x, ld_x, d, out, ld_out, s);
+        launch_spmm_t<false>(indptr, indices, n_dst, x, ld_x, d, out, ld_out, s, label);
 }
 
 }  // namespace gnnav

@@ -17,15 +17,21 @@ def row_errors(gpu: np.ndarray, ref: np.ndarray):
     return diff, norm
 
 
-def assert_rows_close(gpu, ref, tol: float, what: str = ""):
+def assert_rows_close(gpu, ref, tol: float, what: str = "", floor=None):
     """Per-row relative L2 error <= tol.
 
     Rows whose reference norm is below 1e-3 of the median row norm (rows a
     ReLU has mapped to, or near, zero) are held to an absolute bound of
     tol * median row norm instead, since a relative error is meaningless
-    there.  Returns the worst relative error seen on the regular rows.
+    there.  ``floor`` (per-row norms) raises each row's denominator to the
+    scale of its rounding error where the result cancels: for a sum that is
+    the same sum over absolute values (the classical summation error bound
+    is proportional to it).  Returns the worst relative error on the regular
+    rows.
     """
     diff, norm = row_errors(gpu, ref)
+    if floor is not None:
+        norm = np.maximum(norm, np.asarray(floor, dtype=np.float64))
     if diff.size == 0:
         return 0.0
     med = float(np.median(norm)) if np.any(norm > 0) else 0.0

@@ -1,0 +1,101 @@
+"""GPU parity at the full workload sizes, in the launch configuration bench.py times.
+
+For each workload: the device CSR equals the oracle's; a batch through
+MiniBatchStep (the bench's step) gives frontiers, blocks, gathered rows and
+hit/miss counts identical to the oracle's; the logits of sampled seed rows
+match the oracle's receptive-field forward within tolerance.  The 10M-node
+R-MAT workload runs at cache fractions 0, 0.25 and 1.
+"""
+import sys
+import time
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from parity_util import BF16_TOL, FP32_TOL, assert_rows_close
+
+pytestmark = pytest.mark.gpu
+
+FULL = ["chunglu-169k-d128", "chunglu-233k-d602", "chunglu-2450k-d100", "rmat-10m-d128"]
+_state = {}
+
+
+def say(*a):
+    print("[full]", *a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def G():
+    import torch
+    assert torch.cuda.is_available()
+    import paper_2404_09544_amd as g
+    yield g
+    _state.clear()
+
+
+def load(G, name):
+    if name in _state:
+        return _state[name]
+    _state.clear()
+    t = time.perf_counter()
+    wl = W.Workload(name)
+    src, dst = wl.edges()
+    say(name, f"edges {src.size} pairs ({time.perf_counter() - t:.1f}s)")
+    csr = O.build_csr(wl.n, src, dst)
+    say(name, f"oracle CSR nnz={csr.nnz} ({time.perf_counter() - t:.1f}s)")
+    g = G.Graph(wl.n, src, dst, offsets_i64=wl.cfg["offsets_i64"])
+    say(name, f"device CSR ({time.perf_counter() - t:.1f}s)")
+    _state[name] = (wl, src, dst, csr, g)
+    return _state[name]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_csr(G, name):
+    wl, _, _, csr, g = load(G, name)
+    rp, col = g.csr_host()
+    assert g.offsets_i64 == wl.cfg["offsets_i64"]
+    assert np.array_equal(rp, csr.row_ptr)
+    assert np.array_equal(col, csr.col)
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_batch(G, name):
+    import torch
+    from paper_2404_09544_amd.step import MiniBatchStep, to_device_weights
+    wl, _, _, csr, g = load(G, name)
+    feats = wl.features()
+    ws = wl.weights()
+    wd = [O.to_f64(w, wl.dtype) for w in ws]
+    bf16 = wl.dtype == "bf16"
+    tol = BF16_TOL if bf16 else FP32_TOL
+    sweep = wl.cfg.get("cache_sweep", [wl.cfg["cache"]])
+    for r in sweep:
+        t = time.perf_counter()
+        c = G.Cache(g, feats, wl.dtype, r, store_on_device=wl.cfg["store_on_device"])
+        step = MiniBatchStep(g, c, to_device_weights(ws, wl.dtype), wl.dims, wl.fanouts, wl.dtype)
+        _, slot, _ = O.rank_cache(csr, r)
+        for b in ([7] if wl.n > 1_000_000 else [0, 7]):
+            say(name, f"r={r} batch {b}")
+            seeds = wl.seeds(b)
+            logits = step.run(torch.from_numpy(seeds).cuda(), wl.rng_seed(b))
+            got_logits = logits.cpu().numpy()
+            nodes, sizes, ip, nb, ix = step.blocks.to_host()
+            ref_b = O.sample_blocks(csr, seeds, wl.fanouts, wl.rng_seed(b))
+            assert sizes == ref_b.sizes
+            assert np.array_equal(nodes, ref_b.nodes)
+            for h in range(wl.L):
+                assert np.array_equal(ip[h], ref_b.indptr[h]), f"indptr hop {h + 1}"
+                assert np.array_equal(nb[h], ref_b.nbrs[h]), f"neighbours hop {h + 1}"
+                assert np.array_equal(ix[h], ref_b.indices[h]), f"indices hop {h + 1}"
+            h0, counts = O.gather(feats, slot, ref_b.nodes)
+            assert np.array_equal(step.counts.cpu().numpy(), counts)
+            got_h0 = step.h0_view().cpu().numpy()[:, :wl.d]
+            assert np.array_equal(got_h0.view(np.uint8), h0.view(np.uint8))
+            rows = np.random.default_rng(b).choice(sizes[0], size=min(96, sizes[0]), replace=False)
+            ref = O.sage_forward_rows(ref_b, O.to_f64(h0, wl.dtype), wd, rows, bf16=bf16)
+            assert_rows_close(got_logits[rows], ref, tol, f"{name} r={r} logits")
+            say(name, f"r={r} batch {b}: sizes {sizes} hits/misses {counts.tolist()} "
+                      f"({time.perf_counter() - t:.1f}s)")
+        c.close()

@@ -244,9 +244,12 @@ def test_aggregate_mean_parity(G, d, dtype):
     Wt = np.concatenate([np.zeros((d, 1)), np.zeros((d, 1))])
     _, agg = O.sage_layer(ip, ix, O.to_f64(X, dtype), Wt, relu=False, bf16=dtype == "bf16",
                           round_out=False, want_agg=True)
+    _, agg_abs = O.sage_layer(ip, ix, np.abs(O.to_f64(X, dtype)), Wt, relu=False, bf16=False,
+                              round_out=False, want_agg=True)
     empty = np.diff(ip) == 0
     assert not got[empty].any()
-    assert_rows_close(got[~empty], agg[~empty], BF16_TOL if dtype == "bf16" else FP32_TOL, "aggregate")
+    assert_rows_close(got[~empty], agg[~empty], BF16_TOL if dtype == "bf16" else FP32_TOL, "aggregate",
+                      floor=np.linalg.norm(agg_abs[~empty], axis=1))
     if ld > d:
         elt = 2 if dtype == "bf16" else 4
         tail = (-(d * elt)) % 16 // elt

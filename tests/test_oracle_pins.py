@@ -447,3 +447,19 @@ def test_sage_rows_subset_matches_full():
     rows = np.array([0, 7, 3, 49], np.int64)
     part = O.sage_layer(b.indptr[0], b.indices[0], X, Wt, True, False, False, rows=rows)
     np.testing.assert_array_equal(part, full[rows])
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_forward_rows_matches_full_forward(bf16):
+    """The receptive-field forward equals the full forward on the rows asked for."""
+    n, u, v = W.random_graph(n=400, m=3000, seed=17)
+    csr = O.build_csr(n, u, v)
+    b = O.sample_blocks(csr, np.arange(0, n, 5, dtype=np.int32), [4, 3, 2], 21)
+    dt = "bf16" if bf16 else "f32"
+    dims = [6, 5, 4, 3]
+    H0 = O.to_f64(W.features(b.sizes[3], dims[0], dt, seed=2), dt)
+    Ws = [O.to_f64(W.glorot(dims[l], dims[l + 1], dt, seed=l), dt) for l in range(3)]
+    full = O.sage_forward(b, H0, Ws, bf16=bf16)
+    rows = np.array([7, 0, 79, 33, 7], np.int64)
+    part = O.sage_forward_rows(b, H0, Ws, rows, bf16=bf16)
+    np.testing.assert_array_equal(part, full[rows])
