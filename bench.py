@@ -93,7 +93,7 @@ def main():
     import torch
     import workloads as W
     import paper_2404_09544_amd as G
-    from paper_2404_09544_amd.step import MiniBatchStep, to_device_weights
+    from paper_2404_09544_amd.step import MiniBatchStep, Pipeline, to_device_weights
 
     torch.cuda.set_device(0)
     wl = W.Workload(args.workload)
@@ -108,39 +108,67 @@ def main():
     log(f"graph nnz={g.nnz} max_deg={g.max_degree}; cache C={c.n_cached} ld={c.ld} "
         f"({time.perf_counter() - t0:.1f}s)")
     ws = wl.weights()
-    step = MiniBatchStep(g, c, to_device_weights(ws, wl.dtype), wl.dims, wl.fanouts, wl.dtype)
+    wdev = to_device_weights(ws, wl.dtype)
+    step = MiniBatchStep(g, c, wdev, wl.dims, wl.fanouts, wl.dtype)
     n_b = args.warmup + args.steps
     seeds_dev = [torch.from_numpy(wl.seeds(b)).cuda() for b in range(n_b)]
+    L = wl.L
     counts_hist = torch.zeros((n_b, 3), dtype=torch.int64, device="cuda")
-    sizes_hist = []
+    sizes_dev_hist = torch.zeros((n_b, L + 1), dtype=torch.int32, device="cuda")
+
+    def record(slot, b, st):
+        """Copy this batch's counts and frontier sizes aside on its own stream."""
+        ptr, _ = slot.blocks.device_sizes(L)
+        with torch.cuda.stream(st):
+            counts_hist[b].copy_(slot.counts)
+            G._copy_device_i32(sizes_dev_hist[b], ptr, L + 1)
+
+    # ---- phase 1: sequential steps on one stream, every kernel timed -----
+    # One batch after another with no host synchronisation between batches;
+    # the library records HIP events around each kernel (per-kernel figures
+    # and the roofline come from this region).
     stream = torch.cuda.current_stream()
-
     for b in range(args.warmup):
-        step.run(seeds_dev[b], wl.rng_seed(b), stream)
-        counts_hist[b].copy_(step.counts)
+        step.enqueue(seeds_dev[b], wl.rng_seed(b), stream)
+        record(step, b, stream)
     torch.cuda.synchronize()
-
     G.profile_start()
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for b in range(args.warmup, n_b):
-        step.run(seeds_dev[b], wl.rng_seed(b), stream)
-        counts_hist[b].copy_(step.counts)
-        sizes_hist.append(list(step.sizes))
+        step.enqueue(seeds_dev[b], wl.rng_seed(b), stream)
+        record(step, b, stream)
     torch.cuda.synchronize()
     t_end = time.perf_counter()
     prof = G.profile_stop()
+    seq_elapsed = t_end - t_start
+    seq_ms = seq_elapsed * 1e3 / args.steps
+    log(f"sequential {args.steps} steps: {seq_ms:.3f} ms/step, {wl.batch * args.steps / seq_elapsed:,.0f} seeds/s")
+
+    # ---- phase 2: the two-stream pipeline (batch b+1 overlaps batch b) ----
+    pipe = Pipeline(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, depth=2)
+    for b in range(args.warmup):
+        slot = pipe.enqueue(seeds_dev[b], wl.rng_seed(b))
+    pipe.synchronize()
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for b in range(args.warmup, n_b):
+        slot = pipe.enqueue(seeds_dev[b], wl.rng_seed(b))
+        record(slot, b, pipe.streams[(pipe.count - 1) % pipe.depth])
+    pipe.synchronize()
+    torch.cuda.synchronize()
+    t_end = time.perf_counter()
     elapsed = t_end - t_start
     ms_per_step = elapsed * 1e3 / args.steps
     seeds_per_s = wl.batch * args.steps / elapsed
     counts = counts_hist[args.warmup:].cpu().numpy()
-    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, {seeds_per_s:,.0f} seeds/s")
+    sizes_hist = sizes_dev_hist[args.warmup:].cpu().numpy().tolist()
+    log(f"pipelined {args.steps} steps: {ms_per_step:.3f} ms/step, {seeds_per_s:,.0f} seeds/s")
 
     # ---- algorithmic work per timed batch, from the measured sizes -------
     # Re-sampling a batch is deterministic, so the blocks of each timed batch
     # are regenerated here (untimed) to count distinct source rows.
     elt = 2 if wl.dtype == "bf16" else 4
-    L = wl.L
     work = {"gather_hit": 0.0, "gather_miss": 0.0}
     edge = {}
     probe = G.Blocks()
@@ -215,6 +243,16 @@ def main():
                          f"{args.warmup + nb - 1}), single-threaded C oracle, {ct:.1f}s"}
         log(f"oracle: {cpu['value']} seeds/s")
 
+    # Eq. 4 terms per batch from the sequential region: the host-link part
+    # (t_transfer = miss copy), the sampling kernels, and the device compute.
+    def per_batch(names):
+        return sum(prof[n][1] for n in names if n in prof) / args.steps
+    samp = ["dedup_first", "dedup_scan", "count_scan", "sample_hop", "relabel", "reset_map"]
+    comp = [n for n in prof if n.startswith(("aggregate_mean", "combine_gemm"))] + ["classify", "gather_hit"]
+    eq4 = {"t_sample_ms": round(per_batch(samp), 4), "t_transfer_ms": round(per_batch(["gather_miss"]), 4),
+           "t_compute_ms": round(per_batch(comp), 4), "sequential_ms_per_step": round(seq_ms, 4),
+           "pipelined_ms_per_step": round(ms_per_step, 4)}
+    eq4["eq4_max_ms"] = round(max(eq4["t_sample_ms"] + eq4["t_transfer_ms"], eq4["t_compute_ms"]), 4)
     mean_sizes = np.mean(np.array(sizes_hist), axis=0).round(1).tolist()
     hit_rate = float(counts[:, 0].sum() / max(counts[:, :2].sum(), 1))
     out = {
@@ -225,9 +263,11 @@ def main():
         "config": {"workload": wl.name, "n": wl.n, "nnz": g.nnz, "d": wl.d, "fanouts": wl.fanouts,
                    "batch": wl.batch, "layers": wl.L, "dims": wl.dims, "cache_fraction": r,
                    "store_on_device": wl.cfg["store_on_device"], "global_batch": wl.batch},
+        "value_sequential": round(wl.batch * args.steps / seq_elapsed, 2),
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kernels,
+        "eq4": eq4,
         "batch_stats": {"mean_frontier_sizes": mean_sizes, "hit_rate": round(hit_rate, 4),
                         "miss_bytes_per_batch": round(float(counts[:, 1].mean()) * wl.d * elt, 1)},
     }

@@ -152,6 +152,31 @@ gnnav_status gnnav_sample(const gnnav_graph *g, const int32_t *seeds_dev, int64_
                           const int32_t *fanouts, int32_t n_hops, uint64_t rng_seed,
                           gnnav_blocks *blocks, void *stream);
 
+/* gnnav_sample without the final synchronisation: every kernel is enqueued
+ * on `stream` and the call returns at once; frontier and hop sizes stay in
+ * device memory.  Later work on the same stream (gnnav_gather_n,
+ * gnnav_sage_forward) reads them there.  Host-side size views
+ * (gnnav_blocks_hop, n_per_hop of gnnav_blocks_nodes) need
+ * gnnav_blocks_sync first.  A seed outside [0, n) is skipped and reported
+ * as E_RANGE by the next gnnav_blocks_sync.  Same errors as gnnav_sample
+ * otherwise (argument and capacity checks happen before anything is
+ * enqueued).                                                               */
+gnnav_status gnnav_sample_async(const gnnav_graph *g, const int32_t *seeds_dev, int64_t n_seeds,
+                                const int32_t *fanouts, int32_t n_hops, uint64_t rng_seed,
+                                gnnav_blocks *blocks, void *stream);
+
+/* Waits for `stream` and copies the last sample's sizes to the host.
+ * Errors: E_INVALID (never sampled), E_RANGE (seeds outside [0, n) were
+ * skipped), E_DEVICE.                                                      */
+gnnav_status gnnav_blocks_sync(gnnav_blocks *b, void *stream);
+
+/* Device view of the last sample's sizes, valid once the sample's kernels
+ * have run: (*sizes_dev)[h] = |F_h| for h = 0..L and (*sizes_dev)[17 + h] =
+ * E_h for h = 1..L (int32).  bounds (host int64[L+1], may be NULL) receives
+ * the Eq. 12 capacity bounds the buffers were sized for.                  */
+gnnav_status gnnav_blocks_device_sizes(const gnnav_blocks *b, const int32_t **sizes_dev,
+                                       int64_t *bounds);
+
 /* View of hop h (1..n_hops) of the last gnnav_sample. */
 gnnav_status gnnav_blocks_hop(const gnnav_blocks *b, int32_t hop, gnnav_block_view *out);
 
@@ -166,7 +191,8 @@ gnnav_status gnnav_blocks_nodes(const gnnav_blocks *b, const int32_t **nodes_dev
  * stride ld_out elements of the cache dtype) becomes the feature row of
  * ids_dev[i].  Cached vertices are copied from HBM; the rest are read from
  * the host store by zero-copy loads over the host-device link, on a second
- * stream that joins `stream` before the call's work completes.  Each row
+ * stream that joins `stream` before the call's work completes.  Gathers on
+ * the same cache from different streams may overlap.  Each row
  * copies ceil(d * elt / 16) 16-byte units: the columns from d up to the
  * next 16-byte boundary are written with zeros; later columns are untouched.
  * An id outside [0, n) gives a zero row and counts as invalid.
@@ -177,6 +203,15 @@ gnnav_status gnnav_blocks_nodes(const gnnav_blocks *b, const int32_t **nodes_dev
  * E_DEVICE.                                                               */
 gnnav_status gnnav_gather(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_ids,
                           void *out_dev, int64_t ld_out, int64_t *counts_dev, void *stream);
+
+/* gnnav_gather with the request count read from device memory (e.g. the
+ * |F_L| entry of gnnav_blocks_device_sizes) when the work runs.  out_dev
+ * must hold n_ids_max rows; counts as gnnav_gather.  Calls on different
+ * streams may overlap: each stream gets its own scratch inside the cache.
+ * Errors as gnnav_gather, plus E_INVALID for a NULL n_ids_dev.            */
+gnnav_status gnnav_gather_n(const gnnav_cache *c, const int32_t *ids_dev, const int32_t *n_ids_dev,
+                            int64_t n_ids_max, void *out_dev, int64_t ld_out, int64_t *counts_dev,
+                            void *stream);
 
 /* ------------------------------------------------------- SAGE, per layer ---
  * Eq. 1 Aggregate, GraphSAGE mean: for each destination row i < n_dst,
@@ -216,6 +251,8 @@ gnnav_status gnnav_combine(const void *self_dev, int64_t ld_self, const void *ag
  * |F_0| x dims[L] fp32 result (stride ld_out).  dt = BF16 keeps features,
  * weights, aggregates and hidden layers in bfloat16 (fp32 accumulation);
  * the logits stay fp32.  Intermediate buffers live in `b` and are reused.
+ * After gnnav_sample_async (no gnnav_blocks_sync) the row counts are read
+ * from device memory and logits_dev must hold min(n_seeds, n) rows.
  * Errors: E_INVALID (null pointers, n_layers differs from the sampled
  * hops, dims <= 0, strides), E_NOMEM, E_DEVICE.  Asynchronous.            */
 gnnav_status gnnav_sage_forward(gnnav_blocks *b, const void *x_dev, int64_t ld_x,

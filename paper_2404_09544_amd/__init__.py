@@ -29,7 +29,8 @@ EXPORTS = [
     "gnnav_last_error", "gnnav_abi_version", "gnnav_build_csr", "gnnav_graph_info",
     "gnnav_graph_csr_host", "gnnav_graph_free", "gnnav_build_cache", "gnnav_cache_info",
     "gnnav_cache_slot_map_host", "gnnav_cache_free", "gnnav_blocks_create", "gnnav_blocks_free",
-    "gnnav_sample", "gnnav_blocks_hop", "gnnav_blocks_nodes", "gnnav_gather",
+    "gnnav_sample", "gnnav_sample_async", "gnnav_blocks_sync", "gnnav_blocks_device_sizes",
+    "gnnav_blocks_hop", "gnnav_blocks_nodes", "gnnav_gather", "gnnav_gather_n",
     "gnnav_aggregate_mean", "gnnav_combine", "gnnav_sage_forward", "gnnav_profile_start",
     "gnnav_profile_stop", "gnnav_profile_count", "gnnav_profile_get",
 ]
@@ -62,6 +63,10 @@ _sig = {
     "gnnav_blocks_create": ([P], i32),
     "gnnav_blocks_free": ([P], None),
     "gnnav_sample": ([P, P, i64, P, i32, u64, P, P], i32),
+    "gnnav_sample_async": ([P, P, i64, P, i32, u64, P, P], i32),
+    "gnnav_blocks_sync": ([P, P], i32),
+    "gnnav_blocks_device_sizes": ([P, P, P], i32),
+    "gnnav_gather_n": ([P, P, P, i64, P, i64, P, P], i32),
     "gnnav_blocks_hop": ([P, i32, C.POINTER(BlockView)], i32),
     "gnnav_blocks_nodes": ([P, P, P, P], i32),
     "gnnav_gather": ([P, P, i64, P, i64, P, P], i32),
@@ -202,6 +207,22 @@ class Blocks:
         _check(_lib.gnnav_blocks_nodes(self._h, C.byref(ptr), _np_ptr(n), None))
         return [int(x) for x in n], ptr.value
 
+    def sync(self, stream=None):
+        """Publish the last (async) sample's sizes to the host."""
+        _check(_lib.gnnav_blocks_sync(self._h, _stream(stream)))
+
+    def device_sizes(self, n_hops: int):
+        """(device pointer to the int32 size array, host Eq. 12 bounds [L+1])."""
+        ptr = P()
+        bounds = np.zeros(n_hops + 1, np.int64)
+        _check(_lib.gnnav_blocks_device_sizes(self._h, C.byref(ptr), _np_ptr(bounds)))
+        return ptr.value, [int(x) for x in bounds]
+
+    def nodes_ptr(self) -> int:
+        ptr = P()
+        _check(_lib.gnnav_blocks_nodes(self._h, C.byref(ptr), None, None))
+        return ptr.value
+
     def to_host(self):
         """Host copies: (nodes, sizes, [indptr], [neighbors], [indices])."""
         import torch
@@ -246,6 +267,23 @@ def _hip_memcpy_d2h(dst: np.ndarray, src_ptr: int, nbytes: int):
         raise GnnavError(5, f"hipMemcpy failed ({rc})")
 
 
+def _copy_device_i32(dst, src_ptr: int, count: int):
+    """Enqueue a device-to-device copy of `count` int32 from src_ptr into the
+    torch tensor dst on torch's current stream (bookkeeping, not the path)."""
+    global _hip
+    if _hip is None:
+        _hip = C.CDLL("libamdhip64.so")
+        _hip.hipMemcpy.argtypes = [P, P, C.c_size_t, C.c_int]
+        _hip.hipMemcpy.restype = C.c_int
+    fn = _hip.hipMemcpyAsync
+    fn.argtypes = [P, P, C.c_size_t, C.c_int, P]
+    fn.restype = C.c_int
+    import torch
+    rc = fn(dst.data_ptr(), src_ptr, count * 4, 3, torch.cuda.current_stream().cuda_stream)
+    if rc != 0:
+        raise GnnavError(5, f"hipMemcpyAsync failed ({rc})")
+
+
 # --------------------------------------------------------------- the path
 def sample(graph: Graph, seeds, fanouts, rng_seed: int, blocks: Blocks, stream=None):
     """gnnav_sample: seeds is a device int32 tensor."""
@@ -253,6 +291,20 @@ def sample(graph: Graph, seeds, fanouts, rng_seed: int, blocks: Blocks, stream=N
     _check(_lib.gnnav_sample(graph._h, _dev_ptr(seeds), seeds.numel(), _np_ptr(fan), fan.size,
                              int(rng_seed) & 0xFFFFFFFFFFFFFFFF, blocks._h, _stream(stream)))
     return blocks
+
+
+def sample_async(graph: Graph, seeds, fanouts, rng_seed: int, blocks: Blocks, stream=None):
+    """gnnav_sample_async: enqueue only; sizes stay on the device."""
+    fan = np.ascontiguousarray(fanouts, dtype=np.int32)
+    _check(_lib.gnnav_sample_async(graph._h, _dev_ptr(seeds), seeds.numel(), _np_ptr(fan), fan.size,
+                                   int(rng_seed) & 0xFFFFFFFFFFFFFFFF, blocks._h, _stream(stream)))
+    return blocks
+
+
+def gather_n(cache: Cache, ids_ptr: int, n_ids_dev_ptr: int, n_ids_max: int, out, counts, stream=None):
+    """gnnav_gather_n: the request count is read from device memory."""
+    _check(_lib.gnnav_gather_n(cache._h, ids_ptr, n_ids_dev_ptr, n_ids_max, _dev_ptr(out), out.stride(0),
+                               _dev_ptr(counts), _stream(stream)))
 
 
 def gather(cache: Cache, ids_ptr: int, n_ids: int, out, counts, stream=None):

@@ -276,7 +276,18 @@ extern "C" void gnnav_graph_free(gnnav_graph *g) {
     delete g;
 }
 
+static bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
 // ------------------------------------------------------------------ cache
+// Scratch of one gather in flight: hit/miss lists, scan partials, device
+// counts, and the second stream that carries the miss copy.  Each caller
+// stream gets its own, so gathers on different streams may overlap.
+struct GatherWs {
+    hipStream_t stream = nullptr, side = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+    DevBuf hit_list, miss_list, part, dev_counts;
+};
+
 struct gnnav_cache {
     int64_t n = 0, c = 0, d = 0, ld = 0, elt = 4;
     gnnav_dtype dt = GNNAV_F32;
@@ -285,10 +296,23 @@ struct gnnav_cache {
     void *store_host = nullptr;       // pinned, device-mapped
     void *store_ptr = nullptr;        // device-visible address of the store
     std::vector<int32_t> slot_host;
-    hipStream_t side = nullptr;
-    hipEvent_t fork = nullptr, join = nullptr;
-    DevBuf hit_list, miss_list, part, dev_counts;
+    std::mutex ws_mu;
+    std::vector<GatherWs *> ws;
 };
+
+static GatherWs *gather_ws(gnnav_cache *c, hipStream_t s) {
+    std::lock_guard<std::mutex> lk(c->ws_mu);
+    for (auto *w : c->ws)
+        if (w->stream == s) return w;
+    auto *w = new GatherWs();
+    w->stream = s;
+    c->ws.push_back(w);
+    GNNAV_HIP(hipStreamCreateWithFlags(&w->side, hipStreamNonBlocking));
+    GNNAV_HIP(hipEventCreateWithFlags(&w->fork, hipEventDisableTiming));
+    GNNAV_HIP(hipEventCreateWithFlags(&w->join, hipEventDisableTiming));
+    w->dev_counts.ensure(2 * sizeof(int32_t), s);
+    return w;
+}
 
 static void free_cache(gnnav_cache *c) {
     if (!c) return;
@@ -296,14 +320,17 @@ static void free_cache(gnnav_cache *c) {
     c->slot_map.release();
     c->cache_rows.release();
     c->store_dev.release();
-    c->hit_list.release();
-    c->miss_list.release();
-    c->part.release();
-    c->dev_counts.release();
+    for (auto *w : c->ws) {
+        w->hit_list.release();
+        w->miss_list.release();
+        w->part.release();
+        w->dev_counts.release();
+        if (w->side) (void)hipStreamDestroy(w->side);
+        if (w->fork) (void)hipEventDestroy(w->fork);
+        if (w->join) (void)hipEventDestroy(w->join);
+        delete w;
+    }
     if (c->store_host) (void)hipHostFree(c->store_host);
-    if (c->side) (void)hipStreamDestroy(c->side);
-    if (c->fork) (void)hipEventDestroy(c->fork);
-    if (c->join) (void)hipEventDestroy(c->join);
     delete c;
 }
 
@@ -393,10 +420,6 @@ extern "C" gnnav_status gnnav_build_cache(const gnnav_graph *g, const void *feat
                 });
                 GNNAV_HIP(hipHostGetDevicePointer(&c->store_ptr, c->store_host, 0));
             }
-            GNNAV_HIP(hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking));
-            GNNAV_HIP(hipEventCreateWithFlags(&c->fork, hipEventDisableTiming));
-            GNNAV_HIP(hipEventCreateWithFlags(&c->join, hipEventDisableTiming));
-            c->dev_counts.ensure(2 * sizeof(int32_t), s0);
         } catch (...) {
             free_cache(c);
             throw;
@@ -437,8 +460,11 @@ constexpr int kSizeSlots = 48;
 
 struct gnnav_blocks {
     int32_t L = 0;
+    bool host_sizes = false;           // n_h / e_h hold the last sample's sizes
     int64_t n_h[kMaxHops + 1] = {0};
     int64_t e_h[kMaxHops + 1] = {0};
+    int64_t nb[kMaxHops + 1] = {0};    // Eq. 12 capacity bounds of the last sample
+    int64_t eb[kMaxHops + 1] = {0};
     int64_t map_nodes = -1;
     DevBuf map, sizes, nodes, part;
     DevBuf indptr[kMaxHops], nbrs[kMaxHops], indices[kMaxHops];
@@ -479,75 +505,116 @@ extern "C" void gnnav_blocks_free(gnnav_blocks *b) {
     delete b;
 }
 
+// Enqueues the whole expansion on `s`; sizes stay in device memory.
+static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64_t n_seeds, const int32_t *fanouts,
+                       int32_t n_hops, uint64_t rng_seed, gnnav_blocks *b, hipStream_t s) {
+    GNNAV_CHECK(g && b && fanouts, GNNAV_E_INVALID, "NULL graph, blocks or fanouts");
+    GNNAV_CHECK(n_hops >= 1 && n_hops <= kMaxHops, GNNAV_E_INVALID, "n_hops outside [1, 16]");
+    GNNAV_CHECK(n_seeds >= 0, GNNAV_E_INVALID, "n_seeds < 0");
+    GNNAV_CHECK(n_seeds == 0 || seeds_dev, GNNAV_E_INVALID, "seeds_dev is NULL");
+    GNNAV_CHECK(n_seeds <= INT32_MAX, GNNAV_E_CAPACITY, "n_seeds above INT32_MAX");
+    for (int h = 0; h < n_hops; ++h)
+        GNNAV_CHECK(fanouts[h] <= 1024, GNNAV_E_INVALID, "fanout above 1024");
+    // Eq. 12 capacity bounds (tau = 1, no overlap): E_h <= n_(h-1) * k_h,
+    // n_h <= min(n, n_(h-1) + E_h).
+    int64_t nb[kMaxHops + 1], eb[kMaxHops + 1];
+    nb[0] = std::min<int64_t>(n_seeds, g->n);
+    eb[0] = 0;
+    for (int h = 1; h <= n_hops; ++h) {
+        const int64_t k = fanouts[h - 1] < 0 ? g->max_deg : std::min<int64_t>(fanouts[h - 1], g->max_deg);
+        eb[h] = nb[h - 1] * k;
+        nb[h] = std::min<int64_t>(g->n, nb[h - 1] + eb[h]);
+        GNNAV_CHECK(eb[h] < INT32_MAX && nb[h] < INT32_MAX, GNNAV_E_CAPACITY,
+                    "hop " + std::to_string(h) + " bound exceeds the int32 range");
+    }
+    int64_t max_list = n_seeds;
+    for (int h = 1; h <= n_hops; ++h) max_list = std::max(max_list, std::max(eb[h], nb[h - 1] + 1));
+    // workspace
+    if (b->map_nodes < g->n) {
+        b->map.ensure(std::max<int64_t>(g->n, 1) * sizeof(int32_t), s);
+        launch_fill_i32(b->map.as<int32_t>(), INT_MAX, g->n, s);
+        b->map_nodes = g->n;
+    }
+    b->sizes.ensure(kSizeSlots * sizeof(int32_t), s);
+    b->nodes.ensure(std::max<int64_t>(nb[n_hops], 1) * sizeof(int32_t), s);
+    b->part.ensure(scan_parts(max_list) * sizeof(int64_t), s);
+    for (int h = 1; h <= n_hops; ++h) {
+        b->indptr[h - 1].ensure((nb[h - 1] + 1) * sizeof(int32_t), s);
+        b->nbrs[h - 1].ensure(std::max<int64_t>(eb[h], 1) * sizeof(int32_t), s);
+        b->indices[h - 1].ensure(std::max<int64_t>(eb[h], 1) * sizeof(int32_t), s);
+    }
+    int32_t *sz = b->sizes.as<int32_t>();
+    int32_t *map = b->map.as<int32_t>();
+    int32_t *nodes = b->nodes.as<int32_t>();
+    int32_t *part = b->part.as<int32_t>();
+    launch_fill_i32(sz, 0, kSizeSlots, s);
+    // F_0: seeds without repeats, first occurrence kept
+    DedupArgs d0{seeds_dev, n_seeds, nullptr, n_seeds, map, g->n, nodes, nullptr, sz + kSizeN, sz + kSizeErr,
+                 part};
+    launch_dedup(d0, s);
+    for (int h = 1; h <= n_hops; ++h) {
+        SampleHopArgs a{g->row_ptr.p, g->i64, g->col.as<int32_t>(), nodes, sz + kSizeN + h - 1,
+                        b->indptr[h - 1].as<int32_t>(), b->nbrs[h - 1].as<int32_t>(), sz + kSizeE + h,
+                        fanouts[h - 1], rng_seed, (uint32_t)(h - 1), nb[h - 1], part};
+        launch_count_scan(a, s);
+        launch_sample_hop(a, s);
+        DedupArgs dh{b->nbrs[h - 1].as<int32_t>(), 0, sz + kSizeE + h, eb[h], map, g->n, nodes,
+                     sz + kSizeN + h - 1, sz + kSizeN + h, nullptr, part};
+        launch_dedup(dh, s);
+        launch_relabel(b->nbrs[h - 1].as<int32_t>(), sz + kSizeE + h, eb[h], map,
+                       b->indices[h - 1].as<int32_t>(), s);
+    }
+    launch_reset_map(nodes, sz + kSizeN + n_hops, nb[n_hops], map, s);
+    b->L = n_hops;
+    b->host_sizes = false;
+    for (int h = 0; h <= n_hops; ++h) {
+        b->nb[h] = nb[h];
+        b->eb[h] = eb[h];
+    }
+}
+
+// Copies the device sizes of the last sample to the host (waits on `s`).
+static void publish_sizes(gnnav_blocks *b, hipStream_t s) {
+    GNNAV_CHECK(b->sizes.p, GNNAV_E_INVALID, "blocks have not been sampled");
+    GNNAV_HIP(hipMemcpyAsync(b->sizes_host, b->sizes.p, kSizeSlots * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    GNNAV_HIP(hipStreamSynchronize(s));
+    for (int h = 0; h <= b->L; ++h) b->n_h[h] = b->sizes_host[kSizeN + h];
+    for (int h = 1; h <= b->L; ++h) b->e_h[h] = b->sizes_host[kSizeE + h];
+    b->host_sizes = true;
+    GNNAV_CHECK(b->sizes_host[kSizeErr] == 0, GNNAV_E_RANGE,
+                std::to_string(b->sizes_host[kSizeErr]) + " seed(s) outside [0, n)");
+}
+
 extern "C" gnnav_status gnnav_sample(const gnnav_graph *g, const int32_t *seeds_dev, int64_t n_seeds,
                                      const int32_t *fanouts, int32_t n_hops, uint64_t rng_seed,
                                      gnnav_blocks *b, void *stream) {
     return guarded([&] {
-        GNNAV_CHECK(g && b && fanouts, GNNAV_E_INVALID, "NULL graph, blocks or fanouts");
-        GNNAV_CHECK(n_hops >= 1 && n_hops <= kMaxHops, GNNAV_E_INVALID, "n_hops outside [1, 16]");
-        GNNAV_CHECK(n_seeds >= 0, GNNAV_E_INVALID, "n_seeds < 0");
-        GNNAV_CHECK(n_seeds == 0 || seeds_dev, GNNAV_E_INVALID, "seeds_dev is NULL");
-        GNNAV_CHECK(n_seeds <= INT32_MAX, GNNAV_E_CAPACITY, "n_seeds above INT32_MAX");
-        for (int h = 0; h < n_hops; ++h)
-            GNNAV_CHECK(fanouts[h] <= 1024, GNNAV_E_INVALID, "fanout above 1024");
-        hipStream_t s = (hipStream_t)stream;
-        // Eq. 12 capacity bounds (tau = 1, no overlap): E_h <= n_(h-1) * k_h,
-        // n_h <= min(n, n_(h-1) + E_h).
-        int64_t nb[kMaxHops + 1], eb[kMaxHops + 1];
-        nb[0] = std::min<int64_t>(n_seeds, g->n);
-        eb[0] = 0;
-        for (int h = 1; h <= n_hops; ++h) {
-            const int64_t k = fanouts[h - 1] < 0 ? g->max_deg : std::min<int64_t>(fanouts[h - 1], g->max_deg);
-            eb[h] = nb[h - 1] * k;
-            nb[h] = std::min<int64_t>(g->n, nb[h - 1] + eb[h]);
-            GNNAV_CHECK(eb[h] < INT32_MAX && nb[h] < INT32_MAX, GNNAV_E_CAPACITY,
-                        "hop " + std::to_string(h) + " bound exceeds the int32 range");
-        }
-        int64_t max_list = n_seeds;
-        for (int h = 1; h <= n_hops; ++h) max_list = std::max(max_list, std::max(eb[h], nb[h - 1] + 1));
-        // workspace
-        if (b->map_nodes < g->n) {
-            b->map.ensure(std::max<int64_t>(g->n, 1) * sizeof(int32_t), s);
-            launch_fill_i32(b->map.as<int32_t>(), INT_MAX, g->n, s);
-            b->map_nodes = g->n;
-        }
-        b->sizes.ensure(kSizeSlots * sizeof(int32_t), s);
-        b->nodes.ensure(std::max<int64_t>(nb[n_hops], 1) * sizeof(int32_t), s);
-        b->part.ensure(scan_parts(max_list) * sizeof(int64_t), s);
-        for (int h = 1; h <= n_hops; ++h) {
-            b->indptr[h - 1].ensure((nb[h - 1] + 1) * sizeof(int32_t), s);
-            b->nbrs[h - 1].ensure(std::max<int64_t>(eb[h], 1) * sizeof(int32_t), s);
-            b->indices[h - 1].ensure(std::max<int64_t>(eb[h], 1) * sizeof(int32_t), s);
-        }
-        int32_t *sz = b->sizes.as<int32_t>();
-        int32_t *map = b->map.as<int32_t>();
-        int32_t *nodes = b->nodes.as<int32_t>();
-        int32_t *part = b->part.as<int32_t>();
-        launch_fill_i32(sz, 0, kSizeSlots, s);
-        // F_0: seeds without repeats, first occurrence kept
-        DedupArgs d0{seeds_dev, n_seeds, nullptr, n_seeds, map, g->n, nodes, nullptr, sz + kSizeN, sz + kSizeErr,
-                     part};
-        launch_dedup(d0, s);
-        for (int h = 1; h <= n_hops; ++h) {
-            SampleHopArgs a{g->row_ptr.p, g->i64, g->col.as<int32_t>(), nodes, sz + kSizeN + h - 1,
-                            b->indptr[h - 1].as<int32_t>(), b->nbrs[h - 1].as<int32_t>(), sz + kSizeE + h,
-                            fanouts[h - 1], rng_seed, (uint32_t)(h - 1), nb[h - 1], part};
-            launch_count_scan(a, s);
-            launch_sample_hop(a, s);
-            DedupArgs dh{b->nbrs[h - 1].as<int32_t>(), 0, sz + kSizeE + h, eb[h], map, g->n, nodes,
-                         sz + kSizeN + h - 1, sz + kSizeN + h, nullptr, part};
-            launch_dedup(dh, s);
-            launch_relabel(b->nbrs[h - 1].as<int32_t>(), sz + kSizeE + h, eb[h], map,
-                           b->indices[h - 1].as<int32_t>(), s);
-        }
-        launch_reset_map(nodes, sz + kSizeN + n_hops, nb[n_hops], map, s);
-        GNNAV_HIP(hipMemcpyAsync(b->sizes_host, sz, kSizeSlots * sizeof(int32_t), hipMemcpyDeviceToHost, s));
-        GNNAV_HIP(hipStreamSynchronize(s));
-        b->L = n_hops;
-        for (int h = 0; h <= n_hops; ++h) b->n_h[h] = b->sizes_host[kSizeN + h];
-        for (int h = 1; h <= n_hops; ++h) b->e_h[h] = b->sizes_host[kSizeE + h];
-        GNNAV_CHECK(b->sizes_host[kSizeErr] == 0, GNNAV_E_RANGE,
-                    std::to_string(b->sizes_host[kSizeErr]) + " seed(s) outside [0, n)");
+        sample_enqueue(g, seeds_dev, n_seeds, fanouts, n_hops, rng_seed, b, (hipStream_t)stream);
+        publish_sizes(b, (hipStream_t)stream);
+    });
+}
+
+extern "C" gnnav_status gnnav_sample_async(const gnnav_graph *g, const int32_t *seeds_dev, int64_t n_seeds,
+                                           const int32_t *fanouts, int32_t n_hops, uint64_t rng_seed,
+                                           gnnav_blocks *b, void *stream) {
+    return guarded([&] { sample_enqueue(g, seeds_dev, n_seeds, fanouts, n_hops, rng_seed, b, (hipStream_t)stream); });
+}
+
+extern "C" gnnav_status gnnav_blocks_sync(gnnav_blocks *b, void *stream) {
+    return guarded([&] {
+        GNNAV_CHECK(b, GNNAV_E_INVALID, "blocks is NULL");
+        publish_sizes(b, (hipStream_t)stream);
+    });
+}
+
+extern "C" gnnav_status gnnav_blocks_device_sizes(const gnnav_blocks *b, const int32_t **sizes_dev,
+                                                  int64_t *bounds) {
+    return guarded([&] {
+        GNNAV_CHECK(b && sizes_dev, GNNAV_E_INVALID, "NULL argument");
+        GNNAV_CHECK(b->sizes.p, GNNAV_E_INVALID, "blocks have not been sampled");
+        *sizes_dev = b->sizes.as<int32_t>();
+        if (bounds)
+            for (int h = 0; h <= b->L; ++h) bounds[h] = b->nb[h];
     });
 }
 
@@ -555,6 +622,7 @@ extern "C" gnnav_status gnnav_blocks_hop(const gnnav_blocks *b, int32_t hop, gnn
     return guarded([&] {
         GNNAV_CHECK(b && out, GNNAV_E_INVALID, "NULL argument");
         GNNAV_CHECK(hop >= 1 && hop <= b->L, GNNAV_E_INVALID, "hop outside [1, L]");
+        GNNAV_CHECK(b->host_sizes, GNNAV_E_INVALID, "sizes not on the host yet: call gnnav_blocks_sync");
         out->n_dst = b->n_h[hop - 1];
         out->n_src = b->n_h[hop];
         out->nnz = b->e_h[hop];
@@ -569,6 +637,8 @@ extern "C" gnnav_status gnnav_blocks_nodes(const gnnav_blocks *b, const int32_t 
                                            int32_t *n_hops) {
     return guarded([&] {
         GNNAV_CHECK(b, GNNAV_E_INVALID, "blocks is NULL");
+        GNNAV_CHECK(!n_per_hop || b->host_sizes, GNNAV_E_INVALID,
+                    "sizes not on the host yet: call gnnav_blocks_sync");
         if (nodes_dev) *nodes_dev = b->nodes.as<int32_t>();
         if (n_per_hop)
             for (int h = 0; h <= b->L; ++h) n_per_hop[h] = b->n_h[h];
@@ -577,34 +647,44 @@ extern "C" gnnav_status gnnav_blocks_nodes(const gnnav_blocks *b, const int32_t 
 }
 
 // ----------------------------------------------------------------- gather
-static bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+static void gather_impl(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_ids, const int32_t *n_dev,
+                        void *out_dev, int64_t ld_out, int64_t *counts_dev, hipStream_t s) {
+    GNNAV_CHECK(c && counts_dev, GNNAV_E_INVALID, "NULL cache or counts");
+    GNNAV_CHECK(n_ids >= 0 && n_ids < INT32_MAX, GNNAV_E_INVALID, "n_ids outside [0, INT32_MAX)");
+    GNNAV_CHECK(n_ids == 0 || (ids_dev && out_dev), GNNAV_E_INVALID, "NULL ids or out");
+    GNNAV_CHECK(ld_out >= c->d, GNNAV_E_INVALID, "ld_out < d");
+    GNNAV_CHECK((ld_out * c->elt) % 16 == 0 && aligned16(out_dev), GNNAV_E_INVALID,
+                "out rows must be 16-byte aligned");
+    auto *cc = const_cast<gnnav_cache *>(c);
+    GatherWs *w = gather_ws(cc, s);
+    w->hit_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
+    w->miss_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
+    w->part.ensure(scan_parts(n_ids) * sizeof(int64_t), s);
+    GatherArgs a{ids_dev, n_ids, n_dev, c->slot_map.as<int32_t>(), c->n, c->cache_rows.p, c->store_ptr,
+                 c->ld * c->elt, out_dev, ld_out * c->elt, c->d * c->elt, counts_dev, w->dev_counts.as<int32_t>(),
+                 w->hit_list.as<int2>(), w->miss_list.as<int2>(), w->part.as<int32_t>()};
+    launch_classify(a, s);
+    if (n_ids == 0) return;
+    GNNAV_HIP(hipEventRecord(w->fork, s));
+    GNNAV_HIP(hipStreamWaitEvent(w->side, w->fork, 0));
+    launch_gather_rows(a, /*hits=*/false, w->side);
+    launch_gather_rows(a, /*hits=*/true, s);
+    GNNAV_HIP(hipEventRecord(w->join, w->side));
+    GNNAV_HIP(hipStreamWaitEvent(s, w->join, 0));
+}
 
 extern "C" gnnav_status gnnav_gather(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_ids, void *out_dev,
                                      int64_t ld_out, int64_t *counts_dev, void *stream) {
+    return guarded([&] { gather_impl(c, ids_dev, n_ids, nullptr, out_dev, ld_out, counts_dev, (hipStream_t)stream); });
+}
+
+extern "C" gnnav_status gnnav_gather_n(const gnnav_cache *c, const int32_t *ids_dev, const int32_t *n_ids_dev,
+                                       int64_t n_ids_max, void *out_dev, int64_t ld_out, int64_t *counts_dev,
+                                       void *stream) {
     return guarded([&] {
-        GNNAV_CHECK(c && counts_dev, GNNAV_E_INVALID, "NULL cache or counts");
-        GNNAV_CHECK(n_ids >= 0 && n_ids < INT32_MAX, GNNAV_E_INVALID, "n_ids outside [0, INT32_MAX)");
-        GNNAV_CHECK(n_ids == 0 || (ids_dev && out_dev), GNNAV_E_INVALID, "NULL ids or out");
-        GNNAV_CHECK(ld_out >= c->d, GNNAV_E_INVALID, "ld_out < d");
-        GNNAV_CHECK((ld_out * c->elt) % 16 == 0 && aligned16(out_dev), GNNAV_E_INVALID,
-                    "out rows must be 16-byte aligned");
-        hipStream_t s = (hipStream_t)stream;
-        auto *cc = const_cast<gnnav_cache *>(c);
-        cc->hit_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
-        cc->miss_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
-        cc->part.ensure(scan_parts(n_ids) * sizeof(int64_t), s);
-        GatherArgs a{ids_dev, n_ids, c->slot_map.as<int32_t>(), c->n, c->cache_rows.p, c->store_ptr,
-                     c->ld * c->elt, out_dev, ld_out * c->elt, c->d * c->elt, counts_dev,
-                     cc->dev_counts.as<int32_t>(), cc->hit_list.as<int2>(), cc->miss_list.as<int2>(),
-                     cc->part.as<int32_t>()};
-        launch_classify(a, s);
-        if (n_ids == 0) return;
-        GNNAV_HIP(hipEventRecord(cc->fork, s));
-        GNNAV_HIP(hipStreamWaitEvent(cc->side, cc->fork, 0));
-        launch_gather_rows(a, /*hits=*/false, cc->side);
-        launch_gather_rows(a, /*hits=*/true, s);
-        GNNAV_HIP(hipEventRecord(cc->join, cc->side));
-        GNNAV_HIP(hipStreamWaitEvent(s, cc->join, 0));
+        GNNAV_CHECK(n_ids_dev, GNNAV_E_INVALID, "n_ids_dev is NULL");
+        gather_impl(c, ids_dev, n_ids_max, n_ids_dev, out_dev, ld_out, counts_dev, (hipStream_t)stream);
     });
 }
 
@@ -623,8 +703,8 @@ extern "C" gnnav_status gnnav_aggregate_mean(const int32_t *indptr_dev, const in
         GNNAV_CHECK(ld_x >= d && ld_out >= d, GNNAV_E_INVALID, "stride below d");
         GNNAV_CHECK((ld_x * elt) % 16 == 0 && (ld_out * elt) % 16 == 0 && aligned16(x_dev) && aligned16(out_dev),
                     GNNAV_E_INVALID, "rows must be 16-byte aligned");
-        launch_aggregate_mean(indptr_dev, indices_dev, n_dst, x_dev, ld_x, d, dt == GNNAV_BF16, out_dev, ld_out,
-                              (hipStream_t)stream);
+        launch_aggregate_mean(indptr_dev, indices_dev, n_dst, nullptr, x_dev, ld_x, d, dt == GNNAV_BF16, out_dev,
+                              ld_out, (hipStream_t)stream);
     });
 }
 
@@ -642,8 +722,8 @@ extern "C" gnnav_status gnnav_combine(const void *self_dev, int64_t ld_self, con
         GNNAV_CHECK((ld_self * elt) % 16 == 0 && (ld_agg * elt) % 16 == 0 && aligned16(self_dev) &&
                         aligned16(agg_dev),
                     GNNAV_E_INVALID, "operand rows must be 16-byte aligned");
-        launch_combine(self_dev, ld_self, agg_dev, ld_agg, m, d_in, w_dev, d_out, dt == GNNAV_BF16, relu != 0,
-                       out_bf16 != 0, out_dev, ld_out, (hipStream_t)stream);
+        launch_combine(self_dev, ld_self, agg_dev, ld_agg, m, nullptr, d_in, w_dev, d_out, dt == GNNAV_BF16,
+                       relu != 0, out_bf16 != 0, out_dev, ld_out, (hipStream_t)stream);
     });
 }
 
@@ -664,10 +744,17 @@ extern "C" gnnav_status gnnav_sage_forward(gnnav_blocks *b, const void *x_dev, i
                     "x rows must be 16-byte aligned with ld_x >= dims[0]");
         hipStream_t s = (hipStream_t)stream;
         // workspace: agg for the largest layer, two ping-pong hidden buffers
+        // Row counts: exact host sizes after gnnav_sample / gnnav_blocks_sync;
+        // otherwise the kernels read them from device memory and the grids and
+        // buffers follow the Eq. 12 bounds of the sample.
+        const bool host = b->host_sizes;
+        const int32_t *dsz = b->sizes.as<int32_t>();
+        auto rows_of = [&](int hb) { return host ? b->n_h[hb - 1] : b->nb[hb - 1]; };
+        auto rows_dev = [&](int hb) { return host ? (const int32_t *)nullptr : dsz + kSizeN + hb - 1; };
         int64_t agg_bytes = 1, hid_bytes = 1;
         for (int l = 1; l <= L; ++l) {
             const int hb = L - l + 1;
-            const int64_t rows = b->n_h[hb - 1];
+            const int64_t rows = rows_of(hb);
             agg_bytes = std::max(agg_bytes, rows * padded_ld(dims[l - 1], elt) * elt);
             if (l < L) hid_bytes = std::max(hid_bytes, rows * padded_ld(dims[l], elt) * elt);
         }
@@ -685,21 +772,22 @@ extern "C" gnnav_status gnnav_sage_forward(gnnav_blocks *b, const void *x_dev, i
         for (int l = 1; l <= L; ++l) {
             const int tag = l < 4 ? l - 1 : 3;
             const int hb = L - l + 1;
-            const int64_t rows = b->n_h[hb - 1];
+            const int64_t rows = rows_of(hb);
+            const int32_t *rdev = rows_dev(hb);
             const int64_t din = dims[l - 1], dout = dims[l];
             const int64_t lda = padded_ld(din, elt);
-            launch_aggregate_mean(b->indptr[hb - 1].as<int32_t>(), b->indices[hb - 1].as<int32_t>(), rows, x, ldx,
-                                  din, bf, b->agg.p, lda, s, kAggLabel[tag]);
+            launch_aggregate_mean(b->indptr[hb - 1].as<int32_t>(), b->indices[hb - 1].as<int32_t>(), rows, rdev, x,
+                                  ldx, din, bf, b->agg.p, lda, s, kAggLabel[tag]);
             if (l < L) {
                 void *h = b->hid[l & 1].p;
                 const int64_t ldh = padded_ld(dout, elt);
-                launch_combine(x, ldx, b->agg.p, lda, rows, din, W_dev[l - 1], dout, bf, true, bf, h, ldh, s,
+                launch_combine(x, ldx, b->agg.p, lda, rows, rdev, din, W_dev[l - 1], dout, bf, true, bf, h, ldh, s,
                                kGemmLabel[tag]);
                 x = h;
                 ldx = ldh;
             } else {
-                launch_combine(x, ldx, b->agg.p, lda, rows, din, W_dev[l - 1], dout, bf, false, false, logits_dev,
-                               ld_out, s, kGemmLabel[tag]);
+                launch_combine(x, ldx, b->agg.p, lda, rows, rdev, din, W_dev[l - 1], dout, bf, false, false,
+                               logits_dev, ld_out, s, kGemmLabel[tag]);
             }
         }
     });

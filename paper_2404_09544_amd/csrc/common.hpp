@@ -173,7 +173,8 @@ void launch_fill_i32(int32_t *p, int32_t v, int64_t n, hipStream_t s);
 // gather.hip
 struct GatherArgs {
     const int32_t *ids;
-    int64_t n_ids;
+    int64_t n_ids;           // count, or its upper bound when n_ptr is set
+    const int32_t *n_ptr;    // device count (nullable)
     const int32_t *slot_map;
     int64_t n_nodes;
     const void *cache;       // device [C x ld]
@@ -193,11 +194,12 @@ void launch_gather_rows(const GatherArgs &a, bool hits, hipStream_t s);
 
 // spmm.hip
 void launch_aggregate_mean(const int32_t *indptr, const int32_t *indices, int64_t n_dst,
-                           const void *x, int64_t ld_x, int64_t d, bool bf16, void *out,
+                           const int32_t *n_dst_dev, const void *x, int64_t ld_x, int64_t d, bool bf16, void *out,
                            int64_t ld_out, hipStream_t s, const char *label = "aggregate_mean");
 
 // gemm.hip
 void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
+                    const int32_t *m_dev,
                     int64_t d_in, const void *w, int64_t d_out, bool bf16, bool relu,
                     bool out_bf16, void *out, int64_t ld_out, hipStream_t s,
                     const char *label = "combine_gemm");

@@ -18,6 +18,7 @@ namespace gnnav {
 struct ClassifyOp {
     const int32_t *ids;
     int64_t n_ids;
+    const int32_t *n_ptr;
     const int32_t *slot_map;
     int64_t n_nodes;
     int2 *hit_list;
@@ -28,7 +29,7 @@ struct ClassifyOp {
     int64_t out_ld16;
     int64_t chunks;
     // packed value: hits in the high 32 bits, misses in the low 32 bits
-    __device__ int64_t n() const { return n_ids; }
+    __device__ int64_t n() const { return n_ptr ? (int64_t)*n_ptr : n_ids; }
     __device__ int64_t value(int64_t i) const {
         const int32_t id = ids[i];
         if (id < 0 || id >= n_nodes) return 0;
@@ -49,14 +50,14 @@ struct ClassifyOp {
         const int64_t hits = t >> 32, misses = t & 0xffffffff;
         counts[0] = hits;
         counts[1] = misses;
-        counts[2] = n_ids - hits - misses;
+        counts[2] = n() - hits - misses;
         dev_counts[0] = (int32_t)hits;
         dev_counts[1] = (int32_t)misses;
     }
 };
 
 void launch_classify(const GatherArgs &a, hipStream_t s) {
-    ClassifyOp op{a.ids, a.n_ids, a.slot_map, a.n_nodes, a.hit_list, a.miss_list, a.counts,
+    ClassifyOp op{a.ids, a.n_ids, a.n_ptr, a.slot_map, a.n_nodes, a.hit_list, a.miss_list, a.counts,
                   a.dev_counts, (uint4 *)a.out, a.out_ld_bytes / 16, (a.row_bytes + 15) / 16};
     run_scan(op, a.n_ids, (int64_t *)a.part, "classify", s);
 }

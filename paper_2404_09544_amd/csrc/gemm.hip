@@ -3,17 +3,30 @@
 // the concatenation is never stored.
 //
 // Matrix cores: fp32 uses v_mfma_f32_16x16x4_f32 (full fp32 products),
-// bf16 uses v_mfma_f32_16x16x32_bf16 with fp32 accumulation.  A 256-thread
-// workgroup computes a BM x BN tile as 2 x 2 wavefronts; each wavefront owns
-// (BM/2) x (BN/2) = several 16 x 16 MFMA tiles.  K is walked in BK steps:
-// the next step's global loads are issued into registers while the current
-// step's LDS tiles feed the MFMAs.  LDS rows are padded so the fragment
-// reads of the four 16-lane groups fall in different banks.
+// bf16 uses v_mfma_f32_16x16x32_bf16 with fp32 accumulation.
+//
+// Main kernel (enough output tiles to fill the chip): a 256-thread
+// workgroup owns a BM x BN output tile as WM x WN wavefronts, each holding
+// (BM/WM) x (BN/WN) in 16 x 16 MFMA accumulators.  K is walked in BK steps
+// through two LDS buffers: the next step's global loads are issued into
+// registers before the current step's MFMAs and stored into the other buffer
+// afterwards, so there is one barrier per step.
+//
+// Skinny kernel (few output rows, e.g. the last layer over the seeds): a
+// workgroup owns 16 x 64 outputs; its four wavefronts take interleaved
+// 16- or 32-wide K blocks straight from global memory into MFMA fragments
+// and add their partial tiles in LDS in a fixed order (deterministic).
 //
 // MFMA 16x16 fragment layouts (lane l, g = l / 16):
-//   f32 x4:  A[row l%16][k g],        B[k g][col l%16]
-//   bf16 x32: A[row l%16][k 8g..8g+7], B[k 8g..8g+7][col l%16]
-//   result:  D[row 4g + r][col l%16] in accumulator element r.
+//   f32 x4:   A[row l%16][k g],         B[k g][col l%16]
+//   bf16 x32: A[row l%16][k 8g..8g+7],  B[k 8g..8g+7][col l%16]
+//   result:   D[row 4g + r][col l%16] in accumulator element r.
+// Only the pairing of A's and B's k index inside one instruction matters,
+// so the loaders may assign k to (g, element) in any way that is the same
+// for both operands.
+#include <cstdlib>
+#include <mutex>
+
 #include "common.hpp"
 
 namespace gnnav {
@@ -28,25 +41,59 @@ __device__ __forceinline__ void store_out<float>(float *c, float v) { *c = v; }
 template <>
 __device__ __forceinline__ void store_out<uint16_t>(uint16_t *c, float v) { *c = bf16_rne(v); }
 
-// ------------------------------------------------------------------ fp32
-template <int BM, int BN, class OutT>
+template <int TM, int TN, class OutT>
+__device__ __forceinline__ void write_tile(const f32x4 (&acc)[TM][TN], int64_t r0, int64_t c0, int64_t M,
+                                           int64_t N, int relu, OutT *C, int64_t ldc, int g, int l16) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int64_t row = r0 + i * 16 + 4 * g + r;
+                const int64_t col = c0 + j * 16 + l16;
+                if (row < M && col < N) {
+                    float v = acc[i][j][r];
+                    if (relu) v = fmaxf(v, 0.f);
+                    store_out<OutT>(C + row * ldc + col, v);
+                }
+            }
+}
+
+// Workgroups are dispatched round-robin over the 8 XCDs (id % 8), each with
+// its own L2.  Tiles are numbered so that the column tiles of one row band
+// land on the same XCD back to back: the band's A rows are then fetched
+// from HBM once and re-read from that XCD's L2.  The grid is padded to a
+// multiple of 8 * ncol; padding workgroups map past the last row band.
+__device__ __forceinline__ void tile_of(int64_t ncol, int64_t &tile_r, int64_t &tile_c) {
+    const int64_t L = blockIdx.x, xcd = L & 7, j = L >> 3;
+    tile_r = (j / ncol) * 8 + xcd;
+    tile_c = j % ncol;
+}
+
+// ------------------------------------------------------------ fp32 main
+template <int BM, int BN, int WM, int WN, int BK, class OutT>
 __global__ void __launch_bounds__(256) k_combine_f32(const float *__restrict__ A0, int64_t lda0,
                                                      const float *__restrict__ A1, int64_t lda1, int64_t M,
-                                                     int64_t K, const float *__restrict__ W, int64_t N,
-                                                     int relu, OutT *__restrict__ C, int64_t ldc) {
-    constexpr int BK = 16;
-    constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 16, TN = WN / 16;
+                                                     const int32_t *__restrict__ m_dev, int64_t K,
+                                                     const float *__restrict__ W, int64_t N, int relu, int wvec,
+                                                     OutT *__restrict__ C, int64_t ldc) {
+    constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
     constexpr int PA = BM + 16, PB = BN + 16;
-    constexpr int A_ROWS = BM / 64;          // float4 loads per thread for A
-    constexpr int B_PER = BK * BN / 256;     // scalars per thread for B
-    __shared__ float As[BK][PA];
-    __shared__ float Bs[BK][PB];
+    constexpr int A_CH = BM * BK / 4;             // float4 chunks in an A step
+    constexpr int B_CH = BK * BN / 4;             // float4 chunks in a B step
+    constexpr int A_LD = (A_CH + 255) / 256, B_LD = (B_CH + 255) / 256;
+    static_assert(WM * WN == 4 && TM >= 1 && TN >= 1 && BK % 4 == 0, "tile shape");
+    __shared__ __attribute__((aligned(16))) float As[2][BK][PA];
+    __shared__ __attribute__((aligned(16))) float Bs[2][BK][PB];
 
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    const int wm = wid >> 1, wn = wid & 1, g = lane >> 4, l16 = lane & 15;
-    const int64_t m0 = (int64_t)blockIdx.x * BM, n0 = (int64_t)blockIdx.y * BN;
-    const int a_row = tid >> 2, a_k = (tid & 3) * 4;
-    const int b_n = tid % BN, b_k = (tid / BN) * B_PER;
+    const int wm = wid / WN, wn = wid % WN, g = lane >> 4, l16 = lane & 15;
+    if (m_dev) M = *m_dev;
+    int64_t tile_r, tile_c;
+    tile_of((N + BN - 1) / BN, tile_r, tile_c);
+    const int64_t m0 = tile_r * BM, n0 = tile_c * BN;
+    if (m0 >= M) return;
 
     f32x4 acc[TM][TN];
 #pragma unroll
@@ -56,8 +103,7 @@ __global__ void __launch_bounds__(256) k_combine_f32(const float *__restrict__ A
 
     const int64_t kt = (K + BK - 1) / BK;
     const int64_t tiles = 2 * kt;
-    float4 ra[A_ROWS];
-    float rb[B_PER];
+    float4 ra[A_LD], rb[B_LD];
 
     auto load = [&](int64_t t) {
         const bool seg = t >= kt;
@@ -66,11 +112,12 @@ __global__ void __launch_bounds__(256) k_combine_f32(const float *__restrict__ A
         const int64_t lda = seg ? lda1 : lda0;
         const float *Wk = W + (seg ? K : 0) * N;
 #pragma unroll
-        for (int s = 0; s < A_ROWS; ++s) {
-            const int64_t row = m0 + a_row + 64 * s;
-            const int64_t k = k0 + a_k;
+        for (int s = 0; s < A_LD; ++s) {
+            const int c = tid + 256 * s;
+            const int r = c / (BK / 4), kq = (c % (BK / 4)) * 4;
+            const int64_t row = m0 + r, k = k0 + kq;
             float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (row < M) {
+            if (c < A_CH && row < M) {
                 const float *p = A + row * lda + k;
                 if (k + 3 < K) {
                     v = *(const float4 *)p;
@@ -82,85 +129,101 @@ __global__ void __launch_bounds__(256) k_combine_f32(const float *__restrict__ A
             }
             ra[s] = v;
         }
-        const int64_t n = n0 + b_n;
 #pragma unroll
-        for (int e = 0; e < B_PER; ++e) {
-            const int64_t k = k0 + b_k + e;
-            rb[e] = (k < K && n < N) ? Wk[k * N + n] : 0.f;
+        for (int s = 0; s < B_LD; ++s) {
+            const int c = tid + 256 * s;
+            const int kr = c / (BN / 4), nq = (c % (BN / 4)) * 4;
+            const int64_t kk = k0 + kr, n = n0 + nq;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (c < B_CH && kk < K) {
+                const float *q = Wk + kk * N + n;
+                if (wvec && n + 3 < N) {
+                    v = *(const float4 *)q;
+                } else {
+                    if (n < N) v.x = q[0];
+                    if (n + 1 < N) v.y = q[1];
+                    if (n + 2 < N) v.z = q[2];
+                    if (n + 3 < N) v.w = q[3];
+                }
+            }
+            rb[s] = v;
         }
     };
-    auto stash = [&]() {
+    auto stash = [&](int buf) {
 #pragma unroll
-        for (int s = 0; s < A_ROWS; ++s) {
-            As[a_k + 0][a_row + 64 * s] = ra[s].x;
-            As[a_k + 1][a_row + 64 * s] = ra[s].y;
-            As[a_k + 2][a_row + 64 * s] = ra[s].z;
-            As[a_k + 3][a_row + 64 * s] = ra[s].w;
+        for (int s = 0; s < A_LD; ++s) {
+            const int c = tid + 256 * s;
+            if (c < A_CH) {
+                const int r = c / (BK / 4), kq = (c % (BK / 4)) * 4;
+                As[buf][kq + 0][r] = ra[s].x;
+                As[buf][kq + 1][r] = ra[s].y;
+                As[buf][kq + 2][r] = ra[s].z;
+                As[buf][kq + 3][r] = ra[s].w;
+            }
         }
 #pragma unroll
-        for (int e = 0; e < B_PER; ++e) Bs[b_k + e][b_n] = rb[e];
+        for (int s = 0; s < B_LD; ++s) {
+            const int c = tid + 256 * s;
+            if (c < B_CH) *(float4 *)&Bs[buf][c / (BN / 4)][(c % (BN / 4)) * 4] = rb[s];
+        }
     };
 
-    load(0);
-    stash();
-    __syncthreads();
-    for (int64_t t = 0; t < tiles; ++t) {
-        if (t + 1 < tiles) load(t + 1);
+    auto compute = [&](int buf) {
 #pragma unroll
         for (int ks = 0; ks < BK / 4; ++ks) {
             float a[TM], b[TN];
 #pragma unroll
-            for (int i = 0; i < TM; ++i) a[i] = As[ks * 4 + g][wm * WM + i * 16 + l16];
+            for (int i = 0; i < TM; ++i) a[i] = As[buf][ks * 4 + g][wm * WTM + i * 16 + l16];
 #pragma unroll
-            for (int j = 0; j < TN; ++j) b[j] = Bs[ks * 4 + g][wn * WN + j * 16 + l16];
+            for (int j = 0; j < TN; ++j) b[j] = Bs[buf][ks * 4 + g][wn * WTN + j * 16 + l16];
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
         }
+    };
+
+    load(0);
+    stash(0);
+    __syncthreads();
+    for (int64_t t = 0; t < tiles; ++t) {
+        const int buf = (int)(t & 1);
+        if (t + 1 < tiles) load(t + 1);
+        compute(buf);
+        if (t + 1 < tiles) stash(buf ^ 1);
         __syncthreads();
-        if (t + 1 < tiles) {
-            stash();
-            __syncthreads();
-        }
     }
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int64_t row = m0 + wm * WM + i * 16 + 4 * g + r;
-                const int64_t col = n0 + wn * WN + j * 16 + l16;
-                if (row < M && col < N) {
-                    float v = acc[i][j][r];
-                    if (relu) v = fmaxf(v, 0.f);
-                    store_out<OutT>(C + row * ldc + col, v);
-                }
-            }
+    write_tile<TM, TN, OutT>(acc, m0 + wm * WTM, n0 + wn * WTN, M, N, relu, C, ldc, g, l16);
 }
 
-// ------------------------------------------------------------------ bf16
-template <int BM, int BN, class OutT>
+// ------------------------------------------------------------ bf16 main
+// B comes from WT, the weights transposed to [N][2K] once per call, so both
+// operands arrive as 16-byte chunks along k, the layout the bf16 MFMA
+// fragment (8 consecutive k per lane) reads from LDS.
+template <int BM, int BN, int WM, int WN, int BK, class OutT>
 __global__ void __launch_bounds__(256) k_combine_bf16(const uint16_t *__restrict__ A0, int64_t lda0,
                                                       const uint16_t *__restrict__ A1, int64_t lda1,
-                                                      int64_t M, int64_t K, const uint16_t *__restrict__ W,
-                                                      int64_t N, int relu, OutT *__restrict__ C,
-                                                      int64_t ldc) {
-    constexpr int BK = 32;
-    constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 16, TN = WN / 16;
-    constexpr int PK = BK + 8;                // padded k stride (elements)
-    constexpr int A_ROWS = BM / 64;           // 16-byte loads per thread for A
-    constexpr int B_PER = BK * BN / 256;      // scalars per thread for B
-    __shared__ __attribute__((aligned(16))) uint16_t As[BM][PK];
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[BN][PK];
+                                                      int64_t M, const int32_t *__restrict__ m_dev, int64_t K,
+                                                      const uint16_t *__restrict__ WT, int64_t N, int relu,
+                                                      OutT *__restrict__ C, int64_t ldc) {
+    constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
+    constexpr int PK = BK + 8;                    // padded k stride (elements)
+    constexpr int A_CH = BM * BK / 8;             // 16-byte chunks in an A step
+    constexpr int A_LD = (A_CH + 255) / 256;
+    constexpr int B_CH = BN * BK / 8;             // 16-byte chunks in a B step
+    constexpr int B_LD = (B_CH + 255) / 256;
+    static_assert(WM * WN == 4 && TM >= 1 && TN >= 1 && BK % 32 == 0, "tile shape");
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][BM][PK];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN][PK];
 
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    const int wm = wid >> 1, wn = wid & 1, g = lane >> 4, l16 = lane & 15;
-    const int64_t m0 = (int64_t)blockIdx.x * BM, n0 = (int64_t)blockIdx.y * BN;
-    const int a_row = tid >> 2, a_k = (tid & 3) * 8;
-    const int b_n = tid % BN, b_k = (tid / BN) * B_PER;
+    const int wm = wid / WN, wn = wid % WN, g = lane >> 4, l16 = lane & 15;
+    if (m_dev) M = *m_dev;
+    int64_t tile_r, tile_c;
+    tile_of((N + BN - 1) / BN, tile_r, tile_c);
+    const int64_t m0 = tile_r * BM, n0 = tile_c * BN;
+    if (m0 >= M) return;
 
     f32x4 acc[TM][TN];
 #pragma unroll
@@ -170,21 +233,22 @@ __global__ void __launch_bounds__(256) k_combine_bf16(const uint16_t *__restrict
 
     const int64_t kt = (K + BK - 1) / BK;
     const int64_t tiles = 2 * kt;
-    uint4 ra[A_ROWS];
-    uint16_t rb[B_PER];
+    uint4 ra[A_LD], rb[B_LD];
+    const int64_t K2 = 2 * K;
 
     auto load = [&](int64_t t) {
         const bool seg = t >= kt;
         const int64_t k0 = (seg ? t - kt : t) * BK;
         const uint16_t *A = seg ? A1 : A0;
         const int64_t lda = seg ? lda1 : lda0;
-        const uint16_t *Wk = W + (seg ? K : 0) * N;
+        const int64_t wk0 = (seg ? K : 0) + k0;
 #pragma unroll
-        for (int s = 0; s < A_ROWS; ++s) {
-            const int64_t row = m0 + a_row + 64 * s;
-            const int64_t k = k0 + a_k;
+        for (int s = 0; s < A_LD; ++s) {
+            const int c = tid + 256 * s;
+            const int r = c / (BK / 8), kq = (c % (BK / 8)) * 8;
+            const int64_t row = m0 + r, k = k0 + kq;
             uint4 v = make_uint4(0, 0, 0, 0);
-            if (row < M) {
+            if (c < A_CH && row < M) {
                 const uint16_t *p = A + row * lda + k;
                 if (k + 7 < K) {
                     v = *(const uint4 *)p;
@@ -198,91 +262,293 @@ __global__ void __launch_bounds__(256) k_combine_bf16(const uint16_t *__restrict
             }
             ra[s] = v;
         }
-        const int64_t n = n0 + b_n;
 #pragma unroll
-        for (int e = 0; e < B_PER; ++e) {
-            const int64_t k = k0 + b_k + e;
-            rb[e] = (k < K && n < N) ? Wk[k * N + n] : (uint16_t)0;
+        for (int s = 0; s < B_LD; ++s) {
+            const int c = tid + 256 * s;
+            const int nr = c / (BK / 8), kq = (c % (BK / 8)) * 8;
+            const int64_t n = n0 + nr, k = k0 + kq;
+            uint4 v = make_uint4(0, 0, 0, 0);
+            if (c < B_CH && n < N) {
+                const uint16_t *q = WT + n * K2 + wk0 + kq;
+                if (k + 7 < K && (K & 7) == 0) {
+                    v = *(const uint4 *)q;
+                } else {
+                    uint16_t tmp[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                    for (int e = 0; e < 8; ++e)
+                        if (k + e < K) tmp[e] = q[e];
+                    v = make_uint4(tmp[0] | (uint32_t)tmp[1] << 16, tmp[2] | (uint32_t)tmp[3] << 16,
+                                   tmp[4] | (uint32_t)tmp[5] << 16, tmp[6] | (uint32_t)tmp[7] << 16);
+                }
+            }
+            rb[s] = v;
         }
     };
-    auto stash = [&]() {
+    auto stash = [&](int buf) {
 #pragma unroll
-        for (int s = 0; s < A_ROWS; ++s) *(uint4 *)&As[a_row + 64 * s][a_k] = ra[s];
+        for (int s = 0; s < A_LD; ++s) {
+            const int c = tid + 256 * s;
+            if (c < A_CH) *(uint4 *)&As[buf][c / (BK / 8)][(c % (BK / 8)) * 8] = ra[s];
+        }
 #pragma unroll
-        for (int e = 0; e < B_PER; ++e) Bs[b_n][b_k + e] = rb[e];
+        for (int s = 0; s < B_LD; ++s) {
+            const int c = tid + 256 * s;
+            if (c < B_CH) *(uint4 *)&Bs[buf][c / (BK / 8)][(c % (BK / 8)) * 8] = rb[s];
+        }
     };
 
     load(0);
-    stash();
+    stash(0);
     __syncthreads();
     for (int64_t t = 0; t < tiles; ++t) {
+        const int buf = (int)(t & 1);
         if (t + 1 < tiles) load(t + 1);
-        bf16x8 a[TM], b[TN];
 #pragma unroll
-        for (int i = 0; i < TM; ++i) a[i] = *(const bf16x8 *)&As[wm * WM + i * 16 + l16][8 * g];
+        for (int ks = 0; ks < BK / 32; ++ks) {
+            bf16x8 a[TM], b[TN];
 #pragma unroll
-        for (int j = 0; j < TN; ++j) b[j] = *(const bf16x8 *)&Bs[wn * WN + j * 16 + l16][8 * g];
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
+            for (int i = 0; i < TM; ++i)
+                a[i] = *(const bf16x8 *)&As[buf][wm * WTM + i * 16 + l16][ks * 32 + 8 * g];
 #pragma unroll
             for (int j = 0; j < TN; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+                b[j] = *(const bf16x8 *)&Bs[buf][wn * WTN + j * 16 + l16][ks * 32 + 8 * g];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+        if (t + 1 < tiles) stash(buf ^ 1);
         __syncthreads();
-        if (t + 1 < tiles) {
-            stash();
-            __syncthreads();
+    }
+    write_tile<TM, TN, OutT>(acc, m0 + wm * WTM, n0 + wn * WTN, M, N, relu, C, ldc, g, l16);
+}
+
+// --------------------------------------------------------------- skinny
+// 16 x 64 outputs per workgroup; wavefront w takes K blocks w, w+4, ... of
+// both segments (KB = 16 fp32 or 32 bf16 wide); partial tiles are summed in
+// LDS in wavefront order.
+template <bool BF16>
+struct Skinny;
+
+template <>
+struct Skinny<false> {
+    static constexpr int KB = 16;
+    // lane (row l16, group g) loads A[row][kb + 4g .. 4g+3]; MFMA s uses element s.
+    __device__ static void block(const float *A, int64_t lda, int64_t row, bool row_ok, int64_t kb, int64_t K,
+                                 const float *Wk, int64_t N, int64_t n0, int g, int l16, f32x4 (&acc)[4]) {
+        float a[4];
+        const int64_t k = kb + 4 * g;
+        if (row_ok && k + 3 < K) {
+            const float4 v = *(const float4 *)(A + row * lda + k);
+            a[0] = v.x; a[1] = v.y; a[2] = v.z; a[3] = v.w;
+        } else {
+#pragma unroll
+            for (int s = 0; s < 4; ++s) a[s] = (row_ok && k + s < K) ? A[row * lda + k + s] : 0.f;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t n = n0 + j * 16 + l16;
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const float b = (n < N && k + s < K) ? Wk[(k + s) * N + n] : 0.f;
+                acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b, acc[j], 0, 0, 0);
+            }
         }
     }
+};
+
+template <>
+struct Skinny<true> {
+    static constexpr int KB = 32;
+    // lane (row l16, group g) loads A[row][kb + 8g .. 8g+7] as one fragment.
+    __device__ static void block(const uint16_t *A, int64_t lda, int64_t row, bool row_ok, int64_t kb,
+                                 int64_t K, const uint16_t *Wk, int64_t N, int64_t n0, int g, int l16,
+                                 f32x4 (&acc)[4]) {
+        const int64_t k = kb + 8 * g;
+        uint16_t av[8];
+        if (row_ok && k + 7 < K) {
+            const uint4 v = *(const uint4 *)(A + row * lda + k);
+            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int64_t row = m0 + wm * WM + i * 16 + 4 * g + r;
-                const int64_t col = n0 + wn * WN + j * 16 + l16;
-                if (row < M && col < N) {
-                    float v = acc[i][j][r];
-                    if (relu) v = fmaxf(v, 0.f);
-                    store_out<OutT>(C + row * ldc + col, v);
-                }
+            for (int e = 0; e < 4; ++e) {
+                av[2 * e] = (uint16_t)(w[e] & 0xffffu);
+                av[2 * e + 1] = (uint16_t)(w[e] >> 16);
             }
-}
-
-template <int BN>
-static void launch_combine_bn(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
-                              int64_t d_in, const void *w, int64_t d_out, bool bf16, bool relu,
-                              bool out_bf16, void *out, int64_t ld_out, hipStream_t s, const char *label) {
-    constexpr int BM = 64;
-    const dim3 grid((unsigned)((m + BM - 1) / BM), (unsigned)((d_out + BN - 1) / BN));
-    KernelTimer t(label, s);
-    if (!bf16) {
-        if (out_bf16) fail(GNNAV_E_INVALID, "bf16 output needs bf16 operands");
-        hipLaunchKernelGGL((k_combine_f32<BM, BN, float>), grid, dim3(256), 0, s, (const float *)self, ld_self,
-                           (const float *)agg, ld_agg, m, d_in, (const float *)w, d_out, (int)relu,
-                           (float *)out, ld_out);
-    } else if (out_bf16) {
-        hipLaunchKernelGGL((k_combine_bf16<BM, BN, uint16_t>), grid, dim3(256), 0, s, (const uint16_t *)self,
-                           ld_self, (const uint16_t *)agg, ld_agg, m, d_in, (const uint16_t *)w, d_out,
-                           (int)relu, (uint16_t *)out, ld_out);
-    } else {
-        hipLaunchKernelGGL((k_combine_bf16<BM, BN, float>), grid, dim3(256), 0, s, (const uint16_t *)self,
-                           ld_self, (const uint16_t *)agg, ld_agg, m, d_in, (const uint16_t *)w, d_out,
-                           (int)relu, (float *)out, ld_out);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) av[e] = (row_ok && k + e < K) ? A[row * lda + k + e] : (uint16_t)0;
+        }
+        bf16x8 a;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) a[e] = __builtin_bit_cast(__bf16, av[e]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t n = n0 + j * 16 + l16;
+            bf16x8 b;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const uint16_t x = (n < N && k + e < K) ? Wk[(k + e) * N + n] : (uint16_t)0;
+                b[e] = __builtin_bit_cast(__bf16, x);
+            }
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[j], 0, 0, 0);
+        }
     }
-    GNNAV_HIP(hipGetLastError());
+};
+
+template <bool BF16, class InT, class OutT>
+__global__ void __launch_bounds__(256) k_combine_skinny(const InT *__restrict__ A0, int64_t lda0,
+                                                        const InT *__restrict__ A1, int64_t lda1, int64_t M,
+                                                        const int32_t *__restrict__ m_dev, int64_t K,
+                                                        const InT *__restrict__ W, int64_t N, int relu,
+                                                        OutT *__restrict__ C, int64_t ldc) {
+    using S = Skinny<BF16>;
+    __shared__ f32x4 part[4][4][64];
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, g = lane >> 4, l16 = lane & 15;
+    if (m_dev) M = *m_dev;
+    const int64_t m0 = (int64_t)blockIdx.x * 16, n0 = (int64_t)blockIdx.y * 64;
+    if (m0 >= M) return;
+    const int64_t row = m0 + l16;
+    const bool row_ok = row < M;
+    f32x4 acc[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int64_t kblocks = (K + S::KB - 1) / S::KB;
+    for (int64_t b = wid; b < 2 * kblocks; b += 4) {
+        const bool seg = b >= kblocks;
+        const int64_t kb = (seg ? b - kblocks : b) * S::KB;
+        S::block(seg ? A1 : A0, seg ? lda1 : lda0, row, row_ok, kb, K, W + (seg ? K : 0) * N, N, n0, g, l16, acc);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) part[wid][j][lane] = acc[j];
+    __syncthreads();
+    if (wid == 0) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            f32x4 s = part[0][j][lane];
+#pragma unroll
+            for (int w = 1; w < 4; ++w) s += part[w][j][lane];
+            acc[j] = s;
+        }
+        f32x4 t[1][4] = {{acc[0], acc[1], acc[2], acc[3]}};
+        write_tile<1, 4, OutT>(t, m0, n0, M, N, relu, C, ldc, g, l16);
+    }
 }
 
-void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m, int64_t d_in,
-                    const void *w, int64_t d_out, bool bf16, bool relu, bool out_bf16, void *out,
+// --------------------------------------------------------------- launch
+// bf16 weights are transposed to [N][2K] before the main kernel runs.  The
+// copy lives in one process-wide device buffer; an event recorded after the
+// last kernel that reads it orders every later call after it, whichever
+// stream that call uses.
+__global__ void __launch_bounds__(256) k_transpose_u16(const uint16_t *__restrict__ src, int64_t rows,
+                                                       int64_t cols, uint16_t *__restrict__ dst) {
+    const int64_t total = rows * cols;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        const int64_t c = i / rows, r = i % rows;   // consecutive threads write consecutive dst
+        dst[i] = src[r * cols + c];
+    }
+}
+
+namespace {
+struct SharedWorkspace {
+    std::mutex mu;
+    DevBuf buf;
+    hipEvent_t last_use = nullptr;
+};
+SharedWorkspace g_wt;
+}  // namespace
+
+template <int BM, int BN, int WM, int WN, int BKF, int BKH>
+static void launch_main(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
+                        const int32_t *m_dev, int64_t k, const void *w, int64_t n, bool bf16, bool relu,
+                        bool out_bf16, void *out, int64_t ld_out, hipStream_t s) {
+    const int64_t nrow = (m + BM - 1) / BM, ncol = (n + BN - 1) / BN;
+    const dim3 grid((unsigned)(((nrow + 7) / 8) * 8 * ncol));
+    if (!bf16) {
+        const int wvec = (((uintptr_t)w & 15u) == 0) && n % 4 == 0;
+        hipLaunchKernelGGL((k_combine_f32<BM, BN, WM, WN, BKF, float>), grid, dim3(256), 0, s, (const float *)self,
+                           ld_self, (const float *)agg, ld_agg, m, m_dev, k, (const float *)w, n, (int)relu,
+                           wvec, (float *)out, ld_out);
+        return;
+    }
+    std::lock_guard<std::mutex> lk(g_wt.mu);
+    if (!g_wt.last_use) GNNAV_HIP(hipEventCreateWithFlags(&g_wt.last_use, hipEventDisableTiming));
+    GNNAV_HIP(hipStreamWaitEvent(s, g_wt.last_use, 0));
+    g_wt.buf.ensure((size_t)(2 * k * n) * sizeof(uint16_t), s);
+    uint16_t *wt = g_wt.buf.as<uint16_t>();
+    hipLaunchKernelGGL(k_transpose_u16, dim3(grid_for(2 * k * n, 256, 1024)), dim3(256), 0, s, (const uint16_t *)w,
+                       2 * k, n, wt);
+    if (out_bf16)
+        hipLaunchKernelGGL((k_combine_bf16<BM, BN, WM, WN, BKH, uint16_t>), grid, dim3(256), 0, s,
+                           (const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, k,
+                           (const uint16_t *)wt, n, (int)relu, (uint16_t *)out, ld_out);
+    else
+        hipLaunchKernelGGL((k_combine_bf16<BM, BN, WM, WN, BKH, float>), grid, dim3(256), 0, s,
+                           (const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, k,
+                           (const uint16_t *)wt, n, (int)relu, (float *)out, ld_out);
+    GNNAV_HIP(hipEventRecord(g_wt.last_use, s));
+}
+
+// Output tiles below which the main kernel cannot fill 256 compute units.
+constexpr int64_t kSkinnyTiles = 160;
+
+struct GemmChoice {
+    int bm, bn;
+    void (*fn)(const void *, int64_t, const void *, int64_t, int64_t, const int32_t *, int64_t, const void *,
+               int64_t, bool, bool, bool, void *, int64_t, hipStream_t);
+};
+
+// Measured on MI355X (fp32 and bf16 alike): 64 x 64 tiles win until there
+// are enough 128 x 128 tiles to give every compute unit two, after which
+// the larger tile's reuse wins.
+static GemmChoice choose_main(int64_t m, int64_t d_out) {
+#ifdef GNNAV_GEMM_SWEEP
+    if (const char *e = getenv("GNNAV_GEMM_CFG")) {
+        switch (atoi(e)) {
+            case 1: return {64, 128, launch_main<64, 128, 2, 2, 16, 32>};
+            case 2: return {32, 256, launch_main<32, 256, 1, 4, 16, 32>};
+            case 3: return {64, 256, launch_main<64, 256, 1, 4, 16, 32>};
+            case 4: return {128, 128, launch_main<128, 128, 2, 2, 16, 32>};
+            case 5: return {64, 64, launch_main<64, 64, 2, 2, 16, 32>};
+            case 6: return {64, 128, launch_main<64, 128, 2, 2, 32, 64>};
+            case 7: return {64, 256, launch_main<64, 256, 1, 4, 32, 64>};
+            case 8: return {128, 128, launch_main<128, 128, 2, 2, 32, 64>};
+            case 9: return {64, 64, launch_main<64, 64, 2, 2, 32, 64>};
+            default: break;
+        }
+    }
+#endif
+    if (d_out > 64 && ((m + 127) / 128) * ((d_out + 127) / 128) >= 512)
+        return {128, 128, launch_main<128, 128, 2, 2, 16, 32>};
+    return {64, 64, launch_main<64, 64, 2, 2, 16, 32>};
+}
+
+void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
+                    const int32_t *m_dev, int64_t d_in, const void *w, int64_t d_out, bool bf16, bool relu, bool out_bf16, void *out,
                     int64_t ld_out, hipStream_t s, const char *label) {
     if (m <= 0) return;
-    if (d_out <= 64)
-        launch_combine_bn<64>(self, ld_self, agg, ld_agg, m, d_in, w, d_out, bf16, relu, out_bf16, out, ld_out, s,
-                              label);
-    else
-        launch_combine_bn<128>(self, ld_self, agg, ld_agg, m, d_in, w, d_out, bf16, relu, out_bf16, out, ld_out,
-                               s, label);
+    if (!bf16 && out_bf16) fail(GNNAV_E_INVALID, "bf16 output needs bf16 operands");
+    KernelTimer t(label, s);
+    const GemmChoice ch = choose_main(m, d_out);
+    const int64_t tiles = ((m + ch.bm - 1) / ch.bm) * ((d_out + ch.bn - 1) / ch.bn);
+    if (tiles < kSkinnyTiles) {
+        const dim3 grid((unsigned)((m + 15) / 16), (unsigned)((d_out + 63) / 64));
+        if (!bf16)
+            hipLaunchKernelGGL((k_combine_skinny<false, float, float>), grid, dim3(256), 0, s, (const float *)self,
+                               ld_self, (const float *)agg, ld_agg, m, m_dev, d_in, (const float *)w, d_out,
+                               (int)relu, (float *)out, ld_out);
+        else if (out_bf16)
+            hipLaunchKernelGGL((k_combine_skinny<true, uint16_t, uint16_t>), grid, dim3(256), 0, s,
+                               (const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, d_in,
+                               (const uint16_t *)w, d_out, (int)relu, (uint16_t *)out, ld_out);
+        else
+            hipLaunchKernelGGL((k_combine_skinny<true, uint16_t, float>), grid, dim3(256), 0, s,
+                               (const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, d_in,
+                               (const uint16_t *)w, d_out, (int)relu, (float *)out, ld_out);
+    } else {
+        ch.fn(self, ld_self, agg, ld_agg, m, m_dev, d_in, w, d_out, bf16, relu, out_bf16, out, ld_out, s);
+    }
+    GNNAV_HIP(hipGetLastError());
 }
 
 }  // namespace gnnav

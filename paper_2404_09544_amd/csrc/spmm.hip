@@ -49,6 +49,7 @@ struct Unit<true> {
 template <bool BF16, int G, int Q>
 __global__ void __launch_bounds__(256) k_spmm_mean(const int32_t *__restrict__ indptr,
                                                    const int32_t *__restrict__ indices, int64_t n_dst,
+                                                   const int32_t *__restrict__ n_dst_dev,
                                                    const uint4 *__restrict__ x, int64_t x_ld16,
                                                    uint4 *__restrict__ out, int64_t out_ld16, int32_t chunks,
                                                    int32_t d) {
@@ -57,6 +58,7 @@ __global__ void __launch_bounds__(256) k_spmm_mean(const int32_t *__restrict__ i
     constexpr int RPW = kWave / G;
     const int lane = lane_id();
     const int sub = lane / G, c0 = lane % G;
+    if (n_dst_dev) n_dst = *n_dst_dev;
     const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
     for (int64_t r = (((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave) * RPW + sub; r < n_dst;
          r += nwaves * RPW) {
@@ -118,7 +120,8 @@ __global__ void __launch_bounds__(256) k_spmm_mean(const int32_t *__restrict__ i
 }
 
 template <bool BF16>
-static void launch_spmm_t(const int32_t *indptr, const int32_t *indices, int64_t n_dst, const void *x,
+static void launch_spmm_t(const int32_t *indptr, const int32_t *indices, int64_t n_dst,
+                          const int32_t *n_dst_dev, const void *x,
                           int64_t ld_x, int64_t d, void *out, int64_t ld_out, hipStream_t s,
                           const char *label) {
     constexpr int elt = BF16 ? 2 : 4;
@@ -135,7 +138,7 @@ static void launch_spmm_t(const int32_t *indptr, const int32_t *indices, int64_t
     KernelTimer t(label, s);
 #define GNNAV_L(GV, QV)                                                                             \
     hipLaunchKernelGGL((k_spmm_mean<BF16, GV, QV>), dim3(grid), dim3(256), 0, s, indptr, indices,     \
-                       n_dst, xx, xl, oo, ol, chunks, (int32_t)d)
+                       n_dst, n_dst_dev, xx, xl, oo, ol, chunks, (int32_t)d)
     if (g < kWave) {
         switch (g) {
             case 1: GNNAV_L(1, 1); break;
@@ -158,14 +161,15 @@ static void launch_spmm_t(const int32_t *indptr, const int32_t *indices, int64_t
     GNNAV_HIP(hipGetLastError());
 }
 
-void launch_aggregate_mean(const int32_t *indptr, const int32_t *indices, int64_t n_dst, const void *x,
+void launch_aggregate_mean(const int32_t *indptr, const int32_t *indices, int64_t n_dst,
+                           const int32_t *n_dst_dev, const void *x,
                            int64_t ld_x, int64_t d, bool bf16, void *out, int64_t ld_out, hipStream_t s,
                            const char *label) {
     if (n_dst <= 0) return;
     if (bf16)
-        launch_spmm_t<true>(indptr, indices, n_dst, x, ld_x, d, out, ld_out, s, label);
+        launch_spmm_t<true>(indptr, indices, n_dst, n_dst_dev, x, ld_x, d, out, ld_out, s, label);
     else
-        launch_spmm_t<false>(indptr, indices, n_dst, x, ld_x, d, out, ld_out, s, label);
+        launch_spmm_t<false>(indptr, indices, n_dst, n_dst_dev, x, ld_x, d, out, ld_out, s, label);
 }
 
 }  // namespace gnnav

@@ -1,16 +1,27 @@
 """One sampled mini-batch step through the C ABI (Algorithm 1's forward).
 
-``MiniBatchStep.run`` enqueues gnnav_sample -> gnnav_gather(F_L) ->
-gnnav_sage_forward on one stream.  Device buffers (gathered features,
-logits, hit/miss counts) are torch tensors that only grow, so a steady run
-allocates nothing per batch.
+``MiniBatchStep.run`` is the synchronous form: gnnav_sample (which publishes
+the frontier sizes to the host) -> gnnav_gather(F_L) -> gnnav_sage_forward.
+
+``MiniBatchStep.enqueue`` is the asynchronous form: gnnav_sample_async ->
+gnnav_gather_n (row count read on the device) -> gnnav_sage_forward, all on
+one stream with no host synchronisation; ``finish`` waits and returns the
+logits.  Buffers are sized once from the Eq. 12 capacity bounds.
+
+``Pipeline`` runs consecutive batches on alternating streams, each with its
+own step (blocks, gathered rows, logits), so batch b+1's sampling and
+host-link gather overlap batch b's aggregation and combine: the overlap
+Eq. 4 assumes when it takes the epoch time as n_iter times the larger of
+(t_sample + t_transfer) and (t_replace + t_compute).
+
+Device buffers are torch tensors that only grow.
 """
 from __future__ import annotations
 
 import numpy as np
 import torch
 
-from . import BF16, Blocks, Cache, Graph, gather, padded_ld, sage_forward, sample
+from . import Blocks, Cache, Graph, gather, gather_n, sage_forward, sample, sample_async
 
 
 def to_device_weights(ws, dtype: str):
@@ -28,23 +39,29 @@ class MiniBatchStep:
         self.weights = list(weights_dev)
         self.dims = list(dims)
         self.fanouts = list(fanouts)
+        self.L = len(self.fanouts)
         self.dtype = dtype
         self.blocks = Blocks()
         self.ld = cache.ld
-        tdt = torch.int16 if dtype == "bf16" else torch.float32
-        self._tdt = tdt
-        self.h0 = torch.empty((0, self.ld), dtype=tdt, device="cuda")
+        self._tdt = torch.int16 if dtype == "bf16" else torch.float32
+        self.h0 = torch.empty((0, self.ld), dtype=self._tdt, device="cuda")
         self.logits = torch.empty((0, self.dims[-1]), dtype=torch.float32, device="cuda")
         self.counts = torch.zeros(3, dtype=torch.int64, device="cuda")
         self.sizes = None
+        self._seeds = None
+        self._stream = None
 
-    def _grow(self, n_l: int, n_0: int):
+    def _grow(self, n_l: int, n_0: int, stream=None):
+        if self.h0.shape[0] >= n_l and self.logits.shape[0] >= n_0:
+            return
+        if stream is not None:
+            stream.synchronize()        # old buffers may still be read by enqueued work
         if self.h0.shape[0] < n_l:
-            self.h0 = torch.empty((int(n_l * 1.25) + 16, self.ld), dtype=self._tdt, device="cuda")
+            self.h0 = torch.empty((n_l + 16, self.ld), dtype=self._tdt, device="cuda")
         if self.logits.shape[0] < n_0:
-            self.logits = torch.empty((int(n_0 * 1.25) + 16, self.dims[-1]), dtype=torch.float32,
-                                      device="cuda")
+            self.logits = torch.empty((n_0 + 16, self.dims[-1]), dtype=torch.float32, device="cuda")
 
+    # -------------------------------------------------------------- sync
     def run(self, seeds_dev, rng_seed: int, stream=None):
         """Sample, gather and forward one batch; returns the logits view [|F_0|, classes]."""
         sample(self.graph, seeds_dev, self.fanouts, rng_seed, self.blocks, stream)
@@ -55,5 +72,46 @@ class MiniBatchStep:
         sage_forward(self.blocks, self.h0, self.weights, self.dims, self.dtype, self.logits, stream)
         return self.logits[:sizes[0]]
 
+    # ------------------------------------------------------------- async
+    def enqueue(self, seeds_dev, rng_seed: int, stream=None):
+        """Enqueue one batch on `stream` without waiting for it."""
+        st = stream if stream is not None else torch.cuda.current_stream()
+        self._seeds = seeds_dev            # keep alive until the work has run
+        self._stream = st
+        sample_async(self.graph, seeds_dev, self.fanouts, rng_seed, self.blocks, st)
+        sizes_ptr, bounds = self.blocks.device_sizes(self.L)
+        self._grow(bounds[-1], bounds[0], st)
+        gather_n(self.cache, self.blocks.nodes_ptr(), sizes_ptr + 4 * self.L, bounds[-1], self.h0,
+                 self.counts, st)
+        sage_forward(self.blocks, self.h0, self.weights, self.dims, self.dtype, self.logits, st)
+        self.sizes = None
+
+    def finish(self):
+        """Wait for the enqueued batch; returns its logits view [|F_0|, classes]."""
+        self.blocks.sync(self._stream)
+        self.sizes, _ = self.blocks.sizes()
+        return self.logits[:self.sizes[0]]
+
     def h0_view(self):
         return self.h0[:self.sizes[-1]]
+
+
+class Pipeline:
+    """Batches b, b+1, ... on `depth` streams in turn (slot b % depth)."""
+
+    def __init__(self, graph: Graph, cache: Cache, weights_dev, dims, fanouts, dtype: str, depth: int = 2):
+        self.slots = [MiniBatchStep(graph, cache, weights_dev, dims, fanouts, dtype) for _ in range(depth)]
+        self.streams = [torch.cuda.Stream() for _ in range(depth)]
+        self.depth = depth
+        self.count = 0
+
+    def enqueue(self, seeds_dev, rng_seed: int):
+        """Enqueue the next batch; returns the slot it runs in."""
+        k = self.count % self.depth
+        self.slots[k].enqueue(seeds_dev, rng_seed, self.streams[k])
+        self.count += 1
+        return self.slots[k]
+
+    def synchronize(self):
+        for s in self.streams:
+            s.synchronize()

@@ -256,8 +256,11 @@ def test_aggregate_mean_parity(G, d, dtype):
         assert not host(out, dtype)[:, d:d + tail].any()
 
 
+# Small M runs the skinny kernel (fewer than 160 main-kernel tiles); large M
+# the main kernel with 32x256 (N > 128), 64x128 (64 < N <= 128) or 64x64 tiles.
 COMBINE_CASES = [(1, 3, 16), (63, 64, 41), (64, 100, 47), (65, 602, 256), (1000, 128, 64),
-                 (777, 256, 256), (130, 5, 300)]
+                 (777, 256, 256), (130, 5, 300), (20000, 602, 256), (12000, 64, 41),
+                 (12001, 100, 100), (9000, 256, 256), (10240, 3, 47), (6000, 128, 260)]
 
 
 @pytest.mark.parametrize("relu", [False, True])
@@ -361,3 +364,99 @@ def test_determinism(G):
     for a, b in zip(outs[0][1][2:], outs[1][1][2:]):
         for x, y in zip(a, b):
             assert np.array_equal(x, y)
+
+
+# ------------------------------------------------ async step, two streams
+
+def oracle_batch(n, u, v, feats, dtype, dims, fanouts, r, seeds, rng_seed, ws):
+    csr = O.build_csr(n, u, v)
+    ref_b = O.sample_blocks(csr, seeds, fanouts, rng_seed)
+    _, slot, _ = O.rank_cache(csr, r)
+    h0, counts = O.gather(feats, slot, ref_b.nodes)
+    logits = O.sage_forward(ref_b, O.to_f64(h0, dtype), [O.to_f64(w, dtype) for w in ws],
+                            bf16=dtype == "bf16")
+    return ref_b, h0, counts, logits
+
+
+def check_step(G, step, ref, dtype, d):
+    ref_b, h0, counts, logits = ref
+    compare_blocks(G, step.blocks, ref_b)
+    assert np.array_equal(host(step.counts), counts)
+    got_h0 = host(step.h0_view(), dtype)[:, :d]
+    assert np.array_equal(got_h0.view(np.uint8), h0.view(np.uint8))
+    got = host(step.logits[:step.sizes[0]])
+    assert_rows_close(got, logits, BF16_TOL if dtype == "bf16" else FP32_TOL, "logits")
+
+
+@pytest.mark.parametrize("r,on_device", [(0.0, True), (0.3, False)])
+def test_async_step_matches_oracle(G, r, on_device):
+    from paper_2404_09544_amd.step import MiniBatchStep, to_device_weights
+    wl = W.Workload("chunglu-10k-d64")
+    s, d = wl.edges()
+    feats = wl.features()
+    ws = [W.glorot(wl.dims[l], wl.dims[l + 1], wl.dtype, seed=11 + l) for l in range(wl.L)]
+    g = G.Graph(wl.n, s, d)
+    c = G.Cache(g, feats, wl.dtype, r, store_on_device=on_device)
+    step = MiniBatchStep(g, c, to_device_weights(ws, wl.dtype), wl.dims, wl.fanouts, wl.dtype)
+    for b in range(3):
+        say("async step", r, on_device, b)
+        seeds = wl.seeds(b)
+        step.enqueue(dev(seeds), wl.rng_seed(b))
+        step.finish()
+        check_step(G, step, oracle_batch(wl.n, s, d, feats, wl.dtype, wl.dims, wl.fanouts, r, seeds,
+                                         wl.rng_seed(b), ws), wl.dtype, wl.d)
+
+
+def test_async_step_bf16_three_hops(G):
+    from paper_2404_09544_amd.step import MiniBatchStep, to_device_weights
+    n, u, v = W.random_graph(6000, 50000, 21)
+    feats = W.features(n, 128, "bf16", seed=3)
+    dims, fanouts = [128, 64, 48, 10], [6, 4, 3]
+    ws = [W.glorot(dims[l], dims[l + 1], "bf16", seed=11 + l) for l in range(3)]
+    g = G.Graph(n, u, v, offsets_i64=True)
+    c = G.Cache(g, feats, "bf16", 0.25)
+    step = MiniBatchStep(g, c, to_device_weights(ws, "bf16"), dims, fanouts, "bf16")
+    seeds = W.epoch_permutation(n)[:300]
+    say("async bf16")
+    step.enqueue(dev(seeds), 77)
+    step.finish()
+    check_step(G, step, oracle_batch(n, u, v, feats, "bf16", dims, fanouts, 0.25, seeds, 77, ws), "bf16", 128)
+
+
+def test_async_bad_seed_reported_at_sync(G):
+    from paper_2404_09544_amd.step import MiniBatchStep, to_device_weights
+    n, u, v = W.random_graph(500, 4000, 2)
+    g = G.Graph(n, u, v)
+    c = G.Cache(g, W.features(n, 8, "f32"), "f32", 0.5)
+    ws = [W.glorot(8, 4, "f32", seed=1)]
+    step = MiniBatchStep(g, c, to_device_weights(ws, "f32"), [8, 4], [3], "f32")
+    say("async bad seed")
+    step.enqueue(dev(np.array([1, n + 3, 2], np.int32)), 5)
+    with pytest.raises(G.GnnavError) as e:
+        step.finish()
+    assert e.value.status == 2
+
+
+@pytest.mark.parametrize("depth", [2, 3])
+def test_pipeline_matches_oracle(G, depth):
+    """Batches on alternating streams give each batch's oracle result."""
+    from paper_2404_09544_amd.step import Pipeline, to_device_weights
+    wl = W.Workload("chunglu-10k-d64")
+    s, d = wl.edges()
+    feats = wl.features()
+    r = 0.3
+    ws = [W.glorot(wl.dims[l], wl.dims[l + 1], wl.dtype, seed=11 + l) for l in range(wl.L)]
+    g = G.Graph(wl.n, s, d)
+    c = G.Cache(g, feats, wl.dtype, r)
+    pipe = Pipeline(g, c, to_device_weights(ws, wl.dtype), wl.dims, wl.fanouts, wl.dtype, depth=depth)
+    seeds_dev = [dev(wl.seeds(b)) for b in range(2 * depth)]
+    for rnd in range(2):
+        slots = []
+        for k in range(depth):
+            b = rnd * depth + k
+            say("pipeline", depth, b)
+            slots.append((b, pipe.enqueue(seeds_dev[b], wl.rng_seed(b))))
+        for b, slot in slots:
+            slot.finish()
+            check_step(G, slot, oracle_batch(wl.n, s, d, feats, wl.dtype, wl.dims, wl.fanouts, r,
+                                             wl.seeds(b), wl.rng_seed(b), ws), wl.dtype, wl.d)
