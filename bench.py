@@ -72,6 +72,7 @@ def main():
     ap.add_argument("--cache-fraction", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-batches", type=int, default=2)
+    ap.add_argument("--depth", type=int, default=2, help="streams in the pipelined pass")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (scales rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
@@ -145,8 +146,8 @@ def main():
     seq_ms = seq_elapsed * 1e3 / args.steps
     log(f"sequential {args.steps} steps: {seq_ms:.3f} ms/step, {wl.batch * args.steps / seq_elapsed:,.0f} seeds/s")
 
-    # ---- phase 2: the two-stream pipeline (batch b+1 overlaps batch b) ----
-    pipe = Pipeline(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, depth=2)
+    # ---- phase 2: the pipeline (batch b+1 overlaps batch b on another stream)
+    pipe = Pipeline(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, depth=args.depth)
     for b in range(args.warmup):
         slot = pipe.enqueue(seeds_dev[b], wl.rng_seed(b))
     pipe.synchronize()
@@ -260,7 +261,7 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
         "data": "synthetic",
-        "config": {"workload": wl.name, "n": wl.n, "nnz": g.nnz, "d": wl.d, "fanouts": wl.fanouts,
+        "config": {"workload": wl.name, "pipeline_streams": args.depth, "n": wl.n, "nnz": g.nnz, "d": wl.d, "fanouts": wl.fanouts,
                    "batch": wl.batch, "layers": wl.L, "dims": wl.dims, "cache_fraction": r,
                    "store_on_device": wl.cfg["store_on_device"], "global_batch": wl.batch},
         "value_sequential": round(wl.batch * args.steps / seq_elapsed, 2),

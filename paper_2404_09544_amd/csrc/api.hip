@@ -285,7 +285,8 @@ static bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 struct GatherWs {
     hipStream_t stream = nullptr, side = nullptr;
     hipEvent_t fork = nullptr, join = nullptr;
-    DevBuf hit_list, miss_list, part, dev_counts;
+    DevBuf hit_list, miss_list, dev_counts;
+    ScanState scan;   // its look-back timeout counter is not checked (the gather is asynchronous)
 };
 
 struct gnnav_cache {
@@ -323,8 +324,11 @@ static void free_cache(gnnav_cache *c) {
     for (auto *w : c->ws) {
         w->hit_list.release();
         w->miss_list.release();
-        w->part.release();
         w->dev_counts.release();
+        w->scan.status.release();
+        w->scan.sums.release();
+        w->scan.prefix.release();
+        w->scan.ctl.release();
         if (w->side) (void)hipStreamDestroy(w->side);
         if (w->fork) (void)hipEventDestroy(w->fork);
         if (w->join) (void)hipEventDestroy(w->join);
@@ -466,7 +470,8 @@ struct gnnav_blocks {
     int64_t nb[kMaxHops + 1] = {0};    // Eq. 12 capacity bounds of the last sample
     int64_t eb[kMaxHops + 1] = {0};
     int64_t map_nodes = -1;
-    DevBuf map, sizes, nodes, part;
+    DevBuf map, sizes, nodes;
+    ScanState scan;
     DevBuf indptr[kMaxHops], nbrs[kMaxHops], indices[kMaxHops];
     int32_t *sizes_host = nullptr;  // pinned mirror of `sizes`
     DevBuf agg, hid[2];             // forward workspace
@@ -476,7 +481,7 @@ extern "C" gnnav_status gnnav_blocks_create(gnnav_blocks **out) {
     return guarded([&] {
         GNNAV_CHECK(out, GNNAV_E_INVALID, "out is NULL");
         auto *b = new gnnav_blocks();
-        if (hipHostMalloc((void **)&b->sizes_host, kSizeSlots * sizeof(int32_t), hipHostMallocDefault) !=
+        if (hipHostMalloc((void **)&b->sizes_host, (kSizeSlots + 1) * sizeof(int32_t), hipHostMallocDefault) !=
             hipSuccess) {
             (void)hipGetLastError();
             delete b;
@@ -492,7 +497,10 @@ extern "C" void gnnav_blocks_free(gnnav_blocks *b) {
     b->map.release();
     b->sizes.release();
     b->nodes.release();
-    b->part.release();
+    b->scan.status.release();
+    b->scan.sums.release();
+    b->scan.prefix.release();
+    b->scan.ctl.release();
     for (int h = 0; h < kMaxHops; ++h) {
         b->indptr[h].release();
         b->nbrs[h].release();
@@ -537,7 +545,7 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
     }
     b->sizes.ensure(kSizeSlots * sizeof(int32_t), s);
     b->nodes.ensure(std::max<int64_t>(nb[n_hops], 1) * sizeof(int32_t), s);
-    b->part.ensure(scan_parts(max_list) * sizeof(int64_t), s);
+    b->scan.ensure(max_list, s);
     for (int h = 1; h <= n_hops; ++h) {
         b->indptr[h - 1].ensure((nb[h - 1] + 1) * sizeof(int32_t), s);
         b->nbrs[h - 1].ensure(std::max<int64_t>(eb[h], 1) * sizeof(int32_t), s);
@@ -546,20 +554,19 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
     int32_t *sz = b->sizes.as<int32_t>();
     int32_t *map = b->map.as<int32_t>();
     int32_t *nodes = b->nodes.as<int32_t>();
-    int32_t *part = b->part.as<int32_t>();
     launch_fill_i32(sz, 0, kSizeSlots, s);
     // F_0: seeds without repeats, first occurrence kept
     DedupArgs d0{seeds_dev, n_seeds, nullptr, n_seeds, map, g->n, nodes, nullptr, sz + kSizeN, sz + kSizeErr,
-                 part};
+                 &b->scan};
     launch_dedup(d0, s);
     for (int h = 1; h <= n_hops; ++h) {
         SampleHopArgs a{g->row_ptr.p, g->i64, g->col.as<int32_t>(), nodes, sz + kSizeN + h - 1,
                         b->indptr[h - 1].as<int32_t>(), b->nbrs[h - 1].as<int32_t>(), sz + kSizeE + h,
-                        fanouts[h - 1], rng_seed, (uint32_t)(h - 1), nb[h - 1], part};
+                        fanouts[h - 1], rng_seed, (uint32_t)(h - 1), nb[h - 1], &b->scan};
         launch_count_scan(a, s);
         launch_sample_hop(a, s);
         DedupArgs dh{b->nbrs[h - 1].as<int32_t>(), 0, sz + kSizeE + h, eb[h], map, g->n, nodes,
-                     sz + kSizeN + h - 1, sz + kSizeN + h, nullptr, part};
+                     sz + kSizeN + h - 1, sz + kSizeN + h, nullptr, &b->scan};
         launch_dedup(dh, s);
         launch_relabel(b->nbrs[h - 1].as<int32_t>(), sz + kSizeE + h, eb[h], map,
                        b->indices[h - 1].as<int32_t>(), s);
@@ -577,7 +584,10 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
 static void publish_sizes(gnnav_blocks *b, hipStream_t s) {
     GNNAV_CHECK(b->sizes.p, GNNAV_E_INVALID, "blocks have not been sampled");
     GNNAV_HIP(hipMemcpyAsync(b->sizes_host, b->sizes.p, kSizeSlots * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    GNNAV_HIP(hipMemcpyAsync(b->sizes_host + kSizeSlots, b->scan.timeouts(), sizeof(int32_t), hipMemcpyDeviceToHost,
+                             s));
     GNNAV_HIP(hipStreamSynchronize(s));
+    GNNAV_CHECK(b->sizes_host[kSizeSlots] == 0, GNNAV_E_DEVICE, "a device-wide scan's look-back wait timed out");
     for (int h = 0; h <= b->L; ++h) b->n_h[h] = b->sizes_host[kSizeN + h];
     for (int h = 1; h <= b->L; ++h) b->e_h[h] = b->sizes_host[kSizeE + h];
     b->host_sizes = true;
@@ -660,10 +670,10 @@ static void gather_impl(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_
     GatherWs *w = gather_ws(cc, s);
     w->hit_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
     w->miss_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
-    w->part.ensure(scan_parts(n_ids) * sizeof(int64_t), s);
+    w->scan.ensure(n_ids, s);
     GatherArgs a{ids_dev, n_ids, n_dev, c->slot_map.as<int32_t>(), c->n, c->cache_rows.p, c->store_ptr,
                  c->ld * c->elt, out_dev, ld_out * c->elt, c->d * c->elt, counts_dev, w->dev_counts.as<int32_t>(),
-                 w->hit_list.as<int2>(), w->miss_list.as<int2>(), w->part.as<int32_t>()};
+                 w->hit_list.as<int2>(), w->miss_list.as<int2>(), &w->scan};
     launch_classify(a, s);
     if (n_ids == 0) return;
     GNNAV_HIP(hipEventRecord(w->fork, s));

@@ -128,8 +128,8 @@ __device__ __forceinline__ V block_exclusive_sum(V x, V *scratch, V &total) {
 }
 
 // ------------------------------------------------------------ launchers
-// Device-wide exclusive scan + emit in three launches (per-tile sums, one
-// block scanning the tile sums, per-tile scan and emit).  See scan.hpp.
+struct ScanState;   // scan.hpp: state of a one-launch device-wide scan
+void launch_fill_i32(int32_t *p, int32_t v, int64_t n, hipStream_t s);
 
 // sample.hip
 struct SampleHopArgs {
@@ -145,7 +145,7 @@ struct SampleHopArgs {
     uint64_t rng_seed;
     uint32_t hop;            // 0-based
     int64_t rows_bound;
-    int32_t *part;           // scan partials
+    ScanState *scan;
 };
 void launch_count_scan(const SampleHopArgs &a, hipStream_t s);
 void launch_sample_hop(const SampleHopArgs &a, hipStream_t s);
@@ -161,14 +161,13 @@ struct DedupArgs {
     const int32_t *base_ptr; // device |F_(h-1)| (nullptr: 0)
     int32_t *size_out;       // device |F_h|
     int32_t *err;            // device count of out-of-range ids (nullable)
-    int32_t *part;
+    ScanState *scan;
 };
 void launch_dedup(const DedupArgs &a, hipStream_t s);
 void launch_relabel(const int32_t *list, const int32_t *len_ptr, int64_t len_bound,
                     const int32_t *map, int32_t *indices, hipStream_t s);
 void launch_reset_map(const int32_t *nodes, const int32_t *n_ptr, int64_t bound, int32_t *map,
                       hipStream_t s);
-void launch_fill_i32(int32_t *p, int32_t v, int64_t n, hipStream_t s);
 
 // gather.hip
 struct GatherArgs {
@@ -187,7 +186,7 @@ struct GatherArgs {
     int32_t *dev_counts;     // device int32[2]: hits, misses
     int2 *hit_list;
     int2 *miss_list;
-    int32_t *part;
+    ScanState *scan;
 };
 void launch_classify(const GatherArgs &a, hipStream_t s);
 void launch_gather_rows(const GatherArgs &a, bool hits, hipStream_t s);

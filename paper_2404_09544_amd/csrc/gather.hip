@@ -59,7 +59,7 @@ struct ClassifyOp {
 void launch_classify(const GatherArgs &a, hipStream_t s) {
     ClassifyOp op{a.ids, a.n_ids, a.n_ptr, a.slot_map, a.n_nodes, a.hit_list, a.miss_list, a.counts,
                   a.dev_counts, (uint4 *)a.out, a.out_ld_bytes / 16, (a.row_bytes + 15) / 16};
-    run_scan(op, a.n_ids, (int64_t *)a.part, "classify", s);
+    run_scan<ClassifyOp, int64_t>(op, a.n_ids, *a.scan, "classify", s);
 }
 
 // G lanes per row (power of two), 64/G rows per wavefront pass.  Each lane

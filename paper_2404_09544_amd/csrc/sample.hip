@@ -72,10 +72,10 @@ struct CountOp {
 void launch_count_scan(const SampleHopArgs &a, hipStream_t s) {
     if (a.offsets_i64) {
         CountOp<int64_t> op{(const int64_t *)a.row_ptr, a.nodes, a.n_prev, a.fanout, a.indptr, a.e_out};
-        run_scan(op, a.rows_bound, a.part, "count_scan", s);
+        run_scan<CountOp<int64_t>, int32_t>(op, a.rows_bound, *a.scan, "count_scan", s);
     } else {
         CountOp<int32_t> op{(const int32_t *)a.row_ptr, a.nodes, a.n_prev, a.fanout, a.indptr, a.e_out};
-        run_scan(op, a.rows_bound, a.part, "count_scan", s);
+        run_scan<CountOp<int32_t>, int32_t>(op, a.rows_bound, *a.scan, "count_scan", s);
     }
 }
 
@@ -246,7 +246,7 @@ void launch_dedup(const DedupArgs &a, hipStream_t s) {
         GNNAV_HIP(hipGetLastError());
     }
     DedupOp op{a.list, a.len_const, a.len_ptr, a.map, a.n_nodes, a.nodes, a.base_ptr, a.size_out};
-    run_scan(op, a.len_bound, a.part, "dedup_scan", s);
+    run_scan<DedupOp, int32_t>(op, a.len_bound, *a.scan, "dedup_scan", s);
 }
 
 __global__ void __launch_bounds__(256) k_relabel(const int32_t *__restrict__ list,

@@ -1,4 +1,4 @@
-// Device-wide exclusive scan with a per-element emit step.
+// Device-wide exclusive scan with a per-element emit step, in one launch.
 //
 // An Op supplies, on the device:
 //   int64_t n() const                    element count (may be read from HBM)
@@ -6,10 +6,21 @@
 //   void emit(int64_t i, V prefix, V v)  called for every i with its
 //                                        exclusive prefix (sum over j < i)
 //   void total(V t)                      called once with the grand total
-// Three launches: per-tile sums, one block scanning the tile sums into tile
-// offsets (and reporting the total), then per-tile scans that emit.  Each
-// thread owns kItems consecutive elements, so the emit order inside a tile
-// follows the element order and the result does not depend on scheduling.
+//
+// Single-pass scan with decoupled look-back: workgroups claim tiles in order
+// from an atomic ticket (so a tile only ever waits for tiles whose
+// workgroups are already running) until the tiles run out; the grid is
+// capped, not sized to the element bound.  A workgroup reduces its tile,
+// publishes the tile sum, then
+// looks back: its first wavefront polls the 64 preceding tiles at once,
+// finds the nearest one that has published an inclusive prefix, adds that
+// prefix and the tile sums in between (a wave reduction), and moves the
+// window back by 64 tiles if none has.  It then publishes its own inclusive
+// prefix and emits.  Status words carry the call's epoch, so they never need
+// clearing between calls.  Each thread owns kScanItems consecutive elements,
+// so results do not depend on scheduling.  The look-back wait is bounded: a
+// wait that exceeds kSpinLimit polls gives up, counts an error and lets the
+// workgroup finish (the results are then wrong and the caller reports it).
 #pragma once
 
 #include "common.hpp"
@@ -19,92 +30,154 @@ namespace gnnav {
 constexpr int kScanThreads = 256;
 constexpr int kScanItems = 8;
 constexpr int kScanTile = kScanThreads * kScanItems;
-
-template <class Op, class V>
-__global__ void __launch_bounds__(kScanThreads) k_scan_tiles(Op op, V *part) {
-    __shared__ V scratch[kScanThreads / kWave];
-    const int64_t n = op.n();
-    const int64_t base = (int64_t)blockIdx.x * kScanTile;
-    if (base >= n) return;  // uniform across the block
-    const int64_t first = base + (int64_t)threadIdx.x * kScanItems;
-    V s = V(0);
-#pragma unroll
-    for (int j = 0; j < kScanItems; ++j) {
-        int64_t i = first + j;
-        if (i < n) s += op.value(i);
-    }
-    V total;
-    block_exclusive_sum<V, kScanThreads>(s, scratch, total);
-    if (threadIdx.x == 0) part[blockIdx.x] = total;
-}
-
-template <class Op, class V>
-__global__ void __launch_bounds__(1024) k_scan_spine(Op op, V *part) {
-    __shared__ V scratch[1024 / kWave];
-    const int64_t n = op.n();
-    const int64_t tiles = (n + kScanTile - 1) / kScanTile;
-    V carry = V(0);
-    for (int64_t b = 0; b < tiles; b += 1024) {
-        int64_t i = b + threadIdx.x;
-        V x = i < tiles ? part[i] : V(0);
-        V total;
-        V ex = block_exclusive_sum<V, 1024>(x, scratch, total);
-        if (i < tiles) part[i] = carry + ex;
-        carry += total;
-    }
-    if (threadIdx.x == 0) op.total(carry);
-}
-
-template <class Op, class V>
-__global__ void __launch_bounds__(kScanThreads) k_scan_emit(Op op, const V *part) {
-    __shared__ V scratch[kScanThreads / kWave];
-    const int64_t n = op.n();
-    const int64_t base = (int64_t)blockIdx.x * kScanTile;
-    if (base >= n) return;
-    const int64_t first = base + (int64_t)threadIdx.x * kScanItems;
-    V vals[kScanItems];
-    V s = V(0);
-#pragma unroll
-    for (int j = 0; j < kScanItems; ++j) {
-        int64_t i = first + j;
-        vals[j] = i < n ? op.value(i) : V(0);
-        s += vals[j];
-    }
-    V total;
-    V run = block_exclusive_sum<V, kScanThreads>(s, scratch, total) + part[blockIdx.x];
-#pragma unroll
-    for (int j = 0; j < kScanItems; ++j) {
-        int64_t i = first + j;
-        if (i < n) op.emit(i, run, vals[j]);
-        run += vals[j];
-    }
-}
-
-// Enqueue the three launches.  `bound` >= op.n() sizes the grids; `part`
-// must hold ceil(bound / kScanTile) values (at least one).
-template <class Op, class V>
-void run_scan(const Op &op, int64_t bound, V *part, const char *name, hipStream_t s) {
-    const int64_t tiles = (bound + kScanTile - 1) / kScanTile;
-    if (tiles > 0) {
-        KernelTimer t(name, s);
-        hipLaunchKernelGGL((k_scan_tiles<Op, V>), dim3((unsigned)tiles), dim3(kScanThreads), 0, s,
-                           op, part);
-    }
-    {
-        KernelTimer t(name, s);
-        hipLaunchKernelGGL((k_scan_spine<Op, V>), dim3(1), dim3(1024), 0, s, op, part);
-    }
-    if (tiles > 0) {
-        KernelTimer t(name, s);
-        hipLaunchKernelGGL((k_scan_emit<Op, V>), dim3((unsigned)tiles), dim3(kScanThreads), 0, s,
-                           op, (const V *)part);
-    }
-    GNNAV_HIP(hipGetLastError());
-}
+constexpr uint32_t kSpinLimit = 1u << 20;
+constexpr int64_t kScanGrid = 1024;   // workgroups per scan launch, at most
 
 inline int64_t scan_parts(int64_t bound) {
     int64_t t = (bound + kScanTile - 1) / kScanTile;
     return t < 1 ? 1 : t;
+}
+
+// Device state of one scan sequence (calls on one stream, in order).
+struct ScanState {
+    DevBuf status;    // uint32 per tile: (epoch << 2) | 0 none, 1 tile sum, 2 inclusive prefix
+    DevBuf sums;      // int64 per tile
+    DevBuf prefix;    // int64 per tile
+    DevBuf ctl;       // uint32 [0] ticket, [1] look-back timeouts
+    int64_t tiles = 0;
+    uint32_t epoch = 0;
+    void ensure(int64_t bound, hipStream_t s) {
+        const int64_t t = scan_parts(bound);
+        if (!ctl.p) {
+            ctl.ensure(4 * sizeof(uint32_t), s);
+            launch_fill_i32(ctl.as<int32_t>(), 0, 4, s);
+        }
+        if (t > tiles) {
+            status.ensure((size_t)t * sizeof(uint32_t), s);
+            sums.ensure((size_t)t * sizeof(int64_t), s);
+            prefix.ensure((size_t)t * sizeof(int64_t), s);
+            tiles = (int64_t)(status.bytes / sizeof(uint32_t));
+            launch_fill_i32(status.as<int32_t>(), 0, tiles, s);
+        }
+    }
+    uint32_t next_epoch() {
+        epoch = (epoch + 1) & 0x3fffffffu;
+        if (epoch == 0) epoch = 1;
+        return epoch;
+    }
+    uint32_t *timeouts() const { return ctl.as<uint32_t>() + 1; }
+};
+
+template <class V>
+__device__ __forceinline__ void publish(uint32_t *status, V *slot, int64_t tile, V v, uint32_t word) {
+    slot[tile] = v;
+    __hip_atomic_store(&status[tile], word, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <class Op, class V>
+__global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, uint32_t *__restrict__ status,
+                                                                V *__restrict__ sums, V *__restrict__ prefix,
+                                                                uint32_t *__restrict__ ctl, uint32_t epoch) {
+    __shared__ V scratch[kScanThreads / kWave];
+    __shared__ int64_t s_tile;
+    __shared__ V s_prefix;
+    const int64_t n = op.n();
+    int64_t ntiles = (n + kScanTile - 1) / kScanTile;
+    if (ntiles < 1) ntiles = 1;
+    for (;;) {
+        // Every workgroup draws tickets until it draws one past the last tile,
+        // so exactly ntiles + gridDim.x tickets are drawn per launch; the
+        // workgroup that draws the final one resets the counter for the next.
+        if (threadIdx.x == 0) {
+            const uint32_t t = atomicAdd(&ctl[0], 1u);
+            if ((int64_t)t == ntiles + gridDim.x - 1) atomicExch(&ctl[0], 0u);
+            s_tile = t;
+        }
+        __syncthreads();
+        const int64_t tile = s_tile;
+        if (tile >= ntiles) return;   // uniform across the workgroup
+
+        const int64_t first = tile * kScanTile + (int64_t)threadIdx.x * kScanItems;
+        V vals[kScanItems];
+        V s = V(0);
+    #pragma unroll
+        for (int j = 0; j < kScanItems; ++j) {
+            const int64_t i = first + j;
+            vals[j] = i < n ? op.value(i) : V(0);
+            s += vals[j];
+        }
+        V total;
+        const V ex = block_exclusive_sum<V, kScanThreads>(s, scratch, total);
+
+        if (threadIdx.x < kWave) {
+            const int lane = threadIdx.x;
+            const uint32_t tag = epoch << 2;
+            V pre = V(0);
+            if (tile == 0) {
+                if (lane == 0) publish(status, prefix, 0, total, tag | 2u);
+            } else {
+                if (lane == 0) publish(status, sums, tile, total, tag | 1u);
+                int64_t base = tile - 1;
+                uint32_t spins = 0;
+                while (true) {
+                    const int64_t t = base - lane;
+                    // tiles before tile 0 read as a published zero prefix; the
+                    // window that reaches tile 0 always stops there first
+                    const uint32_t st = t >= 0 ? __hip_atomic_load(&status[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                                               : (tag | 2u);
+                    const bool ready = (st & ~3u) == tag && (st & 3u) != 0;
+                    const uint64_t pmask = __ballot(ready && (st & 3u) == 2u);
+                    const int pidx = pmask ? __builtin_ctzll(pmask) : kWave;
+                    const uint64_t need = pidx >= kWave - 1 ? ~0ull : ((1ull << (pidx + 1)) - 1);
+                    if ((__ballot(ready) & need) != need) {
+                        if (++spins > kSpinLimit) {
+                            if (lane == 0) atomicAdd(&ctl[1], 1u);
+                            break;
+                        }
+                        __builtin_amdgcn_s_sleep(1);
+                        continue;
+                    }
+                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+                    V v = V(0);
+                    if (lane <= pidx && t >= 0) v = (st & 3u) == 2u ? prefix[t] : sums[t];
+    #pragma unroll
+                    for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+                    pre += v;
+                    if (pidx < kWave) break;
+                    base -= kWave;
+                    spins = 0;
+                }
+                if (lane == 0) publish(status, prefix, tile, pre + total, tag | 2u);
+            }
+            if (lane == 0) {
+                s_prefix = pre;
+                if (tile == ntiles - 1) op.total(pre + total);
+            }
+        }
+        __syncthreads();
+        V run = ex + s_prefix;
+    #pragma unroll
+        for (int j = 0; j < kScanItems; ++j) {
+            const int64_t i = first + j;
+            if (i < n) op.emit(i, run, vals[j]);
+            run += vals[j];
+        }
+        __syncthreads();   // s_tile / s_prefix are reused by the next ticket
+    }
+}
+
+// Enqueue one scan.  `bound` >= op.n() sizes the grid; `st` must have been
+// ensure()d for `bound` on this stream.
+template <class Op, class V>
+void run_scan(const Op &op, int64_t bound, ScanState &st, const char *name, hipStream_t s) {
+    int64_t grid = scan_parts(bound);
+    if (grid > kScanGrid) grid = kScanGrid;
+    const uint32_t epoch = st.next_epoch();
+    KernelTimer t(name, s);
+    hipLaunchKernelGGL((k_scan_onepass<Op, V>), dim3((unsigned)grid), dim3(kScanThreads), 0, s, op,
+                       st.status.as<uint32_t>(), st.sums.as<V>(), st.prefix.as<V>(), st.ctl.as<uint32_t>(),
+                       epoch);
+    GNNAV_HIP(hipGetLastError());
 }
 
 }  // namespace gnnav

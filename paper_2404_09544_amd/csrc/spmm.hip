@@ -131,7 +131,10 @@ static void launch_spmm_t(const int32_t *indptr, const int32_t *indices, int64_t
     int q = (chunks + g - 1) / g;
     if (q > 4) q = 4;
     const int64_t rows_per_block = (256 / kWave) * (kWave / g);
-    const unsigned grid = grid_for(n_dst, rows_per_block, 65535);
+    // Grid-stride over rows: 8192 workgroups (32 per compute unit) keep the
+    // memory system busy; more only adds empty workgroups when n_dst is an
+    // upper bound read from the device.
+    const unsigned grid = grid_for(n_dst, rows_per_block, 8192);
     const uint4 *xx = (const uint4 *)x;
     uint4 *oo = (uint4 *)out;
     const int64_t xl = ld_x * elt / 16, ol = ld_out * elt / 16;
