@@ -119,8 +119,30 @@ gnnav_status gnnav_build_cache(const gnnav_graph *g, const void *feats_host, int
 gnnav_status gnnav_cache_info(const gnnav_cache *c, int64_t *n_cached, int64_t *d, int64_t *ld,
                               int32_t *dtype, int32_t *store_on_device);
 
-/* Host copy of the slot map (int32[n_nodes]: slot, or -1 if not cached). */
+/* Host copy of the current slot map (int32[n_nodes]: slot, or -1 if not
+ * cached).  Synchronises the device.                                       */
 gnnav_status gnnav_cache_slot_map_host(const gnnav_cache *c, int32_t *slot_map);
+
+/* Host copies of the current cache contents (synchronises the device):
+ * owners (int32[n_cached], vertex held in each slot) and rows
+ * (n_cached x ld elements); either may be NULL.  For tests and tooling.   */
+gnnav_status gnnav_cache_contents_host(const gnnav_cache *c, int32_t *owners, void *rows);
+
+/* Cache update policy (the last step of Section 3.2's transmission
+ * abstraction: after a batch, the cache is updated by its policy; the cost
+ * is Eq. 5's t_replace).  GNNAV_POLICY_STATIC (default) never changes the
+ * cache.  GNNAV_POLICY_FIFO makes the last dynamic_slots cache slots a ring:
+ * after each gather, the batch's misses are admitted in request order, each
+ * taking the slot under the ring pointer (evicting its vertex) and advancing
+ * the pointer; the earlier slots keep their degree-ranked vertices.  Rows
+ * are copied from the gather's own output.  With a dynamic cache, gathers on
+ * different streams run one after another in call order.  The call
+ * synchronises the device and restarts the ring pointer at the ring's
+ * first slot; the cache contents are kept.
+ * Errors: E_INVALID (unknown policy, dynamic_slots outside [0, n_cached]).  */
+#define GNNAV_POLICY_STATIC 0
+#define GNNAV_POLICY_FIFO 1
+gnnav_status gnnav_cache_set_policy(gnnav_cache *c, int32_t policy, int64_t dynamic_slots);
 
 void gnnav_cache_free(gnnav_cache *c);
 

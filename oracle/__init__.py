@@ -57,8 +57,10 @@ def _load():
     lib.oracle_sample_node.restype = i64
     lib.oracle_sample_blocks.argtypes = [i64, P, P, P, i64, P, i32, u64, P, P, P, P, P]
     lib.oracle_sample_blocks.restype = i32
-    lib.oracle_gather.argtypes = [i64, P, i64, P, P, i64, P, P]
+    lib.oracle_gather.argtypes = [i64, P, i64, P, P, i64, P, P, P]
     lib.oracle_gather.restype = None
+    lib.oracle_cache_fifo_admit.argtypes = [P, P, i64, i64, P, P, i64]
+    lib.oracle_cache_fifo_admit.restype = None
     lib.oracle_round_bf16.argtypes = [f64]
     lib.oracle_round_bf16.restype = f64
     lib.oracle_round_bf16_array.argtypes = [P, P, i64]
@@ -194,8 +196,8 @@ def sample_blocks(csr: CSR, seeds, fanouts, rng_seed: int) -> Blocks:
 
 
 # ------------------------------------------------------------------- O7 ---
-def gather(features: np.ndarray, slot_map: np.ndarray, ids):
-    """(rows [n_ids, d] same dtype as features, counts int64[3])."""
+def gather(features: np.ndarray, slot_map: np.ndarray, ids, want_misses: bool = False):
+    """(rows [n_ids, d] same dtype as features, counts int64[3][, missed ids])."""
     feats = np.ascontiguousarray(features)
     n = feats.shape[0]
     ids = _i32(ids)
@@ -203,9 +205,39 @@ def gather(features: np.ndarray, slot_map: np.ndarray, ids):
     out = np.empty((ids.size, feats.shape[1]), feats.dtype)
     counts = np.zeros(3, np.int64)
     sm = _i32(slot_map)
+    misses = np.empty(max(ids.size, 1), np.int32)
     _load().oracle_gather(n, _ptr(feats), row_bytes, _ptr(sm), _ptr(ids), ids.size,
-                          _ptr(out), _ptr(counts))
+                          _ptr(out), _ptr(counts), _ptr(misses))
+    if want_misses:
+        return out, counts, misses[:counts[1]].copy()
     return out, counts
+
+
+class FifoCache:
+    """Oracle state of a cache with a FIFO ring over its last `ring_n` slots.
+
+    Starts from the degree-ranked static cache (rank_cache); after each
+    gather the batch's misses are admitted in request order (see
+    oracle_cache_fifo_admit in oracle.c).
+    """
+
+    def __init__(self, csr: "CSR", r: float, ring_n: int):
+        rank, slot, c = rank_cache(csr, r)
+        self.n, self.c = csr.n, c
+        self.slot_map = slot.copy()
+        self.owner = np.full(max(c, 1), -1, np.int32)[:c].copy()
+        self.owner[:c] = rank[:c]
+        if not 0 <= ring_n <= c:
+            raise ValueError("ring larger than the cache")
+        self.ring_n, self.ring_lo = ring_n, c - ring_n
+        self.ptr = np.zeros(1, np.int64)
+
+    def gather(self, features, ids):
+        rows, counts, misses = gather(features, self.slot_map, ids, want_misses=True)
+        if self.ring_n > 0 and misses.size:
+            _load().oracle_cache_fifo_admit(_ptr(self.slot_map), _ptr(self.owner), self.ring_lo,
+                                            self.ring_n, _ptr(self.ptr), _ptr(misses), misses.size)
+        return rows, counts
 
 
 # ------------------------------------------------------------ bf16, O8 ---

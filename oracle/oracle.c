@@ -243,9 +243,10 @@ int32_t oracle_sample_blocks(int64_t n, const int64_t *row_ptr, const int32_t *c
  * Feature gather through the cache: out row i = features row ids[i] (a
  * bitwise copy of row_bytes bytes).  A request is a hit when the vertex is
  * cached (slot_map >= 0), a miss otherwise; an id outside [0, n) gives a
- * zero row and counts as invalid.  counts = {hits, misses, invalid}.     */
+ * zero row and counts as invalid.  counts = {hits, misses, invalid}.  When
+ * misses is not NULL it receives the missed vertices in request order.   */
 void oracle_gather(int64_t n, const uint8_t *features, int64_t row_bytes, const int32_t *slot_map,
-                   const int32_t *ids, int64_t n_ids, uint8_t *out, int64_t *counts) {
+                   const int32_t *ids, int64_t n_ids, uint8_t *out, int64_t *counts, int32_t *misses) {
     counts[0] = counts[1] = counts[2] = 0;
     for (int64_t i = 0; i < n_ids; ++i) {
         int32_t v = ids[i];
@@ -255,7 +256,31 @@ void oracle_gather(int64_t n, const uint8_t *features, int64_t row_bytes, const 
             continue;
         }
         memcpy(out + i * row_bytes, features + (int64_t)v * row_bytes, (size_t)row_bytes);
-        if (slot_map[v] >= 0) counts[0]++; else counts[1]++;
+        if (slot_map[v] >= 0) {
+            counts[0]++;
+        } else {
+            if (misses) misses[counts[1]] = v;
+            counts[1]++;
+        }
+    }
+}
+
+/* ------------------------------------------------------------- O7 (cont.)
+ * Cache update after a batch (Section 3.2, "Transmission strategies": the
+ * cache is finally updated according to its update policy; its cost is
+ * t_replace of Eq. 5).  Policy FIFO over a ring of slots
+ * [ring_lo, ring_lo + ring_n): the batch's misses are admitted one by one
+ * in request order; each takes the slot under the ring pointer, whose
+ * previous vertex (if any) is evicted, and the pointer advances by one
+ * (wrapping).  owner[slot] is the vertex in a slot or -1.                 */
+void oracle_cache_fifo_admit(int32_t *slot_map, int32_t *owner, int64_t ring_lo, int64_t ring_n, int64_t *ptr,
+                             const int32_t *misses, int64_t m) {
+    for (int64_t i = 0; i < m; ++i) {
+        int64_t s = ring_lo + *ptr;
+        if (owner[s] >= 0) slot_map[owner[s]] = -1;
+        owner[s] = misses[i];
+        slot_map[misses[i]] = (int32_t)s;
+        *ptr = (*ptr + 1) % ring_n;
     }
 }
 

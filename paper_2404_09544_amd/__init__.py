@@ -17,7 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgnnav.so")
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2404_09544_amd.build`")
+    raise ImportError(f"{LIB_PATH} is not built; run `python paper_2404_09544_amd/build.py`")
 
 _lib = C.CDLL(LIB_PATH)
 
@@ -28,7 +28,7 @@ STATUS = {0: "OK", 1: "E_INVALID", 2: "E_RANGE", 3: "E_NOMEM", 4: "E_CAPACITY", 
 EXPORTS = [
     "gnnav_last_error", "gnnav_abi_version", "gnnav_build_csr", "gnnav_graph_info",
     "gnnav_graph_csr_host", "gnnav_graph_free", "gnnav_build_cache", "gnnav_cache_info",
-    "gnnav_cache_slot_map_host", "gnnav_cache_free", "gnnav_blocks_create", "gnnav_blocks_free",
+    "gnnav_cache_slot_map_host", "gnnav_cache_contents_host", "gnnav_cache_set_policy", "gnnav_cache_free", "gnnav_blocks_create", "gnnav_blocks_free",
     "gnnav_sample", "gnnav_sample_async", "gnnav_blocks_sync", "gnnav_blocks_device_sizes",
     "gnnav_blocks_hop", "gnnav_blocks_nodes", "gnnav_gather", "gnnav_gather_n",
     "gnnav_aggregate_mean", "gnnav_combine", "gnnav_sage_forward", "gnnav_profile_start",
@@ -59,6 +59,8 @@ _sig = {
     "gnnav_build_cache": ([P, P, i64, i32, f64, u32, P], i32),
     "gnnav_cache_info": ([P, P, P, P, P, P], i32),
     "gnnav_cache_slot_map_host": ([P, P], i32),
+    "gnnav_cache_contents_host": ([P, P, P], i32),
+    "gnnav_cache_set_policy": ([P, i32, i64], i32),
     "gnnav_cache_free": ([P], None),
     "gnnav_blocks_create": ([P], i32),
     "gnnav_blocks_free": ([P], None),
@@ -171,6 +173,18 @@ class Cache:
         self.n_cached, self.d, self.ld = nc.value, d.value, ld.value
         self.store_on_device = bool(sod.value)
         self.n = graph.n
+
+    def set_policy(self, policy: str, dynamic_slots: int = 0):
+        """'static' or 'fifo' over the last `dynamic_slots` cache slots."""
+        code = {"static": 0, "fifo": 1}[policy]
+        _check(_lib.gnnav_cache_set_policy(self._h, code, int(dynamic_slots)))
+
+    def contents(self):
+        """(owners int32[n_cached], rows [n_cached, ld]) currently in the cache."""
+        owners = np.empty(max(self.n_cached, 1), np.int32)
+        rows = np.empty((max(self.n_cached, 1), self.ld), np.uint16 if self.dtype == "bf16" else np.float32)
+        _check(_lib.gnnav_cache_contents_host(self._h, _np_ptr(owners), _np_ptr(rows)))
+        return owners[:self.n_cached], rows[:self.n_cached]
 
     def slot_map(self) -> np.ndarray:
         out = np.empty(max(self.n, 1), np.int32)

@@ -2,7 +2,8 @@
 
 Every source is compiled for gfx950 only, with packed-fp32 instruction
 selection disabled, then linked into one shared library exporting the
-C ABI of include/gnnav.h.  Usage: python -m paper_2404_09544_amd.build
+C ABI of include/gnnav.h.  Usage: python paper_2404_09544_amd/build.py
+(run as a file: importing the package needs the library already built).
 """
 from __future__ import annotations
 

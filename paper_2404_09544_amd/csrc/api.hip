@@ -297,8 +297,16 @@ struct gnnav_cache {
     void *store_host = nullptr;       // pinned, device-mapped
     void *store_ptr = nullptr;        // device-visible address of the store
     std::vector<int32_t> slot_host;
+    std::vector<int32_t> rank_host;   // degree rank (first C fill the cache)
     std::mutex ws_mu;
     std::vector<GatherWs *> ws;
+    // update policy (GNNAV_POLICY_*); FIFO ring over slots [ring_lo, c)
+    int32_t policy = 0;
+    int64_t ring_lo = 0, ring_n = 0;
+    DevBuf owner, ring_ptr;
+    std::mutex upd_mu;
+    hipEvent_t upd_done = nullptr;
+    bool upd_recorded = false;
 };
 
 static GatherWs *gather_ws(gnnav_cache *c, hipStream_t s) {
@@ -334,6 +342,9 @@ static void free_cache(gnnav_cache *c) {
         if (w->join) (void)hipEventDestroy(w->join);
         delete w;
     }
+    c->owner.release();
+    c->ring_ptr.release();
+    if (c->upd_done) (void)hipEventDestroy(c->upd_done);
     if (c->store_host) (void)hipHostFree(c->store_host);
     delete c;
 }
@@ -397,6 +408,7 @@ extern "C" gnnav_status gnnav_build_cache(const gnnav_graph *g, const void *feat
             c->c = C;
             c->slot_host.assign(n, -1);
             for (int64_t s = 0; s < C; ++s) c->slot_host[rank[s]] = (int32_t)s;
+            c->rank_host.assign(rank.begin(), rank.begin() + C);
             hipStream_t s0 = nullptr;
             c->slot_map.ensure(std::max<int64_t>(n, 1) * sizeof(int32_t), s0);
             if (n > 0)
@@ -447,7 +459,53 @@ extern "C" gnnav_status gnnav_cache_info(const gnnav_cache *c, int64_t *n_cached
 extern "C" gnnav_status gnnav_cache_slot_map_host(const gnnav_cache *c, int32_t *slot_map) {
     return guarded([&] {
         GNNAV_CHECK(c && slot_map, GNNAV_E_INVALID, "NULL argument");
-        std::memcpy(slot_map, c->slot_host.data(), c->n * sizeof(int32_t));
+        GNNAV_HIP(hipDeviceSynchronize());
+        if (c->n > 0)
+            GNNAV_HIP(hipMemcpy(slot_map, c->slot_map.p, c->n * sizeof(int32_t), hipMemcpyDeviceToHost));
+    });
+}
+
+extern "C" gnnav_status gnnav_cache_contents_host(const gnnav_cache *c, int32_t *owners, void *rows) {
+    return guarded([&] {
+        GNNAV_CHECK(c, GNNAV_E_INVALID, "cache is NULL");
+        GNNAV_HIP(hipDeviceSynchronize());
+        if (owners) {
+            if (c->owner.p) {
+                if (c->c > 0)
+                    GNNAV_HIP(hipMemcpy(owners, c->owner.p, c->c * sizeof(int32_t), hipMemcpyDeviceToHost));
+            } else {
+                std::memcpy(owners, c->rank_host.data(), c->c * sizeof(int32_t));
+            }
+        }
+        if (rows && c->c > 0)
+            GNNAV_HIP(hipMemcpy(rows, c->cache_rows.p, (size_t)(c->c * c->ld * c->elt), hipMemcpyDeviceToHost));
+    });
+}
+
+extern "C" gnnav_status gnnav_cache_set_policy(gnnav_cache *c, int32_t policy, int64_t dynamic_slots) {
+    return guarded([&] {
+        GNNAV_CHECK(c, GNNAV_E_INVALID, "cache is NULL");
+        GNNAV_CHECK(policy == GNNAV_POLICY_STATIC || policy == GNNAV_POLICY_FIFO, GNNAV_E_INVALID, "unknown policy");
+        GNNAV_CHECK(policy == GNNAV_POLICY_STATIC || (dynamic_slots >= 0 && dynamic_slots <= c->c), GNNAV_E_INVALID,
+                    "dynamic_slots outside [0, cached rows]");
+        GNNAV_HIP(hipDeviceSynchronize());
+        std::lock_guard<std::mutex> lk(c->upd_mu);
+        c->policy = policy;
+        c->ring_n = policy == GNNAV_POLICY_FIFO ? dynamic_slots : 0;
+        c->ring_lo = c->c - c->ring_n;
+        if (c->ring_n > 0) {
+            hipStream_t s0 = nullptr;
+            if (!c->owner.p) {
+                // first dynamic use: owner table from the degree ranking
+                c->owner.ensure(std::max<int64_t>(c->c, 1) * sizeof(int32_t), s0);
+                GNNAV_HIP(hipMemcpy(c->owner.p, c->rank_host.data(), c->c * sizeof(int32_t), hipMemcpyHostToDevice));
+            }
+            c->ring_ptr.ensure(sizeof(int32_t), s0);
+            GNNAV_HIP(hipMemset(c->ring_ptr.p, 0, sizeof(int32_t)));
+            GNNAV_HIP(hipDeviceSynchronize());
+            if (!c->upd_done) GNNAV_HIP(hipEventCreateWithFlags(&c->upd_done, hipEventDisableTiming));
+            c->upd_recorded = false;
+        }
     });
 }
 
@@ -667,6 +725,14 @@ static void gather_impl(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_
     GNNAV_CHECK((ld_out * c->elt) % 16 == 0 && aligned16(out_dev), GNNAV_E_INVALID,
                 "out rows must be 16-byte aligned");
     auto *cc = const_cast<gnnav_cache *>(c);
+    // A cache that updates itself is shared mutable state: gathers on any
+    // stream are ordered one after another, in call order, through an event.
+    const bool dynamic = cc->ring_n > 0;
+    std::unique_lock<std::mutex> upd_lock(cc->upd_mu, std::defer_lock);
+    if (dynamic) {
+        upd_lock.lock();
+        if (cc->upd_recorded) GNNAV_HIP(hipStreamWaitEvent(s, cc->upd_done, 0));
+    }
     GatherWs *w = gather_ws(cc, s);
     w->hit_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
     w->miss_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
@@ -675,13 +741,20 @@ static void gather_impl(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_
                  c->ld * c->elt, out_dev, ld_out * c->elt, c->d * c->elt, counts_dev, w->dev_counts.as<int32_t>(),
                  w->hit_list.as<int2>(), w->miss_list.as<int2>(), &w->scan};
     launch_classify(a, s);
-    if (n_ids == 0) return;
-    GNNAV_HIP(hipEventRecord(w->fork, s));
-    GNNAV_HIP(hipStreamWaitEvent(w->side, w->fork, 0));
-    launch_gather_rows(a, /*hits=*/false, w->side);
-    launch_gather_rows(a, /*hits=*/true, s);
-    GNNAV_HIP(hipEventRecord(w->join, w->side));
-    GNNAV_HIP(hipStreamWaitEvent(s, w->join, 0));
+    if (n_ids > 0) {
+        GNNAV_HIP(hipEventRecord(w->fork, s));
+        GNNAV_HIP(hipStreamWaitEvent(w->side, w->fork, 0));
+        launch_gather_rows(a, /*hits=*/false, w->side);
+        launch_gather_rows(a, /*hits=*/true, s);
+        GNNAV_HIP(hipEventRecord(w->join, w->side));
+        GNNAV_HIP(hipStreamWaitEvent(s, w->join, 0));
+    }
+    if (dynamic) {
+        launch_fifo_update(a, cc->ring_lo, cc->ring_n, cc->owner.as<int32_t>(), cc->slot_map.as<int32_t>(),
+                           cc->ring_ptr.as<int32_t>(), cc->cache_rows.p, s);
+        GNNAV_HIP(hipEventRecord(cc->upd_done, s));
+        cc->upd_recorded = true;
+    }
 }
 
 extern "C" gnnav_status gnnav_gather(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_ids, void *out_dev,

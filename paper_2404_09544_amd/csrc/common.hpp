@@ -190,6 +190,8 @@ struct GatherArgs {
 };
 void launch_classify(const GatherArgs &a, hipStream_t s);
 void launch_gather_rows(const GatherArgs &a, bool hits, hipStream_t s);
+void launch_fifo_update(const GatherArgs &a, int64_t lo, int64_t rn, int32_t *owner, int32_t *slot_map,
+                        int32_t *ring_ptr, void *cache, hipStream_t s);
 
 // spmm.hip
 void launch_aggregate_mean(const int32_t *indptr, const int32_t *indices, int64_t n_dst,

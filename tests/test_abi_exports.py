@@ -25,7 +25,7 @@ def test_header_declares_the_boundary():
 
 
 def test_library_exports_every_declared_symbol():
-    assert os.path.exists(LIB), "build first: python -m paper_2404_09544_amd.build"
+    assert os.path.exists(LIB), "build first: python paper_2404_09544_amd/build.py"
     lib = ctypes.CDLL(LIB)
     missing = [n for n in declared_functions() if not hasattr(lib, n)]
     assert not missing, missing

@@ -463,3 +463,67 @@ def test_forward_rows_matches_full_forward(bf16):
     rows = np.array([7, 0, 79, 33, 7], np.int64)
     part = O.sage_forward_rows(b, H0, Ws, rows, bf16=bf16)
     np.testing.assert_array_equal(part, full[rows])
+
+
+# ------------------------------------------------- FIFO cache update, O7 --
+
+def _deque_fifo(rank, c, ring_n, batches, n):
+    """Independent FIFO model: a deque of (slot, vertex) plus a set lookup."""
+    from collections import deque
+    static = set(int(x) for x in rank[:c - ring_n])
+    ring = deque(int(x) for x in rank[c - ring_n:c])     # oldest first
+    hist = []
+    for ids in batches:
+        cached = static | set(ring)
+        misses = [int(v) for v in ids if 0 <= v < n and int(v) not in cached]
+        hits = sum(1 for v in ids if 0 <= v < n and int(v) in cached)
+        hist.append((hits, len(misses)))
+        for v in misses:
+            if ring_n:
+                ring.popleft()
+                ring.append(v)
+    return hist, static | set(ring)
+
+
+@pytest.mark.parametrize("r,frac", [(0.1, 1.0), (0.2, 0.5), (0.05, 0.25), (0.3, 0.0)])
+def test_fifo_cache_matches_deque_model(r, frac):
+    n, u, v = W.random_graph(n=600, m=5000, seed=31)
+    csr = O.build_csr(n, u, v)
+    rank, _, c = O.rank_cache(csr, r)
+    ring_n = int(c * frac)
+    rng = np.random.default_rng(7)
+    batches = [np.unique(rng.integers(0, n, 120)).astype(np.int32)[rng.permutation(0)] if False else
+               rng.permutation(np.unique(rng.integers(0, n, 120))).astype(np.int32) for _ in range(8)]
+    feats = W.features(n, 3, "f32", seed=1)
+    cache = O.FifoCache(csr, r, ring_n)
+    got = []
+    for ids in batches:
+        rows, counts = cache.gather(feats, ids)
+        got.append((int(counts[0]), int(counts[1])))
+        assert rows.tobytes() == feats[ids].tobytes()
+    hist, final = _deque_fifo(rank, c, ring_n, batches, n)
+    assert got == hist
+    cached = {int(x) for x in np.nonzero(cache.slot_map >= 0)[0]}
+    assert cached == final
+    # owner <-> slot_map bijection
+    for s, x in enumerate(cache.owner):
+        assert x >= 0 and cache.slot_map[x] == s
+    assert (cache.slot_map >= 0).sum() == c
+
+
+def test_fifo_cache_repeat_batch_hits():
+    """A batch of m <= ring uncached vertices is fully cached after one pass:
+    repeating it right away hits every request."""
+    n, u, v = W.random_graph(n=400, m=3000, seed=32)
+    csr = O.build_csr(n, u, v)
+    feats = W.features(n, 2, "f32", seed=2)
+    cache = O.FifoCache(csr, 0.5, ring_n=120)
+    cold = np.nonzero(cache.slot_map < 0)[0]
+    ids = np.random.default_rng(3).permutation(cold)[:100].astype(np.int32)
+    _, c1 = cache.gather(feats, ids)
+    _, c2 = cache.gather(feats, ids)
+    assert c1.tolist() == [0, 100, 0]
+    assert c2.tolist() == [100, 0, 0]
+    # the 20 oldest ring entries survived; the first 100 were replaced in order
+    ring = cache.owner[cache.c - 120:]
+    assert ring[:100].tolist() == ids.tolist()
