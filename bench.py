@@ -63,6 +63,44 @@ def traffic_for(kernel: str, workload: str):
     return rec.get("bytes_per_launch")
 
 
+def link_calibration(G, cache, wl, torch):
+    """Achievable host-link rates on this machine: a DMA copy from pinned memory,
+    and the library's zero-copy miss path over uncached rows in id order."""
+    out = {}
+    nbytes = 256 << 20
+    src = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    dst = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst.copy_(src, non_blocking=True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(5):
+        dst.copy_(src, non_blocking=True)
+    e1.record()
+    torch.cuda.synchronize()
+    out["dma_h2d_gbs"] = round(5 * nbytes / (e0.elapsed_time(e1) * 1e-3) / 1e9, 2)
+    del src, dst
+    slot = cache.slot_map()
+    ids = np.nonzero(slot < 0)[0].astype(np.int32)[:100_000]
+    if ids.size and not cache.store_on_device:
+        ids_d = torch.from_numpy(ids).cuda()
+        rows = torch.empty((ids.size, cache.ld), dtype=torch.int16 if wl.dtype == "bf16" else torch.float32,
+                           device="cuda")
+        counts = torch.zeros(3, dtype=torch.int64, device="cuda")
+        G.gather(cache, ids_d.data_ptr(), ids.size, rows, counts)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(3):
+            G.gather(cache, ids_d.data_ptr(), ids.size, rows, counts)
+        e1.record()
+        torch.cuda.synchronize()
+        elt = 2 if wl.dtype == "bf16" else 4
+        out["zero_copy_gather_gbs"] = round(3 * ids.size * wl.d * elt / (e0.elapsed_time(e1) * 1e-3) / 1e9, 2)
+    else:
+        out["zero_copy_gather_gbs"] = None
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -73,6 +111,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-batches", type=int, default=2)
     ap.add_argument("--depth", type=int, default=2, help="streams in the pipelined pass")
+    ap.add_argument("--cache-policy", choices=["static", "fifo"], default="static",
+                    help="fifo: admit each batch's misses into a ring over the last cache slots")
+    ap.add_argument("--dynamic-fraction", type=float, default=1.0,
+                    help="share of the cache slots in the FIFO ring (with --cache-policy fifo)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (scales rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
@@ -108,6 +150,13 @@ def main():
     c = G.Cache(g, feats, wl.dtype, r, store_on_device=wl.cfg["store_on_device"])
     log(f"graph nnz={g.nnz} max_deg={g.max_degree}; cache C={c.n_cached} ld={c.ld} "
         f"({time.perf_counter() - t0:.1f}s)")
+    link = link_calibration(G, c, wl, torch)
+    log(f"host link: DMA {link['dma_h2d_gbs']} GB/s, zero-copy gather of uncached rows {link['zero_copy_gather_gbs']} GB/s")
+    ring = 0
+    if args.cache_policy == "fifo":
+        ring = int(round(c.n_cached * min(max(args.dynamic_fraction, 0.0), 1.0)))
+        c.set_policy("fifo", ring)
+        log(f"FIFO ring over the last {ring} of {c.n_cached} cache slots")
     ws = wl.weights()
     wdev = to_device_weights(ws, wl.dtype)
     step = MiniBatchStep(g, c, wdev, wl.dims, wl.fanouts, wl.dtype)
@@ -115,13 +164,14 @@ def main():
     seeds_dev = [torch.from_numpy(wl.seeds(b)).cuda() for b in range(n_b)]
     L = wl.L
     counts_hist = torch.zeros((n_b, 3), dtype=torch.int64, device="cuda")
+    seq_counts_hist = torch.zeros((n_b, 3), dtype=torch.int64, device="cuda")
     sizes_dev_hist = torch.zeros((n_b, L + 1), dtype=torch.int32, device="cuda")
 
-    def record(slot, b, st):
+    def record(slot, b, st, hist=counts_hist):
         """Copy this batch's counts and frontier sizes aside on its own stream."""
         ptr, _ = slot.blocks.device_sizes(L)
         with torch.cuda.stream(st):
-            counts_hist[b].copy_(slot.counts)
+            hist[b].copy_(slot.counts)
             G._copy_device_i32(sizes_dev_hist[b], ptr, L + 1)
 
     # ---- phase 1: sequential steps on one stream, every kernel timed -----
@@ -131,14 +181,14 @@ def main():
     stream = torch.cuda.current_stream()
     for b in range(args.warmup):
         step.enqueue(seeds_dev[b], wl.rng_seed(b), stream)
-        record(step, b, stream)
+        record(step, b, stream, seq_counts_hist)
     torch.cuda.synchronize()
     G.profile_start()
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for b in range(args.warmup, n_b):
         step.enqueue(seeds_dev[b], wl.rng_seed(b), stream)
-        record(step, b, stream)
+        record(step, b, stream, seq_counts_hist)
     torch.cuda.synchronize()
     t_end = time.perf_counter()
     prof = G.profile_stop()
@@ -163,6 +213,7 @@ def main():
     ms_per_step = elapsed * 1e3 / args.steps
     seeds_per_s = wl.batch * args.steps / elapsed
     counts = counts_hist[args.warmup:].cpu().numpy()
+    seq_counts = seq_counts_hist[args.warmup:].cpu().numpy()
     sizes_hist = sizes_dev_hist[args.warmup:].cpu().numpy().tolist()
     log(f"pipelined {args.steps} steps: {ms_per_step:.3f} ms/step, {seeds_per_s:,.0f} seeds/s")
 
@@ -170,14 +221,17 @@ def main():
     # Re-sampling a batch is deterministic, so the blocks of each timed batch
     # are regenerated here (untimed) to count distinct source rows.
     elt = 2 if wl.dtype == "bf16" else 4
-    work = {"gather_hit": 0.0, "gather_miss": 0.0}
+    # (the per-kernel figures come from the sequential region, so its counts)
+    work = {"gather_hit": 0.0, "gather_miss": 0.0, "cache_admit": 0.0}
     edge = {}
     probe = G.Blocks()
     for i, b in enumerate(range(args.warmup, n_b)):
         sz = sizes_hist[i]
-        hits, misses = int(counts[i][0]), int(counts[i][1])
+        hits, misses = int(seq_counts[i][0]), int(seq_counts[i][1])
         work["gather_hit"] += hits * (2 * wl.d * elt + 8)
         work["gather_miss"] += misses * wl.d * elt
+        # admitted rows: read from the gathered batch, written to the cache, plus owner/slot-map entries
+        work["cache_admit"] += min(misses, ring) * (2 * wl.d * elt + 16)
         G.sample(g, seeds_dev[b], wl.fanouts, wl.rng_seed(b), probe)
         _, _, ip, _, ix = probe.to_host()
         for l in range(1, L + 1):
@@ -213,6 +267,8 @@ def main():
                "frac": round(achieved / peak, 4), "per_launch": round(amount / max(launches, 1), 1)}
         if name in edge:
             ent["achieved_edge_effective"] = round(edge[name] / (ms * 1e-3) / 1e9, 2)
+        if name == "gather_miss" and link.get("zero_copy_gather_gbs"):
+            ent["frac_of_measured_link"] = round(achieved / link["zero_copy_gather_gbs"], 4)
         kernels[name].update(ent)
         rows.append((ms, name))
     device_rows = [(ms, n) for ms, n in rows if kernels[n]["bound"] in ("hbm", "mfma")]
@@ -230,13 +286,14 @@ def main():
         t0 = time.perf_counter()
         csr = O.build_csr(wl.n, src, dst)
         _, slot, _ = O.rank_cache(csr, r)
+        fifo = O.FifoCache(csr, r, ring) if ring else None
         wd = [O.to_f64(w, wl.dtype) for w in ws]
         log(f"oracle set-up {time.perf_counter() - t0:.1f}s")
         nb = max(1, args.cpu_batches)
         t0 = time.perf_counter()
         for b in range(args.warmup, args.warmup + nb):
             ob = O.sample_blocks(csr, wl.seeds(b), wl.fanouts, wl.rng_seed(b))
-            h0, _ = O.gather(feats, slot, ob.nodes)
+            h0, _ = fifo.gather(feats, ob.nodes) if fifo else O.gather(feats, slot, ob.nodes)
             O.sage_forward(ob, O.to_f64(h0, wl.dtype), wd, bf16=wl.dtype == "bf16")
         ct = time.perf_counter() - t0
         cpu = {"value": round(wl.batch * nb / ct, 2), "unit": "seeds/s", "cores": 1, "kind": "oracle",
@@ -249,11 +306,15 @@ def main():
     def per_batch(names):
         return sum(prof[n][1] for n in names if n in prof) / args.steps
     samp = ["dedup_first", "dedup_scan", "count_scan", "sample_hop", "relabel", "reset_map"]
-    comp = [n for n in prof if n.startswith(("aggregate_mean", "combine_gemm"))] + ["classify", "gather_hit"]
+    comp = [n for n in prof if n.startswith(("aggregate_mean", "combine_gemm"))] + ["classify", "gather_hit",
+                                                                                     "weights_transpose"]
+    repl = ["cache_evict", "cache_admit", "cache_advance"]
     eq4 = {"t_sample_ms": round(per_batch(samp), 4), "t_transfer_ms": round(per_batch(["gather_miss"]), 4),
+           "t_replace_ms": round(per_batch(repl), 4),
            "t_compute_ms": round(per_batch(comp), 4), "sequential_ms_per_step": round(seq_ms, 4),
            "pipelined_ms_per_step": round(ms_per_step, 4)}
-    eq4["eq4_max_ms"] = round(max(eq4["t_sample_ms"] + eq4["t_transfer_ms"], eq4["t_compute_ms"]), 4)
+    eq4["eq4_max_ms"] = round(max(eq4["t_sample_ms"] + eq4["t_transfer_ms"],
+                                  eq4["t_replace_ms"] + eq4["t_compute_ms"]), 4)
     mean_sizes = np.mean(np.array(sizes_hist), axis=0).round(1).tolist()
     hit_rate = float(counts[:, 0].sum() / max(counts[:, :2].sum(), 1))
     out = {
@@ -263,13 +324,16 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "pipeline_streams": args.depth, "n": wl.n, "nnz": g.nnz, "d": wl.d, "fanouts": wl.fanouts,
                    "batch": wl.batch, "layers": wl.L, "dims": wl.dims, "cache_fraction": r,
-                   "store_on_device": wl.cfg["store_on_device"], "global_batch": wl.batch},
+                   "store_on_device": wl.cfg["store_on_device"], "cache_policy": args.cache_policy,
+                   "fifo_slots": ring, "global_batch": wl.batch},
         "value_sequential": round(wl.batch * args.steps / seq_elapsed, 2),
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kernels,
         "eq4": eq4,
+        "host_link_calibration": link,
         "batch_stats": {"mean_frontier_sizes": mean_sizes, "hit_rate": round(hit_rate, 4),
+                        "hit_rate_sequential": round(float(seq_counts[:, 0].sum() / max(seq_counts[:, :2].sum(), 1)), 4),
                         "miss_bytes_per_batch": round(float(counts[:, 1].mean()) * wl.d * elt, 1)},
     }
     print(json.dumps(out), flush=True)

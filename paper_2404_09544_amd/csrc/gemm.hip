@@ -72,8 +72,129 @@ __device__ __forceinline__ void tile_of(int64_t ncol, int64_t &tile_r, int64_t &
 }
 
 // ------------------------------------------------------------ fp32 main
-template <int BM, int BN, int WM, int WN, int BK, class OutT>
+// Both operands are staged as 16-byte chunks along k: A rows as stored, and
+// B from WT, the weights transposed to [N][2K] once per call.  A lane's
+// chunk holds four consecutive k, and MFMA q of a sub-step takes element q
+// of every lane's chunk, so one 16-byte LDS read per operand feeds four
+// MFMAs.  LDS slots are XOR-swizzled within each row so that both the
+// chunk stores and the fragment reads are free of bank conflicts.
+template <int CH>
+__device__ __forceinline__ int swz(int r, int kc) {
+    return r * CH + (kc ^ (CH == 4 ? ((r >> 1) & 3) : (r & 7)));
+}
+
+template <int BM, int BN, int WM, int WN, int BK>
 __global__ void __launch_bounds__(256) k_combine_f32(const float *__restrict__ A0, int64_t lda0,
+                                                     const float *__restrict__ A1, int64_t lda1, int64_t M,
+                                                     const int32_t *__restrict__ m_dev, int64_t K,
+                                                     const float *__restrict__ WT, int64_t N, int relu,
+                                                     float *__restrict__ C, int64_t ldc) {
+    constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
+    constexpr int CH = BK / 4;                    // chunks per row and step
+    constexpr int A_CH = BM * CH, B_CH = BN * CH;
+    constexpr int A_LD = (A_CH + 255) / 256, B_LD = (B_CH + 255) / 256;
+    static_assert(WM * WN == 4 && TM >= 1 && TN >= 1 && (BK == 16 || BK == 32), "tile shape");
+    __shared__ f32x4 As[2][A_CH];
+    __shared__ f32x4 Bs[2][B_CH];
+
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int wm = wid / WN, wn = wid % WN, g = lane >> 4, l16 = lane & 15;
+    if (m_dev) M = *m_dev;
+    int64_t tile_r, tile_c;
+    tile_of((N + BN - 1) / BN, tile_r, tile_c);
+    const int64_t m0 = tile_r * BM, n0 = tile_c * BN;
+    if (m0 >= M) return;
+
+    f32x4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int64_t kt = (K + BK - 1) / BK;
+    const int64_t tiles = 2 * kt, K2 = 2 * K;
+    f32x4 ra[A_LD], rb[B_LD];
+
+    auto chunk = [&](const float *p, int64_t k) {
+        f32x4 v = {0.f, 0.f, 0.f, 0.f};
+        if (k + 3 < K) {
+            v = *(const f32x4 *)p;
+        } else {
+            if (k < K) v.x = p[0];
+            if (k + 1 < K) v.y = p[1];
+            if (k + 2 < K) v.z = p[2];
+        }
+        return v;
+    };
+    auto load = [&](int64_t t) {
+        const bool seg = t >= kt;
+        const int64_t k0 = (seg ? t - kt : t) * BK;
+        const float *A = seg ? A1 : A0;
+        const int64_t lda = seg ? lda1 : lda0;
+#pragma unroll
+        for (int s = 0; s < A_LD; ++s) {
+            const int c = tid + 256 * s;
+            const int64_t row = m0 + c / CH, k = k0 + (c % CH) * 4;
+            ra[s] = (c < A_CH && row < M) ? chunk(A + row * lda + k, k) : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int s = 0; s < B_LD; ++s) {
+            const int c = tid + 256 * s;
+            const int64_t n = n0 + c / CH, k = k0 + (c % CH) * 4;
+            rb[s] = (c < B_CH && n < N) ? chunk(WT + n * K2 + (seg ? K : 0) + k, k) : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+    };
+    auto stash = [&](int buf) {
+#pragma unroll
+        for (int s = 0; s < A_LD; ++s) {
+            const int c = tid + 256 * s;
+            if (c < A_CH) As[buf][swz<CH>(c / CH, c % CH)] = ra[s];
+        }
+#pragma unroll
+        for (int s = 0; s < B_LD; ++s) {
+            const int c = tid + 256 * s;
+            if (c < B_CH) Bs[buf][swz<CH>(c / CH, c % CH)] = rb[s];
+        }
+    };
+    // kvalid: k values of this step inside [0, K); sub-steps past them are skipped
+    auto compute = [&](int buf, int64_t kvalid) {
+#pragma unroll
+        for (int sub = 0; sub < CH / 4; ++sub) {
+            if (sub * 16 >= kvalid) break;        // uniform across the workgroup
+            f32x4 a[TM], b[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) a[i] = As[buf][swz<CH>(wm * WTM + i * 16 + l16, sub * 4 + g)];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) b[j] = Bs[buf][swz<CH>(wn * WTN + j * 16 + l16, sub * 4 + g)];
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
+        }
+    };
+
+    load(0);
+    stash(0);
+    __syncthreads();
+    for (int64_t t = 0; t < tiles; ++t) {
+        const int buf = (int)(t & 1);
+        if (t + 1 < tiles) load(t + 1);
+        compute(buf, K - (t >= kt ? t - kt : t) * BK);
+        if (t + 1 < tiles) stash(buf ^ 1);
+        __syncthreads();
+    }
+    write_tile<TM, TN, float>(acc, m0 + wm * WTM, n0 + wn * WTN, M, N, relu, C, ldc, g, l16);
+}
+
+// ---------------------------------------------- fp32 main, W as stored
+// Reads W row-major and stages A transposed (k-major) in LDS, one float per
+// lane and k step.  Measured faster than the chunked kernel above when there
+// are many row tiles over a short K (e.g. d_in = 100 over 10^5 rows).
+template <int BM, int BN, int WM, int WN, int BK, class OutT>
+__global__ void __launch_bounds__(256) k_combine_f32_wrow(const float *__restrict__ A0, int64_t lda0,
                                                      const float *__restrict__ A1, int64_t lda1, int64_t M,
                                                      const int32_t *__restrict__ m_dev, int64_t K,
                                                      const float *__restrict__ W, int64_t N, int relu, int wvec,
@@ -196,6 +317,7 @@ __global__ void __launch_bounds__(256) k_combine_f32(const float *__restrict__ A
     }
     write_tile<TM, TN, OutT>(acc, m0 + wm * WTM, n0 + wn * WTN, M, N, relu, C, ldc, g, l16);
 }
+
 
 // ------------------------------------------------------------ bf16 main
 // B comes from WT, the weights transposed to [N][2K] once per call, so both
@@ -435,12 +557,13 @@ __global__ void __launch_bounds__(256) k_combine_skinny(const InT *__restrict__ 
 }
 
 // --------------------------------------------------------------- launch
-// bf16 weights are transposed to [N][2K] before the main kernel runs.  The
-// copy lives in one process-wide device buffer; an event recorded after the
-// last kernel that reads it orders every later call after it, whichever
-// stream that call uses.
-__global__ void __launch_bounds__(256) k_transpose_u16(const uint16_t *__restrict__ src, int64_t rows,
-                                                       int64_t cols, uint16_t *__restrict__ dst) {
+// The main kernels read the weights transposed to [N][2K]; the copy is made
+// before the kernel runs and lives in one process-wide device buffer.  An
+// event recorded after the last kernel that reads it orders every later
+// call after it, whichever stream that call uses.
+template <class T>
+__global__ void __launch_bounds__(256) k_transpose(const T *__restrict__ src, int64_t rows, int64_t cols,
+                                                   T *__restrict__ dst) {
     const int64_t total = rows * cols;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
@@ -458,69 +581,95 @@ struct SharedWorkspace {
 SharedWorkspace g_wt;
 }  // namespace
 
-template <int BM, int BN, int WM, int WN, int BKF, int BKH>
+// WROW selects k_combine_f32_wrow for fp32 (no transposed copy of W).
+template <int BM, int BN, int WM, int WN, int BKF, int BKH, bool WROW = false>
 static void launch_main(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
                         const int32_t *m_dev, int64_t k, const void *w, int64_t n, bool bf16, bool relu,
-                        bool out_bf16, void *out, int64_t ld_out, hipStream_t s) {
+                        bool out_bf16, void *out, int64_t ld_out, hipStream_t s, const char *label) {
     const int64_t nrow = (m + BM - 1) / BM, ncol = (n + BN - 1) / BN;
     const dim3 grid((unsigned)(((nrow + 7) / 8) * 8 * ncol));
-    if (!bf16) {
+    if (!bf16 && WROW) {
         const int wvec = (((uintptr_t)w & 15u) == 0) && n % 4 == 0;
-        hipLaunchKernelGGL((k_combine_f32<BM, BN, WM, WN, BKF, float>), grid, dim3(256), 0, s, (const float *)self,
-                           ld_self, (const float *)agg, ld_agg, m, m_dev, k, (const float *)w, n, (int)relu,
-                           wvec, (float *)out, ld_out);
+        KernelTimer tk(label, s);
+        hipLaunchKernelGGL((k_combine_f32_wrow<BM, BN, WM, WN, BKF, float>), grid, dim3(256), 0, s,
+                           (const float *)self, ld_self, (const float *)agg, ld_agg, m, m_dev, k, (const float *)w, n,
+                           (int)relu, wvec, (float *)out, ld_out);
         return;
     }
     std::lock_guard<std::mutex> lk(g_wt.mu);
     if (!g_wt.last_use) GNNAV_HIP(hipEventCreateWithFlags(&g_wt.last_use, hipEventDisableTiming));
     GNNAV_HIP(hipStreamWaitEvent(s, g_wt.last_use, 0));
-    g_wt.buf.ensure((size_t)(2 * k * n) * sizeof(uint16_t), s);
-    uint16_t *wt = g_wt.buf.as<uint16_t>();
-    hipLaunchKernelGGL(k_transpose_u16, dim3(grid_for(2 * k * n, 256, 1024)), dim3(256), 0, s, (const uint16_t *)w,
-                       2 * k, n, wt);
-    if (out_bf16)
-        hipLaunchKernelGGL((k_combine_bf16<BM, BN, WM, WN, BKH, uint16_t>), grid, dim3(256), 0, s,
-                           (const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, k,
-                           (const uint16_t *)wt, n, (int)relu, (uint16_t *)out, ld_out);
-    else
-        hipLaunchKernelGGL((k_combine_bf16<BM, BN, WM, WN, BKH, float>), grid, dim3(256), 0, s,
-                           (const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, k,
-                           (const uint16_t *)wt, n, (int)relu, (float *)out, ld_out);
+    g_wt.buf.ensure((size_t)(2 * k * n) * (bf16 ? sizeof(uint16_t) : sizeof(float)), s);
+    const dim3 tgrid(grid_for(2 * k * n, 256, 1024));
+    if (!bf16) {
+        float *wt = g_wt.buf.as<float>();
+        {
+            KernelTimer tt("weights_transpose", s);
+            hipLaunchKernelGGL(k_transpose<float>, tgrid, dim3(256), 0, s, (const float *)w, 2 * k, n, wt);
+        }
+        KernelTimer tk(label, s);
+        hipLaunchKernelGGL((k_combine_f32<BM, BN, WM, WN, BKF>), grid, dim3(256), 0, s, (const float *)self, ld_self,
+                           (const float *)agg, ld_agg, m, m_dev, k, (const float *)wt, n, (int)relu, (float *)out,
+                           ld_out);
+    } else {
+        uint16_t *wt = g_wt.buf.as<uint16_t>();
+        {
+            KernelTimer tt("weights_transpose", s);
+            hipLaunchKernelGGL(k_transpose<uint16_t>, tgrid, dim3(256), 0, s, (const uint16_t *)w, 2 * k, n, wt);
+        }
+        KernelTimer tk(label, s);
+        if (out_bf16)
+            hipLaunchKernelGGL((k_combine_bf16<BM, BN, WM, WN, BKH, uint16_t>), grid, dim3(256), 0, s,
+                               (const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, k,
+                               (const uint16_t *)wt, n, (int)relu, (uint16_t *)out, ld_out);
+        else
+            hipLaunchKernelGGL((k_combine_bf16<BM, BN, WM, WN, BKH, float>), grid, dim3(256), 0, s,
+                               (const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, k,
+                               (const uint16_t *)wt, n, (int)relu, (float *)out, ld_out);
+    }
     GNNAV_HIP(hipEventRecord(g_wt.last_use, s));
 }
 
-// Output tiles below which the main kernel cannot fill 256 compute units.
+// Output tiles (counted as 64 x 64) below which the main kernel cannot fill
+// 256 compute units.
 constexpr int64_t kSkinnyTiles = 160;
 
 struct GemmChoice {
     int bm, bn;
     void (*fn)(const void *, int64_t, const void *, int64_t, int64_t, const int32_t *, int64_t, const void *,
-               int64_t, bool, bool, bool, void *, int64_t, hipStream_t);
+               int64_t, bool, bool, bool, void *, int64_t, hipStream_t, const char *);
 };
 
-// Measured on MI355X (fp32 and bf16 alike): 64 x 64 tiles win until there
-// are enough 128 x 128 tiles to give every compute unit two, after which
-// the larger tile's reuse wins.
-static GemmChoice choose_main(int64_t m, int64_t d_out) {
+// Tile shapes measured on MI355X.  fp32: the chunked kernel with 64 x 128
+// tiles and 32-deep k steps (64 x 64 when the output is at most 64 wide);
+// once there are enough 128 x 128 tiles to give every compute unit two, the
+// W-as-stored kernel with 128 x 128 tiles.  bf16: 64 x 64 until that same
+// 128 x 128 point.
+static GemmChoice choose_main(int64_t m, int64_t d_out, bool bf16) {
 #ifdef GNNAV_GEMM_SWEEP
     if (const char *e = getenv("GNNAV_GEMM_CFG")) {
         switch (atoi(e)) {
             case 1: return {64, 128, launch_main<64, 128, 2, 2, 16, 32>};
-            case 2: return {32, 256, launch_main<32, 256, 1, 4, 16, 32>};
-            case 3: return {64, 256, launch_main<64, 256, 1, 4, 16, 32>};
+            case 2: return {64, 128, launch_main<64, 128, 2, 2, 32, 64>};
+            case 3: return {128, 64, launch_main<128, 64, 2, 2, 32, 64>};
             case 4: return {128, 128, launch_main<128, 128, 2, 2, 16, 32>};
             case 5: return {64, 64, launch_main<64, 64, 2, 2, 16, 32>};
-            case 6: return {64, 128, launch_main<64, 128, 2, 2, 32, 64>};
-            case 7: return {64, 256, launch_main<64, 256, 1, 4, 32, 64>};
+            case 6: return {64, 64, launch_main<64, 64, 2, 2, 32, 64>};
             case 8: return {128, 128, launch_main<128, 128, 2, 2, 32, 64>};
-            case 9: return {64, 64, launch_main<64, 64, 2, 2, 32, 64>};
+            case 9: return {128, 128, launch_main<128, 128, 2, 2, 16, 32, true>};
+            case 10: return {64, 64, launch_main<64, 64, 2, 2, 16, 32, true>};
             default: break;
         }
     }
 #endif
-    if (d_out > 64 && ((m + 127) / 128) * ((d_out + 127) / 128) >= 512)
-        return {128, 128, launch_main<128, 128, 2, 2, 16, 32>};
-    return {64, 64, launch_main<64, 64, 2, 2, 16, 32>};
+    const bool big = d_out > 64 && ((m + 127) / 128) * ((d_out + 127) / 128) >= 512;
+    if (bf16) {
+        if (big) return {128, 128, launch_main<128, 128, 2, 2, 16, 32>};
+        return {64, 64, launch_main<64, 64, 2, 2, 16, 32>};
+    }
+    if (big) return {128, 128, launch_main<128, 128, 2, 2, 16, 32, true>};
+    if (d_out <= 64) return {64, 64, launch_main<64, 64, 2, 2, 32, 32>};
+    return {64, 128, launch_main<64, 128, 2, 2, 32, 32>};
 }
 
 void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
@@ -528,11 +677,11 @@ void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t 
                     int64_t ld_out, hipStream_t s, const char *label) {
     if (m <= 0) return;
     if (!bf16 && out_bf16) fail(GNNAV_E_INVALID, "bf16 output needs bf16 operands");
-    KernelTimer t(label, s);
-    const GemmChoice ch = choose_main(m, d_out);
-    const int64_t tiles = ((m + ch.bm - 1) / ch.bm) * ((d_out + ch.bn - 1) / ch.bn);
-    if (tiles < kSkinnyTiles) {
+    const GemmChoice ch = choose_main(m, d_out, bf16);
+    const int64_t tiles64 = ((m + 63) / 64) * ((d_out + 63) / 64);
+    if (tiles64 < kSkinnyTiles) {
         const dim3 grid((unsigned)((m + 15) / 16), (unsigned)((d_out + 63) / 64));
+        KernelTimer t(label, s);
         if (!bf16)
             hipLaunchKernelGGL((k_combine_skinny<false, float, float>), grid, dim3(256), 0, s, (const float *)self,
                                ld_self, (const float *)agg, ld_agg, m, m_dev, d_in, (const float *)w, d_out,
@@ -546,7 +695,7 @@ void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t 
                                (const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, d_in,
                                (const uint16_t *)w, d_out, (int)relu, (float *)out, ld_out);
     } else {
-        ch.fn(self, ld_self, agg, ld_agg, m, m_dev, d_in, w, d_out, bf16, relu, out_bf16, out, ld_out, s);
+        ch.fn(self, ld_self, agg, ld_agg, m, m_dev, d_in, w, d_out, bf16, relu, out_bf16, out, ld_out, s, label);
     }
     GNNAV_HIP(hipGetLastError());
 }

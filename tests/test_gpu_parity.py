@@ -260,7 +260,8 @@ def test_aggregate_mean_parity(G, d, dtype):
 # the main kernel with 32x256 (N > 128), 64x128 (64 < N <= 128) or 64x64 tiles.
 COMBINE_CASES = [(1, 3, 16), (63, 64, 41), (64, 100, 47), (65, 602, 256), (1000, 128, 64),
                  (777, 256, 256), (130, 5, 300), (20000, 602, 256), (12000, 64, 41),
-                 (12001, 100, 100), (9000, 256, 256), (10240, 3, 47), (6000, 128, 260)]
+                 (12001, 100, 100), (9000, 256, 256), (10240, 3, 47), (6000, 128, 260),
+                 (66000, 100, 256), (40000, 37, 130)]
 
 
 @pytest.mark.parametrize("relu", [False, True])
