@@ -330,3 +330,89 @@ def sage_forward_rows(blocks: Blocks, H0: np.ndarray, Ws, out_rows, bf16: bool =
         full = np.zeros((blocks.sizes[b - 1], Ws[l - 1].shape[1]), np.float64)
         full[rows] = part
         X = full
+
+
+# ------------------------------------------------- O9: loss, backward ---
+# The training half of Algorithm 1's iteration (loss, backward, update),
+# written with numpy in float64.  Forward activations come from
+# sage_forward(..., keep=True).
+
+def softmax_xent(Z: np.ndarray, y) -> tuple:
+    """Mean softmax cross-entropy over the rows of Z [n, C] with labels y.
+
+    Returns (loss, dZ) where dZ = (softmax(Z) - onehot(y)) / n is the
+    gradient of the mean loss with respect to Z.
+    """
+    Z = np.asarray(Z, dtype=np.float64)
+    y = np.asarray(y, dtype=np.int64)
+    n = Z.shape[0]
+    if n == 0:
+        return 0.0, np.zeros_like(Z)
+    zmax = Z.max(axis=1, keepdims=True)
+    e = np.exp(Z - zmax)
+    s = e.sum(axis=1, keepdims=True)
+    logp = Z - zmax - np.log(s)
+    loss = -logp[np.arange(n), y].mean()
+    dZ = e / s
+    dZ[np.arange(n), y] -= 1.0
+    return float(loss), dZ / n
+
+
+def aggregate_mean_t(indptr, indices, n_src: int, G: np.ndarray) -> np.ndarray:
+    """Adjoint of the mean aggregation of one block (Eq. 1 Aggregate).
+
+    The forward sets agg[i] = (1/cnt_i) * sum of X[indices[p]] over the
+    row's edges p; so dX[j] = sum over edges p with indices[p] = j of
+    G[i] / cnt_i, where i is the row that holds p.
+    """
+    indptr = np.asarray(indptr, dtype=np.int64)
+    indices = np.asarray(indices, dtype=np.int64)
+    G = np.asarray(G, dtype=np.float64)
+    cnt = np.diff(indptr)
+    row_of_edge = np.repeat(np.arange(cnt.size), cnt)
+    dX = np.zeros((n_src, G.shape[1]), np.float64)
+    if indices.size:
+        np.add.at(dX, indices, G[row_of_edge] / cnt[row_of_edge, None])
+    return dX
+
+
+def sage_backward(blocks: Blocks, H0: np.ndarray, Ws, trace, dZ: np.ndarray):
+    """Weight gradients of the L-layer SAGE for the output gradient dZ.
+
+    Layer l (block b = L-l+1) computed Z_l = [X[0:n_dst] | agg] W_l from
+    its input X = H^(l-1); hence dW_l = [X[0:n_dst] | agg]^T dZ_l.  Below
+    the first layer the gradient flows back: d[X[0:n_dst]] = dZ_l W_top^T,
+    d(agg) = dZ_l W_bot^T, dX = self part + aggregate_mean_t(d(agg)), and
+    through the ReLU of layer l-1: dZ_(l-1) = dX * [H^(l-1) > 0].
+    Returns [dW_1, ..., dW_L].
+    """
+    L = blocks.n_hops
+    dWs = [None] * L
+    G = np.asarray(dZ, dtype=np.float64)
+    for l in range(L, 0, -1):
+        b = L - l + 1
+        X = np.asarray(H0, dtype=np.float64) if l == 1 else trace[l - 2][1]
+        agg = trace[l - 1][0]
+        n_dst = blocks.sizes[b - 1]
+        W = np.asarray(Ws[l - 1], dtype=np.float64)
+        d_in = X.shape[1]
+        dWs[l - 1] = np.concatenate([X[:n_dst], agg], axis=1).T @ G
+        if l == 1:
+            break
+        dX = aggregate_mean_t(blocks.indptr[b - 1], blocks.indices[b - 1], X.shape[0], G @ W[d_in:].T)
+        dX[:n_dst] += G @ W[:d_in].T
+        G = dX * (X > 0)
+    return dWs
+
+
+def train_step(blocks: Blocks, H0: np.ndarray, Ws, y, lr: float):
+    """One iteration: forward, mean softmax-CE over F_0 with labels y,
+    backward, and plain SGD W_l <- W_l - lr * dW_l.
+
+    Returns (loss, logits, [dW_l], [updated W_l]).
+    """
+    Wd = [np.asarray(w, dtype=np.float64) for w in Ws]
+    logits, trace = sage_forward(blocks, H0, Wd, keep=True)
+    loss, dZ = softmax_xent(logits, y)
+    dWs = sage_backward(blocks, H0, Wd, trace, dZ)
+    return loss, logits, dWs, [w - lr * g for w, g in zip(Wd, dWs)]

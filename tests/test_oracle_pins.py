@@ -527,3 +527,114 @@ def test_fifo_cache_repeat_batch_hits():
     # the 20 oldest ring entries survived; the first 100 were replaced in order
     ring = cache.owner[cache.c - 120:]
     assert ring[:100].tolist() == ids.tolist()
+
+
+# ------------------------------------------- loss, backward, update ---
+
+def _loss_of(blocks, H0, Ws, y):
+    logits = O.sage_forward(blocks, H0, Ws)
+    return O.softmax_xent(logits, y)[0]
+
+
+def test_softmax_xent_closed_forms():
+    """Uniform logits give log C; the gradient rows sum to zero and equal
+    (1/C - onehot)/n; a shift of every logit in a row changes nothing."""
+    C, n = 7, 5
+    y = np.array([0, 6, 3, 3, 1])
+    loss, dZ = O.softmax_xent(np.zeros((n, C)), y)
+    assert loss == pytest.approx(math.log(C), abs=1e-15)
+    want = np.full((n, C), 1.0 / C)
+    want[np.arange(n), y] -= 1.0
+    assert np.allclose(dZ, want / n, atol=1e-15)
+    rng = np.random.default_rng(0)
+    Z = rng.normal(size=(n, C)) * 4
+    l1, g1 = O.softmax_xent(Z, y)
+    l2, g2 = O.softmax_xent(Z + rng.normal(size=(n, 1)) * 50, y)
+    assert l1 == pytest.approx(l2, rel=1e-12)
+    assert np.allclose(g1, g2, atol=1e-14)
+    assert np.allclose(g1.sum(axis=1), 0, atol=1e-15)
+    # a one-row, two-class case by hand: loss = log(1 + e^(z1 - z0))
+    l, g = O.softmax_xent(np.array([[0.3, -1.2]]), [0])
+    assert l == pytest.approx(math.log1p(math.exp(-1.5)), rel=1e-14)
+    assert g[0, 1] == pytest.approx(1 / (1 + math.exp(1.5)), rel=1e-14)
+
+
+def test_softmax_xent_finite_difference():
+    rng = np.random.default_rng(1)
+    Z = rng.normal(size=(6, 5)) * 3
+    y = rng.integers(0, 5, 6)
+    _, g = O.softmax_xent(Z, y)
+    eps = 1e-6
+    for i, c in itertools.product(range(6), range(5)):
+        Zp, Zm = Z.copy(), Z.copy()
+        Zp[i, c] += eps
+        Zm[i, c] -= eps
+        fd = (O.softmax_xent(Zp, y)[0] - O.softmax_xent(Zm, y)[0]) / (2 * eps)
+        assert fd == pytest.approx(g[i, c], abs=1e-9)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_aggregate_mean_t_is_the_adjoint(seed):
+    """<agg(X), G> = <X, agg^T(G)>, with agg taken from the C forward
+    (the W = [0; I] pass-through of sage_layer)."""
+    n, u, v = W.random_graph(300, 1500, seed)
+    csr = O.build_csr(n, u, v)
+    seeds = np.arange(0, n, 7, dtype=np.int32)
+    blk = O.sample_blocks(csr, seeds, [4], 11 + seed)
+    ip, ix = blk.indptr[0], blk.indices[0]
+    rng = np.random.default_rng(seed)
+    d = 5
+    X = rng.normal(size=(blk.sizes[1], d))
+    G = rng.normal(size=(blk.sizes[0], d))
+    Wpass = np.concatenate([np.zeros((d, d)), np.eye(d)])
+    agg = O.sage_layer(ip, ix, X, Wpass, relu=False, bf16=False, round_out=False)
+    lhs = float((agg * G).sum())
+    rhs = float((X * O.aggregate_mean_t(ip, ix, X.shape[0], G)).sum())
+    assert lhs == pytest.approx(rhs, rel=1e-12)
+    # isolated destination rows (no edges) send nothing back
+    dX = O.aggregate_mean_t([0, 0, 2], [1, 1], 3, np.ones((2, 1)))
+    assert dX.ravel().tolist() == [0.0, 1.0, 0.0]
+
+
+@pytest.mark.parametrize("fanouts,dims", [([3, 2], [4, 6, 3]), ([2, 3, 2], [3, 5, 4, 4])])
+def test_sage_backward_finite_difference(fanouts, dims):
+    """Every weight gradient against central differences of the loss of the
+    full forward (float64, ReLU kinks are measure-zero for random data)."""
+    n, u, v = W.random_graph(80, 300, 5)
+    csr = O.build_csr(n, u, v)
+    seeds = np.array([3, 17, 40, 41, 77], np.int32)
+    blk = O.sample_blocks(csr, seeds, fanouts, 99)
+    rng = np.random.default_rng(7)
+    H0 = rng.normal(size=(blk.sizes[-1], dims[0]))
+    Ws = [rng.normal(size=(2 * dims[l], dims[l + 1])) * 0.7 for l in range(len(fanouts))]
+    y = rng.integers(0, dims[-1], blk.sizes[0])
+    logits, trace = O.sage_forward(blk, H0, Ws, keep=True)
+    _, dZ = O.softmax_xent(logits, y)
+    dWs = O.sage_backward(blk, H0, Ws, trace, dZ)
+    eps = 1e-6
+    for l, Wl in enumerate(Ws):
+        assert dWs[l].shape == Wl.shape
+        for a, o in itertools.product(range(Wl.shape[0]), range(Wl.shape[1])):
+            Wp = [w.copy() for w in Ws]
+            Wm = [w.copy() for w in Ws]
+            Wp[l][a, o] += eps
+            Wm[l][a, o] -= eps
+            fd = (_loss_of(blk, H0, Wp, y) - _loss_of(blk, H0, Wm, y)) / (2 * eps)
+            assert fd == pytest.approx(dWs[l][a, o], abs=1e-7), (l, a, o)
+
+
+def test_train_step_decreases_loss_and_applies_sgd():
+    n, u, v = W.random_graph(200, 900, 3)
+    csr = O.build_csr(n, u, v)
+    blk = O.sample_blocks(csr, np.arange(0, 200, 9, dtype=np.int32), [4, 3], 5)
+    rng = np.random.default_rng(2)
+    dims = [6, 8, 4]
+    H0 = rng.normal(size=(blk.sizes[-1], dims[0]))
+    Ws = [rng.normal(size=(2 * dims[l], dims[l + 1])) * 0.5 for l in range(2)]
+    y = rng.integers(0, 4, blk.sizes[0])
+    lr = 0.05
+    loss, _, dWs, new = O.train_step(blk, H0, Ws, y, lr)
+    for w, g, w2 in zip(Ws, dWs, new):
+        assert np.array_equal(w2, w - lr * g)
+    # a small step along the negative gradient lowers the loss
+    assert _loss_of(blk, H0, new, y) < loss

@@ -44,6 +44,7 @@ FEAT_SEED = 2
 PERM_SEED = 3
 WEIGHT_SEED = 4
 RNG_BASE = 5
+LABEL_SEED = 6
 
 # The five workloads.  ``cache`` is the fraction r of nodes held in the
 # device cache; ``store_on_device`` keeps the full feature store in HBM.
@@ -192,6 +193,12 @@ def glorot(d_in: int, d_out: int, dtype: str, seed: int) -> np.ndarray:
     return w if dtype == "f32" else f32_to_bf16_bits(w)
 
 
+def labels(n: int, classes: int, seed: int = LABEL_SEED) -> np.ndarray:
+    """Synthetic class label of every node: int32[n], uniform over [0, classes)."""
+    rng = np.random.Generator(np.random.Philox(seed))
+    return rng.integers(0, classes, size=n, dtype=np.int32)
+
+
 def rng_seed_for_batch(b: int) -> int:
     """Sampler key of batch b: (5 << 32) | b."""
     return (RNG_BASE << 32) | int(b)
@@ -264,6 +271,11 @@ class Workload:
 
     def rng_seed(self, b: int) -> int:
         return rng_seed_for_batch(b)
+
+    def labels(self) -> np.ndarray:
+        if getattr(self, "_labels", None) is None:
+            self._labels = labels(self.n, self.dims[-1])
+        return self._labels
 
 
 def tiny_graph(kind: str):
