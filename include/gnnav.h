@@ -281,6 +281,68 @@ gnnav_status gnnav_sage_forward(gnnav_blocks *b, const void *x_dev, int64_t ld_x
                                 const void *const *W_dev, const int32_t *dims, int32_t n_layers,
                                 gnnav_dtype dt, float *logits_dev, int64_t ld_out, void *stream);
 
+/* -------------------------------------------------------------- training ---
+ * The rest of Algorithm 1's iteration after the forward: the loss over the
+ * target vertices, the backward pass through the L SAGE layers and the
+ * weight update.  fp32 only.  The paper fixes neither loss nor optimiser;
+ * these entry points use mean softmax cross-entropy and plain SGD.
+ *
+ * gnnav_sage_train_step: forward as gnnav_sage_forward (dt = F32), keeping
+ * every layer's aggregate and hidden output in `b`; then
+ *   loss = mean over rows i of F_0 of -log softmax(Z_L[i])[y_i], with
+ *          y_i = labels_dev[F_0[i]] (labels_dev: device int32, one per
+ *          graph vertex); written to loss_dev[0];
+ *   dZ_L = (softmax(Z_L) - onehot(y)) / |F_0|;
+ *   for l = L .. 1 (block b = L-l+1, X = H^(l-1), n = |F_(b-1)|):
+ *     dW_l = [X[0:n] | Agg_l]^T dZ_l;
+ *     for l > 1: dX = dZ_l W_top^T on the first n rows plus the adjoint of
+ *     the mean aggregation applied to dZ_l W_bot^T (row j receives
+ *     dAgg[i] / cnt_i from every sampled edge i -> j), and
+ *     dZ_(l-1) = dX * [H^(l-1) > 0];
+ *   W_dev[l-1] -= lr * dW_l, in place, after dZ_(l-1) has been computed.
+ * Every sum runs in a fixed order (no floating-point atomics): repeated
+ * calls on the same inputs give identical bits.  dW_dev: optional array of
+ * L device pointers that receive dW_l (row-major [2*dims[l-1], dims[l]]);
+ * NULL skips the copy.  A label outside [0, dims[L]) makes that row's loss
+ * NaN (so the mean is NaN) and its gradient row zero.
+ * Errors: as gnnav_sage_forward; E_INVALID also for NULL labels/loss or a
+ * non-finite lr.  Asynchronous.                                           */
+gnnav_status gnnav_sage_train_step(gnnav_blocks *b, const float *x_dev, int64_t ld_x,
+                                   float *const *W_dev, const int32_t *dims, int32_t n_layers,
+                                   const int32_t *labels_dev, float lr, float *logits_dev,
+                                   int64_t ld_out, float *loss_dev, float *const *dW_dev, void *stream);
+
+/* The backward kernels one at a time (device pointers, fp32, rows 16-byte
+ * aligned; the three share one process-wide workspace, ordered across
+ * streams by an event).
+ *
+ * gnnav_softmax_xent: loss_dev[0] = mean over the n rows of logits [n x C]
+ * of the softmax cross-entropy with labels_dev[i] (device int32[n]);
+ * dz_dev [n x C] = (softmax - onehot) / n.  Labels outside [0, C) as above.
+ *
+ * gnnav_aggregate_mean_backward: the adjoint of gnnav_aggregate_mean for a
+ * block (indptr [n_dst+1], indices [E] local source ids < n_src):
+ *   out[j] = mask(j) * ( sum over edges p with indices[p] = j, in edge
+ *            order, of dagg[i(p)] / cnt_i  +  dself[j] if j < n_dst ),
+ * for j < n_src; dself_dev and mask_dev may be NULL (no self term; no mask),
+ * mask(j) zeroes the elements where mask_dev[j] <= 0.  Reads indptr[n_dst]
+ * to the host (one synchronous copy).
+ *
+ * gnnav_weight_grad: dw_dev [2*d_in x d_out] (contiguous) =
+ * [self | agg]^T dz for m rows (Eq. 1's combine, differentiated).
+ * Errors: E_INVALID (null pointers, sizes, strides, alignment), E_DEVICE. */
+gnnav_status gnnav_softmax_xent(const float *logits_dev, int64_t ld, int64_t n, int64_t n_classes,
+                                const int32_t *labels_dev, float *dz_dev, int64_t ld_dz,
+                                float *loss_dev, void *stream);
+gnnav_status gnnav_aggregate_mean_backward(const int32_t *indptr_dev, const int32_t *indices_dev,
+                                           int64_t n_dst, int64_t n_src, const float *dagg_dev,
+                                           int64_t ld_dagg, const float *dself_dev, int64_t ld_dself,
+                                           const float *mask_dev, int64_t ld_mask, int64_t d,
+                                           float *out_dev, int64_t ld_out, void *stream);
+gnnav_status gnnav_weight_grad(const float *self_dev, int64_t ld_self, const float *agg_dev,
+                               int64_t ld_agg, int64_t m, int64_t d_in, const float *dz_dev,
+                               int64_t ld_dz, int64_t d_out, float *dw_dev, void *stream);
+
 /* ------------------------------------------------------------ profiling ---
  * Per-kernel timing with HIP events recorded around every kernel launch on
  * the stream it is launched on.  profile_start clears the table and turns

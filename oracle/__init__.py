@@ -376,7 +376,7 @@ def aggregate_mean_t(indptr, indices, n_src: int, G: np.ndarray) -> np.ndarray:
     return dX
 
 
-def sage_backward(blocks: Blocks, H0: np.ndarray, Ws, trace, dZ: np.ndarray):
+def sage_backward(blocks: Blocks, H0: np.ndarray, Ws, trace, dZ: np.ndarray, abs_scale: bool = False):
     """Weight gradients of the L-layer SAGE for the output gradient dZ.
 
     Layer l (block b = L-l+1) computed Z_l = [X[0:n_dst] | agg] W_l from
@@ -384,8 +384,14 @@ def sage_backward(blocks: Blocks, H0: np.ndarray, Ws, trace, dZ: np.ndarray):
     the first layer the gradient flows back: d[X[0:n_dst]] = dZ_l W_top^T,
     d(agg) = dZ_l W_bot^T, dX = self part + aggregate_mean_t(d(agg)), and
     through the ReLU of layer l-1: dZ_(l-1) = dX * [H^(l-1) > 0].
-    Returns [dW_1, ..., dW_L].
+    Returns [dW_1, ..., dW_L].  abs_scale: the same recursion over absolute
+    values (|X|, |agg|, |W|, |dZ|), the scale of each sum's rounding error.
     """
+    if abs_scale:
+        H0 = np.abs(np.asarray(H0, dtype=np.float64))
+        Ws = [np.abs(np.asarray(w, dtype=np.float64)) for w in Ws]
+        trace = [(np.abs(a), np.abs(h)) for a, h in trace]
+        dZ = np.abs(np.asarray(dZ, dtype=np.float64))
     L = blocks.n_hops
     dWs = [None] * L
     G = np.asarray(dZ, dtype=np.float64)

@@ -31,7 +31,8 @@ EXPORTS = [
     "gnnav_cache_slot_map_host", "gnnav_cache_contents_host", "gnnav_cache_set_policy", "gnnav_cache_free", "gnnav_blocks_create", "gnnav_blocks_free",
     "gnnav_sample", "gnnav_sample_async", "gnnav_blocks_sync", "gnnav_blocks_device_sizes",
     "gnnav_blocks_hop", "gnnav_blocks_nodes", "gnnav_gather", "gnnav_gather_n",
-    "gnnav_aggregate_mean", "gnnav_combine", "gnnav_sage_forward", "gnnav_profile_start",
+    "gnnav_aggregate_mean", "gnnav_combine", "gnnav_sage_forward", "gnnav_sage_train_step",
+    "gnnav_softmax_xent", "gnnav_aggregate_mean_backward", "gnnav_weight_grad", "gnnav_profile_start",
     "gnnav_profile_stop", "gnnav_profile_count", "gnnav_profile_get",
 ]
 
@@ -75,6 +76,10 @@ _sig = {
     "gnnav_aggregate_mean": ([P, P, i64, P, i64, i64, i32, P, i64, P], i32),
     "gnnav_combine": ([P, i64, P, i64, i64, i64, P, i64, i32, i32, i32, P, i64, P], i32),
     "gnnav_sage_forward": ([P, P, i64, P, P, i32, i32, P, i64, P], i32),
+    "gnnav_sage_train_step": ([P, P, i64, P, P, i32, P, C.c_float, P, i64, P, P, P], i32),
+    "gnnav_softmax_xent": ([P, i64, i64, i64, P, P, i64, P, P], i32),
+    "gnnav_aggregate_mean_backward": ([P, P, i64, i64, P, i64, P, i64, P, i64, i64, P, i64, P], i32),
+    "gnnav_weight_grad": ([P, i64, P, i64, i64, i64, P, i64, i64, P, P], i32),
     "gnnav_profile_start": ([], i32),
     "gnnav_profile_stop": ([], i32),
     "gnnav_profile_count": ([], i32),
@@ -339,6 +344,37 @@ def combine(self_x, agg, m: int, d_in: int, w, d_out: int, dtype: str, relu: boo
     _check(_lib.gnnav_combine(_dev_ptr(self_x), self_x.stride(0), _dev_ptr(agg), agg.stride(0), m, d_in,
                               _dev_ptr(w), d_out, dtype_code(dtype), int(relu), int(out_bf16),
                               _dev_ptr(out), out.stride(0), _stream(stream)))
+
+
+def sage_train_step(blocks: Blocks, x, weights, dims, labels, lr: float, logits, loss, grads=None,
+                    stream=None):
+    """gnnav_sage_train_step: fp32; `weights` (device tensors) are updated in place."""
+    L = len(weights)
+    wp = (P * L)(*[w.data_ptr() for w in weights])
+    gp = (P * L)(*[g.data_ptr() for g in grads]) if grads is not None else None
+    dm = np.ascontiguousarray(dims, dtype=np.int32)
+    _check(_lib.gnnav_sage_train_step(blocks._h, _dev_ptr(x), x.stride(0), wp, _np_ptr(dm), L,
+                                      _dev_ptr(labels), float(lr), _dev_ptr(logits), logits.stride(0),
+                                      _dev_ptr(loss), gp, _stream(stream)))
+
+
+def softmax_xent(logits, n: int, n_classes: int, labels, dz, loss, stream=None):
+    _check(_lib.gnnav_softmax_xent(_dev_ptr(logits), logits.stride(0), n, n_classes, _dev_ptr(labels),
+                                   _dev_ptr(dz), dz.stride(0), _dev_ptr(loss), _stream(stream)))
+
+
+def aggregate_mean_backward(indptr_ptr: int, indices_ptr: int, n_dst: int, n_src: int, dagg, d: int, out,
+                            dself=None, mask=None, stream=None):
+    _check(_lib.gnnav_aggregate_mean_backward(
+        indptr_ptr, indices_ptr, n_dst, n_src, _dev_ptr(dagg), dagg.stride(0),
+        _dev_ptr(dself) if dself is not None else None, dself.stride(0) if dself is not None else 0,
+        _dev_ptr(mask) if mask is not None else None, mask.stride(0) if mask is not None else 0,
+        d, _dev_ptr(out), out.stride(0), _stream(stream)))
+
+
+def weight_grad(self_x, agg, m: int, d_in: int, dz, d_out: int, dw, stream=None):
+    _check(_lib.gnnav_weight_grad(_dev_ptr(self_x), self_x.stride(0), _dev_ptr(agg), agg.stride(0), m, d_in,
+                                  _dev_ptr(dz), dz.stride(0), d_out, _dev_ptr(dw), _stream(stream)))
 
 
 def sage_forward(blocks: Blocks, x, weights, dims, dtype: str, logits, stream=None):

@@ -533,6 +533,10 @@ struct gnnav_blocks {
     DevBuf indptr[kMaxHops], nbrs[kMaxHops], indices[kMaxHops];
     int32_t *sizes_host = nullptr;  // pinned mirror of `sizes`
     DevBuf agg, hid[2];             // forward workspace
+    // training: activations kept per layer, gradients, transposed blocks
+    DevBuf act_agg[kMaxHops], act_h[kMaxHops];
+    DevBuf dz[2], dself, dagg, wpart, row_loss, dw_tmp;
+    CscWorkspace csc;
 };
 
 extern "C" gnnav_status gnnav_blocks_create(gnnav_blocks **out) {
@@ -567,6 +571,12 @@ extern "C" void gnnav_blocks_free(gnnav_blocks *b) {
     b->agg.release();
     b->hid[0].release();
     b->hid[1].release();
+    for (int h = 0; h < kMaxHops; ++h) {
+        b->act_agg[h].release();
+        b->act_h[h].release();
+    }
+    for (DevBuf *d : {&b->dz[0], &b->dz[1], &b->dself, &b->dagg, &b->wpart, &b->row_loss, &b->dw_tmp}) d->release();
+    b->csc.release();
     if (b->sizes_host) (void)hipHostFree(b->sizes_host);
     delete b;
 }
@@ -810,34 +820,50 @@ extern "C" gnnav_status gnnav_combine(const void *self_dev, int64_t ld_self, con
     });
 }
 
-extern "C" gnnav_status gnnav_sage_forward(gnnav_blocks *b, const void *x_dev, int64_t ld_x,
-                                           const void *const *W_dev, const int32_t *dims, int32_t n_layers,
-                                           gnnav_dtype dt, float *logits_dev, int64_t ld_out, void *stream) {
-    return guarded([&] {
-        GNNAV_CHECK(b && W_dev && dims && logits_dev, GNNAV_E_INVALID, "NULL argument");
-        GNNAV_CHECK(n_layers == b->L && n_layers >= 1, GNNAV_E_INVALID, "n_layers differs from the sampled hops");
-        GNNAV_CHECK(dt == GNNAV_F32 || dt == GNNAV_BF16, GNNAV_E_INVALID, "bad dtype");
-        const int L = n_layers;
-        for (int l = 0; l <= L; ++l) GNNAV_CHECK(dims[l] > 0, GNNAV_E_INVALID, "dims must be positive");
-        for (int l = 0; l < L; ++l) GNNAV_CHECK(W_dev[l], GNNAV_E_INVALID, "NULL weight");
-        GNNAV_CHECK(ld_out >= dims[L], GNNAV_E_INVALID, "ld_out < dims[L]");
-        const bool bf = dt == GNNAV_BF16;
-        const int64_t elt = bf ? 2 : 4;
-        GNNAV_CHECK(ld_x >= dims[0] && (ld_x * elt) % 16 == 0 && aligned16(x_dev), GNNAV_E_INVALID,
-                    "x rows must be 16-byte aligned with ld_x >= dims[0]");
-        hipStream_t s = (hipStream_t)stream;
-        // workspace: agg for the largest layer, two ping-pong hidden buffers
-        // Row counts: exact host sizes after gnnav_sample / gnnav_blocks_sync;
-        // otherwise the kernels read them from device memory and the grids and
-        // buffers follow the Eq. 12 bounds of the sample.
-        const bool host = b->host_sizes;
-        const int32_t *dsz = b->sizes.as<int32_t>();
-        auto rows_of = [&](int hb) { return host ? b->n_h[hb - 1] : b->nb[hb - 1]; };
-        auto rows_dev = [&](int hb) { return host ? (const int32_t *)nullptr : dsz + kSizeN + hb - 1; };
+// Row counts of a block: exact host sizes after gnnav_sample /
+// gnnav_blocks_sync; otherwise the kernels read them from device memory and
+// grids and buffers follow the Eq. 12 bounds of the sample.
+struct BlockRows {
+    const gnnav_blocks *b;
+    // destination rows of block hb (F_(hb-1)); hb = L + 1 gives |F_L|
+    int64_t rows(int hb) const { return b->host_sizes ? b->n_h[hb - 1] : b->nb[hb - 1]; }
+    const int32_t *rows_dev(int hb) const {
+        return b->host_sizes ? nullptr : b->sizes.as<int32_t>() + kSizeN + hb - 1;
+    }
+    int64_t edges(int hb) const { return b->host_sizes ? b->e_h[hb] : b->eb[hb]; }
+    const int32_t *edges_dev(int hb) const { return b->sizes.as<int32_t>() + kSizeE + hb; }
+};
+
+static const char *kAggLabel[] = {"aggregate_mean.l1", "aggregate_mean.l2", "aggregate_mean.l3", "aggregate_mean.l4+"};
+static const char *kGemmLabel[] = {"combine_gemm.l1", "combine_gemm.l2", "combine_gemm.l3", "combine_gemm.l4+"};
+
+static void check_forward_args(const gnnav_blocks *b, const void *x_dev, int64_t ld_x, const void *const *W_dev,
+                               const int32_t *dims, int32_t n_layers, gnnav_dtype dt, const float *logits_dev,
+                               int64_t ld_out) {
+    GNNAV_CHECK(b && W_dev && dims && logits_dev, GNNAV_E_INVALID, "NULL argument");
+    GNNAV_CHECK(n_layers == b->L && n_layers >= 1, GNNAV_E_INVALID, "n_layers differs from the sampled hops");
+    GNNAV_CHECK(dt == GNNAV_F32 || dt == GNNAV_BF16, GNNAV_E_INVALID, "bad dtype");
+    const int L = n_layers;
+    for (int l = 0; l <= L; ++l) GNNAV_CHECK(dims[l] > 0, GNNAV_E_INVALID, "dims must be positive");
+    for (int l = 0; l < L; ++l) GNNAV_CHECK(W_dev[l], GNNAV_E_INVALID, "NULL weight");
+    GNNAV_CHECK(ld_out >= dims[L], GNNAV_E_INVALID, "ld_out < dims[L]");
+    const int64_t elt = dt == GNNAV_BF16 ? 2 : 4;
+    GNNAV_CHECK(ld_x >= dims[0] && (ld_x * elt) % 16 == 0 && aligned16(x_dev), GNNAV_E_INVALID,
+                "x rows must be 16-byte aligned with ld_x >= dims[0]");
+}
+
+// The L-layer forward.  keep: every layer's aggregate and hidden output get
+// a buffer of their own (read again by the backward); otherwise one
+// aggregate buffer and two ping-pong hidden buffers are reused.
+static void forward_impl(gnnav_blocks *b, const void *x_dev, int64_t ld_x, const void *const *W_dev,
+                         const int32_t *dims, int L, bool bf, float *logits_dev, int64_t ld_out, bool keep,
+                         hipStream_t s) {
+    const int64_t elt = bf ? 2 : 4;
+    const BlockRows br{b};
+    if (!keep) {
         int64_t agg_bytes = 1, hid_bytes = 1;
         for (int l = 1; l <= L; ++l) {
-            const int hb = L - l + 1;
-            const int64_t rows = rows_of(hb);
+            const int64_t rows = br.rows(L - l + 1);
             agg_bytes = std::max(agg_bytes, rows * padded_ld(dims[l - 1], elt) * elt);
             if (l < L) hid_bytes = std::max(hid_bytes, rows * padded_ld(dims[l], elt) * elt);
         }
@@ -846,32 +872,198 @@ extern "C" gnnav_status gnnav_sage_forward(gnnav_blocks *b, const void *x_dev, i
             b->hid[0].ensure(hid_bytes, s);
             b->hid[1].ensure(hid_bytes, s);
         }
-        static const char *kAggLabel[] = {"aggregate_mean.l1", "aggregate_mean.l2", "aggregate_mean.l3",
-                                          "aggregate_mean.l4+"};
-        static const char *kGemmLabel[] = {"combine_gemm.l1", "combine_gemm.l2", "combine_gemm.l3",
-                                           "combine_gemm.l4+"};
-        const void *x = x_dev;
-        int64_t ldx = ld_x;
-        for (int l = 1; l <= L; ++l) {
+    }
+    const void *x = x_dev;
+    int64_t ldx = ld_x;
+    for (int l = 1; l <= L; ++l) {
+        const int tag = l < 4 ? l - 1 : 3;
+        const int hb = L - l + 1;
+        const int64_t rows = br.rows(hb);
+        const int32_t *rdev = br.rows_dev(hb);
+        const int64_t din = dims[l - 1], dout = dims[l];
+        const int64_t lda = padded_ld(din, elt);
+        void *agg = b->agg.p;
+        if (keep) {
+            b->act_agg[l - 1].ensure(std::max<int64_t>(rows, 1) * lda * elt, s);
+            agg = b->act_agg[l - 1].p;
+        }
+        launch_aggregate_mean(b->indptr[hb - 1].as<int32_t>(), b->indices[hb - 1].as<int32_t>(), rows, rdev, x, ldx,
+                              din, bf, agg, lda, s, kAggLabel[tag]);
+        if (l < L) {
+            const int64_t ldh = padded_ld(dout, elt);
+            void *h = b->hid[l & 1].p;
+            if (keep) {
+                b->act_h[l - 1].ensure(std::max<int64_t>(rows, 1) * ldh * elt, s);
+                h = b->act_h[l - 1].p;
+            }
+            launch_combine(x, ldx, agg, lda, rows, rdev, din, W_dev[l - 1], dout, bf, true, bf, h, ldh, s,
+                           kGemmLabel[tag]);
+            x = h;
+            ldx = ldh;
+        } else {
+            launch_combine(x, ldx, agg, lda, rows, rdev, din, W_dev[l - 1], dout, bf, false, false, logits_dev,
+                           ld_out, s, kGemmLabel[tag]);
+        }
+    }
+}
+
+extern "C" gnnav_status gnnav_sage_forward(gnnav_blocks *b, const void *x_dev, int64_t ld_x,
+                                           const void *const *W_dev, const int32_t *dims, int32_t n_layers,
+                                           gnnav_dtype dt, float *logits_dev, int64_t ld_out, void *stream) {
+    return guarded([&] {
+        check_forward_args(b, x_dev, ld_x, W_dev, dims, n_layers, dt, logits_dev, ld_out);
+        forward_impl(b, x_dev, ld_x, W_dev, dims, n_layers, dt == GNNAV_BF16, logits_dev, ld_out, false,
+                     (hipStream_t)stream);
+    });
+}
+
+// ------------------------------------------------------------- training
+static const char *kWgradLabel[] = {"wgrad.l1", "wgrad.l2", "wgrad.l3", "wgrad.l4+"};
+static const char *kBwdGemmLabel[] = {"bwd_gemm.l1", "bwd_gemm.l2", "bwd_gemm.l3", "bwd_gemm.l4+"};
+static const char *kAggTLabel[] = {"aggregate_mean_t.l1", "aggregate_mean_t.l2", "aggregate_mean_t.l3",
+                                   "aggregate_mean_t.l4+"};
+static const char *kCscLabel[] = {"csc_build.l1", "csc_build.l2", "csc_build.l3", "csc_build.l4+"};
+
+extern "C" gnnav_status gnnav_sage_train_step(gnnav_blocks *b, const float *x_dev, int64_t ld_x, float *const *W_dev,
+                                              const int32_t *dims, int32_t n_layers, const int32_t *labels_dev,
+                                              float lr, float *logits_dev, int64_t ld_out, float *loss_dev,
+                                              float *const *dW_dev, void *stream) {
+    return guarded([&] {
+        check_forward_args(b, x_dev, ld_x, (const void *const *)W_dev, dims, n_layers, GNNAV_F32, logits_dev, ld_out);
+        GNNAV_CHECK(labels_dev && loss_dev, GNNAV_E_INVALID, "NULL labels or loss");
+        GNNAV_CHECK(std::isfinite(lr), GNNAV_E_INVALID, "lr is not finite");
+        const int L = n_layers;
+        hipStream_t s = (hipStream_t)stream;
+        forward_impl(b, x_dev, ld_x, (const void *const *)W_dev, dims, L, false, logits_dev, ld_out, true, s);
+        const BlockRows br{b};
+        auto ld4 = [](int64_t d) { return padded_ld(d, 4); };
+        // dZ of the last layer: rows F_0
+        {
+            const int64_t n0 = br.rows(1);
+            b->dz[L & 1].ensure(std::max<int64_t>(n0, 1) * ld4(dims[L]) * 4, s);
+            b->row_loss.ensure(std::max<int64_t>(n0, 1) * 4, s);
+            launch_softmax_xent(logits_dev, ld_out, n0, br.rows_dev(1), dims[L], b->nodes.as<int32_t>(), labels_dev,
+                                b->dz[L & 1].as<float>(), ld4(dims[L]), b->row_loss.as<float>(), loss_dev, s);
+        }
+        for (int l = L; l >= 1; --l) {
             const int tag = l < 4 ? l - 1 : 3;
             const int hb = L - l + 1;
-            const int64_t rows = rows_of(hb);
-            const int32_t *rdev = rows_dev(hb);
+            const int64_t n_dst = br.rows(hb), n_src = br.rows(hb + 1);
+            const int32_t *n_dst_dev = br.rows_dev(hb), *n_src_dev = br.rows_dev(hb + 1);
             const int64_t din = dims[l - 1], dout = dims[l];
-            const int64_t lda = padded_ld(din, elt);
-            launch_aggregate_mean(b->indptr[hb - 1].as<int32_t>(), b->indices[hb - 1].as<int32_t>(), rows, rdev, x,
-                                  ldx, din, bf, b->agg.p, lda, s, kAggLabel[tag]);
-            if (l < L) {
-                void *h = b->hid[l & 1].p;
-                const int64_t ldh = padded_ld(dout, elt);
-                launch_combine(x, ldx, b->agg.p, lda, rows, rdev, din, W_dev[l - 1], dout, bf, true, bf, h, ldh, s,
-                               kGemmLabel[tag]);
-                x = h;
-                ldx = ldh;
-            } else {
-                launch_combine(x, ldx, b->agg.p, lda, rows, rdev, din, W_dev[l - 1], dout, bf, false, false,
-                               logits_dev, ld_out, s, kGemmLabel[tag]);
+            const float *X = l == 1 ? x_dev : b->act_h[l - 2].as<float>();
+            const int64_t ldx = l == 1 ? ld_x : ld4(din);
+            const float *G = b->dz[l & 1].as<float>();
+            const int64_t ldg = ld4(dout);
+            const float *W = W_dev[l - 1];
+            if (l > 1) {
+                // gradient of the layer's input: self part and aggregate part
+                b->dself.ensure(std::max<int64_t>(n_dst, 1) * ld4(din) * 4, s);
+                b->dagg.ensure(std::max<int64_t>(n_dst, 1) * ld4(din) * 4, s);
+                launch_matmul_bt(G, ldg, n_dst, n_dst_dev, dout, W, dout, din, b->dself.as<float>(), ld4(din), s,
+                                 kBwdGemmLabel[tag]);
+                launch_matmul_bt(G, ldg, n_dst, n_dst_dev, dout, W + din * dout, dout, din, b->dagg.as<float>(),
+                                 ld4(din), s, kBwdGemmLabel[tag]);
+                b->csc.build(b->indptr[hb - 1].as<int32_t>(), b->indices[hb - 1].as<int32_t>(), n_dst, n_dst_dev,
+                             br.edges_dev(hb), br.edges(hb), n_src, b->scan, s, kCscLabel[tag]);
+                b->dz[(l - 1) & 1].ensure(std::max<int64_t>(n_src, 1) * ld4(din) * 4, s);
+                launch_aggregate_t(b->csc, b->indptr[hb - 1].as<int32_t>(), n_src, n_src_dev, n_dst, n_dst_dev,
+                                   b->dagg.as<float>(), ld4(din), b->dself.as<float>(), ld4(din), X, ldx, din,
+                                   b->dz[(l - 1) & 1].as<float>(), ld4(din), s, kAggTLabel[tag]);
             }
+            // dW_l = [X[0:n_dst] | agg]^T dZ_l, then W_l -= lr * dW_l
+            launch_wgrad(X, ldx, b->act_agg[l - 1].as<float>(), ld4(din), n_dst, n_dst_dev, din, G, ldg, dout,
+                         b->wpart, dW_dev ? dW_dev[l - 1] : nullptr, W_dev[l - 1], lr, s, kWgradLabel[tag]);
         }
+    });
+}
+
+// Stand-alone entry points of the backward kernels.  They share one
+// process-wide workspace; an event recorded after each call orders the next
+// one after it, whichever stream it uses.
+namespace {
+struct TrainWs {
+    std::mutex mu;
+    CscWorkspace csc;
+    ScanState scan;
+    DevBuf part, count;
+    hipEvent_t last_use = nullptr;
+};
+TrainWs g_train;
+
+template <class F>
+void with_train_ws(hipStream_t s, F &&f) {
+    std::lock_guard<std::mutex> lk(g_train.mu);
+    if (!g_train.last_use) GNNAV_HIP(hipEventCreateWithFlags(&g_train.last_use, hipEventDisableTiming));
+    GNNAV_HIP(hipStreamWaitEvent(s, g_train.last_use, 0));
+    f(g_train);
+    GNNAV_HIP(hipEventRecord(g_train.last_use, s));
+}
+}  // namespace
+
+extern "C" gnnav_status gnnav_softmax_xent(const float *logits_dev, int64_t ld, int64_t n, int64_t n_classes,
+                                           const int32_t *labels_dev, float *dz_dev, int64_t ld_dz, float *loss_dev,
+                                           void *stream) {
+    return guarded([&] {
+        GNNAV_CHECK(n >= 0 && n_classes > 0, GNNAV_E_INVALID, "n < 0 or n_classes <= 0");
+        GNNAV_CHECK(loss_dev && (n == 0 || (logits_dev && labels_dev && dz_dev)), GNNAV_E_INVALID, "NULL argument");
+        GNNAV_CHECK(ld >= n_classes && ld_dz >= n_classes, GNNAV_E_INVALID, "stride below n_classes");
+        hipStream_t s = (hipStream_t)stream;
+        with_train_ws(s, [&](TrainWs &w) {
+            w.part.ensure(std::max<int64_t>(n, 1) * sizeof(float), s);
+            launch_softmax_xent(logits_dev, ld, n, nullptr, n_classes, nullptr, labels_dev, dz_dev, ld_dz,
+                                w.part.as<float>(), loss_dev, s);
+        });
+    });
+}
+
+extern "C" gnnav_status gnnav_aggregate_mean_backward(const int32_t *indptr_dev, const int32_t *indices_dev,
+                                                      int64_t n_dst, int64_t n_src, const float *dagg_dev,
+                                                      int64_t ld_dagg, const float *dself_dev, int64_t ld_dself,
+                                                      const float *mask_dev, int64_t ld_mask, int64_t d,
+                                                      float *out_dev, int64_t ld_out, void *stream) {
+    return guarded([&] {
+        GNNAV_CHECK(n_dst >= 0 && n_src >= 0 && d > 0, GNNAV_E_INVALID, "negative size or d <= 0");
+        GNNAV_CHECK(n_src < INT32_MAX && n_dst < INT32_MAX, GNNAV_E_INVALID, "sizes beyond int32");
+        GNNAV_CHECK(n_dst == 0 || (indptr_dev && indices_dev && dagg_dev), GNNAV_E_INVALID, "NULL block or dagg");
+        GNNAV_CHECK(n_src == 0 || out_dev, GNNAV_E_INVALID, "NULL out");
+        auto rows_ok = [&](const float *p, int64_t ld) {
+            return p == nullptr || (ld >= d && ld % 4 == 0 && aligned16(p));
+        };
+        GNNAV_CHECK(rows_ok(dagg_dev, ld_dagg) && rows_ok(dself_dev, ld_dself) && rows_ok(mask_dev, ld_mask) &&
+                        rows_ok(out_dev, ld_out),
+                    GNNAV_E_INVALID, "rows must be 16-byte aligned with ld >= d");
+        GNNAV_CHECK(dself_dev == nullptr || n_dst <= n_src, GNNAV_E_INVALID, "self term needs n_dst <= n_src");
+        if (n_src == 0) return;
+        hipStream_t s = (hipStream_t)stream;
+        int32_t n_edges = 0;
+        if (n_dst > 0)
+            GNNAV_HIP(hipMemcpy(&n_edges, indptr_dev + n_dst, sizeof(int32_t), hipMemcpyDeviceToHost));
+        with_train_ws(s, [&](TrainWs &w) {
+            w.count.ensure(sizeof(int32_t), s);
+            launch_fill_i32(w.count.as<int32_t>(), n_edges, 1, s);
+            w.csc.build(indptr_dev, indices_dev, n_dst, nullptr, w.count.as<int32_t>(), n_edges, n_src, w.scan, s,
+                        "csc_build");
+            launch_aggregate_t(w.csc, indptr_dev, n_src, nullptr, dself_dev ? n_dst : 0, nullptr, dagg_dev, ld_dagg,
+                               dself_dev, ld_dself, mask_dev, ld_mask, d, out_dev, ld_out, s, "aggregate_mean_t");
+        });
+    });
+}
+
+extern "C" gnnav_status gnnav_weight_grad(const float *self_dev, int64_t ld_self, const float *agg_dev,
+                                          int64_t ld_agg, int64_t m, int64_t d_in, const float *dz_dev,
+                                          int64_t ld_dz, int64_t d_out, float *dw_dev, void *stream) {
+    return guarded([&] {
+        GNNAV_CHECK(m >= 0 && d_in > 0 && d_out > 0, GNNAV_E_INVALID, "m < 0 or d <= 0");
+        GNNAV_CHECK(dw_dev && (m == 0 || (self_dev && agg_dev && dz_dev)), GNNAV_E_INVALID, "NULL argument");
+        GNNAV_CHECK(ld_self >= d_in && ld_agg >= d_in && ld_dz >= d_out, GNNAV_E_INVALID, "stride below width");
+        GNNAV_CHECK(ld_self % 4 == 0 && ld_agg % 4 == 0 && ld_dz % 4 == 0 &&
+                        (m == 0 || (aligned16(self_dev) && aligned16(agg_dev) && aligned16(dz_dev))),
+                    GNNAV_E_INVALID, "rows must be 16-byte aligned");
+        hipStream_t s = (hipStream_t)stream;
+        with_train_ws(s, [&](TrainWs &w) {
+            launch_wgrad(self_dev, ld_self, agg_dev, ld_agg, m, nullptr, d_in, dz_dev, ld_dz, d_out, w.part, dw_dev,
+                         nullptr, 0.0f, s, "wgrad");
+        });
     });
 }

@@ -190,6 +190,38 @@ struct GatherArgs {
 };
 void launch_classify(const GatherArgs &a, hipStream_t s);
 void launch_gather_rows(const GatherArgs &a, bool hits, hipStream_t s);
+void launch_matmul_bt(const float *a, int64_t lda, int64_t m, const int32_t *m_dev, int64_t k, const float *b,
+                      int64_t ldb, int64_t n, float *out, int64_t ld_out, hipStream_t s, const char *label);
+// Transpose of a sampled block (destination rows per source column, in
+// edge order) and its column pointers; see train.hip.
+struct ScanState;
+struct CscWorkspace {
+    DevBuf keys[2], vals[2], hist, offs, col_ptr, cnt;
+    const int32_t *sorted_rows = nullptr;
+    void build(const int32_t *indptr, const int32_t *indices, int64_t n_dst, const int32_t *n_dst_dev,
+               const int32_t *n_edges_dev, int64_t e_bound, int64_t n_src_bound, ScanState &scan, hipStream_t s,
+               const char *label);
+    void release() {
+        for (int k = 0; k < 2; ++k) {
+            keys[k].release();
+            vals[k].release();
+        }
+        hist.release();
+        offs.release();
+        col_ptr.release();
+        cnt.release();
+    }
+};
+void launch_softmax_xent(const float *z, int64_t ldz, int64_t n, const int32_t *n_dev, int64_t C,
+                         const int32_t *nodes, const int32_t *labels, float *dz, int64_t lddz, float *row_loss,
+                         float *loss, hipStream_t s);
+void launch_aggregate_t(const CscWorkspace &csc, const int32_t *indptr, int64_t n_src, const int32_t *n_src_dev,
+                        int64_t n_self, const int32_t *n_self_dev, const float *dagg, int64_t ld_dagg,
+                        const float *dself, int64_t ld_dself, const float *mask, int64_t ld_mask, int64_t d,
+                        float *out, int64_t ld_out, hipStream_t s, const char *label);
+void launch_wgrad(const float *x_self, int64_t ld_self, const float *agg, int64_t ld_agg, int64_t m,
+                  const int32_t *m_dev, int64_t d_in, const float *dz, int64_t ld_dz, int64_t d_out, DevBuf &part,
+                  float *dw, float *w, float lr, hipStream_t s, const char *label);
 void launch_fifo_update(const GatherArgs &a, int64_t lo, int64_t rn, int32_t *owner, int32_t *slot_map,
                         int32_t *ring_ptr, void *cache, hipStream_t s);
 

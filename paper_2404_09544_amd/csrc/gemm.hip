@@ -87,8 +87,8 @@ template <int BM, int BN, int WM, int WN, int BK>
 __global__ void __launch_bounds__(256) k_combine_f32(const float *__restrict__ A0, int64_t lda0,
                                                      const float *__restrict__ A1, int64_t lda1, int64_t M,
                                                      const int32_t *__restrict__ m_dev, int64_t K,
-                                                     const float *__restrict__ WT, int64_t N, int relu,
-                                                     float *__restrict__ C, int64_t ldc) {
+                                                     const float *__restrict__ WT, int64_t ldb, int bvec, int nseg,
+                                                     int64_t N, int relu, float *__restrict__ C, int64_t ldc) {
     constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
     constexpr int CH = BK / 4;                    // chunks per row and step
     constexpr int A_CH = BM * CH, B_CH = BN * CH;
@@ -112,13 +112,18 @@ __global__ void __launch_bounds__(256) k_combine_f32(const float *__restrict__ A
         for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     const int64_t kt = (K + BK - 1) / BK;
-    const int64_t tiles = 2 * kt, K2 = 2 * K;
+    const int64_t tiles = nseg * kt;
     f32x4 ra[A_LD], rb[B_LD];
 
-    auto chunk = [&](const float *p, int64_t k) {
+    auto chunk = [&](const float *p, int64_t k, bool vec) {
         f32x4 v = {0.f, 0.f, 0.f, 0.f};
-        if (k + 3 < K) {
+        if (vec && k + 3 < K) {
             v = *(const f32x4 *)p;
+        } else if (k + 3 < K) {
+            v.x = p[0];
+            v.y = p[1];
+            v.z = p[2];
+            v.w = p[3];
         } else {
             if (k < K) v.x = p[0];
             if (k + 1 < K) v.y = p[1];
@@ -135,13 +140,13 @@ __global__ void __launch_bounds__(256) k_combine_f32(const float *__restrict__ A
         for (int s = 0; s < A_LD; ++s) {
             const int c = tid + 256 * s;
             const int64_t row = m0 + c / CH, k = k0 + (c % CH) * 4;
-            ra[s] = (c < A_CH && row < M) ? chunk(A + row * lda + k, k) : f32x4{0.f, 0.f, 0.f, 0.f};
+            ra[s] = (c < A_CH && row < M) ? chunk(A + row * lda + k, k, true) : f32x4{0.f, 0.f, 0.f, 0.f};
         }
 #pragma unroll
         for (int s = 0; s < B_LD; ++s) {
             const int c = tid + 256 * s;
             const int64_t n = n0 + c / CH, k = k0 + (c % CH) * 4;
-            rb[s] = (c < B_CH && n < N) ? chunk(WT + n * K2 + (seg ? K : 0) + k, k) : f32x4{0.f, 0.f, 0.f, 0.f};
+            rb[s] = (c < B_CH && n < N) ? chunk(WT + n * ldb + (seg ? K : 0) + k, k, bvec) : f32x4{0.f, 0.f, 0.f, 0.f};
         }
     };
     auto stash = [&](int buf) {
@@ -609,8 +614,8 @@ static void launch_main(const void *self, int64_t ld_self, const void *agg, int6
         }
         KernelTimer tk(label, s);
         hipLaunchKernelGGL((k_combine_f32<BM, BN, WM, WN, BKF>), grid, dim3(256), 0, s, (const float *)self, ld_self,
-                           (const float *)agg, ld_agg, m, m_dev, k, (const float *)wt, n, (int)relu, (float *)out,
-                           ld_out);
+                           (const float *)agg, ld_agg, m, m_dev, k, (const float *)wt, 2 * k, 1, 2, n, (int)relu,
+                           (float *)out, ld_out);
     } else {
         uint16_t *wt = g_wt.buf.as<uint16_t>();
         {
@@ -696,6 +701,26 @@ void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t 
                                (const uint16_t *)w, d_out, (int)relu, (float *)out, ld_out);
     } else {
         ch.fn(self, ld_self, agg, ld_agg, m, m_dev, d_in, w, d_out, bf16, relu, out_bf16, out, ld_out, s, label);
+    }
+    GNNAV_HIP(hipGetLastError());
+}
+
+// out[M x N] = A[M x K] * B^T with B stored [N][ldb] (row n holds column n of
+// the product's right operand along k): the layout of a row-major weight
+// matrix read backwards, dX = dZ * W^T.  fp32, one segment, no activation.
+void launch_matmul_bt(const float *a, int64_t lda, int64_t m, const int32_t *m_dev, int64_t k, const float *b,
+                      int64_t ldb, int64_t n, float *out, int64_t ld_out, hipStream_t s, const char *label) {
+    if (m <= 0 || n <= 0) return;
+    const int bvec = (((uintptr_t)b & 15u) == 0) && ldb % 4 == 0;
+    KernelTimer t(label, s);
+    if (n <= 64) {
+        const int64_t nrow = (m + 63) / 64, ncol = (n + 63) / 64;
+        hipLaunchKernelGGL((k_combine_f32<64, 64, 2, 2, 32>), dim3((unsigned)(((nrow + 7) / 8) * 8 * ncol)), dim3(256),
+                           0, s, a, lda, a, lda, m, m_dev, k, b, ldb, bvec, 1, n, 0, out, ld_out);
+    } else {
+        const int64_t nrow = (m + 63) / 64, ncol = (n + 127) / 128;
+        hipLaunchKernelGGL((k_combine_f32<64, 128, 2, 2, 32>), dim3((unsigned)(((nrow + 7) / 8) * 8 * ncol)), dim3(256),
+                           0, s, a, lda, a, lda, m, m_dev, k, b, ldb, bvec, 1, n, 0, out, ld_out);
     }
     GNNAV_HIP(hipGetLastError());
 }

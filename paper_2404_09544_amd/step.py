@@ -8,6 +8,10 @@ gnnav_gather_n (row count read on the device) -> gnnav_sage_forward, all on
 one stream with no host synchronisation; ``finish`` waits and returns the
 logits.  Buffers are sized once from the Eq. 12 capacity bounds.
 
+``MiniBatchStep.train`` is a training iteration (fp32): the same sampling
+and gather, then gnnav_sage_train_step (forward, softmax cross-entropy over
+F_0, backward, SGD on the step's weights in place).
+
 ``Pipeline`` runs consecutive batches on alternating streams, each with its
 own step (blocks, gathered rows, logits), so batch b+1's sampling and
 host-link gather overlap batch b's aggregation and combine: the overlap
@@ -21,7 +25,7 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from . import Blocks, Cache, Graph, gather, gather_n, sage_forward, sample, sample_async
+from . import Blocks, Cache, Graph, gather, gather_n, sage_forward, sage_train_step, sample, sample_async
 
 
 def to_device_weights(ws, dtype: str):
@@ -47,6 +51,7 @@ class MiniBatchStep:
         self.h0 = torch.empty((0, self.ld), dtype=self._tdt, device="cuda")
         self.logits = torch.empty((0, self.dims[-1]), dtype=torch.float32, device="cuda")
         self.counts = torch.zeros(3, dtype=torch.int64, device="cuda")
+        self.loss = torch.zeros(1, dtype=torch.float32, device="cuda")
         self.sizes = None
         self._seeds = None
         self._stream = None
@@ -86,6 +91,44 @@ class MiniBatchStep:
         sage_forward(self.blocks, self.h0, self.weights, self.dims, self.dtype, self.logits, st)
         self.sizes = None
 
+    # ------------------------------------------------------------ train
+    def _inputs(self, seeds_dev, rng_seed: int, async_mode: bool, st):
+        """Sample and gather F_L's rows into h0 (on stream st)."""
+        if async_mode:
+            self._seeds = seeds_dev
+            self._stream = st
+            sample_async(self.graph, seeds_dev, self.fanouts, rng_seed, self.blocks, st)
+            sizes_ptr, bounds = self.blocks.device_sizes(self.L)
+            self._grow(bounds[-1], bounds[0], st)
+            gather_n(self.cache, self.blocks.nodes_ptr(), sizes_ptr + 4 * self.L, bounds[-1], self.h0,
+                     self.counts, st)
+            self.sizes = None
+        else:
+            sample(self.graph, seeds_dev, self.fanouts, rng_seed, self.blocks, st)
+            sizes, nodes_ptr = self.blocks.sizes()
+            self.sizes = sizes
+            self._grow(sizes[-1], sizes[0])
+            gather(self.cache, nodes_ptr, sizes[-1], self.h0, self.counts, st)
+
+    def _train_tail(self, labels_dev, lr: float, grads, st):
+        sage_train_step(self.blocks, self.h0, self.weights, self.dims, labels_dev, lr, self.logits, self.loss,
+                        grads, st)
+
+    def train(self, seeds_dev, rng_seed: int, labels_dev, lr: float, grads=None, async_mode: bool = False,
+              stream=None):
+        """One training iteration; labels_dev: device int32 label of every vertex.
+
+        Sync mode returns the logits view [|F_0|, classes]; async mode
+        returns None (call ``finish`` for the view).  The loss lands in
+        ``self.loss``; ``grads`` (optional device tensors) receive dW_l.
+        """
+        if self.dtype != "f32":
+            raise ValueError("training runs in fp32")
+        st = stream if stream is not None else torch.cuda.current_stream()
+        self._inputs(seeds_dev, rng_seed, async_mode, st)
+        self._train_tail(labels_dev, lr, grads, st)
+        return None if async_mode else self.logits[:self.sizes[0]]
+
     def finish(self):
         """Wait for the enqueued batch; returns its logits view [|F_0|, classes]."""
         self.blocks.sync(self._stream)
@@ -104,6 +147,7 @@ class Pipeline:
         self.streams = [torch.cuda.Stream() for _ in range(depth)]
         self.depth = depth
         self.count = 0
+        self._updated = None
 
     def enqueue(self, seeds_dev, rng_seed: int):
         """Enqueue the next batch; returns the slot it runs in."""
@@ -111,6 +155,23 @@ class Pipeline:
         self.slots[k].enqueue(seeds_dev, rng_seed, self.streams[k])
         self.count += 1
         return self.slots[k]
+
+    def enqueue_train(self, seeds_dev, rng_seed: int, labels_dev, lr: float):
+        """Enqueue the next training iteration.  Its sampling and gather may
+        run alongside the previous batch; its forward waits for the previous
+        batch's weight update (the weights are shared)."""
+        k = self.count % self.depth
+        slot, st = self.slots[k], self.streams[k]
+        if slot.dtype != "f32":
+            raise ValueError("training runs in fp32")
+        slot._inputs(seeds_dev, rng_seed, True, st)
+        if self._updated is not None:
+            st.wait_event(self._updated)
+        slot._train_tail(labels_dev, lr, None, st)
+        self._updated = torch.cuda.Event()
+        self._updated.record(st)
+        self.count += 1
+        return slot
 
     def synchronize(self):
         for s in self.streams:

@@ -35,7 +35,7 @@ def assert_rows_close(gpu, ref, tol: float, what: str = "", floor=None):
     if diff.size == 0:
         return 0.0
     med = float(np.median(norm)) if np.any(norm > 0) else 0.0
-    small = norm < 1e-3 * med
+    small = norm <= 1e-3 * med
     rel = np.where(small, 0.0, diff / np.where(small, 1.0, norm))
     worst = float(rel.max())
     assert worst <= tol, f"{what}: worst per-row relative error {worst:.3e} > {tol:.1e} (row {int(rel.argmax())})"
