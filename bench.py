@@ -101,6 +101,69 @@ def link_calibration(G, cache, wl, torch):
     return out
 
 
+def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_weights, MiniBatchStep, Pipeline):
+    """Training iterations on the same batches: one stream with every kernel
+    timed, then the two-stream pipeline (each forward waits for the
+    previous update).  Starts from the bench's initial weights."""
+    labels = torch.from_numpy(wl.labels()).cuda()
+    n_b = args.warmup + args.steps
+    L = wl.L
+    wtrain = to_device_weights(ws, "f32")
+    step = MiniBatchStep(g, c, wtrain, wl.dims, wl.fanouts, "f32")
+    stream = torch.cuda.current_stream()
+    losses = []
+    for b in range(args.warmup):
+        step.train(seeds_dev[b], wl.rng_seed(b), labels, args.lr, async_mode=True, stream=stream)
+    torch.cuda.synchronize()
+    G.profile_start()
+    loss_hist = torch.zeros(n_b, dtype=torch.float32, device="cuda")
+    t0 = time.perf_counter()
+    for b in range(args.warmup, n_b):
+        step.train(seeds_dev[b], wl.rng_seed(b), labels, args.lr, async_mode=True, stream=stream)
+        loss_hist[b].copy_(step.loss[0])
+    torch.cuda.synchronize()
+    seq = time.perf_counter() - t0
+    prof = G.profile_stop()
+    losses = loss_hist[args.warmup:].cpu().numpy()
+    pipe = Pipeline(g, c, wtrain, wl.dims, wl.fanouts, "f32", depth=args.depth)
+    for b in range(args.warmup):
+        pipe.enqueue_train(seeds_dev[b], wl.rng_seed(b), labels, args.lr)
+    pipe.synchronize()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for b in range(args.warmup, n_b):
+        pipe.enqueue_train(seeds_dev[b], wl.rng_seed(b), labels, args.lr)
+    pipe.synchronize()
+    torch.cuda.synchronize()
+    piped = time.perf_counter() - t0
+    log(f"train: sequential {seq * 1e3 / args.steps:.3f} ms/step, pipelined {piped * 1e3 / args.steps:.3f} ms/step, "
+        f"loss {losses[0]:.4f} -> {losses[-1]:.4f}")
+    # algorithmic work of the backward kernels from the measured sizes
+    work = {}
+    for sz in sizes_hist:
+        for l in range(1, L + 1):
+            hb = L - l + 1
+            n_dst, n_src = sz[hb - 1], sz[hb]
+            din, dout = wl.dims[l - 1], wl.dims[l]
+            work[f"wgrad.l{l}"] = work.get(f"wgrad.l{l}", 0.0) + 2.0 * n_dst * (2 * din) * dout
+            if l > 1:
+                work[f"bwd_gemm.l{l}"] = work.get(f"bwd_gemm.l{l}", 0.0) + 2.0 * 2 * n_dst * dout * din
+    kernels = {}
+    for name, (launches, ms) in prof.items():
+        k = {"launches": launches, "total_ms": round(ms, 4), "avg_us": round(ms * 1e3 / max(launches, 1), 3)}
+        if name in work:
+            tf = work[name] / (ms * 1e-3) / 1e12
+            k.update({"bound": "mfma", "achieved": round(tf, 2), "peak": MFMA_PEAK_TFLOPS["f32"], "unit": "TFLOP/s",
+                      "frac": round(tf / MFMA_PEAK_TFLOPS["f32"], 4)})
+        kernels[name] = k
+    return {"metric": "trained seed nodes/sec (sample+gather+forward+softmax-CE+backward+SGD)",
+            "value": round(wl.batch * args.steps / piped, 2), "unit": "seeds/s",
+            "ms_per_step": round(piped * 1e3 / args.steps, 4),
+            "value_sequential": round(wl.batch * args.steps / seq, 2), "lr": args.lr,
+            "loss_first": round(float(losses[0]), 6), "loss_last": round(float(losses[-1]), 6),
+            "kernels": kernels}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -115,6 +178,8 @@ def main():
                     help="fifo: admit each batch's misses into a ring over the last cache slots")
     ap.add_argument("--dynamic-fraction", type=float, default=1.0,
                     help="share of the cache slots in the FIFO ring (with --cache-policy fifo)")
+    ap.add_argument("--no-train", action="store_true", help="skip the training leg")
+    ap.add_argument("--lr", type=float, default=0.01, help="SGD step of the training leg")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (scales rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
@@ -279,6 +344,12 @@ def main():
         roofline = {"kernel": dom, "bound": k["bound"], "achieved": k["achieved"], "peak": k["peak"],
                     "unit": k["unit"], "frac": k["frac"], "traffic": traffic_for(dom, wl.name)}
 
+    # ---- training leg: sample + gather + forward + loss + backward + SGD ----
+    train = None
+    if not args.no_train and wl.dtype == "f32":
+        train = train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_weights, MiniBatchStep,
+                          Pipeline)
+
     # ---- CPU baseline: the oracle on a bounded sample of the same batches --
     cpu = None
     if not args.no_cpu_baseline:
@@ -331,6 +402,7 @@ def main():
         "cpu_baseline": cpu,
         "kernels": kernels,
         "eq4": eq4,
+        "train": train,
         "host_link_calibration": link,
         "batch_stats": {"mean_frontier_sizes": mean_sizes, "hit_rate": round(hit_rate, 4),
                         "hit_rate_sequential": round(float(seq_counts[:, 0].sum() / max(seq_counts[:, :2].sum(), 1)), 4),

@@ -99,3 +99,44 @@ def test_full_batch(G, name):
             say(name, f"r={r} batch {b}: sizes {sizes} hits/misses {counts.tolist()} "
                       f"({time.perf_counter() - t:.1f}s)")
         c.close()
+
+
+TRAIN_FULL = ["chunglu-169k-d128", "chunglu-233k-d602", "chunglu-2450k-d100"]
+
+
+@pytest.mark.parametrize("name", TRAIN_FULL)
+def test_full_train_step(G, name):
+    """One training iteration at full size (the bench's train leg, async):
+    loss and every layer's weight gradient against the oracle's train step,
+    with the absolute-value sums as each gradient row's rounding scale."""
+    import torch
+    from paper_2404_09544_amd.step import MiniBatchStep, to_device_weights
+    wl, _, _, csr, g = load(G, name)
+    feats = wl.features()
+    ws = wl.weights()
+    labels = wl.labels()
+    t = time.perf_counter()
+    c = G.Cache(g, feats, wl.dtype, wl.cfg["cache"], store_on_device=wl.cfg["store_on_device"])
+    step = MiniBatchStep(g, c, to_device_weights(ws, wl.dtype), wl.dims, wl.fanouts, wl.dtype)
+    grads = [torch.zeros((2 * wl.dims[l], wl.dims[l + 1]), device="cuda") for l in range(wl.L)]
+    b, lr = 3, 0.05
+    seeds = wl.seeds(b)
+    step.train(torch.from_numpy(seeds).cuda(), wl.rng_seed(b), torch.from_numpy(labels).cuda(), lr, grads=grads,
+               async_mode=True)
+    step.finish()
+    loss = float(step.loss.cpu().numpy()[0])
+    got = [x.cpu().numpy() for x in grads]
+    say(name, f"GPU train step done ({time.perf_counter() - t:.1f}s)")
+    ref_b = O.sample_blocks(csr, seeds, wl.fanouts, wl.rng_seed(b))
+    H0 = feats[ref_b.nodes].astype(np.float64)
+    y = labels[ref_b.nodes[:ref_b.sizes[0]]]
+    Wd = [O.to_f64(w, wl.dtype) for w in ws]
+    logits, trace = O.sage_forward(ref_b, H0, Wd, keep=True)
+    rloss, dZ = O.softmax_xent(logits, y)
+    rdW = O.sage_backward(ref_b, H0, Wd, trace, dZ)
+    floors = O.sage_backward(ref_b, H0, Wd, trace, dZ, abs_scale=True)
+    say(name, f"oracle train step done ({time.perf_counter() - t:.1f}s), loss {rloss:.6f} vs {loss:.6f}")
+    assert loss == pytest.approx(rloss, rel=FP32_TOL)
+    for l in range(wl.L):
+        assert_rows_close(got[l], rdW[l], FP32_TOL, f"{name} dW{l + 1}", floor=np.linalg.norm(floors[l], axis=1))
+    c.close()
