@@ -55,7 +55,11 @@ def _load():
     lib.oracle_below.restype = u32
     lib.oracle_sample_node.argtypes = [P, P, i64, i32, u64, u32, P]
     lib.oracle_sample_node.restype = i64
-    lib.oracle_sample_blocks.argtypes = [i64, P, P, P, i64, P, i32, u64, P, P, P, P, P]
+    lib.oracle_sample_blocks.argtypes = [i64, P, P, P, i64, P, i32, u64, P, u32, P, P, P, P, P]
+    lib.oracle_sample_node_biased.argtypes = [P, P, i64, i32, u64, u32, P, u32, P]
+    lib.oracle_sample_node_biased.restype = i64
+    lib.oracle_below64.argtypes = [u32, u64]
+    lib.oracle_below64.restype = u64
     lib.oracle_sample_blocks.restype = i32
     lib.oracle_gather.argtypes = [i64, P, i64, P, P, i64, P, P, P]
     lib.oracle_gather.restype = None
@@ -169,8 +173,24 @@ def hop_bounds(n: int, n_seeds: int, fanouts, max_degree: int):
     return eb, nb
 
 
-def sample_blocks(csr: CSR, seeds, fanouts, rng_seed: int) -> Blocks:
+def sample_node_biased(csr: CSR, v: int, k: int, rng_seed: int, hop: int, slot_map, eta: int) -> np.ndarray:
+    """O5b: locality-biased selection (cached neighbours weighted eta)."""
+    deg = int(csr.row_ptr[v + 1] - csr.row_ptr[v])
+    out = np.empty(max(1, deg), np.int32)
+    sm = _i32(slot_map)
+    c = _load().oracle_sample_node_biased(_ptr(csr.row_ptr), _ptr(csr.col), v, k, rng_seed, hop, _ptr(sm),
+                                          int(eta), _ptr(out))
+    return out[:c].copy()
+
+
+def below64(x: int, b: int) -> int:
+    return int(_load().oracle_below64(x, b))
+
+
+def sample_blocks(csr: CSR, seeds, fanouts, rng_seed: int, bias_slot_map=None, eta: int = 1) -> Blocks:
+    """O6 expansion; with bias_slot_map every hop uses O5b with that map."""
     seeds = _i32(seeds)
+    bias = None if bias_slot_map is None else _i32(bias_slot_map)
     fan = _i32(fanouts)
     L = len(fanouts)
     maxdeg = int(csr.degrees().max()) if csr.n > 0 else 0
@@ -183,7 +203,7 @@ def sample_blocks(csr: CSR, seeds, fanouts, rng_seed: int) -> Blocks:
     PP = C.c_void_p * max(1, L)
     rc = _load().oracle_sample_blocks(
         csr.n, _ptr(csr.row_ptr), _ptr(csr.col), _ptr(seeds), seeds.size, _ptr(fan), L,
-        rng_seed, _ptr(nodes), _ptr(sizes), PP(*[_ptr(a) for a in indptr]),
+        rng_seed, _ptr(bias), int(eta), _ptr(nodes), _ptr(sizes), PP(*[_ptr(a) for a in indptr]),
         PP(*[_ptr(a) for a in nbrs]), PP(*[_ptr(a) for a in indices]))
     if rc != 0:
         raise ValueError("seed outside [0, n)")

@@ -193,6 +193,86 @@ int64_t oracle_sample_node(const int64_t *row_ptr, const int32_t *col, int64_t v
     return k;
 }
 
+/* ----------------------------------------------------------------- O5b ---
+ * Locality-biased neighbour selection: the neighbour-selection probability
+ * of Eq. 2 made a function of data locality, p(eta), preferring vertices
+ * already in the device cache.  Reading: successive sampling without
+ * replacement (k picks, each among the not-yet-picked neighbours with
+ * probability proportional to its weight) with weight eta for a cached
+ * neighbour (slot_map >= 0) and 1 for an uncached one; eta = 1 is uniform.
+ * With two weight classes successive sampling splits into
+ *   1. the class of each pick j = 0..k-1, in order: with c_r cached and u_r
+ *      uncached neighbours left, t = floor(x * (eta*c_r + u_r) / 2^32) for
+ *      x = Philox word 1 of counter (j, v, hop); cached when t < eta*c_r;
+ *   2. which members of each class: a uniform subset of the class's size,
+ *      by Floyd's algorithm over the class's neighbours in CSR order, with
+ *      Philox word 2 (cached class) or word 3 (uncached class) of counter
+ *      (j', v, hop) for its j'-th step.
+ * Output: the cached picks in Floyd order, then the uncached picks.
+ * deg <= k (or k < 0): the whole row, as in O5.                           */
+static uint32_t oracle_word(uint64_t rng_seed, uint32_t hop, int64_t v, uint32_t j, int w) {
+    uint32_t ctr[4] = {j, (uint32_t)((uint64_t)v & 0xffffffffu), (uint32_t)((uint64_t)v >> 32), hop};
+    uint32_t key[2] = {(uint32_t)(rng_seed & 0xffffffffu), (uint32_t)(rng_seed >> 32)};
+    uint32_t out[4];
+    oracle_philox4x32_10(ctr, key, out);
+    return out[w];
+}
+
+/* floor(x * b / 2^32) for b up to 2^64 (exact, 128-bit product) */
+uint64_t oracle_below64(uint32_t x, uint64_t b) {
+    return (uint64_t)(((unsigned __int128)x * (unsigned __int128)b) >> 32);
+}
+
+/* Floyd's k-subset of [0, size) with draws from Philox word w; writes the
+ * chosen indices in step order. */
+static void oracle_floyd(int64_t size, int32_t k, uint64_t rng_seed, uint32_t hop, int64_t v, int w,
+                         int64_t *taken) {
+    for (int32_t j = 0; j < k; ++j) {
+        int64_t m = size - k + j;
+        int64_t t = oracle_below(oracle_word(rng_seed, hop, v, (uint32_t)j, w), (uint32_t)(m + 1));
+        int seen = 0;
+        for (int32_t i = 0; i < j; ++i)
+            if (taken[i] == t) seen = 1;
+        taken[j] = seen ? m : t;
+    }
+}
+
+int64_t oracle_sample_node_biased(const int64_t *row_ptr, const int32_t *col, int64_t v, int32_t k,
+                                  uint64_t rng_seed, uint32_t hop, const int32_t *slot_map, uint32_t eta,
+                                  int32_t *out) {
+    int64_t start = row_ptr[v];
+    int64_t deg = row_ptr[v + 1] - start;
+    if (k < 0 || deg <= k) {
+        for (int64_t j = 0; j < deg; ++j) out[j] = col[start + j];
+        return deg;
+    }
+    int64_t *cached = (int64_t *)malloc((size_t)deg * sizeof(int64_t));
+    int64_t *uncached = (int64_t *)malloc((size_t)deg * sizeof(int64_t));
+    int64_t *taken = (int64_t *)malloc((size_t)(k > 0 ? k : 1) * sizeof(int64_t));
+    int64_t c = 0, u = 0;
+    for (int64_t i = 0; i < deg; ++i) {
+        if (slot_map[col[start + i]] >= 0) cached[c++] = start + i;
+        else uncached[u++] = start + i;
+    }
+    int32_t kc = 0;
+    int64_t cr = c, ur = u;
+    for (int32_t j = 0; j < k; ++j) {
+        uint64_t heavy = (uint64_t)eta * (uint64_t)cr;
+        uint64_t t = oracle_below64(oracle_word(rng_seed, hop, v, (uint32_t)j, 1), heavy + (uint64_t)ur);
+        if (t < heavy) { kc++; cr--; }
+        else ur--;
+    }
+    int32_t ku = k - kc;
+    oracle_floyd(c, kc, rng_seed, hop, v, 2, taken);
+    for (int32_t j = 0; j < kc; ++j) out[j] = col[cached[taken[j]]];
+    oracle_floyd(u, ku, rng_seed, hop, v, 3, taken);
+    for (int32_t j = 0; j < ku; ++j) out[kc + j] = col[uncached[taken[j]]];
+    free(cached);
+    free(uncached);
+    free(taken);
+    return k;
+}
+
 /* ------------------------------------------------------------------ O6 ---
  * L-hop expansion with relabelling.
  *   F_0 = seeds with repeats removed (first occurrence kept).
@@ -205,11 +285,14 @@ int64_t oracle_sample_node(const int64_t *row_ptr, const int32_t *col, int64_t v
  * |F_h|.  Per hop h (1-based), indptr[h-1] holds |F_(h-1)|+1 entries and
  * nbrs[h-1] / indices[h-1] hold E_h entries; caller sizes them to the
  * bounds E_h <= |F_(h-1)| * k_h and |F_h| <= |F_(h-1)| * (1 + k_h).
+ * With bias_slot_map != NULL every hop uses the locality-biased selection
+ * of O5b with that cache map and eta.
  * Returns 0, or -1 when a seed lies outside [0, n).                      */
 int32_t oracle_sample_blocks(int64_t n, const int64_t *row_ptr, const int32_t *col,
                              const int32_t *seeds, int64_t n_seeds, const int32_t *fanouts,
-                             int32_t n_hops, uint64_t rng_seed, int32_t *nodes, int64_t *sizes,
-                             int32_t **indptr, int32_t **nbrs, int32_t **indices) {
+                             int32_t n_hops, uint64_t rng_seed, const int32_t *bias_slot_map, uint32_t eta,
+                             int32_t *nodes, int64_t *sizes, int32_t **indptr, int32_t **nbrs,
+                             int32_t **indices) {
     int64_t *pos = (int64_t *)malloc((size_t)(n > 0 ? n : 1) * sizeof(int64_t));
     for (int64_t v = 0; v < n; ++v) pos[v] = -1;
     int64_t cnt = 0;
@@ -224,8 +307,12 @@ int32_t oracle_sample_blocks(int64_t n, const int64_t *row_ptr, const int32_t *c
         int32_t *ip = indptr[h - 1], *nb = nbrs[h - 1], *ix = indices[h - 1];
         for (int64_t i = 0; i < n_prev; ++i) {
             ip[i] = (int32_t)e;
-            e += oracle_sample_node(row_ptr, col, nodes[i], fanouts[h - 1], rng_seed,
-                                    (uint32_t)(h - 1), nb + e);
+            if (bias_slot_map)
+                e += oracle_sample_node_biased(row_ptr, col, nodes[i], fanouts[h - 1], rng_seed,
+                                               (uint32_t)(h - 1), bias_slot_map, eta, nb + e);
+            else
+                e += oracle_sample_node(row_ptr, col, nodes[i], fanouts[h - 1], rng_seed,
+                                        (uint32_t)(h - 1), nb + e);
         }
         ip[n_prev] = (int32_t)e;
         for (int64_t p = 0; p < e; ++p) {

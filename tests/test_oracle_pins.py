@@ -638,3 +638,110 @@ def test_train_step_decreases_loss_and_applies_sgd():
         assert np.array_equal(w2, w - lr * g)
     # a small step along the negative gradient lowers the loss
     assert _loss_of(blk, H0, new, y) < loss
+
+
+# ------------------------------------------- locality-biased selection ---
+
+def _exact_successive(weights, k):
+    """Probability of every k-subset under successive sampling without
+    replacement (each pick proportional to weight among those left), by
+    enumerating the ordered pick sequences."""
+    idx = range(len(weights))
+    probs = {}
+    for seq in itertools.permutations(idx, k):
+        p, left = 1.0, float(sum(weights))
+        for i in seq:
+            p *= weights[i] / left
+            left -= weights[i]
+        key = frozenset(seq)
+        probs[key] = probs.get(key, 0.0) + p
+    return probs
+
+
+def _chi2_against(csr, hub, slot, eta, k, probs, trials, hop=0):
+    counts = {s: 0 for s in probs}
+    for t in range(trials):
+        s = O.sample_node_biased(csr, hub, k, (321 << 32) | t, hop, slot, eta)
+        counts[frozenset(s.tolist())] += 1
+    return sum((counts[s] - trials * p) ** 2 / (trials * p) for s, p in probs.items())
+
+
+@pytest.mark.parametrize("eta,k,cached", [(1, 3, {1, 4}), (3, 2, {2, 5}), (5, 3, {1, 2, 3}), (40, 2, {6})])
+def test_biased_selection_is_weighted_successive_sampling(eta, k, cached):
+    """Subset frequencies of the biased selector against the exact
+    probabilities of successive weighted sampling (eta = 1: uniform)."""
+    csr = _star(7)                               # hub 0, neighbours 1..6
+    slot = np.full(7, -1, np.int32)
+    for v in cached:
+        slot[v] = 0
+    weights = [eta if v in cached else 1 for v in range(1, 7)]
+    probs = {frozenset(v + 1 for v in s): p for s, p in _exact_successive(weights, k).items()}
+    trials = 30000
+    chi2 = _chi2_against(csr, 0, slot, eta, k, probs, trials)
+    dof = len(probs) - 1
+    # P(chi2 > dof + 6 sqrt(2 dof) + 10) is below 1e-4 for these dof
+    assert chi2 < dof + 6 * math.sqrt(2 * dof) + 10, (chi2, dof)
+    if eta == 1:
+        assert all(abs(p - 1 / len(probs)) < 1e-12 for p in probs.values())
+
+
+def test_biased_selection_properties():
+    n, u, v = W.random_graph(n=80, m=900, seed=3)
+    csr = O.build_csr(n, u, v)
+    _, slot, _ = O.rank_cache(csr, 0.3)
+    for node in range(n):
+        row = csr.col[csr.row_ptr[node]:csr.row_ptr[node + 1]]
+        for k, eta in itertools.product([0, 1, 4, 9, 64, -1], [1, 7, 65536]):
+            s = O.sample_node_biased(csr, node, k, 55, 2, slot, eta)
+            want = len(row) if k < 0 else min(len(row), k)
+            assert s.size == want
+            assert len(set(s.tolist())) == s.size
+            assert set(s.tolist()) <= set(row.tolist())
+            if k < 0 or len(row) <= k:
+                assert s.tolist() == row.tolist()
+            else:
+                flags = (slot[s] >= 0).tolist()
+                assert flags == sorted(flags, reverse=True), "cached picks come first"
+            assert np.array_equal(s, O.sample_node_biased(csr, node, k, 55, 2, slot, eta))
+
+
+def test_biased_selection_strong_bias_takes_cached():
+    """With eta = 65536 and at least k cached neighbours, an uncached pick
+    needs a class draw below u / (eta c + u): rare."""
+    csr = _star(101)
+    slot = np.full(101, -1, np.int32)
+    slot[1:31] = np.arange(30)                   # 30 of 100 neighbours cached
+    k, trials, uncached = 10, 2000, 0
+    for t in range(trials):
+        s = O.sample_node_biased(csr, 0, k, t, 1, slot, 65536)
+        uncached += int((slot[s] < 0).sum())
+    # expected uncached picks per trial is about k * 70 / (65536 * 21) ~ 5e-4
+    assert uncached <= 10
+
+
+def test_below64_exact():
+    rng = np.random.default_rng(4)
+    for _ in range(2000):
+        x = int(rng.integers(0, 2 ** 32))
+        b = int(rng.integers(1, 2 ** 63))
+        assert O.below64(x, b) == (x * b) >> 32
+    assert O.below64(2 ** 32 - 1, 2 ** 48) == ((2 ** 32 - 1) * 2 ** 48) >> 32
+
+
+def test_biased_blocks_consistent():
+    n, u, v = W.random_graph(n=400, m=5000, seed=6)
+    csr = O.build_csr(n, u, v)
+    _, slot, _ = O.rank_cache(csr, 0.25)
+    seeds = W.epoch_permutation(n)[:40]
+    blk = O.sample_blocks(csr, seeds, [5, 4], 9, bias_slot_map=slot, eta=8)
+    for h in range(2):
+        ip, nb, ix = blk.indptr[h], blk.nbrs[h], blk.indices[h]
+        assert np.array_equal(blk.nodes[ix], nb)
+        for i in range(blk.sizes[h]):
+            node = blk.nodes[i]
+            want = O.sample_node_biased(csr, int(node), [5, 4][h], 9, h, slot, 8)
+            assert np.array_equal(nb[ip[i]:ip[i + 1]], want)
+    # the bias raises the share of sampled edges that land on cached vertices
+    plain = O.sample_blocks(csr, seeds, [5, 4], 9)
+    share = lambda b: np.mean(np.concatenate([slot[x] >= 0 for x in b.nbrs]))
+    assert share(blk) > share(plain)
