@@ -343,6 +343,31 @@ gnnav_status gnnav_weight_grad(const float *self_dev, int64_t ld_self, const flo
                                int64_t ld_agg, int64_t m, int64_t d_in, const float *dz_dev,
                                int64_t ld_dz, int64_t d_out, float *dw_dev, void *stream);
 
+/* -------------------------------------------------- locality-biased sampler ---
+ * gnnav_sample with the neighbour-selection probability made a function of
+ * data locality, p(eta) (Section 3.2, the sampler abstraction that
+ * reproduces cache-aware samplers): a neighbour held in `cache` (slot map
+ * >= 0) weighs eta, any other 1, and for deg(v) > k the k picks are made by
+ * successive sampling without replacement with those weights (eta = 1 is
+ * uniform; a large eta takes cached neighbours first).  Done as: for pick
+ * j = 0..k-1 in order, with c_r cached and u_r uncached neighbours left,
+ * t = floor(x * (eta*c_r + u_r) / 2^32) with x = Philox4x32-10 word 1 of
+ * the counter of gnnav_sample (j, lo32 v, hi32 v, h-1); the pick is cached
+ * when t < eta*c_r.  Then a uniform subset of each class by Floyd's
+ * selection over the class's neighbours in CSR order, step j using word 2
+ * (cached class) or word 3 (uncached class) of counter (j, v, h-1).  Each
+ * row lists its cached picks (Floyd order), then the uncached ones.
+ * deg(v) <= k takes the whole row as gnnav_sample does.  Frontier union,
+ * blocks and sizes are exactly as gnnav_sample.  async != 0: no final
+ * synchronisation (as gnnav_sample_async).  With a FIFO cache the slot map
+ * is read after the cache's last update (ordered by its event).
+ * Errors: as gnnav_sample; E_INVALID also for a NULL cache, a cache of
+ * another graph, eta outside [1, 65536], or a fanout above 64.          */
+gnnav_status gnnav_sample_biased(const gnnav_graph *g, const gnnav_cache *cache, uint32_t eta,
+                                 const int32_t *seeds_dev, int64_t n_seeds, const int32_t *fanouts,
+                                 int32_t n_hops, uint64_t rng_seed, gnnav_blocks *blocks,
+                                 int32_t async, void *stream);
+
 /* ------------------------------------------------------------ profiling ---
  * Per-kernel timing with HIP events recorded around every kernel launch on
  * the stream it is launched on.  profile_start clears the table and turns

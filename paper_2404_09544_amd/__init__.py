@@ -29,7 +29,7 @@ EXPORTS = [
     "gnnav_last_error", "gnnav_abi_version", "gnnav_build_csr", "gnnav_graph_info",
     "gnnav_graph_csr_host", "gnnav_graph_free", "gnnav_build_cache", "gnnav_cache_info",
     "gnnav_cache_slot_map_host", "gnnav_cache_contents_host", "gnnav_cache_set_policy", "gnnav_cache_free", "gnnav_blocks_create", "gnnav_blocks_free",
-    "gnnav_sample", "gnnav_sample_async", "gnnav_blocks_sync", "gnnav_blocks_device_sizes",
+    "gnnav_sample", "gnnav_sample_async", "gnnav_sample_biased", "gnnav_blocks_sync", "gnnav_blocks_device_sizes",
     "gnnav_blocks_hop", "gnnav_blocks_nodes", "gnnav_gather", "gnnav_gather_n",
     "gnnav_aggregate_mean", "gnnav_combine", "gnnav_sage_forward", "gnnav_sage_train_step",
     "gnnav_softmax_xent", "gnnav_aggregate_mean_backward", "gnnav_weight_grad", "gnnav_profile_start",
@@ -67,6 +67,7 @@ _sig = {
     "gnnav_blocks_free": ([P], None),
     "gnnav_sample": ([P, P, i64, P, i32, u64, P, P], i32),
     "gnnav_sample_async": ([P, P, i64, P, i32, u64, P, P], i32),
+    "gnnav_sample_biased": ([P, P, u32, P, i64, P, i32, u64, P, i32, P], i32),
     "gnnav_blocks_sync": ([P, P], i32),
     "gnnav_blocks_device_sizes": ([P, P, P], i32),
     "gnnav_gather_n": ([P, P, P, i64, P, i64, P, P], i32),
@@ -317,6 +318,16 @@ def sample_async(graph: Graph, seeds, fanouts, rng_seed: int, blocks: Blocks, st
     fan = np.ascontiguousarray(fanouts, dtype=np.int32)
     _check(_lib.gnnav_sample_async(graph._h, _dev_ptr(seeds), seeds.numel(), _np_ptr(fan), fan.size,
                                    int(rng_seed) & 0xFFFFFFFFFFFFFFFF, blocks._h, _stream(stream)))
+    return blocks
+
+
+def sample_biased(graph: Graph, cache: Cache, eta: int, seeds, fanouts, rng_seed: int, blocks: Blocks,
+                  async_: bool = False, stream=None):
+    """gnnav_sample_biased: cached neighbours weigh eta (eta = 1: uniform weights)."""
+    fan = np.ascontiguousarray(fanouts, dtype=np.int32)
+    _check(_lib.gnnav_sample_biased(graph._h, cache._h, int(eta), _dev_ptr(seeds), seeds.numel(), _np_ptr(fan),
+                                    fan.size, int(rng_seed) & 0xFFFFFFFFFFFFFFFF, blocks._h, int(bool(async_)),
+                                    _stream(stream)))
     return blocks
 
 

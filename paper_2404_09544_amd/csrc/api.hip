@@ -583,8 +583,19 @@ extern "C" void gnnav_blocks_free(gnnav_blocks *b) {
 
 // Enqueues the whole expansion on `s`; sizes stay in device memory.
 static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64_t n_seeds, const int32_t *fanouts,
-                       int32_t n_hops, uint64_t rng_seed, gnnav_blocks *b, hipStream_t s) {
+                           int32_t n_hops, uint64_t rng_seed, gnnav_blocks *b, hipStream_t s,
+                           const gnnav_cache *bias = nullptr, uint32_t eta = 1) {
     GNNAV_CHECK(g && b && fanouts, GNNAV_E_INVALID, "NULL graph, blocks or fanouts");
+    if (bias) {
+        GNNAV_CHECK(bias->n == g->n, GNNAV_E_INVALID, "the cache belongs to a graph of another size");
+        GNNAV_CHECK(eta >= 1 && eta <= 65536, GNNAV_E_INVALID, "eta outside [1, 65536]");
+        for (int h = 0; h < n_hops; ++h)
+            GNNAV_CHECK(fanouts[h] <= 64, GNNAV_E_INVALID, "biased sampling supports fanouts up to 64");
+        // a self-updating cache: read its slot map after the last update
+        auto *bc = const_cast<gnnav_cache *>(bias);
+        std::lock_guard<std::mutex> lk(bc->upd_mu);
+        if (bc->ring_n > 0 && bc->upd_recorded) GNNAV_HIP(hipStreamWaitEvent(s, bc->upd_done, 0));
+    }
     GNNAV_CHECK(n_hops >= 1 && n_hops <= kMaxHops, GNNAV_E_INVALID, "n_hops outside [1, 16]");
     GNNAV_CHECK(n_seeds >= 0, GNNAV_E_INVALID, "n_seeds < 0");
     GNNAV_CHECK(n_seeds == 0 || seeds_dev, GNNAV_E_INVALID, "seeds_dev is NULL");
@@ -630,7 +641,8 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
     for (int h = 1; h <= n_hops; ++h) {
         SampleHopArgs a{g->row_ptr.p, g->i64, g->col.as<int32_t>(), nodes, sz + kSizeN + h - 1,
                         b->indptr[h - 1].as<int32_t>(), b->nbrs[h - 1].as<int32_t>(), sz + kSizeE + h,
-                        fanouts[h - 1], rng_seed, (uint32_t)(h - 1), nb[h - 1], &b->scan};
+                        fanouts[h - 1], rng_seed, (uint32_t)(h - 1), nb[h - 1], &b->scan,
+                        bias ? bias->slot_map.as<int32_t>() : nullptr, eta};
         launch_count_scan(a, s);
         launch_sample_hop(a, s);
         DedupArgs dh{b->nbrs[h - 1].as<int32_t>(), 0, sz + kSizeE + h, eb[h], map, g->n, nodes,
@@ -676,6 +688,17 @@ extern "C" gnnav_status gnnav_sample_async(const gnnav_graph *g, const int32_t *
                                            const int32_t *fanouts, int32_t n_hops, uint64_t rng_seed,
                                            gnnav_blocks *b, void *stream) {
     return guarded([&] { sample_enqueue(g, seeds_dev, n_seeds, fanouts, n_hops, rng_seed, b, (hipStream_t)stream); });
+}
+
+extern "C" gnnav_status gnnav_sample_biased(const gnnav_graph *g, const gnnav_cache *cache, uint32_t eta,
+                                            const int32_t *seeds_dev, int64_t n_seeds, const int32_t *fanouts,
+                                            int32_t n_hops, uint64_t rng_seed, gnnav_blocks *b, int32_t async,
+                                            void *stream) {
+    return guarded([&] {
+        GNNAV_CHECK(cache, GNNAV_E_INVALID, "cache is NULL");
+        sample_enqueue(g, seeds_dev, n_seeds, fanouts, n_hops, rng_seed, b, (hipStream_t)stream, cache, eta);
+        if (!async) publish_sizes(b, (hipStream_t)stream);
+    });
 }
 
 extern "C" gnnav_status gnnav_blocks_sync(gnnav_blocks *b, void *stream) {

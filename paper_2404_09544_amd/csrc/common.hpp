@@ -146,6 +146,8 @@ struct SampleHopArgs {
     uint32_t hop;            // 0-based
     int64_t rows_bound;
     ScanState *scan;
+    const int32_t *bias_slot_map = nullptr;   // locality-biased selection when set
+    uint32_t eta = 1;
 };
 void launch_count_scan(const SampleHopArgs &a, hipStream_t s);
 void launch_sample_hop(const SampleHopArgs &a, hipStream_t s);

@@ -41,6 +41,30 @@ __device__ __forceinline__ uint32_t philox_word0(uint32_t c0, uint32_t c1, uint3
     return c0;
 }
 
+// All four output words (the biased selector uses words 1-3).
+__device__ __forceinline__ void philox4(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0, uint32_t k1,
+                                        uint32_t (&w)[4]) {
+    constexpr uint32_t kMulA = 0xD2511F53u, kMulB = 0xCD9E8D57u;
+    constexpr uint32_t kWeylA = 0x9E3779B9u, kWeylB = 0xBB67AE85u;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint32_t lo_a = c0 * kMulA, hi_a = __umulhi(c0, kMulA);
+        const uint32_t lo_b = c2 * kMulB, hi_b = __umulhi(c2, kMulB);
+        const uint32_t x0 = hi_b ^ c1 ^ k0;
+        const uint32_t x2 = hi_a ^ c3 ^ k1;
+        c0 = x0;
+        c1 = lo_b;
+        c2 = x2;
+        c3 = lo_a;
+        k0 += kWeylA;
+        k1 += kWeylB;
+    }
+    w[0] = c0;
+    w[1] = c1;
+    w[2] = c2;
+    w[3] = c3;
+}
+
 template <class OffT>
 __device__ __forceinline__ int64_t row_degree(const OffT *rp, int32_t v, int64_t &start) {
     start = (int64_t)rp[v];
@@ -173,8 +197,119 @@ __global__ void __launch_bounds__(256) k_sample_big(const OffT *__restrict__ row
     }
 }
 
+// Locality-biased selection (k <= 64), one wavefront per row.  Cached
+// neighbours (slot_map >= 0) weigh eta, the others 1; the k picks follow
+// successive sampling without replacement, done as
+//   1. the class of pick j = 0..k-1, in order: with c_r cached and u_r
+//      uncached left, t = floor(x * (eta*c_r + u_r) / 2^32), x = Philox word
+//      1 of counter (j, v, hop); cached when t < eta*c_r;
+//   2. Floyd's uniform subset inside each class: lane j < kc runs cached step
+//      j with word 2 of counter (j, v, hop), lane kc + j runs uncached step j
+//      with word 3 of counter (j, v, hop);
+//   3. the chosen class indices are mapped to row offsets by walking the row
+//      in 64-neighbour chunks with a ballot of the cached flags.
+// Output: cached picks in Floyd order, then the uncached ones.
+template <class OffT>
+__global__ void __launch_bounds__(256) k_sample_biased(const OffT *__restrict__ row_ptr,
+                                                       const int32_t *__restrict__ col,
+                                                       const int32_t *__restrict__ nodes,
+                                                       const int32_t *__restrict__ n_prev,
+                                                       const int32_t *__restrict__ indptr,
+                                                       int32_t *__restrict__ out, int32_t k, uint32_t key0,
+                                                       uint32_t key1, uint32_t hop,
+                                                       const int32_t *__restrict__ slot_map, uint32_t eta) {
+    const int lane = lane_id();
+    const int64_t n_rows = *n_prev;
+    const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
+    for (int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave; i < n_rows; i += nwaves) {
+        const int32_t v = nodes[i];
+        int64_t start;
+        const int64_t deg = row_degree(row_ptr, v, start);
+        int32_t *dst = out + indptr[i];
+        if (k < 0 || deg <= k) {
+            for (int64_t j = lane; j < deg; j += kWave) dst[j] = col[start + j];
+            continue;
+        }
+        // cached neighbours of the row
+        int64_t c = 0;
+        for (int64_t base = 0; base < deg; base += kWave) {
+            const bool f = base + lane < deg && slot_map[col[start + base + lane]] >= 0;
+            c += __popcll(__ballot(f));
+        }
+        const int64_t u = deg - c;
+        // 1. classes
+        uint32_t w[4];
+        philox4((uint32_t)lane, (uint32_t)v, 0u, hop, key0, key1, w);
+        const uint32_t x1 = w[1];
+        int64_t cr = c, ur = u;
+        int32_t kc = 0;
+        for (int j = 0; j < k; ++j) {
+            const uint32_t x = (uint32_t)__builtin_amdgcn_readlane((int)x1, j);
+            const uint64_t heavy = (uint64_t)eta * (uint64_t)cr;
+            const uint64_t b = heavy + (uint64_t)ur;
+            const uint64_t t = (uint64_t)x * (b >> 32) + (((uint64_t)x * (b & 0xffffffffull)) >> 32);
+            if (t < heavy) {
+                ++kc;
+                --cr;
+            } else {
+                --ur;
+            }
+        }
+        // 2. Floyd inside each class
+        const bool cached_lane = lane < kc;
+        const int32_t step = cached_lane ? lane : lane - kc;
+        const int64_t size = cached_lane ? c : u, kk = cached_lane ? kc : k - kc;
+        uint32_t t = 0, m = 0;
+        if (lane < k) {
+            philox4((uint32_t)step, (uint32_t)v, 0u, hop, key0, key1, w);
+            m = (uint32_t)(size - kk + step);
+            t = __umulhi(cached_lane ? w[2] : w[3], m + 1u);
+        }
+        uint32_t pick = t;
+        for (int j = 1; j < k; ++j) {
+            const uint32_t tj = (uint32_t)__builtin_amdgcn_readlane((int)t, j);
+            const bool same = (lane < kc) == (j < kc);
+            const uint64_t clash = __ballot(same && lane < j && pick == tj);
+            if (lane == j && clash != 0) pick = m;
+        }
+        // 3. class index -> row offset
+        int64_t seen = 0, pos = -1;
+        bool need = lane < k;
+        for (int64_t base = 0; base < deg && __ballot(need) != 0; base += kWave) {
+            const bool valid = base + lane < deg;
+            const bool f = valid && slot_map[col[start + base + lane]] >= 0;
+            const uint64_t mc = __ballot(f), mu = __ballot(valid && !f);
+            uint64_t mask = cached_lane ? mc : mu;
+            const int64_t cnt = __popcll(mask);
+            if (need && (int64_t)pick < seen + cnt) {
+                for (int64_t r = (int64_t)pick - seen; r > 0; --r) mask &= mask - 1;
+                pos = base + __builtin_ctzll(mask);
+                need = false;
+            }
+            seen += cnt;
+        }
+        if (lane < k) dst[lane] = col[start + (pos < 0 ? 0 : pos)];   // pos >= 0 whenever pick < class size
+    }
+}
+
 void launch_sample_hop(const SampleHopArgs &a, hipStream_t s) {
     if (a.rows_bound <= 0) return;
+    if (a.bias_slot_map) {
+        GNNAV_CHECK(a.fanout <= kWave, GNNAV_E_INVALID, "biased sampling supports fanouts up to 64");
+        const uint32_t key0 = (uint32_t)(a.rng_seed & 0xffffffffu), key1 = (uint32_t)(a.rng_seed >> 32);
+        const unsigned grid = grid_for(a.rows_bound, 256 / kWave, 16384);
+        KernelTimer t("sample_hop", s);
+        if (a.offsets_i64)
+            hipLaunchKernelGGL(k_sample_biased<int64_t>, dim3(grid), dim3(256), 0, s, (const int64_t *)a.row_ptr, a.col,
+                               a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, a.bias_slot_map,
+                               a.eta);
+        else
+            hipLaunchKernelGGL(k_sample_biased<int32_t>, dim3(grid), dim3(256), 0, s, (const int32_t *)a.row_ptr, a.col,
+                               a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, a.bias_slot_map,
+                               a.eta);
+        GNNAV_HIP(hipGetLastError());
+        return;
+    }
     GNNAV_CHECK(a.fanout <= kMaxFanout, GNNAV_E_INVALID, "fanout above 1024");
     const uint32_t key0 = (uint32_t)(a.rng_seed & 0xffffffffu), key1 = (uint32_t)(a.rng_seed >> 32);
     const unsigned grid = grid_for(a.rows_bound, 256 / kWave, 16384);

@@ -25,7 +25,8 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from . import Blocks, Cache, Graph, gather, gather_n, sage_forward, sage_train_step, sample, sample_async
+from . import (Blocks, Cache, Graph, gather, gather_n, sage_forward, sage_train_step, sample, sample_async,
+               sample_biased)
 
 
 def to_device_weights(ws, dtype: str):
@@ -38,7 +39,10 @@ def to_device_weights(ws, dtype: str):
 
 
 class MiniBatchStep:
-    def __init__(self, graph: Graph, cache: Cache, weights_dev, dims, fanouts, dtype: str):
+    """One batch's sampling, gather and model step.  eta: when set, sampling
+    is locality-biased toward the cache's vertices (gnnav_sample_biased)."""
+
+    def __init__(self, graph: Graph, cache: Cache, weights_dev, dims, fanouts, dtype: str, eta=None):
         self.graph, self.cache = graph, cache
         self.weights = list(weights_dev)
         self.dims = list(dims)
@@ -55,6 +59,14 @@ class MiniBatchStep:
         self.sizes = None
         self._seeds = None
         self._stream = None
+        self.eta = eta
+
+    def _sample(self, seeds_dev, rng_seed: int, async_: bool, st):
+        if self.eta is None:
+            (sample_async if async_ else sample)(self.graph, seeds_dev, self.fanouts, rng_seed, self.blocks, st)
+        else:
+            sample_biased(self.graph, self.cache, self.eta, seeds_dev, self.fanouts, rng_seed, self.blocks,
+                          async_=async_, stream=st)
 
     def _grow(self, n_l: int, n_0: int, stream=None):
         if self.h0.shape[0] >= n_l and self.logits.shape[0] >= n_0:
@@ -69,7 +81,7 @@ class MiniBatchStep:
     # -------------------------------------------------------------- sync
     def run(self, seeds_dev, rng_seed: int, stream=None):
         """Sample, gather and forward one batch; returns the logits view [|F_0|, classes]."""
-        sample(self.graph, seeds_dev, self.fanouts, rng_seed, self.blocks, stream)
+        self._sample(seeds_dev, rng_seed, False, stream)
         sizes, nodes_ptr = self.blocks.sizes()
         self.sizes = sizes
         self._grow(sizes[-1], sizes[0])
@@ -83,7 +95,7 @@ class MiniBatchStep:
         st = stream if stream is not None else torch.cuda.current_stream()
         self._seeds = seeds_dev            # keep alive until the work has run
         self._stream = st
-        sample_async(self.graph, seeds_dev, self.fanouts, rng_seed, self.blocks, st)
+        self._sample(seeds_dev, rng_seed, True, st)
         sizes_ptr, bounds = self.blocks.device_sizes(self.L)
         self._grow(bounds[-1], bounds[0], st)
         gather_n(self.cache, self.blocks.nodes_ptr(), sizes_ptr + 4 * self.L, bounds[-1], self.h0,
@@ -97,14 +109,14 @@ class MiniBatchStep:
         if async_mode:
             self._seeds = seeds_dev
             self._stream = st
-            sample_async(self.graph, seeds_dev, self.fanouts, rng_seed, self.blocks, st)
+            self._sample(seeds_dev, rng_seed, True, st)
             sizes_ptr, bounds = self.blocks.device_sizes(self.L)
             self._grow(bounds[-1], bounds[0], st)
             gather_n(self.cache, self.blocks.nodes_ptr(), sizes_ptr + 4 * self.L, bounds[-1], self.h0,
                      self.counts, st)
             self.sizes = None
         else:
-            sample(self.graph, seeds_dev, self.fanouts, rng_seed, self.blocks, st)
+            self._sample(seeds_dev, rng_seed, False, st)
             sizes, nodes_ptr = self.blocks.sizes()
             self.sizes = sizes
             self._grow(sizes[-1], sizes[0])
@@ -142,8 +154,9 @@ class MiniBatchStep:
 class Pipeline:
     """Batches b, b+1, ... on `depth` streams in turn (slot b % depth)."""
 
-    def __init__(self, graph: Graph, cache: Cache, weights_dev, dims, fanouts, dtype: str, depth: int = 2):
-        self.slots = [MiniBatchStep(graph, cache, weights_dev, dims, fanouts, dtype) for _ in range(depth)]
+    def __init__(self, graph: Graph, cache: Cache, weights_dev, dims, fanouts, dtype: str, depth: int = 2,
+                 eta=None):
+        self.slots = [MiniBatchStep(graph, cache, weights_dev, dims, fanouts, dtype, eta=eta) for _ in range(depth)]
         self.streams = [torch.cuda.Stream() for _ in range(depth)]
         self.depth = depth
         self.count = 0
