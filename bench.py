@@ -101,6 +101,38 @@ def link_calibration(G, cache, wl, torch):
     return out
 
 
+def locality_report(args, G, g, c, wl, seeds_dev, torch, batches=5):
+    """Biased against uniform sampling on the first timed batches (untimed):
+    the hit rate of F_L and the share of sampled picks that land on cached
+    vertices.  Within each class both samplers pick uniformly, so the
+    difference of the two shares is the total-variation distance between the
+    biased and the uniform distribution of a pick."""
+    slot = c.slot_map()
+    out = {"eta": args.eta}
+    for label, eta in (("biased", args.eta), ("uniform", None)):
+        hits = picks = cached = nodes_total = 0
+        blk = G.Blocks()
+        for b in range(args.warmup, args.warmup + batches):
+            if eta is None:
+                G.sample(g, seeds_dev[b], wl.fanouts, wl.rng_seed(b), blk)
+            else:
+                G.sample_biased(g, c, eta, seeds_dev[b], wl.fanouts, wl.rng_seed(b), blk)
+            nodes, _, _, nbrs, _ = blk.to_host()
+            hits += int((slot[nodes] >= 0).sum())
+            nodes_total += nodes.size
+            for nb in nbrs:
+                picks += nb.size
+                cached += int((slot[nb] >= 0).sum())
+        blk.close()
+        out[f"hit_rate_{label}"] = round(hits / max(nodes_total, 1), 4)
+        out[f"cached_pick_share_{label}"] = round(cached / max(picks, 1), 4)
+        out[f"frontier_{label}"] = round(nodes_total / batches, 1)
+    out["pick_distribution_tv_shift"] = round(out["cached_pick_share_biased"] - out["cached_pick_share_uniform"], 4)
+    log(f"locality eta={args.eta}: hit rate {out['hit_rate_uniform']} -> {out['hit_rate_biased']}, "
+        f"cached share of picks {out['cached_pick_share_uniform']} -> {out['cached_pick_share_biased']}")
+    return out
+
+
 def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_weights, MiniBatchStep, Pipeline):
     """Training iterations on the same batches: one stream with every kernel
     timed, then the two-stream pipeline (each forward waits for the
@@ -109,7 +141,7 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
     n_b = args.warmup + args.steps
     L = wl.L
     wtrain = to_device_weights(ws, "f32")
-    step = MiniBatchStep(g, c, wtrain, wl.dims, wl.fanouts, "f32")
+    step = MiniBatchStep(g, c, wtrain, wl.dims, wl.fanouts, "f32", eta=args.eta)
     stream = torch.cuda.current_stream()
     losses = []
     for b in range(args.warmup):
@@ -125,7 +157,7 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
     seq = time.perf_counter() - t0
     prof = G.profile_stop()
     losses = loss_hist[args.warmup:].cpu().numpy()
-    pipe = Pipeline(g, c, wtrain, wl.dims, wl.fanouts, "f32", depth=args.depth)
+    pipe = Pipeline(g, c, wtrain, wl.dims, wl.fanouts, "f32", depth=args.depth, eta=args.eta)
     for b in range(args.warmup):
         pipe.enqueue_train(seeds_dev[b], wl.rng_seed(b), labels, args.lr)
     pipe.synchronize()
@@ -178,6 +210,8 @@ def main():
                     help="fifo: admit each batch's misses into a ring over the last cache slots")
     ap.add_argument("--dynamic-fraction", type=float, default=1.0,
                     help="share of the cache slots in the FIFO ring (with --cache-policy fifo)")
+    ap.add_argument("--eta", type=int, default=None,
+                    help="locality-biased sampling: cached neighbours weigh eta (default: uniform)")
     ap.add_argument("--no-train", action="store_true", help="skip the training leg")
     ap.add_argument("--lr", type=float, default=0.01, help="SGD step of the training leg")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -224,7 +258,7 @@ def main():
         log(f"FIFO ring over the last {ring} of {c.n_cached} cache slots")
     ws = wl.weights()
     wdev = to_device_weights(ws, wl.dtype)
-    step = MiniBatchStep(g, c, wdev, wl.dims, wl.fanouts, wl.dtype)
+    step = MiniBatchStep(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, eta=args.eta)
     n_b = args.warmup + args.steps
     seeds_dev = [torch.from_numpy(wl.seeds(b)).cuda() for b in range(n_b)]
     L = wl.L
@@ -262,7 +296,7 @@ def main():
     log(f"sequential {args.steps} steps: {seq_ms:.3f} ms/step, {wl.batch * args.steps / seq_elapsed:,.0f} seeds/s")
 
     # ---- phase 2: the pipeline (batch b+1 overlaps batch b on another stream)
-    pipe = Pipeline(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, depth=args.depth)
+    pipe = Pipeline(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, depth=args.depth, eta=args.eta)
     for b in range(args.warmup):
         slot = pipe.enqueue(seeds_dev[b], wl.rng_seed(b))
     pipe.synchronize()
@@ -344,6 +378,11 @@ def main():
         roofline = {"kernel": dom, "bound": k["bound"], "achieved": k["achieved"], "peak": k["peak"],
                     "unit": k["unit"], "frac": k["frac"], "traffic": traffic_for(dom, wl.name)}
 
+    # ---- locality-biased sampling: hit rate against the shift it causes --
+    locality = None
+    if args.eta is not None:
+        locality = locality_report(args, G, g, c, wl, seeds_dev, torch)
+
     # ---- training leg: sample + gather + forward + loss + backward + SGD ----
     train = None
     if not args.no_train and wl.dtype == "f32":
@@ -363,7 +402,9 @@ def main():
         nb = max(1, args.cpu_batches)
         t0 = time.perf_counter()
         for b in range(args.warmup, args.warmup + nb):
-            ob = O.sample_blocks(csr, wl.seeds(b), wl.fanouts, wl.rng_seed(b))
+            bias = None if args.eta is None else (fifo.slot_map if fifo else slot)
+            ob = O.sample_blocks(csr, wl.seeds(b), wl.fanouts, wl.rng_seed(b), bias_slot_map=bias,
+                                 eta=args.eta or 1)
             h0, _ = fifo.gather(feats, ob.nodes) if fifo else O.gather(feats, slot, ob.nodes)
             O.sage_forward(ob, O.to_f64(h0, wl.dtype), wd, bf16=wl.dtype == "bf16")
         ct = time.perf_counter() - t0
@@ -396,12 +437,14 @@ def main():
         "config": {"workload": wl.name, "pipeline_streams": args.depth, "n": wl.n, "nnz": g.nnz, "d": wl.d, "fanouts": wl.fanouts,
                    "batch": wl.batch, "layers": wl.L, "dims": wl.dims, "cache_fraction": r,
                    "store_on_device": wl.cfg["store_on_device"], "cache_policy": args.cache_policy,
+                   "sampler": "uniform" if args.eta is None else f"locality-biased eta={args.eta}",
                    "fifo_slots": ring, "global_batch": wl.batch},
         "value_sequential": round(wl.batch * args.steps / seq_elapsed, 2),
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kernels,
         "eq4": eq4,
+        "locality": locality,
         "train": train,
         "host_link_calibration": link,
         "batch_stats": {"mean_frontier_sizes": mean_sizes, "hit_rate": round(hit_rate, 4),

@@ -307,6 +307,12 @@ struct gnnav_cache {
     std::mutex upd_mu;
     hipEvent_t upd_done = nullptr;
     bool upd_recorded = false;
+    // adjacency partitioned by this cache's (static) slot map, for the
+    // biased sampler; built on first use for a graph
+    DevBuf part_col, part_cnt;
+    const void *part_graph = nullptr;
+    int64_t part_nnz = -1;
+    hipEvent_t part_ready = nullptr;
 };
 
 static GatherWs *gather_ws(gnnav_cache *c, hipStream_t s) {
@@ -344,6 +350,9 @@ static void free_cache(gnnav_cache *c) {
     }
     c->owner.release();
     c->ring_ptr.release();
+    c->part_col.release();
+    c->part_cnt.release();
+    if (c->part_ready) (void)hipEventDestroy(c->part_ready);
     if (c->upd_done) (void)hipEventDestroy(c->upd_done);
     if (c->store_host) (void)hipHostFree(c->store_host);
     delete c;
@@ -493,6 +502,7 @@ extern "C" gnnav_status gnnav_cache_set_policy(gnnav_cache *c, int32_t policy, i
         c->policy = policy;
         c->ring_n = policy == GNNAV_POLICY_FIFO ? dynamic_slots : 0;
         c->ring_lo = c->c - c->ring_n;
+        c->part_graph = nullptr;   // the slot map may have moved: rebuild the partition on next use
         if (c->ring_n > 0) {
             hipStream_t s0 = nullptr;
             if (!c->owner.p) {
@@ -591,10 +601,26 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
         GNNAV_CHECK(eta >= 1 && eta <= 65536, GNNAV_E_INVALID, "eta outside [1, 65536]");
         for (int h = 0; h < n_hops; ++h)
             GNNAV_CHECK(fanouts[h] <= 64, GNNAV_E_INVALID, "biased sampling supports fanouts up to 64");
-        // a self-updating cache: read its slot map after the last update
         auto *bc = const_cast<gnnav_cache *>(bias);
         std::lock_guard<std::mutex> lk(bc->upd_mu);
-        if (bc->ring_n > 0 && bc->upd_recorded) GNNAV_HIP(hipStreamWaitEvent(s, bc->upd_done, 0));
+        if (bc->ring_n > 0) {
+            // a self-updating cache: read its slot map after the last update
+            if (bc->upd_recorded) GNNAV_HIP(hipStreamWaitEvent(s, bc->upd_done, 0));
+        } else {
+            // a static cache: rows partitioned by its slot map, built once per graph
+            if (bc->part_graph != (const void *)g || bc->part_nnz != g->nnz) {
+                bc->part_col.ensure(std::max<int64_t>(g->nnz, 1) * sizeof(int32_t), s);
+                bc->part_cnt.ensure(std::max<int64_t>(g->n, 1) * sizeof(int32_t), s);
+                launch_partition_rows(g->row_ptr.p, g->i64, g->col.as<int32_t>(), g->n, bc->slot_map.as<int32_t>(),
+                                      bc->part_col.as<int32_t>(), bc->part_cnt.as<int32_t>(), s);
+                if (!bc->part_ready) GNNAV_HIP(hipEventCreateWithFlags(&bc->part_ready, hipEventDisableTiming));
+                GNNAV_HIP(hipEventRecord(bc->part_ready, s));
+                bc->part_graph = g;
+                bc->part_nnz = g->nnz;
+            } else {
+                GNNAV_HIP(hipStreamWaitEvent(s, bc->part_ready, 0));
+            }
+        }
     }
     GNNAV_CHECK(n_hops >= 1 && n_hops <= kMaxHops, GNNAV_E_INVALID, "n_hops outside [1, 16]");
     GNNAV_CHECK(n_seeds >= 0, GNNAV_E_INVALID, "n_seeds < 0");
@@ -642,7 +668,9 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
         SampleHopArgs a{g->row_ptr.p, g->i64, g->col.as<int32_t>(), nodes, sz + kSizeN + h - 1,
                         b->indptr[h - 1].as<int32_t>(), b->nbrs[h - 1].as<int32_t>(), sz + kSizeE + h,
                         fanouts[h - 1], rng_seed, (uint32_t)(h - 1), nb[h - 1], &b->scan,
-                        bias ? bias->slot_map.as<int32_t>() : nullptr, eta};
+                        bias ? bias->slot_map.as<int32_t>() : nullptr, eta,
+                        bias && bias->ring_n == 0 ? bias->part_col.as<int32_t>() : nullptr,
+                        bias && bias->ring_n == 0 ? bias->part_cnt.as<int32_t>() : nullptr};
         launch_count_scan(a, s);
         launch_sample_hop(a, s);
         DedupArgs dh{b->nbrs[h - 1].as<int32_t>(), 0, sz + kSizeE + h, eb[h], map, g->n, nodes,

@@ -148,7 +148,13 @@ struct SampleHopArgs {
     ScanState *scan;
     const int32_t *bias_slot_map = nullptr;   // locality-biased selection when set
     uint32_t eta = 1;
+    // optional: adjacency with each row's cached neighbours first (CSR order
+    // within each class) and the per-vertex cached counts, for this slot map
+    const int32_t *part_col = nullptr;
+    const int32_t *part_cnt = nullptr;
 };
+void launch_partition_rows(const void *row_ptr, bool offsets_i64, const int32_t *col, int64_t n,
+                           const int32_t *slot_map, int32_t *part_col, int32_t *part_cnt, hipStream_t s);
 void launch_count_scan(const SampleHopArgs &a, hipStream_t s);
 void launch_sample_hop(const SampleHopArgs &a, hipStream_t s);
 

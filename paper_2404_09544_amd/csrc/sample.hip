@@ -217,7 +217,9 @@ __global__ void __launch_bounds__(256) k_sample_biased(const OffT *__restrict__ 
                                                        const int32_t *__restrict__ indptr,
                                                        int32_t *__restrict__ out, int32_t k, uint32_t key0,
                                                        uint32_t key1, uint32_t hop,
-                                                       const int32_t *__restrict__ slot_map, uint32_t eta) {
+                                                       const int32_t *__restrict__ slot_map, uint32_t eta,
+                                                       const int32_t *__restrict__ part_col,
+                                                       const int32_t *__restrict__ part_cnt) {
     const int lane = lane_id();
     const int64_t n_rows = *n_prev;
     const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
@@ -232,9 +234,13 @@ __global__ void __launch_bounds__(256) k_sample_biased(const OffT *__restrict__ 
         }
         // cached neighbours of the row
         int64_t c = 0;
-        for (int64_t base = 0; base < deg; base += kWave) {
-            const bool f = base + lane < deg && slot_map[col[start + base + lane]] >= 0;
-            c += __popcll(__ballot(f));
+        if (part_cnt) {
+            c = part_cnt[v];
+        } else {
+            for (int64_t base = 0; base < deg; base += kWave) {
+                const bool f = base + lane < deg && slot_map[col[start + base + lane]] >= 0;
+                c += __popcll(__ballot(f));
+            }
         }
         const int64_t u = deg - c;
         // 1. classes
@@ -273,6 +279,10 @@ __global__ void __launch_bounds__(256) k_sample_biased(const OffT *__restrict__ 
             if (lane == j && clash != 0) pick = m;
         }
         // 3. class index -> row offset
+        if (part_col) {
+            if (lane < k) dst[lane] = part_col[start + (cached_lane ? 0 : c) + pick];
+            continue;
+        }
         int64_t seen = 0, pos = -1;
         bool need = lane < k;
         for (int64_t base = 0; base < deg && __ballot(need) != 0; base += kWave) {
@@ -292,6 +302,56 @@ __global__ void __launch_bounds__(256) k_sample_biased(const OffT *__restrict__ 
     }
 }
 
+// Each row's neighbours split into cached then uncached, CSR order kept
+// within each class; part_cnt[v] = cached neighbours of v.  One wavefront
+// per row: a ballot per 64 neighbours gives every lane its rank in its class.
+template <class OffT>
+__global__ void __launch_bounds__(256) k_partition_rows(const OffT *__restrict__ row_ptr,
+                                                        const int32_t *__restrict__ col, int64_t n,
+                                                        const int32_t *__restrict__ slot_map,
+                                                        int32_t *__restrict__ part_col, int32_t *__restrict__ part_cnt) {
+    const int lane = lane_id();
+    const uint64_t below = (1ull << lane) - 1ull;
+    const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
+    for (int64_t v = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave; v < n; v += nwaves) {
+        int64_t start;
+        const int64_t deg = row_degree(row_ptr, (int32_t)v, start);
+        int64_t c = 0;
+        for (int64_t base = 0; base < deg; base += kWave) {
+            const bool f = base + lane < deg && slot_map[col[start + base + lane]] >= 0;
+            c += __popcll(__ballot(f));
+        }
+        int64_t seen_c = 0, seen_u = 0;
+        for (int64_t base = 0; base < deg; base += kWave) {
+            const bool valid = base + lane < deg;
+            const int32_t x = valid ? col[start + base + lane] : 0;
+            const bool f = valid && slot_map[x] >= 0;
+            const uint64_t mc = __ballot(f), mu = __ballot(valid && !f);
+            if (valid) {
+                const int64_t at = f ? seen_c + __popcll(mc & below) : c + seen_u + __popcll(mu & below);
+                part_col[start + at] = x;
+            }
+            seen_c += __popcll(mc);
+            seen_u += __popcll(mu);
+        }
+        if (lane == 0) part_cnt[v] = (int32_t)c;
+    }
+}
+
+void launch_partition_rows(const void *row_ptr, bool offsets_i64, const int32_t *col, int64_t n,
+                           const int32_t *slot_map, int32_t *part_col, int32_t *part_cnt, hipStream_t s) {
+    if (n <= 0) return;
+    const unsigned grid = grid_for(n, 256 / kWave, 16384);
+    KernelTimer t("partition_rows", s);
+    if (offsets_i64)
+        hipLaunchKernelGGL(k_partition_rows<int64_t>, dim3(grid), dim3(256), 0, s, (const int64_t *)row_ptr, col, n,
+                           slot_map, part_col, part_cnt);
+    else
+        hipLaunchKernelGGL(k_partition_rows<int32_t>, dim3(grid), dim3(256), 0, s, (const int32_t *)row_ptr, col, n,
+                           slot_map, part_col, part_cnt);
+    GNNAV_HIP(hipGetLastError());
+}
+
 void launch_sample_hop(const SampleHopArgs &a, hipStream_t s) {
     if (a.rows_bound <= 0) return;
     if (a.bias_slot_map) {
@@ -302,11 +362,11 @@ void launch_sample_hop(const SampleHopArgs &a, hipStream_t s) {
         if (a.offsets_i64)
             hipLaunchKernelGGL(k_sample_biased<int64_t>, dim3(grid), dim3(256), 0, s, (const int64_t *)a.row_ptr, a.col,
                                a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, a.bias_slot_map,
-                               a.eta);
+                               a.eta, a.part_col, a.part_cnt);
         else
             hipLaunchKernelGGL(k_sample_biased<int32_t>, dim3(grid), dim3(256), 0, s, (const int32_t *)a.row_ptr, a.col,
                                a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, a.bias_slot_map,
-                               a.eta);
+                               a.eta, a.part_col, a.part_cnt);
         GNNAV_HIP(hipGetLastError());
         return;
     }

@@ -126,3 +126,32 @@ def test_biased_sampling_with_fifo_cache(G, depth):
             assert np.array_equal(host(slot.counts), want[b][1])
     pipe.synchronize()
     assert np.array_equal(c.slot_map(), fifo.slot_map)
+
+
+def test_biased_partition_follows_policy_changes(G):
+    """Static cache: rows partitioned once by the slot map; a FIFO period
+    moves the map, and the partition is rebuilt when static again."""
+    import torch
+    n, u, v = graph_case("random-3000-40000-2")
+    csr = O.build_csr(n, u, v)
+    feats = W.features(n, 8, "f32")
+    g = G.Graph(n, u, v)
+    c = G.Cache(g, feats, "f32", 0.3)
+    seeds = W.epoch_permutation(n, 3)[:200]
+    seeds_d = dev(seeds)
+    b = G.Blocks()
+    for phase in ["static", "fifo", "static"]:
+        if phase == "fifo":
+            c.set_policy("fifo", c.n_cached // 2)
+            ids = dev(W.epoch_permutation(n, 9)[:1500])
+            out = torch.zeros((1500, c.ld), device="cuda")
+            counts = torch.zeros(3, dtype=torch.int64, device="cuda")
+            G.gather(c, ids.data_ptr(), 1500, out, counts)   # moves the slot map
+            torch.cuda.synchronize()
+        else:
+            c.set_policy("static")
+        slot = c.slot_map()
+        say("biased partition", phase)
+        G.sample_biased(g, c, 8, seeds_d, [10, 5], 77, b)
+        compare_blocks(G, b, O.sample_blocks(csr, seeds, [10, 5], 77, bias_slot_map=slot, eta=8))
+    b.close()

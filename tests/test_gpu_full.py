@@ -140,3 +140,34 @@ def test_full_train_step(G, name):
     for l in range(wl.L):
         assert_rows_close(got[l], rdW[l], FP32_TOL, f"{name} dW{l + 1}", floor=np.linalg.norm(floors[l], axis=1))
     c.close()
+
+
+@pytest.mark.parametrize("name", ["chunglu-233k-d602", "chunglu-2450k-d100"])
+def test_full_biased_batch(G, name):
+    """A batch through the bench's step with locality-biased sampling."""
+    import torch
+    from paper_2404_09544_amd.step import MiniBatchStep, to_device_weights
+    wl, _, _, csr, g = load(G, name)
+    feats = wl.features()
+    ws = wl.weights()
+    r, eta, b = wl.cfg["cache"], 8, 5
+    c = G.Cache(g, feats, wl.dtype, r, store_on_device=wl.cfg["store_on_device"])
+    step = MiniBatchStep(g, c, to_device_weights(ws, wl.dtype), wl.dims, wl.fanouts, wl.dtype, eta=eta)
+    _, slot, _ = O.rank_cache(csr, r)
+    seeds = wl.seeds(b)
+    step.enqueue(torch.from_numpy(seeds).cuda(), wl.rng_seed(b))
+    logits = step.finish().cpu().numpy()
+    nodes, sizes, ip, nb, ix = step.blocks.to_host()
+    ref_b = O.sample_blocks(csr, seeds, wl.fanouts, wl.rng_seed(b), bias_slot_map=slot, eta=eta)
+    assert sizes == ref_b.sizes
+    assert np.array_equal(nodes, ref_b.nodes)
+    for h in range(wl.L):
+        assert np.array_equal(nb[h], ref_b.nbrs[h]), f"neighbours hop {h + 1}"
+        assert np.array_equal(ix[h], ref_b.indices[h]), f"indices hop {h + 1}"
+    h0, counts = O.gather(feats, slot, ref_b.nodes)
+    assert np.array_equal(step.counts.cpu().numpy(), counts)
+    rows = np.random.default_rng(b).choice(sizes[0], size=64, replace=False)
+    ref = O.sage_forward_rows(ref_b, O.to_f64(h0, wl.dtype), [O.to_f64(w, wl.dtype) for w in ws], rows)
+    assert_rows_close(logits[rows], ref, FP32_TOL, f"{name} biased logits")
+    say(name, f"biased eta={eta}: hits/misses {counts.tolist()}")
+    c.close()
