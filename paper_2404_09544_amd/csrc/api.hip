@@ -283,8 +283,7 @@ static bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 // counts, and the second stream that carries the miss copy.  Each caller
 // stream gets its own, so gathers on different streams may overlap.
 struct GatherWs {
-    hipStream_t stream = nullptr, side = nullptr;
-    hipEvent_t fork = nullptr, join = nullptr;
+    hipStream_t stream = nullptr;
     DevBuf hit_list, miss_list, dev_counts;
     ScanState scan;   // its look-back timeout counter is not checked (the gather is asynchronous)
 };
@@ -322,9 +321,6 @@ static GatherWs *gather_ws(gnnav_cache *c, hipStream_t s) {
     auto *w = new GatherWs();
     w->stream = s;
     c->ws.push_back(w);
-    GNNAV_HIP(hipStreamCreateWithFlags(&w->side, hipStreamNonBlocking));
-    GNNAV_HIP(hipEventCreateWithFlags(&w->fork, hipEventDisableTiming));
-    GNNAV_HIP(hipEventCreateWithFlags(&w->join, hipEventDisableTiming));
     w->dev_counts.ensure(2 * sizeof(int32_t), s);
     return w;
 }
@@ -343,9 +339,6 @@ static void free_cache(gnnav_cache *c) {
         w->scan.sums.release();
         w->scan.prefix.release();
         w->scan.ctl.release();
-        if (w->side) (void)hipStreamDestroy(w->side);
-        if (w->fork) (void)hipEventDestroy(w->fork);
-        if (w->join) (void)hipEventDestroy(w->join);
         delete w;
     }
     c->owner.release();
@@ -802,14 +795,7 @@ static void gather_impl(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_
                  c->ld * c->elt, out_dev, ld_out * c->elt, c->d * c->elt, counts_dev, w->dev_counts.as<int32_t>(),
                  w->hit_list.as<int2>(), w->miss_list.as<int2>(), &w->scan};
     launch_classify(a, s);
-    if (n_ids > 0) {
-        GNNAV_HIP(hipEventRecord(w->fork, s));
-        GNNAV_HIP(hipStreamWaitEvent(w->side, w->fork, 0));
-        launch_gather_rows(a, /*hits=*/false, w->side);
-        launch_gather_rows(a, /*hits=*/true, s);
-        GNNAV_HIP(hipEventRecord(w->join, w->side));
-        GNNAV_HIP(hipStreamWaitEvent(s, w->join, 0));
-    }
+    if (n_ids > 0) launch_gather_rows(a, s);
     if (dynamic) {
         launch_fifo_update(a, cc->ring_lo, cc->ring_n, cc->owner.as<int32_t>(), cc->slot_map.as<int32_t>(),
                            cc->ring_ptr.as<int32_t>(), cc->cache_rows.p, s);

@@ -197,7 +197,7 @@ struct GatherArgs {
     ScanState *scan;
 };
 void launch_classify(const GatherArgs &a, hipStream_t s);
-void launch_gather_rows(const GatherArgs &a, bool hits, hipStream_t s);
+void launch_gather_rows(const GatherArgs &a, hipStream_t s);
 void launch_matmul_bt(const float *a, int64_t lda, int64_t m, const int32_t *m_dev, int64_t k, const float *b,
                       int64_t ldb, int64_t n, float *out, int64_t ld_out, hipStream_t s, const char *label);
 // Transpose of a sampled block (destination rows per source column, in

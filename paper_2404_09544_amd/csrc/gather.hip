@@ -6,10 +6,10 @@
 //              splits the requests into a hit list (out row, cache slot)
 //              and a miss list (out row, node id) and writes the counts;
 //              out-of-range ids get a zero row right here
-//   rows       copies listed rows in 16-byte units; the hit launch reads
-//              the HBM cache, the miss launch reads the host store through
-//              its device mapping (zero-copy over the host link) and runs on
-//              a second stream so both proceed together
+//   rows       copies listed rows in 16-byte units in one launch: a fixed
+//              share of the workgroups reads the miss rows from the host
+//              store through its device mapping (zero-copy over the host
+//              link), the rest read the hit rows from the HBM cache
 #include <algorithm>
 
 #include "common.hpp"
@@ -64,23 +64,33 @@ void launch_classify(const GatherArgs &a, hipStream_t s) {
     run_scan<ClassifyOp, int64_t>(op, a.n_ids, *a.scan, "classify", s);
 }
 
-// G lanes per row (power of two), 64/G rows per wavefront pass.  Each lane
-// moves 16-byte units c = lane%G, lane%G + G, ... of its row.
+// One launch moves both lists.  Workgroups [0, miss_blocks) copy the miss
+// list from the host store (zero-copy over the host link), the others copy
+// the hit list from the HBM cache, so the two proceed together without a
+// second stream (a second stream would share one of the process's few
+// hardware queues with other work and hold it for the whole transfer).
+// G lanes per row (power of two), 64/G rows per wavefront pass; lane c0
+// moves 16-byte units c0, c0 + G, ... of its row.
 template <int G>
-__global__ void __launch_bounds__(256) k_gather_rows(const int2 *__restrict__ list,
-                                                     const int32_t *__restrict__ count_ptr,
-                                                     const uint4 *__restrict__ src, int64_t src_ld16,
-                                                     uint4 *__restrict__ out, int64_t out_ld16,
-                                                     int32_t chunks) {
+__global__ void __launch_bounds__(256) k_gather_rows(const int2 *__restrict__ hit_list,
+                                                     const int2 *__restrict__ miss_list,
+                                                     const int32_t *__restrict__ dev_counts,
+                                                     const uint4 *__restrict__ cache, const uint4 *__restrict__ store,
+                                                     int64_t src_ld16, uint4 *__restrict__ out, int64_t out_ld16,
+                                                     int32_t chunks, int32_t miss_blocks) {
     constexpr int RPW = kWave / G;
     const int lane = lane_id();
     const int sub = lane / G, c0 = lane % G;
-    const int64_t count = *count_ptr;
-    const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
-    for (int64_t r = (((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave) * RPW + sub; r < count;
-         r += nwaves * RPW) {
+    const bool miss = (int32_t)blockIdx.x < miss_blocks;
+    const int2 *list = miss ? miss_list : hit_list;
+    const uint4 *src_base = miss ? store : cache;
+    const int64_t count = dev_counts[miss ? 1 : 0];
+    const int64_t block = miss ? blockIdx.x : blockIdx.x - miss_blocks;
+    const int64_t nblocks = miss ? miss_blocks : gridDim.x - miss_blocks;
+    const int64_t nwaves = nblocks * (blockDim.x / kWave);
+    for (int64_t r = ((block * blockDim.x + threadIdx.x) / kWave) * RPW + sub; r < count; r += nwaves * RPW) {
         const int2 e = list[r];
-        const uint4 *s = src + (int64_t)e.y * src_ld16;
+        const uint4 *s = src_base + (int64_t)e.y * src_ld16;
         uint4 *d = out + (int64_t)e.x * out_ld16;
         int c = c0;
         for (; c + 3 * G < chunks; c += 4 * G) {
@@ -94,27 +104,26 @@ __global__ void __launch_bounds__(256) k_gather_rows(const int2 *__restrict__ li
     }
 }
 
-void launch_gather_rows(const GatherArgs &a, bool hits, hipStream_t s) {
+void launch_gather_rows(const GatherArgs &a, hipStream_t s) {
     const int32_t chunks = (int32_t)((a.row_bytes + 15) / 16);
     int g = 1;
     while (g < chunks && g < kWave) g <<= 1;
     const int64_t rows_bound = a.n_ids;
     if (rows_bound <= 0 || chunks <= 0) return;
     const int rows_per_block = (256 / kWave) * (kWave / g);
-    // The miss path needs only enough waves to cover the host link's latency
-    // (64 workgroups keep it at ~53 GB/s); more of them queue slow host reads
-    // in the memory system and stall the concurrent HBM copy of the hits.
-    const unsigned grid = grid_for(rows_bound, rows_per_block, hits ? 8192 : 64);
-    const int2 *list = hits ? a.hit_list : a.miss_list;
-    const int32_t *cnt = a.dev_counts + (hits ? 0 : 1);
-    const uint4 *src = (const uint4 *)(hits ? a.cache : a.store);
+    // The miss share needs only enough waves to cover the host link's
+    // latency (64 workgroups keep it at ~53 GB/s); more of them queue slow
+    // host reads in the memory system and stall the HBM copy of the hits.
+    const unsigned miss_blocks = grid_for(rows_bound, rows_per_block, 64);
+    const unsigned hit_blocks = grid_for(rows_bound, rows_per_block, 8192);
     const int64_t sld = a.src_ld_bytes / 16, old = a.out_ld_bytes / 16;
-    KernelTimer t(hits ? "gather_hit" : "gather_miss", s);
+    KernelTimer t("gather_rows", s);
     switch (g) {
-#define GNNAV_G(GV)                                                                                 \
-    case GV:                                                                                        \
-        hipLaunchKernelGGL(k_gather_rows<GV>, dim3(grid), dim3(256), 0, s, list, cnt, src, sld,     \
-                           (uint4 *)a.out, old, chunks);                                            \
+#define GNNAV_G(GV)                                                                                       \
+    case GV:                                                                                              \
+        hipLaunchKernelGGL(k_gather_rows<GV>, dim3(miss_blocks + hit_blocks), dim3(256), 0, s, a.hit_list,  \
+                           a.miss_list, a.dev_counts, (const uint4 *)a.cache, (const uint4 *)a.store, sld,  \
+                           (uint4 *)a.out, old, chunks, (int32_t)miss_blocks);                             \
         break;
         GNNAV_G(1) GNNAV_G(2) GNNAV_G(4) GNNAV_G(8) GNNAV_G(16) GNNAV_G(32) GNNAV_G(64)
 #undef GNNAV_G

@@ -16,7 +16,10 @@ F_0, backward, SGD on the step's weights in place).
 own step (blocks, gathered rows, logits), so batch b+1's sampling and
 host-link gather overlap batch b's aggregation and combine: the overlap
 Eq. 4 assumes when it takes the epoch time as n_iter times the larger of
-(t_sample + t_transfer) and (t_replace + t_compute).
+(t_sample + t_transfer) and (t_replace + t_compute).  Gathers take the host
+link one batch at a time, in batch order (each waits for the previous
+batch's gather): two gathers sharing the link would finish together and
+leave it idle while both batches compute.
 
 Device buffers are torch tensors that only grow.
 """
@@ -56,6 +59,7 @@ class MiniBatchStep:
         self.logits = torch.empty((0, self.dims[-1]), dtype=torch.float32, device="cuda")
         self.counts = torch.zeros(3, dtype=torch.int64, device="cuda")
         self.loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+        self.gathered = torch.cuda.Event()       # recorded after each gather
         self.sizes = None
         self._seeds = None
         self._stream = None
@@ -90,21 +94,25 @@ class MiniBatchStep:
         return self.logits[:sizes[0]]
 
     # ------------------------------------------------------------- async
-    def enqueue(self, seeds_dev, rng_seed: int, stream=None):
-        """Enqueue one batch on `stream` without waiting for it."""
+    def enqueue(self, seeds_dev, rng_seed: int, stream=None, gather_after=None):
+        """Enqueue one batch on `stream` without waiting for it; the gather
+        waits for the event `gather_after` when given."""
         st = stream if stream is not None else torch.cuda.current_stream()
         self._seeds = seeds_dev            # keep alive until the work has run
         self._stream = st
         self._sample(seeds_dev, rng_seed, True, st)
         sizes_ptr, bounds = self.blocks.device_sizes(self.L)
         self._grow(bounds[-1], bounds[0], st)
+        if gather_after is not None:
+            st.wait_event(gather_after)
         gather_n(self.cache, self.blocks.nodes_ptr(), sizes_ptr + 4 * self.L, bounds[-1], self.h0,
                  self.counts, st)
+        self.gathered.record(st)
         sage_forward(self.blocks, self.h0, self.weights, self.dims, self.dtype, self.logits, st)
         self.sizes = None
 
     # ------------------------------------------------------------ train
-    def _inputs(self, seeds_dev, rng_seed: int, async_mode: bool, st):
+    def _inputs(self, seeds_dev, rng_seed: int, async_mode: bool, st, gather_after=None):
         """Sample and gather F_L's rows into h0 (on stream st)."""
         if async_mode:
             self._seeds = seeds_dev
@@ -112,8 +120,11 @@ class MiniBatchStep:
             self._sample(seeds_dev, rng_seed, True, st)
             sizes_ptr, bounds = self.blocks.device_sizes(self.L)
             self._grow(bounds[-1], bounds[0], st)
+            if gather_after is not None:
+                st.wait_event(gather_after)
             gather_n(self.cache, self.blocks.nodes_ptr(), sizes_ptr + 4 * self.L, bounds[-1], self.h0,
                      self.counts, st)
+            self.gathered.record(st)
             self.sizes = None
         else:
             self._sample(seeds_dev, rng_seed, False, st)
@@ -151,21 +162,37 @@ class MiniBatchStep:
         return self.h0[:self.sizes[-1]]
 
 
+_STREAMS = []
+
+
+def pipeline_streams(n: int):
+    """The process's pipeline streams, created once and shared by every
+    Pipeline.  HIP multiplexes streams onto a few hardware queues (four by
+    default); two busy streams that land on one queue run one after the
+    other, so the pipeline keeps its stream count at its depth."""
+    while len(_STREAMS) < n:
+        _STREAMS.append(torch.cuda.Stream())
+    return _STREAMS[:n]
+
+
 class Pipeline:
     """Batches b, b+1, ... on `depth` streams in turn (slot b % depth)."""
 
     def __init__(self, graph: Graph, cache: Cache, weights_dev, dims, fanouts, dtype: str, depth: int = 2,
                  eta=None):
         self.slots = [MiniBatchStep(graph, cache, weights_dev, dims, fanouts, dtype, eta=eta) for _ in range(depth)]
-        self.streams = [torch.cuda.Stream() for _ in range(depth)]
+        self.streams = pipeline_streams(depth)
         self.depth = depth
         self.count = 0
         self._updated = None
 
+    def _previous_gather(self):
+        return self.slots[(self.count - 1) % self.depth].gathered if self.count > 0 else None
+
     def enqueue(self, seeds_dev, rng_seed: int):
         """Enqueue the next batch; returns the slot it runs in."""
         k = self.count % self.depth
-        self.slots[k].enqueue(seeds_dev, rng_seed, self.streams[k])
+        self.slots[k].enqueue(seeds_dev, rng_seed, self.streams[k], gather_after=self._previous_gather())
         self.count += 1
         return self.slots[k]
 
@@ -177,7 +204,7 @@ class Pipeline:
         slot, st = self.slots[k], self.streams[k]
         if slot.dtype != "f32":
             raise ValueError("training runs in fp32")
-        slot._inputs(seeds_dev, rng_seed, True, st)
+        slot._inputs(seeds_dev, rng_seed, True, st, gather_after=self._previous_gather())
         if self._updated is not None:
             st.wait_event(self._updated)
         slot._train_tail(labels_dev, lr, None, st)
