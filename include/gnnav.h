@@ -372,7 +372,9 @@ gnnav_status gnnav_sample_biased(const gnnav_graph *g, const gnnav_cache *cache,
  * Per-kernel timing with HIP events recorded around every kernel launch on
  * the stream it is launched on.  profile_start clears the table and turns
  * recording on; profile_stop synchronises the device, resolves the events
- * and turns recording off.  Entries are read by index.                    */
+ * and turns recording off.  Entries are read by index.  Both launch an
+ * empty kernel, k_profile_mark(1) and k_profile_mark(2), so the recorded
+ * region can be found in an external kernel trace.                        */
 gnnav_status gnnav_profile_start(void);
 gnnav_status gnnav_profile_stop(void);
 int32_t gnnav_profile_count(void);

@@ -103,9 +103,20 @@ KernelTimer::~KernelTimer() {
 }
 }  // namespace gnnav
 
+// An empty kernel launched when recording starts (which = 1) and stops
+// (which = 2): it marks the recorded region in an external kernel trace.
+__global__ void k_profile_mark(int which) { (void)which; }
+
+static void profile_mark(int which) {
+    hipLaunchKernelGGL(k_profile_mark, dim3(1), dim3(64), 0, nullptr, which);
+    GNNAV_HIP(hipGetLastError());
+    GNNAV_HIP(hipDeviceSynchronize());
+}
+
 extern "C" gnnav_status gnnav_profile_start(void) {
     return guarded([&] {
         GNNAV_HIP(hipDeviceSynchronize());
+        profile_mark(1);
         std::lock_guard<std::mutex> lk(g_prof_mu);
         for (auto &p : g_pending) {
             g_event_pool.push_back(p.a);
@@ -120,6 +131,7 @@ extern "C" gnnav_status gnnav_profile_start(void) {
 extern "C" gnnav_status gnnav_profile_stop(void) {
     return guarded([&] {
         GNNAV_HIP(hipDeviceSynchronize());
+        profile_mark(2);
         std::lock_guard<std::mutex> lk(g_prof_mu);
         g_prof_on = false;
         for (auto &p : g_pending) {
