@@ -235,6 +235,16 @@ gnnav_status gnnav_gather_n(const gnnav_cache *c, const int32_t *ids_dev, const 
                             int64_t n_ids_max, void *out_dev, int64_t ld_out, int64_t *counts_dev,
                             void *stream);
 
+/* gnnav_gather_n whose row copies (not the classification) wait for
+ * copy_after_event (a hipEvent_t, or NULL for no wait) to complete: a
+ * pipeline passes the previous batch's gather event, so transfers over the
+ * host link run one after another while each batch's classification runs
+ * ahead.  Same results and errors as gnnav_gather_n.                      */
+gnnav_status gnnav_gather_n_after(const gnnav_cache *c, const int32_t *ids_dev,
+                                  const int32_t *n_ids_dev, int64_t n_ids_max, void *out_dev,
+                                  int64_t ld_out, int64_t *counts_dev, void *copy_after_event,
+                                  void *stream);
+
 /* ------------------------------------------------------- SAGE, per layer ---
  * Eq. 1 Aggregate, GraphSAGE mean: for each destination row i < n_dst,
  * out[i] = (1/cnt_i) * sum over p in [indptr[i], indptr[i+1]) of

@@ -30,7 +30,7 @@ EXPORTS = [
     "gnnav_graph_csr_host", "gnnav_graph_free", "gnnav_build_cache", "gnnav_cache_info",
     "gnnav_cache_slot_map_host", "gnnav_cache_contents_host", "gnnav_cache_set_policy", "gnnav_cache_free", "gnnav_blocks_create", "gnnav_blocks_free",
     "gnnav_sample", "gnnav_sample_async", "gnnav_sample_biased", "gnnav_blocks_sync", "gnnav_blocks_device_sizes",
-    "gnnav_blocks_hop", "gnnav_blocks_nodes", "gnnav_gather", "gnnav_gather_n",
+    "gnnav_blocks_hop", "gnnav_blocks_nodes", "gnnav_gather", "gnnav_gather_n", "gnnav_gather_n_after",
     "gnnav_aggregate_mean", "gnnav_combine", "gnnav_sage_forward", "gnnav_sage_train_step",
     "gnnav_softmax_xent", "gnnav_aggregate_mean_backward", "gnnav_weight_grad", "gnnav_profile_start",
     "gnnav_profile_stop", "gnnav_profile_count", "gnnav_profile_get",
@@ -71,6 +71,7 @@ _sig = {
     "gnnav_blocks_sync": ([P, P], i32),
     "gnnav_blocks_device_sizes": ([P, P, P], i32),
     "gnnav_gather_n": ([P, P, P, i64, P, i64, P, P], i32),
+    "gnnav_gather_n_after": ([P, P, P, i64, P, i64, P, P, P], i32),
     "gnnav_blocks_hop": ([P, i32, C.POINTER(BlockView)], i32),
     "gnnav_blocks_nodes": ([P, P, P, P], i32),
     "gnnav_gather": ([P, P, i64, P, i64, P, P], i32),
@@ -331,10 +332,16 @@ def sample_biased(graph: Graph, cache: Cache, eta: int, seeds, fanouts, rng_seed
     return blocks
 
 
-def gather_n(cache: Cache, ids_ptr: int, n_ids_dev_ptr: int, n_ids_max: int, out, counts, stream=None):
-    """gnnav_gather_n: the request count is read from device memory."""
-    _check(_lib.gnnav_gather_n(cache._h, ids_ptr, n_ids_dev_ptr, n_ids_max, _dev_ptr(out), out.stride(0),
-                               _dev_ptr(counts), _stream(stream)))
+def gather_n(cache: Cache, ids_ptr: int, n_ids_dev_ptr: int, n_ids_max: int, out, counts, stream=None,
+             copy_after=None):
+    """gnnav_gather_n: the request count is read from device memory.
+    copy_after: a recorded torch.cuda.Event the row copies wait for."""
+    if copy_after is None:
+        _check(_lib.gnnav_gather_n(cache._h, ids_ptr, n_ids_dev_ptr, n_ids_max, _dev_ptr(out), out.stride(0),
+                                   _dev_ptr(counts), _stream(stream)))
+    else:
+        _check(_lib.gnnav_gather_n_after(cache._h, ids_ptr, n_ids_dev_ptr, n_ids_max, _dev_ptr(out),
+                                         out.stride(0), _dev_ptr(counts), copy_after.cuda_event, _stream(stream)))
 
 
 def gather(cache: Cache, ids_ptr: int, n_ids: int, out, counts, stream=None):

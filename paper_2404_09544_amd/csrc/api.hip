@@ -783,7 +783,8 @@ extern "C" gnnav_status gnnav_blocks_nodes(const gnnav_blocks *b, const int32_t 
 // ----------------------------------------------------------------- gather
 
 static void gather_impl(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_ids, const int32_t *n_dev,
-                        void *out_dev, int64_t ld_out, int64_t *counts_dev, hipStream_t s) {
+                        void *out_dev, int64_t ld_out, int64_t *counts_dev, hipStream_t s,
+                        hipEvent_t copy_after = nullptr) {
     GNNAV_CHECK(c && counts_dev, GNNAV_E_INVALID, "NULL cache or counts");
     GNNAV_CHECK(n_ids >= 0 && n_ids < INT32_MAX, GNNAV_E_INVALID, "n_ids outside [0, INT32_MAX)");
     GNNAV_CHECK(n_ids == 0 || (ids_dev && out_dev), GNNAV_E_INVALID, "NULL ids or out");
@@ -807,6 +808,7 @@ static void gather_impl(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_
                  c->ld * c->elt, out_dev, ld_out * c->elt, c->d * c->elt, counts_dev, w->dev_counts.as<int32_t>(),
                  w->hit_list.as<int2>(), w->miss_list.as<int2>(), &w->scan};
     launch_classify(a, s);
+    if (copy_after) GNNAV_HIP(hipStreamWaitEvent(s, copy_after, 0));
     if (n_ids > 0) launch_gather_rows(a, s);
     if (dynamic) {
         launch_fifo_update(a, cc->ring_lo, cc->ring_n, cc->owner.as<int32_t>(), cc->slot_map.as<int32_t>(),
@@ -827,6 +829,16 @@ extern "C" gnnav_status gnnav_gather_n(const gnnav_cache *c, const int32_t *ids_
     return guarded([&] {
         GNNAV_CHECK(n_ids_dev, GNNAV_E_INVALID, "n_ids_dev is NULL");
         gather_impl(c, ids_dev, n_ids_max, n_ids_dev, out_dev, ld_out, counts_dev, (hipStream_t)stream);
+    });
+}
+
+extern "C" gnnav_status gnnav_gather_n_after(const gnnav_cache *c, const int32_t *ids_dev, const int32_t *n_ids_dev,
+                                             int64_t n_ids_max, void *out_dev, int64_t ld_out, int64_t *counts_dev,
+                                             void *copy_after_event, void *stream) {
+    return guarded([&] {
+        GNNAV_CHECK(n_ids_dev, GNNAV_E_INVALID, "n_ids_dev is NULL");
+        gather_impl(c, ids_dev, n_ids_max, n_ids_dev, out_dev, ld_out, counts_dev, (hipStream_t)stream,
+                    (hipEvent_t)copy_after_event);
     });
 }
 

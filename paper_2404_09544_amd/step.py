@@ -95,18 +95,16 @@ class MiniBatchStep:
 
     # ------------------------------------------------------------- async
     def enqueue(self, seeds_dev, rng_seed: int, stream=None, gather_after=None):
-        """Enqueue one batch on `stream` without waiting for it; the gather
-        waits for the event `gather_after` when given."""
+        """Enqueue one batch on `stream` without waiting for it; the gather's
+        row copies wait for the event `gather_after` when given."""
         st = stream if stream is not None else torch.cuda.current_stream()
         self._seeds = seeds_dev            # keep alive until the work has run
         self._stream = st
         self._sample(seeds_dev, rng_seed, True, st)
         sizes_ptr, bounds = self.blocks.device_sizes(self.L)
         self._grow(bounds[-1], bounds[0], st)
-        if gather_after is not None:
-            st.wait_event(gather_after)
         gather_n(self.cache, self.blocks.nodes_ptr(), sizes_ptr + 4 * self.L, bounds[-1], self.h0,
-                 self.counts, st)
+                 self.counts, st, copy_after=gather_after)
         self.gathered.record(st)
         sage_forward(self.blocks, self.h0, self.weights, self.dims, self.dtype, self.logits, st)
         self.sizes = None
@@ -120,10 +118,8 @@ class MiniBatchStep:
             self._sample(seeds_dev, rng_seed, True, st)
             sizes_ptr, bounds = self.blocks.device_sizes(self.L)
             self._grow(bounds[-1], bounds[0], st)
-            if gather_after is not None:
-                st.wait_event(gather_after)
             gather_n(self.cache, self.blocks.nodes_ptr(), sizes_ptr + 4 * self.L, bounds[-1], self.h0,
-                     self.counts, st)
+                     self.counts, st, copy_after=gather_after)
             self.gathered.record(st)
             self.sizes = None
         else:

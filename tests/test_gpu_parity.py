@@ -203,6 +203,45 @@ def test_gather_parity(G, d, dtype, store_on_device):
             assert not got[:, d:d + tail].any(), "padding up to the 16-byte boundary must be zero"
 
 
+@pytest.mark.parametrize("wait", [False, True])
+def test_gather_device_count(G, wait):
+    """gather_n reads the request count from device memory; with copy_after
+    the row copies wait for an event recorded on another stream."""
+    import torch
+    n, u, v = graph_case("random-5000-30000-7")
+    csr = O.build_csr(n, u, v)
+    g = G.Graph(n, u, v)
+    feats = W.features(n, 100, "f32", seed=4)
+    c = G.Cache(g, feats, "f32", 0.3)
+    _, slot, _ = O.rank_cache(csr, 0.3)
+    ids = np.random.default_rng(9).integers(0, n, 3001).astype(np.int32)
+    ids_d = dev(ids)
+    other = torch.cuda.Stream()
+    for m in [3001, 1777, 0, 1]:
+        say("gather_n", wait, m)
+        n_d = dev(np.array([m], np.int32))
+        out = torch.full((ids.size, c.ld), -7.0, device="cuda")
+        counts = torch.full((3,), 9, dtype=torch.int64, device="cuda")
+        ev = None
+        if wait:
+            # work on another stream whose end the copies must see: it fills
+            # the output, and the gather then overwrites the requested rows
+            ev = torch.cuda.Event()
+            other.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(other):
+                torch.cuda._sleep(2000000)
+                out.fill_(-5.0)
+                ev.record(other)
+        G.gather_n(c, ids_d.data_ptr(), n_d.data_ptr(), ids.size, out, counts, copy_after=ev)
+        torch.cuda.synchronize()
+        ref_rows, ref_counts = O.gather(feats, slot, ids[:m])
+        got = host(out)
+        assert np.array_equal(host(counts), ref_counts)
+        assert np.array_equal(got[:m, :100].view(np.uint8), ref_rows.view(np.uint8))
+        if wait:
+            assert (got[m:] == -5.0).all()
+
+
 def test_gather_empty_and_errors(G):
     import torch
     n, u, v = graph_case("path")
