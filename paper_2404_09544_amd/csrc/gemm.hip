@@ -2,28 +2,38 @@
 // self * W[0:d_in] + agg * W[d_in:2*d_in] with two A-operand pointers, so
 // the concatenation is never stored.
 //
-// Matrix cores: fp32 uses v_mfma_f32_16x16x4_f32 (full fp32 products),
-// bf16 uses v_mfma_f32_16x16x32_bf16 with fp32 accumulation.
+// Matrix cores: fp32 uses v_mfma_f32_32x32x2_f32 in the ring kernel and
+// v_mfma_f32_16x16x4_f32 elsewhere (full fp32 products either way); bf16
+// uses v_mfma_f32_16x16x32_bf16 with fp32 accumulation.  On MI355X the
+// 32x32 fp32 instruction sustains the full matrix rate with one wavefront
+// per SIMD, the 16x16 one about three quarters of it.
 //
-// Main kernel (enough output tiles to fill the chip): a 256-thread
-// workgroup owns a BM x BN output tile as WM x WN wavefronts, each holding
-// (BM/WM) x (BN/WN) in 16 x 16 MFMA accumulators.  K is walked in BK steps
-// through two LDS buffers: the next step's global loads are issued into
-// registers before the current step's MFMAs and stored into the other buffer
-// afterwards, so there is one barrier per step.
+// fp32 ring kernel (rows 16-byte aligned, the normal case): a 256-thread
+// workgroup owns a BM x BN output tile as 2 x 2 wavefronts.  Both operands
+// travel as 16-byte k-chunks from global memory straight into LDS
+// (global_load_lds_dwordx4) through a ring of STAGES buffers, so no
+// registers hold staged data and the loads of later steps are in flight
+// while the current one is multiplied.
+//
+// Register-staged kernels (unaligned rows, bf16, short K over many rows):
+// K is walked in BK steps through two LDS buffers: the next step's global
+// loads are issued into registers before the current step's MFMAs and
+// stored into the other buffer afterwards, one barrier per step.
 //
 // Skinny kernel (few output rows, e.g. the last layer over the seeds): a
 // workgroup owns 16 x 64 outputs; its four wavefronts take interleaved
 // 16- or 32-wide K blocks straight from global memory into MFMA fragments
 // and add their partial tiles in LDS in a fixed order (deterministic).
 //
-// MFMA 16x16 fragment layouts (lane l, g = l / 16):
-//   f32 x4:   A[row l%16][k g],         B[k g][col l%16]
-//   bf16 x32: A[row l%16][k 8g..8g+7],  B[k 8g..8g+7][col l%16]
-//   result:   D[row 4g + r][col l%16] in accumulator element r.
+// MFMA fragment layouts (lane l):
+//   f32 16x16x4:  A[row l%16][k l/16],  B[k l/16][col l%16]
+//   f32 32x32x2:  A[row l%32][k l/32],  B[k l/32][col l%32]
+//   bf16 16x16x32: A[row l%16][k 8(l/16)..+7], B likewise
+//   16x16 result: D[row 4(l/16) + r][col l%16] in accumulator element r
+//   32x32 result: D[row 8(r/4) + 4(l/32) + r%4][col l%32] in element r
 // Only the pairing of A's and B's k index inside one instruction matters,
-// so the loaders may assign k to (g, element) in any way that is the same
-// for both operands.
+// so the loaders may assign k to (lane group, element) in any way that is
+// the same for both operands.
 #include <cstdlib>
 #include <mutex>
 
@@ -192,6 +202,189 @@ __global__ void __launch_bounds__(256) k_combine_f32(const float *__restrict__ A
         __syncthreads();
     }
     write_tile<TM, TN, float>(acc, m0 + wm * WTM, n0 + wn * WTN, M, N, relu, C, ldc, g, l16);
+}
+
+// ------------------------------------------------------- fp32 ring kernel
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// One wavefront-wide LDS DMA: lane l copies 16 bytes from its own global
+// address g to LDS address lds + 16 * l (lds must be the same for every
+// lane).  Issued from inline assembly, so the compiler does not know that
+// LDS is written and adds no waits of its own: callers track completion
+// with vmcnt (wait_vm) and publish it with a barrier.
+__device__ __forceinline__ void dma16(const void *g, const void *lds) {
+    const uint32_t la = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(la), "v"(g) : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(N): at most N of this wavefront's vector loads pending.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (0 << 8) | (3 << 14));   // lgkmcnt(0)
+    asm volatile("s_barrier" ::: "memory");
+}
+
+// C = act(sum over nseg segments of A_s * B_s^T): A_s is A0 or A1 (M rows,
+// stride lda_s), B_s the N rows of B at column offset s * bseg (stride ldb).
+// Requires 16-byte aligned A0, A1, B and strides, bseg a multiple of 4.
+// Step t covers k in [kb, kb + 32) of one segment; its chunk (row, c) is
+// read whole when it starts below K (a straddling chunk reads the row's
+// padding) and from the row start otherwise, then the elements at k >= K
+// are zeroed in LDS by the lane that loaded them, after its load landed
+// and before the barrier that publishes the step.  Rows past M or N load
+// the last valid row; their results are not stored.
+template <int BM, int BN, int STAGES>
+__global__ void __launch_bounds__(256) k_combine_f32_ring(const float *__restrict__ A0, int64_t lda0,
+                                                          const float *__restrict__ A1, int64_t lda1, int64_t M,
+                                                          const int32_t *__restrict__ m_dev, int64_t K,
+                                                          const float *__restrict__ B, int64_t ldb, int64_t bseg,
+                                                          int nseg, int64_t N, int relu, float *__restrict__ C,
+                                                          int64_t ldc) {
+    constexpr int BK = 32, CH = 8, WN = 2;
+    constexpr int WTM = BM / 2, WTN = BN / 2, TM = WTM / 32, TN = WTN / 32;
+    constexpr int A_CH = BM * CH, B_CH = BN * CH, ST = A_CH + B_CH;
+    constexpr int A_IN = A_CH / 256, B_IN = B_CH / 256, PER = A_IN + B_IN;   // DMAs per wavefront and step
+    static_assert(TM >= 1 && TN >= 1 && A_CH % 256 == 0 && B_CH % 256 == 0, "tile shape");
+    static_assert(STAGES >= 2 && STAGES <= 3 && (STAGES - 1) * PER < 64, "ring depth");
+    __shared__ f32x4 S[STAGES * ST];
+
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int wm = wid / WN, wn = wid % WN, h = lane >> 5, lr = lane & 31;
+    if (m_dev) M = *m_dev;
+    int64_t tile_r, tile_c;
+    tile_of((N + BN - 1) / BN, tile_r, tile_c);
+    const int64_t m0 = tile_r * BM, n0 = tile_c * BN;
+    if (m0 >= M) return;
+
+    // slot s = (row, chunk) with chunk stored at (chunk ^ (row & 7)): the
+    // fragment reads below then touch 8 distinct 16-byte bank groups per
+    // 8 lanes.  This wavefront's DMA instruction q fills slots
+    // [(wid * IN + q) * 64, + 64).
+    const float *pa[2][A_IN];
+    int ka[A_IN];
+#pragma unroll
+    for (int q = 0; q < A_IN; ++q) {
+        const int sl = (wid * A_IN + q) * 64 + lane, r = sl / CH;
+        const int64_t row = m0 + r < M ? m0 + r : M - 1;
+        pa[0][q] = A0 + row * lda0;
+        pa[1][q] = A1 + row * lda1;
+        ka[q] = 4 * ((sl % CH) ^ (r & 7));
+    }
+    const float *pb[B_IN];
+    int kb_[B_IN];
+#pragma unroll
+    for (int q = 0; q < B_IN; ++q) {
+        const int sl = (wid * B_IN + q) * 64 + lane, r = sl / CH;
+        const int64_t n = n0 + r < N ? n0 + r : N - 1;
+        pb[q] = B + n * ldb;
+        kb_[q] = 4 * ((sl % CH) ^ (r & 7));
+    }
+    const int64_t kt = (K + BK - 1) / BK, steps = nseg * kt;
+
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    auto issue = [&](int64_t t) {
+        f32x4 *buf = S + (int)(t % STAGES) * ST;
+        const int seg = t >= kt;
+        const int64_t k0 = (seg ? t - kt : t) * BK;
+#pragma unroll
+        for (int q = 0; q < A_IN; ++q) {
+            const int64_t k = k0 + ka[q];
+            dma16(pa[seg][q] + (k < K ? k : 0), &buf[(wid * A_IN + q) * 64]);
+        }
+#pragma unroll
+        for (int q = 0; q < B_IN; ++q) {
+            const int64_t k = k0 + kb_[q];
+            dma16(pb[q] + seg * bseg + (k < K ? k : 0), &buf[A_CH + (wid * B_IN + q) * 64]);
+        }
+    };
+    auto fixup = [&](int64_t t) {
+        const int64_t k0 = (t >= kt ? t - kt : t) * BK;
+        if (k0 + BK <= K) return;
+        float *base = (float *)(S + (int)(t % STAGES) * ST);
+#pragma unroll
+        for (int q = 0; q < A_IN; ++q) {
+            const int64_t k = k0 + ka[q];
+            float *e = base + 4 * ((wid * A_IN + q) * 64 + lane);
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+                if (k + x >= K) e[x] = 0.f;
+        }
+#pragma unroll
+        for (int q = 0; q < B_IN; ++q) {
+            const int64_t k = k0 + kb_[q];
+            float *e = base + 4 * (A_CH + (wid * B_IN + q) * 64 + lane);
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+                if (k + x >= K) e[x] = 0.f;
+        }
+    };
+    // fragment of lane (h, lr) in sub-step u: row lr of its 32-row block,
+    // chunk 2u + h; MFMA x takes element x, so k pairs up across A and B
+    auto compute = [&](int64_t t) {
+        const f32x4 *buf = S + (int)(t % STAGES) * ST;
+#pragma unroll
+        for (int u = 0; u < CH / 2; ++u) {
+            f32x4 a[TM], b[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int r = wm * WTM + i * 32 + lr;
+                a[i] = buf[r * CH + ((2 * u + h) ^ (r & 7))];
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int r = wn * WTN + j * 32 + lr;
+                b[j] = buf[A_CH + r * CH + ((2 * u + h) ^ (r & 7))];
+            }
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][x], b[j][x], acc[i][j], 0, 0, 0);
+        }
+    };
+
+    // every wavefront issues exactly PER DMAs per step, so "stage t landed"
+    // is "at most PER * (steps issued after t) pending"
+#pragma unroll
+    for (int p = 0; p < STAGES - 1; ++p)
+        if (p < steps) issue(p);
+    for (int64_t t = 0; t < steps; ++t) {
+        if (STAGES == 3 && t + 1 < steps) wait_vm<PER>();
+        else wait_vm<0>();
+        fixup(t);
+        lds_barrier();   // stage t visible to all; everyone is done reading stage t - 1
+        if (t + STAGES - 1 < steps) issue(t + STAGES - 1);
+        compute(t);
+    }
+
+    const int64_t r0 = m0 + wm * WTM, c0 = n0 + wn * WTN;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int64_t row = r0 + i * 32 + 8 * (r / 4) + 4 * h + (r % 4), col = c0 + j * 32 + lr;
+                if (row < M && col < N) {
+                    float v = acc[i][j][r];
+                    if (relu) v = fmaxf(v, 0.f);
+                    C[row * ldc + col] = v;
+                }
+            }
 }
 
 // ---------------------------------------------- fp32 main, W as stored
@@ -562,10 +755,10 @@ __global__ void __launch_bounds__(256) k_combine_skinny(const InT *__restrict__ 
 }
 
 // --------------------------------------------------------------- launch
-// The main kernels read the weights transposed to [N][2K]; the copy is made
-// before the kernel runs and lives in one process-wide device buffer.  An
-// event recorded after the last kernel that reads it orders every later
-// call after it, whichever stream that call uses.
+// The ring and bf16 kernels read the weights transposed ([N][2K] rows along
+// k); the copy is made before the kernel runs and lives in one process-wide
+// device buffer.  An event recorded after the last kernel that reads it
+// orders every later call after it, whichever stream that call uses.
 template <class T>
 __global__ void __launch_bounds__(256) k_transpose(const T *__restrict__ src, int64_t rows, int64_t cols,
                                                    T *__restrict__ dst) {
@@ -577,6 +770,18 @@ __global__ void __launch_bounds__(256) k_transpose(const T *__restrict__ src, in
     }
 }
 
+// W [2K][N] -> WT [N][2 * K4] with each K-long segment zero-padded to K4
+// (a multiple of 4), so that every 16-byte chunk the ring kernel starts
+// below K lies inside its row.
+__global__ void __launch_bounds__(256) k_transpose_pad(const float *__restrict__ W, int64_t K, int64_t N, int64_t K4,
+                                                       float *__restrict__ WT) {
+    const int64_t total = N * 2 * K4, stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        const int64_t n = i / (2 * K4), kk = i % (2 * K4), seg = kk / K4, k = kk % K4;
+        WT[i] = k < K ? W[(seg * K + k) * N + n] : 0.f;
+    }
+}
+
 namespace {
 struct SharedWorkspace {
     std::mutex mu;
@@ -584,19 +789,33 @@ struct SharedWorkspace {
     hipEvent_t last_use = nullptr;
 };
 SharedWorkspace g_wt;
+
+enum class Fp32Kernel { kRing, kWrow };
+
+template <int BM, int BN>
+void launch_ring(const float *a0, int64_t lda0, const float *a1, int64_t lda1, int64_t m, const int32_t *m_dev,
+                 int64_t k, const float *b, int64_t ldb, int64_t bseg, int nseg, int64_t n, bool relu, float *out,
+                 int64_t ld_out, hipStream_t s) {
+    const int64_t nrow = (m + BM - 1) / BM, ncol = (n + BN - 1) / BN;
+    const dim3 grid((unsigned)(((nrow + 7) / 8) * 8 * ncol));
+    hipLaunchKernelGGL((k_combine_f32_ring<BM, BN, 2>), grid, dim3(256), 0, s, a0, lda0, a1, lda1, m, m_dev, k, b,
+                       ldb, bseg, nseg, n, (int)relu, out, ld_out);
+}
 }  // namespace
 
-// WROW selects k_combine_f32_wrow for fp32 (no transposed copy of W).
-template <int BM, int BN, int WM, int WN, int BKF, int BKH, bool WROW = false>
+// fp32: KIND picks the ring kernel (weights transposed and padded first) or
+// the W-as-stored kernel.  bf16: the register-staged kernel on transposed
+// weights.
+template <int BM, int BN, int BKH, Fp32Kernel KIND>
 static void launch_main(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
                         const int32_t *m_dev, int64_t k, const void *w, int64_t n, bool bf16, bool relu,
                         bool out_bf16, void *out, int64_t ld_out, hipStream_t s, const char *label) {
     const int64_t nrow = (m + BM - 1) / BM, ncol = (n + BN - 1) / BN;
     const dim3 grid((unsigned)(((nrow + 7) / 8) * 8 * ncol));
-    if (!bf16 && WROW) {
+    if (!bf16 && KIND == Fp32Kernel::kWrow) {
         const int wvec = (((uintptr_t)w & 15u) == 0) && n % 4 == 0;
         KernelTimer tk(label, s);
-        hipLaunchKernelGGL((k_combine_f32_wrow<BM, BN, WM, WN, BKF, float>), grid, dim3(256), 0, s,
+        hipLaunchKernelGGL((k_combine_f32_wrow<BM, BN, 2, 2, 16, float>), grid, dim3(256), 0, s,
                            (const float *)self, ld_self, (const float *)agg, ld_agg, m, m_dev, k, (const float *)w, n,
                            (int)relu, wvec, (float *)out, ld_out);
         return;
@@ -604,31 +823,33 @@ static void launch_main(const void *self, int64_t ld_self, const void *agg, int6
     std::lock_guard<std::mutex> lk(g_wt.mu);
     if (!g_wt.last_use) GNNAV_HIP(hipEventCreateWithFlags(&g_wt.last_use, hipEventDisableTiming));
     GNNAV_HIP(hipStreamWaitEvent(s, g_wt.last_use, 0));
-    g_wt.buf.ensure((size_t)(2 * k * n) * (bf16 ? sizeof(uint16_t) : sizeof(float)), s);
-    const dim3 tgrid(grid_for(2 * k * n, 256, 1024));
     if (!bf16) {
+        const int64_t k4 = (k + 3) / 4 * 4;
+        g_wt.buf.ensure((size_t)(2 * k4 * n) * sizeof(float), s);
         float *wt = g_wt.buf.as<float>();
         {
             KernelTimer tt("weights_transpose", s);
-            hipLaunchKernelGGL(k_transpose<float>, tgrid, dim3(256), 0, s, (const float *)w, 2 * k, n, wt);
+            hipLaunchKernelGGL(k_transpose_pad, dim3(grid_for(2 * k4 * n, 256, 1024)), dim3(256), 0, s,
+                               (const float *)w, k, n, k4, wt);
         }
         KernelTimer tk(label, s);
-        hipLaunchKernelGGL((k_combine_f32<BM, BN, WM, WN, BKF>), grid, dim3(256), 0, s, (const float *)self, ld_self,
-                           (const float *)agg, ld_agg, m, m_dev, k, (const float *)wt, 2 * k, 1, 2, n, (int)relu,
-                           (float *)out, ld_out);
+        launch_ring<BM, BN>((const float *)self, ld_self, (const float *)agg, ld_agg, m, m_dev, k, wt, 2 * k4, k4, 2,
+                            n, relu, (float *)out, ld_out, s);
     } else {
+        g_wt.buf.ensure((size_t)(2 * k * n) * sizeof(uint16_t), s);
         uint16_t *wt = g_wt.buf.as<uint16_t>();
         {
             KernelTimer tt("weights_transpose", s);
-            hipLaunchKernelGGL(k_transpose<uint16_t>, tgrid, dim3(256), 0, s, (const uint16_t *)w, 2 * k, n, wt);
+            hipLaunchKernelGGL(k_transpose<uint16_t>, dim3(grid_for(2 * k * n, 256, 1024)), dim3(256), 0, s,
+                               (const uint16_t *)w, 2 * k, n, wt);
         }
         KernelTimer tk(label, s);
         if (out_bf16)
-            hipLaunchKernelGGL((k_combine_bf16<BM, BN, WM, WN, BKH, uint16_t>), grid, dim3(256), 0, s,
+            hipLaunchKernelGGL((k_combine_bf16<BM, BN, 2, 2, BKH, uint16_t>), grid, dim3(256), 0, s,
                                (const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, k,
                                (const uint16_t *)wt, n, (int)relu, (uint16_t *)out, ld_out);
         else
-            hipLaunchKernelGGL((k_combine_bf16<BM, BN, WM, WN, BKH, float>), grid, dim3(256), 0, s,
+            hipLaunchKernelGGL((k_combine_bf16<BM, BN, 2, 2, BKH, float>), grid, dim3(256), 0, s,
                                (const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, k,
                                (const uint16_t *)wt, n, (int)relu, (float *)out, ld_out);
     }
@@ -645,36 +866,22 @@ struct GemmChoice {
                int64_t, bool, bool, bool, void *, int64_t, hipStream_t, const char *);
 };
 
-// Tile shapes measured on MI355X.  fp32: the chunked kernel with 64 x 128
-// tiles and 32-deep k steps (64 x 64 when the output is at most 64 wide);
-// once there are enough 128 x 128 tiles to give every compute unit two, the
-// W-as-stored kernel with 128 x 128 tiles.  bf16: 64 x 64 until that same
-// 128 x 128 point.
-static GemmChoice choose_main(int64_t m, int64_t d_out, bool bf16) {
-#ifdef GNNAV_GEMM_SWEEP
-    if (const char *e = getenv("GNNAV_GEMM_CFG")) {
-        switch (atoi(e)) {
-            case 1: return {64, 128, launch_main<64, 128, 2, 2, 16, 32>};
-            case 2: return {64, 128, launch_main<64, 128, 2, 2, 32, 64>};
-            case 3: return {128, 64, launch_main<128, 64, 2, 2, 32, 64>};
-            case 4: return {128, 128, launch_main<128, 128, 2, 2, 16, 32>};
-            case 5: return {64, 64, launch_main<64, 64, 2, 2, 16, 32>};
-            case 6: return {64, 64, launch_main<64, 64, 2, 2, 32, 64>};
-            case 8: return {128, 128, launch_main<128, 128, 2, 2, 32, 64>};
-            case 9: return {128, 128, launch_main<128, 128, 2, 2, 16, 32, true>};
-            case 10: return {64, 64, launch_main<64, 64, 2, 2, 16, 32, true>};
-            default: break;
-        }
-    }
-#endif
+// Tile shapes measured on MI355X.  fp32: the ring kernel with 64 x 128 tiles
+// (64 x 64 when the output is at most 64 wide, 128 x 128 once there are
+// enough of those to give every compute unit two); the W-as-stored kernel
+// when such a large output has a short K (at most 128 per segment), where
+// it measured faster (e.g. 10^5 rows of d_in = 100).  bf16: 64 x 64 until
+// that same 128 x 128 point.
+static GemmChoice choose_main(int64_t m, int64_t d_in, int64_t d_out, bool bf16) {
     const bool big = d_out > 64 && ((m + 127) / 128) * ((d_out + 127) / 128) >= 512;
     if (bf16) {
-        if (big) return {128, 128, launch_main<128, 128, 2, 2, 16, 32>};
-        return {64, 64, launch_main<64, 64, 2, 2, 16, 32>};
+        if (big) return {128, 128, launch_main<128, 128, 32, Fp32Kernel::kRing>};
+        return {64, 64, launch_main<64, 64, 32, Fp32Kernel::kRing>};
     }
-    if (big) return {128, 128, launch_main<128, 128, 2, 2, 16, 32, true>};
-    if (d_out <= 64) return {64, 64, launch_main<64, 64, 2, 2, 32, 32>};
-    return {64, 128, launch_main<64, 128, 2, 2, 32, 32>};
+    if (big && d_in <= 128) return {128, 128, launch_main<128, 128, 32, Fp32Kernel::kWrow>};
+    if (big) return {128, 128, launch_main<128, 128, 32, Fp32Kernel::kRing>};
+    if (d_out <= 64) return {64, 64, launch_main<64, 64, 32, Fp32Kernel::kRing>};
+    return {64, 128, launch_main<64, 128, 32, Fp32Kernel::kRing>};
 }
 
 void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
@@ -682,7 +889,7 @@ void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t 
                     int64_t ld_out, hipStream_t s, const char *label) {
     if (m <= 0) return;
     if (!bf16 && out_bf16) fail(GNNAV_E_INVALID, "bf16 output needs bf16 operands");
-    const GemmChoice ch = choose_main(m, d_out, bf16);
+    const GemmChoice ch = choose_main(m, d_in, d_out, bf16);
     const int64_t tiles64 = ((m + 63) / 64) * ((d_out + 63) / 64);
     if (tiles64 < kSkinnyTiles) {
         const dim3 grid((unsigned)((m + 15) / 16), (unsigned)((d_out + 63) / 64));
@@ -711,15 +918,18 @@ void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t 
 void launch_matmul_bt(const float *a, int64_t lda, int64_t m, const int32_t *m_dev, int64_t k, const float *b,
                       int64_t ldb, int64_t n, float *out, int64_t ld_out, hipStream_t s, const char *label) {
     if (m <= 0 || n <= 0) return;
-    const int bvec = (((uintptr_t)b & 15u) == 0) && ldb % 4 == 0;
+    const bool rows16 = (((uintptr_t)a & 15u) == 0) && lda % 4 == 0 && (((uintptr_t)b & 15u) == 0) && ldb % 4 == 0;
     KernelTimer t(label, s);
-    if (n <= 64) {
+    if (rows16) {
+        if (n <= 64)
+            launch_ring<64, 64>(a, lda, a, lda, m, m_dev, k, b, ldb, 0, 1, n, false, out, ld_out, s);
+        else
+            launch_ring<64, 128>(a, lda, a, lda, m, m_dev, k, b, ldb, 0, 1, n, false, out, ld_out, s);
+    } else {
+        // rows not 16-byte aligned (e.g. W^T of a layer with an odd output width)
+        const int bvec = (((uintptr_t)b & 15u) == 0) && ldb % 4 == 0;
         const int64_t nrow = (m + 63) / 64, ncol = (n + 63) / 64;
         hipLaunchKernelGGL((k_combine_f32<64, 64, 2, 2, 32>), dim3((unsigned)(((nrow + 7) / 8) * 8 * ncol)), dim3(256),
-                           0, s, a, lda, a, lda, m, m_dev, k, b, ldb, bvec, 1, n, 0, out, ld_out);
-    } else {
-        const int64_t nrow = (m + 63) / 64, ncol = (n + 127) / 128;
-        hipLaunchKernelGGL((k_combine_f32<64, 128, 2, 2, 32>), dim3((unsigned)(((nrow + 7) / 8) * 8 * ncol)), dim3(256),
                            0, s, a, lda, a, lda, m, m_dev, k, b, ldb, bvec, 1, n, 0, out, ld_out);
     }
     GNNAV_HIP(hipGetLastError());
