@@ -21,7 +21,7 @@
 // stored into the other buffer afterwards, one barrier per step.
 //
 // Skinny kernel (few output rows, e.g. the last layer over the seeds): a
-// workgroup owns 16 x 64 outputs; its four wavefronts take interleaved
+// workgroup owns 16 x 64 outputs; its sixteen wavefronts take interleaved
 // 16- or 32-wide K blocks straight from global memory into MFMA fragments
 // and add their partial tiles in LDS in a fixed order (deterministic).
 //
@@ -715,14 +715,18 @@ struct Skinny<true> {
     }
 };
 
-template <bool BF16, class InT, class OutT>
-__global__ void __launch_bounds__(256) k_combine_skinny(const InT *__restrict__ A0, int64_t lda0,
-                                                        const InT *__restrict__ A1, int64_t lda1, int64_t M,
-                                                        const int32_t *__restrict__ m_dev, int64_t K,
-                                                        const InT *__restrict__ W, int64_t N, int relu,
-                                                        OutT *__restrict__ C, int64_t ldc) {
+// NW wavefronts split the K blocks of both segments round-robin; their
+// partial tiles are added in LDS in wavefront order (deterministic).  With
+// few output rows the kernel is latency-bound, so many wavefronts per tile
+// keep more loads in flight.
+template <bool BF16, class InT, class OutT, int NW>
+__global__ void __launch_bounds__(64 * NW) k_combine_skinny(const InT *__restrict__ A0, int64_t lda0,
+                                                            const InT *__restrict__ A1, int64_t lda1, int64_t M,
+                                                            const int32_t *__restrict__ m_dev, int64_t K,
+                                                            const InT *__restrict__ W, int64_t N, int relu,
+                                                            OutT *__restrict__ C, int64_t ldc) {
     using S = Skinny<BF16>;
-    __shared__ f32x4 part[4][4][64];
+    __shared__ f32x4 part[NW][4][64];
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, g = lane >> 4, l16 = lane & 15;
     if (m_dev) M = *m_dev;
     const int64_t m0 = (int64_t)blockIdx.x * 16, n0 = (int64_t)blockIdx.y * 64;
@@ -733,7 +737,7 @@ __global__ void __launch_bounds__(256) k_combine_skinny(const InT *__restrict__ 
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int64_t kblocks = (K + S::KB - 1) / S::KB;
-    for (int64_t b = wid; b < 2 * kblocks; b += 4) {
+    for (int64_t b = wid; b < 2 * kblocks; b += NW) {
         const bool seg = b >= kblocks;
         const int64_t kb = (seg ? b - kblocks : b) * S::KB;
         S::block(seg ? A1 : A0, seg ? lda1 : lda0, row, row_ok, kb, K, W + (seg ? K : 0) * N, N, n0, g, l16, acc);
@@ -745,8 +749,7 @@ __global__ void __launch_bounds__(256) k_combine_skinny(const InT *__restrict__ 
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             f32x4 s = part[0][j][lane];
-#pragma unroll
-            for (int w = 1; w < 4; ++w) s += part[w][j][lane];
+            for (int w = 1; w < NW; ++w) s += part[w][j][lane];
             acc[j] = s;
         }
         f32x4 t[1][4] = {{acc[0], acc[1], acc[2], acc[3]}};
@@ -770,15 +773,27 @@ __global__ void __launch_bounds__(256) k_transpose(const T *__restrict__ src, in
     }
 }
 
-// W [2K][N] -> WT [N][2 * K4] with each K-long segment zero-padded to K4
-// (a multiple of 4), so that every 16-byte chunk the ring kernel starts
-// below K lies inside its row.
-__global__ void __launch_bounds__(256) k_transpose_pad(const float *__restrict__ W, int64_t K, int64_t N, int64_t K4,
+// W [2K][N] -> WT [N][2 * KP] with each K-long segment zero-padded to KP (a
+// multiple of 32), so that every 16-byte chunk the ring kernel starts below
+// K lies inside its row and every row starts on a 128-byte boundary.  One
+// workgroup moves a 32 (k) x 32 (n) tile through LDS: reads along n and
+// writes along k are both contiguous.
+__global__ void __launch_bounds__(256) k_transpose_pad(const float *__restrict__ W, int64_t K, int64_t N, int64_t KP,
                                                        float *__restrict__ WT) {
-    const int64_t total = N * 2 * K4, stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
-        const int64_t n = i / (2 * K4), kk = i % (2 * K4), seg = kk / K4, k = kk % K4;
-        WT[i] = k < K ? W[(seg * K + k) * N + n] : 0.f;
+    __shared__ float tile[32][33];
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;          // 32 x 8 threads
+    const int64_t n0 = (int64_t)blockIdx.x * 32, kk0 = (int64_t)blockIdx.y * 32;   // kk over [0, 2 KP)
+    const int64_t seg = kk0 / KP, k0 = kk0 - seg * KP;                // a tile never spans segments
+#pragma unroll
+    for (int r = ty; r < 32; r += 8) {
+        const int64_t k = k0 + r, n = n0 + tx;
+        tile[r][tx] = (k < K && n < N) ? W[(seg * K + k) * N + n] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = ty; r < 32; r += 8) {
+        const int64_t n = n0 + r;
+        if (n < N) WT[n * 2 * KP + kk0 + tx] = tile[tx][r];
     }
 }
 
@@ -824,16 +839,16 @@ static void launch_main(const void *self, int64_t ld_self, const void *agg, int6
     if (!g_wt.last_use) GNNAV_HIP(hipEventCreateWithFlags(&g_wt.last_use, hipEventDisableTiming));
     GNNAV_HIP(hipStreamWaitEvent(s, g_wt.last_use, 0));
     if (!bf16) {
-        const int64_t k4 = (k + 3) / 4 * 4;
-        g_wt.buf.ensure((size_t)(2 * k4 * n) * sizeof(float), s);
+        const int64_t kp = (k + 31) / 32 * 32;
+        g_wt.buf.ensure((size_t)(2 * kp * n) * sizeof(float), s);
         float *wt = g_wt.buf.as<float>();
         {
             KernelTimer tt("weights_transpose", s);
-            hipLaunchKernelGGL(k_transpose_pad, dim3(grid_for(2 * k4 * n, 256, 1024)), dim3(256), 0, s,
-                               (const float *)w, k, n, k4, wt);
+            hipLaunchKernelGGL(k_transpose_pad, dim3((unsigned)((n + 31) / 32), (unsigned)(2 * kp / 32)), dim3(256), 0,
+                               s, (const float *)w, k, n, kp, wt);
         }
         KernelTimer tk(label, s);
-        launch_ring<BM, BN>((const float *)self, ld_self, (const float *)agg, ld_agg, m, m_dev, k, wt, 2 * k4, k4, 2,
+        launch_ring<BM, BN>((const float *)self, ld_self, (const float *)agg, ld_agg, m, m_dev, k, wt, 2 * kp, kp, 2,
                             n, relu, (float *)out, ld_out, s);
     } else {
         g_wt.buf.ensure((size_t)(2 * k * n) * sizeof(uint16_t), s);
@@ -866,7 +881,7 @@ struct GemmChoice {
                int64_t, bool, bool, bool, void *, int64_t, hipStream_t, const char *);
 };
 
-// Tile shapes measured on MI355X.  fp32: the ring kernel with 64 x 128 tiles
+// Tile shapes measured on MI355X.  fp32: the ring kernel with 128 x 64 tiles
 // (64 x 64 when the output is at most 64 wide, 128 x 128 once there are
 // enough of those to give every compute unit two); the W-as-stored kernel
 // when such a large output has a short K (at most 128 per segment), where
@@ -881,7 +896,7 @@ static GemmChoice choose_main(int64_t m, int64_t d_in, int64_t d_out, bool bf16)
     if (big && d_in <= 128) return {128, 128, launch_main<128, 128, 32, Fp32Kernel::kWrow>};
     if (big) return {128, 128, launch_main<128, 128, 32, Fp32Kernel::kRing>};
     if (d_out <= 64) return {64, 64, launch_main<64, 64, 32, Fp32Kernel::kRing>};
-    return {64, 128, launch_main<64, 128, 32, Fp32Kernel::kRing>};
+    return {128, 64, launch_main<128, 64, 32, Fp32Kernel::kRing>};
 }
 
 void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
@@ -893,17 +908,18 @@ void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t 
     const int64_t tiles64 = ((m + 63) / 64) * ((d_out + 63) / 64);
     if (tiles64 < kSkinnyTiles) {
         const dim3 grid((unsigned)((m + 15) / 16), (unsigned)((d_out + 63) / 64));
+        constexpr int NW = 16;
         KernelTimer t(label, s);
         if (!bf16)
-            hipLaunchKernelGGL((k_combine_skinny<false, float, float>), grid, dim3(256), 0, s, (const float *)self,
+            hipLaunchKernelGGL((k_combine_skinny<false, float, float, NW>), grid, dim3(64 * NW), 0, s, (const float *)self,
                                ld_self, (const float *)agg, ld_agg, m, m_dev, d_in, (const float *)w, d_out,
                                (int)relu, (float *)out, ld_out);
         else if (out_bf16)
-            hipLaunchKernelGGL((k_combine_skinny<true, uint16_t, uint16_t>), grid, dim3(256), 0, s,
+            hipLaunchKernelGGL((k_combine_skinny<true, uint16_t, uint16_t, NW>), grid, dim3(64 * NW), 0, s,
                                (const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, d_in,
                                (const uint16_t *)w, d_out, (int)relu, (uint16_t *)out, ld_out);
         else
-            hipLaunchKernelGGL((k_combine_skinny<true, uint16_t, float>), grid, dim3(256), 0, s,
+            hipLaunchKernelGGL((k_combine_skinny<true, uint16_t, float, NW>), grid, dim3(64 * NW), 0, s,
                                (const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, d_in,
                                (const uint16_t *)w, d_out, (int)relu, (float *)out, ld_out);
     } else {
@@ -924,7 +940,7 @@ void launch_matmul_bt(const float *a, int64_t lda, int64_t m, const int32_t *m_d
         if (n <= 64)
             launch_ring<64, 64>(a, lda, a, lda, m, m_dev, k, b, ldb, 0, 1, n, false, out, ld_out, s);
         else
-            launch_ring<64, 128>(a, lda, a, lda, m, m_dev, k, b, ldb, 0, 1, n, false, out, ld_out, s);
+            launch_ring<128, 64>(a, lda, a, lda, m, m_dev, k, b, ldb, 0, 1, n, false, out, ld_out, s);
     } else {
         // rows not 16-byte aligned (e.g. W^T of a layer with an odd output width)
         const int bvec = (((uintptr_t)b & 15u) == 0) && ldb % 4 == 0;
