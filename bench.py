@@ -157,7 +157,8 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
     seq = time.perf_counter() - t0
     prof = G.profile_stop()
     losses = loss_hist[args.warmup:].cpu().numpy()
-    pipe = Pipeline(g, c, wtrain, wl.dims, wl.fanouts, "f32", depth=args.depth, eta=args.eta)
+    pipe = Pipeline(g, c, wtrain, wl.dims, wl.fanouts, "f32", depth=args.depth, eta=args.eta,
+                    link_workgroups=args.train_link_workgroups)
     for b in range(args.warmup):
         pipe.enqueue_train(seeds_dev[b], wl.rng_seed(b), labels, args.lr)
     pipe.synchronize()
@@ -168,6 +169,7 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
     pipe.synchronize()
     torch.cuda.synchronize()
     piped = time.perf_counter() - t0
+    c.set_link_workgroups(64)
     log(f"train: sequential {seq * 1e3 / args.steps:.3f} ms/step, pipelined {piped * 1e3 / args.steps:.3f} ms/step, "
         f"loss {losses[0]:.4f} -> {losses[-1]:.4f}")
     # algorithmic work of the backward kernels from the measured sizes
@@ -192,6 +194,7 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
             "value": round(wl.batch * args.steps / piped, 2), "unit": "seeds/s",
             "ms_per_step": round(piped * 1e3 / args.steps, 4),
             "value_sequential": round(wl.batch * args.steps / seq, 2), "lr": args.lr,
+            "pipeline_link_workgroups": args.train_link_workgroups,
             "loss_first": round(float(losses[0]), 6), "loss_last": round(float(losses[-1]), 6),
             "kernels": kernels}
 
@@ -214,6 +217,9 @@ def main():
                     help="locality-biased sampling: cached neighbours weigh eta (default: uniform)")
     ap.add_argument("--no-train", action="store_true", help="skip the training leg")
     ap.add_argument("--lr", type=float, default=0.01, help="SGD step of the training leg")
+    ap.add_argument("--train-link-workgroups", type=int, default=32,
+                    help="host-link workgroups of the pipelined training gathers (fewer slow the batch "
+                         "computing alongside less; the forward legs keep the default 64)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (scales rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()

@@ -128,6 +128,18 @@ gnnav_status gnnav_cache_slot_map_host(const gnnav_cache *c, int32_t *slot_map);
  * (n_cached x ld elements); either may be NULL.  For tests and tooling.   */
 gnnav_status gnnav_cache_contents_host(const gnnav_cache *c, int32_t *owners, void *rows);
 
+/* Number of workgroups of each later gather that copy the uncached rows
+ * from the host store over the host link (zero-copy reads; Section 3.2's
+ * transmission of the misses).  Default 64, which keeps the link at its
+ * measured rate on MI355X.  Every one of their reads waits microseconds in
+ * the memory system, and while they are queued, kernels running alongside
+ * (the previous batch's compute in a pipeline) see their own memory
+ * accesses slow down; a smaller count (e.g. 32) gives up about 3% of the
+ * link rate for much less of that.  Results do not depend on the count.
+ * Host-side setting, read when a gather is enqueued.
+ * Errors: E_INVALID (NULL cache, workgroups outside [1, 4096]).            */
+gnnav_status gnnav_cache_set_link_workgroups(gnnav_cache *c, int32_t workgroups);
+
 /* Cache update policy (the last step of Section 3.2's transmission
  * abstraction: after a batch, the cache is updated by its policy; the cost
  * is Eq. 5's t_replace).  GNNAV_POLICY_STATIC (default) never changes the

@@ -28,7 +28,8 @@ STATUS = {0: "OK", 1: "E_INVALID", 2: "E_RANGE", 3: "E_NOMEM", 4: "E_CAPACITY", 
 EXPORTS = [
     "gnnav_last_error", "gnnav_abi_version", "gnnav_build_csr", "gnnav_graph_info",
     "gnnav_graph_csr_host", "gnnav_graph_free", "gnnav_build_cache", "gnnav_cache_info",
-    "gnnav_cache_slot_map_host", "gnnav_cache_contents_host", "gnnav_cache_set_policy", "gnnav_cache_free", "gnnav_blocks_create", "gnnav_blocks_free",
+    "gnnav_cache_slot_map_host", "gnnav_cache_contents_host", "gnnav_cache_set_policy",
+    "gnnav_cache_set_link_workgroups", "gnnav_cache_free", "gnnav_blocks_create", "gnnav_blocks_free",
     "gnnav_sample", "gnnav_sample_async", "gnnav_sample_biased", "gnnav_blocks_sync", "gnnav_blocks_device_sizes",
     "gnnav_blocks_hop", "gnnav_blocks_nodes", "gnnav_gather", "gnnav_gather_n", "gnnav_gather_n_after",
     "gnnav_aggregate_mean", "gnnav_combine", "gnnav_sage_forward", "gnnav_sage_train_step",
@@ -62,6 +63,7 @@ _sig = {
     "gnnav_cache_slot_map_host": ([P, P], i32),
     "gnnav_cache_contents_host": ([P, P, P], i32),
     "gnnav_cache_set_policy": ([P, i32, i64], i32),
+    "gnnav_cache_set_link_workgroups": ([P, i32], i32),
     "gnnav_cache_free": ([P], None),
     "gnnav_blocks_create": ([P], i32),
     "gnnav_blocks_free": ([P], None),
@@ -185,6 +187,10 @@ class Cache:
         """'static' or 'fifo' over the last `dynamic_slots` cache slots."""
         code = {"static": 0, "fifo": 1}[policy]
         _check(_lib.gnnav_cache_set_policy(self._h, code, int(dynamic_slots)))
+
+    def set_link_workgroups(self, workgroups: int):
+        """Workgroups of later gathers that copy misses over the host link."""
+        _check(_lib.gnnav_cache_set_link_workgroups(self._h, int(workgroups)))
 
     def contents(self):
         """(owners int32[n_cached], rows [n_cached, ld]) currently in the cache."""

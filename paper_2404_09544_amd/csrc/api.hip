@@ -311,6 +311,7 @@ struct gnnav_cache {
     std::vector<int32_t> rank_host;   // degree rank (first C fill the cache)
     std::mutex ws_mu;
     std::vector<GatherWs *> ws;
+    int32_t link_wgs = 64;            // workgroups copying misses over the host link
     // update policy (GNNAV_POLICY_*); FIFO ring over slots [ring_lo, c)
     int32_t policy = 0;
     int64_t ring_lo = 0, ring_n = 0;
@@ -493,6 +494,14 @@ extern "C" gnnav_status gnnav_cache_contents_host(const gnnav_cache *c, int32_t 
         }
         if (rows && c->c > 0)
             GNNAV_HIP(hipMemcpy(rows, c->cache_rows.p, (size_t)(c->c * c->ld * c->elt), hipMemcpyDeviceToHost));
+    });
+}
+
+extern "C" gnnav_status gnnav_cache_set_link_workgroups(gnnav_cache *c, int32_t workgroups) {
+    return guarded([&] {
+        GNNAV_CHECK(c, GNNAV_E_INVALID, "cache is NULL");
+        GNNAV_CHECK(workgroups >= 1 && workgroups <= 4096, GNNAV_E_INVALID, "workgroups outside [1, 4096]");
+        c->link_wgs = workgroups;
     });
 }
 
@@ -806,7 +815,7 @@ static void gather_impl(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_
     w->scan.ensure(n_ids, s);
     GatherArgs a{ids_dev, n_ids, n_dev, c->slot_map.as<int32_t>(), c->n, c->cache_rows.p, c->store_ptr,
                  c->ld * c->elt, out_dev, ld_out * c->elt, c->d * c->elt, counts_dev, w->dev_counts.as<int32_t>(),
-                 w->hit_list.as<int2>(), w->miss_list.as<int2>(), &w->scan};
+                 w->hit_list.as<int2>(), w->miss_list.as<int2>(), &w->scan, cc->link_wgs};
     launch_classify(a, s);
     if (copy_after) GNNAV_HIP(hipStreamWaitEvent(s, copy_after, 0));
     if (n_ids > 0) launch_gather_rows(a, s);

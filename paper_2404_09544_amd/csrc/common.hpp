@@ -195,6 +195,7 @@ struct GatherArgs {
     int2 *hit_list;
     int2 *miss_list;
     ScanState *scan;
+    int32_t miss_wgs;        // workgroups copying misses over the host link
 };
 void launch_classify(const GatherArgs &a, hipStream_t s);
 void launch_gather_rows(const GatherArgs &a, hipStream_t s);

@@ -112,9 +112,9 @@ void launch_gather_rows(const GatherArgs &a, hipStream_t s) {
     if (rows_bound <= 0 || chunks <= 0) return;
     const int rows_per_block = (256 / kWave) * (kWave / g);
     // The miss share needs only enough waves to cover the host link's
-    // latency (64 workgroups keep it at ~53 GB/s); more of them queue slow
-    // host reads in the memory system and stall the HBM copy of the hits.
-    const unsigned miss_blocks = grid_for(rows_bound, rows_per_block, 64);
+    // latency; more of them queue slow host reads in the memory system,
+    // which stalls the HBM copy of the hits and any concurrent kernel.
+    const unsigned miss_blocks = grid_for(rows_bound, rows_per_block, a.miss_wgs);
     const unsigned hit_blocks = grid_for(rows_bound, rows_per_block, 8192);
     const int64_t sld = a.src_ld_bytes / 16, old = a.out_ld_bytes / 16;
     KernelTimer t("gather_rows", s);

@@ -175,12 +175,21 @@ class Pipeline:
     """Batches b, b+1, ... on `depth` streams in turn (slot b % depth)."""
 
     def __init__(self, graph: Graph, cache: Cache, weights_dev, dims, fanouts, dtype: str, depth: int = 2,
-                 eta=None):
+                 eta=None, link_workgroups=None):
+        """link_workgroups: host-link workgroups of this pipeline's gathers
+        (None keeps the cache's setting); fewer slow the batches computing
+        alongside a gather less, at a small cost in link rate."""
         self.slots = [MiniBatchStep(graph, cache, weights_dev, dims, fanouts, dtype, eta=eta) for _ in range(depth)]
         self.streams = pipeline_streams(depth)
         self.depth = depth
         self.count = 0
         self._updated = None
+        self.cache = cache
+        self.link_workgroups = link_workgroups
+
+    def _link(self):
+        if self.link_workgroups is not None:
+            self.cache.set_link_workgroups(self.link_workgroups)
 
     def _previous_gather(self):
         return self.slots[(self.count - 1) % self.depth].gathered if self.count > 0 else None
@@ -188,6 +197,7 @@ class Pipeline:
     def enqueue(self, seeds_dev, rng_seed: int):
         """Enqueue the next batch; returns the slot it runs in."""
         k = self.count % self.depth
+        self._link()
         self.slots[k].enqueue(seeds_dev, rng_seed, self.streams[k], gather_after=self._previous_gather())
         self.count += 1
         return self.slots[k]
@@ -200,6 +210,7 @@ class Pipeline:
         slot, st = self.slots[k], self.streams[k]
         if slot.dtype != "f32":
             raise ValueError("training runs in fp32")
+        self._link()
         slot._inputs(seeds_dev, rng_seed, True, st, gather_after=self._previous_gather())
         if self._updated is not None:
             st.wait_event(self._updated)

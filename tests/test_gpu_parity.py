@@ -242,6 +242,33 @@ def test_gather_device_count(G, wait):
             assert (got[m:] == -5.0).all()
 
 
+def test_gather_link_workgroups(G):
+    """The number of host-link workgroups changes nothing in the result."""
+    import torch
+    n, u, v = graph_case("random-5000-30000-7")
+    csr = O.build_csr(n, u, v)
+    g = G.Graph(n, u, v)
+    feats = W.features(n, 602, "f32", seed=5)
+    c = G.Cache(g, feats, "f32", 0.2)
+    _, slot, _ = O.rank_cache(csr, 0.2)
+    ids = np.random.default_rng(3).integers(0, n, 4000).astype(np.int32)
+    ids_d = dev(ids)
+    ref_rows, ref_counts = O.gather(feats, slot, ids)
+    for wgs in (1, 3, 32, 64, 4096):
+        say("gather link workgroups", wgs)
+        c.set_link_workgroups(wgs)
+        out = torch.full((ids.size, c.ld), -7.0, device="cuda")
+        counts = torch.zeros(3, dtype=torch.int64, device="cuda")
+        G.gather(c, ids_d.data_ptr(), ids.size, out, counts)
+        assert np.array_equal(host(counts), ref_counts)
+        assert np.array_equal(host(out)[:, :602].view(np.uint8), ref_rows.view(np.uint8))
+    for bad in (0, 4097, -1):
+        with pytest.raises(G.GnnavError) as e:
+            c.set_link_workgroups(bad)
+        assert e.value.status == 1
+    c.set_link_workgroups(64)
+
+
 def test_gather_empty_and_errors(G):
     import torch
     n, u, v = graph_case("path")

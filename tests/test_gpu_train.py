@@ -278,10 +278,12 @@ def test_train_pipeline_matches_sequential(G):
         step.train(seeds[b], wl.rng_seed(b), lab, 0.3, async_mode=True)
         torch.cuda.synchronize()
         seq_losses.append(float(host(step.loss)[0]))
-    w_pipe = to_device_weights(ws, "f32")
-    pipe = Pipeline(g, c, w_pipe, wl.dims, wl.fanouts, "f32", depth=2)
-    slots = [pipe.enqueue_train(seeds[b], wl.rng_seed(b), lab, 0.3) for b in range(6)]
-    pipe.synchronize()
-    for a, b in zip(w_seq, w_pipe):
-        assert np.array_equal(host(a), host(b))
-    assert float(host(slots[-1].loss)[0]) == seq_losses[-1]
+    for link in (None, 32, 1):
+        w_pipe = to_device_weights(ws, "f32")
+        pipe = Pipeline(g, c, w_pipe, wl.dims, wl.fanouts, "f32", depth=2, link_workgroups=link)
+        slots = [pipe.enqueue_train(seeds[b], wl.rng_seed(b), lab, 0.3) for b in range(6)]
+        pipe.synchronize()
+        for a, b in zip(w_seq, w_pipe):
+            assert np.array_equal(host(a), host(b))
+        assert float(host(slots[-1].loss)[0]) == seq_losses[-1]
+    c.set_link_workgroups(64)
