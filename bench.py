@@ -208,6 +208,8 @@ def main():
     ap.add_argument("--cache-fraction", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-batches", type=int, default=2)
+    ap.add_argument("--cpu-threads", type=int, default=16,
+                    help="cap on the threads of the all-core oracle baseline")
     ap.add_argument("--depth", type=int, default=2, help="streams in the pipelined pass")
     ap.add_argument("--cache-policy", choices=["static", "fifo"], default="static",
                     help="fifo: admit each batch's misses into a ring over the last cache slots")
@@ -255,6 +257,13 @@ def main():
     c = G.Cache(g, feats, wl.dtype, r, store_on_device=wl.cfg["store_on_device"])
     log(f"graph nnz={g.nnz} max_deg={g.max_degree}; cache C={c.n_cached} ld={c.ld} "
         f"({time.perf_counter() - t0:.1f}s)")
+    rp, _ = g.csr_host(with_col=False)
+    deg = np.diff(rp)
+    top = np.sort(deg)[::-1][:c.n_cached].sum() if c.n_cached else 0
+    graph_stats = {"n": wl.n, "nnz": g.nnz, "deg_min": int(deg.min()), "deg_mean": round(float(deg.mean()), 2),
+                   "deg_max": int(deg.max()), "cached_rows": c.n_cached,
+                   "nnz_share_of_cached_rows": round(float(top) / max(g.nnz, 1), 4)}
+    del rp, deg
     link = link_calibration(G, c, wl, torch)
     log(f"host link: DMA {link['dma_h2d_gbs']} GB/s, zero-copy gather of uncached rows {link['zero_copy_gather_gbs']} GB/s")
     ring = 0
@@ -290,13 +299,18 @@ def main():
     torch.cuda.synchronize()
     G.profile_start()
     torch.cuda.synchronize()
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t_start = time.perf_counter()
+    marks[0].record(stream)
     for b in range(args.warmup, n_b):
         step.enqueue(seeds_dev[b], wl.rng_seed(b), stream)
         record(step, b, stream, seq_counts_hist)
+        marks[b - args.warmup + 1].record(stream)
     torch.cuda.synchronize()
     t_end = time.perf_counter()
     prof = G.profile_stop()
+    prof_samples = G.profile_samples()
+    batch_ms = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)])
     seq_elapsed = t_end - t_start
     seq_ms = seq_elapsed * 1e3 / args.steps
     log(f"sequential {args.steps} steps: {seq_ms:.3f} ms/step, {wl.batch * args.steps / seq_elapsed:,.0f} seeds/s")
@@ -360,6 +374,10 @@ def main():
     for name, (launches, ms) in prof.items():
         kernels[name] = {"launches": launches, "total_ms": round(ms, 4),
                          "avg_us": round(ms * 1e3 / max(launches, 1), 3)}
+        smp = prof_samples.get(name)
+        if smp is not None and smp.size:
+            q = np.percentile(smp.astype(np.float64) * 1e3, [10, 50, 90])
+            kernels[name].update({"p10_us": round(q[0], 3), "median_us": round(q[1], 3), "p90_us": round(q[2], 3)})
     rows = []
     for name in work:
         if name not in prof:
@@ -406,6 +424,7 @@ def main():
 
     # ---- CPU baseline: the oracle on a bounded sample of the same batches --
     cpu = None
+    cpu_all = None
     if not args.no_cpu_baseline:
         import oracle as O
         t0 = time.perf_counter()
@@ -427,6 +446,27 @@ def main():
                "sample": f"{nb} batch(es) of {wl.batch} seeds of {wl.name} (batches {args.warmup}.."
                          f"{args.warmup + nb - 1}), single-threaded C oracle, {ct:.1f}s"}
         log(f"oracle: {cpu['value']} seeds/s")
+        # all host cores: independent batches on P threads (the C oracle
+        # releases the interpreter lock), P = the cores this process may use
+        P = max(1, min(len(os.sched_getaffinity(0)), args.cpu_threads))
+
+        def one(b):
+            bias = None if args.eta is None else (fifo.slot_map if fifo else slot)
+            ob = O.sample_blocks(csr, wl.seeds(b), wl.fanouts, wl.rng_seed(b), bias_slot_map=bias,
+                                 eta=args.eta or 1)
+            h0, _ = O.gather(feats, slot, ob.nodes)
+            O.sage_forward(ob, O.to_f64(h0, wl.dtype), wd, bf16=wl.dtype == "bf16")
+
+        if P > 1 and fifo is None:
+            import concurrent.futures as cf
+            t0 = time.perf_counter()
+            with cf.ThreadPoolExecutor(max_workers=P) as ex:
+                list(ex.map(one, [args.warmup + (i % args.steps) for i in range(P)]))
+            ct = time.perf_counter() - t0
+            cpu_all = {"value": round(wl.batch * P / ct, 2), "unit": "seeds/s", "cores": P, "kind": "oracle",
+                       "sample": f"{P} batches of {wl.batch} seeds of {wl.name}, one per thread, "
+                                 f"single-threaded C oracle on each, {ct:.1f}s"}
+            log(f"oracle on {P} threads: {cpu_all['value']} seeds/s")
 
     # Eq. 4 terms per batch from the sequential region: the host-link part
     # (t_transfer = miss copy), the sampling kernels, and the device compute.
@@ -456,11 +496,16 @@ def main():
         "value_sequential": round(wl.batch * args.steps / seq_elapsed, 2),
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "cpu_baseline_all_cores": cpu_all,
         "kernels": kernels,
         "eq4": eq4,
         "locality": locality,
         "train": train,
         "host_link_calibration": link,
+        "graph": graph_stats,
+        "sequential_batch_ms": {"median": round(float(np.median(batch_ms)), 4),
+                                "p10": round(float(np.percentile(batch_ms, 10)), 4),
+                                "p90": round(float(np.percentile(batch_ms, 90)), 4)},
         "batch_stats": {"mean_frontier_sizes": mean_sizes, "hit_rate": round(hit_rate, 4),
                         "hit_rate_sequential": round(float(seq_counts[:, 0].sum() / max(seq_counts[:, :2].sum(), 1)), 4),
                         "miss_bytes_per_batch": round(float(counts[:, 1].mean()) * wl.d * elt, 1)},

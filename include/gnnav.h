@@ -92,7 +92,8 @@ gnnav_status gnnav_graph_info(const gnnav_graph *g, int64_t *n_nodes, int64_t *n
                               int64_t *max_degree, int32_t *offsets_i64);
 
 /* Host copies of the CSR: row_ptr (int64, n_nodes+1 entries) and col
- * (int32, nnz entries), caller-allocated.  For tests and tooling.        */
+ * (int32, nnz entries; NULL skips it), caller-allocated.  For tests and
+ * tooling.  Errors: E_INVALID (g or row_ptr NULL), E_DEVICE.              */
 gnnav_status gnnav_graph_csr_host(const gnnav_graph *g, int64_t *row_ptr, int32_t *col);
 
 void gnnav_graph_free(gnnav_graph *g);
@@ -402,6 +403,12 @@ gnnav_status gnnav_profile_stop(void);
 int32_t gnnav_profile_count(void);
 gnnav_status gnnav_profile_get(int32_t i, char *name, int32_t name_cap, int64_t *launches,
                                double *total_ms);
+
+/* Per-launch durations (ms, launch order) of recorded kernel i after
+ * gnnav_profile_stop: copies min(cap, count) of them to ms and the count
+ * to *n (n may be NULL).  Errors: E_INVALID (i out of range, ms NULL with
+ * cap > 0).                                                                */
+gnnav_status gnnav_profile_samples(int32_t i, float *ms, int64_t cap, int64_t *n);
 
 #ifdef __cplusplus
 }

@@ -34,7 +34,7 @@ EXPORTS = [
     "gnnav_blocks_hop", "gnnav_blocks_nodes", "gnnav_gather", "gnnav_gather_n", "gnnav_gather_n_after",
     "gnnav_aggregate_mean", "gnnav_combine", "gnnav_sage_forward", "gnnav_sage_train_step",
     "gnnav_softmax_xent", "gnnav_aggregate_mean_backward", "gnnav_weight_grad", "gnnav_profile_start",
-    "gnnav_profile_stop", "gnnav_profile_count", "gnnav_profile_get",
+    "gnnav_profile_stop", "gnnav_profile_count", "gnnav_profile_get", "gnnav_profile_samples",
 ]
 
 
@@ -88,6 +88,7 @@ _sig = {
     "gnnav_profile_stop": ([], i32),
     "gnnav_profile_count": ([], i32),
     "gnnav_profile_get": ([i32, P, i32, P, P], i32),
+    "gnnav_profile_samples": ([i32, P, i64, P], i32),
 }
 for _name, (_args, _res) in _sig.items():
     _f = getattr(_lib, _name)
@@ -145,11 +146,11 @@ class Graph:
         _check(_lib.gnnav_graph_info(h, C.byref(n), C.byref(nnz), C.byref(md), C.byref(o64)))
         self.n, self.nnz, self.max_degree, self.offsets_i64 = n.value, nnz.value, md.value, bool(o64.value)
 
-    def csr_host(self):
+    def csr_host(self, with_col: bool = True):
         rp = np.empty(self.n + 1, np.int64)
-        col = np.empty(max(self.nnz, 1), np.int32)
-        _check(_lib.gnnav_graph_csr_host(self._h, _np_ptr(rp), _np_ptr(col)))
-        return rp, col[:self.nnz]
+        col = np.empty(max(self.nnz, 1), np.int32) if with_col else None
+        _check(_lib.gnnav_graph_csr_host(self._h, _np_ptr(rp), _np_ptr(col) if with_col else None))
+        return rp, (col[:self.nnz] if with_col else None)
 
     def close(self):
         if getattr(self, "_h", None) and _lib is not None:
@@ -413,6 +414,20 @@ def sage_forward(blocks: Blocks, x, weights, dims, dtype: str, logits, stream=No
 # -------------------------------------------------------------- profiling
 def profile_start():
     _check(_lib.gnnav_profile_start())
+
+
+def profile_samples() -> dict:
+    """After profile_stop: {kernel name: float32 array of per-launch ms}."""
+    out = {}
+    buf = C.create_string_buffer(128)
+    for i in range(_lib.gnnav_profile_count()):
+        n = i64()
+        _check(_lib.gnnav_profile_get(i, buf, 128, None, None))
+        _check(_lib.gnnav_profile_samples(i, None, 0, C.byref(n)))
+        ms = np.empty(max(n.value, 1), np.float32)
+        _check(_lib.gnnav_profile_samples(i, _np_ptr(ms), n.value, None))
+        out[buf.value.decode()] = ms[:n.value]
+    return out
 
 
 def profile_stop() -> dict:

@@ -54,6 +54,7 @@ struct ProfEntry {
     std::string name;
     int64_t launches = 0;
     double ms = 0;
+    std::vector<float> samples;   // per-launch durations, in launch order
 };
 struct Pending {
     int slot;
@@ -87,7 +88,7 @@ KernelTimer::KernelTimer(const char *name, hipStream_t s) : stream(s) {
     for (size_t i = 0; i < g_prof.size(); ++i)
         if (g_prof[i].name == name) idx = (int)i;
     if (idx < 0) {
-        g_prof.push_back(ProfEntry{name, 0, 0});
+        g_prof.push_back(ProfEntry{name, 0, 0, {}});
         idx = (int)g_prof.size() - 1;
     }
     Pending p{idx, take_event(), take_event()};
@@ -138,6 +139,7 @@ extern "C" gnnav_status gnnav_profile_stop(void) {
             float ms = 0;
             GNNAV_HIP(hipEventElapsedTime(&ms, p.a, p.b));
             g_prof[p.slot].ms += ms;
+            g_prof[p.slot].samples.push_back(ms);
             g_event_pool.push_back(p.a);
             g_event_pool.push_back(p.b);
         }
@@ -161,6 +163,18 @@ extern "C" gnnav_status gnnav_profile_get(int32_t i, char *name, int32_t name_ca
         }
         if (launches) *launches = g_prof[i].launches;
         if (total_ms) *total_ms = g_prof[i].ms;
+    });
+}
+
+extern "C" gnnav_status gnnav_profile_samples(int32_t i, float *ms, int64_t cap, int64_t *n) {
+    return guarded([&] {
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        GNNAV_CHECK(i >= 0 && i < (int32_t)g_prof.size(), GNNAV_E_INVALID, "profile index out of range");
+        GNNAV_CHECK(cap >= 0 && (cap == 0 || ms), GNNAV_E_INVALID, "NULL output with cap > 0");
+        const auto &v = g_prof[i].samples;
+        const int64_t k = std::min<int64_t>(cap, (int64_t)v.size());
+        if (k > 0) std::memcpy(ms, v.data(), (size_t)k * sizeof(float));
+        if (n) *n = (int64_t)v.size();
     });
 }
 
@@ -274,9 +288,9 @@ extern "C" gnnav_status gnnav_graph_info(const gnnav_graph *g, int64_t *n_nodes,
 
 extern "C" gnnav_status gnnav_graph_csr_host(const gnnav_graph *g, int64_t *row_ptr, int32_t *col) {
     return guarded([&] {
-        GNNAV_CHECK(g && row_ptr && col, GNNAV_E_INVALID, "NULL argument");
+        GNNAV_CHECK(g && row_ptr, GNNAV_E_INVALID, "NULL argument");
         std::memcpy(row_ptr, g->row_ptr_host.data(), (g->n + 1) * sizeof(int64_t));
-        if (g->nnz > 0) GNNAV_HIP(hipMemcpy(col, g->col.p, g->nnz * sizeof(int32_t), hipMemcpyDeviceToHost));
+        if (col && g->nnz > 0) GNNAV_HIP(hipMemcpy(col, g->col.p, g->nnz * sizeof(int32_t), hipMemcpyDeviceToHost));
     });
 }
 

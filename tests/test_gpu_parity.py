@@ -269,6 +269,31 @@ def test_gather_link_workgroups(G):
     c.set_link_workgroups(64)
 
 
+def test_profile_records_every_launch(G):
+    """Recording counts each timed launch once; per-launch durations add up
+    to the total and the CSR row pointers come back without the columns."""
+    import torch
+    n, u, v = graph_case("random-3000-40000-1")
+    csr = O.build_csr(n, u, v)
+    g = G.Graph(n, u, v)
+    rp, col = g.csr_host(with_col=False)
+    assert col is None and np.array_equal(rp, csr.row_ptr)
+    c = G.Cache(g, W.features(n, 16, "f32"), "f32", 0.5)
+    ids = dev(np.arange(0, n, 2, dtype=np.int32))
+    out = torch.zeros((ids.numel(), c.ld), device="cuda")
+    counts = torch.zeros(3, dtype=torch.int64, device="cuda")
+    G.profile_start()
+    for _ in range(5):
+        G.gather(c, ids.data_ptr(), ids.numel(), out, counts)
+    prof = G.profile_stop()
+    smp = G.profile_samples()
+    assert prof["gather_rows"][0] == 5 and prof["classify"][0] == 5
+    for name, (launches, ms) in prof.items():
+        assert smp[name].size == launches
+        assert abs(float(smp[name].astype(np.float64).sum()) - ms) <= 1e-3 * max(ms, 1e-3)
+        assert (smp[name] >= 0).all()
+
+
 def test_gather_empty_and_errors(G):
     import torch
     n, u, v = graph_case("path")
