@@ -48,7 +48,7 @@ def kernel_source_hash(files) -> str:
 
 KERNEL_SOURCES = {"aggregate_mean": ["spmm.hip", "common.hpp"],
                   "gather_rows": ["gather.hip", "common.hpp"],
-                  "combine_gemm": ["gemm.hip", "common.hpp"]}
+                  "combine_gemm": ["gemm.hip", "common.hpp", "dma.hpp"]}
 
 
 def traffic_for(kernel: str, workload: str):

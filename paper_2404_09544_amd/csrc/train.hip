@@ -20,6 +20,7 @@
 #include <algorithm>
 
 #include "common.hpp"
+#include "dma.hpp"
 #include "scan.hpp"
 
 namespace gnnav {
@@ -469,6 +470,132 @@ __global__ void __launch_bounds__(256) k_wgrad(const float *__restrict__ X0, int
             }
 }
 
+// Ring form of the weight gradient (rows 16-byte aligned): the same
+// partial tile as k_wgrad, with both operands moved row by row (k = row m)
+// straight from global memory into LDS by global_load_lds_dwordx4 through a
+// two-stage ring, and 32x32x2 MFMAs.  LDS holds Xs[m][a] and Gs[m][o] as
+// stored, 16-byte chunk c of row m at c ^ 8 (m & 1), so the fragment reads
+// (lane (h, r): row 2u + h, column r of its 32-wide block, one float) touch
+// 64 distinct banks.  Rows past the split's end load a valid row; the lanes
+// that loaded G chunks for them zero those in LDS before the barrier, so
+// they add nothing.  Columns past d_in or d_out only reach outputs that are
+// not stored.
+template <int BA, int BO>
+__global__ void __launch_bounds__(256) k_wgrad_ring(const float *__restrict__ X0, int64_t ldx0,
+                                                    const float *__restrict__ X1, int64_t ldx1, int64_t M,
+                                                    const int32_t *__restrict__ m_dev, int64_t d_in,
+                                                    const float *__restrict__ Gm, int64_t ldg, int64_t d_out,
+                                                    int64_t splits, float *__restrict__ part) {
+    typedef float f32x16 __attribute__((ext_vector_type(16)));
+    constexpr int BK = 32, XC = BA / 4, GC = BO / 4;                 // chunks per row
+    constexpr int X_CH = BK * XC, G_CH = BK * GC, ST = X_CH + G_CH;
+    constexpr int X_IN = X_CH / 256, G_IN = G_CH / 256;              // DMAs per wavefront and step
+    constexpr int WTA = BA / 2, WTO = BO / 2, TM = WTA / 32, TN = WTO / 32;
+    static_assert(X_CH % 256 == 0 && G_CH % 256 == 0 && TM >= 1 && TN >= 1 && XC >= 16 && GC >= 16, "tile");
+    __shared__ f32x4 S[2 * ST];
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int wa = wid >> 1, wo = wid & 1, h = lane >> 5, lr = lane & 31;
+    if (m_dev) M = *m_dev;
+    const int64_t na = (d_in + BA - 1) / BA, no = (d_out + BO - 1) / BO;
+    const int64_t tile = blockIdx.x, split = blockIdx.y;
+    const int seg = (int)(tile / (na * no));
+    const int64_t a0 = ((tile / no) % na) * BA, o0 = (tile % no) * BO;
+    const float *X = seg ? X1 : X0;
+    const int64_t ldx = seg ? ldx1 : ldx0;
+    const int64_t per = ((M + splits - 1) / splits + BK - 1) / BK * BK;
+    const int64_t m_lo = split * per, m_hi = std::min<int64_t>(M, m_lo + per);
+    const int64_t steps = m_hi > m_lo ? (m_hi - m_lo + BK - 1) / BK : 0;
+
+    // this lane's chunk in each DMA instruction: (row within the step, column)
+    int xr[X_IN], xa[X_IN], gr[G_IN], go[G_IN];
+#pragma unroll
+    for (int q = 0; q < X_IN; ++q) {
+        const int pos = (wid * X_IN + q) * 64 + lane, r = pos / XC;
+        xr[q] = r;
+        xa[q] = 4 * ((pos % XC) ^ (8 * (r & 1)));
+    }
+#pragma unroll
+    for (int q = 0; q < G_IN; ++q) {
+        const int pos = (wid * G_IN + q) * 64 + lane, r = pos / GC;
+        gr[q] = r;
+        go[q] = 4 * ((pos % GC) ^ (8 * (r & 1)));
+    }
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    auto issue = [&](int64_t t) {
+        f32x4 *buf = S + (int)(t & 1) * ST;
+        const int64_t mb = m_lo + t * BK;
+#pragma unroll
+        for (int q = 0; q < X_IN; ++q) {
+            const int64_t m = mb + xr[q] < m_hi ? mb + xr[q] : m_lo;
+            const int64_t a = a0 + xa[q];
+            dma16(X + m * ldx + (a < d_in ? a : 0), &buf[(wid * X_IN + q) * 64]);
+        }
+#pragma unroll
+        for (int q = 0; q < G_IN; ++q) {
+            const int64_t m = mb + gr[q] < m_hi ? mb + gr[q] : m_lo;
+            const int64_t o = o0 + go[q];
+            dma16(Gm + m * ldg + (o < d_out ? o : 0), &buf[X_CH + (wid * G_IN + q) * 64]);
+        }
+    };
+    auto fixup = [&](int64_t t) {
+        const int64_t mb = m_lo + t * BK;
+        if (mb + BK <= m_hi) return;
+        f32x4 *buf = S + (int)(t & 1) * ST;
+#pragma unroll
+        for (int q = 0; q < G_IN; ++q)
+            if (mb + gr[q] >= m_hi) buf[X_CH + (wid * G_IN + q) * 64 + lane] = f32x4{0.f, 0.f, 0.f, 0.f};
+    };
+    auto at = [&](int row, int col, int chunks) {       // float index of (row, col) in a k-major block
+        return (row * chunks + ((col >> 2) ^ (8 * (row & 1)))) * 4 + (col & 3);
+    };
+    auto compute = [&](int64_t t) {
+        const float *xs = (const float *)(S + (int)(t & 1) * ST);
+        const float *gs = xs + 4 * X_CH;
+#pragma unroll
+        for (int u = 0; u < BK / 2; ++u) {
+            const int row = 2 * u + h;
+            float a[TM], b[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) a[i] = xs[at(row, wa * WTA + i * 32 + lr, XC)];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) b[j] = gs[at(row, wo * WTO + j * 32 + lr, GC)];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+    };
+    if (steps > 0) {
+        issue(0);
+        for (int64_t t = 0; t < steps; ++t) {
+            wait_vm<0>();
+            fixup(t);
+            lds_barrier();           // step t visible; everyone is done with step t - 1
+            if (t + 1 < steps) issue(t + 1);
+            compute(t);
+        }
+    }
+    float *P = part + split * (2 * d_in * d_out);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int64_t a = a0 + wa * WTA + i * 32 + 8 * (r / 4) + 4 * h + (r % 4);
+                const int64_t o = o0 + wo * WTO + j * 32 + lr;
+                if (a < d_in && o < d_out) P[(seg * d_in + a) * d_out + o] = acc[i][j][r];
+            }
+}
+
 // dW = sum of the split partials in split order; optionally copied out, and
 // W -= lr * dW when lr != 0.
 __global__ void __launch_bounds__(256) k_wgrad_reduce(const float *__restrict__ part, int64_t total, int64_t splits,
@@ -485,7 +612,10 @@ __global__ void __launch_bounds__(256) k_wgrad_reduce(const float *__restrict__ 
 void launch_wgrad(const float *x_self, int64_t ld_self, const float *agg, int64_t ld_agg, int64_t m,
                   const int32_t *m_dev, int64_t d_in, const float *dz, int64_t ld_dz, int64_t d_out, DevBuf &part,
                   float *dw, float *w, float lr, hipStream_t s, const char *label) {
-    constexpr int BA = 64, BO = 64, BK = 32;
+    auto a16 = [](const void *p, int64_t ld) { return (((uintptr_t)p & 15u) == 0) && ld % 4 == 0; };
+    const bool ring = a16(x_self, ld_self) && a16(agg, ld_agg) && a16(dz, ld_dz);
+    // ring: 128 x 64 tiles; otherwise the register-staged 64 x 64 kernel
+    const int64_t BA = ring ? 128 : 64, BO = 64;
     const int64_t tiles = 2 * ((d_in + BA - 1) / BA) * ((d_out + BO - 1) / BO);
     int64_t splits = (512 + tiles - 1) / tiles;
     splits = std::min<int64_t>(splits, std::max<int64_t>(1, (m + 255) / 256));
@@ -494,8 +624,14 @@ void launch_wgrad(const float *x_self, int64_t ld_self, const float *agg, int64_
     part.ensure((size_t)(splits * total) * sizeof(float), s);
     {
         KernelTimer t(label, s);
-        hipLaunchKernelGGL((k_wgrad<BA, BO, BK>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, s, x_self,
-                           ld_self, agg, ld_agg, m, m_dev, d_in, dz, ld_dz, d_out, splits, part.as<float>());
+        if (ring)
+            hipLaunchKernelGGL((k_wgrad_ring<128, 64>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, s,
+                               x_self, ld_self, agg, ld_agg, m, m_dev, d_in, dz, ld_dz, d_out, splits,
+                               part.as<float>());
+        else
+            hipLaunchKernelGGL((k_wgrad<64, 64, 32>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, s,
+                               x_self, ld_self, agg, ld_agg, m, m_dev, d_in, dz, ld_dz, d_out, splits,
+                               part.as<float>());
     }
     {
         KernelTimer t("wgrad_reduce", s);
