@@ -101,6 +101,46 @@ def link_calibration(G, cache, wl, torch):
     return out
 
 
+def device_calibration(torch, m: int, k: int, n: int, dtype: str):
+    """Context for the roofline fractions on this machine: a plain 1 GiB HBM
+    copy, and the vendor library's GEMM (torch.mm, hipBLASLt; fp32 without
+    reduced-precision shortcuts) on the layer-1 combine shape [m, k] x [k, n]."""
+    out = {}
+    x = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    y.copy_(x)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(5):
+        y.copy_(x)
+    e1.record()
+    torch.cuda.synchronize()
+    out["hbm_copy_gbs"] = round(5 * 2 * x.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
+    del x, y
+    if m > 0:
+        tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+        prev = torch.backends.cuda.matmul.allow_tf32
+        torch.backends.cuda.matmul.allow_tf32 = False
+        a = torch.randn((m, k), device="cuda").to(tdt)
+        b = torch.randn((k, n), device="cuda").to(tdt)
+        for _ in range(3):
+            torch.mm(a, b)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(20):
+            torch.mm(a, b)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / 20
+        tf = 2.0 * m * k * n / (us * 1e-6) / 1e12
+        out["library_gemm"] = {"shape": [m, k, n], "dtype": dtype, "us": round(us, 2), "tflops": round(tf, 2),
+                               "frac": round(tf / MFMA_PEAK_TFLOPS[dtype], 4)}
+        torch.backends.cuda.matmul.allow_tf32 = prev
+        del a, b
+    return out
+
+
 def locality_report(args, G, g, c, wl, seeds_dev, torch, batches=5):
     """Biased against uniform sampling on the first timed batches (untimed):
     the hit rate of F_L and the share of sampled picks that land on cached
@@ -346,6 +386,7 @@ def main():
     work = {"gather_rows": 0.0, "cache_admit": 0.0}
     hit_bytes = miss_bytes = 0.0
     edge = {}
+    gemm_bytes = {}
     probe = G.Blocks()
     for i, b in enumerate(range(args.warmup, n_b)):
         sz = sizes_hist[i]
@@ -366,6 +407,10 @@ def main():
             work[ka] = work.get(ka, 0.0) + u * din * elt + n_dst * din * elt + 4 * (E + n_dst + 1)
             edge[ka] = edge.get(ka, 0.0) + E * din * elt + n_dst * din * elt + 4 * (E + n_dst + 1)
             work[kg] = work.get(kg, 0.0) + 2.0 * n_dst * (2 * din) * dout
+            # the GEMM's compulsory bytes: both A segments, W, the output (hidden
+            # layers in the compute dtype, logits in fp32)
+            out_elt = elt if l < L else 4
+            gemm_bytes[kg] = gemm_bytes.get(kg, 0.0) + (n_dst * 2 * din + 2 * din * dout) * elt + n_dst * dout * out_elt
     probe.close()
     link_bound = miss_bytes > 0
     work["gather_rows"] = miss_bytes if link_bound else hit_bytes
@@ -385,16 +430,25 @@ def main():
         if name == "gather_rows" and link_bound:
             bound, peak, unit = "host_link", HOST_LINK_PEAK_GBS, "GB/s"
         elif name.startswith("combine_gemm"):
-            bound, peak, unit = "mfma", MFMA_PEAK_TFLOPS[wl.dtype], "TFLOP/s"
+            # MFMA-bound when its flops per compulsory byte exceed the ridge
+            # point peak_flops / HBM bandwidth, else HBM-bound
+            ridge = MFMA_PEAK_TFLOPS[wl.dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
+            if work[name] / max(gemm_bytes.get(name, 1.0), 1.0) >= ridge:
+                bound, peak, unit = "mfma", MFMA_PEAK_TFLOPS[wl.dtype], "TFLOP/s"
+            else:
+                bound, peak, unit = "hbm", HBM_PEAK_GBS, "GB/s"
         else:
             bound, peak, unit = "hbm", HBM_PEAK_GBS, "GB/s"
         launches, ms = prof[name]
-        amount = work[name]
+        amount = gemm_bytes[name] if name.startswith("combine_gemm") and bound == "hbm" else work[name]
         achieved = amount / (ms * 1e-3) / (1e12 if unit == "TFLOP/s" else 1e9)
         ent = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
                "frac": round(achieved / peak, 4), "per_launch": round(amount / max(launches, 1), 1)}
         if name in edge:
             ent["achieved_edge_effective"] = round(edge[name] / (ms * 1e-3) / 1e9, 2)
+        if name.startswith("combine_gemm"):
+            ent["tflops"] = round(work[name] / (ms * 1e-3) / 1e12, 2)
+            ent["flop_per_byte"] = round(work[name] / max(gemm_bytes.get(name, 1.0), 1.0), 1)
         if name == "gather_rows" and link_bound:
             if link.get("zero_copy_gather_gbs"):
                 ent["frac_of_measured_link"] = round(achieved / link["zero_copy_gather_gbs"], 4)
@@ -410,6 +464,11 @@ def main():
         k = kernels[dom]
         roofline = {"kernel": dom, "bound": k["bound"], "achieved": k["achieved"], "peak": k["peak"],
                     "unit": k["unit"], "frac": k["frac"], "traffic": traffic_for(dom, wl.name)}
+
+    m1 = int(round(float(np.mean([sz[L - 1] for sz in sizes_hist])))) if sizes_hist else 0
+    device_cal = device_calibration(torch, m1, 2 * wl.dims[0], wl.dims[1], wl.dtype)
+    if roofline is not None and roofline["kernel"] == "combine_gemm.l1" and device_cal.get("library_gemm"):
+        roofline["library_frac_same_shape"] = device_cal["library_gemm"]["frac"]
 
     # ---- locality-biased sampling: hit rate against the shift it causes --
     locality = None
@@ -502,6 +561,7 @@ def main():
         "locality": locality,
         "train": train,
         "host_link_calibration": link,
+        "device_calibration": device_cal,
         "graph": graph_stats,
         "sequential_batch_ms": {"median": round(float(np.median(batch_ms)), 4),
                                 "p10": round(float(np.percentile(batch_ms, 10)), 4),

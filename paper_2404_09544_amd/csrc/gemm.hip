@@ -4,21 +4,23 @@
 //
 // Matrix cores: fp32 uses v_mfma_f32_32x32x2_f32 in the ring kernel and
 // v_mfma_f32_16x16x4_f32 elsewhere (full fp32 products either way); bf16
-// uses v_mfma_f32_16x16x32_bf16 with fp32 accumulation.  On MI355X the
-// 32x32 fp32 instruction sustains the full matrix rate with one wavefront
-// per SIMD, the 16x16 one about three quarters of it.
+// uses v_mfma_f32_32x32x16_bf16 (ring) or v_mfma_f32_16x16x32_bf16 (skinny)
+// with fp32 accumulation.  On MI355X the 32x32 fp32 instruction sustains
+// the full matrix rate with one wavefront per SIMD, the 16x16 one about
+// three quarters of it.
 //
-// fp32 ring kernel (rows 16-byte aligned, the normal case): a 256-thread
-// workgroup owns a BM x BN output tile as 2 x 2 wavefronts.  Both operands
-// travel as 16-byte k-chunks from global memory straight into LDS
+// Ring kernel (rows 16-byte aligned, the normal case; fp32 and bf16): a
+// 256-thread workgroup owns a BM x BN output tile as 2 x 2 wavefronts.  Both
+// operands travel as 16-byte k-chunks from global memory straight into LDS
 // (global_load_lds_dwordx4) through a ring of STAGES buffers, so no
 // registers hold staged data and the loads of later steps are in flight
 // while the current one is multiplied.
 //
-// Register-staged kernels (unaligned rows, bf16, short K over many rows):
-// K is walked in BK steps through two LDS buffers: the next step's global
-// loads are issued into registers before the current step's MFMAs and
-// stored into the other buffer afterwards, one barrier per step.
+// Register-staged kernels (fp32 with unaligned rows, and fp32 with a short
+// K over many rows): K is walked in BK steps through two LDS buffers: the
+// next step's global loads are issued into registers before the current
+// step's MFMAs and stored into the other buffer afterwards, one barrier per
+// step.
 //
 // Skinny kernel (few output rows, e.g. the last layer over the seeds): a
 // workgroup owns 16 x 64 outputs; its sixteen wavefronts take interleaved
@@ -29,6 +31,7 @@
 //   f32 16x16x4:  A[row l%16][k l/16],  B[k l/16][col l%16]
 //   f32 32x32x2:  A[row l%32][k l/32],  B[k l/32][col l%32]
 //   bf16 16x16x32: A[row l%16][k 8(l/16)..+7], B likewise
+//   bf16 32x32x16: A[row l%32][k 8(l/32)..+7], B likewise
 //   16x16 result: D[row 4(l/16) + r][col l%16] in accumulator element r
 //   32x32 result: D[row 8(r/4) + 4(l/32) + r%4][col l%32] in element r
 // Only the pairing of A's and B's k index inside one instruction matters,
@@ -210,21 +213,26 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 // C = act(sum over nseg segments of A_s * B_s^T): A_s is A0 or A1 (M rows,
 // stride lda_s), B_s the N rows of B at column offset s * bseg (stride ldb).
-// Requires 16-byte aligned A0, A1, B and strides, bseg a multiple of 4.
-// Step t covers k in [kb, kb + 32) of one segment; its chunk (row, c) is
-// read whole when it starts below K (a straddling chunk reads the row's
-// padding) and from the row start otherwise, then the elements at k >= K
-// are zeroed in LDS by the lane that loaded them, after its load landed
-// and before the barrier that publishes the step.  Rows past M or N load
-// the last valid row; their results are not stored.
-template <int BM, int BN, int STAGES>
-__global__ void __launch_bounds__(256) k_combine_f32_ring(const float *__restrict__ A0, int64_t lda0,
-                                                          const float *__restrict__ A1, int64_t lda1, int64_t M,
-                                                          const int32_t *__restrict__ m_dev, int64_t K,
-                                                          const float *__restrict__ B, int64_t ldb, int64_t bseg,
-                                                          int nseg, int64_t N, int relu, float *__restrict__ C,
-                                                          int64_t ldc) {
-    constexpr int BK = 32, CH = 8, WN = 2;
+// T is float or uint16_t (bf16 bits); a 16-byte chunk holds E = 16 /
+// sizeof(T) consecutive k.  Requires 16-byte aligned A0, A1, B and strides,
+// bseg a multiple of E.  Step t covers k in [kb, kb + 8E) of one segment; its
+// chunk (row, c) is read whole when it starts below K (a straddling chunk
+// reads the row's padding) and from the row start otherwise, then the
+// elements at k >= K are zeroed in LDS by the lane that loaded them, after
+// its load landed and before the barrier that publishes the step.  Rows
+// past M or N load the last valid row; their results are not stored.
+// fp32: MFMA x of a sub-step takes element x of every lane's chunk (four
+// v_mfma_f32_32x32x2_f32 per chunk pair); bf16: the chunk is the whole
+// fragment of one v_mfma_f32_32x32x16_bf16 (fp32 accumulation).  Output
+// OutT: float, or bf16 rounded to nearest-even.
+template <class T, class OutT, int BM, int BN, int STAGES>
+__global__ void __launch_bounds__(256) k_combine_ring(const T *__restrict__ A0, int64_t lda0,
+                                                      const T *__restrict__ A1, int64_t lda1, int64_t M,
+                                                      const int32_t *__restrict__ m_dev, int64_t K,
+                                                      const T *__restrict__ B, int64_t ldb, int64_t bseg, int nseg,
+                                                      int64_t N, int relu, OutT *__restrict__ C, int64_t ldc) {
+    constexpr bool BF16 = sizeof(T) == 2;
+    constexpr int E = 16 / (int)sizeof(T), CH = 8, BK = CH * E, WN = 2;
     constexpr int WTM = BM / 2, WTN = BN / 2, TM = WTM / 32, TN = WTN / 32;
     constexpr int A_CH = BM * CH, B_CH = BN * CH, ST = A_CH + B_CH;
     constexpr int A_IN = A_CH / 256, B_IN = B_CH / 256, PER = A_IN + B_IN;   // DMAs per wavefront and step
@@ -244,7 +252,7 @@ __global__ void __launch_bounds__(256) k_combine_f32_ring(const float *__restric
     // fragment reads below then touch 8 distinct 16-byte bank groups per
     // 8 lanes.  This wavefront's DMA instruction q fills slots
     // [(wid * IN + q) * 64, + 64).
-    const float *pa[2][A_IN];
+    const T *pa[2][A_IN];
     int ka[A_IN];
 #pragma unroll
     for (int q = 0; q < A_IN; ++q) {
@@ -252,16 +260,16 @@ __global__ void __launch_bounds__(256) k_combine_f32_ring(const float *__restric
         const int64_t row = m0 + r < M ? m0 + r : M - 1;
         pa[0][q] = A0 + row * lda0;
         pa[1][q] = A1 + row * lda1;
-        ka[q] = 4 * ((sl % CH) ^ (r & 7));
+        ka[q] = E * ((sl % CH) ^ (r & 7));
     }
-    const float *pb[B_IN];
+    const T *pb[B_IN];
     int kb_[B_IN];
 #pragma unroll
     for (int q = 0; q < B_IN; ++q) {
         const int sl = (wid * B_IN + q) * 64 + lane, r = sl / CH;
         const int64_t n = n0 + r < N ? n0 + r : N - 1;
         pb[q] = B + n * ldb;
-        kb_[q] = 4 * ((sl % CH) ^ (r & 7));
+        kb_[q] = E * ((sl % CH) ^ (r & 7));
     }
     const int64_t kt = (K + BK - 1) / BK, steps = nseg * kt;
 
@@ -291,26 +299,26 @@ __global__ void __launch_bounds__(256) k_combine_f32_ring(const float *__restric
     auto fixup = [&](int64_t t) {
         const int64_t k0 = (t >= kt ? t - kt : t) * BK;
         if (k0 + BK <= K) return;
-        float *base = (float *)(S + (int)(t % STAGES) * ST);
+        T *base = (T *)(S + (int)(t % STAGES) * ST);
 #pragma unroll
         for (int q = 0; q < A_IN; ++q) {
             const int64_t k = k0 + ka[q];
-            float *e = base + 4 * ((wid * A_IN + q) * 64 + lane);
+            T *e = base + E * ((wid * A_IN + q) * 64 + lane);
 #pragma unroll
-            for (int x = 0; x < 4; ++x)
-                if (k + x >= K) e[x] = 0.f;
+            for (int x = 0; x < E; ++x)
+                if (k + x >= K) e[x] = (T)0;
         }
 #pragma unroll
         for (int q = 0; q < B_IN; ++q) {
             const int64_t k = k0 + kb_[q];
-            float *e = base + 4 * (A_CH + (wid * B_IN + q) * 64 + lane);
+            T *e = base + E * (A_CH + (wid * B_IN + q) * 64 + lane);
 #pragma unroll
-            for (int x = 0; x < 4; ++x)
-                if (k + x >= K) e[x] = 0.f;
+            for (int x = 0; x < E; ++x)
+                if (k + x >= K) e[x] = (T)0;
         }
     };
     // fragment of lane (h, lr) in sub-step u: row lr of its 32-row block,
-    // chunk 2u + h; MFMA x takes element x, so k pairs up across A and B
+    // chunk 2u + h, so k pairs up across A and B
     auto compute = [&](int64_t t) {
         const f32x4 *buf = S + (int)(t % STAGES) * ST;
 #pragma unroll
@@ -326,13 +334,23 @@ __global__ void __launch_bounds__(256) k_combine_f32_ring(const float *__restric
                 const int r = wn * WTN + j * 32 + lr;
                 b[j] = buf[A_CH + r * CH + ((2 * u + h) ^ (r & 7))];
             }
-#pragma unroll
-            for (int x = 0; x < 4; ++x)
+            if constexpr (BF16) {
 #pragma unroll
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
                     for (int j = 0; j < TN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][x], b[j][x], acc[i][j], 0, 0, 0);
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[i]),
+                                                                            __builtin_bit_cast(bf16x8, b[j]),
+                                                                            acc[i][j], 0, 0, 0);
+            } else {
+#pragma unroll
+                for (int x = 0; x < 4; ++x)
+#pragma unroll
+                    for (int i = 0; i < TM; ++i)
+#pragma unroll
+                        for (int j = 0; j < TN; ++j)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][x], b[j][x], acc[i][j], 0, 0, 0);
+            }
         }
     };
 
@@ -361,7 +379,7 @@ __global__ void __launch_bounds__(256) k_combine_f32_ring(const float *__restric
                 if (row < M && col < N) {
                     float v = acc[i][j][r];
                     if (relu) v = fmaxf(v, 0.f);
-                    C[row * ldc + col] = v;
+                    store_out<OutT>(C + row * ldc + col, v);
                 }
             }
 }
@@ -496,136 +514,6 @@ __global__ void __launch_bounds__(256) k_combine_f32_wrow(const float *__restric
 }
 
 
-// ------------------------------------------------------------ bf16 main
-// B comes from WT, the weights transposed to [N][2K] once per call, so both
-// operands arrive as 16-byte chunks along k, the layout the bf16 MFMA
-// fragment (8 consecutive k per lane) reads from LDS.
-template <int BM, int BN, int WM, int WN, int BK, class OutT>
-__global__ void __launch_bounds__(256) k_combine_bf16(const uint16_t *__restrict__ A0, int64_t lda0,
-                                                      const uint16_t *__restrict__ A1, int64_t lda1,
-                                                      int64_t M, const int32_t *__restrict__ m_dev, int64_t K,
-                                                      const uint16_t *__restrict__ WT, int64_t N, int relu,
-                                                      OutT *__restrict__ C, int64_t ldc) {
-    constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
-    constexpr int PK = BK + 8;                    // padded k stride (elements)
-    constexpr int A_CH = BM * BK / 8;             // 16-byte chunks in an A step
-    constexpr int A_LD = (A_CH + 255) / 256;
-    constexpr int B_CH = BN * BK / 8;             // 16-byte chunks in a B step
-    constexpr int B_LD = (B_CH + 255) / 256;
-    static_assert(WM * WN == 4 && TM >= 1 && TN >= 1 && BK % 32 == 0, "tile shape");
-    __shared__ __attribute__((aligned(16))) uint16_t As[2][BM][PK];
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN][PK];
-
-    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    const int wm = wid / WN, wn = wid % WN, g = lane >> 4, l16 = lane & 15;
-    if (m_dev) M = *m_dev;
-    int64_t tile_r, tile_c;
-    tile_of((N + BN - 1) / BN, tile_r, tile_c);
-    const int64_t m0 = tile_r * BM, n0 = tile_c * BN;
-    if (m0 >= M) return;
-
-    f32x4 acc[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int64_t kt = (K + BK - 1) / BK;
-    const int64_t tiles = 2 * kt;
-    uint4 ra[A_LD], rb[B_LD];
-    const int64_t K2 = 2 * K;
-
-    auto load = [&](int64_t t) {
-        const bool seg = t >= kt;
-        const int64_t k0 = (seg ? t - kt : t) * BK;
-        const uint16_t *A = seg ? A1 : A0;
-        const int64_t lda = seg ? lda1 : lda0;
-        const int64_t wk0 = (seg ? K : 0) + k0;
-#pragma unroll
-        for (int s = 0; s < A_LD; ++s) {
-            const int c = tid + 256 * s;
-            const int r = c / (BK / 8), kq = (c % (BK / 8)) * 8;
-            const int64_t row = m0 + r, k = k0 + kq;
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (c < A_CH && row < M) {
-                const uint16_t *p = A + row * lda + k;
-                if (k + 7 < K) {
-                    v = *(const uint4 *)p;
-                } else {
-                    uint16_t tmp[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-                    for (int e = 0; e < 8; ++e)
-                        if (k + e < K) tmp[e] = p[e];
-                    v = make_uint4(tmp[0] | (uint32_t)tmp[1] << 16, tmp[2] | (uint32_t)tmp[3] << 16,
-                                   tmp[4] | (uint32_t)tmp[5] << 16, tmp[6] | (uint32_t)tmp[7] << 16);
-                }
-            }
-            ra[s] = v;
-        }
-#pragma unroll
-        for (int s = 0; s < B_LD; ++s) {
-            const int c = tid + 256 * s;
-            const int nr = c / (BK / 8), kq = (c % (BK / 8)) * 8;
-            const int64_t n = n0 + nr, k = k0 + kq;
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (c < B_CH && n < N) {
-                const uint16_t *q = WT + n * K2 + wk0 + kq;
-                if (k + 7 < K && (K & 7) == 0) {
-                    v = *(const uint4 *)q;
-                } else {
-                    uint16_t tmp[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-                    for (int e = 0; e < 8; ++e)
-                        if (k + e < K) tmp[e] = q[e];
-                    v = make_uint4(tmp[0] | (uint32_t)tmp[1] << 16, tmp[2] | (uint32_t)tmp[3] << 16,
-                                   tmp[4] | (uint32_t)tmp[5] << 16, tmp[6] | (uint32_t)tmp[7] << 16);
-                }
-            }
-            rb[s] = v;
-        }
-    };
-    auto stash = [&](int buf) {
-#pragma unroll
-        for (int s = 0; s < A_LD; ++s) {
-            const int c = tid + 256 * s;
-            if (c < A_CH) *(uint4 *)&As[buf][c / (BK / 8)][(c % (BK / 8)) * 8] = ra[s];
-        }
-#pragma unroll
-        for (int s = 0; s < B_LD; ++s) {
-            const int c = tid + 256 * s;
-            if (c < B_CH) *(uint4 *)&Bs[buf][c / (BK / 8)][(c % (BK / 8)) * 8] = rb[s];
-        }
-    };
-
-    load(0);
-    stash(0);
-    __syncthreads();
-    for (int64_t t = 0; t < tiles; ++t) {
-        const int buf = (int)(t & 1);
-        if (t + 1 < tiles) load(t + 1);
-#pragma unroll
-        for (int ks = 0; ks < BK / 32; ++ks) {
-            bf16x8 a[TM], b[TN];
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-                a[i] = *(const bf16x8 *)&As[buf][wm * WTM + i * 16 + l16][ks * 32 + 8 * g];
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-                b[j] = *(const bf16x8 *)&Bs[buf][wn * WTN + j * 16 + l16][ks * 32 + 8 * g];
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-        }
-        if (t + 1 < tiles) stash(buf ^ 1);
-        __syncthreads();
-    }
-    write_tile<TM, TN, OutT>(acc, m0 + wm * WTM, n0 + wn * WTN, M, N, relu, C, ldc, g, l16);
-}
-
-// --------------------------------------------------------------- skinny
-// 16 x 64 outputs per workgroup; wavefront w takes K blocks w, w+4, ... of
-// both segments (KB = 16 fp32 or 32 bf16 wide); partial tiles are summed in
-// LDS in wavefront order.
 template <bool BF16>
 struct Skinny;
 
@@ -753,20 +641,21 @@ __global__ void __launch_bounds__(256) k_transpose(const T *__restrict__ src, in
 }
 
 // W [2K][N] -> WT [N][2 * KP] with each K-long segment zero-padded to KP (a
-// multiple of 32), so that every 16-byte chunk the ring kernel starts below
-// K lies inside its row and every row starts on a 128-byte boundary.  One
-// workgroup moves a 32 (k) x 32 (n) tile through LDS: reads along n and
-// writes along k are both contiguous.
-__global__ void __launch_bounds__(256) k_transpose_pad(const float *__restrict__ W, int64_t K, int64_t N, int64_t KP,
-                                                       float *__restrict__ WT) {
-    __shared__ float tile[32][33];
+// multiple of 32 and of 128 bytes), so that every 16-byte chunk the ring
+// kernel starts below K lies inside its row and every row starts on a
+// 128-byte boundary.  One workgroup moves a 32 (k) x 32 (n) tile through
+// LDS: reads along n and writes along k are both contiguous.
+template <class T>
+__global__ void __launch_bounds__(256) k_transpose_pad(const T *__restrict__ W, int64_t K, int64_t N, int64_t KP,
+                                                       T *__restrict__ WT) {
+    __shared__ T tile[32][33];
     const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;          // 32 x 8 threads
     const int64_t n0 = (int64_t)blockIdx.x * 32, kk0 = (int64_t)blockIdx.y * 32;   // kk over [0, 2 KP)
     const int64_t seg = kk0 / KP, k0 = kk0 - seg * KP;                // a tile never spans segments
 #pragma unroll
     for (int r = ty; r < 32; r += 8) {
         const int64_t k = k0 + r, n = n0 + tx;
-        tile[r][tx] = (k < K && n < N) ? W[(seg * K + k) * N + n] : 0.f;
+        tile[r][tx] = (k < K && n < N) ? W[(seg * K + k) * N + n] : (T)0;
     }
     __syncthreads();
 #pragma unroll
@@ -786,21 +675,20 @@ SharedWorkspace g_wt;
 
 enum class Fp32Kernel { kRing, kWrow };
 
-template <int BM, int BN>
-void launch_ring(const float *a0, int64_t lda0, const float *a1, int64_t lda1, int64_t m, const int32_t *m_dev,
-                 int64_t k, const float *b, int64_t ldb, int64_t bseg, int nseg, int64_t n, bool relu, float *out,
-                 int64_t ld_out, hipStream_t s) {
+template <int BM, int BN, class T, class OutT>
+void launch_ring(const T *a0, int64_t lda0, const T *a1, int64_t lda1, int64_t m, const int32_t *m_dev, int64_t k,
+                 const T *b, int64_t ldb, int64_t bseg, int nseg, int64_t n, bool relu, OutT *out, int64_t ld_out,
+                 hipStream_t s) {
     const int64_t nrow = (m + BM - 1) / BM, ncol = (n + BN - 1) / BN;
     const dim3 grid((unsigned)(((nrow + 7) / 8) * 8 * ncol));
-    hipLaunchKernelGGL((k_combine_f32_ring<BM, BN, 2>), grid, dim3(256), 0, s, a0, lda0, a1, lda1, m, m_dev, k, b,
-                       ldb, bseg, nseg, n, (int)relu, out, ld_out);
+    hipLaunchKernelGGL((k_combine_ring<T, OutT, BM, BN, 2>), grid, dim3(256), 0, s, a0, lda0, a1, lda1, m, m_dev, k,
+                       b, ldb, bseg, nseg, n, (int)relu, out, ld_out);
 }
 }  // namespace
 
 // fp32: KIND picks the ring kernel (weights transposed and padded first) or
-// the W-as-stored kernel.  bf16: the register-staged kernel on transposed
-// weights.
-template <int BM, int BN, int BKH, Fp32Kernel KIND>
+// the W-as-stored kernel.  bf16: the ring kernel.
+template <int BM, int BN, Fp32Kernel KIND>
 static void launch_main(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
                         const int32_t *m_dev, int64_t k, const void *w, int64_t n, bool bf16, bool relu,
                         bool out_bf16, void *out, int64_t ld_out, hipStream_t s, const char *label) {
@@ -817,36 +705,28 @@ static void launch_main(const void *self, int64_t ld_self, const void *agg, int6
     std::lock_guard<std::mutex> lk(g_wt.mu);
     if (!g_wt.last_use) GNNAV_HIP(hipEventCreateWithFlags(&g_wt.last_use, hipEventDisableTiming));
     GNNAV_HIP(hipStreamWaitEvent(s, g_wt.last_use, 0));
-    if (!bf16) {
-        const int64_t kp = (k + 31) / 32 * 32;
-        g_wt.buf.ensure((size_t)(2 * kp * n) * sizeof(float), s);
-        float *wt = g_wt.buf.as<float>();
-        {
-            KernelTimer tt("weights_transpose", s);
-            hipLaunchKernelGGL(k_transpose_pad, dim3((unsigned)((n + 31) / 32), (unsigned)(2 * kp / 32)), dim3(256), 0,
-                               s, (const float *)w, k, n, kp, wt);
-        }
-        KernelTimer tk(label, s);
-        launch_ring<BM, BN>((const float *)self, ld_self, (const float *)agg, ld_agg, m, m_dev, k, wt, 2 * kp, kp, 2,
-                            n, relu, (float *)out, ld_out, s);
-    } else {
-        g_wt.buf.ensure((size_t)(2 * k * n) * sizeof(uint16_t), s);
-        uint16_t *wt = g_wt.buf.as<uint16_t>();
-        {
-            KernelTimer tt("weights_transpose", s);
-            hipLaunchKernelGGL(k_transpose<uint16_t>, dim3(grid_for(2 * k * n, 256, 1024)), dim3(256), 0, s,
-                               (const uint16_t *)w, 2 * k, n, wt);
-        }
-        KernelTimer tk(label, s);
-        if (out_bf16)
-            hipLaunchKernelGGL((k_combine_bf16<BM, BN, 2, 2, BKH, uint16_t>), grid, dim3(256), 0, s,
-                               (const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, k,
-                               (const uint16_t *)wt, n, (int)relu, (uint16_t *)out, ld_out);
+    const int64_t elt = bf16 ? 2 : 4, kp = bf16 ? (k + 63) / 64 * 64 : (k + 31) / 32 * 32;
+    g_wt.buf.ensure((size_t)(2 * kp * n * elt), s);
+    const dim3 tgrid((unsigned)((n + 31) / 32), (unsigned)(2 * kp / 32));
+    {
+        KernelTimer tt("weights_transpose", s);
+        if (!bf16)
+            hipLaunchKernelGGL(k_transpose_pad<float>, tgrid, dim3(256), 0, s, (const float *)w, k, n, kp,
+                               g_wt.buf.as<float>());
         else
-            hipLaunchKernelGGL((k_combine_bf16<BM, BN, 2, 2, BKH, float>), grid, dim3(256), 0, s,
-                               (const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, k,
-                               (const uint16_t *)wt, n, (int)relu, (float *)out, ld_out);
+            hipLaunchKernelGGL(k_transpose_pad<uint16_t>, tgrid, dim3(256), 0, s, (const uint16_t *)w, k, n, kp,
+                               g_wt.buf.as<uint16_t>());
     }
+    KernelTimer tk(label, s);
+    if (!bf16)
+        launch_ring<BM, BN>((const float *)self, ld_self, (const float *)agg, ld_agg, m, m_dev, k,
+                            g_wt.buf.as<float>(), 2 * kp, kp, 2, n, relu, (float *)out, ld_out, s);
+    else if (out_bf16)
+        launch_ring<BM, BN>((const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, k,
+                            g_wt.buf.as<uint16_t>(), 2 * kp, kp, 2, n, relu, (uint16_t *)out, ld_out, s);
+    else
+        launch_ring<BM, BN>((const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, k,
+                            g_wt.buf.as<uint16_t>(), 2 * kp, kp, 2, n, relu, (float *)out, ld_out, s);
     GNNAV_HIP(hipEventRecord(g_wt.last_use, s));
 }
 
@@ -864,18 +744,20 @@ struct GemmChoice {
 // (64 x 64 when the output is at most 64 wide, 128 x 128 once there are
 // enough of those to give every compute unit two); the W-as-stored kernel
 // when such a large output has a short K (at most 128 per segment), where
-// it measured faster (e.g. 10^5 rows of d_in = 100).  bf16: 64 x 64 until
-// that same 128 x 128 point.
+// it measured faster (e.g. 10^5 rows of d_in = 100).  bf16: the ring kernel
+// with 128 x 64 tiles (64 x 64 for outputs at most 64 wide), 128 x 128 from
+// that same point on.
 static GemmChoice choose_main(int64_t m, int64_t d_in, int64_t d_out, bool bf16) {
     const bool big = d_out > 64 && ((m + 127) / 128) * ((d_out + 127) / 128) >= 512;
     if (bf16) {
-        if (big) return {128, 128, launch_main<128, 128, 32, Fp32Kernel::kRing>};
-        return {64, 64, launch_main<64, 64, 32, Fp32Kernel::kRing>};
+        if (big) return {128, 128, launch_main<128, 128, Fp32Kernel::kRing>};
+        if (d_out <= 64) return {64, 64, launch_main<64, 64, Fp32Kernel::kRing>};
+        return {128, 64, launch_main<128, 64, Fp32Kernel::kRing>};
     }
-    if (big && d_in <= 128) return {128, 128, launch_main<128, 128, 32, Fp32Kernel::kWrow>};
-    if (big) return {128, 128, launch_main<128, 128, 32, Fp32Kernel::kRing>};
-    if (d_out <= 64) return {64, 64, launch_main<64, 64, 32, Fp32Kernel::kRing>};
-    return {128, 64, launch_main<128, 64, 32, Fp32Kernel::kRing>};
+    if (big && d_in <= 128) return {128, 128, launch_main<128, 128, Fp32Kernel::kWrow>};
+    if (big) return {128, 128, launch_main<128, 128, Fp32Kernel::kRing>};
+    if (d_out <= 64) return {64, 64, launch_main<64, 64, Fp32Kernel::kRing>};
+    return {128, 64, launch_main<128, 64, Fp32Kernel::kRing>};
 }
 
 void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
