@@ -473,25 +473,29 @@ __global__ void __launch_bounds__(256) k_wgrad(const float *__restrict__ X0, int
 // Ring form of the weight gradient (rows 16-byte aligned): the same
 // partial tile as k_wgrad, with both operands moved row by row (k = row m)
 // straight from global memory into LDS by global_load_lds_dwordx4 through a
-// two-stage ring, and 32x32x2 MFMAs.  LDS holds Xs[m][a] and Gs[m][o] as
-// stored, 16-byte chunk c of row m at c ^ 8 (m & 1), so the fragment reads
-// (lane (h, r): row 2u + h, column r of its 32-wide block, one float) touch
-// 64 distinct banks.  Rows past the split's end load a valid row; the lanes
-// that loaded G chunks for them zero those in LDS before the barrier, so
-// they add nothing.  Columns past d_in or d_out only reach outputs that are
-// not stored.
-template <int BA, int BO>
+// two-stage ring of BK-row steps, and 32x32x2 MFMAs.  LDS holds Xs[m][a] and
+// Gs[m][o] as stored.  A wavefront owns (32 VA) x (32 VB) outputs as VA x VB
+// MFMA blocks whose rows and columns are interleaved: block (i, j) holds
+// a = base + VA r + i and o = base + VB c + j for fragment row r, column c.
+// A lane then finds all VA of its A values (and all VB of its B values) for
+// one k side by side in LDS, one 4-, 8- or 16-byte read each: two LDS reads
+// feed VA x VB MFMAs (four for 128 x 128 tiles).
+// Rows past the split's end load a valid row; the lanes that loaded G chunks
+// for them zero those in LDS before the barrier, so they add nothing.
+// Columns past d_in or d_out only reach outputs that are not stored.
+template <int BA, int BO, int BK>
 __global__ void __launch_bounds__(256) k_wgrad_ring(const float *__restrict__ X0, int64_t ldx0,
                                                     const float *__restrict__ X1, int64_t ldx1, int64_t M,
                                                     const int32_t *__restrict__ m_dev, int64_t d_in,
                                                     const float *__restrict__ Gm, int64_t ldg, int64_t d_out,
                                                     int64_t splits, float *__restrict__ part) {
     typedef float f32x16 __attribute__((ext_vector_type(16)));
-    constexpr int BK = 32, XC = BA / 4, GC = BO / 4;                 // chunks per row
+    constexpr int VA = BA / 64, VB = BO / 64;                       // MFMA blocks per wavefront, each way
+    constexpr int XC = BA / 4, GC = BO / 4;                         // 16-byte chunks per LDS row
     constexpr int X_CH = BK * XC, G_CH = BK * GC, ST = X_CH + G_CH;
-    constexpr int X_IN = X_CH / 256, G_IN = G_CH / 256;              // DMAs per wavefront and step
-    constexpr int WTA = BA / 2, WTO = BO / 2, TM = WTA / 32, TN = WTO / 32;
-    static_assert(X_CH % 256 == 0 && G_CH % 256 == 0 && TM >= 1 && TN >= 1 && XC >= 16 && GC >= 16, "tile");
+    constexpr int X_IN = X_CH / 256, G_IN = G_CH / 256;             // DMAs per wavefront and step
+    static_assert((VA == 1 || VA == 2 || VA == 4) && (VB == 1 || VB == 2 || VB == 4), "tile");
+    static_assert(X_CH % 256 == 0 && G_CH % 256 == 0 && BK % 2 == 0, "whole wave instructions");
     __shared__ f32x4 S[2 * ST];
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const int wa = wid >> 1, wo = wid & 1, h = lane >> 5, lr = lane & 31;
@@ -506,41 +510,30 @@ __global__ void __launch_bounds__(256) k_wgrad_ring(const float *__restrict__ X0
     const int64_t m_lo = split * per, m_hi = std::min<int64_t>(M, m_lo + per);
     const int64_t steps = m_hi > m_lo ? (m_hi - m_lo + BK - 1) / BK : 0;
 
-    // this lane's chunk in each DMA instruction: (row within the step, column)
-    int xr[X_IN], xa[X_IN], gr[G_IN], go[G_IN];
+    f32x16 acc[VA][VB];
 #pragma unroll
-    for (int q = 0; q < X_IN; ++q) {
-        const int pos = (wid * X_IN + q) * 64 + lane, r = pos / XC;
-        xr[q] = r;
-        xa[q] = 4 * ((pos % XC) ^ (8 * (r & 1)));
-    }
+    for (int i = 0; i < VA; ++i)
 #pragma unroll
-    for (int q = 0; q < G_IN; ++q) {
-        const int pos = (wid * G_IN + q) * 64 + lane, r = pos / GC;
-        gr[q] = r;
-        go[q] = 4 * ((pos % GC) ^ (8 * (r & 1)));
-    }
-    f32x16 acc[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
+        for (int j = 0; j < VB; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+    // DMA slot p of a step holds chunk (row p / C, column 4 (p % C)) of its block
     auto issue = [&](int64_t t) {
         f32x4 *buf = S + (int)(t & 1) * ST;
         const int64_t mb = m_lo + t * BK;
 #pragma unroll
         for (int q = 0; q < X_IN; ++q) {
-            const int64_t m = mb + xr[q] < m_hi ? mb + xr[q] : m_lo;
-            const int64_t a = a0 + xa[q];
+            const int pos = (wid * X_IN + q) * 64 + lane;
+            const int64_t m = mb + pos / XC < m_hi ? mb + pos / XC : m_lo;
+            const int64_t a = a0 + 4 * (pos % XC);
             dma16(X + m * ldx + (a < d_in ? a : 0), &buf[(wid * X_IN + q) * 64]);
         }
 #pragma unroll
         for (int q = 0; q < G_IN; ++q) {
-            const int64_t m = mb + gr[q] < m_hi ? mb + gr[q] : m_lo;
-            const int64_t o = o0 + go[q];
+            const int pos = (wid * G_IN + q) * 64 + lane;
+            const int64_t m = mb + pos / GC < m_hi ? mb + pos / GC : m_lo;
+            const int64_t o = o0 + 4 * (pos % GC);
             dma16(Gm + m * ldg + (o < d_out ? o : 0), &buf[X_CH + (wid * G_IN + q) * 64]);
         }
     };
@@ -549,28 +542,27 @@ __global__ void __launch_bounds__(256) k_wgrad_ring(const float *__restrict__ X0
         if (mb + BK <= m_hi) return;
         f32x4 *buf = S + (int)(t & 1) * ST;
 #pragma unroll
-        for (int q = 0; q < G_IN; ++q)
-            if (mb + gr[q] >= m_hi) buf[X_CH + (wid * G_IN + q) * 64 + lane] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int q = 0; q < G_IN; ++q) {
+            const int pos = (wid * G_IN + q) * 64 + lane;
+            if (mb + pos / GC >= m_hi) buf[X_CH + pos] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
     };
-    auto at = [&](int row, int col, int chunks) {       // float index of (row, col) in a k-major block
-        return (row * chunks + ((col >> 2) ^ (8 * (row & 1)))) * 4 + (col & 3);
-    };
+    typedef float fa_t __attribute__((ext_vector_type(VA)));
+    typedef float fb_t __attribute__((ext_vector_type(VB)));
     auto compute = [&](int64_t t) {
         const float *xs = (const float *)(S + (int)(t & 1) * ST);
         const float *gs = xs + 4 * X_CH;
 #pragma unroll
         for (int u = 0; u < BK / 2; ++u) {
             const int row = 2 * u + h;
-            float a[TM], b[TN];
+            const fa_t a = *(const fa_t *)&xs[row * BA + wa * (32 * VA) + VA * lr];
+            const fb_t b = *(const fb_t *)&gs[row * BO + wo * (32 * VB) + VB * lr];
 #pragma unroll
-            for (int i = 0; i < TM; ++i) a[i] = xs[at(row, wa * WTA + i * 32 + lr, XC)];
+            for (int i = 0; i < VA; ++i)
 #pragma unroll
-            for (int j = 0; j < TN; ++j) b[j] = gs[at(row, wo * WTO + j * 32 + lr, GC)];
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
+                for (int j = 0; j < VB; ++j) {
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
+                }
         }
     };
     if (steps > 0) {
@@ -585,13 +577,14 @@ __global__ void __launch_bounds__(256) k_wgrad_ring(const float *__restrict__ X0
     }
     float *P = part + split * (2 * d_in * d_out);
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < VA; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
+        for (int j = 0; j < VB; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int64_t a = a0 + wa * WTA + i * 32 + 8 * (r / 4) + 4 * h + (r % 4);
-                const int64_t o = o0 + wo * WTO + j * 32 + lr;
+                const int R = 8 * (r / 4) + 4 * h + (r % 4);
+                const int64_t a = a0 + wa * (32 * VA) + VA * R + i;
+                const int64_t o = o0 + wo * (32 * VB) + VB * lr + j;
                 if (a < d_in && o < d_out) P[(seg * d_in + a) * d_out + o] = acc[i][j][r];
             }
 }
@@ -614,8 +607,9 @@ void launch_wgrad(const float *x_self, int64_t ld_self, const float *agg, int64_
                   float *dw, float *w, float lr, hipStream_t s, const char *label) {
     auto a16 = [](const void *p, int64_t ld) { return (((uintptr_t)p & 15u) == 0) && ld % 4 == 0; };
     const bool ring = a16(x_self, ld_self) && a16(agg, ld_agg) && a16(dz, ld_dz);
-    // ring: 128 x 64 tiles; otherwise the register-staged 64 x 64 kernel
-    const int64_t BA = ring ? 128 : 64, BO = 64;
+    // ring: 128 x 128 tiles (128 x 64 for outputs at most 64 wide); otherwise
+    // the register-staged 64 x 64 kernel
+    const int64_t BA = ring ? 128 : 64, BO = ring && d_out > 64 ? 128 : 64;
     const int64_t tiles = 2 * ((d_in + BA - 1) / BA) * ((d_out + BO - 1) / BO);
     int64_t splits = (512 + tiles - 1) / tiles;
     splits = std::min<int64_t>(splits, std::max<int64_t>(1, (m + 255) / 256));
@@ -624,8 +618,12 @@ void launch_wgrad(const float *x_self, int64_t ld_self, const float *agg, int64_
     part.ensure((size_t)(splits * total) * sizeof(float), s);
     {
         KernelTimer t(label, s);
-        if (ring)
-            hipLaunchKernelGGL((k_wgrad_ring<128, 64>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, s,
+        if (ring && BO == 128)
+            hipLaunchKernelGGL((k_wgrad_ring<128, 128, 16>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, s,
+                               x_self, ld_self, agg, ld_agg, m, m_dev, d_in, dz, ld_dz, d_out, splits,
+                               part.as<float>());
+        else if (ring)
+            hipLaunchKernelGGL((k_wgrad_ring<128, 64, 32>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, s,
                                x_self, ld_self, agg, ld_agg, m, m_dev, d_in, dz, ld_dz, d_out, splits,
                                part.as<float>());
         else
