@@ -356,122 +356,9 @@ void launch_aggregate_t(const CscWorkspace &csc, const int32_t *indptr, int64_t 
 }
 
 // --------------------------------------------------------- weight gradient
-// Partial tile of dW[seg * d_in + a][o] = sum over rows m of this split of
-// X_seg[m][a] * G[m][o].  Both operands are staged k-major (k = row m) as
-// they are stored; the MFMA fragments read one float per lane.
-template <int BA, int BO, int BK>
-__global__ void __launch_bounds__(256) k_wgrad(const float *__restrict__ X0, int64_t ldx0,
-                                               const float *__restrict__ X1, int64_t ldx1, int64_t M,
-                                               const int32_t *__restrict__ m_dev, int64_t d_in,
-                                               const float *__restrict__ Gm, int64_t ldg, int64_t d_out,
-                                               int64_t splits, float *__restrict__ part) {
-    constexpr int PA = BA + 16, PB = BO + 16;
-    constexpr int WTA = BA / 2, WTO = BO / 2, TM = WTA / 16, TN = WTO / 16;
-    constexpr int A_CH = BK * BA / 4, B_CH = BK * BO / 4;
-    constexpr int A_LD = (A_CH + 255) / 256, B_LD = (B_CH + 255) / 256;
-    __shared__ __attribute__((aligned(16))) float As[2][BK][PA];
-    __shared__ __attribute__((aligned(16))) float Bs[2][BK][PB];
-    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    const int wa = wid >> 1, wo = wid & 1, g = lane >> 4, l16 = lane & 15;
-    if (m_dev) M = *m_dev;
-    const int64_t na = (d_in + BA - 1) / BA, no = (d_out + BO - 1) / BO;
-    const int64_t tile = blockIdx.x, split = blockIdx.y;
-    const int seg = (int)(tile / (na * no));
-    const int64_t a0 = ((tile / no) % na) * BA, o0 = (tile % no) * BO;
-    const float *X = seg ? X1 : X0;
-    const int64_t ldx = seg ? ldx1 : ldx0;
-    const int64_t per = ((M + splits - 1) / splits + BK - 1) / BK * BK;
-    const int64_t m_lo = split * per, m_hi = std::min<int64_t>(M, m_lo + per);
-
-    f32x4 acc[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int64_t steps = m_hi > m_lo ? (m_hi - m_lo + BK - 1) / BK : 0;
-    f32x4 ra[A_LD], rb[B_LD];
-    auto chunk = [&](const float *p, int64_t col, int64_t lim) {
-        f32x4 v = {0.f, 0.f, 0.f, 0.f};
-        if (col + 3 < lim) {
-            v = *(const f32x4 *)p;
-        } else {
-            if (col < lim) v.x = p[0];
-            if (col + 1 < lim) v.y = p[1];
-            if (col + 2 < lim) v.z = p[2];
-        }
-        return v;
-    };
-    auto load = [&](int64_t t) {
-        const int64_t m0 = m_lo + t * BK;
-#pragma unroll
-        for (int s = 0; s < A_LD; ++s) {
-            const int c = tid + 256 * s;
-            const int64_t m = m0 + c / (BA / 4), a = a0 + (c % (BA / 4)) * 4;
-            ra[s] = (c < A_CH && m < m_hi) ? chunk(X + m * ldx + a, a, d_in) : f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-#pragma unroll
-        for (int s = 0; s < B_LD; ++s) {
-            const int c = tid + 256 * s;
-            const int64_t m = m0 + c / (BO / 4), o = o0 + (c % (BO / 4)) * 4;
-            rb[s] = (c < B_CH && m < m_hi) ? chunk(Gm + m * ldg + o, o, d_out) : f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-    };
-    auto stash = [&](int buf) {
-#pragma unroll
-        for (int s = 0; s < A_LD; ++s) {
-            const int c = tid + 256 * s;
-            if (c < A_CH) *(f32x4 *)&As[buf][c / (BA / 4)][(c % (BA / 4)) * 4] = ra[s];
-        }
-#pragma unroll
-        for (int s = 0; s < B_LD; ++s) {
-            const int c = tid + 256 * s;
-            if (c < B_CH) *(f32x4 *)&Bs[buf][c / (BO / 4)][(c % (BO / 4)) * 4] = rb[s];
-        }
-    };
-    auto compute = [&](int buf) {
-#pragma unroll
-        for (int ks = 0; ks < BK / 4; ++ks) {
-            float a[TM], b[TN];
-#pragma unroll
-            for (int i = 0; i < TM; ++i) a[i] = As[buf][ks * 4 + g][wa * WTA + i * 16 + l16];
-#pragma unroll
-            for (int j = 0; j < TN; ++j) b[j] = Bs[buf][ks * 4 + g][wo * WTO + j * 16 + l16];
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
-        }
-    };
-    if (steps > 0) {
-        load(0);
-        stash(0);
-        __syncthreads();
-        for (int64_t t = 0; t < steps; ++t) {
-            const int buf = (int)(t & 1);
-            if (t + 1 < steps) load(t + 1);
-            compute(buf);
-            if (t + 1 < steps) stash(buf ^ 1);
-            __syncthreads();
-        }
-    }
-    // the partial tile is written even when empty, so the reduce can read
-    // every split unconditionally
-    float *P = part + split * (2 * d_in * d_out);
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int64_t a = a0 + wa * WTA + i * 16 + 4 * g + r, o = o0 + wo * WTO + j * 16 + l16;
-                if (a < d_in && o < d_out) P[(seg * d_in + a) * d_out + o] = acc[i][j][r];
-            }
-}
-
-// Ring form of the weight gradient (rows 16-byte aligned): the same
-// partial tile as k_wgrad, with both operands moved row by row (k = row m)
+// Partial tile of dW[seg * d_in + a][o] = sum over the rows m of this split
+// of X_seg[m][a] * G[m][o] (rows 16-byte aligned), with both operands moved
+// row by row (k = row m)
 // straight from global memory into LDS by global_load_lds_dwordx4 through a
 // two-stage ring of BK-row steps, and 32x32x2 MFMAs.  LDS holds Xs[m][a] and
 // Gs[m][o] as stored.  A wavefront owns (32 VA) x (32 VB) outputs as VA x VB
@@ -606,10 +493,11 @@ void launch_wgrad(const float *x_self, int64_t ld_self, const float *agg, int64_
                   const int32_t *m_dev, int64_t d_in, const float *dz, int64_t ld_dz, int64_t d_out, DevBuf &part,
                   float *dw, float *w, float lr, hipStream_t s, const char *label) {
     auto a16 = [](const void *p, int64_t ld) { return (((uintptr_t)p & 15u) == 0) && ld % 4 == 0; };
-    const bool ring = a16(x_self, ld_self) && a16(agg, ld_agg) && a16(dz, ld_dz);
-    // ring: 128 x 128 tiles (128 x 64 for outputs at most 64 wide); otherwise
-    // the register-staged 64 x 64 kernel
-    const int64_t BA = ring ? 128 : 64, BO = ring && d_out > 64 ? 128 : 64;
+    if (!(a16(x_self, ld_self) && a16(agg, ld_agg) && a16(dz, ld_dz)))
+        fail(GNNAV_E_INVALID, "weight gradient operands need 16-byte aligned rows");
+    // 128 x 128 tiles (128 x 64 for outputs at most 64 wide); the row range
+    // is split so that about 512 workgroups run
+    const int64_t BA = 128, BO = d_out > 64 ? 128 : 64;
     const int64_t tiles = 2 * ((d_in + BA - 1) / BA) * ((d_out + BO - 1) / BO);
     int64_t splits = (512 + tiles - 1) / tiles;
     splits = std::min<int64_t>(splits, std::max<int64_t>(1, (m + 255) / 256));
@@ -618,16 +506,12 @@ void launch_wgrad(const float *x_self, int64_t ld_self, const float *agg, int64_
     part.ensure((size_t)(splits * total) * sizeof(float), s);
     {
         KernelTimer t(label, s);
-        if (ring && BO == 128)
+        if (BO == 128)
             hipLaunchKernelGGL((k_wgrad_ring<128, 128, 16>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, s,
                                x_self, ld_self, agg, ld_agg, m, m_dev, d_in, dz, ld_dz, d_out, splits,
                                part.as<float>());
-        else if (ring)
-            hipLaunchKernelGGL((k_wgrad_ring<128, 64, 32>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, s,
-                               x_self, ld_self, agg, ld_agg, m, m_dev, d_in, dz, ld_dz, d_out, splits,
-                               part.as<float>());
         else
-            hipLaunchKernelGGL((k_wgrad<64, 64, 32>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, s,
+            hipLaunchKernelGGL((k_wgrad_ring<128, 64, 32>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, s,
                                x_self, ld_self, agg, ld_agg, m, m_dev, d_in, dz, ld_dz, d_out, splits,
                                part.as<float>());
     }
