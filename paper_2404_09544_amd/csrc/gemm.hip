@@ -16,11 +16,10 @@
 // registers hold staged data and the loads of later steps are in flight
 // while the current one is multiplied.
 //
-// Register-staged kernels (fp32 with unaligned rows, and fp32 with a short
-// K over many rows): K is walked in BK steps through two LDS buffers: the
-// next step's global loads are issued into registers before the current
-// step's MFMAs and stored into the other buffer afterwards, one barrier per
-// step.
+// W-as-stored kernel (fp32 with a short K over many rows): K is walked in
+// BK steps through two LDS buffers: the next step's global loads are issued
+// into registers before the current step's MFMAs and stored into the other
+// buffer afterwards, one barrier per step.
 //
 // Skinny kernel (few output rows, e.g. the last layer over the seeds): a
 // workgroup owns 16 x 64 outputs; its sixteen wavefronts take interleaved
@@ -83,129 +82,6 @@ __device__ __forceinline__ void tile_of(int64_t ncol, int64_t &tile_r, int64_t &
     const int64_t L = blockIdx.x, xcd = L & 7, j = L >> 3;
     tile_r = (j / ncol) * 8 + xcd;
     tile_c = j % ncol;
-}
-
-// ------------------------------------------------------------ fp32 main
-// Both operands are staged as 16-byte chunks along k: A rows as stored, and
-// B from WT, the weights transposed to [N][2K] once per call.  A lane's
-// chunk holds four consecutive k, and MFMA q of a sub-step takes element q
-// of every lane's chunk, so one 16-byte LDS read per operand feeds four
-// MFMAs.  LDS slots are XOR-swizzled within each row so that both the
-// chunk stores and the fragment reads are free of bank conflicts.
-template <int CH>
-__device__ __forceinline__ int swz(int r, int kc) {
-    return r * CH + (kc ^ (CH == 4 ? ((r >> 1) & 3) : (r & 7)));
-}
-
-template <int BM, int BN, int WM, int WN, int BK>
-__global__ void __launch_bounds__(256) k_combine_f32(const float *__restrict__ A0, int64_t lda0,
-                                                     const float *__restrict__ A1, int64_t lda1, int64_t M,
-                                                     const int32_t *__restrict__ m_dev, int64_t K,
-                                                     const float *__restrict__ WT, int64_t ldb, int bvec, int nseg,
-                                                     int64_t N, int relu, float *__restrict__ C, int64_t ldc) {
-    constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
-    constexpr int CH = BK / 4;                    // chunks per row and step
-    constexpr int A_CH = BM * CH, B_CH = BN * CH;
-    constexpr int A_LD = (A_CH + 255) / 256, B_LD = (B_CH + 255) / 256;
-    static_assert(WM * WN == 4 && TM >= 1 && TN >= 1 && (BK == 16 || BK == 32), "tile shape");
-    __shared__ f32x4 As[2][A_CH];
-    __shared__ f32x4 Bs[2][B_CH];
-
-    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    const int wm = wid / WN, wn = wid % WN, g = lane >> 4, l16 = lane & 15;
-    if (m_dev) M = *m_dev;
-    int64_t tile_r, tile_c;
-    tile_of((N + BN - 1) / BN, tile_r, tile_c);
-    const int64_t m0 = tile_r * BM, n0 = tile_c * BN;
-    if (m0 >= M) return;
-
-    f32x4 acc[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int64_t kt = (K + BK - 1) / BK;
-    const int64_t tiles = nseg * kt;
-    f32x4 ra[A_LD], rb[B_LD];
-
-    auto chunk = [&](const float *p, int64_t k, bool vec) {
-        f32x4 v = {0.f, 0.f, 0.f, 0.f};
-        if (vec && k + 3 < K) {
-            v = *(const f32x4 *)p;
-        } else if (k + 3 < K) {
-            v.x = p[0];
-            v.y = p[1];
-            v.z = p[2];
-            v.w = p[3];
-        } else {
-            if (k < K) v.x = p[0];
-            if (k + 1 < K) v.y = p[1];
-            if (k + 2 < K) v.z = p[2];
-        }
-        return v;
-    };
-    auto load = [&](int64_t t) {
-        const bool seg = t >= kt;
-        const int64_t k0 = (seg ? t - kt : t) * BK;
-        const float *A = seg ? A1 : A0;
-        const int64_t lda = seg ? lda1 : lda0;
-#pragma unroll
-        for (int s = 0; s < A_LD; ++s) {
-            const int c = tid + 256 * s;
-            const int64_t row = m0 + c / CH, k = k0 + (c % CH) * 4;
-            ra[s] = (c < A_CH && row < M) ? chunk(A + row * lda + k, k, true) : f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-#pragma unroll
-        for (int s = 0; s < B_LD; ++s) {
-            const int c = tid + 256 * s;
-            const int64_t n = n0 + c / CH, k = k0 + (c % CH) * 4;
-            rb[s] = (c < B_CH && n < N) ? chunk(WT + n * ldb + (seg ? K : 0) + k, k, bvec) : f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-    };
-    auto stash = [&](int buf) {
-#pragma unroll
-        for (int s = 0; s < A_LD; ++s) {
-            const int c = tid + 256 * s;
-            if (c < A_CH) As[buf][swz<CH>(c / CH, c % CH)] = ra[s];
-        }
-#pragma unroll
-        for (int s = 0; s < B_LD; ++s) {
-            const int c = tid + 256 * s;
-            if (c < B_CH) Bs[buf][swz<CH>(c / CH, c % CH)] = rb[s];
-        }
-    };
-    // kvalid: k values of this step inside [0, K); sub-steps past them are skipped
-    auto compute = [&](int buf, int64_t kvalid) {
-#pragma unroll
-        for (int sub = 0; sub < CH / 4; ++sub) {
-            if (sub * 16 >= kvalid) break;        // uniform across the workgroup
-            f32x4 a[TM], b[TN];
-#pragma unroll
-            for (int i = 0; i < TM; ++i) a[i] = As[buf][swz<CH>(wm * WTM + i * 16 + l16, sub * 4 + g)];
-#pragma unroll
-            for (int j = 0; j < TN; ++j) b[j] = Bs[buf][swz<CH>(wn * WTN + j * 16 + l16, sub * 4 + g)];
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-#pragma unroll
-                for (int i = 0; i < TM; ++i)
-#pragma unroll
-                    for (int j = 0; j < TN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
-        }
-    };
-
-    load(0);
-    stash(0);
-    __syncthreads();
-    for (int64_t t = 0; t < tiles; ++t) {
-        const int buf = (int)(t & 1);
-        if (t + 1 < tiles) load(t + 1);
-        compute(buf, K - (t >= kt ? t - kt : t) * BK);
-        if (t + 1 < tiles) stash(buf ^ 1);
-        __syncthreads();
-    }
-    write_tile<TM, TN, float>(acc, m0 + wm * WTM, n0 + wn * WTN, M, N, relu, C, ldc, g, l16);
 }
 
 // ------------------------------------------------------- fp32 ring kernel
@@ -386,7 +262,7 @@ __global__ void __launch_bounds__(256) k_combine_ring(const T *__restrict__ A0, 
 
 // ---------------------------------------------- fp32 main, W as stored
 // Reads W row-major and stages A transposed (k-major) in LDS, one float per
-// lane and k step.  Measured faster than the chunked kernel above when there
+// lane and k step.  Measured faster than the ring kernel when there
 // are many row tiles over a short K (e.g. d_in = 100 over 10^5 rows).
 template <int BM, int BN, int WM, int WN, int BK, class OutT>
 __global__ void __launch_bounds__(256) k_combine_f32_wrow(const float *__restrict__ A0, int64_t lda0,
@@ -792,22 +668,43 @@ void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t 
 // out[M x N] = A[M x K] * B^T with B stored [N][ldb] (row n holds column n of
 // the product's right operand along k): the layout of a row-major weight
 // matrix read backwards, dX = dZ * W^T.  fp32, one segment, no activation.
+// Rows [n][k] at stride ldb -> [n][k4] (k4 = k rounded up to 4), zero padded,
+// for operands whose rows are not 16-byte aligned.
+__global__ void __launch_bounds__(256) k_pad_rows(const float *__restrict__ b, int64_t ldb, int64_t n, int64_t k,
+                                                  int64_t k4, float *__restrict__ out) {
+    const int64_t total = n * k4, stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        const int64_t r = i / k4, c = i - r * k4;
+        out[i] = c < k ? b[r * ldb + c] : 0.f;
+    }
+}
+
 void launch_matmul_bt(const float *a, int64_t lda, int64_t m, const int32_t *m_dev, int64_t k, const float *b,
                       int64_t ldb, int64_t n, float *out, int64_t ld_out, hipStream_t s, const char *label) {
     if (m <= 0 || n <= 0) return;
-    const bool rows16 = (((uintptr_t)a & 15u) == 0) && lda % 4 == 0 && (((uintptr_t)b & 15u) == 0) && ldb % 4 == 0;
-    KernelTimer t(label, s);
-    if (rows16) {
+    if (!((((uintptr_t)a & 15u) == 0) && lda % 4 == 0))
+        fail(GNNAV_E_INVALID, "matmul_bt: rows of a must be 16-byte aligned");
+    auto run = [&](const float *bb, int64_t ldbb) {
+        KernelTimer t(label, s);
         if (n <= 64)
-            launch_ring<64, 64>(a, lda, a, lda, m, m_dev, k, b, ldb, 0, 1, n, false, out, ld_out, s);
+            launch_ring<64, 64>(a, lda, a, lda, m, m_dev, k, bb, ldbb, 0, 1, n, false, out, ld_out, s);
         else
-            launch_ring<128, 64>(a, lda, a, lda, m, m_dev, k, b, ldb, 0, 1, n, false, out, ld_out, s);
+            launch_ring<128, 64>(a, lda, a, lda, m, m_dev, k, bb, ldbb, 0, 1, n, false, out, ld_out, s);
+    };
+    if ((((uintptr_t)b & 15u) == 0) && ldb % 4 == 0) {
+        run(b, ldb);
     } else {
-        // rows not 16-byte aligned (e.g. W^T of a layer with an odd output width)
-        const int bvec = (((uintptr_t)b & 15u) == 0) && ldb % 4 == 0;
-        const int64_t nrow = (m + 63) / 64, ncol = (n + 63) / 64;
-        hipLaunchKernelGGL((k_combine_f32<64, 64, 2, 2, 32>), dim3((unsigned)(((nrow + 7) / 8) * 8 * ncol)), dim3(256),
-                           0, s, a, lda, a, lda, m, m_dev, k, b, ldb, bvec, 1, n, 0, out, ld_out);
+        // rows of b not 16-byte aligned (W of a layer with an odd output
+        // width): a zero-padded copy in the shared weights buffer first
+        std::lock_guard<std::mutex> lk(g_wt.mu);
+        if (!g_wt.last_use) GNNAV_HIP(hipEventCreateWithFlags(&g_wt.last_use, hipEventDisableTiming));
+        GNNAV_HIP(hipStreamWaitEvent(s, g_wt.last_use, 0));
+        const int64_t k4 = (k + 3) / 4 * 4;
+        g_wt.buf.ensure((size_t)(n * k4) * sizeof(float), s);
+        hipLaunchKernelGGL(k_pad_rows, dim3(grid_for(n * k4, 256, 1024)), dim3(256), 0, s, b, ldb, n, k, k4,
+                           g_wt.buf.as<float>());
+        run(g_wt.buf.as<float>(), k4);
+        GNNAV_HIP(hipEventRecord(g_wt.last_use, s));
     }
     GNNAV_HIP(hipGetLastError());
 }
