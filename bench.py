@@ -173,6 +173,22 @@ def locality_report(args, G, g, c, wl, seeds_dev, torch, batches=5):
     return out
 
 
+# Host-link workgroups of a pipelined leg.  With w workgroups copying
+# misses, the transfer runs at LINK_RATE[w] of the 64-workgroup rate and
+# kernels running alongside it slow down by LINK_SLOWDOWN[w] (both measured
+# on MI355X: a zero-copy gather of 140k random 2416-byte rows next to an HBM
+# stream kernel).  A pipelined step takes about max(transfer, the rest of the
+# batch slowed down), so the count with the smaller estimate is used; the
+# inputs are the sequential leg's per-batch stage times.
+LINK_RATE = {64: 1.0, 32: 0.974}
+LINK_SLOWDOWN = {64: 1.77, 32: 1.31}
+
+
+def pick_link_workgroups(t_transfer_ms: float, t_rest_ms: float):
+    est = {w: max(t_transfer_ms / LINK_RATE[w], t_rest_ms * LINK_SLOWDOWN[w]) for w in LINK_RATE}
+    return min(est, key=lambda w: (est[w], -w)), {str(w): round(v, 4) for w, v in est.items()}
+
+
 def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_weights, MiniBatchStep, Pipeline):
     """Training iterations on the same batches: one stream with every kernel
     timed, then the two-stream pipeline (each forward waits for the
@@ -197,8 +213,14 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
     seq = time.perf_counter() - t0
     prof = G.profile_stop()
     losses = loss_hist[args.warmup:].cpu().numpy()
+    link_est = None
+    if args.train_link_workgroups == "auto":
+        t_tr = prof.get("gather_rows", (0, 0.0))[1] / args.steps
+        link_wgs, link_est = pick_link_workgroups(t_tr, seq * 1e3 / args.steps - t_tr)
+    else:
+        link_wgs = int(args.train_link_workgroups)
     pipe = Pipeline(g, c, wtrain, wl.dims, wl.fanouts, "f32", depth=args.depth, eta=args.eta,
-                    link_workgroups=args.train_link_workgroups)
+                    link_workgroups=link_wgs)
     for b in range(args.warmup):
         pipe.enqueue_train(seeds_dev[b], wl.rng_seed(b), labels, args.lr)
     pipe.synchronize()
@@ -234,7 +256,7 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
             "value": round(wl.batch * args.steps / piped, 2), "unit": "seeds/s",
             "ms_per_step": round(piped * 1e3 / args.steps, 4),
             "value_sequential": round(wl.batch * args.steps / seq, 2), "lr": args.lr,
-            "pipeline_link_workgroups": args.train_link_workgroups,
+            "pipeline_link_workgroups": link_wgs, "link_workgroup_estimates_ms": link_est,
             "loss_first": round(float(losses[0]), 6), "loss_last": round(float(losses[-1]), 6),
             "kernels": kernels}
 
@@ -259,9 +281,11 @@ def main():
                     help="locality-biased sampling: cached neighbours weigh eta (default: uniform)")
     ap.add_argument("--no-train", action="store_true", help="skip the training leg")
     ap.add_argument("--lr", type=float, default=0.01, help="SGD step of the training leg")
-    ap.add_argument("--train-link-workgroups", type=int, default=32,
-                    help="host-link workgroups of the pipelined training gathers (fewer slow the batch "
-                         "computing alongside less; the forward legs keep the default 64)")
+    ap.add_argument("--link-workgroups", default="auto",
+                    help="host-link workgroups of the pipelined forward leg's gathers: a count, or auto "
+                         "(estimated from the sequential leg's stage times)")
+    ap.add_argument("--train-link-workgroups", default="auto",
+                    help="the same for the pipelined training leg")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (scales rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
@@ -356,7 +380,14 @@ def main():
     log(f"sequential {args.steps} steps: {seq_ms:.3f} ms/step, {wl.batch * args.steps / seq_elapsed:,.0f} seeds/s")
 
     # ---- phase 2: the pipeline (batch b+1 overlaps batch b on another stream)
-    pipe = Pipeline(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, depth=args.depth, eta=args.eta)
+    fwd_link_est = None
+    if args.link_workgroups == "auto":
+        t_tr = prof.get("gather_rows", (0, 0.0))[1] / args.steps
+        fwd_link, fwd_link_est = pick_link_workgroups(t_tr, seq_ms - t_tr)
+    else:
+        fwd_link = int(args.link_workgroups)
+    pipe = Pipeline(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, depth=args.depth, eta=args.eta,
+                    link_workgroups=fwd_link)
     for b in range(args.warmup):
         slot = pipe.enqueue(seeds_dev[b], wl.rng_seed(b))
     pipe.synchronize()
@@ -368,6 +399,7 @@ def main():
     pipe.synchronize()
     torch.cuda.synchronize()
     t_end = time.perf_counter()
+    c.set_link_workgroups(64)
     elapsed = t_end - t_start
     ms_per_step = elapsed * 1e3 / args.steps
     seeds_per_s = wl.batch * args.steps / elapsed
@@ -547,7 +579,8 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
         "data": "synthetic",
-        "config": {"workload": wl.name, "pipeline_streams": args.depth, "n": wl.n, "nnz": g.nnz, "d": wl.d, "fanouts": wl.fanouts,
+        "config": {"workload": wl.name, "pipeline_streams": args.depth, "link_workgroups": fwd_link, "link_workgroup_estimates_ms": fwd_link_est,
+                   "n": wl.n, "nnz": g.nnz, "d": wl.d, "fanouts": wl.fanouts,
                    "batch": wl.batch, "layers": wl.L, "dims": wl.dims, "cache_fraction": r,
                    "store_on_device": wl.cfg["store_on_device"], "cache_policy": args.cache_policy,
                    "sampler": "uniform" if args.eta is None else f"locality-biased eta={args.eta}",
