@@ -287,7 +287,7 @@ gnnav_status gnnav_combine(const void *self_dev, int64_t ld_self, const void *ag
                            void *out_dev, int64_t ld_out, void *stream);
 
 /* ---------------------------------------------------------- SAGE forward ---
- * Algorithm 1, lines 4-6 (forward only): n_layers = L of the last
+ * Algorithm 1, its per-layer aggregate/combine loop (forward only): n_layers = L of the last
  * gnnav_sample on `b`.  Layer l (1-based) runs on hop b = L-l+1:
  * destinations F_(b-1), sources F_b; it aggregates (mean) and combines with
  * W_dev[l-1] (device, row-major [2*dims[l-1], dims[l]]), applies ReLU for

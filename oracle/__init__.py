@@ -299,7 +299,7 @@ def sage_layer(indptr, indices, X: np.ndarray, W: np.ndarray, relu: bool, bf16: 
 
 
 def sage_forward(blocks: Blocks, H0: np.ndarray, Ws, bf16: bool = False, keep=False):
-    """L-layer forward (Algorithm 1, lines 4-6, forward only).
+    """L-layer forward (Algorithm 1, its per-layer aggregate/combine loop, forward only).
 
     Layer l (1-based) uses block b = L-l+1: destinations F_(b-1), sources
     F_b; hidden layers apply ReLU (and bf16 rounding in bf16 mode); the last

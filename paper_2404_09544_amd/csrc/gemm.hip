@@ -101,18 +101,19 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 // v_mfma_f32_32x32x2_f32 per chunk pair); bf16: the chunk is the whole
 // fragment of one v_mfma_f32_32x32x16_bf16 (fp32 accumulation).  Output
 // OutT: float, or bf16 rounded to nearest-even.
-template <class T, class OutT, int BM, int BN, int STAGES>
+template <class T, class OutT, int BM, int BN, int STAGES, int WM = 2>
 __global__ void __launch_bounds__(256) k_combine_ring(const T *__restrict__ A0, int64_t lda0,
                                                       const T *__restrict__ A1, int64_t lda1, int64_t M,
                                                       const int32_t *__restrict__ m_dev, int64_t K,
                                                       const T *__restrict__ B, int64_t ldb, int64_t bseg, int nseg,
                                                       int64_t N, int relu, OutT *__restrict__ C, int64_t ldc) {
     constexpr bool BF16 = sizeof(T) == 2;
-    constexpr int E = 16 / (int)sizeof(T), CH = 8, BK = CH * E, WN = 2;
-    constexpr int WTM = BM / 2, WTN = BN / 2, TM = WTM / 32, TN = WTN / 32;
+    constexpr int E = 16 / (int)sizeof(T), CH = 8, BK = CH * E, WN = 4 / WM;
+    constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 32, TN = WTN / 32;
     constexpr int A_CH = BM * CH, B_CH = BN * CH, ST = A_CH + B_CH;
     constexpr int A_IN = A_CH / 256, B_IN = B_CH / 256, PER = A_IN + B_IN;   // DMAs per wavefront and step
-    static_assert(TM >= 1 && TN >= 1 && A_CH % 256 == 0 && B_CH % 256 == 0, "tile shape");
+    static_assert(WM * WN == 4 && TM * 32 == WTM && TN * 32 == WTN && A_CH % 256 == 0 && B_CH % 256 == 0,
+                  "tile shape");
     static_assert(STAGES >= 2 && STAGES <= 3 && (STAGES - 1) * PER < 64, "ring depth");
     __shared__ f32x4 S[STAGES * ST];
 
