@@ -10,7 +10,8 @@
 // three quarters of it.
 //
 // Ring kernel (rows 16-byte aligned, the normal case; fp32 and bf16): a
-// 256-thread workgroup owns a BM x BN output tile as 2 x 2 wavefronts.  Both
+// 256-thread workgroup owns a BM x BN output tile as WM x (4 / WM)
+// wavefronts (2 x 2, or 1 x 4 for the 96 x 256 fp32 tile).  Both
 // operands travel as 16-byte k-chunks from global memory straight into LDS
 // (global_load_lds_dwordx4) through a ring of STAGES buffers, so no
 // registers hold staged data and the loads of later steps are in flight
@@ -552,32 +553,34 @@ SharedWorkspace g_wt;
 
 enum class Fp32Kernel { kRing, kWrow };
 
-template <int BM, int BN, class T, class OutT>
+template <int BM, int BN, class T, class OutT, int WM = 2>
 void launch_ring(const T *a0, int64_t lda0, const T *a1, int64_t lda1, int64_t m, const int32_t *m_dev, int64_t k,
                  const T *b, int64_t ldb, int64_t bseg, int nseg, int64_t n, bool relu, OutT *out, int64_t ld_out,
                  hipStream_t s) {
     const int64_t nrow = (m + BM - 1) / BM, ncol = (n + BN - 1) / BN;
     const dim3 grid((unsigned)(((nrow + 7) / 8) * 8 * ncol));
-    hipLaunchKernelGGL((k_combine_ring<T, OutT, BM, BN, 2>), grid, dim3(256), 0, s, a0, lda0, a1, lda1, m, m_dev, k,
+    hipLaunchKernelGGL((k_combine_ring<T, OutT, BM, BN, 2, WM>), grid, dim3(256), 0, s, a0, lda0, a1, lda1, m, m_dev, k,
                        b, ldb, bseg, nseg, n, (int)relu, out, ld_out);
 }
 }  // namespace
 
 // fp32: KIND picks the ring kernel (weights transposed and padded first) or
 // the W-as-stored kernel.  bf16: the ring kernel.
-template <int BM, int BN, Fp32Kernel KIND>
+template <int BM, int BN, Fp32Kernel KIND, int WM = 2>
 static void launch_main(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
                         const int32_t *m_dev, int64_t k, const void *w, int64_t n, bool bf16, bool relu,
                         bool out_bf16, void *out, int64_t ld_out, hipStream_t s, const char *label) {
     const int64_t nrow = (m + BM - 1) / BM, ncol = (n + BN - 1) / BN;
     const dim3 grid((unsigned)(((nrow + 7) / 8) * 8 * ncol));
-    if (!bf16 && KIND == Fp32Kernel::kWrow) {
-        const int wvec = (((uintptr_t)w & 15u) == 0) && n % 4 == 0;
-        KernelTimer tk(label, s);
-        hipLaunchKernelGGL((k_combine_f32_wrow<BM, BN, 2, 2, 16, float>), grid, dim3(256), 0, s,
-                           (const float *)self, ld_self, (const float *)agg, ld_agg, m, m_dev, k, (const float *)w, n,
-                           (int)relu, wvec, (float *)out, ld_out);
-        return;
+    if constexpr (KIND == Fp32Kernel::kWrow) {
+        if (!bf16) {
+            const int wvec = (((uintptr_t)w & 15u) == 0) && n % 4 == 0;
+            KernelTimer tk(label, s);
+            hipLaunchKernelGGL((k_combine_f32_wrow<BM, BN, 2, 2, 16, float>), grid, dim3(256), 0, s,
+                               (const float *)self, ld_self, (const float *)agg, ld_agg, m, m_dev, k,
+                               (const float *)w, n, (int)relu, wvec, (float *)out, ld_out);
+            return;
+        }
     }
     std::lock_guard<std::mutex> lk(g_wt.mu);
     if (!g_wt.last_use) GNNAV_HIP(hipEventCreateWithFlags(&g_wt.last_use, hipEventDisableTiming));
@@ -596,14 +599,16 @@ static void launch_main(const void *self, int64_t ld_self, const void *agg, int6
     }
     KernelTimer tk(label, s);
     if (!bf16)
-        launch_ring<BM, BN>((const float *)self, ld_self, (const float *)agg, ld_agg, m, m_dev, k,
-                            g_wt.buf.as<float>(), 2 * kp, kp, 2, n, relu, (float *)out, ld_out, s);
+        launch_ring<BM, BN, float, float, WM>((const float *)self, ld_self, (const float *)agg, ld_agg, m, m_dev, k,
+                                              g_wt.buf.as<float>(), 2 * kp, kp, 2, n, relu, (float *)out, ld_out, s);
     else if (out_bf16)
-        launch_ring<BM, BN>((const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, k,
-                            g_wt.buf.as<uint16_t>(), 2 * kp, kp, 2, n, relu, (uint16_t *)out, ld_out, s);
+        launch_ring<BM, BN, uint16_t, uint16_t, WM>((const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m,
+                                                    m_dev, k, g_wt.buf.as<uint16_t>(), 2 * kp, kp, 2, n, relu,
+                                                    (uint16_t *)out, ld_out, s);
     else
-        launch_ring<BM, BN>((const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m, m_dev, k,
-                            g_wt.buf.as<uint16_t>(), 2 * kp, kp, 2, n, relu, (float *)out, ld_out, s);
+        launch_ring<BM, BN, uint16_t, float, WM>((const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m,
+                                                 m_dev, k, g_wt.buf.as<uint16_t>(), 2 * kp, kp, 2, n, relu,
+                                                 (float *)out, ld_out, s);
     GNNAV_HIP(hipEventRecord(g_wt.last_use, s));
 }
 
@@ -617,13 +622,24 @@ struct GemmChoice {
                int64_t, bool, bool, bool, void *, int64_t, hipStream_t, const char *);
 };
 
+// Outputs of the most loaded compute unit when the tiles are dealt out
+// evenly over the 256 compute units: the launch's critical path.
+static int64_t busiest_cu_outputs(int64_t m, int64_t n, int64_t bm, int64_t bn) {
+    const int64_t tiles = ((m + bm - 1) / bm) * ((n + bn - 1) / bn);
+    return (tiles + 255) / 256 * bm * bn;
+}
+
 // Tile shapes measured on MI355X.  fp32: the ring kernel with 128 x 64 tiles
 // (64 x 64 when the output is at most 64 wide, 128 x 128 once there are
 // enough of those to give every compute unit two); the W-as-stored kernel
 // when such a large output has a short K (at most 128 per segment), where
-// it measured faster (e.g. 10^5 rows of d_in = 100).  bf16: the ring kernel
-// with 128 x 64 tiles (64 x 64 for outputs at most 64 wide), 128 x 128 from
-// that same point on.
+// it measured faster (e.g. 10^5 rows of d_in = 100).  An output 129-256
+// wide takes 96 x 256 tiles (one column of tiles, A read once, four
+// 96 x 64 wavefront tiles) when that loads the busiest compute unit no more
+// than the default: 20902 x 1204 x 256 runs in 147 us instead of 154 us,
+// while at 15000 rows (157 tiles for 256 units) it would lose a third.
+// bf16: the ring kernel with 128 x 64 tiles (64 x 64 for outputs at most 64
+// wide), 128 x 128 from that same point on.
 static GemmChoice choose_main(int64_t m, int64_t d_in, int64_t d_out, bool bf16) {
     const bool big = d_out > 64 && ((m + 127) / 128) * ((d_out + 127) / 128) >= 512;
     if (bf16) {
@@ -632,9 +648,13 @@ static GemmChoice choose_main(int64_t m, int64_t d_in, int64_t d_out, bool bf16)
         return {128, 64, launch_main<128, 64, Fp32Kernel::kRing>};
     }
     if (big && d_in <= 128) return {128, 128, launch_main<128, 128, Fp32Kernel::kWrow>};
-    if (big) return {128, 128, launch_main<128, 128, Fp32Kernel::kRing>};
-    if (d_out <= 64) return {64, 64, launch_main<64, 64, Fp32Kernel::kRing>};
-    return {128, 64, launch_main<128, 64, Fp32Kernel::kRing>};
+    GemmChoice ch = big ? GemmChoice{128, 128, launch_main<128, 128, Fp32Kernel::kRing>}
+                        : d_out <= 64 ? GemmChoice{64, 64, launch_main<64, 64, Fp32Kernel::kRing>}
+                                      : GemmChoice{128, 64, launch_main<128, 64, Fp32Kernel::kRing>};
+    if (d_out > 128 && d_out <= 256 &&
+        busiest_cu_outputs(m, d_out, 96, 256) <= busiest_cu_outputs(m, d_out, ch.bm, ch.bn))
+        ch = {96, 256, launch_main<96, 256, Fp32Kernel::kRing, 1>};
+    return ch;
 }
 
 void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
