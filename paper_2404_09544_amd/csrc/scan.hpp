@@ -10,7 +10,10 @@
 // Single-pass scan with decoupled look-back: workgroups claim tiles in order
 // from an atomic ticket (so a tile only ever waits for tiles whose
 // workgroups are already running) until the tiles run out; the grid is
-// capped, not sized to the element bound.  A workgroup reduces its tile,
+// capped, not sized to the element bound, and workgroups beyond the tile
+// count of the actual length (read on the device) leave before touching the
+// ticket, so a loose bound costs an empty workgroup each, not a contended
+// atomic each.  A workgroup reduces its tile,
 // publishes the tile sum, then
 // looks back: its first wavefront polls the 64 preceding tiles at once,
 // finds the nearest one that has published an inclusive prefix, adds that
@@ -84,13 +87,15 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, uint32_t *
     const int64_t n = op.n();
     int64_t ntiles = (n + kScanTile - 1) / kScanTile;
     if (ntiles < 1) ntiles = 1;
+    const int64_t workers = ntiles < (int64_t)gridDim.x ? ntiles : (int64_t)gridDim.x;
+    if ((int64_t)blockIdx.x >= workers) return;
     for (;;) {
-        // Every workgroup draws tickets until it draws one past the last tile,
-        // so exactly ntiles + gridDim.x tickets are drawn per launch; the
+        // Every worker draws tickets until it draws one past the last tile,
+        // so exactly ntiles + workers tickets are drawn per launch; the
         // workgroup that draws the final one resets the counter for the next.
         if (threadIdx.x == 0) {
             const uint32_t t = atomicAdd(&ctl[0], 1u);
-            if ((int64_t)t == ntiles + gridDim.x - 1) atomicExch(&ctl[0], 0u);
+            if ((int64_t)t == ntiles + workers - 1) atomicExch(&ctl[0], 0u);
             s_tile = t;
         }
         __syncthreads();
