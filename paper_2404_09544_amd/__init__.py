@@ -19,6 +19,13 @@ LIB_PATH = os.path.join(_HERE, "libgnnav.so")
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run `python paper_2404_09544_amd/build.py`")
 
+# torch first: its wheel carries its own HIP runtime, which it loads by a
+# file name that differs from the runtime's soname.  Loaded after torch, the
+# library's libamdhip64.so.7 dependency resolves to that same copy; loaded
+# before, the process would end up with two runtimes (two sets of device
+# state), and allocations made through one fail in the other.
+import torch  # noqa: E402,F401
+
 _lib = C.CDLL(LIB_PATH)
 
 F32, BF16 = 0, 1

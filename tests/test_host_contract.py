@@ -1,6 +1,6 @@
 """Host-side contract checks that need no GPU: the package refuses to load
-without its HIP library (there is no CPU fallback), and bench.py measures
-one GPU only."""
+without its HIP library (there is no CPU fallback), shares torch's HIP
+runtime whatever the import order, and bench.py measures one GPU only."""
 import os
 import shutil
 import subprocess
@@ -25,3 +25,14 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU only" in r.stderr
+
+
+def test_one_hip_runtime_whatever_the_import_order():
+    """Importing the package before torch must not load a second HIP runtime
+    next to the copy that ships with torch."""
+    code = ("import paper_2404_09544_amd, torch\n"
+            "libs = {l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l}\n"
+            "print(len(libs)); print(sorted(libs))\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.splitlines()[0] == "1", r.stdout
