@@ -362,10 +362,7 @@ static void free_cache(gnnav_cache *c) {
         w->hit_list.release();
         w->miss_list.release();
         w->dev_counts.release();
-        w->scan.status.release();
-        w->scan.sums.release();
-        w->scan.prefix.release();
-        w->scan.ctl.release();
+        w->scan.release();
         delete w;
     }
     c->owner.release();
@@ -597,10 +594,7 @@ extern "C" void gnnav_blocks_free(gnnav_blocks *b) {
     b->map.release();
     b->sizes.release();
     b->nodes.release();
-    b->scan.status.release();
-    b->scan.sums.release();
-    b->scan.prefix.release();
-    b->scan.ctl.release();
+    b->scan.release();
     for (int h = 0; h < kMaxHops; ++h) {
         b->indptr[h].release();
         b->nbrs[h].release();

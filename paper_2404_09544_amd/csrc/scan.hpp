@@ -19,11 +19,19 @@
 // finds the nearest one that has published an inclusive prefix, adds that
 // prefix and the tile sums in between (a wave reduction), and moves the
 // window back by 64 tiles if none has.  It then publishes its own inclusive
-// prefix and emits.  Status words carry the call's epoch, so they never need
+// prefix and emits.  Records carry the call's epoch, so they never need
 // clearing between calls.  Each thread owns kScanItems consecutive elements,
 // so results do not depend on scheduling.  The look-back wait is bounded: a
 // wait that exceeds kSpinLimit polls gives up, counts an error and lets the
 // workgroup finish (the results are then wrong and the caller reports it).
+//
+// Publication is one 64-bit atomic store per 32-bit half of the value, each
+// word carrying the call's tag (epoch and kind) next to its half, and a
+// reader takes a record only when every word shows the current tag.  No
+// ordering between separate stores is needed, so publishing needs no
+// release fence and reading no acquire fence: on this chip those write back
+// and invalidate the whole L2 of the issuing XCD, a cost every tile would
+// otherwise pay twice and that evicted the other workgroups' working sets.
 #pragma once
 
 #include "common.hpp"
@@ -42,10 +50,13 @@ inline int64_t scan_parts(int64_t bound) {
 }
 
 // Device state of one scan sequence (calls on one stream, in order).
+// Records: per tile, kRecWords words of (tag << 32 | 32-bit half of the
+// value), tag = (epoch << 2) | kind, kind 1 in `sums` (the tile's own sum)
+// and 2 in `prefix` (inclusive prefix through the tile).
+constexpr int kRecWords = 2;   // enough for 64-bit values
 struct ScanState {
-    DevBuf status;    // uint32 per tile: (epoch << 2) | 0 none, 1 tile sum, 2 inclusive prefix
-    DevBuf sums;      // int64 per tile
-    DevBuf prefix;    // int64 per tile
+    DevBuf sums;      // uint64 [tiles][kRecWords]
+    DevBuf prefix;    // uint64 [tiles][kRecWords]
     DevBuf ctl;       // uint32 [0] ticket, [1] look-back timeouts
     int64_t tiles = 0;
     uint32_t epoch = 0;
@@ -56,12 +67,19 @@ struct ScanState {
             launch_fill_i32(ctl.as<int32_t>(), 0, 4, s);
         }
         if (t > tiles) {
-            status.ensure((size_t)t * sizeof(uint32_t), s);
-            sums.ensure((size_t)t * sizeof(int64_t), s);
-            prefix.ensure((size_t)t * sizeof(int64_t), s);
-            tiles = (int64_t)(status.bytes / sizeof(uint32_t));
-            launch_fill_i32(status.as<int32_t>(), 0, tiles, s);
+            const size_t bytes = (size_t)t * kRecWords * sizeof(uint64_t);
+            sums.ensure(bytes, s);
+            prefix.ensure(bytes, s);
+            tiles = (int64_t)(sums.bytes / (kRecWords * sizeof(uint64_t)));
+            launch_fill_i32(sums.as<int32_t>(), 0, tiles * kRecWords * 2, s);
+            launch_fill_i32(prefix.as<int32_t>(), 0, tiles * kRecWords * 2, s);
         }
+    }
+    void release() {
+        sums.release();
+        prefix.release();
+        ctl.release();
+        tiles = 0;
     }
     uint32_t next_epoch() {
         epoch = (epoch + 1) & 0x3fffffffu;
@@ -72,14 +90,35 @@ struct ScanState {
 };
 
 template <class V>
-__device__ __forceinline__ void publish(uint32_t *status, V *slot, int64_t tile, V v, uint32_t word) {
-    slot[tile] = v;
-    __hip_atomic_store(&status[tile], word, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ void publish(uint64_t *rec, int64_t tile, V v, uint32_t tag) {
+    static_assert(sizeof(V) == 4 || sizeof(V) == 8, "32- or 64-bit scan values");
+    const uint64_t bits = sizeof(V) == 8 ? (uint64_t)(int64_t)v : (uint64_t)(uint32_t)(int32_t)v;
+    uint64_t *w = rec + tile * kRecWords;
+    __hip_atomic_store(&w[0], ((uint64_t)tag << 32) | (bits & 0xffffffffull), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    if constexpr (sizeof(V) == 8)
+        __hip_atomic_store(&w[1], ((uint64_t)tag << 32) | (bits >> 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The record of `tile` if every word carries `tag`.
+template <class V>
+__device__ __forceinline__ bool read_record(const uint64_t *rec, int64_t tile, uint32_t tag, V &v) {
+    const uint64_t *w = rec + tile * kRecWords;
+    const uint64_t w0 = __hip_atomic_load(&w[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((uint32_t)(w0 >> 32) != tag) return false;
+    if constexpr (sizeof(V) == 8) {
+        const uint64_t w1 = __hip_atomic_load(&w[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if ((uint32_t)(w1 >> 32) != tag) return false;
+        v = (V)(int64_t)((w1 << 32) | (w0 & 0xffffffffull));
+    } else {
+        v = (V)(int32_t)(uint32_t)w0;
+    }
+    return true;
 }
 
 template <class Op, class V>
-__global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, uint32_t *__restrict__ status,
-                                                                V *__restrict__ sums, V *__restrict__ prefix,
+__global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, uint64_t *__restrict__ sums,
+                                                                uint64_t *__restrict__ prefix,
                                                                 uint32_t *__restrict__ ctl, uint32_t epoch) {
     __shared__ V scratch[kScanThreads / kWave];
     __shared__ int64_t s_tile;
@@ -119,19 +158,22 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, uint32_t *
             const uint32_t tag = epoch << 2;
             V pre = V(0);
             if (tile == 0) {
-                if (lane == 0) publish(status, prefix, 0, total, tag | 2u);
+                if (lane == 0) publish(prefix, 0, total, tag | 2u);
             } else {
-                if (lane == 0) publish(status, sums, tile, total, tag | 1u);
+                if (lane == 0) publish(sums, tile, total, tag | 1u);
                 int64_t base = tile - 1;
                 uint32_t spins = 0;
                 while (true) {
                     const int64_t t = base - lane;
                     // tiles before tile 0 read as a published zero prefix; the
                     // window that reaches tile 0 always stops there first
-                    const uint32_t st = t >= 0 ? __hip_atomic_load(&status[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                                               : (tag | 2u);
-                    const bool ready = (st & ~3u) == tag && (st & 3u) != 0;
-                    const uint64_t pmask = __ballot(ready && (st & 3u) == 2u);
+                    V v = V(0);
+                    bool is_prefix = t < 0, ready = t < 0;
+                    if (t >= 0) {
+                        is_prefix = read_record<V>(prefix, t, tag | 2u, v);
+                        ready = is_prefix || read_record<V>(sums, t, tag | 1u, v);
+                    }
+                    const uint64_t pmask = __ballot(is_prefix);
                     const int pidx = pmask ? __builtin_ctzll(pmask) : kWave;
                     const uint64_t need = pidx >= kWave - 1 ? ~0ull : ((1ull << (pidx + 1)) - 1);
                     if ((__ballot(ready) & need) != need) {
@@ -142,9 +184,7 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, uint32_t *
                         __builtin_amdgcn_s_sleep(1);
                         continue;
                     }
-                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-                    V v = V(0);
-                    if (lane <= pidx && t >= 0) v = (st & 3u) == 2u ? prefix[t] : sums[t];
+                    if (lane > pidx) v = V(0);
     #pragma unroll
                     for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
                     pre += v;
@@ -152,7 +192,7 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, uint32_t *
                     base -= kWave;
                     spins = 0;
                 }
-                if (lane == 0) publish(status, prefix, tile, pre + total, tag | 2u);
+                if (lane == 0) publish(prefix, tile, pre + total, tag | 2u);
             }
             if (lane == 0) {
                 s_prefix = pre;
@@ -180,8 +220,7 @@ void run_scan(const Op &op, int64_t bound, ScanState &st, const char *name, hipS
     const uint32_t epoch = st.next_epoch();
     KernelTimer t(name, s);
     hipLaunchKernelGGL((k_scan_onepass<Op, V>), dim3((unsigned)grid), dim3(kScanThreads), 0, s, op,
-                       st.status.as<uint32_t>(), st.sums.as<V>(), st.prefix.as<V>(), st.ctl.as<uint32_t>(),
-                       epoch);
+                       st.sums.as<uint64_t>(), st.prefix.as<uint64_t>(), st.ctl.as<uint32_t>(), epoch);
     GNNAV_HIP(hipGetLastError());
 }
 
