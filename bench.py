@@ -274,7 +274,7 @@ def main():
                     help="cap on the threads of the all-core oracle baseline")
     ap.add_argument("--depth", type=int, default=3,
                     help="streams in the pipelined pass (3: a third batch in flight keeps the latency-bound "
-                         "sampling kernels busier; 4 would share a hardware queue)")
+                         "sampling kernels busier; 4 measured slower)")
     ap.add_argument("--cache-policy", choices=["static", "fifo"], default="static",
                     help="fifo: admit each batch's misses into a ring over the last cache slots")
     ap.add_argument("--dynamic-fraction", type=float, default=1.0,
