@@ -692,11 +692,11 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
                         fanouts[h - 1], rng_seed, (uint32_t)(h - 1), nb[h - 1], &b->scan,
                         bias ? bias->slot_map.as<int32_t>() : nullptr, eta,
                         bias && bias->ring_n == 0 ? bias->part_col.as<int32_t>() : nullptr,
-                        bias && bias->ring_n == 0 ? bias->part_cnt.as<int32_t>() : nullptr};
+                        bias && bias->ring_n == 0 ? bias->part_cnt.as<int32_t>() : nullptr, map};
         launch_count_scan(a, s);
         launch_sample_hop(a, s);
         DedupArgs dh{b->nbrs[h - 1].as<int32_t>(), 0, sz + kSizeE + h, eb[h], map, g->n, nodes,
-                     sz + kSizeN + h - 1, sz + kSizeN + h, nullptr, &b->scan};
+                     sz + kSizeN + h - 1, sz + kSizeN + h, nullptr, &b->scan, true};
         launch_dedup(dh, s);
         launch_relabel(b->nbrs[h - 1].as<int32_t>(), sz + kSizeE + h, eb[h], map,
                        b->indices[h - 1].as<int32_t>(), s);

@@ -152,6 +152,7 @@ struct SampleHopArgs {
     // within each class) and the per-vertex cached counts, for this slot map
     const int32_t *part_col = nullptr;
     const int32_t *part_cnt = nullptr;
+    int32_t *first_map = nullptr;            // node table: first position of each written id
 };
 void launch_partition_rows(const void *row_ptr, bool offsets_i64, const int32_t *col, int64_t n,
                            const int32_t *slot_map, int32_t *part_col, int32_t *part_cnt, hipStream_t s);
@@ -170,6 +171,7 @@ struct DedupArgs {
     int32_t *size_out;       // device |F_h|
     int32_t *err;            // device count of out-of-range ids (nullable)
     ScanState *scan;
+    bool first_done = false; // first positions already in `map` (taken while writing the list)
 };
 void launch_dedup(const DedupArgs &a, hipStream_t s);
 void launch_relabel(const int32_t *list, const int32_t *len_ptr, int64_t len_bound,

@@ -5,8 +5,9 @@
 //   sample       one wavefront per destination row: copy the row when
 //                deg <= k, else Floyd's k-subset with Philox4x32-10 draws
 //   dedup        first position of each id in N_h (atomicMin on a dense
-//                per-node table), then an order-preserving scan appends the
-//                new ids to the node list and records their local ids
+//                per-node table, taken by the sample kernel as it writes
+//                N_h), then an order-preserving scan appends the new ids to
+//                the node list and records their local ids
 //   relabel      indices_h[p] = local id of N_h[p]
 // The node table lives in HBM (int32 per graph node).  Entry encoding:
 // INT_MAX = unseen, p >= 0 = smallest position seen in the current list,
@@ -103,6 +104,13 @@ void launch_count_scan(const SampleHopArgs &a, hipStream_t s) {
     }
 }
 
+// First position of `id` in the hop's list: positions only ever lower an
+// entry that has not been claimed by the frontier (negative entries are
+// smaller than every position), and the read skips most of the atomics.
+__device__ __forceinline__ void note_first(int32_t *map, int32_t id, int64_t pos) {
+    if (map && map[id] > (int32_t)pos) atomicMin(&map[id], (int32_t)pos);
+}
+
 // ---------------------------------------------------------- sample kernel
 // One wavefront per destination row, grid-stride over rows.  For k <= 64
 // lane j holds draw j: t_j = floor(x_j * (m_j + 1) / 2^32), m_j = deg-k+j.
@@ -116,7 +124,8 @@ __global__ void __launch_bounds__(256) k_sample_small(const OffT *__restrict__ r
                                                       const int32_t *__restrict__ n_prev,
                                                       const int32_t *__restrict__ indptr,
                                                       int32_t *__restrict__ out, int32_t k,
-                                                      uint32_t key0, uint32_t key1, uint32_t hop) {
+                                                      uint32_t key0, uint32_t key1, uint32_t hop,
+                                                      int32_t *__restrict__ first) {
     const int lane = lane_id();
     const int64_t n_rows = *n_prev;
     const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
@@ -124,9 +133,14 @@ __global__ void __launch_bounds__(256) k_sample_small(const OffT *__restrict__ r
         const int32_t v = nodes[i];
         int64_t start;
         const int64_t deg = row_degree(row_ptr, v, start);
-        int32_t *dst = out + indptr[i];
+        const int64_t at = indptr[i];
+        int32_t *dst = out + at;
         if (k < 0 || deg <= k) {
-            for (int64_t j = lane; j < deg; j += kWave) dst[j] = col[start + j];
+            for (int64_t j = lane; j < deg; j += kWave) {
+                const int32_t id = col[start + j];
+                dst[j] = id;
+                note_first(first, id, at + j);
+            }
             continue;
         }
         uint32_t t = 0, m = 0;
@@ -141,7 +155,11 @@ __global__ void __launch_bounds__(256) k_sample_small(const OffT *__restrict__ r
             const uint64_t clash = __ballot(lane < j && pick == tj);
             if (lane == j && clash != 0) pick = m;
         }
-        if (lane < k) dst[lane] = col[start + pick];
+        if (lane < k) {
+            const int32_t id = col[start + pick];
+            dst[lane] = id;
+            note_first(first, id, at + lane);
+        }
     }
 }
 
@@ -156,7 +174,8 @@ __global__ void __launch_bounds__(256) k_sample_big(const OffT *__restrict__ row
                                                     const int32_t *__restrict__ n_prev,
                                                     const int32_t *__restrict__ indptr,
                                                     int32_t *__restrict__ out, int32_t k,
-                                                    uint32_t key0, uint32_t key1, uint32_t hop) {
+                                                    uint32_t key0, uint32_t key1, uint32_t hop,
+                                                    int32_t *__restrict__ first) {
     __shared__ uint32_t taken_all[256 / kWave][kMaxFanout];
     uint32_t *taken = taken_all[threadIdx.x / kWave];
     const int lane = lane_id();
@@ -166,9 +185,14 @@ __global__ void __launch_bounds__(256) k_sample_big(const OffT *__restrict__ row
         const int32_t v = nodes[i];
         int64_t start;
         const int64_t deg = row_degree(row_ptr, v, start);
-        int32_t *dst = out + indptr[i];
+        const int64_t at = indptr[i];
+        int32_t *dst = out + at;
         if (deg <= k) {
-            for (int64_t j = lane; j < deg; j += kWave) dst[j] = col[start + j];
+            for (int64_t j = lane; j < deg; j += kWave) {
+                const int32_t id = col[start + j];
+                dst[j] = id;
+                note_first(first, id, at + j);
+            }
             continue;
         }
         for (int jb = 0; jb < k; jb += kWave) {
@@ -192,7 +216,11 @@ __global__ void __launch_bounds__(256) k_sample_big(const OffT *__restrict__ row
             __builtin_amdgcn_s_waitcnt(0);
             __builtin_amdgcn_wave_barrier();
         }
-        for (int q = lane; q < k; q += kWave) dst[q] = col[start + taken[q]];
+        for (int q = lane; q < k; q += kWave) {
+            const int32_t id = col[start + taken[q]];
+            dst[q] = id;
+            note_first(first, id, at + q);
+        }
         __builtin_amdgcn_wave_barrier();
     }
 }
@@ -219,7 +247,8 @@ __global__ void __launch_bounds__(256) k_sample_biased(const OffT *__restrict__ 
                                                        uint32_t key1, uint32_t hop,
                                                        const int32_t *__restrict__ slot_map, uint32_t eta,
                                                        const int32_t *__restrict__ part_col,
-                                                       const int32_t *__restrict__ part_cnt) {
+                                                       const int32_t *__restrict__ part_cnt,
+                                                       int32_t *__restrict__ first) {
     const int lane = lane_id();
     const int64_t n_rows = *n_prev;
     const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
@@ -227,9 +256,14 @@ __global__ void __launch_bounds__(256) k_sample_biased(const OffT *__restrict__ 
         const int32_t v = nodes[i];
         int64_t start;
         const int64_t deg = row_degree(row_ptr, v, start);
-        int32_t *dst = out + indptr[i];
+        const int64_t at = indptr[i];
+        int32_t *dst = out + at;
         if (k < 0 || deg <= k) {
-            for (int64_t j = lane; j < deg; j += kWave) dst[j] = col[start + j];
+            for (int64_t j = lane; j < deg; j += kWave) {
+                const int32_t id = col[start + j];
+                dst[j] = id;
+                note_first(first, id, at + j);
+            }
             continue;
         }
         // cached neighbours of the row
@@ -280,7 +314,11 @@ __global__ void __launch_bounds__(256) k_sample_biased(const OffT *__restrict__ 
         }
         // 3. class index -> row offset
         if (part_col) {
-            if (lane < k) dst[lane] = part_col[start + (cached_lane ? 0 : c) + pick];
+            if (lane < k) {
+                const int32_t id = part_col[start + (cached_lane ? 0 : c) + pick];
+                dst[lane] = id;
+                note_first(first, id, at + lane);
+            }
             continue;
         }
         int64_t seen = 0, pos = -1;
@@ -298,7 +336,11 @@ __global__ void __launch_bounds__(256) k_sample_biased(const OffT *__restrict__ 
             }
             seen += cnt;
         }
-        if (lane < k) dst[lane] = col[start + (pos < 0 ? 0 : pos)];   // pos >= 0 whenever pick < class size
+        if (lane < k) {
+            const int32_t id = col[start + (pos < 0 ? 0 : pos)];   // pos >= 0 whenever pick < class size
+            dst[lane] = id;
+            note_first(first, id, at + lane);
+        }
     }
 }
 
@@ -362,11 +404,11 @@ void launch_sample_hop(const SampleHopArgs &a, hipStream_t s) {
         if (a.offsets_i64)
             hipLaunchKernelGGL(k_sample_biased<int64_t>, dim3(grid), dim3(256), 0, s, (const int64_t *)a.row_ptr, a.col,
                                a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, a.bias_slot_map,
-                               a.eta, a.part_col, a.part_cnt);
+                               a.eta, a.part_col, a.part_cnt, a.first_map);
         else
             hipLaunchKernelGGL(k_sample_biased<int32_t>, dim3(grid), dim3(256), 0, s, (const int32_t *)a.row_ptr, a.col,
                                a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, a.bias_slot_map,
-                               a.eta, a.part_col, a.part_cnt);
+                               a.eta, a.part_col, a.part_cnt, a.first_map);
         GNNAV_HIP(hipGetLastError());
         return;
     }
@@ -378,11 +420,11 @@ void launch_sample_hop(const SampleHopArgs &a, hipStream_t s) {
     if (a.offsets_i64) {
         auto kern = big ? k_sample_big<int64_t> : k_sample_small<int64_t>;
         hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, (const int64_t *)a.row_ptr, a.col,
-                           a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop);
+                           a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, a.first_map);
     } else {
         auto kern = big ? k_sample_big<int32_t> : k_sample_small<int32_t>;
         hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, (const int32_t *)a.row_ptr, a.col,
-                           a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop);
+                           a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, a.first_map);
     }
     GNNAV_HIP(hipGetLastError());
 }
@@ -434,7 +476,7 @@ struct DedupOp {
 };
 
 void launch_dedup(const DedupArgs &a, hipStream_t s) {
-    if (a.len_bound > 0) {
+    if (a.len_bound > 0 && !a.first_done) {
         KernelTimer t("dedup_first", s);
         hipLaunchKernelGGL(k_first_position, dim3(grid_for(a.len_bound, 256, 8192)), dim3(256), 0, s,
                            a.list, a.len_const, a.len_ptr, a.map, a.n_nodes, a.err);
