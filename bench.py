@@ -565,7 +565,7 @@ def main():
     # (t_transfer = miss copy), the sampling kernels, and the device compute.
     def per_batch(names):
         return sum(prof[n][1] for n in names if n in prof) / args.steps
-    samp = ["dedup_first", "dedup_scan", "count_scan", "sample_hop", "relabel", "reset_map"]
+    samp = ["dedup_first", "dedup_scan", "count_scan", "sample_hop", "relabel"]
     comp = [n for n in prof if n.startswith(("aggregate_mean", "combine_gemm"))] + ["classify", "weights_transpose"]
     repl = ["cache_evict", "cache_admit", "cache_advance"]
     eq4 = {"t_sample_ms": round(per_batch(samp), 4), "t_transfer_ms": round(per_batch(["gather_rows"]), 4),

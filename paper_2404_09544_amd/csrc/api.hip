@@ -563,6 +563,7 @@ struct gnnav_blocks {
     int64_t nb[kMaxHops + 1] = {0};    // Eq. 12 capacity bounds of the last sample
     int64_t eb[kMaxHops + 1] = {0};
     int64_t map_nodes = -1;
+    uint32_t map_epoch = 0;            // sampling calls since the node table was last filled
     DevBuf map, sizes, nodes;
     ScanState scan;
     DevBuf indptr[kMaxHops], nbrs[kMaxHops], indices[kMaxHops];
@@ -665,11 +666,15 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
     int64_t max_list = n_seeds;
     for (int h = 1; h <= n_hops; ++h) max_list = std::max(max_list, std::max(eb[h], nb[h - 1] + 1));
     // workspace
-    if (b->map_nodes < g->n) {
-        b->map.ensure(std::max<int64_t>(g->n, 1) * sizeof(int32_t), s);
-        launch_fill_i32(b->map.as<int32_t>(), INT_MAX, g->n, s);
+    // node table: all-ones entries are older than every call's tag; after
+    // 2^32 - 2 calls the tags would wrap, so the table is filled again
+    if (b->map_nodes < g->n || b->map_epoch == 0xfffffffeu) {
+        b->map.ensure(std::max<int64_t>(g->n, 1) * sizeof(uint64_t), s);
+        launch_fill_i32(b->map.as<int32_t>(), -1, 2 * std::max<int64_t>(g->n, 1), s);
         b->map_nodes = g->n;
+        b->map_epoch = 0;
     }
+    const uint32_t tag = 0xffffffffu - ++b->map_epoch;
     b->sizes.ensure(kSizeSlots * sizeof(int32_t), s);
     b->nodes.ensure(std::max<int64_t>(nb[n_hops], 1) * sizeof(int32_t), s);
     b->scan.ensure(max_list, s);
@@ -679,11 +684,11 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
         b->indices[h - 1].ensure(std::max<int64_t>(eb[h], 1) * sizeof(int32_t), s);
     }
     int32_t *sz = b->sizes.as<int32_t>();
-    int32_t *map = b->map.as<int32_t>();
+    uint64_t *map = b->map.as<uint64_t>();
     int32_t *nodes = b->nodes.as<int32_t>();
     launch_fill_i32(sz, 0, kSizeSlots, s);
     // F_0: seeds without repeats, first occurrence kept
-    DedupArgs d0{seeds_dev, n_seeds, nullptr, n_seeds, map, g->n, nodes, nullptr, sz + kSizeN, sz + kSizeErr,
+    DedupArgs d0{seeds_dev, n_seeds, nullptr, n_seeds, map, tag, g->n, nodes, nullptr, sz + kSizeN, sz + kSizeErr,
                  &b->scan};
     launch_dedup(d0, s);
     for (int h = 1; h <= n_hops; ++h) {
@@ -692,16 +697,15 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
                         fanouts[h - 1], rng_seed, (uint32_t)(h - 1), nb[h - 1], &b->scan,
                         bias ? bias->slot_map.as<int32_t>() : nullptr, eta,
                         bias && bias->ring_n == 0 ? bias->part_col.as<int32_t>() : nullptr,
-                        bias && bias->ring_n == 0 ? bias->part_cnt.as<int32_t>() : nullptr, map};
+                        bias && bias->ring_n == 0 ? bias->part_cnt.as<int32_t>() : nullptr, map, tag};
         launch_count_scan(a, s);
         launch_sample_hop(a, s);
-        DedupArgs dh{b->nbrs[h - 1].as<int32_t>(), 0, sz + kSizeE + h, eb[h], map, g->n, nodes,
+        DedupArgs dh{b->nbrs[h - 1].as<int32_t>(), 0, sz + kSizeE + h, eb[h], map, tag, g->n, nodes,
                      sz + kSizeN + h - 1, sz + kSizeN + h, nullptr, &b->scan, true};
         launch_dedup(dh, s);
         launch_relabel(b->nbrs[h - 1].as<int32_t>(), sz + kSizeE + h, eb[h], map,
                        b->indices[h - 1].as<int32_t>(), s);
     }
-    launch_reset_map(nodes, sz + kSizeN + n_hops, nb[n_hops], map, s);
     b->L = n_hops;
     b->host_sizes = false;
     for (int h = 0; h <= n_hops; ++h) {

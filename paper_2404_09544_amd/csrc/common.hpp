@@ -152,7 +152,8 @@ struct SampleHopArgs {
     // within each class) and the per-vertex cached counts, for this slot map
     const int32_t *part_col = nullptr;
     const int32_t *part_cnt = nullptr;
-    int32_t *first_map = nullptr;            // node table: first position of each written id
+    uint64_t *first_map = nullptr;           // node table: first position of each written id
+    uint32_t map_tag = 0;                    // the node table tag of this sampling call
 };
 void launch_partition_rows(const void *row_ptr, bool offsets_i64, const int32_t *col, int64_t n,
                            const int32_t *slot_map, int32_t *part_col, int32_t *part_cnt, hipStream_t s);
@@ -164,7 +165,8 @@ struct DedupArgs {
     int64_t len_const;       // used when len_ptr == nullptr
     const int32_t *len_ptr;  // device length
     int64_t len_bound;
-    int32_t *map;            // int32[n_nodes]
+    uint64_t *map;           // node table, uint64[n_nodes] (sample.hip)
+    uint32_t tag;            // this sampling call's tag in it
     int64_t n_nodes;
     int32_t *nodes;
     const int32_t *base_ptr; // device |F_(h-1)| (nullptr: 0)
@@ -175,9 +177,7 @@ struct DedupArgs {
 };
 void launch_dedup(const DedupArgs &a, hipStream_t s);
 void launch_relabel(const int32_t *list, const int32_t *len_ptr, int64_t len_bound,
-                    const int32_t *map, int32_t *indices, hipStream_t s);
-void launch_reset_map(const int32_t *nodes, const int32_t *n_ptr, int64_t bound, int32_t *map,
-                      hipStream_t s);
+                    const uint64_t *map, int32_t *indices, hipStream_t s);
 
 // gather.hip
 struct GatherArgs {

@@ -9,9 +9,12 @@
 //                N_h), then an order-preserving scan appends the new ids to
 //                the node list and records their local ids
 //   relabel      indices_h[p] = local id of N_h[p]
-// The node table lives in HBM (int32 per graph node).  Entry encoding:
-// INT_MAX = unseen, p >= 0 = smallest position seen in the current list,
-// -(local+1) = already in the frontier with that local id.
+// The node table lives in HBM, one 64-bit entry per graph node:
+// (tag << 32) | word with tag = 0xffffffff - (the sampling call's epoch), so
+// every entry left by an earlier call compares above every entry of the
+// current one and counts as unseen; nothing is cleared between calls.
+// Current-call words: the local id (< 2^31) once the node is in the
+// frontier, 2^31 + p for the smallest position p seen in the current list.
 #include "common.hpp"
 #include "scan.hpp"
 
@@ -104,11 +107,19 @@ void launch_count_scan(const SampleHopArgs &a, hipStream_t s) {
     }
 }
 
-// First position of `id` in the hop's list: positions only ever lower an
-// entry that has not been claimed by the frontier (negative entries are
+__device__ __forceinline__ uint64_t node_position(uint32_t tag, int64_t p) {
+    return ((uint64_t)tag << 32) | (0x80000000ull + (uint64_t)p);
+}
+__device__ __forceinline__ uint64_t node_local(uint32_t tag, int64_t local) {
+    return ((uint64_t)tag << 32) | (uint64_t)local;
+}
+
+// First position of `id` in the hop's list: a position only ever lowers a
+// stale entry or a larger position of this call (frontier entries are
 // smaller than every position), and the read skips most of the atomics.
-__device__ __forceinline__ void note_first(int32_t *map, int32_t id, int64_t pos) {
-    if (map && map[id] > (int32_t)pos) atomicMin(&map[id], (int32_t)pos);
+__device__ __forceinline__ void note_first(unsigned long long *map, uint32_t tag, int32_t id, int64_t pos) {
+    const unsigned long long e = node_position(tag, pos);
+    if (map && map[id] > e) atomicMin(&map[id], e);
 }
 
 // ---------------------------------------------------------- sample kernel
@@ -125,7 +136,7 @@ __global__ void __launch_bounds__(256) k_sample_small(const OffT *__restrict__ r
                                                       const int32_t *__restrict__ indptr,
                                                       int32_t *__restrict__ out, int32_t k,
                                                       uint32_t key0, uint32_t key1, uint32_t hop,
-                                                      int32_t *__restrict__ first) {
+                                                      unsigned long long *__restrict__ first, uint32_t tag) {
     const int lane = lane_id();
     const int64_t n_rows = *n_prev;
     const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
@@ -139,7 +150,7 @@ __global__ void __launch_bounds__(256) k_sample_small(const OffT *__restrict__ r
             for (int64_t j = lane; j < deg; j += kWave) {
                 const int32_t id = col[start + j];
                 dst[j] = id;
-                note_first(first, id, at + j);
+                note_first(first, tag, id, at + j);
             }
             continue;
         }
@@ -158,7 +169,7 @@ __global__ void __launch_bounds__(256) k_sample_small(const OffT *__restrict__ r
         if (lane < k) {
             const int32_t id = col[start + pick];
             dst[lane] = id;
-            note_first(first, id, at + lane);
+            note_first(first, tag, id, at + lane);
         }
     }
 }
@@ -175,7 +186,7 @@ __global__ void __launch_bounds__(256) k_sample_big(const OffT *__restrict__ row
                                                     const int32_t *__restrict__ indptr,
                                                     int32_t *__restrict__ out, int32_t k,
                                                     uint32_t key0, uint32_t key1, uint32_t hop,
-                                                    int32_t *__restrict__ first) {
+                                                    unsigned long long *__restrict__ first, uint32_t tag) {
     __shared__ uint32_t taken_all[256 / kWave][kMaxFanout];
     uint32_t *taken = taken_all[threadIdx.x / kWave];
     const int lane = lane_id();
@@ -191,7 +202,7 @@ __global__ void __launch_bounds__(256) k_sample_big(const OffT *__restrict__ row
             for (int64_t j = lane; j < deg; j += kWave) {
                 const int32_t id = col[start + j];
                 dst[j] = id;
-                note_first(first, id, at + j);
+                note_first(first, tag, id, at + j);
             }
             continue;
         }
@@ -219,7 +230,7 @@ __global__ void __launch_bounds__(256) k_sample_big(const OffT *__restrict__ row
         for (int q = lane; q < k; q += kWave) {
             const int32_t id = col[start + taken[q]];
             dst[q] = id;
-            note_first(first, id, at + q);
+            note_first(first, tag, id, at + q);
         }
         __builtin_amdgcn_wave_barrier();
     }
@@ -248,7 +259,7 @@ __global__ void __launch_bounds__(256) k_sample_biased(const OffT *__restrict__ 
                                                        const int32_t *__restrict__ slot_map, uint32_t eta,
                                                        const int32_t *__restrict__ part_col,
                                                        const int32_t *__restrict__ part_cnt,
-                                                       int32_t *__restrict__ first) {
+                                                       unsigned long long *__restrict__ first, uint32_t tag) {
     const int lane = lane_id();
     const int64_t n_rows = *n_prev;
     const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
@@ -262,7 +273,7 @@ __global__ void __launch_bounds__(256) k_sample_biased(const OffT *__restrict__ 
             for (int64_t j = lane; j < deg; j += kWave) {
                 const int32_t id = col[start + j];
                 dst[j] = id;
-                note_first(first, id, at + j);
+                note_first(first, tag, id, at + j);
             }
             continue;
         }
@@ -317,7 +328,7 @@ __global__ void __launch_bounds__(256) k_sample_biased(const OffT *__restrict__ 
             if (lane < k) {
                 const int32_t id = part_col[start + (cached_lane ? 0 : c) + pick];
                 dst[lane] = id;
-                note_first(first, id, at + lane);
+                note_first(first, tag, id, at + lane);
             }
             continue;
         }
@@ -339,7 +350,7 @@ __global__ void __launch_bounds__(256) k_sample_biased(const OffT *__restrict__ 
         if (lane < k) {
             const int32_t id = col[start + (pos < 0 ? 0 : pos)];   // pos >= 0 whenever pick < class size
             dst[lane] = id;
-            note_first(first, id, at + lane);
+            note_first(first, tag, id, at + lane);
         }
     }
 }
@@ -404,11 +415,11 @@ void launch_sample_hop(const SampleHopArgs &a, hipStream_t s) {
         if (a.offsets_i64)
             hipLaunchKernelGGL(k_sample_biased<int64_t>, dim3(grid), dim3(256), 0, s, (const int64_t *)a.row_ptr, a.col,
                                a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, a.bias_slot_map,
-                               a.eta, a.part_col, a.part_cnt, a.first_map);
+                               a.eta, a.part_col, a.part_cnt, (unsigned long long *)a.first_map, a.map_tag);
         else
             hipLaunchKernelGGL(k_sample_biased<int32_t>, dim3(grid), dim3(256), 0, s, (const int32_t *)a.row_ptr, a.col,
                                a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, a.bias_slot_map,
-                               a.eta, a.part_col, a.part_cnt, a.first_map);
+                               a.eta, a.part_col, a.part_cnt, (unsigned long long *)a.first_map, a.map_tag);
         GNNAV_HIP(hipGetLastError());
         return;
     }
@@ -420,11 +431,11 @@ void launch_sample_hop(const SampleHopArgs &a, hipStream_t s) {
     if (a.offsets_i64) {
         auto kern = big ? k_sample_big<int64_t> : k_sample_small<int64_t>;
         hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, (const int64_t *)a.row_ptr, a.col,
-                           a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, a.first_map);
+                           a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, (unsigned long long *)a.first_map, a.map_tag);
     } else {
         auto kern = big ? k_sample_big<int32_t> : k_sample_small<int32_t>;
         hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, (const int32_t *)a.row_ptr, a.col,
-                           a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, a.first_map);
+                           a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, (unsigned long long *)a.first_map, a.map_tag);
     }
     GNNAV_HIP(hipGetLastError());
 }
@@ -434,8 +445,8 @@ __device__ __forceinline__ int64_t list_len(int64_t c, const int32_t *p) { retur
 
 __global__ void __launch_bounds__(256) k_first_position(const int32_t *__restrict__ list, int64_t len_const,
                                                         const int32_t *__restrict__ len_ptr,
-                                                        int32_t *__restrict__ map, int64_t n_nodes,
-                                                        int32_t *__restrict__ err) {
+                                                        unsigned long long *__restrict__ map, uint32_t tag,
+                                                        int64_t n_nodes, int32_t *__restrict__ err) {
     const int64_t len = list_len(len_const, len_ptr);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     int32_t bad = 0;
@@ -445,7 +456,7 @@ __global__ void __launch_bounds__(256) k_first_position(const int32_t *__restric
             ++bad;
             continue;
         }
-        if (map[id] > (int32_t)p) atomicMin(&map[id], (int32_t)p);
+        note_first(map, tag, id, p);
     }
     if (bad && err) atomicAdd(err, bad);
 }
@@ -454,7 +465,8 @@ struct DedupOp {
     const int32_t *list;
     int64_t len_const;
     const int32_t *len_ptr;
-    int32_t *map;
+    unsigned long long *map;
+    uint32_t tag;
     int64_t n_nodes;
     int32_t *nodes;
     const int32_t *base_ptr;
@@ -463,14 +475,14 @@ struct DedupOp {
     __device__ int32_t value(int64_t p) const {
         const int32_t id = list[p];
         if (id < 0 || id >= n_nodes) return 0;
-        return map[id] == (int32_t)p ? 1 : 0;
+        return map[id] == node_position(tag, p) ? 1 : 0;
     }
     __device__ void emit(int64_t p, int32_t prefix, int32_t v) const {
         if (!v) return;
         const int32_t id = list[p];
         const int32_t local = (base_ptr ? *base_ptr : 0) + prefix;
         nodes[local] = id;
-        map[id] = -(local + 1);
+        map[id] = node_local(tag, local);
     }
     __device__ void total(int32_t t) const { *size_out = (base_ptr ? *base_ptr : 0) + t; }
 };
@@ -479,46 +491,30 @@ void launch_dedup(const DedupArgs &a, hipStream_t s) {
     if (a.len_bound > 0 && !a.first_done) {
         KernelTimer t("dedup_first", s);
         hipLaunchKernelGGL(k_first_position, dim3(grid_for(a.len_bound, 256, 8192)), dim3(256), 0, s,
-                           a.list, a.len_const, a.len_ptr, a.map, a.n_nodes, a.err);
+                           a.list, a.len_const, a.len_ptr, (unsigned long long *)a.map, a.tag, a.n_nodes, a.err);
         GNNAV_HIP(hipGetLastError());
     }
-    DedupOp op{a.list, a.len_const, a.len_ptr, a.map, a.n_nodes, a.nodes, a.base_ptr, a.size_out};
+    DedupOp op{a.list, a.len_const, a.len_ptr, (unsigned long long *)a.map, a.tag, a.n_nodes, a.nodes, a.base_ptr,
+               a.size_out};
     run_scan<DedupOp, int32_t>(op, a.len_bound, *a.scan, "dedup_scan", s);
 }
 
 __global__ void __launch_bounds__(256) k_relabel(const int32_t *__restrict__ list,
                                                  const int32_t *__restrict__ len_ptr,
-                                                 const int32_t *__restrict__ map,
+                                                 const uint64_t *__restrict__ map,
                                                  int32_t *__restrict__ indices) {
     const int64_t len = *len_ptr;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < len; p += stride)
-        indices[p] = -map[list[p]] - 1;
+        indices[p] = (int32_t)(uint32_t)map[list[p]];   // every listed id is in the frontier by now
 }
 
-void launch_relabel(const int32_t *list, const int32_t *len_ptr, int64_t len_bound, const int32_t *map,
+void launch_relabel(const int32_t *list, const int32_t *len_ptr, int64_t len_bound, const uint64_t *map,
                     int32_t *indices, hipStream_t s) {
     if (len_bound <= 0) return;
     KernelTimer t("relabel", s);
     hipLaunchKernelGGL(k_relabel, dim3(grid_for(len_bound, 256, 8192)), dim3(256), 0, s, list, len_ptr,
                        map, indices);
-    GNNAV_HIP(hipGetLastError());
-}
-
-__global__ void __launch_bounds__(256) k_reset_map(const int32_t *__restrict__ nodes,
-                                                   const int32_t *__restrict__ n_ptr,
-                                                   int32_t *__restrict__ map) {
-    const int64_t n = *n_ptr;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
-        map[nodes[i]] = INT_MAX;
-}
-
-void launch_reset_map(const int32_t *nodes, const int32_t *n_ptr, int64_t bound, int32_t *map,
-                      hipStream_t s) {
-    if (bound <= 0) return;
-    KernelTimer t("reset_map", s);
-    hipLaunchKernelGGL(k_reset_map, dim3(grid_for(bound, 256, 8192)), dim3(256), 0, s, nodes, n_ptr, map);
     GNNAV_HIP(hipGetLastError());
 }
 

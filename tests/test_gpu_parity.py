@@ -167,6 +167,23 @@ def test_sample_bad_seed_then_reuse(G):
     assert e.value.status == 1
 
 
+def test_sample_blocks_reused_across_graphs(G):
+    """One Blocks object (one node table, never cleared between calls) sampling
+    a larger graph, a smaller one, and the larger one again: entries left by
+    earlier calls must count as unseen."""
+    big = graph_case("random-3000-40000-1")
+    n2, u2, v2 = graph_case("random-3000-40000-2")
+    keep = (u2 < 2000) & (v2 < 2000)
+    small = (2000, u2[keep], v2[keep])
+    blocks = G.Blocks()
+    for i, (n, u, v) in enumerate([big, small, big, small]):
+        say("blocks reuse", i, n)
+        g = G.Graph(n, u, v)
+        seeds = np.random.default_rng(i).integers(0, n, 500).astype(np.int32)
+        G.sample(g, dev(seeds), [10, 5], 40 + i, blocks)
+        compare_blocks(G, blocks, O.sample_blocks(O.build_csr(n, u, v), seeds, [10, 5], 40 + i))
+
+
 # ---------------------------------------------------------------- gather
 
 GATHER_CASES = [(1, "f32"), (3, "f32"), (64, "f32"), (100, "f32"), (602, "f32"),
