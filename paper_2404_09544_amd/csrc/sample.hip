@@ -15,6 +15,8 @@
 // current one and counts as unseen; nothing is cleared between calls.
 // Current-call words: the local id (< 2^31) once the node is in the
 // frontier, 2^31 + p for the smallest position p seen in the current list.
+#include <type_traits>
+
 #include "common.hpp"
 #include "scan.hpp"
 
@@ -170,6 +172,56 @@ __global__ void __launch_bounds__(256) k_sample_small(const OffT *__restrict__ r
             const int32_t id = col[start + pick];
             dst[lane] = id;
             note_first(first, tag, id, at + lane);
+        }
+    }
+}
+
+// 0 < k <= G <= 32: the same selection with G lanes per row, 64 / G rows
+// per wavefront (a hop's fanout is uniform, so the rows of a wavefront walk
+// the same j loop; lane j of a row reads t_j of its own row by a width-G
+// shuffle and tests the row's bits of one ballot).
+template <class OffT, int G>
+__global__ void __launch_bounds__(256) k_sample_group(const OffT *__restrict__ row_ptr,
+                                                      const int32_t *__restrict__ col,
+                                                      const int32_t *__restrict__ nodes,
+                                                      const int32_t *__restrict__ n_prev,
+                                                      const int32_t *__restrict__ indptr,
+                                                      int32_t *__restrict__ out, int32_t k,
+                                                      uint32_t key0, uint32_t key1, uint32_t hop,
+                                                      unsigned long long *__restrict__ first, uint32_t tag) {
+    constexpr int R = kWave / G;
+    const int lane = lane_id(), r = lane / G, gl = lane % G;
+    const int64_t n_rows = *n_prev;
+    const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
+    for (int64_t base = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave * R; base < n_rows;
+         base += nwaves * R) {
+        const int64_t i = base + r;
+        const bool valid = i < n_rows;
+        int32_t v = 0;
+        int64_t start = 0, deg = 0, at = 0;
+        if (valid) {
+            v = nodes[i];
+            deg = row_degree(row_ptr, v, start);
+            at = indptr[i];
+        }
+        const bool draw = valid && deg > k;
+        uint32_t t = 0, m = 0;
+        if (draw && gl < k) {
+            m = (uint32_t)(deg - k + gl);
+            const uint32_t x = philox_word0((uint32_t)gl, (uint32_t)v, 0u, hop, key0, key1);
+            t = __umulhi(x, m + 1u);
+        }
+        uint32_t pick = t;
+        for (int j = 1; j < k; ++j) {
+            const uint32_t tj = (uint32_t)__shfl((int)t, j, G);
+            const uint64_t clash = (__ballot(gl < j && pick == tj) >> (r * G)) & ((1ull << j) - 1ull);
+            if (gl == j && clash != 0) pick = m;
+        }
+        const bool writes = draw ? gl < k : (valid && gl < deg);
+        if (writes) {
+            const int32_t id = col[start + (draw ? (int64_t)pick : (int64_t)gl)];
+            out[at + gl] = id;
+            note_first(first, tag, id, at + gl);
         }
     }
 }
@@ -427,16 +479,30 @@ void launch_sample_hop(const SampleHopArgs &a, hipStream_t s) {
     const uint32_t key0 = (uint32_t)(a.rng_seed & 0xffffffffu), key1 = (uint32_t)(a.rng_seed >> 32);
     const unsigned grid = grid_for(a.rows_bound, 256 / kWave, 16384);
     KernelTimer t("sample_hop", s);
-    const bool big = a.fanout > kWave;
-    if (a.offsets_i64) {
-        auto kern = big ? k_sample_big<int64_t> : k_sample_small<int64_t>;
-        hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, (const int64_t *)a.row_ptr, a.col,
-                           a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, (unsigned long long *)a.first_map, a.map_tag);
-    } else {
-        auto kern = big ? k_sample_big<int32_t> : k_sample_small<int32_t>;
-        hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, (const int32_t *)a.row_ptr, a.col,
-                           a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, (unsigned long long *)a.first_map, a.map_tag);
-    }
+    auto first = (unsigned long long *)a.first_map;
+    auto run = [&](auto row_ptr) {
+        using OffT = std::remove_const_t<std::remove_pointer_t<decltype(row_ptr)>>;
+        const int k = a.fanout;
+        auto group = [&](auto kern, int rows_per_wave) {
+            hipLaunchKernelGGL(kern, dim3(grid_for(a.rows_bound, (256 / kWave) * rows_per_wave, 16384)), dim3(256), 0,
+                               s, row_ptr, a.col, a.nodes, a.n_prev, a.indptr, a.nbrs, k, key0, key1, a.hop, first,
+                               a.map_tag);
+        };
+        if (k > 0 && k <= 8)
+            group(k_sample_group<OffT, 8>, 8);
+        else if (k > 0 && k <= 16)
+            group(k_sample_group<OffT, 16>, 4);
+        else if (k > 0 && k <= 32)
+            group(k_sample_group<OffT, 32>, 2);
+        else
+            hipLaunchKernelGGL(k > kWave ? k_sample_big<OffT> : k_sample_small<OffT>, dim3(grid), dim3(256), 0, s,
+                               row_ptr, a.col, a.nodes, a.n_prev, a.indptr, a.nbrs, k, key0, key1, a.hop, first,
+                               a.map_tag);
+    };
+    if (a.offsets_i64)
+        run((const int64_t *)a.row_ptr);
+    else
+        run((const int32_t *)a.row_ptr);
     GNNAV_HIP(hipGetLastError());
 }
 
