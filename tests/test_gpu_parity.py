@@ -121,6 +121,11 @@ SAMPLE_CASES = [
     ("random-3000-40000-5", "none", [5, 5]),
     ("chunglu-10k-d64", "batch", [5, 5]),
     ("chunglu-10k-d64", "batch", [25, 10, 5]),
+    # edges of the rows-per-wavefront selection (8, 16 and 32 lanes per row)
+    ("random-3000-40000-6", "rand", [8, 9]),
+    ("random-3000-40000-7", "rand", [16, 17, 2]),
+    ("random-3000-40000-8", "rand", [32, 33]),
+    ("star", "all", [8, 16]),
 ]
 
 
@@ -364,7 +369,9 @@ def test_aggregate_mean_parity(G, d, dtype):
         assert not host(out, dtype)[:, d:d + tail].any()
 
 
-# Small M runs the skinny kernel (fewer than 160 64x64 tiles); larger M the
+# Small M runs the skinny kernel (fewer than 160 64x64 tiles; 16 wavefronts
+# per 16x16 output while there are at most 512 of those, else 8: 8000 and
+# 2100 rows here); larger M the
 # ring kernel with 128x64 tiles (64x64 when N <= 64) and, from 512 128x128
 # tiles on, 128x128 tiles (bf16, and fp32 with d_in > 128) or the fp32
 # W-as-stored kernel (d_in <= 128); fp32 outputs 129-256 wide take 96x256
@@ -374,7 +381,8 @@ def test_aggregate_mean_parity(G, d, dtype):
 COMBINE_CASES = [(1, 3, 16), (63, 64, 41), (64, 100, 47), (65, 602, 256), (1000, 128, 64),
                  (777, 256, 256), (130, 5, 300), (20000, 602, 256), (12000, 64, 41),
                  (12001, 100, 100), (9000, 256, 256), (10240, 3, 47), (6000, 128, 260),
-                 (66000, 100, 256), (40000, 37, 130), (33000, 300, 256), (24001, 300, 250)]
+                 (66000, 100, 256), (40000, 37, 130), (33000, 300, 256), (24001, 300, 250),
+                 (8000, 256, 64), (2100, 128, 100)]
 
 
 @pytest.mark.parametrize("relu", [False, True])
