@@ -276,7 +276,10 @@ gnnav_status gnnav_aggregate_mean(const int32_t *indptr_dev, const int32_t *indi
 /* Eq. 1 Combine for SAGE: out = act(self * W[0:d_in] + agg * W[d_in:2*d_in])
  * for m rows, with W row-major [2*d_in, d_out] (device), self and agg
  * device [m x d_in] with strides ld_self, ld_agg.  act is ReLU when relu is
- * nonzero.  dt = F32: fp32 operands, fp32 MFMA, fp32 output.  dt = BF16:
+ * nonzero.  dt = F32: fp32 operands and output, fp32-accurate products: fp32
+ * MFMA for few rows, otherwise both operands cut into three bf16 parts on
+ * the bf16 matrix cores (six part products per fp32 product, accumulated in
+ * fp32; see gnnav_combine_kernel).  dt = BF16:
  * bf16 operands, fp32 accumulation, output bf16 (nearest-even) when
  * out_bf16 is nonzero, else fp32.  The concatenation [self | agg] is never
  * formed.  Errors: E_INVALID (null pointers with m > 0, d_in or d_out <= 0,
@@ -285,6 +288,16 @@ gnnav_status gnnav_combine(const void *self_dev, int64_t ld_self, const void *ag
                            int64_t ld_agg, int64_t m, int64_t d_in, const void *w_dev,
                            int64_t d_out, gnnav_dtype dt, int32_t relu, int32_t out_bf16,
                            void *out_dev, int64_t ld_out, void *stream);
+
+/* Which kernel a combine of m rows (the row count, or its bound when the
+ * count is read on the device) and d_out output columns runs, the one
+ * gnnav_combine, gnnav_sage_forward and gnnav_sage_train_step launch:
+ * GNNAV_COMBINE_SKINNY: few rows, fp32 or bf16 MFMA as the dtype;
+ * GNNAV_COMBINE_RING: bf16 MFMA; GNNAV_COMBINE_SPLIT: fp32 through the
+ * three-way bf16 split, six bf16 MFMA products per fp32 product.  Host only,
+ * no device work; -1 for dt other than F32/BF16 or sizes <= 0.           */
+enum { GNNAV_COMBINE_SKINNY = 0, GNNAV_COMBINE_RING = 1, GNNAV_COMBINE_SPLIT = 2 };
+int32_t gnnav_combine_kernel(int64_t m, int64_t d_out, gnnav_dtype dt);
 
 /* ---------------------------------------------------------- SAGE forward ---
  * Algorithm 1, its per-layer aggregate/combine loop (forward only): n_layers = L of the last

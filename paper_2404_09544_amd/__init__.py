@@ -39,7 +39,7 @@ EXPORTS = [
     "gnnav_cache_set_link_workgroups", "gnnav_cache_free", "gnnav_blocks_create", "gnnav_blocks_free",
     "gnnav_sample", "gnnav_sample_async", "gnnav_sample_biased", "gnnav_blocks_sync", "gnnav_blocks_device_sizes",
     "gnnav_blocks_hop", "gnnav_blocks_nodes", "gnnav_gather", "gnnav_gather_n", "gnnav_gather_n_after",
-    "gnnav_aggregate_mean", "gnnav_combine", "gnnav_sage_forward", "gnnav_sage_train_step",
+    "gnnav_aggregate_mean", "gnnav_combine", "gnnav_combine_kernel", "gnnav_sage_forward", "gnnav_sage_train_step",
     "gnnav_softmax_xent", "gnnav_aggregate_mean_backward", "gnnav_weight_grad", "gnnav_profile_start",
     "gnnav_profile_stop", "gnnav_profile_count", "gnnav_profile_get", "gnnav_profile_samples",
 ]
@@ -86,6 +86,7 @@ _sig = {
     "gnnav_gather": ([P, P, i64, P, i64, P, P], i32),
     "gnnav_aggregate_mean": ([P, P, i64, P, i64, i64, i32, P, i64, P], i32),
     "gnnav_combine": ([P, i64, P, i64, i64, i64, P, i64, i32, i32, i32, P, i64, P], i32),
+    "gnnav_combine_kernel": ([i64, i64, i32], i32),
     "gnnav_sage_forward": ([P, P, i64, P, P, i32, i32, P, i64, P], i32),
     "gnnav_sage_train_step": ([P, P, i64, P, P, i32, P, C.c_float, P, i64, P, P, P], i32),
     "gnnav_softmax_xent": ([P, i64, i64, i64, P, P, i64, P, P], i32),
@@ -377,6 +378,17 @@ def combine(self_x, agg, m: int, d_in: int, w, d_out: int, dtype: str, relu: boo
                               _dev_ptr(w), d_out, dtype_code(dtype), int(relu), int(out_bf16),
                               _dev_ptr(out), out.stride(0), _stream(stream)))
 
+
+
+COMBINE_KERNELS = {0: "skinny", 1: "ring", 2: "split"}
+
+
+def combine_kernel(m: int, d_out: int, dtype: str) -> str:
+    """gnnav_combine_kernel: which kernel a combine of m rows runs."""
+    k = _lib.gnnav_combine_kernel(int(m), int(d_out), dtype_code(dtype))
+    if k < 0:
+        raise GnnavError(1, "bad combine_kernel arguments")
+    return COMBINE_KERNELS[k]
 
 def sage_train_step(blocks: Blocks, x, weights, dims, labels, lr: float, logits, loss, grads=None,
                     stream=None):

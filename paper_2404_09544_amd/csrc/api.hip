@@ -883,6 +883,11 @@ extern "C" gnnav_status gnnav_aggregate_mean(const int32_t *indptr_dev, const in
     });
 }
 
+extern "C" int32_t gnnav_combine_kernel(int64_t m, int64_t d_out, gnnav_dtype dt) {
+    if ((dt != GNNAV_F32 && dt != GNNAV_BF16) || m <= 0 || d_out <= 0) return -1;
+    return combine_kernel_kind(m, d_out, dt == GNNAV_BF16);
+}
+
 extern "C" gnnav_status gnnav_combine(const void *self_dev, int64_t ld_self, const void *agg_dev, int64_t ld_agg,
                                       int64_t m, int64_t d_in, const void *w_dev, int64_t d_out, gnnav_dtype dt,
                                       int32_t relu, int32_t out_bf16, void *out_dev, int64_t ld_out,

@@ -242,6 +242,7 @@ void launch_aggregate_mean(const int32_t *indptr, const int32_t *indices, int64_
                            int64_t ld_out, hipStream_t s, const char *label = "aggregate_mean");
 
 // gemm.hip
+int combine_kernel_kind(int64_t m, int64_t d_out, bool bf16);   // a GNNAV_COMBINE_* value
 void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
                     const int32_t *m_dev,
                     int64_t d_in, const void *w, int64_t d_out, bool bf16, bool relu,

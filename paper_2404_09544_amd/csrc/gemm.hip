@@ -2,25 +2,19 @@
 // self * W[0:d_in] + agg * W[d_in:2*d_in] with two A-operand pointers, so
 // the concatenation is never stored.
 //
-// Matrix cores: fp32 uses v_mfma_f32_32x32x2_f32 in the ring kernel and
-// v_mfma_f32_16x16x4_f32 elsewhere (full fp32 products either way); bf16
-// uses v_mfma_f32_32x32x16_bf16 (ring) or v_mfma_f32_16x16x32_bf16 (skinny)
-// with fp32 accumulation.  On MI355X the 32x32 fp32 instruction sustains
-// the full matrix rate with one wavefront per SIMD, the 16x16 one about
-// three quarters of it.
+// Matrix cores: fp32 runs on the bf16 matrix cores through a three-way
+// bf16 split of both operands (k_combine_split, fp32-accurate; see there);
+// the backward product dX = dZ * W^T (launch_matmul_bt) uses
+// v_mfma_f32_32x32x2_f32 in the ring kernel; bf16 uses
+// v_mfma_f32_32x32x16_bf16 (ring) or v_mfma_f32_16x16x32_bf16 (skinny) with
+// fp32 accumulation; the skinny fp32 kernel v_mfma_f32_16x16x4_f32.
 //
-// Ring kernel (rows 16-byte aligned, the normal case; fp32 and bf16): a
-// 256-thread workgroup owns a BM x BN output tile as WM x (4 / WM)
-// wavefronts (2 x 2, or 1 x 4 for the 96 x 256 fp32 tile).  Both
+// Ring kernel (rows 16-byte aligned; fp32 and bf16): a 256-thread
+// workgroup owns a BM x BN output tile as WM x (4 / WM) wavefronts.  Both
 // operands travel as 16-byte k-chunks from global memory straight into LDS
 // (global_load_lds_dwordx4) through a ring of STAGES buffers, so no
 // registers hold staged data and the loads of later steps are in flight
-// while the current one is multiplied.
-//
-// W-as-stored kernel (fp32 with a short K over many rows): K is walked in
-// BK steps through two LDS buffers: the next step's global loads are issued
-// into registers before the current step's MFMAs and stored into the other
-// buffer afterwards, one barrier per step.
+// while the current one is multiplied.  The split kernel uses the same ring.
 //
 // Skinny kernel (few output rows, e.g. the last layer over the seeds): a
 // workgroup owns 16 x 16 outputs; its 8 or 16 wavefronts take interleaved
@@ -263,135 +257,218 @@ __global__ void __launch_bounds__(256) k_combine_ring(const T *__restrict__ A0, 
             }
 }
 
-// ---------------------------------------------- fp32 main, W as stored
-// Reads W row-major and stages A transposed (k-major) in LDS, one float per
-// lane and k step.  Measured faster than the ring kernel when there
-// are many row tiles over a short K (e.g. d_in = 100 over 10^5 rows).
-template <int BM, int BN, int WM, int WN, int BK, class OutT>
-__global__ void __launch_bounds__(256) k_combine_f32_wrow(const float *__restrict__ A0, int64_t lda0,
-                                                     const float *__restrict__ A1, int64_t lda1, int64_t M,
-                                                     const int32_t *__restrict__ m_dev, int64_t K,
-                                                     const float *__restrict__ W, int64_t N, int relu, int wvec,
-                                                     OutT *__restrict__ C, int64_t ldc) {
-    constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
-    constexpr int PA = BM + 16, PB = BN + 16;
-    constexpr int A_CH = BM * BK / 4;             // float4 chunks in an A step
-    constexpr int B_CH = BK * BN / 4;             // float4 chunks in a B step
-    constexpr int A_LD = (A_CH + 255) / 256, B_LD = (B_CH + 255) / 256;
-    static_assert(WM * WN == 4 && TM >= 1 && TN >= 1 && BK % 4 == 0, "tile shape");
-    __shared__ __attribute__((aligned(16))) float As[2][BK][PA];
-    __shared__ __attribute__((aligned(16))) float Bs[2][BK][PB];
+// ------------------------------------------ fp32 through split bf16
+// fp32 products on the bf16 matrix cores (the bf16x6 scheme of Henry, Tang
+// and Heinecke, "Leveraging the bfloat16 artificial intelligence datatype
+// for higher-precision computations", ARITH 2019): every fp32 operand x is
+// cut by truncation into three bf16 parts x = x1 + x2 + x3 + e with
+// |e| < 2^-23 |x| (x1 = the top 16 bits of x, x2 those of x - x1, x3 those
+// of x - x1 - x2; both differences are exact in fp32), and a product takes
+// the six part products a1 b1, a1 b2, a2 b1, a1 b3, a3 b1, a2 b2; the three
+// dropped ones are below 2^-30 |a b|.  Part products are exact in fp32 and
+// the matrix cores add them in fp32, so the result carries fp32 rounding,
+// not bf16 rounding.  One 32x32x16 bf16 MFMA takes half the cycles of the
+// eight 32x32x2 fp32 MFMAs covering the same 16 k, so six of them cost
+// three eighths of the plain fp32 path.
+//
+// Same ring as k_combine_ring: A (fp32) arrives in 16-byte k-chunks, 32 k
+// per step, swizzled chunk ^ (row & 7); B arrives already split, three
+// bf16 planes [3][N][ldb], 4 chunks (32 k) per plane and row per step,
+// stored [plane][row][chunk ^ ((row >> 1) & 3)] so that the fragment reads
+// of 8 consecutive rows hit distinct bank groups.  A fragment of sub-step
+// u (16 k) is the lane's 8 fp32 values, split in registers.
+__device__ __forceinline__ uint32_t hi16_pair(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
+
+// 8 fp32 values (two chunks) -> their three bf16 parts as MFMA fragments
+__device__ __forceinline__ void split3(const f32x4 &c0, const f32x4 &c1, bf16x8 &p1, bf16x8 &p2, bf16x8 &p3) {
+    uint32_t q1[4], q2[4], q3[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float x0 = e < 2 ? c0[2 * e] : c1[2 * e - 4], x1 = e < 2 ? c0[2 * e + 1] : c1[2 * e - 3];
+        const uint32_t u0 = __float_as_uint(x0), u1 = __float_as_uint(x1);
+        const float r0 = x0 - __uint_as_float(u0 & 0xffff0000u), r1 = x1 - __uint_as_float(u1 & 0xffff0000u);
+        const uint32_t v0 = __float_as_uint(r0), v1 = __float_as_uint(r1);
+        const float s0 = r0 - __uint_as_float(v0 & 0xffff0000u), s1 = r1 - __uint_as_float(v1 & 0xffff0000u);
+        q1[e] = hi16_pair(u0, u1);
+        q2[e] = hi16_pair(v0, v1);
+        q3[e] = hi16_pair(__float_as_uint(s0), __float_as_uint(s1));
+    }
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    p1 = __builtin_bit_cast(bf16x8, u32x4{q1[0], q1[1], q1[2], q1[3]});
+    p2 = __builtin_bit_cast(bf16x8, u32x4{q2[0], q2[1], q2[2], q2[3]});
+    p3 = __builtin_bit_cast(bf16x8, u32x4{q3[0], q3[1], q3[2], q3[3]});
+}
+
+template <class OutT, int BM, int BN, int WM>
+__global__ void __launch_bounds__(256) k_combine_split(const float *__restrict__ A0, int64_t lda0,
+                                                       const float *__restrict__ A1, int64_t lda1, int64_t M,
+                                                       const int32_t *__restrict__ m_dev, int64_t K,
+                                                       const uint16_t *__restrict__ B, int64_t ldb, int64_t pstride,
+                                                       int64_t bseg, int nseg, int64_t N, int relu,
+                                                       OutT *__restrict__ C, int64_t ldc) {
+    constexpr int STAGES = 2, CH = 8, BK = 32, WN = 4 / WM;
+    constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 32, TN = WTN / 32;
+    constexpr int A_CH = BM * CH, B_PL = BN * 4, B_CH = 3 * B_PL, ST = A_CH + B_CH;
+    constexpr int A_IN = A_CH / 256, B_IN = B_CH / 256, PER = A_IN + B_IN;
+    static_assert(WM * WN == 4 && TM * 32 == WTM && TN * 32 == WTN && A_CH % 256 == 0 && B_CH % 256 == 0 &&
+                      PER < 64, "tile shape");
+    __shared__ f32x4 S[STAGES * ST];
 
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    const int wm = wid / WN, wn = wid % WN, g = lane >> 4, l16 = lane & 15;
+    const int wm = wid / WN, wn = wid % WN, h = lane >> 5, lr = lane & 31;
     if (m_dev) M = *m_dev;
     int64_t tile_r, tile_c;
     tile_of((N + BN - 1) / BN, tile_r, tile_c);
     const int64_t m0 = tile_r * BM, n0 = tile_c * BN;
     if (m0 >= M) return;
 
-    f32x4 acc[TM][TN];
+    const float *pa[2][A_IN];
+    int ka[A_IN];
+#pragma unroll
+    for (int q = 0; q < A_IN; ++q) {
+        const int sl = (wid * A_IN + q) * 64 + lane, r = sl / CH;
+        const int64_t row = m0 + r < M ? m0 + r : M - 1;
+        pa[0][q] = A0 + row * lda0;
+        pa[1][q] = A1 + row * lda1;
+        ka[q] = 4 * ((sl % CH) ^ (r & 7));
+    }
+    const uint16_t *pb[B_IN];
+#pragma unroll
+    for (int q = 0; q < B_IN; ++q) {
+        const int sl = (wid * B_IN + q) * 64 + lane, p = sl / B_PL, rem = sl % B_PL, r = rem / 4;
+        const int64_t n = n0 + r < N ? n0 + r : N - 1;
+        pb[q] = B + p * pstride + n * ldb + 8 * ((rem % 4) ^ ((r >> 1) & 3));
+    }
+    const int64_t kt = (K + BK - 1) / BK, steps = nseg * kt;
+
+    f32x16 acc[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    const int64_t kt = (K + BK - 1) / BK;
-    const int64_t tiles = 2 * kt;
-    float4 ra[A_LD], rb[B_LD];
-
-    auto load = [&](int64_t t) {
-        const bool seg = t >= kt;
+    auto issue = [&](int64_t t) {
+        f32x4 *buf = S + (int)(t % STAGES) * ST;
+        const int seg = t >= kt;
         const int64_t k0 = (seg ? t - kt : t) * BK;
-        const float *A = seg ? A1 : A0;
-        const int64_t lda = seg ? lda1 : lda0;
-        const float *Wk = W + (seg ? K : 0) * N;
 #pragma unroll
-        for (int s = 0; s < A_LD; ++s) {
-            const int c = tid + 256 * s;
-            const int r = c / (BK / 4), kq = (c % (BK / 4)) * 4;
-            const int64_t row = m0 + r, k = k0 + kq;
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (c < A_CH && row < M) {
-                const float *p = A + row * lda + k;
-                if (k + 3 < K) {
-                    v = *(const float4 *)p;
-                } else {
-                    if (k < K) v.x = p[0];
-                    if (k + 1 < K) v.y = p[1];
-                    if (k + 2 < K) v.z = p[2];
-                }
-            }
-            ra[s] = v;
+        for (int q = 0; q < A_IN; ++q) {
+            const int64_t k = k0 + ka[q];
+            dma16(pa[seg][q] + (k < K ? k : 0), &buf[(wid * A_IN + q) * 64]);
         }
+        // B planes are zero-padded to a multiple of 32 k per segment
 #pragma unroll
-        for (int s = 0; s < B_LD; ++s) {
-            const int c = tid + 256 * s;
-            const int kr = c / (BN / 4), nq = (c % (BN / 4)) * 4;
-            const int64_t kk = k0 + kr, n = n0 + nq;
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (c < B_CH && kk < K) {
-                const float *q = Wk + kk * N + n;
-                if (wvec && n + 3 < N) {
-                    v = *(const float4 *)q;
-                } else {
-                    if (n < N) v.x = q[0];
-                    if (n + 1 < N) v.y = q[1];
-                    if (n + 2 < N) v.z = q[2];
-                    if (n + 3 < N) v.w = q[3];
-                }
-            }
-            rb[s] = v;
+        for (int q = 0; q < B_IN; ++q) dma16(pb[q] + seg * bseg + k0, &buf[A_CH + (wid * B_IN + q) * 64]);
+    };
+    auto fixup = [&](int64_t t) {
+        const int64_t k0 = (t >= kt ? t - kt : t) * BK;
+        if (k0 + BK <= K) return;
+        float *base = (float *)(S + (int)(t % STAGES) * ST);
+#pragma unroll
+        for (int q = 0; q < A_IN; ++q) {
+            const int64_t k = k0 + ka[q];
+            float *e = base + 4 * ((wid * A_IN + q) * 64 + lane);
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+                if (k + x >= K) e[x] = 0.f;
         }
     };
-    auto stash = [&](int buf) {
+    auto compute = [&](int64_t t) {
+        const f32x4 *buf = S + (int)(t % STAGES) * ST;
 #pragma unroll
-        for (int s = 0; s < A_LD; ++s) {
-            const int c = tid + 256 * s;
-            if (c < A_CH) {
-                const int r = c / (BK / 4), kq = (c % (BK / 4)) * 4;
-                As[buf][kq + 0][r] = ra[s].x;
-                As[buf][kq + 1][r] = ra[s].y;
-                As[buf][kq + 2][r] = ra[s].z;
-                As[buf][kq + 3][r] = ra[s].w;
+        for (int u = 0; u < 2; ++u) {
+            bf16x8 a1[TM], a2[TM], a3[TM], b1[TN], b2[TN], b3[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int r = wm * WTM + i * 32 + lr;
+                split3(buf[r * CH + ((4 * u + 2 * h) ^ (r & 7))], buf[r * CH + ((4 * u + 2 * h + 1) ^ (r & 7))],
+                       a1[i], a2[i], a3[i]);
             }
-        }
 #pragma unroll
-        for (int s = 0; s < B_LD; ++s) {
-            const int c = tid + 256 * s;
-            if (c < B_CH) *(float4 *)&Bs[buf][c / (BN / 4)][(c % (BN / 4)) * 4] = rb[s];
-        }
-    };
-
-    auto compute = [&](int buf) {
-#pragma unroll
-        for (int ks = 0; ks < BK / 4; ++ks) {
-            float a[TM], b[TN];
-#pragma unroll
-            for (int i = 0; i < TM; ++i) a[i] = As[buf][ks * 4 + g][wm * WTM + i * 16 + l16];
-#pragma unroll
-            for (int j = 0; j < TN; ++j) b[j] = Bs[buf][ks * 4 + g][wn * WTN + j * 16 + l16];
+            for (int j = 0; j < TN; ++j) {
+                const int r = wn * WTN + j * 32 + lr;
+                const int c = (2 * u + h) ^ ((r >> 1) & 3);
+                b1[j] = __builtin_bit_cast(bf16x8, buf[A_CH + r * 4 + c]);
+                b2[j] = __builtin_bit_cast(bf16x8, buf[A_CH + B_PL + r * 4 + c]);
+                b3[j] = __builtin_bit_cast(bf16x8, buf[A_CH + 2 * B_PL + r * 4 + c]);
+            }
+            // smallest part products first
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+                for (int j = 0; j < TN; ++j) {
+                    f32x16 c = acc[i][j];
+                    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[i], b2[j], c, 0, 0, 0);
+                    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3[i], b1[j], c, 0, 0, 0);
+                    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b3[j], c, 0, 0, 0);
+                    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[i], b1[j], c, 0, 0, 0);
+                    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b2[j], c, 0, 0, 0);
+                    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b1[j], c, 0, 0, 0);
+                    acc[i][j] = c;
+                }
         }
     };
 
-    load(0);
-    stash(0);
-    __syncthreads();
-    for (int64_t t = 0; t < tiles; ++t) {
-        const int buf = (int)(t & 1);
-        if (t + 1 < tiles) load(t + 1);
-        compute(buf);
-        if (t + 1 < tiles) stash(buf ^ 1);
-        __syncthreads();
+#pragma unroll
+    for (int p = 0; p < STAGES - 1; ++p)
+        if (p < steps) issue(p);
+    for (int64_t t = 0; t < steps; ++t) {
+        wait_vm<0>();
+        fixup(t);
+        lds_barrier();   // stage t visible to all; everyone is done reading stage t - 1
+        if (t + STAGES - 1 < steps) issue(t + STAGES - 1);
+        compute(t);
     }
-    write_tile<TM, TN, OutT>(acc, m0 + wm * WTM, n0 + wn * WTN, M, N, relu, C, ldc, g, l16);
+
+    const int64_t r0 = m0 + wm * WTM, c0 = n0 + wn * WTN;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int64_t row = r0 + i * 32 + 8 * (r / 4) + 4 * h + (r % 4), col = c0 + j * 32 + lr;
+                if (row < M && col < N) {
+                    float v = acc[i][j][r];
+                    if (relu) v = fmaxf(v, 0.f);
+                    store_out<OutT>(C + row * ldc + col, v);
+                }
+            }
 }
 
+// W [2K][N] fp32 -> its three bf16 parts, transposed: WS[p][n][kk] over
+// kk in [0, 2 KP) with each K-long segment zero-padded to KP (a multiple of
+// 32), the layout k_combine_split reads.  32 x 32 tiles through LDS.
+__global__ void __launch_bounds__(256) k_split_transpose(const float *__restrict__ W, int64_t K, int64_t N, int64_t KP,
+                                                         uint16_t *__restrict__ WS) {
+    __shared__ float tile[32][33];
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+    const int64_t n0 = (int64_t)blockIdx.x * 32, kk0 = (int64_t)blockIdx.y * 32;
+    const int64_t seg = kk0 / KP, k0 = kk0 - seg * KP;
+#pragma unroll
+    for (int r = ty; r < 32; r += 8) {
+        const int64_t k = k0 + r, n = n0 + tx;
+        tile[r][tx] = (k < K && n < N) ? W[(seg * K + k) * N + n] : 0.f;
+    }
+    __syncthreads();
+    const int64_t plane = N * 2 * KP;
+#pragma unroll
+    for (int r = ty; r < 32; r += 8) {
+        const int64_t n = n0 + r;
+        if (n >= N) continue;
+        const float x = tile[tx][r];
+        const uint32_t u = __float_as_uint(x);
+        const float rx = x - __uint_as_float(u & 0xffff0000u);
+        const uint32_t v = __float_as_uint(rx);
+        const float sx = rx - __uint_as_float(v & 0xffff0000u);
+        uint16_t *o = WS + n * 2 * KP + kk0 + tx;
+        o[0] = (uint16_t)(u >> 16);
+        o[plane] = (uint16_t)(v >> 16);
+        o[2 * plane] = (uint16_t)(__float_as_uint(sx) >> 16);
+    }
+}
 
 template <bool BF16, int TN>
 struct Skinny;
@@ -555,8 +632,6 @@ struct SharedWorkspace {
 };
 SharedWorkspace g_wt;
 
-enum class Fp32Kernel { kRing, kWrow };
-
 template <int BM, int BN, class T, class OutT, int WM = 2>
 void launch_ring(const T *a0, int64_t lda0, const T *a1, int64_t lda1, int64_t m, const int32_t *m_dev, int64_t k,
                  const T *b, int64_t ldb, int64_t bseg, int nseg, int64_t n, bool relu, OutT *out, int64_t ld_out,
@@ -570,49 +645,44 @@ void launch_ring(const T *a0, int64_t lda0, const T *a1, int64_t lda1, int64_t m
 
 // fp32: KIND picks the ring kernel (weights transposed and padded first) or
 // the W-as-stored kernel.  bf16: the ring kernel.
-template <int BM, int BN, Fp32Kernel KIND, int WM = 2>
+// fp32: the weights are split into three bf16 parts and transposed, then
+// k_combine_split runs; bf16: the weights are transposed and padded, then
+// the ring kernel runs.
+template <int BM, int BN>
 static void launch_main(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
                         const int32_t *m_dev, int64_t k, const void *w, int64_t n, bool bf16, bool relu,
                         bool out_bf16, void *out, int64_t ld_out, hipStream_t s, const char *label) {
-    const int64_t nrow = (m + BM - 1) / BM, ncol = (n + BN - 1) / BN;
-    const dim3 grid((unsigned)(((nrow + 7) / 8) * 8 * ncol));
-    if constexpr (KIND == Fp32Kernel::kWrow) {
-        if (!bf16) {
-            const int wvec = (((uintptr_t)w & 15u) == 0) && n % 4 == 0;
-            KernelTimer tk(label, s);
-            hipLaunchKernelGGL((k_combine_f32_wrow<BM, BN, 2, 2, 16, float>), grid, dim3(256), 0, s,
-                               (const float *)self, ld_self, (const float *)agg, ld_agg, m, m_dev, k,
-                               (const float *)w, n, (int)relu, wvec, (float *)out, ld_out);
-            return;
-        }
-    }
     std::lock_guard<std::mutex> lk(g_wt.mu);
     if (!g_wt.last_use) GNNAV_HIP(hipEventCreateWithFlags(&g_wt.last_use, hipEventDisableTiming));
     GNNAV_HIP(hipStreamWaitEvent(s, g_wt.last_use, 0));
-    const int64_t elt = bf16 ? 2 : 4, kp = bf16 ? (k + 63) / 64 * 64 : (k + 31) / 32 * 32;
-    g_wt.buf.ensure((size_t)(2 * kp * n * elt), s);
+    const int64_t kp = bf16 ? (k + 63) / 64 * 64 : (k + 31) / 32 * 32;
+    g_wt.buf.ensure((size_t)(2 * kp * n * (bf16 ? 2 : 6)), s);
     const dim3 tgrid((unsigned)((n + 31) / 32), (unsigned)(2 * kp / 32));
     {
         KernelTimer tt("weights_transpose", s);
         if (!bf16)
-            hipLaunchKernelGGL(k_transpose_pad<float>, tgrid, dim3(256), 0, s, (const float *)w, k, n, kp,
-                               g_wt.buf.as<float>());
+            hipLaunchKernelGGL(k_split_transpose, tgrid, dim3(256), 0, s, (const float *)w, k, n, kp,
+                               g_wt.buf.as<uint16_t>());
         else
             hipLaunchKernelGGL(k_transpose_pad<uint16_t>, tgrid, dim3(256), 0, s, (const uint16_t *)w, k, n, kp,
                                g_wt.buf.as<uint16_t>());
     }
     KernelTimer tk(label, s);
-    if (!bf16)
-        launch_ring<BM, BN, float, float, WM>((const float *)self, ld_self, (const float *)agg, ld_agg, m, m_dev, k,
-                                              g_wt.buf.as<float>(), 2 * kp, kp, 2, n, relu, (float *)out, ld_out, s);
-    else if (out_bf16)
-        launch_ring<BM, BN, uint16_t, uint16_t, WM>((const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m,
-                                                    m_dev, k, g_wt.buf.as<uint16_t>(), 2 * kp, kp, 2, n, relu,
-                                                    (uint16_t *)out, ld_out, s);
-    else
-        launch_ring<BM, BN, uint16_t, float, WM>((const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m,
-                                                 m_dev, k, g_wt.buf.as<uint16_t>(), 2 * kp, kp, 2, n, relu,
-                                                 (float *)out, ld_out, s);
+    if (!bf16) {
+        const int64_t nrow = (m + BM - 1) / BM, ncol = (n + BN - 1) / BN;
+        const dim3 grid((unsigned)(((nrow + 7) / 8) * 8 * ncol));
+        hipLaunchKernelGGL((k_combine_split<float, BM, BN, 2>), grid, dim3(256), 0, s, (const float *)self, ld_self,
+                           (const float *)agg, ld_agg, m, m_dev, k, g_wt.buf.as<uint16_t>(), 2 * kp, n * 2 * kp, kp, 2,
+                           n, (int)relu, (float *)out, ld_out);
+    } else if (out_bf16) {
+        launch_ring<BM, BN, uint16_t, uint16_t>((const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m,
+                                                m_dev, k, g_wt.buf.as<uint16_t>(), 2 * kp, kp, 2, n, relu,
+                                                (uint16_t *)out, ld_out, s);
+    } else {
+        launch_ring<BM, BN, uint16_t, float>((const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m,
+                                             m_dev, k, g_wt.buf.as<uint16_t>(), 2 * kp, kp, 2, n, relu,
+                                             (float *)out, ld_out, s);
+    }
     GNNAV_HIP(hipEventRecord(g_wt.last_use, s));
 }
 
@@ -633,32 +703,29 @@ static int64_t busiest_cu_outputs(int64_t m, int64_t n, int64_t bm, int64_t bn) 
     return (tiles + 255) / 256 * bm * bn;
 }
 
-// Tile shapes measured on MI355X.  fp32: the ring kernel with 128 x 64 tiles
-// (64 x 64 when the output is at most 64 wide, 128 x 128 once there are
-// enough of those to give every compute unit two); the W-as-stored kernel
-// when such a large output has a short K (at most 128 per segment), where
-// it measured faster (e.g. 10^5 rows of d_in = 100).  An output 129-256
-// wide takes 96 x 256 tiles (one column of tiles, A read once, four
-// 96 x 64 wavefront tiles) when that loads the busiest compute unit no more
-// than the default: 20902 x 1204 x 256 runs in 147 us instead of 154 us,
-// while at 15000 rows (157 tiles for 256 units) it would lose a third.
-// bf16: the ring kernel with 128 x 64 tiles (64 x 64 for outputs at most 64
-// wide), 128 x 128 from that same point on.
-static GemmChoice choose_main(int64_t m, int64_t d_in, int64_t d_out, bool bf16) {
-    const bool big = d_out > 64 && ((m + 127) / 128) * ((d_out + 127) / 128) >= 512;
+// Tile shapes measured on MI355X.  fp32 (split kernel): 128 x 128 or
+// 64 x 64, whichever loads the busiest compute unit less, counting a 64 x 64
+// output as 1/0.7 of its size (its per-output rate measured ~0.7 of the
+// larger tile's): e.g. 20902 x 1204 x 256 takes 128 x 128 (106 us), 6915 x
+// 256 x 256 and 40000 x 74 x 130 take 64 x 64.  bf16 (ring kernel): 128 x 64
+// tiles (64 x 64 for outputs at most 64 wide), 128 x 128 once there are
+// enough of those to give every compute unit two.
+static GemmChoice choose_main(int64_t m, int64_t d_out, bool bf16) {
     if (bf16) {
-        if (big) return {128, 128, launch_main<128, 128, Fp32Kernel::kRing>};
-        if (d_out <= 64) return {64, 64, launch_main<64, 64, Fp32Kernel::kRing>};
-        return {128, 64, launch_main<128, 64, Fp32Kernel::kRing>};
+        const bool big = d_out > 64 && ((m + 127) / 128) * ((d_out + 127) / 128) >= 512;
+        if (big) return {128, 128, launch_main<128, 128>};
+        if (d_out <= 64) return {64, 64, launch_main<64, 64>};
+        return {128, 64, launch_main<128, 64>};
     }
-    if (big && d_in <= 128) return {128, 128, launch_main<128, 128, Fp32Kernel::kWrow>};
-    GemmChoice ch = big ? GemmChoice{128, 128, launch_main<128, 128, Fp32Kernel::kRing>}
-                        : d_out <= 64 ? GemmChoice{64, 64, launch_main<64, 64, Fp32Kernel::kRing>}
-                                      : GemmChoice{128, 64, launch_main<128, 64, Fp32Kernel::kRing>};
-    if (d_out > 128 && d_out <= 256 &&
-        busiest_cu_outputs(m, d_out, 96, 256) <= busiest_cu_outputs(m, d_out, ch.bm, ch.bn))
-        ch = {96, 256, launch_main<96, 256, Fp32Kernel::kRing, 1>};
-    return ch;
+    if (d_out > 64 && 7 * busiest_cu_outputs(m, d_out, 128, 128) <= 10 * busiest_cu_outputs(m, d_out, 64, 64))
+        return {128, 128, launch_main<128, 128>};
+    return {64, 64, launch_main<64, 64>};
+}
+
+int combine_kernel_kind(int64_t m, int64_t d_out, bool bf16) {
+    const int64_t tiles64 = ((m + 63) / 64) * ((d_out + 63) / 64);
+    if (tiles64 < kSkinnyTiles) return GNNAV_COMBINE_SKINNY;
+    return bf16 ? GNNAV_COMBINE_RING : GNNAV_COMBINE_SPLIT;
 }
 
 void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t ld_agg, int64_t m,
@@ -666,9 +733,7 @@ void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t 
                     int64_t ld_out, hipStream_t s, const char *label) {
     if (m <= 0) return;
     if (!bf16 && out_bf16) fail(GNNAV_E_INVALID, "bf16 output needs bf16 operands");
-    const GemmChoice ch = choose_main(m, d_in, d_out, bf16);
-    const int64_t tiles64 = ((m + 63) / 64) * ((d_out + 63) / 64);
-    if (tiles64 < kSkinnyTiles) {
+    if (combine_kernel_kind(m, d_out, bf16) == GNNAV_COMBINE_SKINNY) {
         // one 16 x 16 output fragment per workgroup; 16 wavefronts split K
         // while that leaves at most 512 workgroups, 8 beyond (measured)
         const dim3 grid((unsigned)((m + 15) / 16), (unsigned)((d_out + 15) / 16));
@@ -693,6 +758,7 @@ void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t 
         else
             run(std::integral_constant<int, 8>{});
     } else {
+        const GemmChoice ch = choose_main(m, d_out, bf16);
         ch.fn(self, ld_self, agg, ld_agg, m, m_dev, d_in, w, d_out, bf16, relu, out_bf16, out, ld_out, s, label);
     }
     GNNAV_HIP(hipGetLastError());

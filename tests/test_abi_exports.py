@@ -36,3 +36,21 @@ def test_binding_covers_every_export():
     assert sorted(g.EXPORTS) == declared_functions()
     assert g.abi_version() == 1
     assert g._lib.gnnav_last_error() == b""
+
+
+def test_combine_kernel_choice():
+    """Host-only query of the combine kernel a launch takes: few rows run the
+    skinny kernel, larger fp32 the split-bf16 kernel, larger bf16 the ring."""
+    import paper_2404_09544_amd as g
+    assert g.combine_kernel(1024, 41, "f32") == "skinny"      # 16 64x64 tiles
+    assert g.combine_kernel(10176, 64, "f32") == "skinny"     # 159 64x64 tiles
+    assert g.combine_kernel(10177, 47, "f32") == "split"      # 160 tiles
+    assert g.combine_kernel(20902, 256, "f32") == "split"
+    assert g.combine_kernel(106857, 256, "bf16") == "ring"
+    assert g.combine_kernel(100, 3000, "bf16") == "skinny"
+    for bad in [(0, 5, "f32"), (5, 0, "f32")]:
+        try:
+            g.combine_kernel(*bad)
+        except g.GnnavError:
+            continue
+        raise AssertionError(f"{bad} accepted")

@@ -371,13 +371,10 @@ def test_aggregate_mean_parity(G, d, dtype):
 
 # Small M runs the skinny kernel (fewer than 160 64x64 tiles; 16 wavefronts
 # per 16x16 output while there are at most 512 of those, else 8: 8000 and
-# 2100 rows here); larger M the
-# ring kernel with 128x64 tiles (64x64 when N <= 64) and, from 512 128x128
-# tiles on, 128x128 tiles (bf16, and fp32 with d_in > 128) or the fp32
-# W-as-stored kernel (d_in <= 128); fp32 outputs 129-256 wide take 96x256
-# tiles when those load the busiest compute unit no more (20000 and 24001
-# rows here, the latter with ragged M and N).  K tails: d_in not a multiple
-# of the 32 (fp32) or 64 (bf16) k step.
+# 2100 rows here).  Larger M: fp32 runs the split-bf16 kernel on 128x128 or
+# 64x64 tiles (both taken here, e.g. 20000 x 602 x 256 and 40000 x 37 x
+# 130), bf16 the ring kernel on 128x64 / 64x64 / 128x128 tiles.  K tails:
+# d_in not a multiple of the 32 (fp32) or 64 (bf16) k step; ragged M and N.
 COMBINE_CASES = [(1, 3, 16), (63, 64, 41), (64, 100, 47), (65, 602, 256), (1000, 128, 64),
                  (777, 256, 256), (130, 5, 300), (20000, 602, 256), (12000, 64, 41),
                  (12001, 100, 100), (9000, 256, 256), (10240, 3, 47), (6000, 128, 260),
