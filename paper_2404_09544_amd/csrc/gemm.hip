@@ -35,13 +35,13 @@
 #include <mutex>
 #include <type_traits>
 
+#include "bf16split.hpp"
 #include "common.hpp"
 #include "dma.hpp"
 
 namespace gnnav {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 template <class OutT>
 __device__ __forceinline__ void store_out(OutT *c, float v);
@@ -258,18 +258,11 @@ __global__ void __launch_bounds__(256) k_combine_ring(const T *__restrict__ A0, 
 }
 
 // ------------------------------------------ fp32 through split bf16
-// fp32 products on the bf16 matrix cores (the bf16x6 scheme of Henry, Tang
-// and Heinecke, "Leveraging the bfloat16 artificial intelligence datatype
-// for higher-precision computations", ARITH 2019): every fp32 operand x is
-// cut by truncation into three bf16 parts x = x1 + x2 + x3 + e with
-// |e| < 2^-23 |x| (x1 = the top 16 bits of x, x2 those of x - x1, x3 those
-// of x - x1 - x2; both differences are exact in fp32), and a product takes
-// the six part products a1 b1, a1 b2, a2 b1, a1 b3, a3 b1, a2 b2; the three
-// dropped ones are below 2^-30 |a b|.  Part products are exact in fp32 and
-// the matrix cores add them in fp32, so the result carries fp32 rounding,
-// not bf16 rounding.  One 32x32x16 bf16 MFMA takes half the cycles of the
-// eight 32x32x2 fp32 MFMAs covering the same 16 k, so six of them cost
-// three eighths of the plain fp32 path.
+// fp32 products on the bf16 matrix cores (bf16split.hpp): both operands as
+// three bf16 parts, six part products per fp32 product accumulated in fp32,
+// so the result carries fp32 rounding, not bf16 rounding.  One 32x32x16 bf16
+// MFMA takes half the cycles of the eight 32x32x2 fp32 MFMAs covering the
+// same 16 k, so six of them cost three eighths of the plain fp32 path.
 //
 // Same ring as k_combine_ring: A (fp32) arrives in 16-byte k-chunks, 32 k
 // per step, swizzled chunk ^ (row & 7); B arrives already split, three
@@ -277,41 +270,20 @@ __global__ void __launch_bounds__(256) k_combine_ring(const T *__restrict__ A0, 
 // stored [plane][row][chunk ^ ((row >> 1) & 3)] so that the fragment reads
 // of 8 consecutive rows hit distinct bank groups.  A fragment of sub-step
 // u (16 k) is the lane's 8 fp32 values, split in registers.
-__device__ __forceinline__ uint32_t hi16_pair(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
-
-// 8 fp32 values (two chunks) -> their three bf16 parts as MFMA fragments
-__device__ __forceinline__ void split3(const f32x4 &c0, const f32x4 &c1, bf16x8 &p1, bf16x8 &p2, bf16x8 &p3) {
-    uint32_t q1[4], q2[4], q3[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const float x0 = e < 2 ? c0[2 * e] : c1[2 * e - 4], x1 = e < 2 ? c0[2 * e + 1] : c1[2 * e - 3];
-        const uint32_t u0 = __float_as_uint(x0), u1 = __float_as_uint(x1);
-        const float r0 = x0 - __uint_as_float(u0 & 0xffff0000u), r1 = x1 - __uint_as_float(u1 & 0xffff0000u);
-        const uint32_t v0 = __float_as_uint(r0), v1 = __float_as_uint(r1);
-        const float s0 = r0 - __uint_as_float(v0 & 0xffff0000u), s1 = r1 - __uint_as_float(v1 & 0xffff0000u);
-        q1[e] = hi16_pair(u0, u1);
-        q2[e] = hi16_pair(v0, v1);
-        q3[e] = hi16_pair(__float_as_uint(s0), __float_as_uint(s1));
-    }
-    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-    p1 = __builtin_bit_cast(bf16x8, u32x4{q1[0], q1[1], q1[2], q1[3]});
-    p2 = __builtin_bit_cast(bf16x8, u32x4{q2[0], q2[1], q2[2], q2[3]});
-    p3 = __builtin_bit_cast(bf16x8, u32x4{q3[0], q3[1], q3[2], q3[3]});
-}
-
-template <class OutT, int BM, int BN, int WM>
+template <class OutT, int BM, int BN, int WM, int STAGES = 2>
 __global__ void __launch_bounds__(256) k_combine_split(const float *__restrict__ A0, int64_t lda0,
                                                        const float *__restrict__ A1, int64_t lda1, int64_t M,
                                                        const int32_t *__restrict__ m_dev, int64_t K,
                                                        const uint16_t *__restrict__ B, int64_t ldb, int64_t pstride,
                                                        int64_t bseg, int nseg, int64_t N, int relu,
                                                        OutT *__restrict__ C, int64_t ldc) {
-    constexpr int STAGES = 2, CH = 8, BK = 32, WN = 4 / WM;
+    constexpr int CH = 8, BK = 32, WN = 4 / WM;
     constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 32, TN = WTN / 32;
     constexpr int A_CH = BM * CH, B_PL = BN * 4, B_CH = 3 * B_PL, ST = A_CH + B_CH;
     constexpr int A_IN = A_CH / 256, B_IN = B_CH / 256, PER = A_IN + B_IN;
-    static_assert(WM * WN == 4 && TM * 32 == WTM && TN * 32 == WTN && A_CH % 256 == 0 && B_CH % 256 == 0 &&
-                      PER < 64, "tile shape");
+    static_assert(WM * WN == 4 && TM * 32 == WTM && TN * 32 == WTN && A_CH % 256 == 0 && B_CH % 256 == 0,
+                  "tile shape");
+    static_assert(STAGES >= 2 && STAGES <= 3 && (STAGES - 1) * PER < 64, "ring depth");
     __shared__ f32x4 S[STAGES * ST];
 
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
@@ -383,8 +355,10 @@ __global__ void __launch_bounds__(256) k_combine_split(const float *__restrict__
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
                 const int r = wm * WTM + i * 32 + lr;
-                split3(buf[r * CH + ((4 * u + 2 * h) ^ (r & 7))], buf[r * CH + ((4 * u + 2 * h + 1) ^ (r & 7))],
-                       a1[i], a2[i], a3[i]);
+                const f32x4 c0 = buf[r * CH + ((4 * u + 2 * h) ^ (r & 7))];
+                const f32x4 c1 = buf[r * CH + ((4 * u + 2 * h + 1) ^ (r & 7))];
+                const float x[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
+                split3(x, a1[i], a2[i], a3[i]);
             }
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
@@ -394,28 +368,22 @@ __global__ void __launch_bounds__(256) k_combine_split(const float *__restrict__
                 b2[j] = __builtin_bit_cast(bf16x8, buf[A_CH + B_PL + r * 4 + c]);
                 b3[j] = __builtin_bit_cast(bf16x8, buf[A_CH + 2 * B_PL + r * 4 + c]);
             }
-            // smallest part products first
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < TN; ++j) {
-                    f32x16 c = acc[i][j];
-                    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[i], b2[j], c, 0, 0, 0);
-                    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3[i], b1[j], c, 0, 0, 0);
-                    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b3[j], c, 0, 0, 0);
-                    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[i], b1[j], c, 0, 0, 0);
-                    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b2[j], c, 0, 0, 0);
-                    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b1[j], c, 0, 0, 0);
-                    acc[i][j] = c;
-                }
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = mfma_split6(a1[i], a2[i], a3[i], b1[j], b2[j], b3[j], acc[i][j]);
         }
     };
 
 #pragma unroll
     for (int p = 0; p < STAGES - 1; ++p)
         if (p < steps) issue(p);
+    // every wavefront issues exactly PER DMAs per step, so "stage t landed"
+    // is "at most PER * (steps issued after t) pending"
     for (int64_t t = 0; t < steps; ++t) {
-        wait_vm<0>();
+        if (STAGES == 3 && t + 1 < steps) wait_vm<PER>();
+        else wait_vm<0>();
         fixup(t);
         lds_barrier();   // stage t visible to all; everyone is done reading stage t - 1
         if (t + STAGES - 1 < steps) issue(t + STAGES - 1);
@@ -458,15 +426,12 @@ __global__ void __launch_bounds__(256) k_split_transpose(const float *__restrict
     for (int r = ty; r < 32; r += 8) {
         const int64_t n = n0 + r;
         if (n >= N) continue;
-        const float x = tile[tx][r];
-        const uint32_t u = __float_as_uint(x);
-        const float rx = x - __uint_as_float(u & 0xffff0000u);
-        const uint32_t v = __float_as_uint(rx);
-        const float sx = rx - __uint_as_float(v & 0xffff0000u);
+        uint16_t p1, p2, p3;
+        split3_bits(tile[tx][r], p1, p2, p3);
         uint16_t *o = WS + n * 2 * KP + kk0 + tx;
-        o[0] = (uint16_t)(u >> 16);
-        o[plane] = (uint16_t)(v >> 16);
-        o[2 * plane] = (uint16_t)(__float_as_uint(sx) >> 16);
+        o[0] = p1;
+        o[plane] = p2;
+        o[2 * plane] = p3;
     }
 }
 

@@ -20,6 +20,7 @@
 #include <algorithm>
 
 #include "common.hpp"
+#include "bf16split.hpp"
 #include "dma.hpp"
 #include "scan.hpp"
 
@@ -357,32 +358,35 @@ void launch_aggregate_t(const CscWorkspace &csc, const int32_t *indptr, int64_t 
 
 // --------------------------------------------------------- weight gradient
 // Partial tile of dW[seg * d_in + a][o] = sum over the rows m of this split
-// of X_seg[m][a] * G[m][o] (rows 16-byte aligned), with both operands moved
-// row by row (k = row m)
+// of X_seg[m][a] * G[m][o] (rows 16-byte aligned), on the bf16 matrix cores
+// through the three-way bf16 split of both operands (bf16split.hpp), so the
+// sums carry fp32 rounding.  Both operands move row by row (k = row m)
 // straight from global memory into LDS by global_load_lds_dwordx4 through a
-// two-stage ring of BK-row steps, and 32x32x2 MFMAs.  LDS holds Xs[m][a] and
-// Gs[m][o] as stored.  A wavefront owns (32 VA) x (32 VB) outputs as VA x VB
-// MFMA blocks whose rows and columns are interleaved: block (i, j) holds
-// a = base + VA r + i and o = base + VB c + j for fragment row r, column c.
-// A lane then finds all VA of its A values (and all VB of its B values) for
-// one k side by side in LDS, one 4-, 8- or 16-byte read each: two LDS reads
-// feed VA x VB MFMAs (four for 128 x 128 tiles).
-// Rows past the split's end load a valid row; the lanes that loaded G chunks
-// for them zero those in LDS before the barrier, so they add nothing.
-// Columns past d_in or d_out only reach outputs that are not stored.
-template <int BA, int BO, int BK>
-__global__ void __launch_bounds__(256) k_wgrad_ring(const float *__restrict__ X0, int64_t ldx0,
-                                                    const float *__restrict__ X1, int64_t ldx1, int64_t M,
-                                                    const int32_t *__restrict__ m_dev, int64_t d_in,
-                                                    const float *__restrict__ Gm, int64_t ldg, int64_t d_out,
-                                                    int64_t splits, float *__restrict__ part) {
+// two-stage ring of 32-row steps; LDS holds Xs[m][a] and Gs[m][o] as
+// stored.  A wavefront owns (32 VA) x (32 VB) outputs as VA x VB MFMA blocks
+// whose rows and columns are interleaved: block (i, j) holds
+// a = base + VA r + i and o = base + VB c + j for fragment row r, column c,
+// so a lane finds all VA of its X values (and all VB of its G values) for
+// one row side by side in LDS, one 4-, 8- or 16-byte read each.  Per 16-row
+// sub-step each lane gathers its 8 consecutive rows (k), splits them in
+// registers and issues six 32x32x16 bf16 MFMAs per block.  Rows past the
+// split's end load a valid row; the lanes that loaded G chunks for them
+// zero those in LDS before the barrier, so they add nothing.  Columns past
+// d_in or d_out only reach outputs that are not stored.
+template <int BA, int BO>
+__global__ void __launch_bounds__(256) k_wgrad_split(const float *__restrict__ X0, int64_t ldx0,
+                                                     const float *__restrict__ X1, int64_t ldx1, int64_t M,
+                                                     const int32_t *__restrict__ m_dev, int64_t d_in,
+                                                     const float *__restrict__ Gm, int64_t ldg, int64_t d_out,
+                                                     int64_t splits, float *__restrict__ part) {
     typedef float f32x16 __attribute__((ext_vector_type(16)));
-    constexpr int VA = BA / 64, VB = BO / 64;                       // MFMA blocks per wavefront, each way
-    constexpr int XC = BA / 4, GC = BO / 4;                         // 16-byte chunks per LDS row
+    constexpr int BK = 32;
+    constexpr int VA = BA / 64, VB = BO / 64;
+    constexpr int XC = BA / 4, GC = BO / 4;
     constexpr int X_CH = BK * XC, G_CH = BK * GC, ST = X_CH + G_CH;
-    constexpr int X_IN = X_CH / 256, G_IN = G_CH / 256;             // DMAs per wavefront and step
+    constexpr int X_IN = X_CH / 256, G_IN = G_CH / 256;
     static_assert((VA == 1 || VA == 2 || VA == 4) && (VB == 1 || VB == 2 || VB == 4), "tile");
-    static_assert(X_CH % 256 == 0 && G_CH % 256 == 0 && BK % 2 == 0, "whole wave instructions");
+    static_assert(X_CH % 256 == 0 && G_CH % 256 == 0, "whole wave instructions");
     __shared__ f32x4 S[2 * ST];
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const int wa = wid >> 1, wo = wid & 1, h = lane >> 5, lr = lane & 31;
@@ -405,7 +409,6 @@ __global__ void __launch_bounds__(256) k_wgrad_ring(const float *__restrict__ X0
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    // DMA slot p of a step holds chunk (row p / C, column 4 (p % C)) of its block
     auto issue = [&](int64_t t) {
         f32x4 *buf = S + (int)(t & 1) * ST;
         const int64_t mb = m_lo + t * BK;
@@ -440,16 +443,28 @@ __global__ void __launch_bounds__(256) k_wgrad_ring(const float *__restrict__ X0
         const float *xs = (const float *)(S + (int)(t & 1) * ST);
         const float *gs = xs + 4 * X_CH;
 #pragma unroll
-        for (int u = 0; u < BK / 2; ++u) {
-            const int row = 2 * u + h;
-            const fa_t a = *(const fa_t *)&xs[row * BA + wa * (32 * VA) + VA * lr];
-            const fb_t b = *(const fb_t *)&gs[row * BO + wo * (32 * VB) + VB * lr];
+        for (int u = 0; u < BK / 16; ++u) {
+            float xa[VA][8], xb[VB][8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int row = 16 * u + 8 * h + q;
+                const fa_t a = *(const fa_t *)&xs[row * BA + wa * (32 * VA) + VA * lr];
+                const fb_t b = *(const fb_t *)&gs[row * BO + wo * (32 * VB) + VB * lr];
+#pragma unroll
+                for (int i = 0; i < VA; ++i) xa[i][q] = a[i];
+#pragma unroll
+                for (int j = 0; j < VB; ++j) xb[j][q] = b[j];
+            }
+            bf16x8 a1[VA], a2[VA], a3[VA], b1[VB], b2[VB], b3[VB];
+#pragma unroll
+            for (int i = 0; i < VA; ++i) split3(xa[i], a1[i], a2[i], a3[i]);
+#pragma unroll
+            for (int j = 0; j < VB; ++j) split3(xb[j], b1[j], b2[j], b3[j]);
 #pragma unroll
             for (int i = 0; i < VA; ++i)
 #pragma unroll
-                for (int j = 0; j < VB; ++j) {
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
-                }
+                for (int j = 0; j < VB; ++j)
+                    acc[i][j] = mfma_split6(a1[i], a2[i], a3[i], b1[j], b2[j], b3[j], acc[i][j]);
         }
     };
     if (steps > 0) {
@@ -507,11 +522,11 @@ void launch_wgrad(const float *x_self, int64_t ld_self, const float *agg, int64_
     {
         KernelTimer t(label, s);
         if (BO == 128)
-            hipLaunchKernelGGL((k_wgrad_ring<128, 128, 16>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, s,
+            hipLaunchKernelGGL((k_wgrad_split<128, 128>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, s,
                                x_self, ld_self, agg, ld_agg, m, m_dev, d_in, dz, ld_dz, d_out, splits,
                                part.as<float>());
         else
-            hipLaunchKernelGGL((k_wgrad_ring<128, 64, 32>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, s,
+            hipLaunchKernelGGL((k_wgrad_split<128, 64>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, s,
                                x_self, ld_self, agg, ld_agg, m, m_dev, d_in, dz, ld_dz, d_out, splits,
                                part.as<float>());
     }
