@@ -636,7 +636,10 @@ static void launch_main(const void *self, int64_t ld_self, const void *agg, int6
     if (!bf16) {
         const int64_t nrow = (m + BM - 1) / BM, ncol = (n + BN - 1) / BN;
         const dim3 grid((unsigned)(((nrow + 7) / 8) * 8 * ncol));
-        hipLaunchKernelGGL((k_combine_split<float, BM, BN, 2>), grid, dim3(256), 0, s, (const float *)self, ld_self,
+        // 128 x 128 tiles as 4 x 1 wavefronts: each splits only its own 32
+        // rows of A (2 x 2 split every row twice); measured 2-6% faster
+        constexpr int WM = BM == 128 ? 4 : 2;
+        hipLaunchKernelGGL((k_combine_split<float, BM, BN, WM>), grid, dim3(256), 0, s, (const float *)self, ld_self,
                            (const float *)agg, ld_agg, m, m_dev, k, g_wt.buf.as<uint16_t>(), 2 * kp, n * 2 * kp, kp, 2,
                            n, (int)relu, (float *)out, ld_out);
     } else if (out_bf16) {
