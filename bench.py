@@ -51,6 +51,17 @@ KERNEL_SOURCES = {"aggregate_mean": ["spmm.hip", "common.hpp"],
                   "combine_gemm": ["gemm.hip", "common.hpp", "dma.hpp", "bf16split.hpp"]}
 
 
+def cpu_model() -> str:
+    """The host CPU's model name as /proc/cpuinfo gives it."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def traffic_for(kernel: str, workload: str):
     """HBM bytes per launch from committed rocprofv3 counter runs, if still current."""
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
@@ -462,6 +473,10 @@ def main():
         gemm_kind[f"combine_gemm.l{l}"] = G.combine_kernel(m_mean, wl.dims[l], wl.dtype)
     link_bound = miss_bytes > 0
     work["gather_rows"] = miss_bytes if link_bound else hit_bytes
+    # the committed counter runs used the workload's default cache, a static
+    # policy and uniform sampling: their bytes apply only to such runs
+    profiled_config = ((args.cache_fraction is None or args.cache_fraction == wl.cfg["cache"])
+                       and args.eta is None and args.cache_policy == "static")
 
     kernels = {}
     for name, (launches, ms) in prof.items():
@@ -499,6 +514,16 @@ def main():
                "frac": round(achieved / peak, 4), "per_launch": round(amount / max(launches, 1), 1)}
         if name in edge:
             ent["achieved_edge_effective"] = round(edge[name] / (ms * 1e-3) / 1e9, 2)
+        counted = traffic_for(name, wl.name) if profiled_config else None
+        if counted:
+            # rocprofv3-counted HBM bytes per launch (committed summary, same
+            # kernel source): the counted rate, and compulsory / counted bytes
+            byte_work = gemm_bytes.get(name) if name.startswith("combine_gemm") else (
+                hit_bytes if name == "gather_rows" else work[name])
+            ent["counted_bytes_per_launch"] = counted
+            ent["counted_gbs"] = round(counted * launches / (ms * 1e-3) / 1e9, 2)
+            if byte_work and not (name == "gather_rows" and link_bound):
+                ent["useful_byte_efficiency"] = round(byte_work / max(launches, 1) / counted, 4)
         if name.startswith("combine_gemm"):
             ent["kernel"] = gemm_kind.get(name)
             ent["tflops"] = round(work[name] / (ms * 1e-3) / 1e12, 2)   # algorithmic (fp32-equivalent) rate
@@ -519,7 +544,8 @@ def main():
     if dom:
         k = kernels[dom]
         roofline = {"kernel": dom, "bound": k["bound"], "achieved": k["achieved"], "peak": k["peak"],
-                    "unit": k["unit"], "frac": k["frac"], "traffic": traffic_for(dom, wl.name)}
+                    "unit": k["unit"], "frac": k["frac"],
+                    "traffic": traffic_for(dom, wl.name) if profiled_config else None}
         if dom.startswith("combine_gemm") and k.get("kernel") == "split":
             roofline["method"] = "fp32 through a three-way bf16 split: 6 bf16 MFMA products per fp32 product"
             roofline["fp32_equivalent_tflops"] = k["tflops"]
@@ -562,6 +588,7 @@ def main():
             O.sage_forward(ob, O.to_f64(h0, wl.dtype), wd, bf16=wl.dtype == "bf16")
         ct = time.perf_counter() - t0
         cpu = {"value": round(wl.batch * nb / ct, 2), "unit": "seeds/s", "cores": 1, "kind": "oracle",
+               "cpu_model": cpu_model(),
                "sample": f"{nb} batch(es) of {wl.batch} seeds of {wl.name} (batches {args.warmup}.."
                          f"{args.warmup + nb - 1}), single-threaded C oracle, {ct:.1f}s"}
         log(f"oracle: {cpu['value']} seeds/s")
@@ -583,6 +610,7 @@ def main():
                 list(ex.map(one, [args.warmup + (i % args.steps) for i in range(P)]))
             ct = time.perf_counter() - t0
             cpu_all = {"value": round(wl.batch * P / ct, 2), "unit": "seeds/s", "cores": P, "kind": "oracle",
+                       "cpu_model": cpu_model(),
                        "sample": f"{P} batches of {wl.batch} seeds of {wl.name}, one per thread, "
                                  f"single-threaded C oracle on each, {ct:.1f}s"}
             log(f"oracle on {P} threads: {cpu_all['value']} seeds/s")
@@ -607,7 +635,11 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
         "data": "synthetic",
-        "config": {"workload": wl.name, "pipeline_streams": args.depth, "link_workgroups": fwd_link, "link_workgroup_estimates_ms": fwd_link_est,
+        "config": {"workload": wl.name,
+                   "seeds": {"graph": W.GRAPH_SEED, "features": W.FEAT_SEED, "permutation": W.PERM_SEED,
+                             "weights": W.WEIGHT_SEED, "labels": W.LABEL_SEED,
+                             "sampler_batch_b": f"({W.RNG_BASE} << 32) | b"},
+                   "pipeline_streams": args.depth, "link_workgroups": fwd_link, "link_workgroup_estimates_ms": fwd_link_est,
                    "n": wl.n, "nnz": g.nnz, "d": wl.d, "fanouts": wl.fanouts,
                    "batch": wl.batch, "layers": wl.L, "dims": wl.dims, "cache_fraction": r,
                    "store_on_device": wl.cfg["store_on_device"], "cache_policy": args.cache_policy,
