@@ -698,14 +698,20 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
                         bias ? bias->slot_map.as<int32_t>() : nullptr, eta,
                         bias && bias->ring_n == 0 ? bias->part_col.as<int32_t>() : nullptr,
                         bias && bias->ring_n == 0 ? bias->part_cnt.as<int32_t>() : nullptr, map, tag};
+        if (h > 1) {   // hop h - 1's relabel rides along with this count scan
+            a.relabel_list = b->nbrs[h - 2].as<int32_t>();
+            a.relabel_len = sz + kSizeE + h - 1;
+            a.relabel_bound = eb[h - 1];
+            a.relabel_indices = b->indices[h - 2].as<int32_t>();
+        }
         launch_count_scan(a, s);
         launch_sample_hop(a, s);
         DedupArgs dh{b->nbrs[h - 1].as<int32_t>(), 0, sz + kSizeE + h, eb[h], map, tag, g->n, nodes,
                      sz + kSizeN + h - 1, sz + kSizeN + h, nullptr, &b->scan, true};
         launch_dedup(dh, s);
-        launch_relabel(b->nbrs[h - 1].as<int32_t>(), sz + kSizeE + h, eb[h], map,
-                       b->indices[h - 1].as<int32_t>(), s);
     }
+    launch_relabel(b->nbrs[n_hops - 1].as<int32_t>(), sz + kSizeE + n_hops, eb[n_hops], map,
+                   b->indices[n_hops - 1].as<int32_t>(), s);
     b->L = n_hops;
     b->host_sizes = false;
     for (int h = 0; h <= n_hops; ++h) {

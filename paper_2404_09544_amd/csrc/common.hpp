@@ -154,6 +154,12 @@ struct SampleHopArgs {
     const int32_t *part_cnt = nullptr;
     uint64_t *first_map = nullptr;           // node table: first position of each written id
     uint32_t map_tag = 0;                    // the node table tag of this sampling call
+    // optional: the previous hop's relabel, run in the count scan's launch
+    // (indices[p] = local id of list[p] from first_map)
+    const int32_t *relabel_list = nullptr;
+    const int32_t *relabel_len = nullptr;    // device length
+    int64_t relabel_bound = 0;
+    int32_t *relabel_indices = nullptr;
 };
 void launch_partition_rows(const void *row_ptr, bool offsets_i64, const int32_t *col, int64_t n,
                            const int32_t *slot_map, int32_t *part_col, int32_t *part_cnt, hipStream_t s);

@@ -99,14 +99,31 @@ struct CountOp {
     }
 };
 
+// Local ids of the previous hop's list (its relabel), carried by the count
+// scan's launch: both only need that hop's dedup finished.
+struct RelabelSide {
+    const int32_t *list;
+    const int32_t *len_ptr;
+    const uint64_t *map;
+    int32_t *indices;
+    __device__ int64_t n() const { return *len_ptr; }
+    __device__ void run(int64_t p) const { indices[p] = (int32_t)(uint32_t)map[list[p]]; }
+};
+
 void launch_count_scan(const SampleHopArgs &a, hipStream_t s) {
-    if (a.offsets_i64) {
-        CountOp<int64_t> op{(const int64_t *)a.row_ptr, a.nodes, a.n_prev, a.fanout, a.indptr, a.e_out};
-        run_scan<CountOp<int64_t>, int32_t>(op, a.rows_bound, *a.scan, "count_scan", s);
-    } else {
-        CountOp<int32_t> op{(const int32_t *)a.row_ptr, a.nodes, a.n_prev, a.fanout, a.indptr, a.e_out};
-        run_scan<CountOp<int32_t>, int32_t>(op, a.rows_bound, *a.scan, "count_scan", s);
-    }
+    auto run = [&](auto op) {
+        using Op = decltype(op);
+        if (a.relabel_list)
+            run_scan<Op, int32_t, RelabelSide>(
+                op, a.rows_bound, *a.scan, "count_scan", s,
+                RelabelSide{a.relabel_list, a.relabel_len, a.first_map, a.relabel_indices}, a.relabel_bound);
+        else
+            run_scan<Op, int32_t>(op, a.rows_bound, *a.scan, "count_scan", s);
+    };
+    if (a.offsets_i64)
+        run(CountOp<int64_t>{(const int64_t *)a.row_ptr, a.nodes, a.n_prev, a.fanout, a.indptr, a.e_out});
+    else
+        run(CountOp<int32_t>{(const int32_t *)a.row_ptr, a.nodes, a.n_prev, a.fanout, a.indptr, a.e_out});
 }
 
 __device__ __forceinline__ uint64_t node_position(uint32_t tag, int64_t p) {

@@ -116,17 +116,32 @@ __device__ __forceinline__ bool read_record(const uint64_t *rec, int64_t tile, u
     return true;
 }
 
-template <class Op, class V>
-__global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, uint64_t *__restrict__ sums,
+// An element-wise job that rides along in a scan's launch (Side::n() items,
+// Side::run(i) for each) on workgroups of its own: independent work that
+// would otherwise cost a launch of its own.
+struct NoSide {
+    __device__ int64_t n() const { return 0; }
+    __device__ void run(int64_t) const {}
+};
+
+template <class Op, class V, class Side>
+__global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, Side side, int scan_grid,
+                                                                uint64_t *__restrict__ sums,
                                                                 uint64_t *__restrict__ prefix,
                                                                 uint32_t *__restrict__ ctl, uint32_t epoch) {
     __shared__ V scratch[kScanThreads / kWave];
     __shared__ int64_t s_tile;
     __shared__ V s_prefix;
+    if ((int)blockIdx.x >= scan_grid) {   // the side job's workgroups
+        const int64_t m = side.n(), stride = (int64_t)(gridDim.x - scan_grid) * kScanThreads;
+        for (int64_t i = (int64_t)(blockIdx.x - scan_grid) * kScanThreads + threadIdx.x; i < m; i += stride)
+            side.run(i);
+        return;
+    }
     const int64_t n = op.n();
     int64_t ntiles = (n + kScanTile - 1) / kScanTile;
     if (ntiles < 1) ntiles = 1;
-    const int64_t workers = ntiles < (int64_t)gridDim.x ? ntiles : (int64_t)gridDim.x;
+    const int64_t workers = ntiles < (int64_t)scan_grid ? ntiles : (int64_t)scan_grid;
     if ((int64_t)blockIdx.x >= workers) return;
     for (;;) {
         // Every worker draws tickets until it draws one past the last tile,
@@ -211,16 +226,20 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, uint64_t *
     }
 }
 
-// Enqueue one scan.  `bound` >= op.n() sizes the grid; `st` must have been
-// ensure()d for `bound` on this stream.
-template <class Op, class V>
-void run_scan(const Op &op, int64_t bound, ScanState &st, const char *name, hipStream_t s) {
+// Enqueue one scan, and with it the side job over at most side_bound items.
+// `bound` >= op.n() sizes the grid; `st` must have been ensure()d for
+// `bound` on this stream.
+template <class Op, class V, class Side = NoSide>
+void run_scan(const Op &op, int64_t bound, ScanState &st, const char *name, hipStream_t s,
+              const Side &side = Side(), int64_t side_bound = 0) {
     int64_t grid = scan_parts(bound);
     if (grid > kScanGrid) grid = kScanGrid;
+    const int64_t side_grid = side_bound > 0 ? (int64_t)grid_for(side_bound, kScanThreads, 2048) : 0;
     const uint32_t epoch = st.next_epoch();
     KernelTimer t(name, s);
-    hipLaunchKernelGGL((k_scan_onepass<Op, V>), dim3((unsigned)grid), dim3(kScanThreads), 0, s, op,
-                       st.sums.as<uint64_t>(), st.prefix.as<uint64_t>(), st.ctl.as<uint32_t>(), epoch);
+    hipLaunchKernelGGL((k_scan_onepass<Op, V, Side>), dim3((unsigned)(grid + side_grid)), dim3(kScanThreads), 0, s,
+                       op, side, (int)grid, st.sums.as<uint64_t>(), st.prefix.as<uint64_t>(),
+                       st.ctl.as<uint32_t>(), epoch);
     GNNAV_HIP(hipGetLastError());
 }
 
