@@ -213,7 +213,7 @@ void launch_matmul_bt(const float *a, int64_t lda, int64_t m, const int32_t *m_d
 // edge order) and its column pointers; see train.hip.
 struct ScanState;
 struct CscWorkspace {
-    DevBuf keys[2], vals[2], hist, offs, col_ptr, cnt;
+    DevBuf keys[2], vals[2], hist, offs, col_ptr;
     const int32_t *sorted_rows = nullptr;
     void build(const int32_t *indptr, const int32_t *indices, int64_t n_dst, const int32_t *n_dst_dev,
                const int32_t *n_edges_dev, int64_t e_bound, int64_t n_src_bound, ScanState &scan, hipStream_t s,
@@ -226,7 +226,6 @@ struct CscWorkspace {
         hist.release();
         offs.release();
         col_ptr.release();
-        cnt.release();
     }
 };
 void launch_softmax_xent(const float *z, int64_t ldz, int64_t n, const int32_t *n_dev, int64_t C,

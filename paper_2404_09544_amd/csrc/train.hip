@@ -7,13 +7,15 @@
 //                  workgroup in a fixed order
 //   csc            the transpose of a sampled block, by a stable LSD radix
 //                  sort of (source local id, destination row) pairs in edge
-//                  order, so every column lists its edges in edge order
+//                  order, so every column lists its edges in edge order;
+//                  column pointers by a lower-bound search of the sorted keys
 //   aggregate_t    the adjoint of the mean aggregation: for each source row j,
 //                  the sum over its column of dAgg[i] / cnt_i, in column
 //                  order, plus the self-term gradient, times the ReLU mask of
 //                  the layer below; no floating-point atomics, so the result
 //                  is the same on every run
-//   wgrad          dW = [X_self | Agg]^T dZ: MFMA tiles over (input feature,
+//   wgrad          dW = [X_self | Agg]^T dZ (bf16 matrix cores through the
+//                  three-way bf16 split): MFMA tiles over (input feature,
 //                  output feature), the row dimension split into ranges whose
 //                  partial tiles are summed in range order by the reduce
 //                  kernel, which also applies W -= lr * dW
@@ -181,26 +183,23 @@ __global__ void __launch_bounds__(256) k_radix_scatter(const int32_t *__restrict
     }
 }
 
-// Column lengths; ids outside [0, n_src) are not counted (they are never read).
-__global__ void __launch_bounds__(256) k_col_count(const int32_t *__restrict__ keys, const int32_t *__restrict__ n_ptr,
-                                                   int64_t n_src, int32_t *__restrict__ cnt) {
+// Column pointers from the sorted keys: col_ptr[s] = the number of keys
+// below s (a lower-bound search per s), for s in [0, n_src_bound].  The keys
+// are local source ids, all below n_src_bound.
+__global__ void __launch_bounds__(256) k_col_ptr(const int32_t *__restrict__ keys, const int32_t *__restrict__ n_ptr,
+                                                 int64_t n_src_bound, int32_t *__restrict__ col_ptr) {
     const int64_t n = *n_ptr;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += stride) {
-        const int32_t k = keys[e];
-        if (k >= 0 && k < n_src) atomicAdd(&cnt[k], 1);
+    for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c <= n_src_bound; c += stride) {
+        int64_t lo = 0, hi = n;
+        while (lo < hi) {
+            const int64_t mid = (lo + hi) >> 1;
+            if (keys[mid] < c) lo = mid + 1;
+            else hi = mid;
+        }
+        col_ptr[c] = (int32_t)lo;
     }
 }
-
-struct ColPtrOp {
-    const int32_t *cnt;
-    int32_t *col_ptr;
-    int64_t count;
-    __device__ int64_t n() const { return count; }
-    __device__ int32_t value(int64_t i) const { return cnt[i]; }
-    __device__ void emit(int64_t i, int32_t prefix, int32_t) const { col_ptr[i] = prefix; }
-    __device__ void total(int32_t t) const { col_ptr[count] = t; }
-};
 
 // Sorted (source, destination row) pairs of one block and its column
 // pointers.  n_edges_dev: device edge count (<= e_bound); n_src_bound sizes
@@ -218,7 +217,6 @@ void CscWorkspace::build(const int32_t *indptr, const int32_t *indices, int64_t 
     hist.ensure(256 * ntiles * sizeof(int32_t), s);
     offs.ensure(256 * ntiles * sizeof(int32_t), s);
     col_ptr.ensure((n_src_bound + 1) * sizeof(int32_t), s);
-    cnt.ensure(std::max<int64_t>(n_src_bound, 1) * sizeof(int32_t), s);
     // pass 0 reads the block's indices directly; values are destination rows
     hipLaunchKernelGGL(k_edge_rows, dim3(grid_for(n_dst, 256, 4096)), dim3(256), 0, s, indptr, n_dst, n_dst_dev,
                        vals[1].as<int32_t>());
@@ -241,12 +239,8 @@ void CscWorkspace::build(const int32_t *indptr, const int32_t *indices, int64_t 
         cur ^= 1;
     }
     sorted_rows = vin;
-    launch_fill_i32(cnt.as<int32_t>(), 0, std::max<int64_t>(n_src_bound, 1), s);
-    hipLaunchKernelGGL(k_col_count, dim3(grid_for(eb, 256, 4096)), dim3(256), 0, s, kin, n_edges_dev, n_src_bound,
-                       cnt.as<int32_t>());
-    scan.ensure(n_src_bound, s);
-    run_scan<ColPtrOp, int32_t>(ColPtrOp{cnt.as<int32_t>(), col_ptr.as<int32_t>(), n_src_bound}, n_src_bound, scan,
-                                "csc_scan", s);
+    hipLaunchKernelGGL(k_col_ptr, dim3(grid_for(n_src_bound + 1, 256, 4096)), dim3(256), 0, s, kin, n_edges_dev,
+                       n_src_bound, col_ptr.as<int32_t>());
     GNNAV_HIP(hipGetLastError());
 }
 
