@@ -30,22 +30,29 @@ struct ClassifyOp {
     uint4 *out;
     int64_t out_ld16;
     int64_t chunks;
+    // the request and its slot, read once for both scan passes (slot -2:
+    // id out of range)
+    struct Item {
+        int32_t id, slot;
+    };
     // packed value: hits in the high 32 bits, misses in the low 32 bits
     __device__ int64_t n() const { return n_ptr ? (int64_t)*n_ptr : n_ids; }
-    __device__ int64_t value(int64_t i) const {
+    __device__ Item load(int64_t i) const {
         const int32_t id = ids[i];
-        if (id < 0 || id >= n_nodes) return 0;
-        return slot_map[id] >= 0 ? (int64_t(1) << 32) : int64_t(1);
+        return Item{id, (id < 0 || id >= n_nodes) ? -2 : slot_map[id]};
     }
-    __device__ void emit(int64_t i, int64_t prefix, int64_t v) const {
-        const int32_t id = ids[i];
+    __device__ int64_t value(const Item &it) const {
+        if (it.slot == -2) return 0;
+        return it.slot >= 0 ? (int64_t(1) << 32) : int64_t(1);
+    }
+    __device__ void emit(int64_t i, int64_t prefix, int64_t v, const Item &it) const {
         if (v == 0) {
             uint4 *row = out + i * out_ld16;
             for (int64_t c = 0; c < chunks; ++c) row[c] = make_uint4(0, 0, 0, 0);
         } else if (v == 1) {
-            miss_list[(int32_t)(prefix & 0xffffffff)] = make_int2((int32_t)i, id);
+            miss_list[(int32_t)(prefix & 0xffffffff)] = make_int2((int32_t)i, it.id);
         } else {
-            hit_list[(int32_t)(prefix >> 32)] = make_int2((int32_t)i, slot_map[id]);
+            hit_list[(int32_t)(prefix >> 32)] = make_int2((int32_t)i, it.slot);
         }
     }
     __device__ void total(int64_t t) const {

@@ -554,18 +554,22 @@ struct DedupOp {
     int32_t *nodes;
     const int32_t *base_ptr;
     int32_t *size_out;
+    // the id and whether p is its first position, read once for both passes
+    struct Item {
+        int32_t id, first;
+    };
     __device__ int64_t n() const { return list_len(len_const, len_ptr); }
-    __device__ int32_t value(int64_t p) const {
+    __device__ Item load(int64_t p) const {
         const int32_t id = list[p];
-        if (id < 0 || id >= n_nodes) return 0;
-        return map[id] == node_position(tag, p) ? 1 : 0;
+        if (id < 0 || id >= n_nodes) return Item{id, 0};
+        return Item{id, map[id] == node_position(tag, p) ? 1 : 0};
     }
-    __device__ void emit(int64_t p, int32_t prefix, int32_t v) const {
+    __device__ int32_t value(const Item &it) const { return it.first; }
+    __device__ void emit(int64_t p, int32_t prefix, int32_t v, const Item &it) const {
         if (!v) return;
-        const int32_t id = list[p];
         const int32_t local = (base_ptr ? *base_ptr : 0) + prefix;
-        nodes[local] = id;
-        map[id] = node_local(tag, local);
+        nodes[local] = it.id;
+        map[it.id] = node_local(tag, local);
     }
     __device__ void total(int32_t t) const { *size_out = (base_ptr ? *base_ptr : 0) + t; }
 };

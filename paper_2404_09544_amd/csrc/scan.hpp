@@ -6,6 +6,10 @@
 //   void emit(int64_t i, V prefix, V v)  called for every i with its
 //                                        exclusive prefix (sum over j < i)
 //   void total(V t)                      called once with the grand total
+// or, to read each element's inputs once for both passes, a type Item with
+//   Item load(int64_t i) const, V value(const Item &) const and
+//   void emit(int64_t i, V prefix, V v, const Item &) const
+// (the items stay in registers between the two passes).
 //
 // Single-pass scan with decoupled look-back: workgroups claim tiles in order
 // from an atomic ticket (so a tile only ever waits for tiles whose
@@ -34,6 +38,8 @@
 // otherwise pay twice and that evicted the other workgroups' working sets.
 #pragma once
 
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace gnnav {
@@ -41,6 +47,30 @@ namespace gnnav {
 constexpr int kScanThreads = 256;
 constexpr int kScanItems = 8;
 constexpr int kScanTile = kScanThreads * kScanItems;
+
+template <class Op, class = void>
+struct ScanHasItem : std::false_type {};
+template <class Op>
+struct ScanHasItem<Op, std::void_t<typename Op::Item>> : std::true_type {};
+
+template <class Op, bool = ScanHasItem<Op>::value>
+struct ScanItems {   // no items: values are recomputed by index
+    __device__ void load(const Op &, int, int64_t) {}
+    template <class V>
+    __device__ V value(const Op &op, int, int64_t i) const { return op.value(i); }
+    template <class V>
+    __device__ void emit(const Op &op, int, int64_t i, V prefix, V v) const { op.emit(i, prefix, v); }
+};
+template <class Op>
+struct ScanItems<Op, true> {
+    typename Op::Item it[kScanItems];
+    __device__ void load(const Op &op, int j, int64_t i) { it[j] = op.load(i); }
+    template <class V>
+    __device__ V value(const Op &op, int j, int64_t) const { return op.value(it[j]); }
+    template <class V>
+    __device__ void emit(const Op &op, int j, int64_t i, V prefix, V v) const { op.emit(i, prefix, v, it[j]); }
+};
+
 constexpr uint32_t kSpinLimit = 1u << 20;
 constexpr int64_t kScanGrid = 1024;   // workgroups per scan launch, at most
 
@@ -158,11 +188,17 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, Side side,
 
         const int64_t first = tile * kScanTile + (int64_t)threadIdx.x * kScanItems;
         V vals[kScanItems];
+        ScanItems<Op> items;
         V s = V(0);
     #pragma unroll
         for (int j = 0; j < kScanItems; ++j) {
             const int64_t i = first + j;
-            vals[j] = i < n ? op.value(i) : V(0);
+            if (i < n) items.load(op, j, i);
+        }
+    #pragma unroll
+        for (int j = 0; j < kScanItems; ++j) {
+            const int64_t i = first + j;
+            vals[j] = i < n ? items.template value<V>(op, j, i) : V(0);
             s += vals[j];
         }
         V total;
@@ -219,7 +255,7 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, Side side,
     #pragma unroll
         for (int j = 0; j < kScanItems; ++j) {
             const int64_t i = first + j;
-            if (i < n) op.emit(i, run, vals[j]);
+            if (i < n) items.emit(op, j, i, run, vals[j]);
             run += vals[j];
         }
         __syncthreads();   // s_tile / s_prefix are reused by the next ticket
