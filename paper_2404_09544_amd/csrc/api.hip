@@ -687,9 +687,15 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
     uint64_t *map = b->map.as<uint64_t>();
     int32_t *nodes = b->nodes.as<int32_t>();
     launch_fill_i32(sz, 0, kSizeSlots, s);
-    // F_0: seeds without repeats, first occurrence kept
+    // F_0 (seeds without repeats, first occurrence kept) and hop 1's row
+    // counts (indptr_1, E_1) in one scan
     DedupArgs d0{seeds_dev, n_seeds, nullptr, n_seeds, map, tag, g->n, nodes, nullptr, sz + kSizeN, sz + kSizeErr,
                  &b->scan};
+    d0.count_row_ptr = g->row_ptr.p;
+    d0.count_i64 = g->i64;
+    d0.count_k = fanouts[0];
+    d0.count_indptr = b->indptr[0].as<int32_t>();
+    d0.count_e_out = sz + kSizeE + 1;
     launch_dedup(d0, s);
     for (int h = 1; h <= n_hops; ++h) {
         SampleHopArgs a{g->row_ptr.p, g->i64, g->col.as<int32_t>(), nodes, sz + kSizeN + h - 1,
@@ -704,7 +710,7 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
             a.relabel_bound = eb[h - 1];
             a.relabel_indices = b->indices[h - 2].as<int32_t>();
         }
-        launch_count_scan(a, s);
+        if (h > 1) launch_count_scan(a, s);   // hop 1's ran with the seeds' dedup
         launch_sample_hop(a, s);
         DedupArgs dh{b->nbrs[h - 1].as<int32_t>(), 0, sz + kSizeE + h, eb[h], map, tag, g->n, nodes,
                      sz + kSizeN + h - 1, sz + kSizeN + h, nullptr, &b->scan, true};

@@ -180,6 +180,13 @@ struct DedupArgs {
     int32_t *err;            // device count of out-of-range ids (nullable)
     ScanState *scan;
     bool first_done = false; // first positions already in `map` (taken while writing the list)
+    // optional, for the seeds (base_ptr null): hop 1's count scan folded in,
+    // writing indptr (|F_0| + 1 entries) and the edge count of fanout k
+    const void *count_row_ptr = nullptr;
+    bool count_i64 = false;
+    int32_t count_k = 0;
+    int32_t *count_indptr = nullptr;
+    int32_t *count_e_out = nullptr;
 };
 void launch_dedup(const DedupArgs &a, hipStream_t s);
 void launch_relabel(const int32_t *list, const int32_t *len_ptr, int64_t len_bound,

@@ -2,7 +2,9 @@
 //
 // Per hop h:
 //   count scan   indptr_h = exclusive scan of min(deg(v), k) over F_(h-1)
-//   sample       one wavefront per destination row: copy the row when
+//                (for h = 1 folded into the seeds' dedup scan; for h > 1 it
+//                also carries hop h-1's relabel on extra workgroups)
+//   sample       one or more rows per wavefront: copy the row when
 //                deg <= k, else Floyd's k-subset with Philox4x32-10 draws
 //   dedup        first position of each id in N_h (atomicMin on a dense
 //                per-node table, taken by the sample kernel as it writes
@@ -574,6 +576,46 @@ struct DedupOp {
     __device__ void total(int32_t t) const { *size_out = (base_ptr ? *base_ptr : 0) + t; }
 };
 
+// The seeds' dedup with hop 1's count scan folded in: F_0 is exactly the
+// seeds' first occurrences in order, so one scan of (first, min(deg, k))
+// pairs gives both the local ids and indptr_1 (edges in the high half).
+template <class OffT>
+struct SeedDedupCountOp {
+    DedupOp d;
+    const OffT *row_ptr;
+    int32_t k;
+    int32_t *indptr;
+    int32_t *e_out;
+    struct Item {
+        int32_t id, first, count;
+    };
+    __device__ int64_t n() const { return d.n(); }
+    __device__ Item load(int64_t p) const {
+        const DedupOp::Item b = d.load(p);
+        int32_t c = 0;
+        if (b.first) {
+            int64_t st;
+            const int64_t deg = row_degree(row_ptr, b.id, st);
+            c = (int32_t)((k < 0 || deg <= k) ? deg : k);
+        }
+        return Item{b.id, b.first, c};
+    }
+    __device__ int64_t value(const Item &it) const { return ((int64_t)it.count << 32) | (int64_t)it.first; }
+    __device__ void emit(int64_t p, int64_t prefix, int64_t v, const Item &it) const {
+        if (!it.first) return;
+        const int32_t local = (int32_t)(prefix & 0xffffffff);
+        d.nodes[local] = it.id;
+        d.map[it.id] = node_local(d.tag, local);
+        indptr[local] = (int32_t)(prefix >> 32);
+    }
+    __device__ void total(int64_t t) const {
+        const int32_t nf = (int32_t)(t & 0xffffffff), e = (int32_t)(t >> 32);
+        *d.size_out = nf;
+        indptr[nf] = e;
+        *e_out = e;
+    }
+};
+
 void launch_dedup(const DedupArgs &a, hipStream_t s) {
     if (a.len_bound > 0 && !a.first_done) {
         KernelTimer t("dedup_first", s);
@@ -583,6 +625,18 @@ void launch_dedup(const DedupArgs &a, hipStream_t s) {
     }
     DedupOp op{a.list, a.len_const, a.len_ptr, (unsigned long long *)a.map, a.tag, a.n_nodes, a.nodes, a.base_ptr,
                a.size_out};
+    if (a.count_row_ptr) {
+        GNNAV_CHECK(!a.base_ptr, GNNAV_E_INVALID, "a folded count scan needs an empty frontier before the list");
+        if (a.count_i64)
+            run_scan<SeedDedupCountOp<int64_t>, int64_t>(
+                SeedDedupCountOp<int64_t>{op, (const int64_t *)a.count_row_ptr, a.count_k, a.count_indptr, a.count_e_out},
+                a.len_bound, *a.scan, "dedup_scan", s);
+        else
+            run_scan<SeedDedupCountOp<int32_t>, int64_t>(
+                SeedDedupCountOp<int32_t>{op, (const int32_t *)a.count_row_ptr, a.count_k, a.count_indptr, a.count_e_out},
+                a.len_bound, *a.scan, "dedup_scan", s);
+        return;
+    }
     run_scan<DedupOp, int32_t>(op, a.len_bound, *a.scan, "dedup_scan", s);
 }
 
