@@ -241,20 +241,56 @@ __global__ void __launch_bounds__(256) k_combine_ring(const T *__restrict__ A0, 
         compute(t);
     }
 
-    const int64_t r0 = m0 + wm * WTM, c0 = n0 + wn * WTN;
+    if constexpr (sizeof(OutT) == 2) {
+        // bf16 out: the accumulators' 2-byte column-strided stores would
+        // leave each row as 64-byte pieces; the tile goes through the (now
+        // idle) ring as bf16 rows instead and leaves in 16-byte row chunks
+        // (7% at 107k x 256, 13% at 400k x 256 over the direct stores)
+        constexpr int LDT = BN + 8, CPR = BN / 8;
+        static_assert(BM * LDT * 2 <= STAGES * ST * 16, "output tile fits the ring");
+        uint16_t *tile = (uint16_t *)S;
+        lds_barrier();   // every wavefront is done reading the last stage
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
+            for (int j = 0; j < TN; ++j)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int64_t row = r0 + i * 32 + 8 * (r / 4) + 4 * h + (r % 4), col = c0 + j * 32 + lr;
-                if (row < M && col < N) {
+                for (int r = 0; r < 16; ++r) {
+                    const int rl = wm * WTM + i * 32 + 8 * (r / 4) + 4 * h + (r % 4), cl = wn * WTN + j * 32 + lr;
                     float v = acc[i][j][r];
                     if (relu) v = fmaxf(v, 0.f);
-                    store_out<OutT>(C + row * ldc + col, v);
+                    tile[rl * LDT + cl] = bf16_rne(v);
                 }
+        __syncthreads();
+        const bool vec = ((reinterpret_cast<uintptr_t>(C) | (uintptr_t)(ldc * 2)) & 15) == 0;
+        for (int c = tid; c < BM * CPR; c += 256) {
+            const int rl = c / CPR, cc = c % CPR;
+            const int64_t row = m0 + rl, col = n0 + cc * 8;
+            if (row >= M || col >= N) continue;
+            const uint16_t *src = tile + rl * LDT + cc * 8;
+            OutT *dst = C + row * ldc + col;
+            if (vec && col + 8 <= N) {
+                *(uint4 *)dst = *(const uint4 *)src;
+            } else {
+                for (int e = 0; e < 8 && col + e < N; ++e) dst[e] = src[e];
             }
+        }
+    } else {
+        const int64_t r0 = m0 + wm * WTM, c0 = n0 + wn * WTN;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t row = r0 + i * 32 + 8 * (r / 4) + 4 * h + (r % 4), col = c0 + j * 32 + lr;
+                    if (row < M && col < N) {
+                        float v = acc[i][j][r];
+                        if (relu) v = fmaxf(v, 0.f);
+                        store_out<OutT>(C + row * ldc + col, v);
+                    }
+                }
+    }
 }
 
 // ------------------------------------------ fp32 through split bf16
