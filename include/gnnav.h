@@ -282,8 +282,10 @@ gnnav_status gnnav_aggregate_mean(const int32_t *indptr_dev, const int32_t *indi
  * fp32; see gnnav_combine_kernel).  dt = BF16:
  * bf16 operands, fp32 accumulation, output bf16 (nearest-even) when
  * out_bf16 is nonzero, else fp32.  The concatenation [self | agg] is never
- * formed.  Errors: E_INVALID (null pointers with m > 0, d_in or d_out <= 0,
- * strides too small), E_DEVICE.  Asynchronous.                            */
+ * formed.  self and agg rows start 16-byte aligned; out needs only its
+ * element's alignment (aligned rows are stored 16 bytes at a time).
+ * Errors: E_INVALID (null pointers with m > 0, d_in or d_out <= 0, strides
+ * too small, self or agg rows misaligned), E_DEVICE.  Asynchronous.       */
 gnnav_status gnnav_combine(const void *self_dev, int64_t ld_self, const void *agg_dev,
                            int64_t ld_agg, int64_t m, int64_t d_in, const void *w_dev,
                            int64_t d_out, gnnav_dtype dt, int32_t relu, int32_t out_bf16,

@@ -410,6 +410,30 @@ def test_combine_parity(G, m, d_in, d_out, relu, mode):
     assert_rows_close(got, z, BF16_TOL if dtype == "bf16" else FP32_TOL, "combine")
 
 
+# bf16 output rows that are not 16-byte aligned (odd stride, base one element
+# in): the kernels fall back from 16-byte row stores to element stores.  The
+# words around each row must keep their sentinel.
+@pytest.mark.parametrize("m,d_in,d_out", [(20000, 128, 256), (12001, 100, 47), (40000, 37, 130), (500, 64, 33)])
+def test_combine_bf16_unaligned_out(G, m, d_in, d_out):
+    import torch
+    say("combine unaligned out", m, d_in, d_out)
+    S = W.features(m, d_in, "bf16", seed=m + 5)
+    A = W.features(m, d_in, "bf16", seed=m + 6)
+    Wt = W.glorot(d_in, d_out, "bf16", seed=d_out + 1)
+    Sd, Ad, Wd = dev(padded(S, "bf16")), dev(padded(A, "bf16")), dev(Wt)
+    ld_o = d_out + 1 if d_out % 2 == 0 else d_out + 2
+    buf = torch.full((m * ld_o + 2,), -7, dtype=torch.int16, device="cuda")
+    out = buf[1:1 + m * ld_o].view(m, ld_o)
+    G.combine(Sd, Ad, m, d_in, Wd, d_out, "bf16", True, True, out)
+    got_all = buf.cpu().numpy()
+    rows = got_all[1:1 + m * ld_o].reshape(m, ld_o)
+    assert got_all[0] == -7 and got_all[-1] == -7 and (rows[:, d_out:] == -7).all()
+    got = O.to_f64(rows[:, :d_out].view(np.uint16), "bf16")
+    z = np.concatenate([O.to_f64(S, "bf16"), O.to_f64(A, "bf16")], axis=1) @ O.to_f64(Wt, "bf16")
+    z = O.round_bf16_array(np.maximum(z, 0))
+    assert_rows_close(got, z, BF16_TOL, "combine")
+
+
 # -------------------------------------------------------------- end to end
 
 def run_pipeline_case(G, n, u, v, feats, dtype, dims, fanouts, r, seeds, rng_seed,
