@@ -549,6 +549,8 @@ def main():
         if dom.startswith("combine_gemm") and k.get("kernel") == "split":
             roofline["method"] = "fp32 through a three-way bf16 split: 6 bf16 MFMA products per fp32 product"
             roofline["fp32_equivalent_tflops"] = k["tflops"]
+            # context: the same fp32 work against the fp32 matrix-core peak
+            roofline["fp32_equivalent_frac_of_f32_peak"] = round(k["tflops"] / MFMA_PEAK_TFLOPS["f32"], 4)
 
     m1 = int(round(float(np.mean([sz[L - 1] for sz in sizes_hist])))) if sizes_hist else 0
     device_cal = device_calibration(torch, m1, 2 * wl.dims[0], wl.dims[1], wl.dtype)
