@@ -287,7 +287,10 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cache-fraction", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-batches", type=int, default=2)
+    ap.add_argument("--cpu-batches", type=int, default=16,
+                    help="most batches the single-core oracle baseline runs")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="the single-core oracle baseline runs batches until this much time has passed")
     ap.add_argument("--cpu-threads", type=int, default=16,
                     help="cap on the threads of the all-core oracle baseline")
     ap.add_argument("--depth", type=int, default=3,
@@ -580,14 +583,17 @@ def main():
         fifo = O.FifoCache(csr, r, ring) if ring else None
         wd = [O.to_f64(w, wl.dtype) for w in ws]
         log(f"oracle set-up {time.perf_counter() - t0:.1f}s")
-        nb = max(1, args.cpu_batches)
+        # whole batches until --cpu-seconds have passed (at most --cpu-batches)
+        nb = 0
         t0 = time.perf_counter()
-        for b in range(args.warmup, args.warmup + nb):
+        while nb < max(1, args.cpu_batches) and (nb == 0 or time.perf_counter() - t0 < args.cpu_seconds):
+            b = args.warmup + nb
             bias = None if args.eta is None else (fifo.slot_map if fifo else slot)
             ob = O.sample_blocks(csr, wl.seeds(b), wl.fanouts, wl.rng_seed(b), bias_slot_map=bias,
                                  eta=args.eta or 1)
             h0, _ = fifo.gather(feats, ob.nodes) if fifo else O.gather(feats, slot, ob.nodes)
             O.sage_forward(ob, O.to_f64(h0, wl.dtype), wd, bf16=wl.dtype == "bf16")
+            nb += 1
         ct = time.perf_counter() - t0
         cpu = {"value": round(wl.batch * nb / ct, 2), "unit": "seeds/s", "cores": 1, "kind": "oracle",
                "cpu_model": cpu_model(),
