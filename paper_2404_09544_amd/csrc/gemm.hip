@@ -15,6 +15,7 @@
 // (global_load_lds_dwordx4) through a ring of STAGES buffers, so no
 // registers hold staged data and the loads of later steps are in flight
 // while the current one is multiplied.  The split kernel uses the same ring.
+// bf16 output tiles leave through the idle ring as 16-byte row chunks.
 //
 // Skinny kernel (few output rows, e.g. the last layer over the seeds): a
 // workgroup owns 16 x 16 outputs; its 8 or 16 wavefronts take interleaved
