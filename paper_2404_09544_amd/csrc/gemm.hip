@@ -313,7 +313,8 @@ __global__ void __launch_bounds__(256) k_combine_split(const float *__restrict__
                                                        const int32_t *__restrict__ m_dev, int64_t K,
                                                        const uint16_t *__restrict__ B, int64_t ldb, int64_t pstride,
                                                        int64_t bseg, int nseg, int64_t N, int relu,
-                                                       OutT *__restrict__ C, int64_t ldc) {
+                                                       OutT *__restrict__ C, int64_t ldc, int64_t Rw,
+                                                       float *__restrict__ P, int64_t ldp, int64_t pseg) {
     constexpr int CH = 8, BK = 32, WN = 4 / WM;
     constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 32, TN = WTN / 32;
     constexpr int A_CH = BM * CH, B_PL = BN * 4, B_CH = 3 * B_PL, ST = A_CH + B_CH;
@@ -327,7 +328,23 @@ __global__ void __launch_bounds__(256) k_combine_split(const float *__restrict__
     const int wm = wid / WN, wn = wid % WN, h = lane >> 5, lr = lane & 31;
     if (m_dev) M = *m_dev;
     int64_t tile_r, tile_c;
-    tile_of((N + BN - 1) / BN, tile_r, tile_c);
+    // Workgroups below Rw * ncol take whole tiles of the first Rw row bands
+    // (XCD-aware as tile_of); the rest take one segment each of the tail
+    // bands' tiles, two workgroups per tile, into partial planes P[0], P[1]
+    // (rows from Rw * BM on) that k_tail_sum adds.
+    const int64_t ncol = (N + BN - 1) / BN, Lb = blockIdx.x, Gw = Rw * ncol;
+    int64_t seg_only = -1, rbase = 0;
+    if (Lb < Gw) {
+        const int64_t xcd = Lb & 7, j = Lb >> 3;
+        tile_r = (j / ncol) * 8 + xcd;
+        tile_c = j % ncol;
+    } else {
+        const int64_t q = Lb - Gw, pair = q >> 1;
+        seg_only = q & 1;
+        tile_r = Rw + pair / ncol;
+        tile_c = pair % ncol;
+        rbase = Rw * BM;
+    }
     const int64_t m0 = tile_r * BM, n0 = tile_c * BN;
     if (m0 >= M) return;
 
@@ -348,7 +365,8 @@ __global__ void __launch_bounds__(256) k_combine_split(const float *__restrict__
         const int64_t n = n0 + r < N ? n0 + r : N - 1;
         pb[q] = B + p * pstride + n * ldb + 8 * ((rem % 4) ^ ((r >> 1) & 3));
     }
-    const int64_t kt = (K + BK - 1) / BK, steps = nseg * kt;
+    const int64_t kt = (K + BK - 1) / BK, t_first = seg_only < 0 ? 0 : seg_only * kt,
+                  steps = seg_only < 0 ? nseg * kt : t_first + kt;
 
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -415,10 +433,10 @@ __global__ void __launch_bounds__(256) k_combine_split(const float *__restrict__
 
 #pragma unroll
     for (int p = 0; p < STAGES - 1; ++p)
-        if (p < steps) issue(p);
+        if (t_first + p < steps) issue(t_first + p);
     // every wavefront issues exactly PER DMAs per step, so "stage t landed"
     // is "at most PER * (steps issued after t) pending"
-    for (int64_t t = 0; t < steps; ++t) {
+    for (int64_t t = t_first; t < steps; ++t) {
         if (STAGES == 3 && t + 1 < steps) wait_vm<PER>();
         else wait_vm<0>();
         fixup(t);
@@ -437,10 +455,29 @@ __global__ void __launch_bounds__(256) k_combine_split(const float *__restrict__
                 const int64_t row = r0 + i * 32 + 8 * (r / 4) + 4 * h + (r % 4), col = c0 + j * 32 + lr;
                 if (row < M && col < N) {
                     float v = acc[i][j][r];
-                    if (relu) v = fmaxf(v, 0.f);
-                    store_out<OutT>(C + row * ldc + col, v);
+                    if (seg_only >= 0) {
+                        P[seg_only * pseg + (row - rbase) * ldp + col] = v;
+                    } else {
+                        if (relu) v = fmaxf(v, 0.f);
+                        store_out<OutT>(C + row * ldc + col, v);
+                    }
                 }
             }
+}
+
+// Tail bands of a split combine: C[r] = act(P[0][r - r0] + P[1][r - r0]) for
+// rows r0 <= r < M (M read on the device when m_dev is given).
+__global__ void __launch_bounds__(256) k_tail_sum(const float *__restrict__ P, int64_t ldp, int64_t pseg, int64_t r0,
+                                                  int64_t M, const int32_t *__restrict__ m_dev, int64_t N, int relu,
+                                                  float *__restrict__ C, int64_t ldc) {
+    if (m_dev) M = *m_dev;
+    const int64_t total = (M - r0) * N;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+        const int64_t r = i / N, c = i - r * N;
+        float v = P[r * ldp + c] + P[pseg + r * ldp + c];
+        if (relu) v = fmaxf(v, 0.f);
+        C[(r0 + r) * ldc + c] = v;
+    }
 }
 
 // W [2K][N] fp32 -> its three bf16 parts, transposed: WS[p][n][kk] over
@@ -638,8 +675,6 @@ void launch_ring(const T *a0, int64_t lda0, const T *a1, int64_t lda1, int64_t m
 }
 }  // namespace
 
-// fp32: KIND picks the ring kernel (weights transposed and padded first) or
-// the W-as-stored kernel.  bf16: the ring kernel.
 // fp32: the weights are split into three bf16 parts and transposed, then
 // k_combine_split runs; bf16: the weights are transposed and padded, then
 // the ring kernel runs.
@@ -651,7 +686,20 @@ static void launch_main(const void *self, int64_t ld_self, const void *agg, int6
     if (!g_wt.last_use) GNNAV_HIP(hipEventCreateWithFlags(&g_wt.last_use, hipEventDisableTiming));
     GNNAV_HIP(hipStreamWaitEvent(s, g_wt.last_use, 0));
     const int64_t kp = bf16 ? (k + 63) / 64 * 64 : (k + 31) / 32 * 32;
-    g_wt.buf.ensure((size_t)(2 * kp * n * (bf16 ? 2 : 6)), s);
+    const int64_t nrow = (m + BM - 1) / BM, ncol = (n + BN - 1) / BN, nrow8 = (nrow + 7) / 8 * 8;
+    // fp32, 128 x 128 tiles, between one and 2.5 tiles per compute unit: one
+    // whole tile for each of the first 256 (as 8-band groups), the tail
+    // bands' tiles split by segment over twice the workgroups, so the
+    // busiest unit holds 1.5 tiles' work instead of 2 (20902 x 1204 x 256:
+    // 124 -> 99 us including the partial sums)
+    int64_t rw = nrow8;
+    if (!bf16 && BM == 128) {
+        const int64_t w8 = 256 / ncol / 8 * 8, tiles = nrow * ncol;
+        if (tiles > 256 && tiles <= 640 && w8 >= 8 && w8 < nrow) rw = w8;
+    }
+    const int64_t tail_rows = rw < nrow ? m - rw * BM : 0;
+    const size_t wt_bytes = (size_t)(2 * kp * n * (bf16 ? 2 : 6)), part_off = (wt_bytes + 255) / 256 * 256;
+    g_wt.buf.ensure(part_off + (size_t)(2 * tail_rows * n) * sizeof(float), s);
     const dim3 tgrid((unsigned)((n + 31) / 32), (unsigned)(2 * kp / 32));
     {
         KernelTimer tt("weights_transpose", s);
@@ -664,14 +712,17 @@ static void launch_main(const void *self, int64_t ld_self, const void *agg, int6
     }
     KernelTimer tk(label, s);
     if (!bf16) {
-        const int64_t nrow = (m + BM - 1) / BM, ncol = (n + BN - 1) / BN;
-        const dim3 grid((unsigned)(((nrow + 7) / 8) * 8 * ncol));
+        const dim3 grid((unsigned)(rw * ncol + 2 * (nrow8 > rw ? nrow - rw : 0) * ncol));
+        float *part = (float *)((char *)g_wt.buf.p + part_off);
         // 128 x 128 tiles as 4 x 1 wavefronts: each splits only its own 32
         // rows of A (2 x 2 split every row twice); measured 2-6% faster
         constexpr int WM = BM == 128 ? 4 : 2;
         hipLaunchKernelGGL((k_combine_split<float, BM, BN, WM>), grid, dim3(256), 0, s, (const float *)self, ld_self,
                            (const float *)agg, ld_agg, m, m_dev, k, g_wt.buf.as<uint16_t>(), 2 * kp, n * 2 * kp, kp, 2,
-                           n, (int)relu, (float *)out, ld_out);
+                           n, (int)relu, (float *)out, ld_out, rw, part, n, tail_rows * n);
+        if (tail_rows > 0)
+            hipLaunchKernelGGL(k_tail_sum, dim3(grid_for(tail_rows * n, 256 * 8, 1024)), dim3(256), 0, s, part, n,
+                               tail_rows * n, rw * BM, m, m_dev, n, (int)relu, (float *)out, ld_out);
     } else if (out_bf16) {
         launch_ring<BM, BN, uint16_t, uint16_t>((const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m,
                                                 m_dev, k, g_wt.buf.as<uint16_t>(), 2 * kp, kp, 2, n, relu,
