@@ -16,6 +16,9 @@
 // registers hold staged data and the loads of later steps are in flight
 // while the current one is multiplied.  The split kernel uses the same ring.
 // bf16 output tiles leave through the idle ring as 16-byte row chunks.
+// Between one and 2.5 fp32 tiles per compute unit, the tiles past the
+// first 256 are split by segment over two workgroups and summed after
+// (k_tail_sum), so no unit runs two whole tiles.
 //
 // Skinny kernel (few output rows, e.g. the last layer over the seeds): a
 // workgroup owns 16 x 16 outputs; its 8 or 16 wavefronts take interleaved
