@@ -678,6 +678,21 @@ void launch_ring(const T *a0, int64_t lda0, const T *a1, int64_t lda1, int64_t m
 }
 }  // namespace
 
+// Row bands of 128 x 128 tiles taken whole when an fp32 combine splits its
+// tail tiles by segment (0: no split).  Between one and 2.5 tiles per
+// compute unit the first 256 tiles (as 8-band groups) stay whole and the
+// rest go to two workgroups each, one per segment, summed after by
+// k_tail_sum: the busiest unit holds 1.5 tiles' work instead of 2 up to 384
+// tiles.  Measured on MI355X (cold caches, 1204-deep k): 17000 rows 119 ->
+// 93 us, 20902 rows 124 -> 99 us, 28000 rows 144 -> 138 us, 40000 rows
+// 214 -> 175 us.  Below 128-deep segments the partial sums cost more than
+// the balance gains (40000 x 74 x 130: 44 -> 48 us).
+static int64_t tail_split_bands(int64_t m, int64_t n, int64_t k) {
+    const int64_t nrow = (m + 127) / 128, ncol = (n + 127) / 128, tiles = nrow * ncol, w8 = 256 / ncol / 8 * 8;
+    if (k < 128 || tiles <= 256 || tiles > 640 || w8 < 8 || w8 >= nrow) return 0;
+    return w8;
+}
+
 // fp32: the weights are split into three bf16 parts and transposed, then
 // k_combine_split runs; bf16: the weights are transposed and padded, then
 // the ring kernel runs.
@@ -690,16 +705,8 @@ static void launch_main(const void *self, int64_t ld_self, const void *agg, int6
     GNNAV_HIP(hipStreamWaitEvent(s, g_wt.last_use, 0));
     const int64_t kp = bf16 ? (k + 63) / 64 * 64 : (k + 31) / 32 * 32;
     const int64_t nrow = (m + BM - 1) / BM, ncol = (n + BN - 1) / BN, nrow8 = (nrow + 7) / 8 * 8;
-    // fp32, 128 x 128 tiles, between one and 2.5 tiles per compute unit: one
-    // whole tile for each of the first 256 (as 8-band groups), the tail
-    // bands' tiles split by segment over twice the workgroups, so the
-    // busiest unit holds 1.5 tiles' work instead of 2 (20902 x 1204 x 256:
-    // 124 -> 99 us including the partial sums)
-    int64_t rw = nrow8;
-    if (!bf16 && BM == 128) {
-        const int64_t w8 = 256 / ncol / 8 * 8, tiles = nrow * ncol;
-        if (tiles > 256 && tiles <= 640 && w8 >= 8 && w8 < nrow) rw = w8;
-    }
+    const int64_t split_bands = !bf16 && BM == 128 ? tail_split_bands(m, n, k) : 0;
+    const int64_t rw = split_bands > 0 ? split_bands : nrow8;
     const int64_t tail_rows = rw < nrow ? m - rw * BM : 0;
     const size_t wt_bytes = (size_t)(2 * kp * n * (bf16 ? 2 : 6)), part_off = (wt_bytes + 255) / 256 * 256;
     g_wt.buf.ensure(part_off + (size_t)(2 * tail_rows * n) * sizeof(float), s);
@@ -755,22 +762,31 @@ static int64_t busiest_cu_outputs(int64_t m, int64_t n, int64_t bm, int64_t bn) 
     return (tiles + 255) / 256 * bm * bn;
 }
 
+// Busiest compute unit's outputs under the tail split: one whole tile plus
+// its share of the half tiles.
+static int64_t busiest_cu_outputs_tail(int64_t m, int64_t n) {
+    const int64_t tiles = ((m + 127) / 128) * ((n + 127) / 128), halves = 2 * (tiles - 256);
+    return 128 * 128 * (2 + (halves + 255) / 256) / 2;
+}
+
 // Tile shapes measured on MI355X.  fp32 (split kernel): 128 x 128 or
 // 64 x 64, whichever loads the busiest compute unit less, counting a 64 x 64
 // output as 1/0.7 of its size (its per-output rate measured ~0.7 of the
-// larger tile's): e.g. 20902 x 1204 x 256 takes 128 x 128 (106 us), 6915 x
-// 256 x 256 and 40000 x 74 x 130 take 64 x 64.  bf16 (ring kernel): 128 x 64
+// larger tile's) and 128 x 128 with the tail split where it applies: e.g.
+// 17000 and 20902 x 1204 x 256 take 128 x 128, 6915 x 256 x 256 and 40000 x
+// 74 x 130 take 64 x 64.  bf16 (ring kernel): 128 x 64
 // tiles (64 x 64 for outputs at most 64 wide), 128 x 128 once there are
 // enough of those to give every compute unit two.
-static GemmChoice choose_main(int64_t m, int64_t d_out, bool bf16) {
+static GemmChoice choose_main(int64_t m, int64_t d_in, int64_t d_out, bool bf16) {
     if (bf16) {
         const bool big = d_out > 64 && ((m + 127) / 128) * ((d_out + 127) / 128) >= 512;
         if (big) return {128, 128, launch_main<128, 128>};
         if (d_out <= 64) return {64, 64, launch_main<64, 64>};
         return {128, 64, launch_main<128, 64>};
     }
-    if (d_out > 64 && 7 * busiest_cu_outputs(m, d_out, 128, 128) <= 10 * busiest_cu_outputs(m, d_out, 64, 64))
-        return {128, 128, launch_main<128, 128>};
+    const int64_t b128 = tail_split_bands(m, d_out, d_in) > 0 ? busiest_cu_outputs_tail(m, d_out)
+                                                               : busiest_cu_outputs(m, d_out, 128, 128);
+    if (d_out > 64 && 7 * b128 <= 10 * busiest_cu_outputs(m, d_out, 64, 64)) return {128, 128, launch_main<128, 128>};
     return {64, 64, launch_main<64, 64>};
 }
 
@@ -810,7 +826,7 @@ void launch_combine(const void *self, int64_t ld_self, const void *agg, int64_t 
         else
             run(std::integral_constant<int, 8>{});
     } else {
-        const GemmChoice ch = choose_main(m, d_out, bf16);
+        const GemmChoice ch = choose_main(m, d_in, d_out, bf16);
         ch.fn(self, ld_self, agg, ld_agg, m, m_dev, d_in, w, d_out, bf16, relu, out_bf16, out, ld_out, s, label);
     }
     GNNAV_HIP(hipGetLastError());
