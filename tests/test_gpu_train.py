@@ -131,8 +131,10 @@ def test_aggregate_mean_backward_many_sources(G):
 
 # ---------------------------------------------------------- weight grad
 
+# 2 * d_in * d_out not a multiple of 4 takes the reduce's one-element lanes:
+# (1, 3, 41) with one split, (3000, 3, 41) with 12, (40000, 5, 33) with 64.
 WGRAD_CASES = [(0, 8, 16), (1, 3, 41), (100, 100, 47), (5000, 602, 256), (20902, 602, 256), (95651, 100, 256),
-               (13042, 256, 256), (1024, 256, 41), (777, 130, 70)]
+               (13042, 256, 256), (1024, 256, 41), (777, 130, 70), (3000, 3, 41), (40000, 5, 33)]
 
 
 @pytest.mark.parametrize("m,d_in,d_out", WGRAD_CASES)
