@@ -522,10 +522,12 @@ void launch_wgrad(const float *x_self, int64_t ld_self, const float *agg, int64_
     if (!(a16(x_self, ld_self) && a16(agg, ld_agg) && a16(dz, ld_dz)))
         fail(GNNAV_E_INVALID, "weight gradient operands need 16-byte aligned rows");
     // 128 x 128 tiles (128 x 64 for outputs at most 64 wide); the row range
-    // is split so that about 512 workgroups run
+    // is split so that at most 512 workgroups run, two per compute unit all
+    // at once (rounding up left a few for a second round: 233k layer 1 with
+    // 20 tiles ran 520)
     const int64_t BA = 128, BO = d_out > 64 ? 128 : 64;
     const int64_t tiles = 2 * ((d_in + BA - 1) / BA) * ((d_out + BO - 1) / BO);
-    int64_t splits = (512 + tiles - 1) / tiles;
+    int64_t splits = 512 / tiles;
     splits = std::min<int64_t>(splits, std::max<int64_t>(1, (m + 255) / 256));
     splits = std::max<int64_t>(1, std::min<int64_t>(splits, 64));
     const int64_t total = 2 * d_in * d_out;
