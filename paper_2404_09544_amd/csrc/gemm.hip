@@ -469,17 +469,24 @@ __global__ void __launch_bounds__(256) k_combine_split(const float *__restrict__
 }
 
 // Tail bands of a split combine: C[r] = act(P[0][r - r0] + P[1][r - r0]) for
-// rows r0 <= r < M (M read on the device when m_dev is given).
+// rows r0 <= r < M (M read on the device when m_dev is given).  V = 4:
+// 16-byte lanes (N, ldp, pseg and ldc multiples of 4, P and C 16-byte
+// aligned).
+template <int V>
 __global__ void __launch_bounds__(256) k_tail_sum(const float *__restrict__ P, int64_t ldp, int64_t pseg, int64_t r0,
                                                   int64_t M, const int32_t *__restrict__ m_dev, int64_t N, int relu,
                                                   float *__restrict__ C, int64_t ldc) {
+    typedef float fv __attribute__((ext_vector_type(V)));
     if (m_dev) M = *m_dev;
-    const int64_t total = (M - r0) * N;
+    const int64_t nv = N / V, total = (M - r0) * nv;
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
-        const int64_t r = i / N, c = i - r * N;
-        float v = P[r * ldp + c] + P[pseg + r * ldp + c];
-        if (relu) v = fmaxf(v, 0.f);
-        C[(r0 + r) * ldc + c] = v;
+        const int64_t r = i / nv, c = (i - r * nv) * V;
+        fv v = *(const fv *)(P + r * ldp + c) + *(const fv *)(P + pseg + r * ldp + c);
+        if (relu) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) v[e] = fmaxf(v[e], 0.f);
+        }
+        *(fv *)(C + (r0 + r) * ldc + c) = v;
     }
 }
 
@@ -730,9 +737,14 @@ static void launch_main(const void *self, int64_t ld_self, const void *agg, int6
         hipLaunchKernelGGL((k_combine_split<float, BM, BN, WM>), grid, dim3(256), 0, s, (const float *)self, ld_self,
                            (const float *)agg, ld_agg, m, m_dev, k, g_wt.buf.as<uint16_t>(), 2 * kp, n * 2 * kp, kp, 2,
                            n, (int)relu, (float *)out, ld_out, rw, part, n, tail_rows * n);
-        if (tail_rows > 0)
-            hipLaunchKernelGGL(k_tail_sum, dim3(grid_for(tail_rows * n, 256 * 8, 1024)), dim3(256), 0, s, part, n,
-                               tail_rows * n, rw * BM, m, m_dev, n, (int)relu, (float *)out, ld_out);
+        if (tail_rows > 0) {
+            if (n % 4 == 0 && ld_out % 4 == 0 && ((uintptr_t)out & 15u) == 0)
+                hipLaunchKernelGGL(k_tail_sum<4>, dim3(grid_for(tail_rows * n / 4, 256 * 2, 1024)), dim3(256), 0, s,
+                                   part, n, tail_rows * n, rw * BM, m, m_dev, n, (int)relu, (float *)out, ld_out);
+            else
+                hipLaunchKernelGGL(k_tail_sum<1>, dim3(grid_for(tail_rows * n, 256 * 8, 1024)), dim3(256), 0, s,
+                                   part, n, tail_rows * n, rw * BM, m, m_dev, n, (int)relu, (float *)out, ld_out);
+        }
     } else if (out_bf16) {
         launch_ring<BM, BN, uint16_t, uint16_t>((const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m,
                                                 m_dev, k, g_wt.buf.as<uint16_t>(), 2 * kp, kp, 2, n, relu,
