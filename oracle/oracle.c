@@ -358,13 +358,16 @@ void oracle_gather(int64_t n, const uint8_t *features, int64_t row_bytes, const 
  * t_replace of Eq. 5).  Policy FIFO over a ring of slots
  * [ring_lo, ring_lo + ring_n): the batch's misses are admitted one by one
  * in request order; each takes the slot under the ring pointer, whose
- * previous vertex (if any) is evicted, and the pointer advances by one
- * (wrapping).  owner[slot] is the vertex in a slot or -1.                 */
+ * previous vertex (if any) is evicted -- unmapped if the slot map still
+ * points at this slot (a vertex requested twice in one batch is admitted
+ * twice; it keeps its later slot, and evicting the earlier copy must not
+ * unmap it) -- and the pointer advances by one (wrapping).  owner[slot] is
+ * the vertex in a slot or -1.                                             */
 void oracle_cache_fifo_admit(int32_t *slot_map, int32_t *owner, int64_t ring_lo, int64_t ring_n, int64_t *ptr,
                              const int32_t *misses, int64_t m) {
     for (int64_t i = 0; i < m; ++i) {
         int64_t s = ring_lo + *ptr;
-        if (owner[s] >= 0) slot_map[owner[s]] = -1;
+        if (owner[s] >= 0 && slot_map[owner[s]] == (int32_t)s) slot_map[owner[s]] = -1;
         owner[s] = misses[i];
         slot_map[misses[i]] = (int32_t)s;
         *ptr = (*ptr + 1) % ring_n;

@@ -511,6 +511,37 @@ def test_fifo_cache_matches_deque_model(r, frac):
     assert (cache.slot_map >= 0).sum() == c
 
 
+@pytest.mark.parametrize("r,frac", [(0.1, 1.0), (0.2, 0.5), (0.05, 0.1)])
+def test_fifo_cache_repeated_ids_match_deque_model(r, frac):
+    """Batches that request some vertices several times: each request that
+    misses is admitted, so a repeated vertex takes two ring slots; the vertex
+    stays cached while any of its copies is in the ring (the deque model's
+    set semantics), and every mapped vertex's slot holds that vertex."""
+    n, u, v = W.random_graph(n=500, m=4000, seed=33)
+    csr = O.build_csr(n, u, v)
+    rank, _, c = O.rank_cache(csr, r)
+    ring_n = max(1, int(c * frac))
+    rng = np.random.default_rng(8)
+    batches = []
+    for _ in range(10):
+        ids = rng.integers(0, n, 90).astype(np.int32)
+        ids[rng.integers(0, 90, 20)] = ids[rng.integers(0, 90, 20)]   # plant repeats
+        batches.append(ids)
+    assert any(np.unique(b).size < b.size for b in batches)
+    feats = W.features(n, 3, "f32", seed=4)
+    cache = O.FifoCache(csr, r, ring_n)
+    got = []
+    for ids in batches:
+        rows, counts = cache.gather(feats, ids)
+        got.append((int(counts[0]), int(counts[1])))
+        assert rows.tobytes() == feats[ids].tobytes()
+    hist, final = _deque_fifo(rank, c, ring_n, batches, n)
+    assert got == hist
+    assert {int(x) for x in np.nonzero(cache.slot_map >= 0)[0]} == final
+    for x in np.nonzero(cache.slot_map >= 0)[0]:
+        assert cache.owner[cache.slot_map[x]] == x
+
+
 def test_fifo_cache_repeat_batch_hits():
     """A batch of m <= ring uncached vertices is fully cached after one pass:
     repeating it right away hits every request."""
