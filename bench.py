@@ -6,10 +6,15 @@ HBM, misses from the pinned host store), and the L-layer SAGE forward
 (mean aggregation + combine GEMM).  Seeds for every batch are staged in HBM
 before the timed region; graph, cache and weights are built once.
 
-Prints one JSON line: seeds/s over the timed steps, a roofline entry for
-the dominant device kernel (algorithmic bytes or flops per launch over its
-average HIP-event duration, measured inside the timed region), per-kernel
-figures, and the CPU oracle timed on a bounded sample of the same batches.
+Prints one JSON line: seeds/s over the timed steps; a roofline entry for the
+kernel with the largest share of the step, whatever bounds it (host link,
+HBM or matrix cores), and one for the largest device-bound kernel (each the
+algorithmic bytes or flops of its launches over their HIP-event durations,
+measured inside the timed region); per-kernel figures, the sampling chain
+included; the same batches with every row cached (r = 1, where the gather
+is the HBM-bound hit copy alone); and the CPU oracle timed on a bounded
+sample of the same batches.  Every leg ends at a synchronisation point that
+fails the run if device-side work reported an error.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 """
@@ -57,7 +62,14 @@ def kernel_source_hash(files) -> str:
 
 KERNEL_SOURCES = {"aggregate_mean": ["spmm.hip", "common.hpp"],
                   "gather_rows": ["gather.hip", "common.hpp"],
-                  "combine_gemm": ["gemm.hip", "common.hpp", "dma.hpp", "bf16split.hpp"]}
+                  "cache_admit": ["gather.hip", "common.hpp"],
+                  "classify": ["gather.hip", "scan.hpp", "common.hpp"],
+                  "combine_gemm": ["gemm.hip", "common.hpp", "dma.hpp", "bf16split.hpp"],
+                  "sample_hop": ["sample.hip", "common.hpp"],
+                  "dedup_first": ["sample.hip", "common.hpp"],
+                  "dedup_scan": ["sample.hip", "scan.hpp", "common.hpp"],
+                  "count_scan": ["sample.hip", "scan.hpp", "common.hpp"],
+                  "relabel": ["sample.hip", "common.hpp"]}
 
 
 def cpu_model() -> str:
@@ -71,16 +83,22 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def traffic_for(kernel: str, workload: str):
-    """HBM bytes per launch from committed rocprofv3 counter runs, if still current."""
-    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
-    if not os.path.exists(path):
+def traffic_for(kernel: str, trace: str):
+    """Counted bytes per launch of `kernel` from the committed rocprofv3
+    counter runs of the run named `trace` (profiles/*_traffic.json), if they
+    were taken on the current kernel source; else None.  The record holds
+    bytes_per_launch (FETCH_SIZE and WRITE_SIZE scaled by a plain copy's
+    readings) and, where collected, the requests the L2 sent to the memory
+    side (dram_*) and to the host link (io_*), in bytes per launch."""
+    src = KERNEL_SOURCES.get(kernel.split(".")[0])
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{trace}_traffic.json")
+    if src is None or not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("source_hash") != kernel_source_hash(KERNEL_SOURCES[kernel.split(".")[0]]):
+    if rec.get("source_hash") != kernel_source_hash(src):
         return None
-    return rec.get("bytes_per_launch")
+    return rec
 
 
 def link_calibration(G, cache, wl, torch):
@@ -232,6 +250,7 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
     torch.cuda.synchronize()
     seq = time.perf_counter() - t0
     prof = G.profile_stop()
+    G.sync(stream)
     losses = loss_hist[args.warmup:].cpu().numpy()
     link_est = None
     if args.train_link_workgroups == "auto":
@@ -248,9 +267,10 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
     t0 = time.perf_counter()
     for b in range(args.warmup, n_b):
         pipe.enqueue_train(seeds_dev[b], wl.rng_seed(b), labels, args.lr)
-    pipe.synchronize()
+    pipe.synchronize()          # raises if device-side work reported a failure
     torch.cuda.synchronize()
     piped = time.perf_counter() - t0
+    G.sync()
     c.set_link_workgroups(64)
     log(f"train: sequential {seq * 1e3 / args.steps:.3f} ms/step, pipelined {piped * 1e3 / args.steps:.3f} ms/step, "
         f"loss {losses[0]:.4f} -> {losses[-1]:.4f}")
@@ -270,11 +290,14 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
         if name in work:
             tf = work[name] / (ms * 1e-3) / 1e12
             if name.startswith("wgrad.l"):
-                # the weight gradient runs on the bf16 matrix cores through the
-                # three-way bf16 split: six executed bf16 MFMA flops per fp32 flop
-                k.update({"bound": "mfma", "achieved": round(6 * tf, 2), "peak": MFMA_PEAK_TFLOPS["bf16"],
-                          "unit": "TFLOP/s", "frac": round(6 * tf / MFMA_PEAK_TFLOPS["bf16"], 4),
-                          "fp32_equivalent_tflops": round(tf, 2), "mfma_products_per_flop": 6})
+                # fp32 products computed on the bf16 matrix cores through the
+                # three-way bf16 split (six executed bf16 MFMA products per fp32
+                # product): the algorithmic rate against the fp32 peak, the
+                # executed bf16 work beside it
+                k.update({"bound": "mfma", "achieved": round(tf, 2), "peak": MFMA_PEAK_TFLOPS["f32"],
+                          "unit": "TFLOP/s", "frac": round(tf / MFMA_PEAK_TFLOPS["f32"], 4),
+                          "executed_bf16_tflops": round(6 * tf, 2),
+                          "executed_frac_of_bf16_peak": round(6 * tf / MFMA_PEAK_TFLOPS["bf16"], 4)})
             else:
                 k.update({"bound": "mfma", "achieved": round(tf, 2), "peak": MFMA_PEAK_TFLOPS["f32"],
                           "unit": "TFLOP/s", "frac": round(tf / MFMA_PEAK_TFLOPS["f32"], 4)})
@@ -286,6 +309,248 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
             "pipeline_link_workgroups": link_wgs, "link_workgroup_estimates_ms": link_est,
             "loss_first": round(float(losses[0]), 6), "loss_last": round(float(losses[-1]), 6),
             "kernels": kernels}
+
+
+SIZE_SLOTS = 24      # device size array: |F_h| at [h], E_h at [17 + h] (L <= 3 fits in 24)
+
+
+def sampling_bytes(wl, n_h, e_h, off_bytes: int) -> dict:
+    """Algorithmic bytes of one batch's sampling-chain kernels (Eq. 2 and its
+    union), by kernel label: each datum a kernel must read or write counted
+    once at its own width -- 4-byte ids and counts, `off_bytes` row offsets,
+    8-byte node-table entries (an atomic update counted as a read and a
+    write).  These kernels make 4- to 8-byte random accesses, so they are
+    bound by memory transactions, not by these bytes."""
+    L = wl.L
+    b0 = wl.batch
+    out = {"dedup_first": b0 * (4 + 16),
+           # the seeds' dedup with hop 1's counts: ids, table, F_0, row offsets, indptr_1
+           "dedup_scan": b0 * (4 + 8) + n_h[0] * (4 + 8 + 2 * off_bytes + 4) + 4,
+           "sample_hop": 0, "count_scan": 0, "relabel": 0}
+    for h in range(1, L + 1):
+        rows, e, new = n_h[h - 1], e_h[h], n_h[h] - n_h[h - 1]
+        # rows' ids, offsets and indptr; picked columns read, neighbours written, first positions noted
+        out["sample_hop"] += rows * (4 + 2 * off_bytes + 4) + e * (4 + 4 + 16)
+        out["dedup_scan"] += e * (4 + 8) + new * (4 + 8)
+        if h >= 2:   # this hop's counts plus hop h-1's relabel riding along
+            out["count_scan"] += rows * (4 + 2 * off_bytes) + (rows + 1) * 4 + e_h[h - 1] * (4 + 8 + 4)
+    out["relabel"] = e_h[L] * (4 + 8 + 4)
+    out["classify"] = n_h[L] * (4 + 4 + 8)
+    return out
+
+
+def forward_legs(args, G, g, c, wl, wdev, seeds_dev, torch, MiniBatchStep, Pipeline, link_override=None):
+    """The forward measurement on cache `c`: a sequential leg on one stream
+    with every kernel timed by HIP events (the per-kernel figures), then the
+    pipelined leg (the throughput).  Both end at a synchronisation point that
+    raises if device-side work reported a failure."""
+    L = wl.L
+    n_b = args.warmup + args.steps
+    step = MiniBatchStep(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, eta=args.eta)
+    counts_hist = torch.zeros((n_b, 3), dtype=torch.int64, device="cuda")
+    seq_counts_hist = torch.zeros((n_b, 3), dtype=torch.int64, device="cuda")
+    sizes_dev_hist = torch.zeros((n_b, SIZE_SLOTS), dtype=torch.int32, device="cuda")
+
+    def record(slot, b, st, hist):
+        """Copy this batch's counts and frontier/hop sizes aside on its own stream."""
+        ptr, _ = slot.blocks.device_sizes(L)
+        with torch.cuda.stream(st):
+            hist[b].copy_(slot.counts)
+            G._copy_device_i32(sizes_dev_hist[b], ptr, SIZE_SLOTS)
+
+    # ---- sequential steps on one stream, every kernel timed --------------
+    stream = torch.cuda.current_stream()
+    for b in range(args.warmup):
+        step.enqueue(seeds_dev[b], wl.rng_seed(b), stream)
+        record(step, b, stream, seq_counts_hist)
+    G.sync(stream)
+    G.profile_start()
+    torch.cuda.synchronize()
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    t_start = time.perf_counter()
+    marks[0].record(stream)
+    for b in range(args.warmup, n_b):
+        step.enqueue(seeds_dev[b], wl.rng_seed(b), stream)
+        record(step, b, stream, seq_counts_hist)
+        marks[b - args.warmup + 1].record(stream)
+    torch.cuda.synchronize()
+    t_end = time.perf_counter()
+    prof = G.profile_stop()
+    G.sync(stream)
+    prof_samples = G.profile_samples()
+    batch_ms = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)])
+    seq_elapsed = t_end - t_start
+    seq_ms = seq_elapsed * 1e3 / args.steps
+    log(f"r={c.n_cached / max(wl.n, 1):.3g} sequential {args.steps} steps: {seq_ms:.3f} ms/step, "
+        f"{wl.batch * args.steps / seq_elapsed:,.0f} seeds/s")
+    sizes_all = sizes_dev_hist[args.warmup:].cpu().numpy()
+
+    # ---- the pipeline (batch b+1 overlaps batch b on another stream) -----
+    link_est = None
+    if link_override is not None:
+        link_wgs = link_override
+    elif args.link_workgroups == "auto":
+        t_tr = prof.get("gather_rows", (0, 0.0))[1] / args.steps
+        link_wgs, link_est = pick_link_workgroups(t_tr, seq_ms - t_tr)
+    else:
+        link_wgs = int(args.link_workgroups)
+    pipe = Pipeline(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, depth=args.depth, eta=args.eta,
+                    link_workgroups=link_wgs)
+    for b in range(args.warmup):
+        pipe.enqueue(seeds_dev[b], wl.rng_seed(b))
+    pipe.synchronize()
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for b in range(args.warmup, n_b):
+        slot = pipe.enqueue(seeds_dev[b], wl.rng_seed(b))
+        record(slot, b, pipe.streams[(pipe.count - 1) % pipe.depth], counts_hist)
+    pipe.synchronize()          # raises if device-side work reported a failure
+    torch.cuda.synchronize()
+    t_end = time.perf_counter()
+    G.sync()
+    c.set_link_workgroups(64)
+    elapsed = t_end - t_start
+    log(f"r={c.n_cached / max(wl.n, 1):.3g} pipelined {args.steps} steps: {elapsed * 1e3 / args.steps:.3f} ms/step, "
+        f"{wl.batch * args.steps / elapsed:,.0f} seeds/s")
+    piped_sizes = sizes_dev_hist[args.warmup:].cpu().numpy()
+    assert np.array_equal(piped_sizes[:, :L + 1], sizes_all[:, :L + 1]), "pipelined batches differ in size"
+    return {"prof": prof, "prof_samples": prof_samples, "batch_ms": batch_ms, "seq_elapsed": seq_elapsed,
+            "seq_ms": seq_ms, "elapsed": elapsed, "ms_per_step": elapsed * 1e3 / args.steps,
+            "counts": counts_hist[args.warmup:].cpu().numpy(),
+            "seq_counts": seq_counts_hist[args.warmup:].cpu().numpy(),
+            "n_h": sizes_all[:, :L + 1].astype(np.int64), "e_h": sizes_all[:, 17:17 + L + 1].astype(np.int64),
+            "link_workgroups": link_wgs, "link_est": link_est}
+
+
+def kernel_entries(args, G, g, wl, fwd, seeds_dev, ring, link, profiled_config, trace_name):
+    """Per-kernel figures of a sequential leg: each kernel's algorithmic work
+    over the timed batches (from their measured sizes) divided by its total
+    HIP-event time, against the roofline that bounds it."""
+    L = wl.L
+    prof, prof_samples = fwd["prof"], fwd["prof_samples"]
+    elt = 2 if wl.dtype == "bf16" else 4
+    off = 8 if g.offsets_i64 else 4
+    # gather_rows moves hits (HBM) and misses (host link) in one launch: it is
+    # host-link bound when there are misses, HBM bound otherwise
+    work = {"gather_rows": 0.0, "cache_admit": 0.0}
+    hit_bytes = miss_bytes = 0.0
+    edge, gemm_bytes, samp = {}, {}, {}
+    probe = G.Blocks()
+    for i, b in enumerate(range(args.warmup, args.warmup + args.steps)):
+        n_h, e_h = fwd["n_h"][i], fwd["e_h"][i]
+        hits, misses = int(fwd["seq_counts"][i][0]), int(fwd["seq_counts"][i][1])
+        hit_bytes += hits * (2 * wl.d * elt + 8)
+        miss_bytes += misses * wl.d * elt
+        work["cache_admit"] += min(misses, ring) * (2 * wl.d * elt + 16)
+        for k, v in sampling_bytes(wl, n_h, e_h, off).items():
+            samp[k] = samp.get(k, 0.0) + v
+        # re-sampling a batch is deterministic: regenerate its blocks (untimed)
+        # to count the distinct source rows of each aggregation
+        G.sample(g, seeds_dev[b], wl.fanouts, wl.rng_seed(b), probe)
+        _, sz, ip, _, ix = probe.to_host()
+        assert sz == [int(x) for x in n_h], "re-sampled batch differs"
+        for l in range(1, L + 1):
+            hb = L - l + 1
+            n_dst, E = int(n_h[hb - 1]), int(ip[hb - 1][-1])
+            u = np.unique(ix[hb - 1]).size
+            din, dout = wl.dims[l - 1], wl.dims[l]
+            ka, kg = f"aggregate_mean.l{l}", f"combine_gemm.l{l}"
+            # compulsory bytes: each distinct source row once, each output row once, the CSR
+            work[ka] = work.get(ka, 0.0) + u * din * elt + n_dst * din * elt + 4 * (E + n_dst + 1)
+            edge[ka] = edge.get(ka, 0.0) + E * din * elt + n_dst * din * elt + 4 * (E + n_dst + 1)
+            work[kg] = work.get(kg, 0.0) + 2.0 * n_dst * (2 * din) * dout
+            out_elt = elt if l < L else 4
+            gemm_bytes[kg] = gemm_bytes.get(kg, 0.0) + (n_dst * 2 * din + 2 * din * dout) * elt + n_dst * dout * out_elt
+    probe.close()
+    work.update(samp)
+    gemm_kind = {}
+    for l in range(1, L + 1):
+        m_mean = max(1, int(round(float(np.mean(fwd["n_h"][:, L - l])))))
+        gemm_kind[f"combine_gemm.l{l}"] = G.combine_kernel(m_mean, wl.dims[l], wl.dtype)
+    link_bound = miss_bytes > 0
+    work["gather_rows"] = miss_bytes if link_bound else hit_bytes
+
+    kernels = {}
+    for name, (launches, ms) in prof.items():
+        kernels[name] = {"launches": launches, "total_ms": round(ms, 4),
+                         "avg_us": round(ms * 1e3 / max(launches, 1), 3)}
+        smp = prof_samples.get(name)
+        if smp is not None and smp.size:
+            q = np.percentile(smp.astype(np.float64) * 1e3, [10, 50, 90])
+            kernels[name].update({"p10_us": round(q[0], 3), "median_us": round(q[1], 3), "p90_us": round(q[2], 3)})
+    rows = []
+    for name in work:
+        if name not in prof or work[name] <= 0:
+            continue
+        launches, ms = prof[name]
+        split = gemm_kind.get(name) == "split"
+        if name == "gather_rows" and link_bound:
+            bound, peak, unit, amount = "host_link", HOST_LINK_PEAK_GBS, "GB/s", work[name]
+        elif name.startswith("combine_gemm"):
+            # the algorithmic flops (2*M*K*N) against the peak of the precision
+            # the result carries (the split kernel computes fp32 products on
+            # the bf16 matrix cores; its executed bf16 work is a side figure);
+            # HBM-bound below the ridge point of that peak
+            ridge = MFMA_PEAK_TFLOPS[wl.dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
+            if work[name] / max(gemm_bytes.get(name, 1.0), 1.0) >= ridge:
+                bound, peak, unit, amount = "mfma", MFMA_PEAK_TFLOPS[wl.dtype], "TFLOP/s", work[name]
+            else:
+                bound, peak, unit, amount = "hbm", HBM_PEAK_GBS, "GB/s", gemm_bytes[name]
+        else:
+            bound, peak, unit, amount = "hbm", HBM_PEAK_GBS, "GB/s", work[name]
+        achieved = amount / (ms * 1e-3) / (1e12 if unit == "TFLOP/s" else 1e9)
+        ent = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+               "frac": round(achieved / peak, 4), "per_launch": round(amount / max(launches, 1), 1)}
+        if name in edge:
+            ent["achieved_edge_effective"] = round(edge[name] / (ms * 1e-3) / 1e9, 2)
+        if name in samp:
+            ent["note"] = "4-8 byte random accesses: transaction-bound"
+        rec = traffic_for(name, trace_name) if profiled_config else None
+        if rec:
+            counted = rec.get("bytes_per_launch")
+            byte_work = gemm_bytes.get(name) if name.startswith("combine_gemm") else (
+                hit_bytes if name == "gather_rows" else work[name])
+            ent["counted_bytes_per_launch"] = counted
+            ent["counted_gbs"] = round(counted * launches / (ms * 1e-3) / 1e9, 2)
+            if byte_work and not (name == "gather_rows" and link_bound):
+                ent["useful_byte_efficiency"] = round(byte_work / max(launches, 1) / counted, 4)
+            for key in ("dram_read_bytes_per_launch", "dram_write_bytes_per_launch", "io_read_bytes_per_launch"):
+                if rec.get(key) is not None:
+                    ent[key] = rec[key]
+            if rec.get("io_read_bytes_per_launch"):
+                ent["io_read_gbs_counted"] = round(rec["io_read_bytes_per_launch"] * launches / (ms * 1e-3) / 1e9, 2)
+        if name.startswith("combine_gemm"):
+            ent["kernel"] = gemm_kind.get(name)
+            ent["tflops"] = round(work[name] / (ms * 1e-3) / 1e12, 2)
+            ent["flop_per_byte"] = round(work[name] / max(gemm_bytes.get(name, 1.0), 1.0), 1)
+            if split:
+                ex = 6 * work[name] / (ms * 1e-3) / 1e12
+                ent["method"] = "fp32 products as six bf16 part products on the bf16 matrix cores"
+                ent["executed_bf16_tflops"] = round(ex, 2)
+                ent["executed_frac_of_bf16_peak"] = round(ex / MFMA_PEAK_TFLOPS["bf16"], 4)
+        if name == "gather_rows":
+            ent["hit_bytes_per_launch"] = round(hit_bytes / max(launches, 1), 1)
+            if link_bound:
+                if link.get("zero_copy_gather_gbs"):
+                    ent["frac_of_measured_link"] = round(achieved / link["zero_copy_gather_gbs"], 4)
+                ent["hit_hbm_gbs_alongside"] = round(hit_bytes / (ms * 1e-3) / 1e9, 2)
+        kernels[name].update(ent)
+        rows.append((ms, name))
+    return kernels, rows, {"hit_bytes": hit_bytes, "miss_bytes": miss_bytes, "link_bound": link_bound,
+                           "gemm_kind": gemm_kind}
+
+
+def roofline_of(kernels, name, trace_name, profiled_config):
+    k = kernels[name]
+    rec = traffic_for(name, trace_name) if profiled_config else None
+    out = {"kernel": name, "bound": k["bound"], "achieved": k["achieved"], "peak": k["peak"], "unit": k["unit"],
+           "frac": k["frac"], "traffic": rec.get("bytes_per_launch") if rec else None}
+    for key in ("method", "executed_bf16_tflops", "executed_frac_of_bf16_peak", "frac_of_measured_link",
+                "hit_bytes_per_launch", "useful_byte_efficiency", "io_read_bytes_per_launch",
+                "io_read_gbs_counted", "dram_read_bytes_per_launch", "dram_write_bytes_per_launch"):
+        if key in k:
+            out[key] = k[key]
+    return out
 
 
 def main():
@@ -312,6 +577,8 @@ def main():
     ap.add_argument("--eta", type=int, default=None,
                     help="locality-biased sampling: cached neighbours weigh eta (default: uniform)")
     ap.add_argument("--no-train", action="store_true", help="skip the training leg")
+    ap.add_argument("--no-r1", action="store_true",
+                    help="skip the extra forward leg with every row cached (r = 1: the hit gather alone)")
     ap.add_argument("--lr", type=float, default=0.01, help="SGD step of the training leg")
     ap.add_argument("--link-workgroups", default="auto",
                     help="host-link workgroups of the pipelined forward leg's gathers: a count, or auto "
@@ -369,206 +636,53 @@ def main():
         log(f"FIFO ring over the last {ring} of {c.n_cached} cache slots")
     ws = wl.weights()
     wdev = to_device_weights(ws, wl.dtype)
-    step = MiniBatchStep(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, eta=args.eta)
     n_b = args.warmup + args.steps
     seeds_dev = [torch.from_numpy(wl.seeds(b)).cuda() for b in range(n_b)]
     L = wl.L
-    counts_hist = torch.zeros((n_b, 3), dtype=torch.int64, device="cuda")
-    seq_counts_hist = torch.zeros((n_b, 3), dtype=torch.int64, device="cuda")
-    sizes_dev_hist = torch.zeros((n_b, L + 1), dtype=torch.int32, device="cuda")
 
-    def record(slot, b, st, hist=counts_hist):
-        """Copy this batch's counts and frontier sizes aside on its own stream."""
-        ptr, _ = slot.blocks.device_sizes(L)
-        with torch.cuda.stream(st):
-            hist[b].copy_(slot.counts)
-            G._copy_device_i32(sizes_dev_hist[b], ptr, L + 1)
-
-    # ---- phase 1: sequential steps on one stream, every kernel timed -----
-    # One batch after another with no host synchronisation between batches;
-    # the library records HIP events around each kernel (per-kernel figures
-    # and the roofline come from this region).
-    stream = torch.cuda.current_stream()
-    for b in range(args.warmup):
-        step.enqueue(seeds_dev[b], wl.rng_seed(b), stream)
-        record(step, b, stream, seq_counts_hist)
-    torch.cuda.synchronize()
-    G.profile_start()
-    torch.cuda.synchronize()
-    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    t_start = time.perf_counter()
-    marks[0].record(stream)
-    for b in range(args.warmup, n_b):
-        step.enqueue(seeds_dev[b], wl.rng_seed(b), stream)
-        record(step, b, stream, seq_counts_hist)
-        marks[b - args.warmup + 1].record(stream)
-    torch.cuda.synchronize()
-    t_end = time.perf_counter()
-    prof = G.profile_stop()
-    prof_samples = G.profile_samples()
-    batch_ms = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)])
-    seq_elapsed = t_end - t_start
-    seq_ms = seq_elapsed * 1e3 / args.steps
-    log(f"sequential {args.steps} steps: {seq_ms:.3f} ms/step, {wl.batch * args.steps / seq_elapsed:,.0f} seeds/s")
-
-    # ---- phase 2: the pipeline (batch b+1 overlaps batch b on another stream)
-    fwd_link_est = None
-    if args.link_workgroups == "auto":
-        t_tr = prof.get("gather_rows", (0, 0.0))[1] / args.steps
-        fwd_link, fwd_link_est = pick_link_workgroups(t_tr, seq_ms - t_tr)
-    else:
-        fwd_link = int(args.link_workgroups)
-    pipe = Pipeline(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, depth=args.depth, eta=args.eta,
-                    link_workgroups=fwd_link)
-    for b in range(args.warmup):
-        slot = pipe.enqueue(seeds_dev[b], wl.rng_seed(b))
-    pipe.synchronize()
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for b in range(args.warmup, n_b):
-        slot = pipe.enqueue(seeds_dev[b], wl.rng_seed(b))
-        record(slot, b, pipe.streams[(pipe.count - 1) % pipe.depth])
-    pipe.synchronize()
-    torch.cuda.synchronize()
-    t_end = time.perf_counter()
-    c.set_link_workgroups(64)
-    elapsed = t_end - t_start
-    ms_per_step = elapsed * 1e3 / args.steps
-    seeds_per_s = wl.batch * args.steps / elapsed
-    counts = counts_hist[args.warmup:].cpu().numpy()
-    seq_counts = seq_counts_hist[args.warmup:].cpu().numpy()
-    sizes_hist = sizes_dev_hist[args.warmup:].cpu().numpy().tolist()
-    log(f"pipelined {args.steps} steps: {ms_per_step:.3f} ms/step, {seeds_per_s:,.0f} seeds/s")
-
-    # ---- algorithmic work per timed batch, from the measured sizes -------
-    # Re-sampling a batch is deterministic, so the blocks of each timed batch
-    # are regenerated here (untimed) to count distinct source rows.
-    elt = 2 if wl.dtype == "bf16" else 4
-    # (the per-kernel figures come from the sequential region, so its counts)
-    # gather_rows moves hits (HBM) and misses (host link) in one launch: it is
-    # host-link bound when there are misses, HBM bound otherwise
-    work = {"gather_rows": 0.0, "cache_admit": 0.0}
-    hit_bytes = miss_bytes = 0.0
-    edge = {}
-    gemm_bytes = {}
-    probe = G.Blocks()
-    for i, b in enumerate(range(args.warmup, n_b)):
-        sz = sizes_hist[i]
-        hits, misses = int(seq_counts[i][0]), int(seq_counts[i][1])
-        hit_bytes += hits * (2 * wl.d * elt + 8)
-        miss_bytes += misses * wl.d * elt
-        # admitted rows: read from the gathered batch, written to the cache, plus owner/slot-map entries
-        work["cache_admit"] += min(misses, ring) * (2 * wl.d * elt + 16)
-        G.sample(g, seeds_dev[b], wl.fanouts, wl.rng_seed(b), probe)
-        _, _, ip, _, ix = probe.to_host()
-        for l in range(1, L + 1):
-            hb = L - l + 1
-            n_dst, E = sz[hb - 1], int(ip[hb - 1][-1])
-            u = np.unique(ix[hb - 1]).size
-            din, dout = wl.dims[l - 1], wl.dims[l]
-            ka, kg = f"aggregate_mean.l{l}", f"combine_gemm.l{l}"
-            # compulsory bytes: each distinct source row once, each output row once, the CSR
-            work[ka] = work.get(ka, 0.0) + u * din * elt + n_dst * din * elt + 4 * (E + n_dst + 1)
-            edge[ka] = edge.get(ka, 0.0) + E * din * elt + n_dst * din * elt + 4 * (E + n_dst + 1)
-            work[kg] = work.get(kg, 0.0) + 2.0 * n_dst * (2 * din) * dout
-            # the GEMM's compulsory bytes: both A segments, W, the output (hidden
-            # layers in the compute dtype, logits in fp32)
-            out_elt = elt if l < L else 4
-            gemm_bytes[kg] = gemm_bytes.get(kg, 0.0) + (n_dst * 2 * din + 2 * din * dout) * elt + n_dst * dout * out_elt
-    probe.close()
-    # which combine kernel each layer ran: the split-bf16 kernel executes six
-    # bf16 MFMA products per fp32 product, so its roofline is the bf16 peak
-    # over the executed flops (the fp32-equivalent rate is reported beside it)
-    gemm_kind = {}
-    for l in range(1, L + 1):
-        m_mean = max(1, int(round(float(np.mean([sz[L - l] for sz in sizes_hist])))))
-        gemm_kind[f"combine_gemm.l{l}"] = G.combine_kernel(m_mean, wl.dims[l], wl.dtype)
-    link_bound = miss_bytes > 0
-    work["gather_rows"] = miss_bytes if link_bound else hit_bytes
-    # the committed counter runs used the workload's default cache, a static
-    # policy and uniform sampling: their bytes apply only to such runs
-    profiled_config = ((args.cache_fraction is None or args.cache_fraction == wl.cfg["cache"])
-                       and args.eta is None and args.cache_policy == "static")
-
-    kernels = {}
-    for name, (launches, ms) in prof.items():
-        kernels[name] = {"launches": launches, "total_ms": round(ms, 4),
-                         "avg_us": round(ms * 1e3 / max(launches, 1), 3)}
-        smp = prof_samples.get(name)
-        if smp is not None and smp.size:
-            q = np.percentile(smp.astype(np.float64) * 1e3, [10, 50, 90])
-            kernels[name].update({"p10_us": round(q[0], 3), "median_us": round(q[1], 3), "p90_us": round(q[2], 3)})
-    rows = []
-    for name in work:
-        if name not in prof:
-            continue
-        if name == "gather_rows" and link_bound:
-            bound, peak, unit = "host_link", HOST_LINK_PEAK_GBS, "GB/s"
-        elif name.startswith("combine_gemm"):
-            # MFMA-bound when its executed flops per compulsory byte exceed
-            # the ridge point peak_flops / HBM bandwidth, else HBM-bound
-            split = gemm_kind.get(name) == "split"
-            mfma_dtype = "bf16" if split else wl.dtype
-            executed = work[name] * (6 if split else 1)
-            ridge = MFMA_PEAK_TFLOPS[mfma_dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
-            if executed / max(gemm_bytes.get(name, 1.0), 1.0) >= ridge:
-                bound, peak, unit = "mfma", MFMA_PEAK_TFLOPS[mfma_dtype], "TFLOP/s"
-            else:
-                bound, peak, unit = "hbm", HBM_PEAK_GBS, "GB/s"
-        else:
-            bound, peak, unit = "hbm", HBM_PEAK_GBS, "GB/s"
-        launches, ms = prof[name]
-        amount = work[name]
-        if name.startswith("combine_gemm"):
-            amount = gemm_bytes[name] if bound == "hbm" else work[name] * (6 if gemm_kind.get(name) == "split" else 1)
-        achieved = amount / (ms * 1e-3) / (1e12 if unit == "TFLOP/s" else 1e9)
-        ent = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-               "frac": round(achieved / peak, 4), "per_launch": round(amount / max(launches, 1), 1)}
-        if name in edge:
-            ent["achieved_edge_effective"] = round(edge[name] / (ms * 1e-3) / 1e9, 2)
-        counted = traffic_for(name, wl.name) if profiled_config else None
-        if counted:
-            # rocprofv3-counted HBM bytes per launch (committed summary, same
-            # kernel source): the counted rate, and compulsory / counted bytes
-            byte_work = gemm_bytes.get(name) if name.startswith("combine_gemm") else (
-                hit_bytes if name == "gather_rows" else work[name])
-            ent["counted_bytes_per_launch"] = counted
-            ent["counted_gbs"] = round(counted * launches / (ms * 1e-3) / 1e9, 2)
-            if byte_work and not (name == "gather_rows" and link_bound):
-                ent["useful_byte_efficiency"] = round(byte_work / max(launches, 1) / counted, 4)
-        if name.startswith("combine_gemm"):
-            ent["kernel"] = gemm_kind.get(name)
-            ent["tflops"] = round(work[name] / (ms * 1e-3) / 1e12, 2)   # algorithmic (fp32-equivalent) rate
-            ent["flop_per_byte"] = round(work[name] / max(gemm_bytes.get(name, 1.0), 1.0), 1)
-            if gemm_kind.get(name) == "split":
-                ent["mfma_products_per_flop"] = 6
-        if name == "gather_rows" and link_bound:
-            if link.get("zero_copy_gather_gbs"):
-                ent["frac_of_measured_link"] = round(achieved / link["zero_copy_gather_gbs"], 4)
-            # the hit rows move in the same launch, alongside the misses
-            ent["hit_bytes_per_launch"] = round(hit_bytes / max(launches, 1), 1)
-            ent["hit_hbm_gbs_alongside"] = round(hit_bytes / (ms * 1e-3) / 1e9, 2)
-        kernels[name].update(ent)
-        rows.append((ms, name))
+    # ---- the forward step at the workload's cache fraction (the headline) --
+    fwd = forward_legs(args, G, g, c, wl, wdev, seeds_dev, torch, MiniBatchStep, Pipeline)
+    prof = fwd["prof"]
+    # counter runs are committed per workload and cache fraction, with a
+    # static cache and uniform sampling: their bytes apply only to such runs
+    profiled_config = args.eta is None and args.cache_policy == "static"
+    trace_name = wl.name if r == wl.cfg["cache"] else f"{wl.name}_r{r:g}"
+    kernels, rows, fstats = kernel_entries(args, G, g, wl, fwd, seeds_dev, ring, link, profiled_config, trace_name)
+    # the roofline entry: the kernel with the largest total time in the timed
+    # sequential leg, whatever bounds it (the host link, HBM or the matrix
+    # cores); the largest device-bound (HBM or MFMA) kernel is given beside it
+    dom = max(rows)[1] if rows else None
+    roofline = roofline_of(kernels, dom, trace_name, profiled_config) if dom else None
     device_rows = [(ms, n) for ms, n in rows if kernels[n]["bound"] in ("hbm", "mfma")]
-    dom = max(device_rows)[1] if device_rows else None
-    roofline = None
-    if dom:
-        k = kernels[dom]
-        roofline = {"kernel": dom, "bound": k["bound"], "achieved": k["achieved"], "peak": k["peak"],
-                    "unit": k["unit"], "frac": k["frac"],
-                    "traffic": traffic_for(dom, wl.name) if profiled_config else None}
-        if dom.startswith("combine_gemm") and k.get("kernel") == "split":
-            roofline["method"] = "fp32 through a three-way bf16 split: 6 bf16 MFMA products per fp32 product"
-            roofline["fp32_equivalent_tflops"] = k["tflops"]
-            # context: the same fp32 work against the fp32 matrix-core peak
-            roofline["fp32_equivalent_frac_of_f32_peak"] = round(k["tflops"] / MFMA_PEAK_TFLOPS["f32"], 4)
+    dom_dev = max(device_rows)[1] if device_rows else None
+    roofline_device = roofline_of(kernels, dom_dev, trace_name, profiled_config) if dom_dev else None
 
-    m1 = int(round(float(np.mean([sz[L - 1] for sz in sizes_hist])))) if sizes_hist else 0
+    m1 = int(round(float(np.mean(fwd["n_h"][:, L - 1])))) if args.steps else 0
     device_cal = device_calibration(torch, m1, 2 * wl.dims[0], wl.dims[1], wl.dtype)
-    if roofline is not None and roofline["kernel"] == "combine_gemm.l1" and device_cal.get("library_gemm"):
-        roofline["library_frac_same_shape"] = device_cal["library_gemm"]["frac"]
-        roofline["library_tflops_same_shape"] = device_cal["library_gemm"]["tflops"]
+    for rl in (roofline, roofline_device):
+        if rl is not None and rl["kernel"] == "combine_gemm.l1" and device_cal.get("library_gemm"):
+            rl["library_frac_same_shape"] = device_cal["library_gemm"]["frac"]
+            rl["library_tflops_same_shape"] = device_cal["library_gemm"]["tflops"]
+
+    # ---- the same batches with every row cached: the hit gather alone ----
+    r1 = None
+    if not args.no_r1 and r < 1.0 and args.cache_policy == "static" and not wl.cfg["store_on_device"]:
+        t0 = time.perf_counter()
+        c1 = G.Cache(g, feats, wl.dtype, 1.0)
+        log(f"cache r=1: C={c1.n_cached} ({time.perf_counter() - t0:.1f}s)")
+        f1 = forward_legs(args, G, g, c1, wl, wdev, seeds_dev, torch, MiniBatchStep, Pipeline, link_override=64)
+        k1, rows1, _ = kernel_entries(args, G, g, wl, f1, seeds_dev, 0, link, args.eta is None,
+                                      f"{wl.name}_r1")
+        r1 = {"cache_fraction": 1.0, "value": round(wl.batch * args.steps / f1["elapsed"], 2), "unit": "seeds/s",
+              "ms_per_step": round(f1["ms_per_step"], 4),
+              "value_sequential": round(wl.batch * args.steps / f1["seq_elapsed"], 2),
+              "roofline_gather": roofline_of(k1, "gather_rows", f"{wl.name}_r1", args.eta is None)
+              if "gather_rows" in k1 and k1["gather_rows"].get("bound") else None,
+              "roofline": roofline_of(k1, max(rows1)[1], f"{wl.name}_r1", args.eta is None) if rows1 else None,
+              "kernels": k1}
+        c1.close()
+        if r1["roofline_gather"]:
+            log(f"r=1 gather: {r1['roofline_gather']['achieved']} GB/s = {r1['roofline_gather']['frac']} of HBM")
 
     # ---- locality-biased sampling: hit rate against the shift it causes --
     locality = None
@@ -577,6 +691,7 @@ def main():
 
     # ---- training leg: sample + gather + forward + loss + backward + SGD ----
     train = None
+    sizes_hist = fwd["n_h"].tolist()
     if not args.no_train and wl.dtype == "f32":
         train = train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_weights, MiniBatchStep,
                           Pipeline)
@@ -638,35 +753,43 @@ def main():
         return sum(prof[n][1] for n in names if n in prof) / args.steps
     samp = ["dedup_first", "dedup_scan", "count_scan", "sample_hop", "relabel"]
     comp = [n for n in prof if n.startswith(("aggregate_mean", "combine_gemm"))] + ["classify", "weights_transpose"]
-    repl = ["cache_evict", "cache_admit", "cache_advance"]
+    repl = ["cache_evict", "cache_admit", "cache_map", "cache_advance"]
     eq4 = {"t_sample_ms": round(per_batch(samp), 4), "t_transfer_ms": round(per_batch(["gather_rows"]), 4),
            "t_replace_ms": round(per_batch(repl), 4),
-           "t_compute_ms": round(per_batch(comp), 4), "sequential_ms_per_step": round(seq_ms, 4),
-           "pipelined_ms_per_step": round(ms_per_step, 4)}
+           "t_compute_ms": round(per_batch(comp), 4), "sequential_ms_per_step": round(fwd["seq_ms"], 4),
+           "pipelined_ms_per_step": round(fwd["ms_per_step"], 4)}
     eq4["eq4_max_ms"] = round(max(eq4["t_sample_ms"] + eq4["t_transfer_ms"],
                                   eq4["t_replace_ms"] + eq4["t_compute_ms"]), 4)
-    mean_sizes = np.mean(np.array(sizes_hist), axis=0).round(1).tolist()
+    counts, seq_counts = fwd["counts"], fwd["seq_counts"]
+    mean_sizes = np.mean(fwd["n_h"], axis=0).round(1).tolist()
+    mean_edges = np.mean(fwd["e_h"][:, 1:], axis=0).round(1).tolist()
     hit_rate = float(counts[:, 0].sum() / max(counts[:, :2].sum(), 1))
+    elt = 2 if wl.dtype == "bf16" else 4
+    seeds_per_s = wl.batch * args.steps / fwd["elapsed"]
+    batch_ms = fwd["batch_ms"]
     out = {
         "metric": METRIC, "value": round(seeds_per_s, 2), "unit": "seeds/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(fwd["ms_per_step"], 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
         "data": "synthetic",
         "config": {"workload": wl.name,
                    "seeds": {"graph": W.GRAPH_SEED, "features": W.FEAT_SEED, "permutation": W.PERM_SEED,
                              "weights": W.WEIGHT_SEED, "labels": W.LABEL_SEED,
                              "sampler_batch_b": f"({W.RNG_BASE} << 32) | b"},
-                   "pipeline_streams": args.depth, "link_workgroups": fwd_link, "link_workgroup_estimates_ms": fwd_link_est,
+                   "pipeline_streams": args.depth, "link_workgroups": fwd["link_workgroups"],
+                   "link_workgroup_estimates_ms": fwd["link_est"],
                    "n": wl.n, "nnz": g.nnz, "d": wl.d, "fanouts": wl.fanouts,
                    "batch": wl.batch, "layers": wl.L, "dims": wl.dims, "cache_fraction": r,
                    "store_on_device": wl.cfg["store_on_device"], "cache_policy": args.cache_policy,
                    "sampler": "uniform" if args.eta is None else f"locality-biased eta={args.eta}",
                    "fifo_slots": ring, "global_batch": wl.batch},
-        "value_sequential": round(wl.batch * args.steps / seq_elapsed, 2),
+        "value_sequential": round(wl.batch * args.steps / fwd["seq_elapsed"], 2),
         "roofline": roofline,
+        "roofline_device": roofline_device,
         "cpu_baseline": cpu,
         "cpu_baseline_all_cores": cpu_all,
         "kernels": kernels,
+        "r1": r1,
         "eq4": eq4,
         "locality": locality,
         "train": train,
@@ -676,10 +799,12 @@ def main():
         "sequential_batch_ms": {"median": round(float(np.median(batch_ms)), 4),
                                 "p10": round(float(np.percentile(batch_ms, 10)), 4),
                                 "p90": round(float(np.percentile(batch_ms, 90)), 4)},
-        "batch_stats": {"mean_frontier_sizes": mean_sizes, "hit_rate": round(hit_rate, 4),
+        "batch_stats": {"mean_frontier_sizes": mean_sizes, "mean_edges_per_hop": mean_edges,
+                        "hit_rate": round(hit_rate, 4),
                         "hit_rate_sequential": round(float(seq_counts[:, 0].sum() / max(seq_counts[:, :2].sum(), 1)), 4),
                         "miss_bytes_per_batch": round(float(counts[:, 1].mean()) * wl.d * elt, 1)},
     }
+    G.sync()
     print(json.dumps(out), flush=True)
 
 

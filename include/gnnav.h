@@ -23,7 +23,14 @@
  *     multiple of 16 and the base pointer is 16-byte aligned).
  *   - Handles are created by gnnav_build_* / gnnav_blocks_create and freed by
  *     the matching *_free, which accepts NULL.  Handles copy their inputs;
- *     callers keep ownership of every buffer they pass in.
+ *     callers keep ownership of every buffer they pass in.  A call that fails
+ *     leaves its output handle (*out) unwritten.
+ *   - Asynchronous calls (gather, aggregate, combine, forward, train step,
+ *     gnnav_sample_async) report argument and allocation errors at once;
+ *     a failure the device itself detects while running them (a device-wide
+ *     scan whose look-back wait gave up) is counted in a per-device error
+ *     word and reported as E_DEVICE by the next synchronisation point:
+ *     gnnav_sync, gnnav_blocks_sync or gnnav_sample.
  */
 #ifndef GNNAV_H
 #define GNNAV_H
@@ -42,7 +49,8 @@ typedef enum gnnav_status {
     GNNAV_E_RANGE = 2,     /* a node id outside [0, n) where ids must be valid */
     GNNAV_E_NOMEM = 3,     /* host, pinned or device allocation failed */
     GNNAV_E_CAPACITY = 4,  /* a size bound exceeds the 32-bit local-id range */
-    GNNAV_E_DEVICE = 5     /* a HIP runtime error (its text is in last_error) */
+    GNNAV_E_DEVICE = 5     /* a HIP runtime error, or a failure the device reported
+                              (gnnav_sync); its text is in last_error */
 } gnnav_status;
 
 typedef enum gnnav_dtype { GNNAV_F32 = 0, GNNAV_BF16 = 1 } gnnav_dtype;
@@ -73,6 +81,15 @@ const char *gnnav_last_error(void);
 
 /* GNNAV_ABI_VERSION of the loaded library. */
 int32_t gnnav_abi_version(void);
+
+/* Synchronisation point for asynchronous work: waits for `stream`, then
+ * returns E_DEVICE if device-side work on the current device (any stream)
+ * has reported a failure since the last report -- a device-wide scan (the
+ * classification of gnnav_gather*, the sampler's count and dedup scans, the
+ * backward's block transpose) whose look-back wait gave up, which leaves
+ * that work's results unreliable.  Each failure is reported once.
+ * Errors: E_DEVICE.                                                        */
+gnnav_status gnnav_sync(void *stream);
 
 /* ---------------------------------------------------------------- graph ---
  * Graph G(V, E) of Algorithm 1's input, as CSR in HBM.
@@ -146,8 +163,13 @@ gnnav_status gnnav_cache_set_link_workgroups(gnnav_cache *c, int32_t workgroups)
  * is Eq. 5's t_replace).  GNNAV_POLICY_STATIC (default) never changes the
  * cache.  GNNAV_POLICY_FIFO makes the last dynamic_slots cache slots a ring:
  * after each gather, the batch's misses are admitted in request order, each
- * taking the slot under the ring pointer (evicting its vertex) and advancing
- * the pointer; the earlier slots keep their degree-ranked vertices.  Rows
+ * taking the slot under the ring pointer and advancing the pointer; the
+ * slot's previous vertex is evicted (unmapped unless the slot map already
+ * points it at another slot); the earlier slots keep their degree-ranked
+ * vertices.  A vertex requested more than once in one gather is admitted
+ * once per missing request and stays mapped to the last of its slots (the
+ * others hold copies of its row until the ring reaches them); request lists
+ * without repeats, such as a frontier, never do this.  Rows
  * are copied from the gather's own output.  With a dynamic cache, gathers on
  * different streams run one after another in call order.  The call
  * synchronises the device and restarts the ring pointer at the ring's
@@ -180,9 +202,11 @@ void gnnav_blocks_free(gnnav_blocks *b);
  * enqueues its kernels on `stream` and synchronises that stream once at the
  * end to publish the per-hop sizes to the host.
  * Errors: E_INVALID (null pointers, n_hops < 1 or > 16, n_seeds < 0),
- * E_CAPACITY (an Eq. 12 bound exceeds INT32_MAX), E_RANGE (a seed outside
- * [0, n); the blocks' contents are then unspecified but reusable),
- * E_NOMEM, E_DEVICE.                                                      */
+ * E_CAPACITY (an Eq. 12 bound exceeds INT32_MAX; checked on the host
+ * before anything is enqueued, so the blocks keep the previous sample),
+ * E_RANGE (a seed outside [0, n); the blocks' contents are then unspecified
+ * but reusable), E_NOMEM (the blocks' contents are then unspecified but
+ * reusable), E_DEVICE (also: a device-side failure, see gnnav_sync).      */
 gnnav_status gnnav_sample(const gnnav_graph *g, const int32_t *seeds_dev, int64_t n_seeds,
                           const int32_t *fanouts, int32_t n_hops, uint64_t rng_seed,
                           gnnav_blocks *blocks, void *stream);
@@ -202,7 +226,8 @@ gnnav_status gnnav_sample_async(const gnnav_graph *g, const int32_t *seeds_dev, 
 
 /* Waits for `stream` and copies the last sample's sizes to the host.
  * Errors: E_INVALID (never sampled), E_RANGE (seeds outside [0, n) were
- * skipped), E_DEVICE.                                                      */
+ * skipped), E_DEVICE (a HIP error, or a device-side failure reported as by
+ * gnnav_sync; the sizes are then not published).                           */
 gnnav_status gnnav_blocks_sync(gnnav_blocks *b, void *stream);
 
 /* Device view of the last sample's sizes, valid once the sample's kernels
@@ -232,7 +257,8 @@ gnnav_status gnnav_blocks_nodes(const gnnav_blocks *b, const int32_t **nodes_dev
  * next 16-byte boundary are written with zeros; later columns are untouched.
  * An id outside [0, n) gives a zero row and counts as invalid.
  * counts_dev: device int64[3] receiving {hits, misses, invalid}; overwritten.
- * Asynchronous with respect to the host.
+ * Asynchronous with respect to the host; a device-side failure of the
+ * classification is reported by the next gnnav_sync.
  * Errors: E_INVALID (null pointers with n_ids > 0, ld_out < d, row stride
  * not a multiple of 16 bytes or out_dev not 16-byte aligned), E_NOMEM,
  * E_DEVICE.                                                               */
@@ -424,6 +450,23 @@ gnnav_status gnnav_profile_get(int32_t i, char *name, int32_t name_cap, int64_t 
  * to *n (n may be NULL).  Errors: E_INVALID (i out of range, ms NULL with
  * cap > 0).                                                                */
 gnnav_status gnnav_profile_samples(int32_t i, float *ms, int64_t cap, int64_t *n);
+
+/* -------------------------------------------------------------- testing ---
+ * Hooks that force failure paths from the host, so tests can reach them
+ * while every kernel still runs to its normal end.  Process-wide settings,
+ * not meant for production use.
+ *
+ * gnnav_debug_set_spin_limit: look-back polls after which a device-wide
+ * scan's wait gives up (default 2^20).  0 makes every tile after a scan's
+ * first give up before its first poll: the scan's results are wrong, every
+ * kernel still ends, and the next synchronisation point returns E_DEVICE.
+ *
+ * gnnav_debug_fail_allocations: after `after` more successful device or
+ * pinned host allocations by the library, every further one fails as if
+ * memory were exhausted (E_NOMEM); a negative value turns this off.
+ * Both always return GNNAV_OK.                                             */
+gnnav_status gnnav_debug_set_spin_limit(uint32_t polls);
+gnnav_status gnnav_debug_fail_allocations(int64_t after);
 
 #ifdef __cplusplus
 }

@@ -42,6 +42,7 @@ EXPORTS = [
     "gnnav_aggregate_mean", "gnnav_combine", "gnnav_combine_kernel", "gnnav_sage_forward", "gnnav_sage_train_step",
     "gnnav_softmax_xent", "gnnav_aggregate_mean_backward", "gnnav_weight_grad", "gnnav_profile_start",
     "gnnav_profile_stop", "gnnav_profile_count", "gnnav_profile_get", "gnnav_profile_samples",
+    "gnnav_sync", "gnnav_debug_set_spin_limit", "gnnav_debug_fail_allocations",
 ]
 
 
@@ -97,6 +98,9 @@ _sig = {
     "gnnav_profile_count": ([], i32),
     "gnnav_profile_get": ([i32, P, i32, P, P], i32),
     "gnnav_profile_samples": ([i32, P, i64, P], i32),
+    "gnnav_sync": ([P], i32),
+    "gnnav_debug_set_spin_limit": ([u32], i32),
+    "gnnav_debug_fail_allocations": ([i64], i32),
 }
 for _name, (_args, _res) in _sig.items():
     _f = getattr(_lib, _name)
@@ -118,6 +122,23 @@ def _stream(stream):
         import torch
         return torch.cuda.current_stream().cuda_stream
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def sync(stream=None):
+    """gnnav_sync: wait for `stream`; raises E_DEVICE if device-side work has
+    reported a failure (a scan whose look-back wait gave up) since the last
+    report."""
+    _check(_lib.gnnav_sync(_stream(stream)))
+
+
+def debug_set_spin_limit(polls: int):
+    """Testing hook: look-back polls before a scan's wait gives up (0: at once)."""
+    _check(_lib.gnnav_debug_set_spin_limit(int(polls)))
+
+
+def debug_fail_allocations(after: int):
+    """Testing hook: allocations after the next `after` fail (negative: off)."""
+    _check(_lib.gnnav_debug_fail_allocations(int(after)))
 
 
 def _dev_ptr(t):

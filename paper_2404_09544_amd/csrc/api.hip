@@ -4,6 +4,7 @@
 // orchestration that enqueues the kernels of sample.hip, gather.hip,
 // spmm.hip and gemm.hip.
 #include <algorithm>
+#include <atomic>
 #include <functional>
 #include <cmath>
 #include <cstring>
@@ -24,6 +25,39 @@ void set_last_error(const std::string &msg) { t_last_error = msg; }
 extern "C" const char *gnnav_last_error(void) { return t_last_error.c_str(); }
 extern "C" int32_t gnnav_abi_version(void) { return GNNAV_ABI_VERSION; }
 
+// ------------------------------------------------- allocation-failure hook
+// Testing aid (gnnav_debug_fail_allocations): after `g_alloc_budget` more
+// successful device or pinned allocations, every further one fails as if the
+// memory were exhausted.  Negative: off.
+namespace {
+std::atomic<int64_t> g_alloc_budget{-1};
+bool alloc_denied() {
+    int64_t b = g_alloc_budget.load();
+    while (b >= 0) {
+        if (b == 0) return true;
+        if (g_alloc_budget.compare_exchange_weak(b, b - 1)) return false;
+    }
+    return false;
+}
+}  // namespace
+
+namespace gnnav {
+void host_pinned_alloc(void **p, size_t bytes, unsigned flags, const char *what) {
+    *p = nullptr;
+    if (alloc_denied() || hipHostMalloc(p, bytes, flags) != hipSuccess) {
+        (void)hipGetLastError();
+        *p = nullptr;
+        fail(GNNAV_E_NOMEM, std::string("pinned host allocation of ") + std::to_string(bytes) + " bytes (" + what +
+                                ") failed");
+    }
+}
+}  // namespace gnnav
+
+extern "C" gnnav_status gnnav_debug_fail_allocations(int64_t after) {
+    g_alloc_budget.store(after < 0 ? -1 : after);
+    return GNNAV_OK;
+}
+
 // ---------------------------------------------------------- device buffer
 void DevBuf::ensure(size_t need, hipStream_t stream) {
     if (need <= bytes && p) return;
@@ -35,12 +69,78 @@ void DevBuf::ensure(size_t need, hipStream_t stream) {
     }
     size_t b = need < 256 ? 256 : need;
     b += b / 8;  // headroom so slowly growing batches do not reallocate every time
-    if (hipMalloc(&p, b) != hipSuccess) {
+    if (alloc_denied() || hipMalloc(&p, b) != hipSuccess) {
         (void)hipGetLastError();
         p = nullptr;
         fail(GNNAV_E_NOMEM, "device allocation of " + std::to_string(b) + " bytes failed");
     }
     bytes = b;
+}
+
+// ----------------------------------------------------- device error word
+// One word per device, counting the device-wide scans' look-back waits that
+// gave up (see scan.hpp).  It only grows; each synchronisation point compares
+// it with the count already reported on that device, so a failure of any
+// asynchronous work is reported once, by the first synchronisation point that
+// follows it.  A static device variable: nothing is allocated for it.
+static __device__ uint32_t g_device_errors;
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_err_mu;
+uint32_t *g_err_ptr[kMaxDevices] = {};
+uint32_t g_err_seen[kMaxDevices] = {};
+std::atomic<uint32_t> g_spin_limit{kSpinLimit};
+
+int current_device() {
+    int dev = 0;
+    GNNAV_HIP(hipGetDevice(&dev));
+    GNNAV_CHECK(dev >= 0 && dev < kMaxDevices, GNNAV_E_DEVICE, "device index beyond the library's table");
+    return dev;
+}
+}  // namespace
+
+namespace gnnav {
+uint32_t scan_spin_limit() { return g_spin_limit.load(); }
+
+uint32_t *device_error_word() {
+    const int dev = current_device();
+    std::lock_guard<std::mutex> lk(g_err_mu);
+    if (!g_err_ptr[dev]) {
+        void *ptr = nullptr;
+        GNNAV_HIP(hipGetSymbolAddress(&ptr, HIP_SYMBOL(g_device_errors)));
+        g_err_ptr[dev] = (uint32_t *)ptr;
+    }
+    return g_err_ptr[dev];
+}
+
+// Waits for `s`, then fails with E_DEVICE if the current device's error word
+// has grown since it was last reported.
+void check_device_errors(hipStream_t s) {
+    uint32_t *w = device_error_word();
+    uint32_t now = 0;
+    GNNAV_HIP(hipMemcpyAsync(&now, w, sizeof(now), hipMemcpyDeviceToHost, s));
+    GNNAV_HIP(hipStreamSynchronize(s));
+    const int dev = current_device();
+    uint32_t fresh;
+    {
+        std::lock_guard<std::mutex> lk(g_err_mu);
+        fresh = now - g_err_seen[dev];
+        g_err_seen[dev] = now;
+    }
+    GNNAV_CHECK(fresh == 0, GNNAV_E_DEVICE,
+                std::to_string(fresh) + " device-wide scan look-back wait(s) gave up; results of the work "
+                "enqueued since the last synchronisation point are unreliable");
+}
+}  // namespace gnnav
+
+extern "C" gnnav_status gnnav_sync(void *stream) {
+    return guarded([&] { check_device_errors((hipStream_t)stream); });
+}
+
+extern "C" gnnav_status gnnav_debug_set_spin_limit(uint32_t polls) {
+    g_spin_limit.store(polls);
+    return GNNAV_OK;
 }
 void DevBuf::release() {
     if (p) (void)hipFree(p);
@@ -311,7 +411,7 @@ static bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 struct GatherWs {
     hipStream_t stream = nullptr;
     DevBuf hit_list, miss_list, dev_counts;
-    ScanState scan;   // its look-back timeout counter is not checked (the gather is asynchronous)
+    ScanState scan;
 };
 
 struct gnnav_cache {
@@ -348,7 +448,6 @@ static GatherWs *gather_ws(gnnav_cache *c, hipStream_t s) {
     auto *w = new GatherWs();
     w->stream = s;
     c->ws.push_back(w);
-    w->dev_counts.ensure(2 * sizeof(int32_t), s);
     return w;
 }
 
@@ -382,7 +481,7 @@ static void upload_rows(void *dst_dev, const uint8_t *feats, int64_t row_bytes, 
     if (count <= 0) return;
     const int64_t chunk_rows = std::max<int64_t>(1, (64 << 20) / pitch);
     void *stage = nullptr;
-    GNNAV_HIP(hipHostMalloc(&stage, (size_t)(chunk_rows * pitch), hipHostMallocDefault));
+    host_pinned_alloc(&stage, (size_t)(chunk_rows * pitch), hipHostMallocDefault, "upload staging");
     try {
         for (int64_t r0 = 0; r0 < count; r0 += chunk_rows) {
             const int64_t rn = std::min(chunk_rows, count - r0);
@@ -448,11 +547,7 @@ extern "C" gnnav_status gnnav_build_cache(const gnnav_graph *g, const void *feat
                 c->store_ptr = c->store_dev.p;
             } else {
                 const size_t bytes = (size_t)std::max<int64_t>(n, 1) * pitch;
-                if (hipHostMalloc(&c->store_host, bytes, hipHostMallocMapped) != hipSuccess) {
-                    (void)hipGetLastError();
-                    c->store_host = nullptr;
-                    fail(GNNAV_E_NOMEM, "pinned host store of " + std::to_string(bytes) + " bytes failed");
-                }
+                host_pinned_alloc(&c->store_host, bytes, hipHostMallocMapped, "feature store");
                 uint8_t *hp = (uint8_t *)c->store_host;
                 parallel_for(n, [&](int64_t b, int64_t e) {
                     for (int64_t v = b; v < e; ++v) {
@@ -579,11 +674,12 @@ extern "C" gnnav_status gnnav_blocks_create(gnnav_blocks **out) {
     return guarded([&] {
         GNNAV_CHECK(out, GNNAV_E_INVALID, "out is NULL");
         auto *b = new gnnav_blocks();
-        if (hipHostMalloc((void **)&b->sizes_host, (kSizeSlots + 1) * sizeof(int32_t), hipHostMallocDefault) !=
-            hipSuccess) {
-            (void)hipGetLastError();
+        try {
+            host_pinned_alloc((void **)&b->sizes_host, (kSizeSlots + 1) * sizeof(int32_t), hipHostMallocDefault,
+                              "size mirror");
+        } catch (...) {
             delete b;
-            fail(GNNAV_E_NOMEM, "pinned size buffer");
+            throw;
         }
         *out = b;
     });
@@ -618,12 +714,34 @@ extern "C" void gnnav_blocks_free(gnnav_blocks *b) {
 static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64_t n_seeds, const int32_t *fanouts,
                            int32_t n_hops, uint64_t rng_seed, gnnav_blocks *b, hipStream_t s,
                            const gnnav_cache *bias = nullptr, uint32_t eta = 1) {
+    // Every argument and capacity check comes before any state changes, so a
+    // call that fails here leaves the blocks (and the cache) as they were.
     GNNAV_CHECK(g && b && fanouts, GNNAV_E_INVALID, "NULL graph, blocks or fanouts");
+    GNNAV_CHECK(n_hops >= 1 && n_hops <= kMaxHops, GNNAV_E_INVALID, "n_hops outside [1, 16]");
+    GNNAV_CHECK(n_seeds >= 0, GNNAV_E_INVALID, "n_seeds < 0");
+    GNNAV_CHECK(n_seeds == 0 || seeds_dev, GNNAV_E_INVALID, "seeds_dev is NULL");
+    GNNAV_CHECK(n_seeds <= INT32_MAX, GNNAV_E_CAPACITY, "n_seeds above INT32_MAX");
+    for (int h = 0; h < n_hops; ++h)
+        GNNAV_CHECK(fanouts[h] <= 1024, GNNAV_E_INVALID, "fanout above 1024");
     if (bias) {
         GNNAV_CHECK(bias->n == g->n, GNNAV_E_INVALID, "the cache belongs to a graph of another size");
         GNNAV_CHECK(eta >= 1 && eta <= 65536, GNNAV_E_INVALID, "eta outside [1, 65536]");
         for (int h = 0; h < n_hops; ++h)
             GNNAV_CHECK(fanouts[h] <= 64, GNNAV_E_INVALID, "biased sampling supports fanouts up to 64");
+    }
+    // Eq. 12 capacity bounds (tau = 1, no overlap): E_h <= n_(h-1) * k_h,
+    // n_h <= min(n, n_(h-1) + E_h).
+    int64_t nb[kMaxHops + 1], eb[kMaxHops + 1];
+    nb[0] = std::min<int64_t>(n_seeds, g->n);
+    eb[0] = 0;
+    for (int h = 1; h <= n_hops; ++h) {
+        const int64_t k = fanouts[h - 1] < 0 ? g->max_deg : std::min<int64_t>(fanouts[h - 1], g->max_deg);
+        eb[h] = nb[h - 1] * k;
+        nb[h] = std::min<int64_t>(g->n, nb[h - 1] + eb[h]);
+        GNNAV_CHECK(eb[h] < INT32_MAX && nb[h] < INT32_MAX, GNNAV_E_CAPACITY,
+                    "hop " + std::to_string(h) + " bound exceeds the int32 range");
+    }
+    if (bias) {
         auto *bc = const_cast<gnnav_cache *>(bias);
         std::lock_guard<std::mutex> lk(bc->upd_mu);
         if (bc->ring_n > 0) {
@@ -644,24 +762,6 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
                 GNNAV_HIP(hipStreamWaitEvent(s, bc->part_ready, 0));
             }
         }
-    }
-    GNNAV_CHECK(n_hops >= 1 && n_hops <= kMaxHops, GNNAV_E_INVALID, "n_hops outside [1, 16]");
-    GNNAV_CHECK(n_seeds >= 0, GNNAV_E_INVALID, "n_seeds < 0");
-    GNNAV_CHECK(n_seeds == 0 || seeds_dev, GNNAV_E_INVALID, "seeds_dev is NULL");
-    GNNAV_CHECK(n_seeds <= INT32_MAX, GNNAV_E_CAPACITY, "n_seeds above INT32_MAX");
-    for (int h = 0; h < n_hops; ++h)
-        GNNAV_CHECK(fanouts[h] <= 1024, GNNAV_E_INVALID, "fanout above 1024");
-    // Eq. 12 capacity bounds (tau = 1, no overlap): E_h <= n_(h-1) * k_h,
-    // n_h <= min(n, n_(h-1) + E_h).
-    int64_t nb[kMaxHops + 1], eb[kMaxHops + 1];
-    nb[0] = std::min<int64_t>(n_seeds, g->n);
-    eb[0] = 0;
-    for (int h = 1; h <= n_hops; ++h) {
-        const int64_t k = fanouts[h - 1] < 0 ? g->max_deg : std::min<int64_t>(fanouts[h - 1], g->max_deg);
-        eb[h] = nb[h - 1] * k;
-        nb[h] = std::min<int64_t>(g->n, nb[h - 1] + eb[h]);
-        GNNAV_CHECK(eb[h] < INT32_MAX && nb[h] < INT32_MAX, GNNAV_E_CAPACITY,
-                    "hop " + std::to_string(h) + " bound exceeds the int32 range");
     }
     int64_t max_list = n_seeds;
     for (int h = 1; h <= n_hops; ++h) max_list = std::max(max_list, std::max(eb[h], nb[h - 1] + 1));
@@ -708,6 +808,7 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
             a.relabel_list = b->nbrs[h - 2].as<int32_t>();
             a.relabel_len = sz + kSizeE + h - 1;
             a.relabel_bound = eb[h - 1];
+            a.relabel_n = sz + kSizeN + h - 1;
             a.relabel_indices = b->indices[h - 2].as<int32_t>();
         }
         if (h > 1) launch_count_scan(a, s);   // hop 1's ran with the seeds' dedup
@@ -716,7 +817,7 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
                      sz + kSizeN + h - 1, sz + kSizeN + h, nullptr, &b->scan, true};
         launch_dedup(dh, s);
     }
-    launch_relabel(b->nbrs[n_hops - 1].as<int32_t>(), sz + kSizeE + n_hops, eb[n_hops], map,
+    launch_relabel(b->nbrs[n_hops - 1].as<int32_t>(), sz + kSizeE + n_hops, eb[n_hops], map, sz + kSizeN + n_hops,
                    b->indices[n_hops - 1].as<int32_t>(), s);
     b->L = n_hops;
     b->host_sizes = false;
@@ -730,10 +831,7 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
 static void publish_sizes(gnnav_blocks *b, hipStream_t s) {
     GNNAV_CHECK(b->sizes.p, GNNAV_E_INVALID, "blocks have not been sampled");
     GNNAV_HIP(hipMemcpyAsync(b->sizes_host, b->sizes.p, kSizeSlots * sizeof(int32_t), hipMemcpyDeviceToHost, s));
-    GNNAV_HIP(hipMemcpyAsync(b->sizes_host + kSizeSlots, b->scan.timeouts(), sizeof(int32_t), hipMemcpyDeviceToHost,
-                             s));
-    GNNAV_HIP(hipStreamSynchronize(s));
-    GNNAV_CHECK(b->sizes_host[kSizeSlots] == 0, GNNAV_E_DEVICE, "a device-wide scan's look-back wait timed out");
+    check_device_errors(s);   // also waits for s
     for (int h = 0; h <= b->L; ++h) b->n_h[h] = b->sizes_host[kSizeN + h];
     for (int h = 1; h <= b->L; ++h) b->e_h[h] = b->sizes_host[kSizeE + h];
     b->host_sizes = true;
@@ -834,6 +932,7 @@ static void gather_impl(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_
         if (cc->upd_recorded) GNNAV_HIP(hipStreamWaitEvent(s, cc->upd_done, 0));
     }
     GatherWs *w = gather_ws(cc, s);
+    w->dev_counts.ensure(2 * sizeof(int32_t), s);
     w->hit_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
     w->miss_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
     w->scan.ensure(n_ids, s);

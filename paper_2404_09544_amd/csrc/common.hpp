@@ -32,6 +32,13 @@ struct Error {
         if (!(cond)) ::gnnav::fail((st), (msg));      \
     } while (0)
 
+// Pinned host allocation (hipHostMalloc with `flags`); E_NOMEM on failure.
+void host_pinned_alloc(void **p, size_t bytes, unsigned flags, const char *what);
+
+// Waits for stream `s`; E_DEVICE if device-side work has reported a failure
+// (a scan look-back wait that gave up) since the last such report.
+void check_device_errors(hipStream_t s);
+
 // Runs `body`, converting exceptions into a status and the thread's error text.
 void set_last_error(const std::string &msg);
 template <class F>
@@ -159,6 +166,7 @@ struct SampleHopArgs {
     const int32_t *relabel_list = nullptr;
     const int32_t *relabel_len = nullptr;    // device length
     int64_t relabel_bound = 0;
+    const int32_t *relabel_n = nullptr;      // device size of the frontier the list was merged into
     int32_t *relabel_indices = nullptr;
 };
 void launch_partition_rows(const void *row_ptr, bool offsets_i64, const int32_t *col, int64_t n,
@@ -190,7 +198,7 @@ struct DedupArgs {
 };
 void launch_dedup(const DedupArgs &a, hipStream_t s);
 void launch_relabel(const int32_t *list, const int32_t *len_ptr, int64_t len_bound,
-                    const uint64_t *map, int32_t *indices, hipStream_t s);
+                    const uint64_t *map, const int32_t *n_frontier, int32_t *indices, hipStream_t s);
 
 // gather.hip
 struct GatherArgs {

@@ -101,15 +101,26 @@ struct CountOp {
     }
 };
 
+// Local id of a listed node from its node-table entry.  Every listed id is
+// in the frontier by the time this runs, so its entry holds a local id below
+// the frontier size; anything else (only possible after a scan whose
+// look-back wait gave up, which the next synchronisation point reports)
+// becomes 0, so no later kernel reads outside the source rows.
+__device__ __forceinline__ int32_t local_id(uint64_t entry, const int32_t *n_frontier) {
+    const uint32_t w = (uint32_t)entry;
+    return w < (uint32_t)*n_frontier ? (int32_t)w : 0;
+}
+
 // Local ids of the previous hop's list (its relabel), carried by the count
 // scan's launch: both only need that hop's dedup finished.
 struct RelabelSide {
     const int32_t *list;
     const int32_t *len_ptr;
     const uint64_t *map;
+    const int32_t *n_frontier;
     int32_t *indices;
     __device__ int64_t n() const { return *len_ptr; }
-    __device__ void run(int64_t p) const { indices[p] = (int32_t)(uint32_t)map[list[p]]; }
+    __device__ void run(int64_t p) const { indices[p] = local_id(map[list[p]], n_frontier); }
 };
 
 void launch_count_scan(const SampleHopArgs &a, hipStream_t s) {
@@ -118,7 +129,8 @@ void launch_count_scan(const SampleHopArgs &a, hipStream_t s) {
         if (a.relabel_list)
             run_scan<Op, int32_t, RelabelSide>(
                 op, a.rows_bound, *a.scan, "count_scan", s,
-                RelabelSide{a.relabel_list, a.relabel_len, a.first_map, a.relabel_indices}, a.relabel_bound);
+                RelabelSide{a.relabel_list, a.relabel_len, a.first_map, a.relabel_n, a.relabel_indices},
+                a.relabel_bound);
         else
             run_scan<Op, int32_t>(op, a.rows_bound, *a.scan, "count_scan", s);
     };
@@ -643,19 +655,20 @@ void launch_dedup(const DedupArgs &a, hipStream_t s) {
 __global__ void __launch_bounds__(256) k_relabel(const int32_t *__restrict__ list,
                                                  const int32_t *__restrict__ len_ptr,
                                                  const uint64_t *__restrict__ map,
+                                                 const int32_t *__restrict__ n_frontier,
                                                  int32_t *__restrict__ indices) {
     const int64_t len = *len_ptr;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < len; p += stride)
-        indices[p] = (int32_t)(uint32_t)map[list[p]];   // every listed id is in the frontier by now
+        indices[p] = local_id(map[list[p]], n_frontier);
 }
 
 void launch_relabel(const int32_t *list, const int32_t *len_ptr, int64_t len_bound, const uint64_t *map,
-                    int32_t *indices, hipStream_t s) {
+                    const int32_t *n_frontier, int32_t *indices, hipStream_t s) {
     if (len_bound <= 0) return;
     KernelTimer t("relabel", s);
     hipLaunchKernelGGL(k_relabel, dim3(grid_for(len_bound, 256, 8192)), dim3(256), 0, s, list, len_ptr,
-                       map, indices);
+                       map, n_frontier, indices);
     GNNAV_HIP(hipGetLastError());
 }
 

@@ -26,8 +26,12 @@
 // prefix and emits.  Records carry the call's epoch, so they never need
 // clearing between calls.  Each thread owns kScanItems consecutive elements,
 // so results do not depend on scheduling.  The look-back wait is bounded: a
-// wait that exceeds kSpinLimit polls gives up, counts an error and lets the
-// workgroup finish (the results are then wrong and the caller reports it).
+// wait that exceeds the spin limit (kSpinLimit polls unless a test lowers it)
+// gives up, adds one to the library's device error word and lets the
+// workgroup finish.  The prefix it publishes is then the part it had summed,
+// never more than the true one, so every position derived from it stays
+// inside the buffers sized for the true one; the results are wrong and the
+// next synchronisation point reports E_DEVICE.
 //
 // Publication is one 64-bit atomic store per 32-bit half of the value, each
 // word carrying the call's tag (epoch and kind) next to its half, and a
@@ -74,6 +78,12 @@ struct ScanItems<Op, true> {
 constexpr uint32_t kSpinLimit = 1u << 20;
 constexpr int64_t kScanGrid = 1024;   // workgroups per scan launch, at most
 
+// Look-back polls before a wait gives up (kSpinLimit unless lowered for a
+// test; 0 gives up before the first poll, so every tile after the first
+// times out), and the device word that counts the waits that gave up (api.hip).
+uint32_t scan_spin_limit();
+uint32_t *device_error_word();
+
 inline int64_t scan_parts(int64_t bound) {
     int64_t t = (bound + kScanTile - 1) / kScanTile;
     return t < 1 ? 1 : t;
@@ -87,7 +97,7 @@ constexpr int kRecWords = 2;   // enough for 64-bit values
 struct ScanState {
     DevBuf sums;      // uint64 [tiles][kRecWords]
     DevBuf prefix;    // uint64 [tiles][kRecWords]
-    DevBuf ctl;       // uint32 [0] ticket, [1] look-back timeouts
+    DevBuf ctl;       // uint32 [0] ticket
     int64_t tiles = 0;
     uint32_t epoch = 0;
     void ensure(int64_t bound, hipStream_t s) {
@@ -116,7 +126,6 @@ struct ScanState {
         if (epoch == 0) epoch = 1;
         return epoch;
     }
-    uint32_t *timeouts() const { return ctl.as<uint32_t>() + 1; }
 };
 
 template <class V>
@@ -158,7 +167,8 @@ template <class Op, class V, class Side>
 __global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, Side side, int scan_grid,
                                                                 uint64_t *__restrict__ sums,
                                                                 uint64_t *__restrict__ prefix,
-                                                                uint32_t *__restrict__ ctl, uint32_t epoch) {
+                                                                uint32_t *__restrict__ ctl, uint32_t epoch,
+                                                                uint32_t *__restrict__ errors, uint32_t spin_limit) {
     __shared__ V scratch[kScanThreads / kWave];
     __shared__ int64_t s_tile;
     __shared__ V s_prefix;
@@ -215,6 +225,10 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, Side side,
                 int64_t base = tile - 1;
                 uint32_t spins = 0;
                 while (true) {
+                    if (spins >= spin_limit) {
+                        if (lane == 0) atomicAdd(errors, 1u);
+                        break;
+                    }
                     const int64_t t = base - lane;
                     // tiles before tile 0 read as a published zero prefix; the
                     // window that reaches tile 0 always stops there first
@@ -228,10 +242,7 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, Side side,
                     const int pidx = pmask ? __builtin_ctzll(pmask) : kWave;
                     const uint64_t need = pidx >= kWave - 1 ? ~0ull : ((1ull << (pidx + 1)) - 1);
                     if ((__ballot(ready) & need) != need) {
-                        if (++spins > kSpinLimit) {
-                            if (lane == 0) atomicAdd(&ctl[1], 1u);
-                            break;
-                        }
+                        ++spins;
                         __builtin_amdgcn_s_sleep(1);
                         continue;
                     }
@@ -275,7 +286,7 @@ void run_scan(const Op &op, int64_t bound, ScanState &st, const char *name, hipS
     KernelTimer t(name, s);
     hipLaunchKernelGGL((k_scan_onepass<Op, V, Side>), dim3((unsigned)(grid + side_grid)), dim3(kScanThreads), 0, s,
                        op, side, (int)grid, st.sums.as<uint64_t>(), st.prefix.as<uint64_t>(),
-                       st.ctl.as<uint32_t>(), epoch);
+                       st.ctl.as<uint32_t>(), epoch, device_error_word(), scan_spin_limit());
     GNNAV_HIP(hipGetLastError());
 }
 

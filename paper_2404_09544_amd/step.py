@@ -29,7 +29,7 @@ import numpy as np
 import torch
 
 from . import (Blocks, Cache, Graph, gather, gather_n, sage_forward, sage_train_step, sample, sample_async,
-               sample_biased)
+               sample_biased, sync)
 
 
 def to_device_weights(ws, dtype: str):
@@ -221,5 +221,7 @@ class Pipeline:
         return slot
 
     def synchronize(self):
+        """Wait for every slot's stream; raises if device-side work reported
+        a failure (gnnav_sync)."""
         for s in self.streams:
-            s.synchronize()
+            sync(s)

@@ -1,10 +1,15 @@
-"""GPU parity at the full workload sizes, in the launch configuration bench.py times.
+"""GPU parity at the full workload sizes.
 
 For each workload: the device CSR equals the oracle's; a batch through
-MiniBatchStep (the bench's step) gives frontiers, blocks, gathered rows and
-hit/miss counts identical to the oracle's; the logits of sampled seed rows
-match the oracle's receptive-field forward within tolerance.  The 10M-node
-R-MAT workload runs at cache fractions 0, 0.25 and 1.
+MiniBatchStep's synchronous form gives frontiers, blocks, gathered rows and
+hit/miss counts identical to the oracle's, and the logits of sampled seed
+rows match the oracle's receptive-field forward within tolerance (the
+10M-node R-MAT workload at cache fractions 0, 0.25 and 1).  Then the launch
+configuration bench.py times: the first three batches through the
+three-stream Pipeline (asynchronous sampling, gathers ordered on the host
+link, grids and GEMM tiles planned from the Eq. 12 bounds), each slot
+checked in full against the oracle -- every logits row of F_0 where the
+oracle's forward takes seconds, sampled rows on the two largest graphs.
 """
 import sys
 import time
@@ -76,7 +81,7 @@ def test_full_batch(G, name):
         c = G.Cache(g, feats, wl.dtype, r, store_on_device=wl.cfg["store_on_device"])
         step = MiniBatchStep(g, c, to_device_weights(ws, wl.dtype), wl.dims, wl.fanouts, wl.dtype)
         _, slot, _ = O.rank_cache(csr, r)
-        for b in ([7] if wl.n > 1_000_000 else [0, 7]):
+        for b in ([7] if wl.n > 1_000_000 else [0, 1, 2, 7]):
             say(name, f"r={r} batch {b}")
             seeds = wl.seeds(b)
             logits = step.run(torch.from_numpy(seeds).cuda(), wl.rng_seed(b))
@@ -99,6 +104,62 @@ def test_full_batch(G, name):
             say(name, f"r={r} batch {b}: sizes {sizes} hits/misses {counts.tolist()} "
                       f"({time.perf_counter() - t:.1f}s)")
         c.close()
+
+
+# logits rows checked per pipelined batch: every row of F_0 (None) where the
+# oracle's double-precision forward of the whole batch takes seconds
+PIPE_ROWS = {"chunglu-169k-d128": None, "chunglu-233k-d602": None, "chunglu-2450k-d100": 256,
+             "rmat-10m-d128": 256}
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_pipeline(G, name):
+    """Batches 0, 1, 2 through Pipeline.enqueue on three streams with the
+    bench's link-workgroup setting (64), exactly as the bench's pipelined
+    leg enqueues them; every slot against the oracle."""
+    import torch
+    from paper_2404_09544_amd.step import Pipeline, to_device_weights
+    wl, _, _, csr, g = load(G, name)
+    feats = wl.features()
+    ws = wl.weights()
+    wd = [O.to_f64(w, wl.dtype) for w in ws]
+    bf16 = wl.dtype == "bf16"
+    tol = BF16_TOL if bf16 else FP32_TOL
+    r = wl.cfg["cache"]
+    t = time.perf_counter()
+    c = G.Cache(g, feats, wl.dtype, r, store_on_device=wl.cfg["store_on_device"])
+    _, slot_map, _ = O.rank_cache(csr, r)
+    pipe = Pipeline(g, c, to_device_weights(ws, wl.dtype), wl.dims, wl.fanouts, wl.dtype, depth=3,
+                    link_workgroups=64)
+    seeds_dev = [torch.from_numpy(wl.seeds(b)).cuda() for b in range(3)]
+    slots = [pipe.enqueue(seeds_dev[b], wl.rng_seed(b)) for b in range(3)]
+    pipe.synchronize()
+    say(name, f"pipeline of 3 batches done ({time.perf_counter() - t:.1f}s)")
+    for b, st in enumerate(slots):
+        logits = st.finish().cpu().numpy()
+        nodes, sizes, ip, nb, ix = st.blocks.to_host()
+        ref_b = O.sample_blocks(csr, wl.seeds(b), wl.fanouts, wl.rng_seed(b))
+        assert sizes == ref_b.sizes, f"batch {b} sizes"
+        assert np.array_equal(nodes, ref_b.nodes)
+        for h in range(wl.L):
+            assert np.array_equal(ip[h], ref_b.indptr[h]), f"batch {b} indptr hop {h + 1}"
+            assert np.array_equal(nb[h], ref_b.nbrs[h]), f"batch {b} neighbours hop {h + 1}"
+            assert np.array_equal(ix[h], ref_b.indices[h]), f"batch {b} indices hop {h + 1}"
+        h0, counts = O.gather(feats, slot_map, ref_b.nodes)
+        assert np.array_equal(st.counts.cpu().numpy(), counts), f"batch {b} counts"
+        got_h0 = st.h0_view().cpu().numpy()[:, :wl.d]
+        assert np.array_equal(got_h0.view(np.uint8), h0.view(np.uint8)), f"batch {b} gathered rows"
+        k = PIPE_ROWS[name]
+        if k is None:
+            ref = O.sage_forward(ref_b, O.to_f64(h0, wl.dtype), wd, bf16=bf16)
+            got = logits
+        else:
+            rows = np.random.default_rng(100 + b).choice(sizes[0], size=min(k, sizes[0]), replace=False)
+            ref = O.sage_forward_rows(ref_b, O.to_f64(h0, wl.dtype), wd, rows, bf16=bf16)
+            got = logits[rows]
+        assert_rows_close(got, ref, tol, f"{name} pipelined batch {b} logits ({got.shape[0]} rows)")
+        say(name, f"pipelined batch {b}: sizes {sizes} ({time.perf_counter() - t:.1f}s)")
+    c.close()
 
 
 TRAIN_FULL = ["chunglu-169k-d128", "chunglu-233k-d602", "chunglu-2450k-d100"]
