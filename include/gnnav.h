@@ -284,6 +284,23 @@ gnnav_status gnnav_gather_n_after(const gnnav_cache *c, const int32_t *ids_dev,
                                   int64_t ld_out, int64_t *counts_dev, void *copy_after_event,
                                   void *stream);
 
+/* gnnav_gather for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same results as gnnav_gather (static or FIFO cache) for at most
+ * 1,048,576 ids, with no hipMalloc, hipFree or other allocation.  Its
+ * workspace (hit and miss lists, counts, the classification scan's ticket
+ * and tile records; about 16.02 MiB per device) is a static device array
+ * that each device the library runs on holds until the process ends.  Every
+ * call on a device shares that device's array: calls whose work overlaps on
+ * one device race (this one enqueues its work after the previous call's on
+ * the same stream; across streams the caller must order them).  The array
+ * keeps the last call's contents; nothing in it needs clearing.  Per-kernel
+ * profiling records nothing for these calls.
+ * Errors: E_CAPACITY (n_ids above 1,048,576, before any work), otherwise as
+ * gnnav_gather without E_NOMEM.                                            */
+gnnav_status gnnav_gather_noalloc(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_ids,
+                                  void *out_dev, int64_t ld_out, int64_t *counts_dev, void *stream);
+
 /* ------------------------------------------------------- SAGE, per layer ---
  * Eq. 1 Aggregate, GraphSAGE mean: for each destination row i < n_dst,
  * out[i] = (1/cnt_i) * sum over p in [indptr[i], indptr[i+1]) of

@@ -42,7 +42,7 @@ EXPORTS = [
     "gnnav_aggregate_mean", "gnnav_combine", "gnnav_combine_kernel", "gnnav_sage_forward", "gnnav_sage_train_step",
     "gnnav_softmax_xent", "gnnav_aggregate_mean_backward", "gnnav_weight_grad", "gnnav_profile_start",
     "gnnav_profile_stop", "gnnav_profile_count", "gnnav_profile_get", "gnnav_profile_samples",
-    "gnnav_sync", "gnnav_debug_set_spin_limit", "gnnav_debug_fail_allocations",
+    "gnnav_sync", "gnnav_debug_set_spin_limit", "gnnav_debug_fail_allocations", "gnnav_gather_noalloc",
 ]
 
 
@@ -101,6 +101,7 @@ _sig = {
     "gnnav_sync": ([P], i32),
     "gnnav_debug_set_spin_limit": ([u32], i32),
     "gnnav_debug_fail_allocations": ([i64], i32),
+    "gnnav_gather_noalloc": ([P, P, i64, P, i64, P, P], i32),
 }
 for _name, (_args, _res) in _sig.items():
     _f = getattr(_lib, _name)
@@ -385,6 +386,13 @@ def gather(cache: Cache, ids_ptr: int, n_ids: int, out, counts, stream=None):
     ld = out.stride(0)
     _check(_lib.gnnav_gather(cache._h, ids_ptr, n_ids, _dev_ptr(out), ld, _dev_ptr(counts),
                              _stream(stream)))
+
+
+def gather_noalloc(cache: Cache, ids_ptr: int, n_ids: int, out, counts, stream=None):
+    """gnnav_gather_noalloc: gnnav_gather with its workspace in static device
+    memory (at most 2**20 ids; calls overlapping on one device race)."""
+    _check(_lib.gnnav_gather_noalloc(cache._h, ids_ptr, n_ids, _dev_ptr(out), out.stride(0), _dev_ptr(counts),
+                                     _stream(stream)))
 
 
 def aggregate_mean(indptr_ptr: int, indices_ptr: int, n_dst: int, x, d: int, dtype: str, out,

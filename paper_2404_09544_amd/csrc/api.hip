@@ -176,13 +176,15 @@ hipEvent_t take_event() {
     GNNAV_HIP(hipEventCreate(&e));
     return e;
 }
+
+thread_local bool t_timers_off = false;
 }  // namespace
 
 namespace gnnav {
 bool profiling_on() { return g_prof_on; }
 
 KernelTimer::KernelTimer(const char *name, hipStream_t s) : stream(s) {
-    if (!g_prof_on) return;
+    if (!g_prof_on || t_timers_off) return;
     std::lock_guard<std::mutex> lk(g_prof_mu);
     int idx = -1;
     for (size_t i = 0; i < g_prof.size(); ++i)
@@ -203,6 +205,13 @@ KernelTimer::~KernelTimer() {
     g_prof[g_pending[slot].slot].launches++;
 }
 }  // namespace gnnav
+
+// Turns per-kernel timing off on this thread while it lives.
+struct TimersOff {
+    bool prev;
+    TimersOff() : prev(t_timers_off) { t_timers_off = true; }
+    ~TimersOff() { t_timers_off = prev; }
+};
 
 // An empty kernel launched when recording starts (which = 1) and stops
 // (which = 2): it marks the recorded region in an external kernel trace.
@@ -913,9 +922,12 @@ extern "C" gnnav_status gnnav_blocks_nodes(const gnnav_blocks *b, const int32_t 
 
 // ----------------------------------------------------------------- gather
 
+// `fixed`: a workspace to use instead of the stream's own (the no-allocation
+// entry point passes one that lives in static device memory, large enough
+// for the request count, so nothing is allocated here).
 static void gather_impl(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_ids, const int32_t *n_dev,
                         void *out_dev, int64_t ld_out, int64_t *counts_dev, hipStream_t s,
-                        hipEvent_t copy_after = nullptr) {
+                        hipEvent_t copy_after = nullptr, GatherWs *fixed = nullptr) {
     GNNAV_CHECK(c && counts_dev, GNNAV_E_INVALID, "NULL cache or counts");
     GNNAV_CHECK(n_ids >= 0 && n_ids < INT32_MAX, GNNAV_E_INVALID, "n_ids outside [0, INT32_MAX)");
     GNNAV_CHECK(n_ids == 0 || (ids_dev && out_dev), GNNAV_E_INVALID, "NULL ids or out");
@@ -931,11 +943,14 @@ static void gather_impl(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_
         upd_lock.lock();
         if (cc->upd_recorded) GNNAV_HIP(hipStreamWaitEvent(s, cc->upd_done, 0));
     }
-    GatherWs *w = gather_ws(cc, s);
-    w->dev_counts.ensure(2 * sizeof(int32_t), s);
-    w->hit_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
-    w->miss_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
-    w->scan.ensure(n_ids, s);
+    GatherWs *w = fixed;
+    if (!w) {
+        w = gather_ws(cc, s);
+        w->dev_counts.ensure(2 * sizeof(int32_t), s);
+        w->hit_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
+        w->miss_list.ensure(std::max<int64_t>(n_ids, 1) * sizeof(int2), s);
+        w->scan.ensure(n_ids, s);
+    }
     GatherArgs a{ids_dev, n_ids, n_dev, c->slot_map.as<int32_t>(), c->n, c->cache_rows.p, c->store_ptr,
                  c->ld * c->elt, out_dev, ld_out * c->elt, c->d * c->elt, counts_dev, w->dev_counts.as<int32_t>(),
                  w->hit_list.as<int2>(), w->miss_list.as<int2>(), &w->scan, cc->link_wgs};
@@ -971,6 +986,74 @@ extern "C" gnnav_status gnnav_gather_n_after(const gnnav_cache *c, const int32_t
         GNNAV_CHECK(n_ids_dev, GNNAV_E_INVALID, "n_ids_dev is NULL");
         gather_impl(c, ids_dev, n_ids_max, n_ids_dev, out_dev, ld_out, counts_dev, (hipStream_t)stream,
                     (hipEvent_t)copy_after_event);
+    });
+}
+
+// --------------------------------------------- gather without allocation
+// gnnav_gather_noalloc keeps its workspace -- hit and miss lists, the two
+// device counts, the classification scan's ticket and tile records -- in
+// `scratch`, a static device array (each device holds its own copy until the
+// process ends).  Nothing in it needs clearing between calls: the lists and
+// counts are written before they are read, the ticket returns to zero at the
+// end of every scan launch, and tile records carry the call's epoch (the
+// array starts zeroed, and epoch 0 is never used).
+namespace {
+constexpr int64_t kNoAllocMaxIds = int64_t(1) << 20;
+constexpr size_t kNaListBytes = (size_t)kNoAllocMaxIds * sizeof(int2);
+constexpr size_t kNaRecBytes = (size_t)(kNoAllocMaxIds / kScanTile) * kRecWords * sizeof(uint64_t);
+constexpr size_t kNaHit = 0, kNaMiss = kNaListBytes, kNaCounts = 2 * kNaListBytes, kNaCtl = kNaCounts + 256,
+                 kNaSums = kNaCtl + 256, kNaPrefix = kNaSums + kNaRecBytes, kNaBytes = kNaPrefix + kNaRecBytes;
+static_assert(kNoAllocMaxIds % kScanTile == 0, "whole scan tiles");
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kNaBytes];
+
+namespace {
+struct NoAllocWs {
+    bool ready = false;
+    GatherWs ws;       // its buffers point into this device's `scratch` and are never released
+    std::mutex mu;     // one call at a time per device on the host side
+};
+NoAllocWs g_noalloc[kMaxDevices];
+
+// This device's workspace view; its address comes from hipGetSymbolAddress
+// on the first call on the device (with that device current).
+NoAllocWs &noalloc_ws() {
+    const int dev = current_device();
+    NoAllocWs &na = g_noalloc[dev];
+    std::lock_guard<std::mutex> lk(g_err_mu);
+    if (!na.ready) {
+        void *ptr = nullptr;
+        GNNAV_HIP(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+        GNNAV_CHECK(ptr != nullptr, GNNAV_E_DEVICE, "no device address for the static workspace");
+        char *base = (char *)ptr;
+        auto view = [&](DevBuf &b, size_t off, size_t bytes) {
+            b.p = base + off;
+            b.bytes = bytes;
+        };
+        view(na.ws.hit_list, kNaHit, kNaListBytes);
+        view(na.ws.miss_list, kNaMiss, kNaListBytes);
+        view(na.ws.dev_counts, kNaCounts, 256);
+        view(na.ws.scan.ctl, kNaCtl, 256);
+        view(na.ws.scan.sums, kNaSums, kNaRecBytes);
+        view(na.ws.scan.prefix, kNaPrefix, kNaRecBytes);
+        na.ws.scan.tiles = kNoAllocMaxIds / kScanTile;
+        na.ready = true;
+    }
+    return na;
+}
+}  // namespace
+
+extern "C" gnnav_status gnnav_gather_noalloc(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_ids,
+                                             void *out_dev, int64_t ld_out, int64_t *counts_dev, void *stream) {
+    return guarded([&] {
+        GNNAV_CHECK(n_ids <= kNoAllocMaxIds, GNNAV_E_CAPACITY,
+                    "gnnav_gather_noalloc takes at most " + std::to_string(kNoAllocMaxIds) + " ids per call, got " +
+                        std::to_string(n_ids));
+        NoAllocWs &na = noalloc_ws();
+        std::lock_guard<std::mutex> lk(na.mu);
+        TimersOff quiet;   // per-kernel timing would create event objects
+        gather_impl(c, ids_dev, n_ids, nullptr, out_dev, ld_out, counts_dev, (hipStream_t)stream, nullptr, &na.ws);
     });
 }
 
