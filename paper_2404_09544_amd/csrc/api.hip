@@ -655,7 +655,7 @@ namespace {
 constexpr int kMaxHops = 16;
 constexpr int kSizeN = 0;         // sizes[kSizeN + h] = |F_h|
 constexpr int kSizeE = 17;        // sizes[kSizeE + h] = E_h (h >= 1)
-constexpr int kSizeErr = 40;      // out-of-range seed count
+constexpr int kSizeErr = 40;      // out-of-range seed count: slot 40 + (call parity)
 constexpr int kSizeSlots = 48;
 }  // namespace
 
@@ -667,6 +667,7 @@ struct gnnav_blocks {
     int64_t nb[kMaxHops + 1] = {0};    // Eq. 12 capacity bounds of the last sample
     int64_t eb[kMaxHops + 1] = {0};
     int64_t map_nodes = -1;
+    uint64_t calls = 0;                // sampling calls; their parity picks the error-count slot
     uint32_t map_epoch = 0;            // sampling calls since the node table was last filled
     DevBuf map, sizes, nodes;
     ScanState scan;
@@ -784,7 +785,10 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
         b->map_epoch = 0;
     }
     const uint32_t tag = 0xffffffffu - ++b->map_epoch;
-    b->sizes.ensure(kSizeSlots * sizeof(int32_t), s);
+    if (!b->sizes.p) {
+        b->sizes.ensure(kSizeSlots * sizeof(int32_t), s);
+        launch_fill_i32(b->sizes.as<int32_t>(), 0, kSizeSlots, s);   // once: both error-count slots start at 0
+    }
     b->nodes.ensure(std::max<int64_t>(nb[n_hops], 1) * sizeof(int32_t), s);
     b->scan.ensure(max_list, s);
     for (int h = 1; h <= n_hops; ++h) {
@@ -795,11 +799,15 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
     int32_t *sz = b->sizes.as<int32_t>();
     uint64_t *map = b->map.as<uint64_t>();
     int32_t *nodes = b->nodes.as<int32_t>();
-    launch_fill_i32(sz, 0, kSizeSlots, s);
+    // Every size slot is written by this call's scans; the out-of-range seed
+    // count alternates between two slots, the other one cleared by this call
+    // for the next (so no clearing launch is needed).
+    const int par = (int)(++b->calls & 1);
     // F_0 (seeds without repeats, first occurrence kept) and hop 1's row
     // counts (indptr_1, E_1) in one scan
-    DedupArgs d0{seeds_dev, n_seeds, nullptr, n_seeds, map, tag, g->n, nodes, nullptr, sz + kSizeN, sz + kSizeErr,
-                 &b->scan};
+    DedupArgs d0{seeds_dev, n_seeds, nullptr, n_seeds, map, tag, g->n, nodes, nullptr, sz + kSizeN,
+                 sz + kSizeErr + par, &b->scan};
+    d0.err_next = sz + kSizeErr + (par ^ 1);
     d0.count_row_ptr = g->row_ptr.p;
     d0.count_i64 = g->i64;
     d0.count_k = fanouts[0];
@@ -844,8 +852,8 @@ static void publish_sizes(gnnav_blocks *b, hipStream_t s) {
     for (int h = 0; h <= b->L; ++h) b->n_h[h] = b->sizes_host[kSizeN + h];
     for (int h = 1; h <= b->L; ++h) b->e_h[h] = b->sizes_host[kSizeE + h];
     b->host_sizes = true;
-    GNNAV_CHECK(b->sizes_host[kSizeErr] == 0, GNNAV_E_RANGE,
-                std::to_string(b->sizes_host[kSizeErr]) + " seed(s) outside [0, n)");
+    const int32_t bad = b->sizes_host[kSizeErr + (int)(b->calls & 1)];
+    GNNAV_CHECK(bad == 0, GNNAV_E_RANGE, std::to_string(bad) + " seed(s) outside [0, n)");
 }
 
 extern "C" gnnav_status gnnav_sample(const gnnav_graph *g, const int32_t *seeds_dev, int64_t n_seeds,

@@ -195,6 +195,7 @@ struct DedupArgs {
     int32_t count_k = 0;
     int32_t *count_indptr = nullptr;
     int32_t *count_e_out = nullptr;
+    int32_t *err_next = nullptr;  // the count slot of the next call, cleared by this one (nullable)
 };
 void launch_dedup(const DedupArgs &a, hipStream_t s);
 void launch_relabel(const int32_t *list, const int32_t *len_ptr, int64_t len_bound,

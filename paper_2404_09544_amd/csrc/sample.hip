@@ -540,12 +540,19 @@ void launch_sample_hop(const SampleHopArgs &a, hipStream_t s) {
 // ------------------------------------------------------------------ dedup
 __device__ __forceinline__ int64_t list_len(int64_t c, const int32_t *p) { return p ? (int64_t)*p : c; }
 
+// First positions of a list's ids in the node table; out-of-range ids are
+// counted into *err.  err_next (nullable) is the count slot of the next call
+// on the same blocks, cleared here so that no separate launch has to clear a
+// slot before each call (its previous value was reported by the call that
+// used it).
 __global__ void __launch_bounds__(256) k_first_position(const int32_t *__restrict__ list, int64_t len_const,
                                                         const int32_t *__restrict__ len_ptr,
                                                         unsigned long long *__restrict__ map, uint32_t tag,
-                                                        int64_t n_nodes, int32_t *__restrict__ err) {
+                                                        int64_t n_nodes, int32_t *__restrict__ err,
+                                                        int32_t *__restrict__ err_next) {
     const int64_t len = list_len(len_const, len_ptr);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    if (err_next && blockIdx.x == 0 && threadIdx.x == 0) *err_next = 0;
     int32_t bad = 0;
     for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < len; p += stride) {
         const int32_t id = list[p];
@@ -629,10 +636,11 @@ struct SeedDedupCountOp {
 };
 
 void launch_dedup(const DedupArgs &a, hipStream_t s) {
-    if (a.len_bound > 0 && !a.first_done) {
+    if ((a.len_bound > 0 || a.err_next) && !a.first_done) {
         KernelTimer t("dedup_first", s);
         hipLaunchKernelGGL(k_first_position, dim3(grid_for(a.len_bound, 256, 8192)), dim3(256), 0, s,
-                           a.list, a.len_const, a.len_ptr, (unsigned long long *)a.map, a.tag, a.n_nodes, a.err);
+                           a.list, a.len_const, a.len_ptr, (unsigned long long *)a.map, a.tag, a.n_nodes, a.err,
+                           a.err_next);
         GNNAV_HIP(hipGetLastError());
     }
     DedupOp op{a.list, a.len_const, a.len_ptr, (unsigned long long *)a.map, a.tag, a.n_nodes, a.nodes, a.base_ptr,
