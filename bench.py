@@ -422,7 +422,7 @@ def forward_legs(args, G, g, c, wl, wdev, seeds_dev, torch, MiniBatchStep, Pipel
             "link_workgroups": link_wgs, "link_est": link_est}
 
 
-def kernel_entries(args, G, g, wl, fwd, seeds_dev, ring, link, profiled_config, trace_name):
+def kernel_entries(args, G, g, c, wl, fwd, seeds_dev, ring, link, profiled_config, trace_name):
     """Per-kernel figures of a sequential leg: each kernel's algorithmic work
     over the timed batches (from their measured sizes) divided by its total
     HIP-event time, against the roofline that bounds it."""
@@ -444,11 +444,18 @@ def kernel_entries(args, G, g, wl, fwd, seeds_dev, ring, link, profiled_config, 
         work["cache_admit"] += min(misses, ring) * (2 * wl.d * elt + 16)
         for k, v in sampling_bytes(wl, n_h, e_h, off).items():
             samp[k] = samp.get(k, 0.0) + v
-        # re-sampling a batch is deterministic: regenerate its blocks (untimed)
-        # to count the distinct source rows of each aggregation
-        G.sample(g, seeds_dev[b], wl.fanouts, wl.rng_seed(b), probe)
+        # re-sampling a batch is deterministic: regenerate its blocks (untimed,
+        # with the leg's own sampler) to count the distinct source rows of
+        # each aggregation
+        if args.eta is None:
+            G.sample(g, seeds_dev[b], wl.fanouts, wl.rng_seed(b), probe)
+        else:
+            G.sample_biased(g, c, args.eta, seeds_dev[b], wl.fanouts, wl.rng_seed(b), probe)
         _, sz, ip, _, ix = probe.to_host()
-        assert sz == [int(x) for x in n_h], "re-sampled batch differs"
+        if sz != [int(x) for x in n_h]:
+            # only a biased sampler over a cache that moved since (FIFO) can
+            # do this; the distinct-row counts are then of a similar batch
+            log(f"batch {b}: re-sampled sizes {sz} differ from the timed batch's {[int(x) for x in n_h]}")
         for l in range(1, L + 1):
             hb = L - l + 1
             n_dst, E = int(n_h[hb - 1]), int(ip[hb - 1][-1])
@@ -647,7 +654,8 @@ def main():
     # static cache and uniform sampling: their bytes apply only to such runs
     profiled_config = args.eta is None and args.cache_policy == "static"
     trace_name = wl.name if r == wl.cfg["cache"] else f"{wl.name}_r{r:g}"
-    kernels, rows, fstats = kernel_entries(args, G, g, wl, fwd, seeds_dev, ring, link, profiled_config, trace_name)
+    kernels, rows, fstats = kernel_entries(args, G, g, c, wl, fwd, seeds_dev, ring, link, profiled_config,
+                                           trace_name)
     # the roofline entry: the kernel with the largest total time in the timed
     # sequential leg, whatever bounds it (the host link, HBM or the matrix
     # cores); the largest device-bound (HBM or MFMA) kernel is given beside it
@@ -671,7 +679,7 @@ def main():
         c1 = G.Cache(g, feats, wl.dtype, 1.0)
         log(f"cache r=1: C={c1.n_cached} ({time.perf_counter() - t0:.1f}s)")
         f1 = forward_legs(args, G, g, c1, wl, wdev, seeds_dev, torch, MiniBatchStep, Pipeline, link_override=64)
-        k1, rows1, _ = kernel_entries(args, G, g, wl, f1, seeds_dev, 0, link, args.eta is None,
+        k1, rows1, _ = kernel_entries(args, G, g, c1, wl, f1, seeds_dev, 0, link, args.eta is None,
                                       f"{wl.name}_r1")
         r1 = {"cache_fraction": 1.0, "value": round(wl.batch * args.steps / f1["elapsed"], 2), "unit": "seeds/s",
               "ms_per_step": round(f1["ms_per_step"], 4),
