@@ -125,7 +125,9 @@ void gnnav_graph_free(gnnav_graph *g);
  * degree (ties: smaller id first) get cache slots 0..C-1 in that order and
  * their rows are copied into HBM.  Every row is also copied into a pinned,
  * device-mapped host store (or an HBM store with GNNAV_STORE_ON_DEVICE).
- * Rows in both are padded with zeros to a 16-byte stride (see cache_info).
+ * Cache rows are padded with zeros to a 16-byte stride (see cache_info);
+ * rows of a host store start on 128-byte boundaries, so the zero-copy reads
+ * of a miss cross as few of the link's read blocks as the row allows.
  * Errors: E_INVALID (null pointers, d <= 0, cache_fraction outside [0, 1]
  * or NaN, bad dtype), E_NOMEM, E_DEVICE.  On error *out is unchanged.     */
 gnnav_status gnnav_build_cache(const gnnav_graph *g, const void *feats_host, int64_t d,
@@ -133,7 +135,7 @@ gnnav_status gnnav_build_cache(const gnnav_graph *g, const void *feats_host, int
                                gnnav_cache **out);
 
 /* Cache geometry; any output pointer may be NULL.  ld is the padded row
- * stride in elements used by the cache and the store.                   */
+ * stride in elements of the HBM cache (and of an HBM store).            */
 gnnav_status gnnav_cache_info(const gnnav_cache *c, int64_t *n_cached, int64_t *d, int64_t *ld,
                               int32_t *dtype, int32_t *store_on_device);
 

@@ -414,6 +414,7 @@ extern "C" void gnnav_graph_free(gnnav_graph *g) {
 static bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
 // ------------------------------------------------------------------ cache
+constexpr int64_t kStoreAlign = 128;  // host store row alignment, bytes (one L2 line)
 // Scratch of one gather in flight: hit/miss lists, scan partials, device
 // counts, and the second stream that carries the miss copy.  Each caller
 // stream gets its own, so gathers on different streams may overlap.
@@ -430,6 +431,7 @@ struct gnnav_cache {
     DevBuf slot_map, cache_rows, store_dev;
     void *store_host = nullptr;       // pinned, device-mapped
     void *store_ptr = nullptr;        // device-visible address of the store
+    int64_t store_pitch = 0;          // store row stride in bytes
     std::vector<int32_t> slot_host;
     std::vector<int32_t> rank_host;   // degree rank (first C fill the cache)
     std::mutex ws_mu;
@@ -551,17 +553,23 @@ extern "C" gnnav_status gnnav_build_cache(const gnnav_graph *g, const void *feat
             c->cache_rows.ensure(std::max<int64_t>(C, 1) * pitch, s0);
             upload_rows(c->cache_rows.p, feats, row_bytes, pitch, rank.data(), C);
             if (c->store_on_device) {
+                c->store_pitch = pitch;
                 c->store_dev.ensure(std::max<int64_t>(n, 1) * pitch, s0);
                 upload_rows(c->store_dev.p, feats, row_bytes, pitch, nullptr, n);
                 c->store_ptr = c->store_dev.p;
             } else {
-                const size_t bytes = (size_t)std::max<int64_t>(n, 1) * pitch;
+                // Rows of the host store start on kStoreAlign-byte boundaries:
+                // the zero-copy reads of a miss then cross as few of the
+                // link's read blocks as the row's length allows.
+                const int64_t sp = (row_bytes + kStoreAlign - 1) / kStoreAlign * kStoreAlign;
+                c->store_pitch = sp;
+                const size_t bytes = (size_t)std::max<int64_t>(n, 1) * sp;
                 host_pinned_alloc(&c->store_host, bytes, hipHostMallocMapped, "feature store");
                 uint8_t *hp = (uint8_t *)c->store_host;
                 parallel_for(n, [&](int64_t b, int64_t e) {
                     for (int64_t v = b; v < e; ++v) {
-                        std::memcpy(hp + v * pitch, feats + v * row_bytes, (size_t)row_bytes);
-                        std::memset(hp + v * pitch + row_bytes, 0, (size_t)(pitch - row_bytes));
+                        std::memcpy(hp + v * sp, feats + v * row_bytes, (size_t)row_bytes);
+                        std::memset(hp + v * sp + row_bytes, 0, (size_t)(sp - row_bytes));
                     }
                 });
                 GNNAV_HIP(hipHostGetDevicePointer(&c->store_ptr, c->store_host, 0));
@@ -826,6 +834,7 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
             a.relabel_len = sz + kSizeE + h - 1;
             a.relabel_bound = eb[h - 1];
             a.relabel_n = sz + kSizeN + h - 1;
+            a.n_nodes = g->n;
             a.relabel_indices = b->indices[h - 2].as<int32_t>();
         }
         if (h > 1) launch_count_scan(a, s);   // hop 1's ran with the seeds' dedup
@@ -834,8 +843,8 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
                      sz + kSizeN + h - 1, sz + kSizeN + h, nullptr, &b->scan, true};
         launch_dedup(dh, s);
     }
-    launch_relabel(b->nbrs[n_hops - 1].as<int32_t>(), sz + kSizeE + n_hops, eb[n_hops], map, sz + kSizeN + n_hops,
-                   b->indices[n_hops - 1].as<int32_t>(), s);
+    launch_relabel(b->nbrs[n_hops - 1].as<int32_t>(), sz + kSizeE + n_hops, eb[n_hops], map, g->n,
+                   sz + kSizeN + n_hops, b->indices[n_hops - 1].as<int32_t>(), s);
     b->L = n_hops;
     b->host_sizes = false;
     for (int h = 0; h <= n_hops; ++h) {
@@ -960,7 +969,7 @@ static void gather_impl(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_
         w->scan.ensure(n_ids, s);
     }
     GatherArgs a{ids_dev, n_ids, n_dev, c->slot_map.as<int32_t>(), c->n, c->cache_rows.p, c->store_ptr,
-                 c->ld * c->elt, out_dev, ld_out * c->elt, c->d * c->elt, counts_dev, w->dev_counts.as<int32_t>(),
+                 c->ld * c->elt, c->store_pitch, out_dev, ld_out * c->elt, c->d * c->elt, counts_dev, w->dev_counts.as<int32_t>(),
                  w->hit_list.as<int2>(), w->miss_list.as<int2>(), &w->scan, cc->link_wgs};
     launch_classify(a, s);
     if (copy_after) GNNAV_HIP(hipStreamWaitEvent(s, copy_after, 0));

@@ -167,6 +167,7 @@ struct SampleHopArgs {
     const int32_t *relabel_len = nullptr;    // device length
     int64_t relabel_bound = 0;
     const int32_t *relabel_n = nullptr;      // device size of the frontier the list was merged into
+    int64_t n_nodes = 0;                     // graph size (ids outside [0, n) are never looked up)
     int32_t *relabel_indices = nullptr;
 };
 void launch_partition_rows(const void *row_ptr, bool offsets_i64, const int32_t *col, int64_t n,
@@ -199,7 +200,8 @@ struct DedupArgs {
 };
 void launch_dedup(const DedupArgs &a, hipStream_t s);
 void launch_relabel(const int32_t *list, const int32_t *len_ptr, int64_t len_bound,
-                    const uint64_t *map, const int32_t *n_frontier, int32_t *indices, hipStream_t s);
+                    const uint64_t *map, int64_t n_nodes, const int32_t *n_frontier, int32_t *indices,
+                    hipStream_t s);
 
 // gather.hip
 struct GatherArgs {
@@ -209,8 +211,9 @@ struct GatherArgs {
     const int32_t *slot_map;
     int64_t n_nodes;
     const void *cache;       // device [C x ld]
-    const void *store;       // device-visible store [n x ld] (host-mapped or HBM)
-    int64_t src_ld_bytes;
+    const void *store;       // device-visible store [n rows] (host-mapped or HBM)
+    int64_t src_ld_bytes;    // cache row stride
+    int64_t store_ld_bytes;  // store row stride
     void *out;
     int64_t out_ld_bytes;
     int64_t row_bytes;       // d * elt

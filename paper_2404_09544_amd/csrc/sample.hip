@@ -101,13 +101,18 @@ struct CountOp {
     }
 };
 
-// Local id of a listed node from its node-table entry.  Every listed id is
-// in the frontier by the time this runs, so its entry holds a local id below
-// the frontier size; anything else (only possible after a scan whose
-// look-back wait gave up, which the next synchronisation point reports)
-// becomes 0, so no later kernel reads outside the source rows.
-__device__ __forceinline__ int32_t local_id(uint64_t entry, const int32_t *n_frontier) {
-    const uint32_t w = (uint32_t)entry;
+// Local id of the listed node `id`.  Every listed id is a node of the
+// graph and in the frontier by the time this runs, so its node-table entry
+// holds a local id below the frontier size.  Anything else is only possible
+// after a scan whose look-back wait gave up (reported by the next
+// synchronisation point), which can leave list positions unwritten by this
+// call: an id outside [0, n) is not looked up, and an entry that is not a
+// local id of this frontier becomes 0, so no later kernel reads outside its
+// buffers.
+__device__ __forceinline__ int32_t local_id(const uint64_t *map, int32_t id, int64_t n_nodes,
+                                            const int32_t *n_frontier) {
+    if (id < 0 || id >= n_nodes) return 0;
+    const uint32_t w = (uint32_t)map[id];
     return w < (uint32_t)*n_frontier ? (int32_t)w : 0;
 }
 
@@ -117,10 +122,11 @@ struct RelabelSide {
     const int32_t *list;
     const int32_t *len_ptr;
     const uint64_t *map;
+    int64_t n_nodes;
     const int32_t *n_frontier;
     int32_t *indices;
     __device__ int64_t n() const { return *len_ptr; }
-    __device__ void run(int64_t p) const { indices[p] = local_id(map[list[p]], n_frontier); }
+    __device__ void run(int64_t p) const { indices[p] = local_id(map, list[p], n_nodes, n_frontier); }
 };
 
 void launch_count_scan(const SampleHopArgs &a, hipStream_t s) {
@@ -129,7 +135,7 @@ void launch_count_scan(const SampleHopArgs &a, hipStream_t s) {
         if (a.relabel_list)
             run_scan<Op, int32_t, RelabelSide>(
                 op, a.rows_bound, *a.scan, "count_scan", s,
-                RelabelSide{a.relabel_list, a.relabel_len, a.first_map, a.relabel_n, a.relabel_indices},
+                RelabelSide{a.relabel_list, a.relabel_len, a.first_map, a.n_nodes, a.relabel_n, a.relabel_indices},
                 a.relabel_bound);
         else
             run_scan<Op, int32_t>(op, a.rows_bound, *a.scan, "count_scan", s);
@@ -662,21 +668,21 @@ void launch_dedup(const DedupArgs &a, hipStream_t s) {
 
 __global__ void __launch_bounds__(256) k_relabel(const int32_t *__restrict__ list,
                                                  const int32_t *__restrict__ len_ptr,
-                                                 const uint64_t *__restrict__ map,
+                                                 const uint64_t *__restrict__ map, int64_t n_nodes,
                                                  const int32_t *__restrict__ n_frontier,
                                                  int32_t *__restrict__ indices) {
     const int64_t len = *len_ptr;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < len; p += stride)
-        indices[p] = local_id(map[list[p]], n_frontier);
+        indices[p] = local_id(map, list[p], n_nodes, n_frontier);
 }
 
 void launch_relabel(const int32_t *list, const int32_t *len_ptr, int64_t len_bound, const uint64_t *map,
-                    const int32_t *n_frontier, int32_t *indices, hipStream_t s) {
+                    int64_t n_nodes, const int32_t *n_frontier, int32_t *indices, hipStream_t s) {
     if (len_bound <= 0) return;
     KernelTimer t("relabel", s);
     hipLaunchKernelGGL(k_relabel, dim3(grid_for(len_bound, 256, 8192)), dim3(256), 0, s, list, len_ptr,
-                       map, n_frontier, indices);
+                       map, n_nodes, n_frontier, indices);
     GNNAV_HIP(hipGetLastError());
 }
 
