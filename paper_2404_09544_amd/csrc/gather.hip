@@ -77,12 +77,14 @@ void launch_classify(const GatherArgs &a, hipStream_t s) {
 // second stream (a second stream would share one of the process's few
 // hardware queues with other work and hold it for the whole transfer).
 // G lanes per row (power of two), 64/G rows per wavefront pass; lane c0
-// moves 16-byte units c0, c0 + G, ... of its row.  A miss lane group keeps
-// U rows in flight, each row's units (up to 4 per lane) loaded before any is
-// stored: a zero-copy read waits microseconds, so the link needs many reads
-// outstanding per wavefront (measured: 400-byte rows 41.6 -> 43.7 GB/s).  A
-// hit lane group copies one row at a time, four units in flight (more rows
-// at once measured slower from HBM: 90 -> 170 us for 99.6k 2.4 KB rows).
+// moves 16-byte units c0, c0 + G, ... of its row.  For rows of at most 512
+// bytes (G < 64) a miss lane group keeps 4 rows in flight, each row's units
+// loaded before any is stored: a zero-copy read waits microseconds, so short
+// rows need several outstanding per lane (400-byte rows: 41.6 -> 43.7 GB/s).
+// Longer rows already keep several units per lane in flight, and more rows
+// at once measured slower (2.4 KB rows: 55.9 -> 55.1 GB/s with 4, and the
+// pipelined step slower still); hits copy one row at a time (four rows in
+// flight measured 90 -> 170 us for 99.6k 2.4 KB rows from HBM).
 // A list entry whose output row lies outside the request count is skipped:
 // only a classification whose scan gave up (reported as a device error) can
 // leave such an entry, a stale one of an earlier call, and the output
@@ -153,7 +155,8 @@ __global__ void __launch_bounds__(256) k_gather_rows(const int2 *__restrict__ hi
     const int64_t nwaves = nblocks * (blockDim.x / kWave);
     const int64_t first = ((block * blockDim.x + threadIdx.x) / kWave) * RPW + sub, step = nwaves * RPW;
     if (miss)
-        copy_rows<G, 4>(miss_list, dev_counts[1], first, step, n_req, store, store_ld16, out, out_ld16, chunks, c0);
+        copy_rows<G, (G < kWave ? 4 : 1)>(miss_list, dev_counts[1], first, step, n_req, store, store_ld16, out,
+                                          out_ld16, chunks, c0);
     else
         copy_rows<G, 1>(hit_list, dev_counts[0], first, step, n_req, cache, cache_ld16, out, out_ld16, chunks, c0);
 }
