@@ -314,26 +314,39 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
 SIZE_SLOTS = 24      # device size array: |F_h| at [h], E_h at [17 + h] (L <= 3 fits in 24)
 
 
-def sampling_bytes(wl, n_h, e_h, off_bytes: int) -> dict:
+def sampling_bytes(wl, n_h, e_h, off_bytes: int, max_deg: int) -> dict:
     """Algorithmic bytes of one batch's sampling-chain kernels (Eq. 2 and its
     union), by kernel label: each datum a kernel must read or write counted
-    once at its own width -- 4-byte ids and counts, `off_bytes` row offsets,
-    8-byte node-table entries (an atomic update counted as a read and a
-    write).  These kernels make 4- to 8-byte random accesses, so they are
-    bound by memory transactions, not by these bytes."""
+    once at its own width -- 4-byte ids, counts and slots, `off_bytes` row
+    offsets, 8-byte node-table entries (an atomic update counted as a read
+    and a write).  A hop with 0 < k <= 64 samples into a slot list of
+    min(k, max_deg) slots per row that its dedup scan compacts (no count
+    scan); other hops count first.  These kernels make 4- to 8-byte random
+    accesses, so they are bound by memory transactions, not by these bytes."""
     L = wl.L
     b0 = wl.batch
+    slotted = [0 < k <= 64 and max_deg > 0 for k in wl.fanouts]
+    # the seeds' dedup: ids, table, F_0; with hop 1's counts when hop 1 counts
     out = {"dedup_first": b0 * (4 + 16),
-           # the seeds' dedup with hop 1's counts: ids, table, F_0, row offsets, indptr_1
-           "dedup_scan": b0 * (4 + 8) + n_h[0] * (4 + 8 + 2 * off_bytes + 4) + 4,
+           "dedup_scan": b0 * (4 + 8) + n_h[0] * (4 + 8)
+           + (0 if slotted[0] else n_h[0] * (2 * off_bytes + 4) + 4),
            "sample_hop": 0, "count_scan": 0, "relabel": 0}
     for h in range(1, L + 1):
         rows, e, new = n_h[h - 1], e_h[h], n_h[h] - n_h[h - 1]
-        # rows' ids, offsets and indptr; picked columns read, neighbours written, first positions noted
-        out["sample_hop"] += rows * (4 + 2 * off_bytes + 4) + e * (4 + 4 + 16)
-        out["dedup_scan"] += e * (4 + 8) + new * (4 + 8)
-        if h >= 2:   # this hop's counts plus hop h-1's relabel riding along
-            out["count_scan"] += rows * (4 + 2 * off_bytes) + (rows + 1) * 4 + e_h[h - 1] * (4 + 8 + 4)
+        relabel_prev = e_h[h - 1] * (4 + 8 + 4) if h >= 2 else 0
+        if slotted[h - 1]:
+            slots = rows * min(wl.fanouts[h - 1], max_deg)
+            # rows' ids and offsets, every slot written, picked columns read, first positions noted
+            out["sample_hop"] += rows * (4 + 2 * off_bytes) + slots * 4 + e * (4 + 16)
+            # slots read, table read for used slots, N_h and indptr written, new
+            # ids appended; hop h-1's relabel riding along
+            out["dedup_scan"] += slots * 4 + e * (8 + 4) + (rows + 1) * 4 + new * (4 + 8) + relabel_prev
+        else:
+            # rows' ids, offsets and indptr; picked columns read, neighbours written, first positions noted
+            out["sample_hop"] += rows * (4 + 2 * off_bytes + 4) + e * (4 + 4 + 16)
+            out["dedup_scan"] += e * (4 + 8) + new * (4 + 8)
+            if h >= 2:   # this hop's counts plus hop h-1's relabel riding along
+                out["count_scan"] += rows * (4 + 2 * off_bytes) + (rows + 1) * 4 + relabel_prev
     out["relabel"] = e_h[L] * (4 + 8 + 4)
     out["classify"] = n_h[L] * (4 + 4 + 8)
     return out
@@ -442,7 +455,7 @@ def kernel_entries(args, G, g, c, wl, fwd, seeds_dev, ring, link, profiled_confi
         hit_bytes += hits * (2 * wl.d * elt + 8)
         miss_bytes += misses * wl.d * elt
         work["cache_admit"] += min(misses, ring) * (2 * wl.d * elt + 16)
-        for k, v in sampling_bytes(wl, n_h, e_h, off).items():
+        for k, v in sampling_bytes(wl, n_h, e_h, off, g.max_degree).items():
             samp[k] = samp.get(k, 0.0) + v
         # re-sampling a batch is deterministic: regenerate its blocks (untimed,
         # with the leg's own sampler) to count the distinct source rows of

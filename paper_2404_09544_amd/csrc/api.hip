@@ -661,6 +661,7 @@ extern "C" void gnnav_cache_free(gnnav_cache *c) { free_cache(c); }
 // ----------------------------------------------------------------- blocks
 namespace {
 constexpr int kMaxHops = 16;
+constexpr int32_t kSlotFanout = 64;   // largest fanout sampled into slot lists
 constexpr int kSizeN = 0;         // sizes[kSizeN + h] = |F_h|
 constexpr int kSizeE = 17;        // sizes[kSizeE + h] = E_h (h >= 1)
 constexpr int kSizeErr = 40;      // out-of-range seed count: slot 40 + (call parity)
@@ -680,6 +681,7 @@ struct gnnav_blocks {
     DevBuf map, sizes, nodes;
     ScanState scan;
     DevBuf indptr[kMaxHops], nbrs[kMaxHops], indices[kMaxHops];
+    DevBuf slots[kMaxHops];            // slot lists of hops with 0 < k <= 64
     int32_t *sizes_host = nullptr;  // pinned mirror of `sizes`
     DevBuf agg, hid[2];             // forward workspace
     // training: activations kept per layer, gradients, transposed blocks
@@ -714,6 +716,7 @@ extern "C" void gnnav_blocks_free(gnnav_blocks *b) {
         b->indptr[h].release();
         b->nbrs[h].release();
         b->indices[h].release();
+        b->slots[h].release();
     }
     b->agg.release();
     b->hid[0].release();
@@ -750,10 +753,15 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
     // Eq. 12 capacity bounds (tau = 1, no overlap): E_h <= n_(h-1) * k_h,
     // n_h <= min(n, n_(h-1) + E_h).
     int64_t nb[kMaxHops + 1], eb[kMaxHops + 1];
+    // Hops with 0 < k <= 64 sample into slot lists of stride min(k, max
+    // degree) (no count scan before them); the stride is also their per-row
+    // edge bound.
+    int32_t stride[kMaxHops + 1] = {0};
     nb[0] = std::min<int64_t>(n_seeds, g->n);
     eb[0] = 0;
     for (int h = 1; h <= n_hops; ++h) {
         const int64_t k = fanouts[h - 1] < 0 ? g->max_deg : std::min<int64_t>(fanouts[h - 1], g->max_deg);
+        if (fanouts[h - 1] > 0 && fanouts[h - 1] <= kSlotFanout && k > 0) stride[h] = (int32_t)k;
         eb[h] = nb[h - 1] * k;
         nb[h] = std::min<int64_t>(g->n, nb[h - 1] + eb[h]);
         GNNAV_CHECK(eb[h] < INT32_MAX && nb[h] < INT32_MAX, GNNAV_E_CAPACITY,
@@ -803,6 +811,7 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
         b->indptr[h - 1].ensure((nb[h - 1] + 1) * sizeof(int32_t), s);
         b->nbrs[h - 1].ensure(std::max<int64_t>(eb[h], 1) * sizeof(int32_t), s);
         b->indices[h - 1].ensure(std::max<int64_t>(eb[h], 1) * sizeof(int32_t), s);
+        if (stride[h]) b->slots[h - 1].ensure(std::max<int64_t>(eb[h], 1) * sizeof(int32_t), s);
     }
     int32_t *sz = b->sizes.as<int32_t>();
     uint64_t *map = b->map.as<uint64_t>();
@@ -811,36 +820,58 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
     // count alternates between two slots, the other one cleared by this call
     // for the next (so no clearing launch is needed).
     const int par = (int)(++b->calls & 1);
-    // F_0 (seeds without repeats, first occurrence kept) and hop 1's row
-    // counts (indptr_1, E_1) in one scan
+    // F_0 (seeds without repeats, first occurrence kept), with hop 1's row
+    // counts (indptr_1, E_1) in the same scan unless hop 1 uses a slot list
     DedupArgs d0{seeds_dev, n_seeds, nullptr, n_seeds, map, tag, g->n, nodes, nullptr, sz + kSizeN,
                  sz + kSizeErr + par, &b->scan};
     d0.err_next = sz + kSizeErr + (par ^ 1);
-    d0.count_row_ptr = g->row_ptr.p;
-    d0.count_i64 = g->i64;
-    d0.count_k = fanouts[0];
-    d0.count_indptr = b->indptr[0].as<int32_t>();
-    d0.count_e_out = sz + kSizeE + 1;
+    if (!stride[1]) {
+        d0.count_row_ptr = g->row_ptr.p;
+        d0.count_i64 = g->i64;
+        d0.count_k = fanouts[0];
+        d0.count_indptr = b->indptr[0].as<int32_t>();
+        d0.count_e_out = sz + kSizeE + 1;
+    }
     launch_dedup(d0, s);
     for (int h = 1; h <= n_hops; ++h) {
+        const bool slotted = stride[h] > 0;
         SampleHopArgs a{g->row_ptr.p, g->i64, g->col.as<int32_t>(), nodes, sz + kSizeN + h - 1,
-                        b->indptr[h - 1].as<int32_t>(), b->nbrs[h - 1].as<int32_t>(), sz + kSizeE + h,
-                        fanouts[h - 1], rng_seed, (uint32_t)(h - 1), nb[h - 1], &b->scan,
+                        b->indptr[h - 1].as<int32_t>(), (slotted ? b->slots : b->nbrs)[h - 1].as<int32_t>(),
+                        sz + kSizeE + h, fanouts[h - 1], rng_seed, (uint32_t)(h - 1), nb[h - 1], &b->scan,
                         bias ? bias->slot_map.as<int32_t>() : nullptr, eta,
                         bias && bias->ring_n == 0 ? bias->part_col.as<int32_t>() : nullptr,
                         bias && bias->ring_n == 0 ? bias->part_cnt.as<int32_t>() : nullptr, map, tag};
-        if (h > 1) {   // hop h - 1's relabel rides along with this count scan
-            a.relabel_list = b->nbrs[h - 2].as<int32_t>();
-            a.relabel_len = sz + kSizeE + h - 1;
-            a.relabel_bound = eb[h - 1];
-            a.relabel_n = sz + kSizeN + h - 1;
-            a.n_nodes = g->n;
-            a.relabel_indices = b->indices[h - 2].as<int32_t>();
+        a.slot_stride = stride[h];
+        a.n_nodes = g->n;
+        // hop h - 1's relabel rides along with this hop's first scan
+        const int32_t *rl_list = h > 1 ? b->nbrs[h - 2].as<int32_t>() : nullptr;
+        if (!slotted) {
+            if (rl_list) {
+                a.relabel_list = rl_list;
+                a.relabel_len = sz + kSizeE + h - 1;
+                a.relabel_bound = eb[h - 1];
+                a.relabel_n = sz + kSizeN + h - 1;
+                a.relabel_indices = b->indices[h - 2].as<int32_t>();
+            }
+            if (h > 1) launch_count_scan(a, s);   // hop 1's ran with the seeds' dedup
         }
-        if (h > 1) launch_count_scan(a, s);   // hop 1's ran with the seeds' dedup
         launch_sample_hop(a, s);
-        DedupArgs dh{b->nbrs[h - 1].as<int32_t>(), 0, sz + kSizeE + h, eb[h], map, tag, g->n, nodes,
-                     sz + kSizeN + h - 1, sz + kSizeN + h, nullptr, &b->scan, true};
+        DedupArgs dh{(slotted ? b->slots : b->nbrs)[h - 1].as<int32_t>(), 0, sz + kSizeE + h, eb[h], map, tag,
+                     g->n, nodes, sz + kSizeN + h - 1, sz + kSizeN + h, nullptr, &b->scan, true};
+        if (slotted) {
+            dh.len_ptr = nullptr;
+            dh.slot_stride = stride[h];
+            dh.compact_out = b->nbrs[h - 1].as<int32_t>();
+            dh.indptr_out = b->indptr[h - 1].as<int32_t>();
+            dh.e_out = sz + kSizeE + h;
+            if (rl_list) {
+                dh.relabel_list = rl_list;
+                dh.relabel_len = sz + kSizeE + h - 1;
+                dh.relabel_bound = eb[h - 1];
+                dh.relabel_n = sz + kSizeN + h - 1;
+                dh.relabel_indices = b->indices[h - 2].as<int32_t>();
+            }
+        }
         launch_dedup(dh, s);
     }
     launch_relabel(b->nbrs[n_hops - 1].as<int32_t>(), sz + kSizeE + n_hops, eb[n_hops], map, g->n,

@@ -169,6 +169,10 @@ struct SampleHopArgs {
     const int32_t *relabel_n = nullptr;      // device size of the frontier the list was merged into
     int64_t n_nodes = 0;                     // graph size (ids outside [0, n) are never looked up)
     int32_t *relabel_indices = nullptr;
+    // > 0: row i's picks go to slots [i * slot_stride, (i + 1) * slot_stride)
+    // of nbrs (unused slots -1) and indptr is not read; the dedup of the slot
+    // list then compacts it (no count scan before the hop)
+    int32_t slot_stride = 0;
 };
 void launch_partition_rows(const void *row_ptr, bool offsets_i64, const int32_t *col, int64_t n,
                            const int32_t *slot_map, int32_t *part_col, int32_t *part_cnt, hipStream_t s);
@@ -197,6 +201,20 @@ struct DedupArgs {
     int32_t *count_indptr = nullptr;
     int32_t *count_e_out = nullptr;
     int32_t *err_next = nullptr;  // the count slot of the next call, cleared by this one (nullable)
+    // optional, a slot list (SampleHopArgs::slot_stride): `list` holds
+    // *base_ptr rows of slot_stride slots, -1 where unused; the scan also
+    // writes the used slots in order to compact_out, their row offsets to
+    // indptr_out (*base_ptr + 1 entries) and their count to e_out
+    int32_t slot_stride = 0;
+    int32_t *compact_out = nullptr;
+    int32_t *indptr_out = nullptr;
+    int32_t *e_out = nullptr;
+    // optional: the previous hop's relabel, run in this scan's launch
+    const int32_t *relabel_list = nullptr;
+    const int32_t *relabel_len = nullptr;
+    int64_t relabel_bound = 0;
+    const int32_t *relabel_n = nullptr;
+    int32_t *relabel_indices = nullptr;
 };
 void launch_dedup(const DedupArgs &a, hipStream_t s);
 void launch_relabel(const int32_t *list, const int32_t *len_ptr, int64_t len_bound,

@@ -1,16 +1,22 @@
 // Eq. 2 node-wise fanout sampling and the per-hop frontier union.
 //
-// Per hop h:
-//   count scan   indptr_h = exclusive scan of min(deg(v), k) over F_(h-1)
-//                (for h = 1 folded into the seeds' dedup scan; for h > 1 it
-//                also carries hop h-1's relabel on extra workgroups)
+// Per hop h, for 0 < k <= 64 (slot lists):
 //   sample       one or more rows per wavefront: copy the row when
-//                deg <= k, else Floyd's k-subset with Philox4x32-10 draws
-//   dedup        first position of each id in N_h (atomicMin on a dense
-//                per-node table, taken by the sample kernel as it writes
-//                N_h), then an order-preserving scan appends the new ids to
-//                the node list and records their local ids
+//                deg <= k, else Floyd's k-subset with Philox4x32-10 draws;
+//                row i writes slots [i s, (i + 1) s) of a slot list,
+//                s = min(k, max degree), unused slots -1
+//   dedup        first position of each id in the slot list (atomicMin on a
+//                dense per-node table, taken by the sample kernel as it
+//                writes), then one order-preserving scan of (used, first)
+//                pairs compacts the slot list into N_h, writes indptr_h and
+//                E_h, appends the new ids to the node list and records their
+//                local ids; hop h-1's relabel rides along on extra workgroups
 //   relabel      indices_h[p] = local id of N_h[p]
+// For other fanouts (k < 0: every neighbour; k > 64) a count scan comes
+// first, indptr_h = exclusive scan of min(deg(v), k) over F_(h-1) (for h = 1
+// folded into the seeds' dedup scan; for h > 1 carrying hop h-1's relabel),
+// the sample kernel writes N_h at those offsets and the dedup scan only
+// appends the new ids.
 // The node table lives in HBM, one 64-bit entry per graph node:
 // (tag << 32) | word with tag = 0xffffffff - (the sampling call's epoch), so
 // every entry left by an earlier call compares above every entry of the
@@ -79,6 +85,20 @@ __device__ __forceinline__ int64_t row_degree(const OffT *rp, int32_t v, int64_t
     return (int64_t)rp[v + 1] - start;
 }
 
+// The degree of frontier entry v.  Frontier entries are graph nodes; one
+// outside [0, n) is only possible after a scan whose look-back wait gave up
+// (reported by the next synchronisation point), which can leave stale list
+// positions: it counts as a row without neighbours, so no read leaves the
+// CSR.
+template <class OffT>
+__device__ __forceinline__ int64_t frontier_degree(const OffT *rp, int32_t v, int64_t n_nodes, int64_t &start) {
+    if (v < 0 || v >= n_nodes) {
+        start = 0;
+        return 0;
+    }
+    return row_degree(rp, v, start);
+}
+
 // ------------------------------------------------------------ count scan
 template <class OffT>
 struct CountOp {
@@ -88,10 +108,11 @@ struct CountOp {
     int32_t k;
     int32_t *indptr;
     int32_t *e_out;
+    int64_t n_nodes;
     __device__ int64_t n() const { return *n_ptr; }
     __device__ int32_t value(int64_t i) const {
         int64_t st;
-        int64_t deg = row_degree(row_ptr, nodes[i], st);
+        int64_t deg = frontier_degree(row_ptr, nodes[i], n_nodes, st);
         return (int32_t)((k < 0 || deg <= k) ? deg : k);
     }
     __device__ void emit(int64_t i, int32_t prefix, int32_t) const { indptr[i] = prefix; }
@@ -141,9 +162,9 @@ void launch_count_scan(const SampleHopArgs &a, hipStream_t s) {
             run_scan<Op, int32_t>(op, a.rows_bound, *a.scan, "count_scan", s);
     };
     if (a.offsets_i64)
-        run(CountOp<int64_t>{(const int64_t *)a.row_ptr, a.nodes, a.n_prev, a.fanout, a.indptr, a.e_out});
+        run(CountOp<int64_t>{(const int64_t *)a.row_ptr, a.nodes, a.n_prev, a.fanout, a.indptr, a.e_out, a.n_nodes});
     else
-        run(CountOp<int32_t>{(const int32_t *)a.row_ptr, a.nodes, a.n_prev, a.fanout, a.indptr, a.e_out});
+        run(CountOp<int32_t>{(const int32_t *)a.row_ptr, a.nodes, a.n_prev, a.fanout, a.indptr, a.e_out, a.n_nodes});
 }
 
 __device__ __forceinline__ uint64_t node_position(uint32_t tag, int64_t p) {
@@ -175,15 +196,16 @@ __global__ void __launch_bounds__(256) k_sample_small(const OffT *__restrict__ r
                                                       const int32_t *__restrict__ indptr,
                                                       int32_t *__restrict__ out, int32_t k,
                                                       uint32_t key0, uint32_t key1, uint32_t hop,
-                                                      unsigned long long *__restrict__ first, uint32_t tag) {
+                                                      unsigned long long *__restrict__ first, uint32_t tag,
+                                                      int32_t stride, int64_t n_nodes) {
     const int lane = lane_id();
     const int64_t n_rows = *n_prev;
     const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
     for (int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave; i < n_rows; i += nwaves) {
         const int32_t v = nodes[i];
         int64_t start;
-        const int64_t deg = row_degree(row_ptr, v, start);
-        const int64_t at = indptr[i];
+        const int64_t deg = frontier_degree(row_ptr, v, n_nodes, start);
+        const int64_t at = stride ? i * stride : (int64_t)indptr[i];
         int32_t *dst = out + at;
         if (k < 0 || deg <= k) {
             for (int64_t j = lane; j < deg; j += kWave) {
@@ -191,6 +213,7 @@ __global__ void __launch_bounds__(256) k_sample_small(const OffT *__restrict__ r
                 dst[j] = id;
                 note_first(first, tag, id, at + j);
             }
+            for (int64_t j = deg + lane; j < stride; j += kWave) dst[j] = -1;
             continue;
         }
         uint32_t t = 0, m = 0;
@@ -225,7 +248,8 @@ __global__ void __launch_bounds__(256) k_sample_group(const OffT *__restrict__ r
                                                       const int32_t *__restrict__ indptr,
                                                       int32_t *__restrict__ out, int32_t k,
                                                       uint32_t key0, uint32_t key1, uint32_t hop,
-                                                      unsigned long long *__restrict__ first, uint32_t tag) {
+                                                      unsigned long long *__restrict__ first, uint32_t tag,
+                                                      int32_t stride, int64_t n_nodes) {
     constexpr int R = kWave / G;
     const int lane = lane_id(), r = lane / G, gl = lane % G;
     const int64_t n_rows = *n_prev;
@@ -238,8 +262,8 @@ __global__ void __launch_bounds__(256) k_sample_group(const OffT *__restrict__ r
         int64_t start = 0, deg = 0, at = 0;
         if (valid) {
             v = nodes[i];
-            deg = row_degree(row_ptr, v, start);
-            at = indptr[i];
+            deg = frontier_degree(row_ptr, v, n_nodes, start);
+            at = stride ? i * stride : (int64_t)indptr[i];
         }
         const bool draw = valid && deg > k;
         uint32_t t = 0, m = 0;
@@ -259,6 +283,8 @@ __global__ void __launch_bounds__(256) k_sample_group(const OffT *__restrict__ r
             const int32_t id = col[start + (draw ? (int64_t)pick : (int64_t)gl)];
             out[at + gl] = id;
             note_first(first, tag, id, at + gl);
+        } else if (valid && gl < stride) {
+            out[at + gl] = -1;
         }
     }
 }
@@ -275,7 +301,8 @@ __global__ void __launch_bounds__(256) k_sample_big(const OffT *__restrict__ row
                                                     const int32_t *__restrict__ indptr,
                                                     int32_t *__restrict__ out, int32_t k,
                                                     uint32_t key0, uint32_t key1, uint32_t hop,
-                                                    unsigned long long *__restrict__ first, uint32_t tag) {
+                                                    unsigned long long *__restrict__ first, uint32_t tag,
+                                                    int32_t stride, int64_t n_nodes) {
     __shared__ uint32_t taken_all[256 / kWave][kMaxFanout];
     uint32_t *taken = taken_all[threadIdx.x / kWave];
     const int lane = lane_id();
@@ -284,8 +311,8 @@ __global__ void __launch_bounds__(256) k_sample_big(const OffT *__restrict__ row
     for (int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave; i < n_rows; i += nwaves) {
         const int32_t v = nodes[i];
         int64_t start;
-        const int64_t deg = row_degree(row_ptr, v, start);
-        const int64_t at = indptr[i];
+        const int64_t deg = frontier_degree(row_ptr, v, n_nodes, start);
+        const int64_t at = stride ? i * stride : (int64_t)indptr[i];
         int32_t *dst = out + at;
         if (deg <= k) {
             for (int64_t j = lane; j < deg; j += kWave) {
@@ -293,6 +320,7 @@ __global__ void __launch_bounds__(256) k_sample_big(const OffT *__restrict__ row
                 dst[j] = id;
                 note_first(first, tag, id, at + j);
             }
+            for (int64_t j = deg + lane; j < stride; j += kWave) dst[j] = -1;
             continue;
         }
         for (int jb = 0; jb < k; jb += kWave) {
@@ -348,15 +376,16 @@ __global__ void __launch_bounds__(256) k_sample_biased(const OffT *__restrict__ 
                                                        const int32_t *__restrict__ slot_map, uint32_t eta,
                                                        const int32_t *__restrict__ part_col,
                                                        const int32_t *__restrict__ part_cnt,
-                                                       unsigned long long *__restrict__ first, uint32_t tag) {
+                                                       unsigned long long *__restrict__ first, uint32_t tag,
+                                                       int32_t stride, int64_t n_nodes) {
     const int lane = lane_id();
     const int64_t n_rows = *n_prev;
     const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
     for (int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave; i < n_rows; i += nwaves) {
         const int32_t v = nodes[i];
         int64_t start;
-        const int64_t deg = row_degree(row_ptr, v, start);
-        const int64_t at = indptr[i];
+        const int64_t deg = frontier_degree(row_ptr, v, n_nodes, start);
+        const int64_t at = stride ? i * stride : (int64_t)indptr[i];
         int32_t *dst = out + at;
         if (k < 0 || deg <= k) {
             for (int64_t j = lane; j < deg; j += kWave) {
@@ -364,6 +393,7 @@ __global__ void __launch_bounds__(256) k_sample_biased(const OffT *__restrict__ 
                 dst[j] = id;
                 note_first(first, tag, id, at + j);
             }
+            for (int64_t j = deg + lane; j < stride; j += kWave) dst[j] = -1;
             continue;
         }
         // cached neighbours of the row
@@ -498,21 +528,27 @@ void launch_sample_hop(const SampleHopArgs &a, hipStream_t s) {
     if (a.rows_bound <= 0) return;
     if (a.bias_slot_map) {
         GNNAV_CHECK(a.fanout <= kWave, GNNAV_E_INVALID, "biased sampling supports fanouts up to 64");
+        GNNAV_CHECK(a.slot_stride == 0 || (a.fanout > 0 && a.slot_stride <= a.fanout), GNNAV_E_INVALID,
+                    "slot lists need 0 < slot stride <= fanout");
         const uint32_t key0 = (uint32_t)(a.rng_seed & 0xffffffffu), key1 = (uint32_t)(a.rng_seed >> 32);
         const unsigned grid = grid_for(a.rows_bound, 256 / kWave, 16384);
         KernelTimer t("sample_hop", s);
         if (a.offsets_i64)
             hipLaunchKernelGGL(k_sample_biased<int64_t>, dim3(grid), dim3(256), 0, s, (const int64_t *)a.row_ptr, a.col,
                                a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, a.bias_slot_map,
-                               a.eta, a.part_col, a.part_cnt, (unsigned long long *)a.first_map, a.map_tag);
+                               a.eta, a.part_col, a.part_cnt, (unsigned long long *)a.first_map, a.map_tag,
+                               a.slot_stride, a.n_nodes);
         else
             hipLaunchKernelGGL(k_sample_biased<int32_t>, dim3(grid), dim3(256), 0, s, (const int32_t *)a.row_ptr, a.col,
                                a.nodes, a.n_prev, a.indptr, a.nbrs, a.fanout, key0, key1, a.hop, a.bias_slot_map,
-                               a.eta, a.part_col, a.part_cnt, (unsigned long long *)a.first_map, a.map_tag);
+                               a.eta, a.part_col, a.part_cnt, (unsigned long long *)a.first_map, a.map_tag,
+                               a.slot_stride, a.n_nodes);
         GNNAV_HIP(hipGetLastError());
         return;
     }
     GNNAV_CHECK(a.fanout <= kMaxFanout, GNNAV_E_INVALID, "fanout above 1024");
+    GNNAV_CHECK(a.slot_stride == 0 || (a.fanout > 0 && a.fanout <= kWave && a.slot_stride <= a.fanout),
+                GNNAV_E_INVALID, "slot lists need 0 < slot stride <= fanout <= 64");
     const uint32_t key0 = (uint32_t)(a.rng_seed & 0xffffffffu), key1 = (uint32_t)(a.rng_seed >> 32);
     const unsigned grid = grid_for(a.rows_bound, 256 / kWave, 16384);
     KernelTimer t("sample_hop", s);
@@ -523,7 +559,7 @@ void launch_sample_hop(const SampleHopArgs &a, hipStream_t s) {
         auto group = [&](auto kern, int rows_per_wave) {
             hipLaunchKernelGGL(kern, dim3(grid_for(a.rows_bound, (256 / kWave) * rows_per_wave, 16384)), dim3(256), 0,
                                s, row_ptr, a.col, a.nodes, a.n_prev, a.indptr, a.nbrs, k, key0, key1, a.hop, first,
-                               a.map_tag);
+                               a.map_tag, a.slot_stride, a.n_nodes);
         };
         if (k > 0 && k <= 8)
             group(k_sample_group<OffT, 8>, 8);
@@ -534,7 +570,7 @@ void launch_sample_hop(const SampleHopArgs &a, hipStream_t s) {
         else
             hipLaunchKernelGGL(k > kWave ? k_sample_big<OffT> : k_sample_small<OffT>, dim3(grid), dim3(256), 0, s,
                                row_ptr, a.col, a.nodes, a.n_prev, a.indptr, a.nbrs, k, key0, key1, a.hop, first,
-                               a.map_tag);
+                               a.map_tag, a.slot_stride, a.n_nodes);
     };
     if (a.offsets_i64)
         run((const int64_t *)a.row_ptr);
@@ -641,6 +677,54 @@ struct SeedDedupCountOp {
     }
 };
 
+// The dedup of a slot list (rows of `stride` slots, -1 where unused), with
+// the list's compaction folded in: one scan of (used, first) pairs, the used
+// count in the high half, gives every used slot its position in N_h, every
+// row its offset (the prefix at its first slot) and every first occurrence
+// its local id.  The slot list is in row order, so N_h keeps the order of
+// the rows and, within a row, of the picks.
+struct DedupCompactOp {
+    const int32_t *slots;
+    const int32_t *rows_ptr;   // device: rows (= |F_(h-1)|, also the local id base)
+    int32_t stride;
+    unsigned long long *map;
+    uint32_t tag;
+    int64_t n_nodes;
+    int32_t *nodes;
+    int32_t *size_out;
+    int32_t *compact;
+    int32_t *indptr;
+    int32_t *e_out;
+    struct Item {
+        int32_t id, used, first;
+    };
+    __device__ int64_t n() const { return (int64_t)*rows_ptr * stride; }
+    __device__ Item load(int64_t p) const {
+        const int32_t id = slots[p];
+        if (id < 0 || id >= n_nodes) return Item{id, 0, 0};
+        return Item{id, 1, map[id] == node_position(tag, p) ? 1 : 0};
+    }
+    __device__ int64_t value(const Item &it) const { return ((int64_t)it.used << 32) | (int64_t)it.first; }
+    __device__ void emit(int64_t p, int64_t prefix, int64_t, const Item &it) const {
+        const int32_t at = (int32_t)(prefix >> 32);
+        const int64_t row = p / stride;
+        if (row * stride == p) indptr[row] = at;
+        if (!it.used) return;
+        compact[at] = it.id;
+        if (it.first) {
+            const int32_t local = *rows_ptr + (int32_t)(prefix & 0xffffffff);
+            nodes[local] = it.id;
+            map[it.id] = node_local(tag, local);
+        }
+    }
+    __device__ void total(int64_t t) const {
+        const int32_t e = (int32_t)(t >> 32), rows = *rows_ptr;
+        indptr[rows] = e;
+        *e_out = e;
+        *size_out = rows + (int32_t)(t & 0xffffffff);
+    }
+};
+
 void launch_dedup(const DedupArgs &a, hipStream_t s) {
     if ((a.len_bound > 0 || a.err_next) && !a.first_done) {
         KernelTimer t("dedup_first", s);
@@ -648,6 +732,20 @@ void launch_dedup(const DedupArgs &a, hipStream_t s) {
                            a.list, a.len_const, a.len_ptr, (unsigned long long *)a.map, a.tag, a.n_nodes, a.err,
                            a.err_next);
         GNNAV_HIP(hipGetLastError());
+    }
+    if (a.slot_stride > 0) {
+        GNNAV_CHECK(a.first_done && a.base_ptr && a.compact_out && a.indptr_out && a.e_out, GNNAV_E_INVALID,
+                    "a slot list's dedup needs its sampler's first positions, row count and outputs");
+        DedupCompactOp op{a.list, a.base_ptr, a.slot_stride, (unsigned long long *)a.map, a.tag, a.n_nodes,
+                          a.nodes, a.size_out, a.compact_out, a.indptr_out, a.e_out};
+        if (a.relabel_list)
+            run_scan<DedupCompactOp, int64_t, RelabelSide>(
+                op, a.len_bound, *a.scan, "dedup_scan", s,
+                RelabelSide{a.relabel_list, a.relabel_len, a.map, a.n_nodes, a.relabel_n, a.relabel_indices},
+                a.relabel_bound);
+        else
+            run_scan<DedupCompactOp, int64_t>(op, a.len_bound, *a.scan, "dedup_scan", s);
+        return;
     }
     DedupOp op{a.list, a.len_const, a.len_ptr, (unsigned long long *)a.map, a.tag, a.n_nodes, a.nodes, a.base_ptr,
                a.size_out};

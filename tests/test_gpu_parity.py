@@ -127,7 +127,7 @@ SAMPLE_CASES = [
     ("random-3000-40000-8", "rand", [32, 33]),
     ("star", "all", [8, 16]),
     # one hop (its relabel is the only one) and four hops (each relabel rides
-    # with the next hop's count scan)
+    # with the next hop's first scan)
     ("random-3000-40000-9", "rand", [7]),
     ("chunglu-10k-d64", "batch", [3, 4, 3, 2]),
 ]
