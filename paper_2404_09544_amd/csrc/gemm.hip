@@ -17,7 +17,7 @@
 // while the current one is multiplied.  The split kernel uses the same ring.
 // bf16 output tiles leave through the idle ring as 16-byte row chunks.
 // Between one and 2.5 fp32 tiles per compute unit, the tiles past the
-// first 256 are split by segment over two workgroups and summed after
+// first 256 are split along k over two or three workgroups and summed after
 // (k_tail_sum), so no unit runs two whole tiles.
 //
 // Skinny kernel (few output rows, e.g. the last layer over the seeds): a
@@ -317,7 +317,8 @@ __global__ void __launch_bounds__(256) k_combine_split(const float *__restrict__
                                                        const uint16_t *__restrict__ B, int64_t ldb, int64_t pstride,
                                                        int64_t bseg, int nseg, int64_t N, int relu,
                                                        OutT *__restrict__ C, int64_t ldc, int64_t Rw,
-                                                       float *__restrict__ P, int64_t ldp, int64_t pseg) {
+                                                       float *__restrict__ P, int64_t ldp, int64_t pseg,
+                                                       int pieces) {
     constexpr int CH = 8, BK = 32, WN = 4 / WM;
     constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 32, TN = WTN / 32;
     constexpr int A_CH = BM * CH, B_PL = BN * 4, B_CH = 3 * B_PL, ST = A_CH + B_CH;
@@ -332,20 +333,20 @@ __global__ void __launch_bounds__(256) k_combine_split(const float *__restrict__
     if (m_dev) M = *m_dev;
     int64_t tile_r, tile_c;
     // Workgroups below Rw * ncol take whole tiles of the first Rw row bands
-    // (XCD-aware as tile_of); the rest take one segment each of the tail
-    // bands' tiles, two workgroups per tile, into partial planes P[0], P[1]
-    // (rows from Rw * BM on) that k_tail_sum adds.
+    // (XCD-aware as tile_of); the rest take one of `pieces` consecutive
+    // k-step ranges each of the tail bands' tiles into partial planes
+    // P[0 .. pieces) (rows from Rw * BM on) that k_tail_sum adds in order.
     const int64_t ncol = (N + BN - 1) / BN, Lb = blockIdx.x, Gw = Rw * ncol;
-    int64_t seg_only = -1, rbase = 0;
+    int64_t piece = -1, rbase = 0;
     if (Lb < Gw) {
         const int64_t xcd = Lb & 7, j = Lb >> 3;
         tile_r = (j / ncol) * 8 + xcd;
         tile_c = j % ncol;
     } else {
-        const int64_t q = Lb - Gw, pair = q >> 1;
-        seg_only = q & 1;
-        tile_r = Rw + pair / ncol;
-        tile_c = pair % ncol;
+        const int64_t q = Lb - Gw, tile = q / pieces;
+        piece = q - tile * pieces;
+        tile_r = Rw + tile / ncol;
+        tile_c = tile % ncol;
         rbase = Rw * BM;
     }
     const int64_t m0 = tile_r * BM, n0 = tile_c * BN;
@@ -368,8 +369,9 @@ __global__ void __launch_bounds__(256) k_combine_split(const float *__restrict__
         const int64_t n = n0 + r < N ? n0 + r : N - 1;
         pb[q] = B + p * pstride + n * ldb + 8 * ((rem % 4) ^ ((r >> 1) & 3));
     }
-    const int64_t kt = (K + BK - 1) / BK, t_first = seg_only < 0 ? 0 : seg_only * kt,
-                  steps = seg_only < 0 ? nseg * kt : t_first + kt;
+    const int64_t kt = (K + BK - 1) / BK, all_steps = nseg * kt,
+                  t_first = piece < 0 ? 0 : piece * all_steps / pieces,
+                  steps = piece < 0 ? all_steps : (piece + 1) * all_steps / pieces;
 
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -458,8 +460,8 @@ __global__ void __launch_bounds__(256) k_combine_split(const float *__restrict__
                 const int64_t row = r0 + i * 32 + 8 * (r / 4) + 4 * h + (r % 4), col = c0 + j * 32 + lr;
                 if (row < M && col < N) {
                     float v = acc[i][j][r];
-                    if (seg_only >= 0) {
-                        P[seg_only * pseg + (row - rbase) * ldp + col] = v;
+                    if (piece >= 0) {
+                        P[piece * pseg + (row - rbase) * ldp + col] = v;
                     } else {
                         if (relu) v = fmaxf(v, 0.f);
                         store_out<OutT>(C + row * ldc + col, v);
@@ -468,20 +470,21 @@ __global__ void __launch_bounds__(256) k_combine_split(const float *__restrict__
             }
 }
 
-// Tail bands of a split combine: C[r] = act(P[0][r - r0] + P[1][r - r0]) for
-// rows r0 <= r < M (M read on the device when m_dev is given).  V = 4:
-// 16-byte lanes (N, ldp, pseg and ldc multiples of 4, P and C 16-byte
-// aligned).
+// Tail bands of a split combine: C[r] = act(P[0][r - r0] + ... +
+// P[pieces - 1][r - r0]), added in piece order, for rows r0 <= r < M (M read
+// on the device when m_dev is given).  V = 4: 16-byte lanes (N, ldp, pseg
+// and ldc multiples of 4, P and C 16-byte aligned).
 template <int V>
-__global__ void __launch_bounds__(256) k_tail_sum(const float *__restrict__ P, int64_t ldp, int64_t pseg, int64_t r0,
-                                                  int64_t M, const int32_t *__restrict__ m_dev, int64_t N, int relu,
-                                                  float *__restrict__ C, int64_t ldc) {
+__global__ void __launch_bounds__(256) k_tail_sum(const float *__restrict__ P, int64_t ldp, int64_t pseg, int pieces,
+                                                  int64_t r0, int64_t M, const int32_t *__restrict__ m_dev, int64_t N,
+                                                  int relu, float *__restrict__ C, int64_t ldc) {
     typedef float fv __attribute__((ext_vector_type(V)));
     if (m_dev) M = *m_dev;
     const int64_t nv = N / V, total = (M - r0) * nv;
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
         const int64_t r = i / nv, c = (i - r * nv) * V;
-        fv v = *(const fv *)(P + r * ldp + c) + *(const fv *)(P + pseg + r * ldp + c);
+        fv v = *(const fv *)(P + r * ldp + c);
+        for (int p = 1; p < pieces; ++p) v += *(const fv *)(P + p * pseg + r * ldp + c);
         if (relu) {
 #pragma unroll
             for (int e = 0; e < V; ++e) v[e] = fmaxf(v[e], 0.f);
@@ -686,19 +689,25 @@ void launch_ring(const T *a0, int64_t lda0, const T *a1, int64_t lda1, int64_t m
 }  // namespace
 
 // Row bands of 128 x 128 tiles taken whole when an fp32 combine splits its
-// tail tiles by segment (0: no split).  Between one and 2.5 tiles per
-// compute unit the first 256 tiles (as 8-band groups) stay whole and the
-// rest go to two workgroups each, one per segment, summed after by
-// k_tail_sum: the busiest unit holds 1.5 tiles' work instead of 2 up to 384
-// tiles.  Measured on MI355X (cold caches, 1204-deep k): 17000 rows 119 ->
-// 93 us, 20902 rows 124 -> 99 us, 28000 rows 144 -> 138 us, 40000 rows
-// 214 -> 175 us.  Below 128-deep segments the partial sums cost more than
-// the balance gains (40000 x 74 x 130: 44 -> 48 us).
+// tail tiles along k (0: no split).  Between one and 2.5 tiles per compute
+// unit the first 256 tiles (as 8-band groups) stay whole and the rest go to
+// tail_pieces() workgroups each, one k-step range per workgroup, summed
+// after by k_tail_sum: the busiest unit holds 1.33-1.5 tiles' work instead
+// of 2.  Measured on MI355X (cold caches, 1204-deep k), no split -> two
+// pieces: 17000 rows 119 -> 93 us, 20902 rows 124 -> 99 us, 28000 rows 144
+// -> 138 us, 40000 rows 214 -> 175 us.  Below 128-deep segments the partial
+// sums cost more than the balance gains (40000 x 74 x 130: 44 -> 48 us).
 static int64_t tail_split_bands(int64_t m, int64_t n, int64_t k) {
     const int64_t nrow = (m + 127) / 128, ncol = (n + 127) / 128, tiles = nrow * ncol, w8 = 256 / ncol / 8 * 8;
     if (k < 128 || tiles <= 256 || tiles > 640 || w8 < 8 || w8 >= nrow) return 0;
     return w8;
 }
+
+// k-pieces per tail tile: three while the pieces fit the compute units
+// about once more (the busiest unit then holds 1 + 1/3 tiles), two beyond.
+// Measured at 1204-deep k (us, two -> three pieces, cold caches): 17000
+// rows 103 -> 101, 20902 rows 117 -> 113, 26600 rows 154 -> 138.
+static int tail_pieces(int64_t tail_tiles) { return tail_tiles <= 192 ? 3 : 2; }
 
 // fp32: the weights are split into three bf16 parts and transposed, then
 // k_combine_split runs; bf16: the weights are transposed and padded, then
@@ -715,8 +724,9 @@ static void launch_main(const void *self, int64_t ld_self, const void *agg, int6
     const int64_t split_bands = !bf16 && BM == 128 ? tail_split_bands(m, n, k) : 0;
     const int64_t rw = split_bands > 0 ? split_bands : nrow8;
     const int64_t tail_rows = rw < nrow ? m - rw * BM : 0;
+    const int pieces = tail_rows > 0 ? tail_pieces((nrow - rw) * ncol) : 1;
     const size_t wt_bytes = (size_t)(2 * kp * n * (bf16 ? 2 : 6)), part_off = (wt_bytes + 255) / 256 * 256;
-    g_wt.buf.ensure(part_off + (size_t)(2 * tail_rows * n) * sizeof(float), s);
+    g_wt.buf.ensure(part_off + (size_t)(pieces * tail_rows * n) * sizeof(float), s);
     const dim3 tgrid((unsigned)((n + 31) / 32), (unsigned)(2 * kp / 32));
     {
         KernelTimer tt("weights_transpose", s);
@@ -729,21 +739,23 @@ static void launch_main(const void *self, int64_t ld_self, const void *agg, int6
     }
     KernelTimer tk(label, s);
     if (!bf16) {
-        const dim3 grid((unsigned)(rw * ncol + 2 * (nrow8 > rw ? nrow - rw : 0) * ncol));
+        const dim3 grid((unsigned)(rw * ncol + pieces * (nrow8 > rw ? nrow - rw : 0) * ncol));
         float *part = (float *)((char *)g_wt.buf.p + part_off);
         // 128 x 128 tiles as 4 x 1 wavefronts: each splits only its own 32
         // rows of A (2 x 2 split every row twice); measured 2-6% faster
         constexpr int WM = BM == 128 ? 4 : 2;
         hipLaunchKernelGGL((k_combine_split<float, BM, BN, WM>), grid, dim3(256), 0, s, (const float *)self, ld_self,
                            (const float *)agg, ld_agg, m, m_dev, k, g_wt.buf.as<uint16_t>(), 2 * kp, n * 2 * kp, kp, 2,
-                           n, (int)relu, (float *)out, ld_out, rw, part, n, tail_rows * n);
+                           n, (int)relu, (float *)out, ld_out, rw, part, n, tail_rows * n, pieces);
         if (tail_rows > 0) {
             if (n % 4 == 0 && ld_out % 4 == 0 && ((uintptr_t)out & 15u) == 0)
                 hipLaunchKernelGGL(k_tail_sum<4>, dim3(grid_for(tail_rows * n / 4, 256 * 2, 1024)), dim3(256), 0, s,
-                                   part, n, tail_rows * n, rw * BM, m, m_dev, n, (int)relu, (float *)out, ld_out);
+                                   part, n, tail_rows * n, pieces, rw * BM, m, m_dev, n, (int)relu, (float *)out,
+                                   ld_out);
             else
                 hipLaunchKernelGGL(k_tail_sum<1>, dim3(grid_for(tail_rows * n, 256 * 8, 1024)), dim3(256), 0, s,
-                                   part, n, tail_rows * n, rw * BM, m, m_dev, n, (int)relu, (float *)out, ld_out);
+                                   part, n, tail_rows * n, pieces, rw * BM, m, m_dev, n, (int)relu, (float *)out,
+                                   ld_out);
         }
     } else if (out_bf16) {
         launch_ring<BM, BN, uint16_t, uint16_t>((const uint16_t *)self, ld_self, (const uint16_t *)agg, ld_agg, m,
@@ -775,10 +787,11 @@ static int64_t busiest_cu_outputs(int64_t m, int64_t n, int64_t bm, int64_t bn) 
 }
 
 // Busiest compute unit's outputs under the tail split: one whole tile plus
-// its share of the half tiles.
+// its share of the tail tiles' k-pieces.
 static int64_t busiest_cu_outputs_tail(int64_t m, int64_t n) {
-    const int64_t tiles = ((m + 127) / 128) * ((n + 127) / 128), halves = 2 * (tiles - 256);
-    return 128 * 128 * (2 + (halves + 255) / 256) / 2;
+    const int64_t tiles = ((m + 127) / 128) * ((n + 127) / 128), tail = tiles - 256;
+    const int p = tail_pieces(tail);
+    return 128 * 128 * (p + (p * tail + 255) / 256) / p;
 }
 
 // Tile shapes measured on MI355X.  fp32 (split kernel): 128 x 128 or

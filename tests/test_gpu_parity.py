@@ -379,9 +379,9 @@ def test_aggregate_mean_parity(G, d, dtype):
 # 64x64 tiles (both taken here, e.g. 20000 x 602 x 256 and 40000 x 37 x
 # 130), bf16 the ring kernel on 128x64 / 64x64 / 128x128 tiles.  K tails:
 # d_in not a multiple of the 32 (fp32) or 64 (bf16) k step; ragged M and N.
-# fp32 tail split (d_in >= 128, 256 < 128x128 tiles <= 640): 20000 x 602 x
-# 256, 33000 x 300 x 256, 24001 x 300 x 250, and one / three tile columns
-# (40000 x 128 x 100, 20000 x 160 x 300).
+# fp32 tail split (d_in >= 128, 256 < 128x128 tiles <= 640), three k-pieces
+# per tail tile: 20000 x 602 x 256, 24001 x 300 x 250, 40000 x 128 x 100 (one
+# tile column); two: 33000 x 300 x 256, 20000 x 160 x 300 (three columns).
 COMBINE_CASES = [(1, 3, 16), (63, 64, 41), (64, 100, 47), (65, 602, 256), (1000, 128, 64),
                  (777, 256, 256), (130, 5, 300), (20000, 602, 256), (12000, 64, 41),
                  (12001, 100, 100), (9000, 256, 256), (10240, 3, 47), (6000, 128, 260),
