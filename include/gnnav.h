@@ -252,9 +252,10 @@ gnnav_status gnnav_blocks_nodes(const gnnav_blocks *b, const int32_t **nodes_dev
  * Section 3.2's cache step for n_ids requested vertices: out row i (device,
  * stride ld_out elements of the cache dtype) becomes the feature row of
  * ids_dev[i].  Cached vertices are copied from HBM; the rest are read from
- * the host store by zero-copy loads over the host-device link, on a second
- * stream that joins `stream` before the call's work completes.  Gathers on
- * the same cache from different streams may overlap.  Each row
+ * the host store by zero-copy loads over the host-device link, in the same
+ * launch on `stream` (a share of its workgroups, gnnav_cache_set_link_
+ * workgroups).  Gathers on the same static cache from different streams may
+ * overlap.  Each row
  * copies ceil(d * elt / 16) 16-byte units: the columns from d up to the
  * next 16-byte boundary are written with zeros; later columns are untouched.
  * An id outside [0, n) gives a zero row and counts as invalid.
