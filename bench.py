@@ -528,18 +528,19 @@ def kernel_entries(args, G, g, c, wl, fwd, seeds_dev, ring, link, profiled_confi
         rec = traffic_for(name, trace_name) if profiled_config else None
         if rec:
             counted = rec.get("bytes_per_launch")
-            # a link-bound gather's HBM-side work: hit rows read and written
-            # plus the miss rows written and their list entries (the link
-            # carries the miss rows in; `achieved` counts those)
+            # a link-bound gather's counted traffic (the L2's fetches from
+            # memory and from the host link, and its writes) against the
+            # launch's algorithmic bytes: hit rows read and written, miss rows
+            # read over the link and written, list entries
             byte_work = gemm_bytes.get(name) if name.startswith("combine_gemm") else (
-                (hit_bytes + miss_bytes * (1 + 8 / (wl.d * elt)) if link_bound else hit_bytes)
+                (hit_bytes + miss_bytes * (2 + 8 / (wl.d * elt)) if link_bound else hit_bytes)
                 if name == "gather_rows" else work[name])
             ent["counted_bytes_per_launch"] = counted
             ent["counted_gbs"] = round(counted * launches / (ms * 1e-3) / 1e9, 2)
             if byte_work:
                 ent["useful_byte_efficiency"] = round(byte_work / max(launches, 1) / counted, 4)
             if name == "gather_rows" and link_bound:
-                ent["hbm_bytes_per_launch"] = round(byte_work / max(launches, 1), 1)
+                ent["algorithmic_bytes_per_launch"] = round(byte_work / max(launches, 1), 1)
             for key in ("dram_read_bytes_per_launch", "dram_write_bytes_per_launch", "io_read_bytes_per_launch"):
                 if rec.get(key) is not None:
                     ent[key] = rec[key]
@@ -572,7 +573,8 @@ def roofline_of(kernels, name, trace_name, profiled_config):
     out = {"kernel": name, "bound": k["bound"], "achieved": k["achieved"], "peak": k["peak"], "unit": k["unit"],
            "frac": k["frac"], "traffic": rec.get("bytes_per_launch") if rec else None}
     for key in ("method", "executed_bf16_tflops", "executed_frac_of_bf16_peak", "frac_of_measured_link",
-                "hit_bytes_per_launch", "hbm_bytes_per_launch", "useful_byte_efficiency", "io_read_bytes_per_launch",
+                "hit_bytes_per_launch", "algorithmic_bytes_per_launch", "useful_byte_efficiency",
+                "io_read_bytes_per_launch",
                 "io_read_gbs_counted", "dram_read_bytes_per_launch", "dram_write_bytes_per_launch"):
         if key in k:
             out[key] = k[key]
