@@ -227,6 +227,26 @@ def pick_link_workgroups(t_transfer_ms: float, t_rest_ms: float):
     return min(est, key=lambda w: (est[w], -w)), {str(w): round(v, 4) for w, v in est.items()}
 
 
+def pick_pipeline(args, t_transfer_ms: float, t_rest_ms: float):
+    """(cu_partition, depth) of a pipelined leg.  With the partition each
+    batch in flight runs on its own share of the compute units, so the
+    host-link workgroups of one batch's gather never share a unit with the
+    other batch's kernels.  auto takes it when the transfer is at least
+    twice the rest of the step, i.e. when the rest still fits beside the
+    transfer at half the units.  Measured on MI355X (ms/step, none at depth
+    3 -> two shares at depth 2): 233k/602-d r=0.5 1.364 -> 1.320, 2.45M
+    1.798 -> 1.747; R-MAT r=0.25, where sampling and compute dominate,
+    0.244 -> 0.276; 169k and 10k within 1%."""
+    if args.cu_partition == "on":
+        part = True
+    elif args.cu_partition == "off":
+        part = False
+    else:
+        part = t_rest_ms > 0 and t_transfer_ms >= 2.0 * t_rest_ms
+    depth = args.depth if args.depth is not None else (2 if part else 3)
+    return part, depth
+
+
 def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_weights, MiniBatchStep, Pipeline):
     """Training iterations on the same batches: one stream with every kernel
     timed, then the two-stream pipeline (each forward waits for the
@@ -253,13 +273,14 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
     G.sync(stream)
     losses = loss_hist[args.warmup:].cpu().numpy()
     link_est = None
+    t_tr = prof.get("gather_rows", (0, 0.0))[1] / args.steps
     if args.train_link_workgroups == "auto":
-        t_tr = prof.get("gather_rows", (0, 0.0))[1] / args.steps
         link_wgs, link_est = pick_link_workgroups(t_tr, seq * 1e3 / args.steps - t_tr)
     else:
         link_wgs = int(args.train_link_workgroups)
-    pipe = Pipeline(g, c, wtrain, wl.dims, wl.fanouts, "f32", depth=args.depth, eta=args.eta,
-                    link_workgroups=link_wgs)
+    part, depth = pick_pipeline(args, t_tr, seq * 1e3 / args.steps - t_tr)
+    pipe = Pipeline(g, c, wtrain, wl.dims, wl.fanouts, "f32", depth=depth, eta=args.eta,
+                    link_workgroups=link_wgs, cu_partition=part)
     for b in range(args.warmup):
         pipe.enqueue_train(seeds_dev[b], wl.rng_seed(b), labels, args.lr)
     pipe.synchronize()
@@ -307,6 +328,7 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
             "ms_per_step": round(piped * 1e3 / args.steps, 4),
             "value_sequential": round(wl.batch * args.steps / seq, 2), "lr": args.lr,
             "pipeline_link_workgroups": link_wgs, "link_workgroup_estimates_ms": link_est,
+            "pipeline_streams": depth, "cu_partition": part,
             "loss_first": round(float(losses[0]), 6), "loss_last": round(float(losses[-1]), 6),
             "kernels": kernels}
 
@@ -400,15 +422,16 @@ def forward_legs(args, G, g, c, wl, wdev, seeds_dev, torch, MiniBatchStep, Pipel
 
     # ---- the pipeline (batch b+1 overlaps batch b on another stream) -----
     link_est = None
+    t_tr = prof.get("gather_rows", (0, 0.0))[1] / args.steps
     if link_override is not None:
         link_wgs = link_override
     elif args.link_workgroups == "auto":
-        t_tr = prof.get("gather_rows", (0, 0.0))[1] / args.steps
         link_wgs, link_est = pick_link_workgroups(t_tr, seq_ms - t_tr)
     else:
         link_wgs = int(args.link_workgroups)
-    pipe = Pipeline(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, depth=args.depth, eta=args.eta,
-                    link_workgroups=link_wgs)
+    part, depth = pick_pipeline(args, t_tr, seq_ms - t_tr)
+    pipe = Pipeline(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, depth=depth, eta=args.eta,
+                    link_workgroups=link_wgs, cu_partition=part)
     for b in range(args.warmup):
         pipe.enqueue(seeds_dev[b], wl.rng_seed(b))
     pipe.synchronize()
@@ -432,7 +455,7 @@ def forward_legs(args, G, g, c, wl, wdev, seeds_dev, torch, MiniBatchStep, Pipel
             "counts": counts_hist[args.warmup:].cpu().numpy(),
             "seq_counts": seq_counts_hist[args.warmup:].cpu().numpy(),
             "n_h": sizes_all[:, :L + 1].astype(np.int64), "e_h": sizes_all[:, 17:17 + L + 1].astype(np.int64),
-            "link_workgroups": link_wgs, "link_est": link_est}
+            "link_workgroups": link_wgs, "link_est": link_est, "depth": depth, "cu_partition": part}
 
 
 def kernel_entries(args, G, g, c, wl, fwd, seeds_dev, ring, link, profiled_config, trace_name):
@@ -595,9 +618,13 @@ def main():
                     help="the single-core oracle baseline runs batches until this much time has passed")
     ap.add_argument("--cpu-threads", type=int, default=16,
                     help="cap on the threads of the all-core oracle baseline")
-    ap.add_argument("--depth", type=int, default=3,
-                    help="streams in the pipelined pass (3: a third batch in flight keeps the latency-bound "
-                         "sampling kernels busier; 4 measured slower)")
+    ap.add_argument("--depth", type=int, default=None,
+                    help="streams in the pipelined pass (default 2 with the compute units partitioned, else "
+                         "3: a third batch in flight keeps the latency-bound sampling kernels busier; 4 "
+                         "measured slower)")
+    ap.add_argument("--cu-partition", choices=["auto", "on", "off"], default="auto",
+                    help="run each pipelined batch on its own share of the compute units (auto: when the "
+                         "sequential leg's host-link transfer is at least twice the rest of its step)")
     ap.add_argument("--cache-policy", choices=["static", "fifo"], default="static",
                     help="fifo: admit each batch's misses into a ring over the last cache slots")
     ap.add_argument("--dynamic-fraction", type=float, default=1.0,
@@ -805,7 +832,8 @@ def main():
                    "seeds": {"graph": W.GRAPH_SEED, "features": W.FEAT_SEED, "permutation": W.PERM_SEED,
                              "weights": W.WEIGHT_SEED, "labels": W.LABEL_SEED,
                              "sampler_batch_b": f"({W.RNG_BASE} << 32) | b"},
-                   "pipeline_streams": args.depth, "link_workgroups": fwd["link_workgroups"],
+                   "pipeline_streams": fwd["depth"], "cu_partition": fwd["cu_partition"],
+                   "link_workgroups": fwd["link_workgroups"],
                    "link_workgroup_estimates_ms": fwd["link_est"],
                    "n": wl.n, "nnz": g.nnz, "d": wl.d, "fanouts": wl.fanouts,
                    "batch": wl.batch, "layers": wl.L, "dims": wl.dims, "cache_fraction": r,

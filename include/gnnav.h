@@ -91,6 +91,28 @@ int32_t gnnav_abi_version(void);
  * Errors: E_DEVICE.                                                        */
 gnnav_status gnnav_sync(void *stream);
 
+/* A stream whose kernels run on one share of the device's compute units,
+ * for pipelines that overlap one batch's host-link transfer with another
+ * batch's sampling and computation (Eq. 4's max of the two): batches
+ * enqueued on streams of different shares never share a compute unit, so
+ * the host-link workgroups of one batch's gather keep their issue rate
+ * while the other batch runs.  Share `part` of `parts` takes the CU-mask
+ * bits i with (i / 8) mod parts == part; on MI355X the runtime deals mask
+ * bits out to the eight XCDs in turn, so a share holds every parts-th
+ * compute unit of every XCD.  Results of work on such a stream are those of
+ * any other stream; only its speed differs (a share of the units), which
+ * pays where the transfer dominates the step and costs where it does not.
+ * The stream has the default priority.  The caller owns it: release it
+ * with gnnav_stream_destroy.  *out is written only on success.
+ * Errors: E_INVALID (NULL out, parts outside [1, 8], part outside
+ * [0, parts), fewer than 8 compute units per share), E_DEVICE (the runtime
+ * refused the stream).                                                     */
+gnnav_status gnnav_stream_create(int32_t part, int32_t parts, void **out);
+
+/* Waits for the work on a stream from gnnav_stream_create, then releases
+ * it.  NULL is allowed.  Errors: E_DEVICE.                                  */
+gnnav_status gnnav_stream_destroy(void *stream);
+
 /* ---------------------------------------------------------------- graph ---
  * Graph G(V, E) of Algorithm 1's input, as CSR in HBM.
  * src, dst: host arrays of n_edges node ids in [0, n_nodes).  Self pairs are

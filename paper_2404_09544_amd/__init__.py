@@ -43,6 +43,7 @@ EXPORTS = [
     "gnnav_softmax_xent", "gnnav_aggregate_mean_backward", "gnnav_weight_grad", "gnnav_profile_start",
     "gnnav_profile_stop", "gnnav_profile_count", "gnnav_profile_get", "gnnav_profile_samples",
     "gnnav_sync", "gnnav_debug_set_spin_limit", "gnnav_debug_fail_allocations", "gnnav_gather_noalloc",
+    "gnnav_stream_create", "gnnav_stream_destroy",
 ]
 
 
@@ -102,6 +103,8 @@ _sig = {
     "gnnav_debug_set_spin_limit": ([u32], i32),
     "gnnav_debug_fail_allocations": ([i64], i32),
     "gnnav_gather_noalloc": ([P, P, i64, P, i64, P, P], i32),
+    "gnnav_stream_create": ([i32, i32, P], i32),
+    "gnnav_stream_destroy": ([P], i32),
 }
 for _name, (_args, _res) in _sig.items():
     _f = getattr(_lib, _name)
@@ -130,6 +133,21 @@ def sync(stream=None):
     reported a failure (a scan whose look-back wait gave up) since the last
     report."""
     _check(_lib.gnnav_sync(_stream(stream)))
+
+
+def stream_create(part: int, parts: int):
+    """gnnav_stream_create: a stream on share `part` of `parts` of the
+    compute units, as a torch.cuda.ExternalStream.  The library's stream
+    outlives the wrapper; release it with stream_destroy."""
+    import torch
+    h = C.c_void_p()
+    _check(_lib.gnnav_stream_create(int(part), int(parts), C.byref(h)))
+    return torch.cuda.ExternalStream(h.value)
+
+
+def stream_destroy(stream):
+    """gnnav_stream_destroy: waits for the stream, then releases it."""
+    _check(_lib.gnnav_stream_destroy(_stream(stream)))
 
 
 def debug_set_spin_limit(polls: int):

@@ -138,6 +138,36 @@ extern "C" gnnav_status gnnav_sync(void *stream) {
     return guarded([&] { check_device_errors((hipStream_t)stream); });
 }
 
+// Share `part` of `parts`: CU-mask bits i with (i / 8) % parts == part.  The
+// runtime deals mask bits out to the eight XCDs in turn (bit i drives unit
+// i / 8 of XCD i % 8, read back from the XCC and HW_ID registers of the
+// workgroups of masked streams), so each share holds every parts-th unit of
+// every XCD; with two shares, two of the four shader engines of each XCD.
+extern "C" gnnav_status gnnav_stream_create(int32_t part, int32_t parts, void **out) {
+    return guarded([&] {
+        GNNAV_CHECK(out, GNNAV_E_INVALID, "out is NULL");
+        GNNAV_CHECK(parts >= 1 && parts <= 8, GNNAV_E_INVALID, "parts outside [1, 8]");
+        GNNAV_CHECK(part >= 0 && part < parts, GNNAV_E_INVALID, "part outside [0, parts)");
+        int n_cu = 0;
+        GNNAV_HIP(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, current_device()));
+        GNNAV_CHECK(n_cu >= 8 * parts, GNNAV_E_INVALID, "fewer than 8 compute units per share");
+        std::vector<uint32_t> mask((size_t)(n_cu + 31) / 32, 0u);
+        for (int i = 0; i < n_cu; ++i)
+            if ((i / 8) % parts == part) mask[(size_t)i / 32] |= 1u << (i % 32);
+        hipStream_t s = nullptr;
+        GNNAV_HIP(hipExtStreamCreateWithCUMask(&s, (uint32_t)mask.size(), mask.data()));
+        *out = (void *)s;
+    });
+}
+
+extern "C" gnnav_status gnnav_stream_destroy(void *stream) {
+    return guarded([&] {
+        if (!stream) return;
+        GNNAV_HIP(hipStreamSynchronize((hipStream_t)stream));
+        GNNAV_HIP(hipStreamDestroy((hipStream_t)stream));
+    });
+}
+
 extern "C" gnnav_status gnnav_debug_set_spin_limit(uint32_t polls) {
     g_spin_limit.store(polls);
     return GNNAV_OK;

@@ -29,7 +29,7 @@ import numpy as np
 import torch
 
 from . import (Blocks, Cache, Graph, gather, gather_n, sage_forward, sage_train_step, sample, sample_async,
-               sample_biased, sync)
+               sample_biased, stream_create, sync)
 
 
 def to_device_weights(ws, dtype: str):
@@ -159,13 +159,20 @@ class MiniBatchStep:
 
 
 _STREAMS = []
+_PART_STREAMS = {}
 
 
-def pipeline_streams(n: int):
+def pipeline_streams(n: int, cu_partition: bool = False):
     """The process's pipeline streams, created once and shared by every
     Pipeline.  HIP multiplexes streams onto a few hardware queues (four by
     default); two busy streams that land on one queue run one after the
-    other, so the pipeline keeps its stream count at its depth."""
+    other, so the pipeline keeps its stream count at its depth.  With
+    cu_partition, stream j runs on share j of n of the compute units
+    (gnnav_stream_create), so the batches in flight never share a unit."""
+    if cu_partition:
+        if n not in _PART_STREAMS:
+            _PART_STREAMS[n] = [stream_create(j, n) for j in range(n)]
+        return _PART_STREAMS[n]
     while len(_STREAMS) < n:
         _STREAMS.append(torch.cuda.Stream())
     return _STREAMS[:n]
@@ -175,12 +182,15 @@ class Pipeline:
     """Batches b, b+1, ... on `depth` streams in turn (slot b % depth)."""
 
     def __init__(self, graph: Graph, cache: Cache, weights_dev, dims, fanouts, dtype: str, depth: int = 2,
-                 eta=None, link_workgroups=None):
+                 eta=None, link_workgroups=None, cu_partition: bool = False):
         """link_workgroups: host-link workgroups of this pipeline's gathers
         (None keeps the cache's setting); fewer slow the batches computing
-        alongside a gather less, at a small cost in link rate."""
+        alongside a gather less, at a small cost in link rate.
+        cu_partition: each slot's stream runs on its own 1/depth share of
+        the compute units, which speeds up steps whose host-link transfer
+        dominates and slows down the others."""
         self.slots = [MiniBatchStep(graph, cache, weights_dev, dims, fanouts, dtype, eta=eta) for _ in range(depth)]
-        self.streams = pipeline_streams(depth)
+        self.streams = pipeline_streams(depth, cu_partition)
         self.depth = depth
         self.count = 0
         self._updated = None

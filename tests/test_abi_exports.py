@@ -54,3 +54,17 @@ def test_combine_kernel_choice():
         except g.GnnavError:
             continue
         raise AssertionError(f"{bad} accepted")
+
+
+def test_stream_create_argument_checks():
+    """gnnav_stream_create rejects a bad share before touching the device,
+    and leaves *out unwritten when it fails."""
+    import paper_2404_09544_amd as g
+    lib = g._lib
+    out = ctypes.c_void_p(12345)
+    for part, parts in [(0, 0), (0, 9), (-1, 2), (2, 2), (3, 1)]:
+        assert lib.gnnav_stream_create(part, parts, ctypes.byref(out)) == 1, (part, parts)
+        assert out.value == 12345
+        assert b"outside" in lib.gnnav_last_error()
+    assert lib.gnnav_stream_create(0, 2, None) == 1
+    assert lib.gnnav_stream_destroy(None) == 0

@@ -6,9 +6,10 @@ hit/miss counts identical to the oracle's, and the logits of sampled seed
 rows match the oracle's receptive-field forward within tolerance (the
 10M-node R-MAT workload at cache fractions 0, 0.25 and 1).  Then the launch
 configuration bench.py times: the first three batches through the
-three-stream Pipeline (asynchronous sampling, gathers ordered on the host
-link, grids and GEMM tiles planned from the Eq. 12 bounds), each slot
-checked in full against the oracle -- every logits row of F_0 where the
+Pipeline (asynchronous sampling, gathers ordered on the host
+link, grids and GEMM tiles planned from the Eq. 12 bounds, the compute
+units partitioned between the streams where the bench partitions them),
+each batch checked in full against the oracle -- every logits row of F_0 where the
 oracle's forward takes seconds, sampled rows on the two largest graphs.
 """
 import sys
@@ -110,13 +111,19 @@ def test_full_batch(G, name):
 # oracle's double-precision forward of the whole batch takes seconds
 PIPE_ROWS = {"chunglu-169k-d128": None, "chunglu-233k-d602": None, "chunglu-2450k-d100": 256,
              "rmat-10m-d128": 256}
+# (streams, compute units partitioned) of bench.py's pipelined leg on MI355X:
+# its rule partitions where the host-link transfer is at least twice the rest
+# of the step (the 233k and 2.45M workloads), with two streams
+PIPE_CFG = {"chunglu-169k-d128": (3, False), "chunglu-233k-d602": (2, True), "chunglu-2450k-d100": (2, True),
+            "rmat-10m-d128": (3, False)}
 
 
 @pytest.mark.parametrize("name", FULL)
 def test_full_pipeline(G, name):
-    """Batches 0, 1, 2 through Pipeline.enqueue on three streams with the
-    bench's link-workgroup setting (64), exactly as the bench's pipelined
-    leg enqueues them; every slot against the oracle."""
+    """Batches 0, 1, 2 through Pipeline.enqueue with the bench's streams,
+    compute-unit partition and link-workgroup setting (64), as the bench's
+    pipelined leg enqueues them (with two streams: batches 0 and 1 in flight
+    together, then batch 2); every batch against the oracle."""
     import torch
     from paper_2404_09544_amd.step import Pipeline, to_device_weights
     wl, _, _, csr, g = load(G, name)
@@ -129,13 +136,16 @@ def test_full_pipeline(G, name):
     t = time.perf_counter()
     c = G.Cache(g, feats, wl.dtype, r, store_on_device=wl.cfg["store_on_device"])
     _, slot_map, _ = O.rank_cache(csr, r)
-    pipe = Pipeline(g, c, to_device_weights(ws, wl.dtype), wl.dims, wl.fanouts, wl.dtype, depth=3,
-                    link_workgroups=64)
+    depth, part = PIPE_CFG[name]
+    pipe = Pipeline(g, c, to_device_weights(ws, wl.dtype), wl.dims, wl.fanouts, wl.dtype, depth=depth,
+                    link_workgroups=64, cu_partition=part)
     seeds_dev = [torch.from_numpy(wl.seeds(b)).cuda() for b in range(3)]
-    slots = [pipe.enqueue(seeds_dev[b], wl.rng_seed(b)) for b in range(3)]
-    pipe.synchronize()
-    say(name, f"pipeline of 3 batches done ({time.perf_counter() - t:.1f}s)")
-    for b, st in enumerate(slots):
+    for b in range(3):
+        if b % depth == 0:
+            slots = [pipe.enqueue(seeds_dev[x], wl.rng_seed(x)) for x in range(b, min(b + depth, 3))]
+            pipe.synchronize()
+            say(name, f"pipeline of batches {b}..{b + len(slots) - 1} done ({time.perf_counter() - t:.1f}s)")
+        st = slots[b % depth]
         logits = st.finish().cpu().numpy()
         nodes, sizes, ip, nb, ix = st.blocks.to_host()
         ref_b = O.sample_blocks(csr, wl.seeds(b), wl.fanouts, wl.rng_seed(b))

@@ -263,7 +263,8 @@ def test_train_steps_lower_the_loss(G):
 
 def test_train_pipeline_matches_sequential(G):
     """Training batches on two streams (each batch's forward waits for the
-    previous update) end with the same weights as one stream."""
+    previous update), also on two shares of the compute units, end with the
+    same weights as one stream."""
     import torch
     from paper_2404_09544_amd.step import MiniBatchStep, Pipeline, to_device_weights
     wl = W.Workload("chunglu-10k-d64")
@@ -280,9 +281,11 @@ def test_train_pipeline_matches_sequential(G):
         step.train(seeds[b], wl.rng_seed(b), lab, 0.3, async_mode=True)
         torch.cuda.synchronize()
         seq_losses.append(float(host(step.loss)[0]))
-    for link in (None, 32, 1):
+    for link, part in ((None, False), (32, False), (1, False), (64, True)):
+        say("train pipeline", link, part)
         w_pipe = to_device_weights(ws, "f32")
-        pipe = Pipeline(g, c, w_pipe, wl.dims, wl.fanouts, "f32", depth=2, link_workgroups=link)
+        pipe = Pipeline(g, c, w_pipe, wl.dims, wl.fanouts, "f32", depth=2, link_workgroups=link,
+                        cu_partition=part)
         slots = [pipe.enqueue_train(seeds[b], wl.rng_seed(b), lab, 0.3) for b in range(6)]
         pipe.synchronize()
         for a, b in zip(w_seq, w_pipe):
