@@ -227,24 +227,44 @@ def pick_link_workgroups(t_transfer_ms: float, t_rest_ms: float):
     return min(est, key=lambda w: (est[w], -w)), {str(w): round(v, 4) for w, v in est.items()}
 
 
-def pick_pipeline(args, t_transfer_ms: float, t_rest_ms: float):
-    """(cu_partition, depth) of a pipelined leg.  With the partition each
-    batch in flight runs on its own share of the compute units, so the
-    host-link workgroups of one batch's gather never share a unit with the
-    other batch's kernels.  auto takes it when the transfer is at least
-    twice the rest of the step, i.e. when the rest still fits beside the
-    transfer at half the units.  Measured on MI355X (ms/step, none at depth
-    3 -> two shares at depth 2): 233k/602-d r=0.5 1.364 -> 1.320, 2.45M
-    1.798 -> 1.747; R-MAT r=0.25, where sampling and compute dominate,
-    0.244 -> 0.276; 169k and 10k within 1%."""
-    if args.cu_partition == "on":
-        part = True
-    elif args.cu_partition == "off":
-        part = False
-    else:
-        part = t_rest_ms > 0 and t_transfer_ms >= 2.0 * t_rest_ms
-    depth = args.depth if args.depth is not None else (2 if part else 3)
-    return part, depth
+# (compute units partitioned, streams) a pipelined leg may take
+PIPE_CANDIDATES = [(False, 3), (True, 2), (True, 3)]
+
+
+def pick_pipeline(args, make, enqueue, n_b: int, torch, n_time: int = 12):
+    """(cu_partition, streams, trial ms/step per candidate) of a pipelined
+    leg.  With the partition each batch in flight runs on its own share of
+    the compute units (gnnav_stream_create), so the host-link workgroups of
+    one batch's gather never share a unit with another batch's kernels; that
+    pays where the transfer dominates and costs where sampling and compute
+    do.  auto times n_time batches through each candidate (after one untimed
+    batch per stream) before the timed region and keeps the fastest.
+    Measured on MI355X (ms/step; three streams on all units / two on halves
+    / three on thirds): 233k/602-d r=0.5 1.364 / 1.320 / 1.349, 2.45M 1.798
+    / 1.747 / 1.770, 169k 0.168-0.181 / 0.171-0.179 / 0.164-0.165, R-MAT
+    r=0.25 0.233-0.240 / 0.270-0.276 / 0.276-0.278; training 169k 0.258-0.262
+    / 0.228-0.231 / 0.264, 233k 1.343 / 1.310."""
+    if args.cu_partition != "auto":
+        part = args.cu_partition == "on"
+        depth = args.depth if args.depth is not None else (2 if part else 3)
+        return part, depth, None
+    cands = PIPE_CANDIDATES if args.depth is None else [(False, args.depth), (True, args.depth)]
+    trial = {}
+    for part, depth in cands:
+        pipe = make(depth, part)
+        for i in range(depth):
+            enqueue(pipe, i % n_b)
+        pipe.synchronize()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(n_time):
+            enqueue(pipe, i % n_b)
+        pipe.synchronize()
+        torch.cuda.synchronize()
+        trial[(part, depth)] = (time.perf_counter() - t0) * 1e3 / n_time
+        del pipe
+    part, depth = min(trial, key=trial.get)
+    return part, depth, {f"{'shares' if p else 'all_units'}_{d}": round(v, 4) for (p, d), v in trial.items()}
 
 
 def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_weights, MiniBatchStep, Pipeline):
@@ -278,9 +298,13 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
         link_wgs, link_est = pick_link_workgroups(t_tr, seq * 1e3 / args.steps - t_tr)
     else:
         link_wgs = int(args.train_link_workgroups)
-    part, depth = pick_pipeline(args, t_tr, seq * 1e3 / args.steps - t_tr)
-    pipe = Pipeline(g, c, wtrain, wl.dims, wl.fanouts, "f32", depth=depth, eta=args.eta,
-                    link_workgroups=link_wgs, cu_partition=part)
+    def make(depth, part):
+        return Pipeline(g, c, wtrain, wl.dims, wl.fanouts, "f32", depth=depth, eta=args.eta,
+                        link_workgroups=link_wgs, cu_partition=part)
+
+    part, depth, trial = pick_pipeline(
+        args, make, lambda p, b: p.enqueue_train(seeds_dev[b], wl.rng_seed(b), labels, args.lr), n_b, torch)
+    pipe = make(depth, part)
     for b in range(args.warmup):
         pipe.enqueue_train(seeds_dev[b], wl.rng_seed(b), labels, args.lr)
     pipe.synchronize()
@@ -328,7 +352,7 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
             "ms_per_step": round(piped * 1e3 / args.steps, 4),
             "value_sequential": round(wl.batch * args.steps / seq, 2), "lr": args.lr,
             "pipeline_link_workgroups": link_wgs, "link_workgroup_estimates_ms": link_est,
-            "pipeline_streams": depth, "cu_partition": part,
+            "pipeline_streams": depth, "cu_partition": part, "pipeline_trial_ms": trial,
             "loss_first": round(float(losses[0]), 6), "loss_last": round(float(losses[-1]), 6),
             "kernels": kernels}
 
@@ -429,9 +453,13 @@ def forward_legs(args, G, g, c, wl, wdev, seeds_dev, torch, MiniBatchStep, Pipel
         link_wgs, link_est = pick_link_workgroups(t_tr, seq_ms - t_tr)
     else:
         link_wgs = int(args.link_workgroups)
-    part, depth = pick_pipeline(args, t_tr, seq_ms - t_tr)
-    pipe = Pipeline(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, depth=depth, eta=args.eta,
-                    link_workgroups=link_wgs, cu_partition=part)
+    def make(depth, part):
+        return Pipeline(g, c, wdev, wl.dims, wl.fanouts, wl.dtype, depth=depth, eta=args.eta,
+                        link_workgroups=link_wgs, cu_partition=part)
+
+    part, depth, trial = pick_pipeline(args, make, lambda p, b: p.enqueue(seeds_dev[b], wl.rng_seed(b)), n_b,
+                                       torch)
+    pipe = make(depth, part)
     for b in range(args.warmup):
         pipe.enqueue(seeds_dev[b], wl.rng_seed(b))
     pipe.synchronize()
@@ -455,7 +483,8 @@ def forward_legs(args, G, g, c, wl, wdev, seeds_dev, torch, MiniBatchStep, Pipel
             "counts": counts_hist[args.warmup:].cpu().numpy(),
             "seq_counts": seq_counts_hist[args.warmup:].cpu().numpy(),
             "n_h": sizes_all[:, :L + 1].astype(np.int64), "e_h": sizes_all[:, 17:17 + L + 1].astype(np.int64),
-            "link_workgroups": link_wgs, "link_est": link_est, "depth": depth, "cu_partition": part}
+            "link_workgroups": link_wgs, "link_est": link_est, "depth": depth, "cu_partition": part,
+            "trial": trial}
 
 
 def kernel_entries(args, G, g, c, wl, fwd, seeds_dev, ring, link, profiled_config, trace_name):
@@ -619,12 +648,13 @@ def main():
     ap.add_argument("--cpu-threads", type=int, default=16,
                     help="cap on the threads of the all-core oracle baseline")
     ap.add_argument("--depth", type=int, default=None,
-                    help="streams in the pipelined pass (default 2 with the compute units partitioned, else "
-                         "3: a third batch in flight keeps the latency-bound sampling kernels busier; 4 "
-                         "measured slower)")
+                    help="streams in the pipelined pass (default: chosen with the partition; 3 without it: "
+                         "a third batch in flight keeps the latency-bound sampling kernels busier, 4 measured "
+                         "slower)")
     ap.add_argument("--cu-partition", choices=["auto", "on", "off"], default="auto",
-                    help="run each pipelined batch on its own share of the compute units (auto: when the "
-                         "sequential leg's host-link transfer is at least twice the rest of its step)")
+                    help="run each pipelined batch on its own share of the compute units (auto: time a few "
+                         "batches of three streams on all units, two on halves and three on thirds before "
+                         "the timed region and keep the fastest)")
     ap.add_argument("--cache-policy", choices=["static", "fifo"], default="static",
                     help="fifo: admit each batch's misses into a ring over the last cache slots")
     ap.add_argument("--dynamic-fraction", type=float, default=1.0,
@@ -732,6 +762,7 @@ def main():
         r1 = {"cache_fraction": 1.0, "value": round(wl.batch * args.steps / f1["elapsed"], 2), "unit": "seeds/s",
               "ms_per_step": round(f1["ms_per_step"], 4),
               "value_sequential": round(wl.batch * args.steps / f1["seq_elapsed"], 2),
+              "pipeline_streams": f1["depth"], "cu_partition": f1["cu_partition"], "pipeline_trial_ms": f1["trial"],
               "roofline_gather": roofline_of(k1, "gather_rows", f"{wl.name}_r1", args.eta is None)
               if "gather_rows" in k1 and k1["gather_rows"].get("bound") else None,
               "roofline": roofline_of(k1, max(rows1)[1], f"{wl.name}_r1", args.eta is None) if rows1 else None,
@@ -833,6 +864,7 @@ def main():
                              "weights": W.WEIGHT_SEED, "labels": W.LABEL_SEED,
                              "sampler_batch_b": f"({W.RNG_BASE} << 32) | b"},
                    "pipeline_streams": fwd["depth"], "cu_partition": fwd["cu_partition"],
+                   "pipeline_trial_ms": fwd["trial"],
                    "link_workgroups": fwd["link_workgroups"],
                    "link_workgroup_estimates_ms": fwd["link_est"],
                    "n": wl.n, "nnz": g.nnz, "d": wl.d, "fanouts": wl.fanouts,

@@ -5,12 +5,12 @@ MiniBatchStep's synchronous form gives frontiers, blocks, gathered rows and
 hit/miss counts identical to the oracle's, and the logits of sampled seed
 rows match the oracle's receptive-field forward within tolerance (the
 10M-node R-MAT workload at cache fractions 0, 0.25 and 1).  Then the launch
-configuration bench.py times: the first three batches through the
-Pipeline (asynchronous sampling, gathers ordered on the host
-link, grids and GEMM tiles planned from the Eq. 12 bounds, the compute
-units partitioned between the streams where the bench partitions them),
-each batch checked in full against the oracle -- every logits row of F_0 where the
-oracle's forward takes seconds, sampled rows on the two largest graphs.
+configuration bench.py times: the first three batches through the Pipeline
+(asynchronous sampling, gathers ordered on the host link, grids and GEMM
+tiles planned from the Eq. 12 bounds) in each stream and compute-unit
+setting the bench may pick, each batch checked in full against the oracle
+-- every logits row of F_0 where the oracle's forward takes seconds, sampled
+rows on the two largest graphs.
 """
 import sys
 import time
@@ -111,15 +111,14 @@ def test_full_batch(G, name):
 # oracle's double-precision forward of the whole batch takes seconds
 PIPE_ROWS = {"chunglu-169k-d128": None, "chunglu-233k-d602": None, "chunglu-2450k-d100": 256,
              "rmat-10m-d128": 256}
-# (streams, compute units partitioned) of bench.py's pipelined leg on MI355X:
-# its rule partitions where the host-link transfer is at least twice the rest
-# of the step (the 233k and 2.45M workloads), with two streams
-PIPE_CFG = {"chunglu-169k-d128": (3, False), "chunglu-233k-d602": (2, True), "chunglu-2450k-d100": (2, True),
-            "rmat-10m-d128": (3, False)}
+# (streams, compute units partitioned): every setting bench.py's pipelined
+# leg may time (it keeps the fastest of a short trial of each)
+PIPE_CFG = [(3, False), (2, True), (3, True)]
 
 
+@pytest.mark.parametrize("cfg", PIPE_CFG, ids=lambda c: f"{c[0]}streams-{'shares' if c[1] else 'all'}")
 @pytest.mark.parametrize("name", FULL)
-def test_full_pipeline(G, name):
+def test_full_pipeline(G, name, cfg):
     """Batches 0, 1, 2 through Pipeline.enqueue with the bench's streams,
     compute-unit partition and link-workgroup setting (64), as the bench's
     pipelined leg enqueues them (with two streams: batches 0 and 1 in flight
@@ -136,7 +135,7 @@ def test_full_pipeline(G, name):
     t = time.perf_counter()
     c = G.Cache(g, feats, wl.dtype, r, store_on_device=wl.cfg["store_on_device"])
     _, slot_map, _ = O.rank_cache(csr, r)
-    depth, part = PIPE_CFG[name]
+    depth, part = cfg
     pipe = Pipeline(g, c, to_device_weights(ws, wl.dtype), wl.dims, wl.fanouts, wl.dtype, depth=depth,
                     link_workgroups=64, cu_partition=part)
     seeds_dev = [torch.from_numpy(wl.seeds(b)).cuda() for b in range(3)]
