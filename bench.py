@@ -466,12 +466,25 @@ def forward_legs(args, G, g, c, wl, wdev, seeds_dev, torch, MiniBatchStep, Pipel
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for b in range(args.warmup, n_b):
-        slot = pipe.enqueue(seeds_dev[b], wl.rng_seed(b))
-        record(slot, b, pipe.streams[(pipe.count - 1) % pipe.depth], counts_hist)
+        pipe.enqueue(seeds_dev[b], wl.rng_seed(b))
     pipe.synchronize()          # raises if device-side work reported a failure
     torch.cuda.synchronize()
     t_end = time.perf_counter()
     G.sync()
+    # the timed pass's last batches, still in their slots, against the
+    # sequential leg's frontier sizes
+    for j in range(min(pipe.depth, args.steps)):
+        st = pipe.slots[(pipe.count - 1 - j) % pipe.depth]
+        st.finish()
+        assert list(st.sizes) == sizes_all[args.steps - 1 - j, :L + 1].tolist(), "pipelined batch differs in size"
+    # the same batches again, untimed, each one's counts and sizes copied
+    # aside as it completes (the results are deterministic): the copies would
+    # otherwise add two enqueues per batch to the timed host loop
+    for b in range(args.warmup, n_b):
+        slot = pipe.enqueue(seeds_dev[b], wl.rng_seed(b))
+        record(slot, b, pipe.streams[(pipe.count - 1) % pipe.depth], counts_hist)
+    pipe.synchronize()
+    torch.cuda.synchronize()
     c.set_link_workgroups(64)
     elapsed = t_end - t_start
     log(f"r={c.n_cached / max(wl.n, 1):.3g} pipelined {args.steps} steps: {elapsed * 1e3 / args.steps:.3f} ms/step, "
