@@ -11,6 +11,8 @@
  *   uint64 rng_seed; int32 src[m], dst[m]; float feats[n*d];
  *   int32 fanouts[L]; int32 dims[L+1]; int32 seeds[n_seeds];
  *   then for l = 1..L float W_l[2*dims[l-1]*dims[l]] (row-major).
+ * The batch runs on a stream restricted to one half of the compute units
+ * (gnnav_stream_create), which changes no result.
  * OUT: int64 sizes[L+1]; int64 counts[3]; float logits[sizes[0]*dims[L]].
  * Exit status 0 on success; on a failing call the status, the call and
  * gnnav_last_error() go to stderr and the status is 1. */
@@ -83,6 +85,9 @@ int main(int argc, char **argv) {
     gnnav_graph_free(NULL);
     gnnav_cache_free(NULL);
     gnnav_blocks_free(NULL);
+    CHECK(gnnav_stream_destroy(NULL));
+    void *stream = NULL;
+    CHECK(gnnav_stream_create(1, 2, &stream));
 
     gnnav_graph *g = NULL;
     gnnav_cache *c = NULL;
@@ -96,7 +101,7 @@ int main(int argc, char **argv) {
     int32_t *seeds_d = NULL;
     HIP(hipMalloc((void **)&seeds_d, (size_t)(n_seeds ? n_seeds : 1) * 4));
     HIP(hipMemcpy(seeds_d, seeds, (size_t)n_seeds * 4, hipMemcpyHostToDevice));
-    CHECK(gnnav_sample(g, seeds_d, n_seeds, fanouts, (int32_t)L, rng_seed, b, NULL));
+    CHECK(gnnav_sample(g, seeds_d, n_seeds, fanouts, (int32_t)L, rng_seed, b, stream));
 
     const int32_t *nodes_d = NULL;
     int64_t sizes[17];
@@ -119,7 +124,7 @@ int main(int argc, char **argv) {
     int64_t *counts_d = NULL;
     HIP(hipMalloc((void **)&h0, (size_t)(sizes[L] ? sizes[L] : 1) * (size_t)ld * 4));
     HIP(hipMalloc((void **)&counts_d, 3 * sizeof(int64_t)));
-    CHECK(gnnav_gather(c, nodes_d, sizes[L], h0, ld, counts_d, NULL));
+    CHECK(gnnav_gather(c, nodes_d, sizes[L], h0, ld, counts_d, stream));
 
     float *w_dev[16];
     for (int64_t l = 1; l <= L; ++l) {
@@ -130,8 +135,8 @@ int main(int argc, char **argv) {
     const int64_t ld_out = dims[L];
     HIP(hipMalloc((void **)&logits, (size_t)(sizes[0] ? sizes[0] : 1) * (size_t)ld_out * 4));
     CHECK(gnnav_sage_forward(b, h0, ld, (const void *const *)w_dev, dims, (int32_t)L, GNNAV_F32, logits, ld_out,
-                             NULL));
-    CHECK(gnnav_sync(NULL));
+                             stream));
+    CHECK(gnnav_sync(stream));
 
     int64_t counts[3];
     float *out_logits = malloc((size_t)(sizes[0] ? sizes[0] : 1) * (size_t)ld_out * 4);
@@ -157,6 +162,7 @@ int main(int argc, char **argv) {
     gnnav_blocks_free(b);
     gnnav_cache_free(c);
     gnnav_graph_free(g);
+    CHECK(gnnav_stream_destroy(stream));
     free(out_logits);
     free(seeds);
     free(feats);
