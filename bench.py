@@ -360,6 +360,9 @@ def train_leg(args, G, g, c, wl, ws, seeds_dev, sizes_hist, torch, to_device_wei
 SIZE_SLOTS = 24      # device size array: |F_h| at [h], E_h at [17 + h] (L <= 3 fits in 24)
 
 
+SEED_TILE = 2048     # seeds the library dedups in one workgroup (one scan tile)
+
+
 def sampling_bytes(wl, n_h, e_h, off_bytes: int, max_deg: int) -> dict:
     """Algorithmic bytes of one batch's sampling-chain kernels (Eq. 2 and its
     union), by kernel label: each datum a kernel must read or write counted
@@ -395,6 +398,9 @@ def sampling_bytes(wl, n_h, e_h, off_bytes: int, max_deg: int) -> dict:
                 out["count_scan"] += rows * (4 + 2 * off_bytes) + (rows + 1) * 4 + relabel_prev
     out["relabel"] = e_h[L] * (4 + 8 + 4)
     out["classify"] = n_h[L] * (4 + 4 + 8)
+    if slotted[0] and b0 <= SEED_TILE:
+        # seeds that fit one scan tile: first positions and their scan in one launch
+        out["dedup_scan"] += out.pop("dedup_first")
     return out
 
 

@@ -607,6 +607,74 @@ __global__ void __launch_bounds__(256) k_first_position(const int32_t *__restric
     if (bad && err) atomicAdd(err, bad);
 }
 
+// The seeds' dedup when they fit one scan tile (at most kScanTile ids, no
+// frontier before them, no folded count scan): first positions and the
+// order-preserving scan of first-occurrence flags in one workgroup, which
+// saves the separate first-position launch.  Between the two phases every
+// wavefront waits for its node-table atomics to be performed in L2, then
+// the workgroup meets at a barrier; the flags then read the table with
+// device-scope loads, past the compute unit's cache, which may hold lines
+// read before the atomics.  Results equal those of k_first_position
+// followed by the DedupOp scan.
+__global__ void __launch_bounds__(kScanThreads) k_seed_dedup_tile(const int32_t *__restrict__ list, int64_t len,
+                                                                  unsigned long long *__restrict__ map, uint32_t tag,
+                                                                  int64_t n_nodes, int32_t *__restrict__ nodes,
+                                                                  int32_t *__restrict__ size_out,
+                                                                  int32_t *__restrict__ err,
+                                                                  int32_t *__restrict__ err_next) {
+    __shared__ int32_t scratch[kScanThreads / kWave];
+    __shared__ int32_t s_bad;
+    if (threadIdx.x == 0) {
+        s_bad = 0;
+        if (err_next) *err_next = 0;
+    }
+    __syncthreads();
+    const int64_t first = (int64_t)threadIdx.x * kScanItems;
+    // every load of a phase issued before any of its results is used
+    int32_t ids[kScanItems];
+    bool ok[kScanItems];
+    int32_t bad = 0;
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) ids[j] = first + j < len ? list[first + j] : -1;
+    unsigned long long cur[kScanItems];
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) {
+        ok[j] = first + j < len && ids[j] >= 0 && ids[j] < n_nodes;
+        bad += first + j < len && !ok[j];
+        cur[j] = ok[j] ? map[ids[j]] : 0ull;
+    }
+    // a position only lowers a stale entry or a larger position of this call
+    bool lower[kScanItems];
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) lower[j] = ok[j] && cur[j] > node_position(tag, first + j);
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j)
+        if (lower[j]) atomicMin(&map[ids[j]], node_position(tag, first + j));
+    if (bad) atomicAdd(&s_bad, bad);
+    __builtin_amdgcn_s_waitcnt(0);   // vmcnt(0), lgkmcnt(0): this wavefront's atomics are done
+    __syncthreads();
+    if (threadIdx.x == 0 && s_bad && err) atomicAdd(err, s_bad);
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j)
+        cur[j] = ok[j] ? __hip_atomic_load(&map[ids[j]], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
+    int32_t flag[kScanItems], cnt = 0;
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) {
+        flag[j] = ok[j] && cur[j] == node_position(tag, first + j);
+        cnt += flag[j];
+    }
+    int32_t total;
+    int32_t at = block_exclusive_sum<int32_t, kScanThreads>(cnt, scratch, total);
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) {
+        if (!flag[j]) continue;
+        nodes[at] = ids[j];
+        map[ids[j]] = node_local(tag, at);
+        ++at;
+    }
+    if (threadIdx.x == 0) *size_out = total;
+}
+
 struct DedupOp {
     const int32_t *list;
     int64_t len_const;
@@ -726,6 +794,14 @@ struct DedupCompactOp {
 };
 
 void launch_dedup(const DedupArgs &a, hipStream_t s) {
+    if (!a.first_done && !a.len_ptr && !a.base_ptr && !a.count_row_ptr && a.slot_stride == 0 &&
+        a.len_const <= kScanTile) {
+        KernelTimer t("dedup_scan", s);
+        hipLaunchKernelGGL(k_seed_dedup_tile, dim3(1), dim3(kScanThreads), 0, s, a.list, a.len_const,
+                           (unsigned long long *)a.map, a.tag, a.n_nodes, a.nodes, a.size_out, a.err, a.err_next);
+        GNNAV_HIP(hipGetLastError());
+        return;
+    }
     if ((a.len_bound > 0 || a.err_next) && !a.first_done) {
         KernelTimer t("dedup_first", s);
         hipLaunchKernelGGL(k_first_position, dim3(grid_for(a.len_bound, 256, 8192)), dim3(256), 0, s,
