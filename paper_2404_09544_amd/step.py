@@ -25,11 +25,13 @@ Device buffers are torch tensors that only grow.
 """
 from __future__ import annotations
 
+import atexit
+
 import numpy as np
 import torch
 
 from . import (Blocks, Cache, Graph, gather, gather_n, sage_forward, sage_train_step, sample, sample_async,
-               sample_biased, stream_create, sync)
+               sample_biased, stream_create, stream_destroy, sync)
 
 
 def to_device_weights(ws, dtype: str):
@@ -160,6 +162,19 @@ class MiniBatchStep:
 
 _STREAMS = []
 _PART_STREAMS = {}
+
+
+@atexit.register
+def _release_part_streams():
+    """The library's compute-unit-share streams, released at exit after their
+    work (a failure here has already been reported by the work itself)."""
+    for streams in _PART_STREAMS.values():
+        for st in streams:
+            try:
+                stream_destroy(st)
+            except Exception:
+                pass
+    _PART_STREAMS.clear()
 
 
 def pipeline_streams(n: int, cu_partition: bool = False):
