@@ -36,3 +36,55 @@ def test_one_hip_runtime_whatever_the_import_order():
     r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=300)
     assert r.returncode == 0, r.stderr
     assert r.stdout.splitlines()[0] == "1", r.stdout
+
+
+def test_bench_pipeline_choice():
+    """bench.py's pipelined legs: forced settings are taken as given, and in
+    auto mode every candidate is timed and the fastest kept (a stand-in
+    pipeline whose batches take a known time per setting)."""
+    import argparse
+    import time as _time
+    sys.path.insert(0, ROOT)
+    import bench
+
+    class FakeCuda:
+        @staticmethod
+        def synchronize():
+            pass
+
+    class FakeTorch:
+        cuda = FakeCuda
+
+    cost = {(False, 3): 0.004, (True, 2): 0.001, (True, 3): 0.003}
+    made = []
+
+    class FakePipe:
+        def __init__(self, depth, part):
+            self.key = (part, depth)
+            made.append(self)
+
+        def enqueue(self, b):
+            _time.sleep(cost[self.key])
+
+        def synchronize(self):
+            pass
+
+    def run(**kw):
+        a = argparse.Namespace(cu_partition="auto", depth=None)
+        for k, v in kw.items():
+            setattr(a, k, v)
+        return bench.pick_pipeline(a, lambda d, p: FakePipe(d, p), lambda p, b: p.enqueue(b), 4, FakeTorch,
+                                   n_time=3)
+
+    assert run(cu_partition="on")[:2] == (True, 2)
+    assert run(cu_partition="off")[:2] == (False, 3)
+    assert run(cu_partition="on", depth=4)[:2] == (True, 4)
+    made.clear()
+    part, depth, trial = run()
+    assert (part, depth) == (True, 2)
+    assert set(trial) == {"all_units_3", "shares_2", "shares_3"}
+    assert min(trial, key=trial.get) == "shares_2"
+    assert len(made) == 3
+    made.clear()
+    part, depth, trial = run(depth=3)
+    assert depth == 3 and set(trial) == {"all_units_3", "shares_3"} and part is True
