@@ -96,9 +96,10 @@ class MiniBatchStep:
         return self.logits[:sizes[0]]
 
     # ------------------------------------------------------------- async
-    def enqueue(self, seeds_dev, rng_seed: int, stream=None, gather_after=None):
+    def enqueue(self, seeds_dev, rng_seed: int, stream=None, gather_after=None, record_gather: bool = True):
         """Enqueue one batch on `stream` without waiting for it; the gather's
-        row copies wait for the event `gather_after` when given."""
+        row copies wait for the event `gather_after` when given, and
+        `self.gathered` is recorded after them unless record_gather is off."""
         st = stream if stream is not None else torch.cuda.current_stream()
         self._seeds = seeds_dev            # keep alive until the work has run
         self._stream = st
@@ -107,7 +108,8 @@ class MiniBatchStep:
         self._grow(bounds[-1], bounds[0], st)
         gather_n(self.cache, self.blocks.nodes_ptr(), sizes_ptr + 4 * self.L, bounds[-1], self.h0,
                  self.counts, st, copy_after=gather_after)
-        self.gathered.record(st)
+        if record_gather:
+            self.gathered.record(st)
         sage_forward(self.blocks, self.h0, self.weights, self.dims, self.dtype, self.logits, st)
         self.sizes = None
 
@@ -220,10 +222,15 @@ class Pipeline:
         return self.slots[(self.count - 1) % self.depth].gathered if self.count > 0 else None
 
     def enqueue(self, seeds_dev, rng_seed: int):
-        """Enqueue the next batch; returns the slot it runs in."""
+        """Enqueue the next batch; returns the slot it runs in.  With the
+        whole feature store in HBM no gather crosses the host link, so the
+        gathers are not ordered (no event per batch)."""
         k = self.count % self.depth
         self._link()
-        self.slots[k].enqueue(seeds_dev, rng_seed, self.streams[k], gather_after=self._previous_gather())
+        if self.cache.store_on_device:
+            self.slots[k].enqueue(seeds_dev, rng_seed, self.streams[k], record_gather=False)
+        else:
+            self.slots[k].enqueue(seeds_dev, rng_seed, self.streams[k], gather_after=self._previous_gather())
         self.count += 1
         return self.slots[k]
 

@@ -587,11 +587,13 @@ def test_async_bad_seed_reported_at_sync(G):
     assert e.value.status == 2
 
 
+@pytest.mark.parametrize("on_device", [False, True])
 @pytest.mark.parametrize("cu_partition", [False, True])
 @pytest.mark.parametrize("depth", [2, 3])
-def test_pipeline_matches_oracle(G, depth, cu_partition):
+def test_pipeline_matches_oracle(G, depth, cu_partition, on_device):
     """Batches on alternating streams give each batch's oracle result, also
-    with each stream on its own share of the compute units."""
+    with each stream on its own share of the compute units, and with the
+    whole store in HBM (then the gathers are not ordered on the link)."""
     from paper_2404_09544_amd.step import Pipeline, to_device_weights
     wl = W.Workload("chunglu-10k-d64")
     s, d = wl.edges()
@@ -599,7 +601,7 @@ def test_pipeline_matches_oracle(G, depth, cu_partition):
     r = 0.3
     ws = [W.glorot(wl.dims[l], wl.dims[l + 1], wl.dtype, seed=11 + l) for l in range(wl.L)]
     g = G.Graph(wl.n, s, d)
-    c = G.Cache(g, feats, wl.dtype, r)
+    c = G.Cache(g, feats, wl.dtype, r, store_on_device=on_device)
     pipe = Pipeline(g, c, to_device_weights(ws, wl.dtype), wl.dims, wl.fanouts, wl.dtype, depth=depth,
                     cu_partition=cu_partition)
     seeds_dev = [dev(wl.seeds(b)) for b in range(2 * depth)]
@@ -607,7 +609,7 @@ def test_pipeline_matches_oracle(G, depth, cu_partition):
         slots = []
         for k in range(depth):
             b = rnd * depth + k
-            say("pipeline", depth, cu_partition, b)
+            say("pipeline", depth, cu_partition, on_device, b)
             slots.append((b, pipe.enqueue(seeds_dev[b], wl.rng_seed(b))))
         for b, slot in slots:
             slot.finish()
