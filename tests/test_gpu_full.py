@@ -107,6 +107,47 @@ def test_full_batch(G, name):
         c.close()
 
 
+@pytest.mark.parametrize("name", ["chunglu-2450k-d100", "rmat-10m-d128"])
+def test_full_large_batch(G, name):
+    """A batch of 16,384 seeds (consecutive batches of the epoch permutation
+    taken together) on the two largest graphs: frontiers of millions of
+    nodes, multi-thousand-tile scans and the widest grids, every block,
+    count and gathered row bit-exact, sampled logits rows within tolerance."""
+    import torch
+    from paper_2404_09544_amd.step import MiniBatchStep, to_device_weights
+    wl, _, _, csr, g = load(G, name)
+    feats = wl.features()
+    ws = wl.weights()
+    wd = [O.to_f64(w, wl.dtype) for w in ws]
+    bf16 = wl.dtype == "bf16"
+    r = wl.cfg["cache"]
+    t = time.perf_counter()
+    c = G.Cache(g, feats, wl.dtype, r, store_on_device=wl.cfg["store_on_device"])
+    step = MiniBatchStep(g, c, to_device_weights(ws, wl.dtype), wl.dims, wl.fanouts, wl.dtype)
+    _, slot, _ = O.rank_cache(csr, r)
+    seeds = np.concatenate([wl.seeds(b) for b in range(16384 // wl.batch)])
+    rng = wl.rng_seed(99)
+    logits = step.run(torch.from_numpy(seeds).cuda(), rng).cpu().numpy()
+    nodes, sizes, ip, nb, ix = step.blocks.to_host()
+    say(name, f"large batch on the GPU: sizes {sizes} ({time.perf_counter() - t:.1f}s)")
+    ref_b = O.sample_blocks(csr, seeds, wl.fanouts, rng)
+    assert sizes == ref_b.sizes
+    assert np.array_equal(nodes, ref_b.nodes)
+    for h in range(wl.L):
+        assert np.array_equal(ip[h], ref_b.indptr[h]), f"indptr hop {h + 1}"
+        assert np.array_equal(nb[h], ref_b.nbrs[h]), f"neighbours hop {h + 1}"
+        assert np.array_equal(ix[h], ref_b.indices[h]), f"indices hop {h + 1}"
+    h0, counts = O.gather(feats, slot, ref_b.nodes)
+    assert np.array_equal(step.counts.cpu().numpy(), counts)
+    got_h0 = step.h0_view().cpu().numpy()[:, :wl.d]
+    assert np.array_equal(got_h0.view(np.uint8), h0.view(np.uint8))
+    rows = np.random.default_rng(5).choice(sizes[0], size=128, replace=False)
+    ref = O.sage_forward_rows(ref_b, O.to_f64(h0, wl.dtype), wd, rows, bf16=bf16)
+    assert_rows_close(logits[rows], ref, BF16_TOL if bf16 else FP32_TOL, f"{name} large-batch logits")
+    say(name, f"large batch checked: hits/misses {counts.tolist()} ({time.perf_counter() - t:.1f}s)")
+    c.close()
+
+
 # logits rows checked per pipelined batch: every row of F_0 (None) where the
 # oracle's double-precision forward of the whole batch takes seconds
 PIPE_ROWS = {"chunglu-169k-d128": None, "chunglu-233k-d602": None, "chunglu-2450k-d100": 256,
