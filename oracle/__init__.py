@@ -65,6 +65,8 @@ def _load():
     lib.oracle_gather.restype = None
     lib.oracle_cache_fifo_admit.argtypes = [P, P, i64, i64, P, P, i64]
     lib.oracle_cache_fifo_admit.restype = None
+    lib.oracle_cache_lru_update.argtypes = [P, P, i64, i64, P, P, P, i64, P, i64]
+    lib.oracle_cache_lru_update.restype = None
     lib.oracle_round_bf16.argtypes = [f64]
     lib.oracle_round_bf16.restype = f64
     lib.oracle_round_bf16_array.argtypes = [P, P, i64]
@@ -258,6 +260,38 @@ class FifoCache:
             _load().oracle_cache_fifo_admit(_ptr(self.slot_map), _ptr(self.owner), self.ring_lo,
                                             self.ring_n, _ptr(self.ptr), _ptr(misses), misses.size)
         return rows, counts
+
+
+class LruCache(FifoCache):
+    """Oracle state of a cache with an LRU policy over its last `ring_n` slots.
+
+    Starts from the degree-ranked static cache with the ring's slots in
+    index order as the initial recency (lowest slot least recent); after each
+    gather the ring slots the batch hit become the most recent and the
+    misses are admitted into the least recently used slots (see
+    oracle_cache_lru_update in oracle.c).
+    """
+
+    def __init__(self, csr: "CSR", r: float, ring_n: int):
+        super().__init__(csr, r, ring_n)
+        self.order = np.arange(self.ring_lo, self.c, dtype=np.int32)
+        self.head = np.zeros(1, np.int64)
+
+    def gather(self, features, ids):
+        ids = _i32(ids)
+        ok = (ids >= 0) & (ids < self.n)
+        slots = self.slot_map[ids[ok]]
+        hit_slots = np.ascontiguousarray(slots[slots >= 0], dtype=np.int32)
+        rows, counts, misses = gather(features, self.slot_map, ids, want_misses=True)
+        if self.ring_n > 0:
+            _load().oracle_cache_lru_update(_ptr(self.slot_map), _ptr(self.owner), self.ring_lo, self.ring_n,
+                                            _ptr(self.order), _ptr(self.head), _ptr(hit_slots),
+                                            hit_slots.size, _ptr(misses), misses.size)
+        return rows, counts
+
+    def recency(self) -> np.ndarray:
+        """Ring slots from least to most recently used."""
+        return np.roll(self.order, -int(self.head[0]))
 
 
 # ------------------------------------------------------------ bf16, O8 ---

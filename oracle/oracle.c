@@ -374,6 +374,53 @@ void oracle_cache_fifo_admit(int32_t *slot_map, int32_t *owner, int64_t ring_lo,
     }
 }
 
+/* Policy LRU over the same ring of slots.  `order` lists the ring's slots
+ * from least to most recently used, as a circular list that starts at
+ * order[*head].  Recency is counted in batches: every request of one batch
+ * is a use at the same time.  After a gather that hit the slots
+ * hit_slots[0..n_hits) (any slots, repeats allowed; those outside the ring
+ * are ignored) and missed misses[0..m) (request order):
+ *   1. the ring slots hit by the batch become the most recently used, after
+ *      every slot it did not touch; each group keeps its earlier relative
+ *      order (ties within a batch go to the earlier recency);
+ *   2. the misses are admitted one by one in request order, as in FIFO: each
+ *      takes the least recently used slot, whose vertex is evicted (unmapped
+ *      if the slot map still points at the slot), and that slot becomes the
+ *      most recently used.
+ * With no ring slot ever hit this is the FIFO policy above.               */
+void oracle_cache_lru_update(int32_t *slot_map, int32_t *owner, int64_t ring_lo, int64_t ring_n, int32_t *order,
+                             int64_t *head, const int32_t *hit_slots, int64_t n_hits, const int32_t *misses,
+                             int64_t m) {
+    if (ring_n <= 0) return;
+    /* step 1: stable partition of the recency list (untouched, then hit) */
+    unsigned char *hit = calloc((size_t)ring_n, 1);
+    int32_t *list = malloc((size_t)ring_n * sizeof(int32_t));
+    for (int64_t i = 0; i < n_hits; ++i) {
+        int64_t s = hit_slots[i];
+        if (s >= ring_lo && s < ring_lo + ring_n) hit[s - ring_lo] = 1;
+    }
+    int64_t k = 0;
+    for (int pass = 0; pass < 2; ++pass)
+        for (int64_t j = 0; j < ring_n; ++j) {
+            int32_t s = order[(*head + j) % ring_n];
+            if (hit[s - ring_lo] == pass) list[k++] = s;
+        }
+    for (int64_t j = 0; j < ring_n; ++j) order[j] = list[j];
+    *head = 0;
+    /* step 2: admissions, least recently used slot first */
+    for (int64_t i = 0; i < m; ++i) {
+        int32_t s = order[*head];
+        if (owner[s] >= 0 && slot_map[owner[s]] == s) slot_map[owner[s]] = -1;
+        owner[s] = misses[i];
+        slot_map[misses[i]] = s;
+        /* the slot leaves the front and rejoins at the back: in the circular
+         * list that is the same cell with the start moved past it */
+        *head = (*head + 1) % ring_n;
+    }
+    free(hit);
+    free(list);
+}
+
 /* ------------------------------------------------------------- bf16 RNE ---
  * Nearest bfloat16 value of a double, ties to even (IEEE 754-2008 binary
  * rounding with 8 significant bits, exponent range of binary32).  Values at

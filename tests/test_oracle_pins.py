@@ -560,6 +560,159 @@ def test_fifo_cache_repeat_batch_hits():
     assert ring[:100].tolist() == ids.tolist()
 
 
+# -------------------------------------------------- LRU cache update, O7 --
+
+def _hub_graph(n, hubs):
+    """Vertices `hubs` joined to every other vertex, nothing else: the hubs
+    rank first (ties by id), so they are the cache's initial contents."""
+    u = [h for h in hubs for x in range(n) if x not in hubs]
+    v = [x for h in hubs for x in range(n) if x not in hubs]
+    return O.build_csr(n, u, v)
+
+
+def _faults(cache, refs, n):
+    feats = W.features(n, 2, "f32", seed=0)
+    misses = 0
+    for x in refs:
+        _, counts = cache.gather(feats, np.array([x], np.int32))
+        misses += int(counts[1])
+    return misses
+
+
+# Page-replacement textbook values (one request per batch, frames = ring
+# slots, the ring's initial vertices never requested, so it starts "empty"):
+#   Silberschatz, Galvin, Gagne, Operating System Concepts, ch. "Virtual
+#   Memory": reference string 7 0 1 2 0 3 0 4 2 3 0 3 2 1 2 0 1 7 0 1 with 3
+#   frames gives 15 faults under FIFO and 12 under LRU;
+#   Belady, Nelson, Shedler, CACM 12(6) 1969: 1 2 3 4 1 2 5 1 2 3 4 5 gives 9
+#   FIFO faults with 3 frames and 10 with 4 (Belady's anomaly); LRU, a stack
+#   algorithm (Mattson et al., IBM Syst. J. 9(2) 1970), gives 10 and 8.
+_SILBERSCHATZ = [7, 0, 1, 2, 0, 3, 0, 4, 2, 3, 0, 3, 2, 1, 2, 0, 1, 7, 0, 1]
+_BELADY = [1, 2, 3, 4, 1, 2, 5, 1, 2, 3, 4, 5]
+
+
+@pytest.mark.parametrize("refs,frames,fifo,lru", [(_SILBERSCHATZ, 3, 15, 12), (_BELADY, 3, 9, 10),
+                                                  (_BELADY, 4, 10, 8)])
+def test_cache_policies_textbook_fault_counts(refs, frames, fifo, lru):
+    n = 20
+    csr = _hub_graph(n, list(range(n - frames, n)))
+    r = (frames + 0.5) / n
+    f, l = O.FifoCache(csr, r, frames), O.LruCache(csr, r, frames)
+    assert f.c == frames and sorted(f.owner.tolist()) == list(range(n - frames, n))
+    assert _faults(f, refs, n) == fifo
+    assert _faults(l, refs, n) == lru
+
+
+def test_lru_cache_worked_batches():
+    """Three multi-request batches on a ring of 4 slots, worked by hand.
+    Slots 0..3 start with A..D = vertices 16..19, least recent first.
+      batch [C, X, A, Y]: C, A hit; recency 1 3 0 2 (untouched B, D first,
+        then the hit slots in their earlier order); X takes slot 1 (B out),
+        Y slot 3 (D out); recency 0 2 1 3.
+      batch [Z, D, B, W, V]: five misses for four slots: Z -> 0 (A out),
+        D -> 2 (C out), B -> 1 (X out), W -> 3 (Y out), V -> 0 (Z out);
+        recency 2 1 3 0.
+      batch [W, Q, B]: W, B hit; recency 2 0 1 3; Q takes slot 2 (D out);
+        recency 0 1 3 2."""
+    n = 20
+    csr = _hub_graph(n, [16, 17, 18, 19])
+    A, B, C, D = 16, 17, 18, 19
+    X, Y, Z, Wv, V, Q = 1, 2, 3, 4, 5, 6
+    cache = O.LruCache(csr, 0.2, 4)
+    feats = W.features(n, 3, "f32", seed=5)
+    steps = [([C, X, A, Y], [2, 2, 0], [A, X, C, Y], [0, 2, 1, 3]),
+             ([Z, D, B, Wv, V], [0, 5, 0], [V, B, D, Wv], [2, 1, 3, 0]),
+             ([Wv, Q, B], [2, 1, 0], [V, B, Q, Wv], [0, 1, 3, 2])]
+    for ids, counts, owners, recency in steps:
+        rows, got = cache.gather(feats, np.array(ids, np.int32))
+        assert rows.tobytes() == feats[ids].tobytes()
+        assert got.tolist() == counts
+        assert cache.owner.tolist() == owners
+        assert cache.recency().tolist() == recency
+        for s, x in enumerate(owners):
+            assert cache.slot_map[x] == s
+        assert (cache.slot_map >= 0).sum() == 4
+    assert cache.slot_map[[A, C, X, Y, Z, D]].tolist() == [-1] * 6
+
+
+def _list_lru(rank, c, ring_n, batches, n):
+    """Independent LRU model: a Python list of [slot, vertex] pairs, least
+    recent first, and a dict of the mapped ring vertices."""
+    lo = c - ring_n
+    static = set(int(x) for x in rank[:lo])
+    ring = [[lo + j, int(rank[lo + j])] for j in range(ring_n)]
+    mapped = {v: s for s, v in ring}
+    hist, ring_hits = [], 0
+    for ids in batches:
+        cached = static | set(mapped)
+        req = [int(v) for v in ids if 0 <= v < n]
+        hits = [v for v in req if v in cached]
+        misses = [v for v in req if v not in cached]
+        hist.append((len(hits), len(misses)))
+        touched = {mapped[v] for v in hits if v in mapped}
+        ring_hits += len(touched)
+        ring = [e for e in ring if e[0] not in touched] + [e for e in ring if e[0] in touched]
+        for v in misses:
+            if not ring:
+                break
+            s, old = ring.pop(0)
+            if mapped.get(old) == s:
+                del mapped[old]
+            mapped[v] = s
+            ring.append([s, v])
+    return hist, static | set(mapped), [s for s, _ in ring], ring_hits
+
+
+@pytest.mark.parametrize("r,frac,repeats", [(0.1, 1.0, False), (0.2, 0.5, False), (0.05, 0.25, True),
+                                            (0.3, 0.0, False), (0.1, 0.1, True)])
+def test_lru_cache_matches_list_model(r, frac, repeats):
+    """Batches drawn with a hot set (so ring slots are hit again), some with
+    repeated vertices and with out-of-range ids."""
+    n, u, v = W.random_graph(n=600, m=5000, seed=35)
+    csr = O.build_csr(n, u, v)
+    rank, _, c = O.rank_cache(csr, r)
+    ring_n = int(c * frac)
+    rng = np.random.default_rng(9)
+    hot = rng.choice(n, 80, replace=False)
+    batches = []
+    for _ in range(12):
+        ids = np.concatenate([rng.choice(hot, 40), rng.integers(0, n, 60)]).astype(np.int32)
+        if not repeats:
+            ids = np.unique(ids)
+        ids = rng.permutation(ids)
+        ids[rng.integers(0, ids.size, 2)] = [-1, n]
+        batches.append(ids)
+    feats = W.features(n, 3, "f32", seed=6)
+    cache = O.LruCache(csr, r, ring_n)
+    got = []
+    for ids in batches:
+        rows, counts = cache.gather(feats, ids)
+        got.append((int(counts[0]), int(counts[1])))
+    hist, final, recency, ring_hits = _list_lru(rank, c, ring_n, batches, n)
+    assert got == hist
+    assert (ring_hits > 0) == (frac > 0)    # the recency reorder is exercised
+    assert {int(x) for x in np.nonzero(cache.slot_map >= 0)[0]} == final
+    assert cache.recency().tolist() == recency
+    for x in np.nonzero(cache.slot_map >= 0)[0]:
+        assert cache.owner[cache.slot_map[x]] == x
+
+
+def test_lru_without_ring_hits_is_fifo():
+    """Batches of vertices never cached before, so no request hits the ring:
+    LRU then admits exactly as FIFO does."""
+    n, u, v = W.random_graph(n=500, m=4000, seed=36)
+    csr = O.build_csr(n, u, v)
+    f, l = O.FifoCache(csr, 0.2, 60), O.LruCache(csr, 0.2, 60)
+    cold = np.random.default_rng(4).permutation(np.nonzero(f.slot_map < 0)[0]).astype(np.int32)
+    feats = W.features(n, 2, "f32", seed=3)
+    for ids in np.array_split(cold[:350], 7):   # 50 a batch: older admissions are gone before reuse
+        _, cf = f.gather(feats, ids)
+        _, cl = l.gather(feats, ids)
+        assert cf.tolist() == cl.tolist() == [0, ids.size, 0]
+        assert f.owner.tolist() == l.owner.tolist()
+        assert f.slot_map.tolist() == l.slot_map.tolist()
+
+
 # ------------------------------------------- loss, backward, update ---
 
 def _loss_of(blocks, H0, Ws, y):
