@@ -62,7 +62,7 @@ def kernel_source_hash(files) -> str:
 
 KERNEL_SOURCES = {"aggregate_mean": ["spmm.hip", "common.hpp"],
                   "gather_rows": ["gather.hip", "common.hpp"],
-                  "cache_admit": ["gather.hip", "common.hpp"],
+                  "cache_admit": ["cache_update.hip", "scan.hpp", "common.hpp"],
                   "classify": ["gather.hip", "scan.hpp", "common.hpp"],
                   "combine_gemm": ["gemm.hip", "common.hpp", "dma.hpp", "bf16split.hpp"],
                   "sample_hop": ["sample.hip", "common.hpp"],
@@ -537,7 +537,7 @@ def kernel_entries(args, G, g, c, wl, fwd, seeds_dev, ring, link, profiled_confi
             G.sample_biased(g, c, args.eta, seeds_dev[b], wl.fanouts, wl.rng_seed(b), probe)
         _, sz, ip, _, ix = probe.to_host()
         if sz != [int(x) for x in n_h]:
-            # only a biased sampler over a cache that moved since (FIFO) can
+            # only a biased sampler over a cache that moved since (FIFO or LRU) can
             # do this; the distinct-row counts are then of a similar batch
             log(f"batch {b}: re-sampled sizes {sz} differ from the timed batch's {[int(x) for x in n_h]}")
         for l in range(1, L + 1):
@@ -674,10 +674,11 @@ def main():
                     help="run each pipelined batch on its own share of the compute units (auto: time a few "
                          "batches of three streams on all units, two on halves and three on thirds before "
                          "the timed region and keep the fastest)")
-    ap.add_argument("--cache-policy", choices=["static", "fifo"], default="static",
-                    help="fifo: admit each batch's misses into a ring over the last cache slots")
+    ap.add_argument("--cache-policy", choices=["static", "fifo", "lru"], default="static",
+                    help="fifo: admit each batch's misses into a ring over the last cache slots; lru: the same "
+                         "ring, evicting the least recently used slots first")
     ap.add_argument("--dynamic-fraction", type=float, default=1.0,
-                    help="share of the cache slots in the FIFO ring (with --cache-policy fifo)")
+                    help="share of the cache slots in the ring (with --cache-policy fifo or lru)")
     ap.add_argument("--eta", type=int, default=None,
                     help="locality-biased sampling: cached neighbours weigh eta (default: uniform)")
     ap.add_argument("--no-train", action="store_true", help="skip the training leg")
@@ -734,10 +735,10 @@ def main():
     link = link_calibration(G, c, wl, torch)
     log(f"host link: DMA {link['dma_h2d_gbs']} GB/s, zero-copy gather of uncached rows {link['zero_copy_gather_gbs']} GB/s")
     ring = 0
-    if args.cache_policy == "fifo":
+    if args.cache_policy != "static":
         ring = int(round(c.n_cached * min(max(args.dynamic_fraction, 0.0), 1.0)))
-        c.set_policy("fifo", ring)
-        log(f"FIFO ring over the last {ring} of {c.n_cached} cache slots")
+        c.set_policy(args.cache_policy, ring)
+        log(f"{args.cache_policy.upper()} ring over the last {ring} of {c.n_cached} cache slots")
     ws = wl.weights()
     wdev = to_device_weights(ws, wl.dtype)
     n_b = args.warmup + args.steps
@@ -810,7 +811,7 @@ def main():
         t0 = time.perf_counter()
         csr = O.build_csr(wl.n, src, dst)
         _, slot, _ = O.rank_cache(csr, r)
-        fifo = O.FifoCache(csr, r, ring) if ring else None
+        dyn = ({"fifo": O.FifoCache, "lru": O.LruCache}[args.cache_policy](csr, r, ring) if ring else None)
         wd = [O.to_f64(w, wl.dtype) for w in ws]
         log(f"oracle set-up {time.perf_counter() - t0:.1f}s")
         # whole batches until --cpu-seconds have passed (at most --cpu-batches)
@@ -818,10 +819,10 @@ def main():
         t0 = time.perf_counter()
         while nb < max(1, args.cpu_batches) and (nb == 0 or time.perf_counter() - t0 < args.cpu_seconds):
             b = args.warmup + nb
-            bias = None if args.eta is None else (fifo.slot_map if fifo else slot)
+            bias = None if args.eta is None else (dyn.slot_map if dyn else slot)
             ob = O.sample_blocks(csr, wl.seeds(b), wl.fanouts, wl.rng_seed(b), bias_slot_map=bias,
                                  eta=args.eta or 1)
-            h0, _ = fifo.gather(feats, ob.nodes) if fifo else O.gather(feats, slot, ob.nodes)
+            h0, _ = dyn.gather(feats, ob.nodes) if dyn else O.gather(feats, slot, ob.nodes)
             O.sage_forward(ob, O.to_f64(h0, wl.dtype), wd, bf16=wl.dtype == "bf16")
             nb += 1
         ct = time.perf_counter() - t0
@@ -835,13 +836,13 @@ def main():
         P = max(1, min(len(os.sched_getaffinity(0)), args.cpu_threads))
 
         def one(b):
-            bias = None if args.eta is None else (fifo.slot_map if fifo else slot)
+            bias = None if args.eta is None else (dyn.slot_map if dyn else slot)
             ob = O.sample_blocks(csr, wl.seeds(b), wl.fanouts, wl.rng_seed(b), bias_slot_map=bias,
                                  eta=args.eta or 1)
             h0, _ = O.gather(feats, slot, ob.nodes)
             O.sage_forward(ob, O.to_f64(h0, wl.dtype), wd, bf16=wl.dtype == "bf16")
 
-        if P > 1 and fifo is None:
+        if P > 1 and dyn is None:
             import concurrent.futures as cf
             t0 = time.perf_counter()
             with cf.ThreadPoolExecutor(max_workers=P) as ex:
@@ -890,7 +891,7 @@ def main():
                    "batch": wl.batch, "layers": wl.L, "dims": wl.dims, "cache_fraction": r,
                    "store_on_device": wl.cfg["store_on_device"], "cache_policy": args.cache_policy,
                    "sampler": "uniform" if args.eta is None else f"locality-biased eta={args.eta}",
-                   "fifo_slots": ring, "global_batch": wl.batch},
+                   "dynamic_slots": ring, "global_batch": wl.batch},
         "value_sequential": round(wl.batch * args.steps / fwd["seq_elapsed"], 2),
         "roofline": roofline,
         "roofline_device": roofline_device,

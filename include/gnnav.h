@@ -193,14 +193,24 @@ gnnav_status gnnav_cache_set_link_workgroups(gnnav_cache *c, int32_t workgroups)
  * vertices.  A vertex requested more than once in one gather is admitted
  * once per missing request and stays mapped to the last of its slots (the
  * others hold copies of its row until the ring reaches them); request lists
- * without repeats, such as a frontier, never do this.  Rows
- * are copied from the gather's own output.  With a dynamic cache, gathers on
- * different streams run one after another in call order.  The call
- * synchronises the device and restarts the ring pointer at the ring's
- * first slot; the cache contents are kept.
+ * without repeats, such as a frontier, never do this.
+ * GNNAV_POLICY_LRU uses the same ring with a recency order in place of the
+ * pointer (least recently used first, counted in batches: all requests of
+ * one gather are one use).  After each gather the ring slots it hit move
+ * behind every slot it did not touch, each group keeping its earlier
+ * order; then the misses are admitted in request order as above, each
+ * taking the least recently used slot, which becomes the most recent.
+ * With no hit on the ring this is FIFO.  The ring holds per slot 12 bytes
+ * of device state besides the row.
+ * Rows are copied from the gather's own output.  With a dynamic cache,
+ * gathers on different streams run one after another in call order.  The
+ * call synchronises the device and restarts the ring pointer at the ring's
+ * first slot (LRU: the recency order at the slot order, lowest slot least
+ * recent); the cache contents are kept.
  * Errors: E_INVALID (unknown policy, dynamic_slots outside [0, n_cached]).  */
 #define GNNAV_POLICY_STATIC 0
 #define GNNAV_POLICY_FIFO 1
+#define GNNAV_POLICY_LRU 2
 gnnav_status gnnav_cache_set_policy(gnnav_cache *c, int32_t policy, int64_t dynamic_slots);
 
 void gnnav_cache_free(gnnav_cache *c);
@@ -311,7 +321,7 @@ gnnav_status gnnav_gather_n_after(const gnnav_cache *c, const int32_t *ids_dev,
 
 /* gnnav_gather for callers that cannot allocate device memory (code under
  * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
- * the same results as gnnav_gather (static or FIFO cache) for at most
+ * the same results as gnnav_gather (any update policy) for at most
  * 1,048,576 ids, with no hipMalloc, hipFree or other allocation.  Its
  * workspace (hit and miss lists, counts, the classification scan's ticket
  * and tile records; about 16.02 MiB per device) is a static device array
@@ -465,8 +475,9 @@ gnnav_status gnnav_weight_grad(const float *self_dev, int64_t ld_self, const flo
  * row lists its cached picks (Floyd order), then the uncached ones.
  * deg(v) <= k takes the whole row as gnnav_sample does.  Frontier union,
  * blocks and sizes are exactly as gnnav_sample.  async != 0: no final
- * synchronisation (as gnnav_sample_async).  With a FIFO cache the slot map
- * is read after the cache's last update (ordered by its event).
+ * synchronisation (as gnnav_sample_async).  With an updating (FIFO or LRU)
+ * cache the slot map is read after the cache's last update (ordered by its
+ * event).
  * Errors: as gnnav_sample; E_INVALID also for a NULL cache, a cache of
  * another graph, eta outside [1, 65536], or a fanout above 64.          */
 gnnav_status gnnav_sample_biased(const gnnav_graph *g, const gnnav_cache *cache, uint32_t eta,

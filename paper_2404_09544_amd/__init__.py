@@ -233,8 +233,8 @@ class Cache:
         self.n = graph.n
 
     def set_policy(self, policy: str, dynamic_slots: int = 0):
-        """'static' or 'fifo' over the last `dynamic_slots` cache slots."""
-        code = {"static": 0, "fifo": 1}[policy]
+        """'static', or 'fifo' / 'lru' over the last `dynamic_slots` cache slots."""
+        code = {"static": 0, "fifo": 1, "lru": 2}[policy]
         _check(_lib.gnnav_cache_set_policy(self._h, code, int(dynamic_slots)))
 
     def set_link_workgroups(self, workgroups: int):

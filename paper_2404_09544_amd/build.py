@@ -19,7 +19,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libgnnav.so")
-SOURCES = ["api.hip", "sample.hip", "gather.hip", "spmm.hip", "gemm.hip", "train.hip"]
+SOURCES = ["api.hip", "sample.hip", "gather.hip", "cache_update.hip", "spmm.hip", "gemm.hip", "train.hip"]
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE,
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

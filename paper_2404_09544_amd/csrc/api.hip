@@ -467,10 +467,13 @@ struct gnnav_cache {
     std::mutex ws_mu;
     std::vector<GatherWs *> ws;
     int32_t link_wgs = 64;            // workgroups copying misses over the host link
-    // update policy (GNNAV_POLICY_*); FIFO ring over slots [ring_lo, c)
+    // update policy (GNNAV_POLICY_*) over the ring of slots [ring_lo, c):
+    // FIFO's ring pointer, LRU's recency list, stamps and partition scan
     int32_t policy = 0;
     int64_t ring_lo = 0, ring_n = 0;
     DevBuf owner, ring_ptr;
+    DevBuf lru_order, lru_part, lru_stamp, lru_ctl;
+    ScanState lru_scan;
     std::mutex upd_mu;
     hipEvent_t upd_done = nullptr;
     bool upd_recorded = false;
@@ -507,6 +510,11 @@ static void free_cache(gnnav_cache *c) {
     }
     c->owner.release();
     c->ring_ptr.release();
+    c->lru_order.release();
+    c->lru_part.release();
+    c->lru_stamp.release();
+    c->lru_ctl.release();
+    c->lru_scan.release();
     c->part_col.release();
     c->part_cnt.release();
     if (c->part_ready) (void)hipEventDestroy(c->part_ready);
@@ -661,13 +669,14 @@ extern "C" gnnav_status gnnav_cache_set_link_workgroups(gnnav_cache *c, int32_t 
 extern "C" gnnav_status gnnav_cache_set_policy(gnnav_cache *c, int32_t policy, int64_t dynamic_slots) {
     return guarded([&] {
         GNNAV_CHECK(c, GNNAV_E_INVALID, "cache is NULL");
-        GNNAV_CHECK(policy == GNNAV_POLICY_STATIC || policy == GNNAV_POLICY_FIFO, GNNAV_E_INVALID, "unknown policy");
+        GNNAV_CHECK(policy == GNNAV_POLICY_STATIC || policy == GNNAV_POLICY_FIFO || policy == GNNAV_POLICY_LRU,
+                    GNNAV_E_INVALID, "unknown policy");
         GNNAV_CHECK(policy == GNNAV_POLICY_STATIC || (dynamic_slots >= 0 && dynamic_slots <= c->c), GNNAV_E_INVALID,
                     "dynamic_slots outside [0, cached rows]");
         GNNAV_HIP(hipDeviceSynchronize());
         std::lock_guard<std::mutex> lk(c->upd_mu);
         c->policy = policy;
-        c->ring_n = policy == GNNAV_POLICY_FIFO ? dynamic_slots : 0;
+        c->ring_n = policy == GNNAV_POLICY_STATIC ? 0 : dynamic_slots;
         c->ring_lo = c->c - c->ring_n;
         c->part_graph = nullptr;   // the slot map may have moved: rebuild the partition on next use
         if (c->ring_n > 0) {
@@ -679,6 +688,23 @@ extern "C" gnnav_status gnnav_cache_set_policy(gnnav_cache *c, int32_t policy, i
             }
             c->ring_ptr.ensure(sizeof(int32_t), s0);
             GNNAV_HIP(hipMemset(c->ring_ptr.p, 0, sizeof(int32_t)));
+            if (policy == GNNAV_POLICY_LRU) {
+                // recency starts in slot order (lowest ring slot least
+                // recent); `part` starts as a copy, so it only ever holds ring
+                // slots, even where a partition scan that gave up left a gap
+                const size_t bytes = (size_t)c->ring_n * sizeof(int32_t);
+                c->lru_order.ensure(bytes, s0);
+                c->lru_part.ensure(bytes, s0);
+                c->lru_stamp.ensure(bytes, s0);
+                c->lru_ctl.ensure(2 * sizeof(uint32_t), s0);
+                std::vector<int32_t> order((size_t)c->ring_n);
+                for (int64_t j = 0; j < c->ring_n; ++j) order[(size_t)j] = (int32_t)(c->ring_lo + j);
+                GNNAV_HIP(hipMemcpy(c->lru_order.p, order.data(), bytes, hipMemcpyHostToDevice));
+                GNNAV_HIP(hipMemcpy(c->lru_part.p, order.data(), bytes, hipMemcpyHostToDevice));
+                GNNAV_HIP(hipMemset(c->lru_stamp.p, 0, bytes));
+                GNNAV_HIP(hipMemset(c->lru_ctl.p, 0, 2 * sizeof(uint32_t)));
+                c->lru_scan.ensure(c->ring_n, s0);
+            }
             GNNAV_HIP(hipDeviceSynchronize());
             if (!c->upd_done) GNNAV_HIP(hipEventCreateWithFlags(&c->upd_done, hipEventDisableTiming));
             c->upd_recorded = false;
@@ -1036,8 +1062,15 @@ static void gather_impl(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_
     if (copy_after) GNNAV_HIP(hipStreamWaitEvent(s, copy_after, 0));
     if (n_ids > 0) launch_gather_rows(a, s);
     if (dynamic) {
-        launch_fifo_update(a, cc->ring_lo, cc->ring_n, cc->owner.as<int32_t>(), cc->slot_map.as<int32_t>(),
-                           cc->ring_ptr.as<int32_t>(), cc->cache_rows.p, s);
+        if (cc->policy == GNNAV_POLICY_LRU)
+            launch_lru_update(a,
+                              LruState{cc->ring_lo, cc->ring_n, cc->lru_order.as<int32_t>(),
+                                       cc->lru_part.as<int32_t>(), cc->lru_stamp.as<uint32_t>(),
+                                       cc->lru_ctl.as<uint32_t>(), &cc->lru_scan},
+                              cc->owner.as<int32_t>(), cc->slot_map.as<int32_t>(), cc->cache_rows.p, s);
+        else
+            launch_fifo_update(a, cc->ring_lo, cc->ring_n, cc->owner.as<int32_t>(), cc->slot_map.as<int32_t>(),
+                               cc->ring_ptr.as<int32_t>(), cc->cache_rows.p, s);
         GNNAV_HIP(hipEventRecord(cc->upd_done, s));
         cc->upd_recorded = true;
     }

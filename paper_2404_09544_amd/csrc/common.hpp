@@ -275,8 +275,21 @@ void launch_aggregate_t(const CscWorkspace &csc, const int32_t *indptr, int64_t 
 void launch_wgrad(const float *x_self, int64_t ld_self, const float *agg, int64_t ld_agg, int64_t m,
                   const int32_t *m_dev, int64_t d_in, const float *dz, int64_t ld_dz, int64_t d_out, DevBuf &part,
                   float *dw, float *w, float lr, hipStream_t s, const char *label);
+
+// cache_update.hip: the cache's update policies over the ring of dynamic
+// slots [lo, lo + rn), run after a gather on its lists and output.
 void launch_fifo_update(const GatherArgs &a, int64_t lo, int64_t rn, int32_t *owner, int32_t *slot_map,
                         int32_t *ring_ptr, void *cache, hipStream_t s);
+struct LruState {
+    int64_t lo, rn;
+    int32_t *order;     // [rn] ring slots, least recently used first
+    int32_t *part;      // [rn] the list reordered by the last batch's hits
+    uint32_t *stamp;    // [rn] epoch of the last batch that hit slot lo + i
+    uint32_t *ctl;      // [0] epoch of the last batch, [1] untouched count
+    ScanState *scan;    // ensure()d for rn
+};
+void launch_lru_update(const GatherArgs &a, const LruState &st, int32_t *owner, int32_t *slot_map, void *cache,
+                       hipStream_t s);
 
 // spmm.hip
 void launch_aggregate_mean(const int32_t *indptr, const int32_t *indices, int64_t n_dst,

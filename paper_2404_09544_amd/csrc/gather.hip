@@ -191,126 +191,4 @@ void launch_gather_rows(const GatherArgs &a, hipStream_t s) {
     GNNAV_HIP(hipGetLastError());
 }
 
-// ------------------------------------------------------------ cache update
-// FIFO policy over ring slots [lo, lo + rn): the batch's misses, in request
-// order, are admitted one by one, each taking the slot under the ring
-// pointer; the slot's previous vertex is unmapped if the slot map still
-// points at that slot (a vertex requested twice in one batch is admitted
-// twice and keeps its later slot; its earlier one holds a stale copy until
-// the ring comes round).  Done in parallel with the same final state: with m
-// misses the slots p0 .. p0 + min(m, rn) - 1 (mod rn) are evicted (unmapped
-// where still mapped), miss i >= first = max(0, m - rn) takes slot
-// p0 + i (mod rn), and among repeats of a vertex the last admitted one is
-// mapped: the admit pass takes the minimum of -3 - (i - first) per vertex in
-// the slot map (codes below every slot and below -1), the map pass lets the
-// one admission whose code won write its slot.  The new rows are copied from
-// the gather's output, so nothing is read twice over the host link.  Entries
-// whose output row lies outside the request count are skipped (see
-// k_gather_rows).
-__global__ void __launch_bounds__(256) k_fifo_evict(const int32_t *__restrict__ m_ptr,
-                                                    const int32_t *__restrict__ ring_ptr, int64_t lo, int64_t rn,
-                                                    const int32_t *__restrict__ owner,
-                                                    int32_t *__restrict__ slot_map) {
-    const int64_t m = *m_ptr, p0 = *ring_ptr;
-    const int64_t cnt = m < rn ? m : rn;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < cnt; j += stride) {
-        const int64_t slot = lo + (p0 + j) % rn;
-        const int32_t v = owner[slot];
-        if (v >= 0 && slot_map[v] == (int32_t)slot) slot_map[v] = -1;
-    }
-}
-
-__device__ __forceinline__ int32_t fifo_code(int64_t i, int64_t first) { return (int32_t)(-3 - (i - first)); }
-
-template <int G>
-__global__ void __launch_bounds__(256) k_fifo_admit(const int2 *__restrict__ miss_list,
-                                                    const int32_t *__restrict__ m_ptr,
-                                                    const int32_t *__restrict__ n_ptr, int64_t n_req,
-                                                    const int32_t *__restrict__ ring_ptr, int64_t lo, int64_t rn,
-                                                    int32_t *__restrict__ owner, int32_t *__restrict__ slot_map,
-                                                    const uint4 *__restrict__ out, int64_t out_ld16,
-                                                    uint4 *__restrict__ cache, int64_t cache_ld16, int32_t chunks) {
-    constexpr int RPW = kWave / G;
-    const int lane = lane_id();
-    const int sub = lane / G, c0 = lane % G;
-    const int64_t m = *m_ptr, p0 = *ring_ptr;
-    if (n_ptr) n_req = *n_ptr;
-    const int64_t first = m > rn ? m - rn : 0;
-    const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / kWave;
-    for (int64_t i = first + (((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave) * RPW + sub; i < m;
-         i += nwaves * RPW) {
-        const int2 e = miss_list[i];
-        if ((uint32_t)e.x >= (uint64_t)n_req) continue;
-        const int64_t slot = lo + (p0 + i) % rn;
-        if (c0 == 0) {
-            owner[slot] = e.y;
-            atomicMin(&slot_map[e.y], fifo_code(i, first));
-        }
-        const uint4 *src = out + (int64_t)e.x * out_ld16;
-        uint4 *dst = cache + slot * cache_ld16;
-        for (int c = c0; c < chunks; c += G) dst[c] = src[c];
-    }
-}
-
-__global__ void __launch_bounds__(256) k_fifo_map(const int2 *__restrict__ miss_list,
-                                                  const int32_t *__restrict__ m_ptr,
-                                                  const int32_t *__restrict__ n_ptr, int64_t n_req,
-                                                  const int32_t *__restrict__ ring_ptr, int64_t lo, int64_t rn,
-                                                  int32_t *__restrict__ slot_map) {
-    const int64_t m = *m_ptr, p0 = *ring_ptr;
-    if (n_ptr) n_req = *n_ptr;
-    const int64_t first = m > rn ? m - rn : 0;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = first + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < m; i += stride) {
-        const int2 e = miss_list[i];
-        if ((uint32_t)e.x >= (uint64_t)n_req) continue;
-        if (slot_map[e.y] == fifo_code(i, first)) slot_map[e.y] = (int32_t)(lo + (p0 + i) % rn);
-    }
-}
-
-__global__ void k_fifo_advance(const int32_t *__restrict__ m_ptr, int32_t *__restrict__ ring_ptr, int64_t rn) {
-    if (threadIdx.x == 0 && blockIdx.x == 0) *ring_ptr = (int32_t)(((int64_t)*ring_ptr + *m_ptr) % rn);
-}
-
-void launch_fifo_update(const GatherArgs &a, int64_t lo, int64_t rn, int32_t *owner, int32_t *slot_map,
-                        int32_t *ring_ptr, void *cache, hipStream_t s) {
-    if (rn <= 0 || a.n_ids <= 0) return;
-    const int32_t *m_ptr = a.dev_counts + 1;
-    const int32_t chunks = (int32_t)((a.row_bytes + 15) / 16);
-    int g = 1;
-    while (g < chunks && g < kWave) g <<= 1;
-    {
-        KernelTimer t("cache_evict", s);
-        hipLaunchKernelGGL(k_fifo_evict, dim3(grid_for(std::min<int64_t>(a.n_ids, rn), 256, 4096)), dim3(256), 0,
-                           s, m_ptr, ring_ptr, lo, rn, owner, slot_map);
-    }
-    {
-        KernelTimer t("cache_admit", s);
-        const unsigned grid = grid_for(std::min<int64_t>(a.n_ids, rn), (256 / kWave) * (kWave / g), 4096);
-        switch (g) {
-#define GNNAV_G(GV)                                                                                     \
-    case GV:                                                                                            \
-        hipLaunchKernelGGL(k_fifo_admit<GV>, dim3(grid), dim3(256), 0, s, a.miss_list, m_ptr, a.n_ptr, a.n_ids, \
-                           ring_ptr, lo, rn, owner, slot_map, (const uint4 *)a.out, a.out_ld_bytes / 16,  \
-                           (uint4 *)cache, a.src_ld_bytes / 16, chunks);                                  \
-        break;
-            GNNAV_G(1) GNNAV_G(2) GNNAV_G(4) GNNAV_G(8) GNNAV_G(16) GNNAV_G(32) GNNAV_G(64)
-#undef GNNAV_G
-            default:
-                fail(GNNAV_E_INVALID, "bad row width");
-        }
-    }
-    {
-        KernelTimer t("cache_map", s);
-        hipLaunchKernelGGL(k_fifo_map, dim3(grid_for(std::min<int64_t>(a.n_ids, rn), 256, 4096)), dim3(256), 0, s,
-                           a.miss_list, m_ptr, a.n_ptr, a.n_ids, ring_ptr, lo, rn, slot_map);
-    }
-    {
-        KernelTimer t("cache_advance", s);
-        hipLaunchKernelGGL(k_fifo_advance, dim3(1), dim3(64), 0, s, m_ptr, ring_ptr, rn);
-    }
-    GNNAV_HIP(hipGetLastError());
-}
-
 }  // namespace gnnav

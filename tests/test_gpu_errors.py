@@ -199,20 +199,21 @@ def test_allocation_failure_leaves_handles_unwritten(hooks):
 
 
 @pytest.mark.parametrize("d,dtype,r,ring", [(32, "f32", 0.3, None), (64, "f32", 0.2, 50), (128, "bf16", 0.25, 7)])
-def test_fifo_repeated_ids_match_oracle(G, d, dtype, r, ring):
-    """Request lists with repeated ids through a FIFO cache: counts, rows,
-    slot map, owners and cached rows after every gather equal the oracle's
-    one-at-a-time admission."""
+@pytest.mark.parametrize("policy", ["fifo", "lru"])
+def test_dynamic_repeated_ids_match_oracle(G, policy, d, dtype, r, ring):
+    """Request lists with repeated ids through a FIFO or LRU cache: counts,
+    rows, slot map, owners and cached rows after every gather equal the
+    oracle's one-at-a-time admission."""
     import torch
-    from test_gpu_cache_update import check_cache
+    from test_gpu_cache_update import POLICY, check_cache
     n, u, v = graph_case("random-4000-30000-9")
     csr = O.build_csr(n, u, v)
     g = G.Graph(n, u, v)
     feats = W.features(n, d, dtype, seed=d)
     c = G.Cache(g, feats, dtype, r)
     ring = c.n_cached if ring is None else ring
-    c.set_policy("fifo", ring)
-    ref = O.FifoCache(csr, r, ring)
+    c.set_policy(policy, ring)
+    ref = POLICY[policy](csr, r, ring)
     rng = np.random.default_rng(d + 1)
     counts = torch.zeros(3, dtype=torch.int64, device="cuda")
     for b in range(6):
@@ -220,7 +221,7 @@ def test_fifo_repeated_ids_match_oracle(G, d, dtype, r, ring):
         ids = rng.integers(0, n, m).astype(np.int32)
         k = max(1, m // 4)
         ids[rng.integers(0, m, k)] = ids[rng.integers(0, m, k)]       # repeats
-        say("fifo-repeats", d, dtype, r, ring, b, m)
+        say(policy, "repeats", d, dtype, r, ring, b, m)
         out = torch.zeros((m, c.ld), dtype=torch.int16 if dtype == "bf16" else torch.float32, device="cuda")
         ids_d = dev(ids)
         G.gather(c, ids_d.data_ptr(), m, out, counts)

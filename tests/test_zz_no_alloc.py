@@ -3,7 +3,7 @@ memory, with its workspace in a static device array.  Checked against
 gnnav_gather on the same requests -- rows bit-exact, counts equal -- on two
 calls in a row, the second with fewer ids (the array keeps the first call's
 contents), with the library's allocation hook armed so that any allocation
-on the path would fail the call; a FIFO cache is checked against a twin
+on the path would fail the call; a FIFO and an LRU cache are checked against a twin
 cache updated by gnnav_gather; sizes above the maximum are refused.
 """
 import numpy as np
@@ -65,16 +65,17 @@ def test_noalloc_matches_gather(G, d, dtype, r, on_device):
     c.close()
 
 
-def test_noalloc_fifo_matches_gather_on_a_twin_cache(G):
+@pytest.mark.parametrize("policy", ["fifo", "lru"])
+def test_noalloc_dynamic_matches_gather_on_a_twin_cache(G, policy):
     import torch
-    from test_gpu_cache_update import check_cache
+    from test_gpu_cache_update import POLICY, check_cache
     n, u, v = graph_case("random-6000-40000-12")
     g = G.Graph(n, u, v)
     feats = W.features(n, 48, "f32", seed=12)
     ca_, cb_ = (G.Cache(g, feats, "f32", 0.3) for _ in range(2))
     for c in (ca_, cb_):
-        c.set_policy("fifo", 400)
-    ref = O.FifoCache(O.build_csr(n, u, v), 0.3, 400)
+        c.set_policy(policy, 400)
+    ref = POLICY[policy](O.build_csr(n, u, v), 0.3, 400)
     rng = np.random.default_rng(4)
     for m in (3000, 700):
         ids = rng.integers(0, n, m).astype(np.int32)
