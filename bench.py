@@ -860,7 +860,7 @@ def main():
         return sum(prof[n][1] for n in names if n in prof) / args.steps
     samp = ["dedup_first", "dedup_scan", "count_scan", "sample_hop", "relabel"]
     comp = [n for n in prof if n.startswith(("aggregate_mean", "combine_gemm"))] + ["classify", "weights_transpose"]
-    repl = ["cache_evict", "cache_admit", "cache_map", "cache_advance"]
+    repl = [n for n in prof if n.startswith("cache_")]   # every kernel of the update policy
     eq4 = {"t_sample_ms": round(per_batch(samp), 4), "t_transfer_ms": round(per_batch(["gather_rows"]), 4),
            "t_replace_ms": round(per_batch(repl), 4),
            "t_compute_ms": round(per_batch(comp), 4), "sequential_ms_per_step": round(fwd["seq_ms"], 4),

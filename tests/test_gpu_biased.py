@@ -1,7 +1,7 @@
 """GPU parity of the locality-biased sampler (cached neighbours weigh eta).
 
 Frontiers, blocks and local ids must equal the oracle's bit for bit, for
-static and self-updating (FIFO) caches, alone and inside the full step.
+static and self-updating (FIFO, LRU) caches, alone and inside the full step.
 """
 import numpy as np
 import pytest
@@ -93,8 +93,10 @@ def test_biased_step_matches_oracle(G):
 
 
 @pytest.mark.parametrize("depth", [1, 2])
-def test_biased_sampling_with_fifo_cache(G, depth):
+@pytest.mark.parametrize("policy", ["fifo", "lru"])
+def test_biased_sampling_with_dynamic_cache(G, policy, depth):
     """Each batch is sampled against the cache as the previous batch left it."""
+    from test_gpu_cache_update import POLICY
     from paper_2404_09544_amd.step import Pipeline, to_device_weights
     wl = W.Workload("chunglu-10k-d64")
     s, d = wl.edges()
@@ -104,19 +106,19 @@ def test_biased_sampling_with_fifo_cache(G, depth):
     g = G.Graph(wl.n, s, d)
     c = G.Cache(g, feats, "f32", r)
     ring = c.n_cached // 2
-    c.set_policy("fifo", ring)
+    c.set_policy(policy, ring)
     pipe = Pipeline(g, c, to_device_weights(ws, "f32"), wl.dims, wl.fanouts, "f32", depth=depth, eta=eta)
     csr = O.build_csr(wl.n, s, d)
-    fifo = O.FifoCache(csr, r, ring)
+    dyn = POLICY[policy](csr, r, ring)
     want = []
     for b in range(5):
-        ref_b = O.sample_blocks(csr, wl.seeds(b), wl.fanouts, wl.rng_seed(b), bias_slot_map=fifo.slot_map.copy(),
+        ref_b = O.sample_blocks(csr, wl.seeds(b), wl.fanouts, wl.rng_seed(b), bias_slot_map=dyn.slot_map.copy(),
                                 eta=eta)
-        _, counts = fifo.gather(feats, ref_b.nodes)
+        _, counts = dyn.gather(feats, ref_b.nodes)
         want.append((ref_b, counts))
     seeds_dev = [dev(wl.seeds(b)) for b in range(5)]
     for b in range(5):
-        say("biased fifo", depth, b)
+        say("biased", policy, depth, b)
         slot = pipe.enqueue(seeds_dev[b], wl.rng_seed(b))
         if depth == 1 or b % depth == depth - 1 or b == 4:
             pipe.synchronize()
@@ -125,7 +127,7 @@ def test_biased_sampling_with_fifo_cache(G, depth):
             compare_blocks(G, slot.blocks, want[b][0])
             assert np.array_equal(host(slot.counts), want[b][1])
     pipe.synchronize()
-    assert np.array_equal(c.slot_map(), fifo.slot_map)
+    assert np.array_equal(c.slot_map(), dyn.slot_map)
 
 
 def test_biased_partition_follows_policy_changes(G):

@@ -10,7 +10,9 @@ configuration bench.py times: the first three batches through the Pipeline
 tiles planned from the Eq. 12 bounds) in each stream and compute-unit
 setting the bench may pick, each batch checked in full against the oracle
 -- every logits row of F_0 where the oracle's forward takes seconds, sampled
-rows on the two largest graphs.
+rows on the two largest graphs.  With a self-updating cache (FIFO, LRU) on
+the 233k workload: counts, rows and the cache's state after four pipelined
+batches.
 """
 import sys
 import time
@@ -281,4 +283,46 @@ def test_full_biased_batch(G, name):
     ref = O.sage_forward_rows(ref_b, O.to_f64(h0, wl.dtype), [O.to_f64(w, wl.dtype) for w in ws], rows)
     assert_rows_close(logits[rows], ref, FP32_TOL, f"{name} biased logits")
     say(name, f"biased eta={eta}: hits/misses {counts.tolist()}")
+    c.close()
+
+
+@pytest.mark.parametrize("policy", ["fifo", "lru"])
+def test_full_dynamic_cache(G, policy):
+    """The 233k workload with a self-updating cache (ring over half the
+    cached rows), four batches through two pipelined streams on halves of
+    the compute units: each batch's hit/miss counts and gathered rows, then
+    the slot map, every slot's vertex and sampled cached rows, against the
+    oracle's policy applied batch after batch."""
+    import torch
+    from paper_2404_09544_amd.step import Pipeline, to_device_weights
+    name = "chunglu-233k-d602"
+    wl, _, _, csr, g = load(G, name)
+    feats = wl.features()
+    r = wl.cfg["cache"]
+    t = time.perf_counter()
+    c = G.Cache(g, feats, wl.dtype, r, store_on_device=wl.cfg["store_on_device"])
+    ring = c.n_cached // 2
+    c.set_policy(policy, ring)
+    ref = {"fifo": O.FifoCache, "lru": O.LruCache}[policy](csr, r, ring)
+    pipe = Pipeline(g, c, to_device_weights(wl.weights(), wl.dtype), wl.dims, wl.fanouts, wl.dtype, depth=2,
+                    link_workgroups=64, cu_partition=True)
+    seeds_dev = [torch.from_numpy(wl.seeds(b)).cuda() for b in range(4)]
+    for b0 in (0, 2):
+        slots = [pipe.enqueue(seeds_dev[b], wl.rng_seed(b)) for b in (b0, b0 + 1)]
+        pipe.synchronize()
+        for b, st in zip((b0, b0 + 1), slots):
+            st.finish()
+            ref_b = O.sample_blocks(csr, wl.seeds(b), wl.fanouts, wl.rng_seed(b))
+            h0, counts = ref.gather(feats, ref_b.nodes)
+            assert np.array_equal(st.counts.cpu().numpy(), counts), f"batch {b} counts"
+            got = st.h0_view().cpu().numpy()[:, :wl.d]
+            assert np.array_equal(got.view(np.uint8), h0.view(np.uint8)), f"batch {b} gathered rows"
+            say(name, policy, f"batch {b}: hits/misses {counts[:2].tolist()} ({time.perf_counter() - t:.1f}s)")
+    pipe.synchronize()
+    assert np.array_equal(c.slot_map(), ref.slot_map)
+    owners, rows = c.contents()
+    assert np.array_equal(owners, ref.owner)
+    pick = np.random.default_rng(7).choice(c.n_cached, 4096, replace=False)
+    pick = np.concatenate([pick, np.arange(c.n_cached - ring, c.n_cached - ring + 512)])
+    assert np.array_equal(rows[pick, :wl.d].view(np.uint8), feats[owners[pick]].view(np.uint8))
     c.close()
