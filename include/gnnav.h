@@ -201,7 +201,9 @@ gnnav_status gnnav_cache_set_link_workgroups(gnnav_cache *c, int32_t workgroups)
  * order; then the misses are admitted in request order as above, each
  * taking the least recently used slot, which becomes the most recent.
  * With no hit on the ring this is FIFO.  The ring holds per slot 12 bytes
- * of device state besides the row.
+ * of device state besides the row.  If the device-wide scan that reorders
+ * the list gives up (E_DEVICE at the next synchronisation point), that
+ * gather's update is skipped and the cache stays as it was.
  * Rows are copied from the gather's own output.  With a dynamic cache,
  * gathers on different streams run one after another in call order.  The
  * call synchronises the device and restarts the ring pointer at the ring's

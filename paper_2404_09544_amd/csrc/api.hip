@@ -696,13 +696,13 @@ extern "C" gnnav_status gnnav_cache_set_policy(gnnav_cache *c, int32_t policy, i
                 c->lru_order.ensure(bytes, s0);
                 c->lru_part.ensure(bytes, s0);
                 c->lru_stamp.ensure(bytes, s0);
-                c->lru_ctl.ensure(2 * sizeof(uint32_t), s0);
+                c->lru_ctl.ensure(4 * sizeof(uint32_t), s0);
                 std::vector<int32_t> order((size_t)c->ring_n);
                 for (int64_t j = 0; j < c->ring_n; ++j) order[(size_t)j] = (int32_t)(c->ring_lo + j);
                 GNNAV_HIP(hipMemcpy(c->lru_order.p, order.data(), bytes, hipMemcpyHostToDevice));
                 GNNAV_HIP(hipMemcpy(c->lru_part.p, order.data(), bytes, hipMemcpyHostToDevice));
                 GNNAV_HIP(hipMemset(c->lru_stamp.p, 0, bytes));
-                GNNAV_HIP(hipMemset(c->lru_ctl.p, 0, 2 * sizeof(uint32_t)));
+                GNNAV_HIP(hipMemset(c->lru_ctl.p, 0, 4 * sizeof(uint32_t)));
                 c->lru_scan.ensure(c->ring_n, s0);
             }
             GNNAV_HIP(hipDeviceSynchronize());

@@ -36,7 +36,12 @@
 // that makes `part` the next batch's list (the admitted slots, in
 // admission order, now last).  Epochs are 32-bit and stamps start at 0: a
 // slot untouched for 2^32 - 1 batches would read as touched once, which
-// only reorders it.
+// only reorders it.  A partition scan whose look-back wait gave up may leave
+// `part` with repeats, and two admissions in one slot would corrupt the
+// cache; so the device error word (which only grows) is read before and
+// after the scan, one thread records whether it moved, and if it did the
+// update is skipped as a whole: the cache stays as it was, and the next
+// synchronisation point reports the failure.
 #include <algorithm>
 
 #include "common.hpp"
@@ -50,18 +55,21 @@ namespace {
 struct FifoPick {
     const int32_t *ring_ptr;
     int64_t lo, rn;
+    __device__ bool ok() const { return true; }
     __device__ int64_t base() const { return *ring_ptr; }
     __device__ int64_t slot(int64_t i, int64_t b) const { return lo + (b + i) % rn; }
 };
 
 // S(i) for LRU: the reordered list is part[0 .. b) (untouched, in order)
 // followed by part[rn-1], part[rn-2], ..., part[b] (touched, in order);
-// b = untouched count, written by the partition scan.
+// b = untouched count, written by the partition scan; ok() is false when
+// that scan gave up (the update is then skipped).
 struct LruPick {
     const int32_t *part;
-    const int32_t *n_untouched;
+    const uint32_t *ctl;   // [1] untouched count, [3] 1 if the partition is sound
     int64_t rn;
-    __device__ int64_t base() const { return *n_untouched; }
+    __device__ bool ok() const { return ctl[3] != 0u; }
+    __device__ int64_t base() const { return (int64_t)ctl[1]; }
     __device__ int64_t slot(int64_t i, int64_t b) const {
         const int64_t j = i % rn;
         return j < b ? part[j] : part[rn - 1 - (j - b)];
@@ -74,6 +82,7 @@ template <class Pick>
 __global__ void __launch_bounds__(256) k_ring_evict(const int32_t *__restrict__ m_ptr, Pick pick, int64_t rn,
                                                     const int32_t *__restrict__ owner,
                                                     int32_t *__restrict__ slot_map) {
+    if (!pick.ok()) return;
     const int64_t m = *m_ptr, b = pick.base();
     const int64_t first = m > rn ? m - rn : 0;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -93,6 +102,7 @@ __global__ void __launch_bounds__(256) k_ring_admit(const int2 *__restrict__ mis
                                                     int64_t out_ld16, uint4 *__restrict__ cache, int64_t cache_ld16,
                                                     int32_t chunks) {
     constexpr int RPW = kWave / G;
+    if (!pick.ok()) return;
     const int lane = lane_id();
     const int sub = lane / G, c0 = lane % G;
     const int64_t m = *m_ptr, b = pick.base();
@@ -119,6 +129,7 @@ __global__ void __launch_bounds__(256) k_ring_map(const int2 *__restrict__ miss_
                                                   const int32_t *__restrict__ m_ptr,
                                                   const int32_t *__restrict__ n_ptr, int64_t n_req, Pick pick,
                                                   int64_t rn, int32_t *__restrict__ slot_map) {
+    if (!pick.ok()) return;
     const int64_t m = *m_ptr, b = pick.base();
     if (n_ptr) n_req = *n_ptr;
     const int64_t first = m > rn ? m - rn : 0;
@@ -169,15 +180,21 @@ __global__ void k_fifo_advance(const int32_t *__restrict__ m_ptr, int32_t *__res
     if (threadIdx.x == 0 && blockIdx.x == 0) *ring_ptr = (int32_t)(((int64_t)*ring_ptr + *m_ptr) % rn);
 }
 
-// LRU: stamp the ring slots this batch hit with the next epoch (ctl[0] + 1).
+__device__ __forceinline__ uint32_t error_count(const uint32_t *err) {
+    return __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// LRU: stamp the ring slots this batch hit with the next epoch (ctl[0] + 1);
+// record the device error count (ctl[2]) before the partition scan.
 __global__ void __launch_bounds__(256) k_lru_touch(const int2 *__restrict__ hit_list,
                                                    const int32_t *__restrict__ h_ptr,
                                                    const int32_t *__restrict__ n_ptr, int64_t n_req, int64_t lo,
                                                    int64_t rn, uint32_t *__restrict__ stamp,
-                                                   const uint32_t *__restrict__ ctl) {
+                                                   uint32_t *__restrict__ ctl, const uint32_t *__restrict__ err) {
     const int64_t h = *h_ptr;
     if (n_ptr) n_req = *n_ptr;
     const uint32_t next = ctl[0] + 1u;
+    if (blockIdx.x == 0 && threadIdx.x == 0) ctl[2] = error_count(err);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < h; i += stride) {
         const int2 e = hit_list[i];
@@ -214,14 +231,22 @@ struct LruPartitionOp {
     __device__ void total(int64_t t) const { ctl[1] = (uint32_t)(t & 0xffffffff); }
 };
 
+// LRU: ctl[3] = 1 if no look-back wait gave up since the touch kernel ran.
+__global__ void k_lru_check(uint32_t *__restrict__ ctl, const uint32_t *__restrict__ err) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) ctl[3] = error_count(err) == ctl[2] ? 1u : 0u;
+}
+
 // LRU: the next batch's list is the reordered one rotated by m (the slots
-// S(0 .. m-1) were used last, in admission order); then the epoch advances.
+// S(0 .. m-1) were used last, in admission order; kept as it was when the
+// update was skipped); then the epoch advances.
 __global__ void __launch_bounds__(256) k_lru_rotate(LruPick pick, const int32_t *__restrict__ m_ptr,
                                                     int32_t *__restrict__ order, uint32_t *__restrict__ ctl) {
-    const int64_t m = *m_ptr, b = pick.base();
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < pick.rn; p += stride)
-        order[p] = (int32_t)pick.slot(p + m, b);
+    if (pick.ok()) {
+        const int64_t m = *m_ptr, b = pick.base();
+        const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+        for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < pick.rn; p += stride)
+            order[p] = (int32_t)pick.slot(p + m, b);
+    }
     if (blockIdx.x == 0 && threadIdx.x == 0) ctl[0] += 1u;
 }
 
@@ -245,11 +270,16 @@ void launch_lru_update(const GatherArgs &a, const LruState &st, int32_t *owner, 
     {
         KernelTimer t("cache_touch", s);
         hipLaunchKernelGGL(k_lru_touch, dim3(grid_for(std::min<int64_t>(a.n_ids, rn), 256, 4096)), dim3(256), 0, s,
-                           a.hit_list, a.dev_counts, a.n_ptr, a.n_ids, st.lo, rn, st.stamp, st.ctl);
+                           a.hit_list, a.dev_counts, a.n_ptr, a.n_ids, st.lo, rn, st.stamp, st.ctl,
+                           device_error_word());
     }
     run_scan<LruPartitionOp, int64_t>(LruPartitionOp{st.order, st.stamp, st.ctl, st.part, st.lo, rn}, rn, *st.scan,
                                       "cache_order", s);
-    const LruPick pick{st.part, (const int32_t *)(st.ctl + 1), rn};
+    {
+        KernelTimer t("cache_check", s);
+        hipLaunchKernelGGL(k_lru_check, dim3(1), dim3(64), 0, s, st.ctl, (const uint32_t *)device_error_word());
+    }
+    const LruPick pick{st.part, st.ctl, rn};
     launch_admissions(a, pick, rn, owner, slot_map, cache, s);
     {
         KernelTimer t("cache_rotate", s);

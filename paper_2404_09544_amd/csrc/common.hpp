@@ -285,7 +285,8 @@ struct LruState {
     int32_t *order;     // [rn] ring slots, least recently used first
     int32_t *part;      // [rn] the list reordered by the last batch's hits
     uint32_t *stamp;    // [rn] epoch of the last batch that hit slot lo + i
-    uint32_t *ctl;      // [0] epoch of the last batch, [1] untouched count
+    uint32_t *ctl;      // [0] epoch of the last batch, [1] untouched count,
+                        // [2] error count before the partition, [3] partition sound
     ScanState *scan;    // ensure()d for rn
 };
 void launch_lru_update(const GatherArgs &a, const LruState &st, int32_t *owner, int32_t *slot_map, void *cache,

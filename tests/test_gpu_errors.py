@@ -3,8 +3,9 @@ ends normally: a device-wide scan whose look-back wait gives up (reported by
 the next synchronisation point), the Eq. 12 capacity bound (checked on the
 host before any work), allocation failure (a test hook makes the library's
 allocations fail), and that a failed call leaves its output handle and the
-previous results unchanged.  Also the FIFO cache with repeated ids in one
-request list, against the oracle's one-at-a-time admission.
+previous results unchanged; an LRU update whose partition scan gave up is
+skipped whole.  Also FIFO and LRU caches with repeated ids in one request
+list, against the oracle's one-at-a-time admission.
 """
 import ctypes as C
 
@@ -92,6 +93,59 @@ def test_sample_scan_timeout_reported_by_blocks_sync(hooks):
     assert sizes == ref.sizes and np.array_equal(nodes, ref.nodes)
     for h in range(2):
         assert np.array_equal(ip[h], ref.indptr[h]) and np.array_equal(ix[h], ref.indices[h])
+
+
+def test_lru_partition_timeout_skips_the_update(hooks):
+    """An LRU ring of 5,000 slots (three partition tiles) under spin limit 0,
+    gathering 1,500 ids (one classification tile, so the gather itself is
+    exact): the partition's waits give up, the update is skipped as a whole
+    -- slot map, slot owners and cached rows stay as they were -- and
+    gnnav_sync reports E_DEVICE.  With the limit restored the cache goes on
+    exactly as the oracle's LRU without that batch."""
+    import torch
+    from test_gpu_cache_update import check_cache
+    G = hooks
+    n, u, v = graph_case("random-20000-100000-5")
+    csr = O.build_csr(n, u, v)
+    g = G.Graph(n, u, v)
+    feats = W.features(n, 24, "f32", seed=6)
+    c = G.Cache(g, feats, "f32", 0.3)
+    ring = 5000
+    c.set_policy("lru", ring)
+    ref = O.LruCache(csr, 0.3, ring)
+    rng = np.random.default_rng(2)
+    hot = rng.permutation(n)[:3000].astype(np.int32)
+    out = torch.zeros((1500, c.ld), device="cuda")
+    counts = torch.zeros(3, dtype=torch.int64, device="cuda")
+
+    def gather(ids):
+        ids_d = dev(ids)
+        G.gather(c, ids_d.data_ptr(), ids.size, out, counts)
+        return ids_d
+
+    for b in range(2):
+        ids = rng.choice(hot, 1500, replace=False).astype(np.int32)
+        ids_d = gather(ids)
+        G.sync()
+        ref_rows, ref_counts = ref.gather(feats, ids)
+        assert np.array_equal(host(counts), ref_counts) and np.array_equal(host(out)[:, :24], ref_rows)
+        check_cache(c, ref, feats)
+    ids = rng.choice(hot, 1500, replace=False).astype(np.int32)
+    say("errors", "LRU gather with spin limit 0")
+    G.debug_set_spin_limit(0)
+    ids_d = gather(ids)
+    assert _status(G.sync) == E_DEVICE
+    G.debug_set_spin_limit(DEFAULT_SPIN_LIMIT)
+    ref_rows, ref_counts = O.gather(feats, ref.slot_map, ids)
+    assert np.array_equal(host(counts), ref_counts) and np.array_equal(host(out)[:, :24], ref_rows)
+    check_cache(c, ref, feats)          # unchanged: the update was skipped
+    for b in range(2):
+        ids = rng.choice(hot, 1500, replace=False).astype(np.int32)
+        ids_d = gather(ids)
+        G.sync()
+        ref.gather(feats, ids)
+        check_cache(c, ref, feats)
+    del ids_d
 
 
 def test_capacity_bound_checked_before_any_work(hooks):
