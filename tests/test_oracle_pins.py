@@ -635,6 +635,30 @@ def test_lru_cache_worked_batches():
     assert cache.slot_map[[A, C, X, Y, Z, D]].tolist() == [-1] * 6
 
 
+def test_lru_cache_repeated_miss_keeps_later_copy():
+    """A vertex missed twice in one batch takes two slots and stays mapped to
+    the later one; evicting the earlier (stale) copy must not unmap it.
+    Ring of 3 slots holding hubs 17, 18, 19 (least recent first):
+      [X, X]: X -> slot 0, X -> slot 1 (mapped); recency 2 0 1.
+      [Y]: Y -> slot 2 (19 out); recency 0 1 2.
+      [Z]: Z -> slot 0, whose stale X copy goes; X stays mapped to slot 1;
+        recency 1 2 0.
+      [X]: a hit on slot 1; recency 2 0 1."""
+    n = 20
+    csr = _hub_graph(n, [17, 18, 19])
+    X, Y, Z = 3, 4, 5
+    cache = O.LruCache(csr, 3.5 / n, 3)
+    feats = W.features(n, 2, "f32", seed=7)
+    steps = [([X, X], [0, 2, 0], [X, X, 19], 1), ([Y], [0, 1, 0], [X, X, Y], 1), ([Z], [0, 1, 0], [Z, X, Y], 1),
+             ([X], [1, 0, 0], [Z, X, Y], 1)]
+    for ids, counts, owners, x_slot in steps:
+        _, got = cache.gather(feats, np.array(ids, np.int32))
+        assert got.tolist() == counts
+        assert cache.owner.tolist() == owners
+        assert cache.slot_map[X] == x_slot
+    assert cache.recency().tolist() == [2, 0, 1]
+
+
 def _list_lru(rank, c, ring_n, batches, n):
     """Independent LRU model: a Python list of [slot, vertex] pairs, least
     recent first, and a dict of the mapped ring vertices."""
@@ -664,7 +688,7 @@ def _list_lru(rank, c, ring_n, batches, n):
 
 
 @pytest.mark.parametrize("r,frac,repeats", [(0.1, 1.0, False), (0.2, 0.5, False), (0.05, 0.25, True),
-                                            (0.3, 0.0, False), (0.1, 0.1, True)])
+                                            (0.3, 0.0, False), (0.1, 0.1, True), (0.3, 1.0, True)])
 def test_lru_cache_matches_list_model(r, frac, repeats):
     """Batches drawn with a hot set (so ring slots are hit again), some with
     repeated vertices and with out-of-range ids."""
