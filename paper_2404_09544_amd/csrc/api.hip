@@ -471,7 +471,8 @@ struct gnnav_cache {
     // FIFO's ring pointer, LRU's recency list, stamps and partition scan
     int32_t policy = 0;
     int64_t ring_lo = 0, ring_n = 0;
-    DevBuf owner, ring_ptr;
+    DevBuf owner, ring_ptr;   // FIFO: two pointer words, ring_parity the current one
+    int ring_parity = 0;
     DevBuf lru_order, lru_part, lru_stamp, lru_ctl;
     ScanState lru_scan;
     std::mutex upd_mu;
@@ -686,8 +687,9 @@ extern "C" gnnav_status gnnav_cache_set_policy(gnnav_cache *c, int32_t policy, i
                 c->owner.ensure(std::max<int64_t>(c->c, 1) * sizeof(int32_t), s0);
                 GNNAV_HIP(hipMemcpy(c->owner.p, c->rank_host.data(), c->c * sizeof(int32_t), hipMemcpyHostToDevice));
             }
-            c->ring_ptr.ensure(sizeof(int32_t), s0);
-            GNNAV_HIP(hipMemset(c->ring_ptr.p, 0, sizeof(int32_t)));
+            c->ring_ptr.ensure(2 * sizeof(int32_t), s0);
+            GNNAV_HIP(hipMemset(c->ring_ptr.p, 0, 2 * sizeof(int32_t)));
+            c->ring_parity = 0;
             if (policy == GNNAV_POLICY_LRU) {
                 // recency starts in slot order (lowest ring slot least
                 // recent); `part` starts as a copy, so it only ever holds ring
@@ -696,13 +698,13 @@ extern "C" gnnav_status gnnav_cache_set_policy(gnnav_cache *c, int32_t policy, i
                 c->lru_order.ensure(bytes, s0);
                 c->lru_part.ensure(bytes, s0);
                 c->lru_stamp.ensure(bytes, s0);
-                c->lru_ctl.ensure(4 * sizeof(uint32_t), s0);
+                c->lru_ctl.ensure(3 * sizeof(uint32_t), s0);
                 std::vector<int32_t> order((size_t)c->ring_n);
                 for (int64_t j = 0; j < c->ring_n; ++j) order[(size_t)j] = (int32_t)(c->ring_lo + j);
                 GNNAV_HIP(hipMemcpy(c->lru_order.p, order.data(), bytes, hipMemcpyHostToDevice));
                 GNNAV_HIP(hipMemcpy(c->lru_part.p, order.data(), bytes, hipMemcpyHostToDevice));
                 GNNAV_HIP(hipMemset(c->lru_stamp.p, 0, bytes));
-                GNNAV_HIP(hipMemset(c->lru_ctl.p, 0, 4 * sizeof(uint32_t)));
+                GNNAV_HIP(hipMemset(c->lru_ctl.p, 0, 3 * sizeof(uint32_t)));
                 c->lru_scan.ensure(c->ring_n, s0);
             }
             GNNAV_HIP(hipDeviceSynchronize());
@@ -1070,7 +1072,7 @@ static void gather_impl(const gnnav_cache *c, const int32_t *ids_dev, int64_t n_
                               cc->owner.as<int32_t>(), cc->slot_map.as<int32_t>(), cc->cache_rows.p, s);
         else
             launch_fifo_update(a, cc->ring_lo, cc->ring_n, cc->owner.as<int32_t>(), cc->slot_map.as<int32_t>(),
-                               cc->ring_ptr.as<int32_t>(), cc->cache_rows.p, s);
+                               cc->ring_ptr.as<int32_t>(), &cc->ring_parity, cc->cache_rows.p, s);
         GNNAV_HIP(hipEventRecord(cc->upd_done, s));
         cc->upd_recorded = true;
     }

@@ -278,15 +278,17 @@ void launch_wgrad(const float *x_self, int64_t ld_self, const float *agg, int64_
 
 // cache_update.hip: the cache's update policies over the ring of dynamic
 // slots [lo, lo + rn), run after a gather on its lists and output.
+// FIFO: ring_ptr holds two pointer words; *parity names the current one and
+// flips when an update is enqueued.
 void launch_fifo_update(const GatherArgs &a, int64_t lo, int64_t rn, int32_t *owner, int32_t *slot_map,
-                        int32_t *ring_ptr, void *cache, hipStream_t s);
+                        int32_t *ring_ptr, int *parity, void *cache, hipStream_t s);
 struct LruState {
     int64_t lo, rn;
     int32_t *order;     // [rn] ring slots, least recently used first
     int32_t *part;      // [rn] the list reordered by the last batch's hits
     uint32_t *stamp;    // [rn] epoch of the last batch that hit slot lo + i
     uint32_t *ctl;      // [0] epoch of the last batch, [1] untouched count,
-                        // [2] error count before the partition, [3] partition sound
+                        // [2] 1 while the partition is sound
     ScanState *scan;    // ensure()d for rn
 };
 void launch_lru_update(const GatherArgs &a, const LruState &st, int32_t *owner, int32_t *slot_map, void *cache,

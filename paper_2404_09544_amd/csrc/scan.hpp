@@ -9,7 +9,9 @@
 // or, to read each element's inputs once for both passes, a type Item with
 //   Item load(int64_t i) const, V value(const Item &) const and
 //   void emit(int64_t i, V prefix, V v, const Item &) const
-// (the items stay in registers between the two passes).
+// (the items stay in registers between the two passes), and optionally
+//   void gave_up() const                 called by a tile whose look-back
+//                                        wait gave up (see below).
 //
 // Single-pass scan with decoupled look-back: workgroups claim tiles in order
 // from an atomic ticket (so a tile only ever waits for tiles whose
@@ -43,6 +45,7 @@
 #pragma once
 
 #include <type_traits>
+#include <utility>
 
 #include "common.hpp"
 
@@ -56,6 +59,11 @@ template <class Op, class = void>
 struct ScanHasItem : std::false_type {};
 template <class Op>
 struct ScanHasItem<Op, std::void_t<typename Op::Item>> : std::true_type {};
+
+template <class Op, class = void>
+struct ScanHasGaveUp : std::false_type {};
+template <class Op>
+struct ScanHasGaveUp<Op, std::void_t<decltype(std::declval<const Op &>().gave_up())>> : std::true_type {};
 
 template <class Op, bool = ScanHasItem<Op>::value>
 struct ScanItems {   // no items: values are recomputed by index
@@ -226,7 +234,10 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_onepass(Op op, Side side,
                 uint32_t spins = 0;
                 while (true) {
                     if (spins >= spin_limit) {
-                        if (lane == 0) atomicAdd(errors, 1u);
+                        if (lane == 0) {
+                            atomicAdd(errors, 1u);
+                            if constexpr (ScanHasGaveUp<Op>::value) op.gave_up();
+                        }
                         break;
                     }
                     const int64_t t = base - lane;
