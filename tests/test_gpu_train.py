@@ -261,6 +261,49 @@ def test_train_steps_lower_the_loss(G):
     assert losses[-1] < losses[0]
 
 
+@pytest.mark.parametrize("policy", ["fifo", "lru"])
+def test_train_with_dynamic_cache(G, policy):
+    """Training batches through a self-updating cache (ring over half the
+    cached rows), on one stream and on two streams over halves of the
+    compute units: bit-identical weights and losses, and both caches end as
+    the oracle's policy leaves them after gathering the same frontiers."""
+    import torch
+    from paper_2404_09544_amd.step import MiniBatchStep, Pipeline, to_device_weights
+    from test_gpu_cache_update import POLICY, check_cache
+    wl = W.Workload("chunglu-10k-d64")
+    s, d = wl.edges()
+    csr = O.build_csr(wl.n, s, d)
+    g = G.Graph(wl.n, s, d)
+    feats = wl.features()
+    r = 0.3
+    caches = [G.Cache(g, feats, "f32", r) for _ in range(2)]
+    ring = caches[0].n_cached // 2
+    for c in caches:
+        c.set_policy(policy, ring)
+    ref = POLICY[policy](csr, r, ring)
+    ws = [W.glorot(wl.dims[l], wl.dims[l + 1], "f32", seed=3 + l) for l in range(wl.L)]
+    lab = dev(W.labels(wl.n, wl.dims[-1]))
+    seeds = [dev(wl.seeds(b)) for b in range(6)]
+    w_seq = to_device_weights(ws, "f32")
+    step = MiniBatchStep(g, caches[0], w_seq, wl.dims, wl.fanouts, "f32")
+    for b in range(6):
+        say("train", policy, "sequential", b)
+        step.train(seeds[b], wl.rng_seed(b), lab, 0.3, async_mode=True)
+        torch.cuda.synchronize()
+        ref.gather(feats, O.sample_blocks(csr, wl.seeds(b), wl.fanouts, wl.rng_seed(b)).nodes)
+    loss_seq = float(host(step.loss)[0])
+    w_pipe = to_device_weights(ws, "f32")
+    pipe = Pipeline(g, caches[1], w_pipe, wl.dims, wl.fanouts, "f32", depth=2, cu_partition=True)
+    say("train", policy, "pipeline")
+    slots = [pipe.enqueue_train(seeds[b], wl.rng_seed(b), lab, 0.3) for b in range(6)]
+    pipe.synchronize()
+    for a, b in zip(w_seq, w_pipe):
+        assert np.array_equal(host(a), host(b))
+    assert float(host(slots[-1].loss)[0]) == loss_seq
+    for c in caches:
+        check_cache(c, ref, feats)
+
+
 def test_train_pipeline_matches_sequential(G):
     """Training batches on two streams (each batch's forward waits for the
     previous update), also on two shares of the compute units, end with the
