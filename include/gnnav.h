@@ -210,7 +210,7 @@ gnnav_status gnnav_cache_set_link_workgroups(gnnav_cache *c, int32_t workgroups)
  * first slot (LRU: the recency order at the slot order, lowest slot least
  * recent); the cache contents are kept.
  * Errors: E_INVALID (unknown policy, dynamic_slots outside [0, n_cached]);
- * E_NOMEM (the ring's device state).                                      */
+ * E_NOMEM (the ring's device state; the cache is then left static).       */
 #define GNNAV_POLICY_STATIC 0
 #define GNNAV_POLICY_FIFO 1
 #define GNNAV_POLICY_LRU 2

@@ -472,6 +472,7 @@ struct gnnav_cache {
     int32_t policy = 0;
     int64_t ring_lo = 0, ring_n = 0;
     DevBuf owner, ring_ptr;   // FIFO: two pointer words, ring_parity the current one
+    bool owner_filled = false;   // owner holds the degree ranking (or later contents)
     int ring_parity = 0;
     DevBuf lru_order, lru_part, lru_stamp, lru_ctl;
     ScanState lru_scan;
@@ -647,7 +648,7 @@ extern "C" gnnav_status gnnav_cache_contents_host(const gnnav_cache *c, int32_t 
         GNNAV_CHECK(c, GNNAV_E_INVALID, "cache is NULL");
         GNNAV_HIP(hipDeviceSynchronize());
         if (owners) {
-            if (c->owner.p) {
+            if (c->owner_filled) {
                 if (c->c > 0)
                     GNNAV_HIP(hipMemcpy(owners, c->owner.p, c->c * sizeof(int32_t), hipMemcpyDeviceToHost));
             } else {
@@ -676,16 +677,21 @@ extern "C" gnnav_status gnnav_cache_set_policy(gnnav_cache *c, int32_t policy, i
                     "dynamic_slots outside [0, cached rows]");
         GNNAV_HIP(hipDeviceSynchronize());
         std::lock_guard<std::mutex> lk(c->upd_mu);
-        c->policy = policy;
-        c->ring_n = policy == GNNAV_POLICY_STATIC ? 0 : dynamic_slots;
-        c->ring_lo = c->c - c->ring_n;
+        const int64_t rn = policy == GNNAV_POLICY_STATIC ? 0 : dynamic_slots, lo = c->c - rn;
+        // The cache reads as static until the ring's state is in place, so a
+        // call that fails here (E_NOMEM) leaves it static, never pointing a
+        // gather at buffers that are missing or not yet filled.
+        c->policy = GNNAV_POLICY_STATIC;
+        c->ring_n = 0;
+        c->ring_lo = c->c;
         c->part_graph = nullptr;   // the slot map may have moved: rebuild the partition on next use
-        if (c->ring_n > 0) {
+        if (rn > 0) {
             hipStream_t s0 = nullptr;
-            if (!c->owner.p) {
+            if (!c->owner_filled) {
                 // first dynamic use: owner table from the degree ranking
                 c->owner.ensure(std::max<int64_t>(c->c, 1) * sizeof(int32_t), s0);
                 GNNAV_HIP(hipMemcpy(c->owner.p, c->rank_host.data(), c->c * sizeof(int32_t), hipMemcpyHostToDevice));
+                c->owner_filled = true;
             }
             c->ring_ptr.ensure(2 * sizeof(int32_t), s0);
             GNNAV_HIP(hipMemset(c->ring_ptr.p, 0, 2 * sizeof(int32_t)));
@@ -694,23 +700,26 @@ extern "C" gnnav_status gnnav_cache_set_policy(gnnav_cache *c, int32_t policy, i
                 // recency starts in slot order (lowest ring slot least
                 // recent); `part` starts as a copy, so it only ever holds ring
                 // slots, even where a partition scan that gave up left a gap
-                const size_t bytes = (size_t)c->ring_n * sizeof(int32_t);
+                const size_t bytes = (size_t)rn * sizeof(int32_t);
                 c->lru_order.ensure(bytes, s0);
                 c->lru_part.ensure(bytes, s0);
                 c->lru_stamp.ensure(bytes, s0);
                 c->lru_ctl.ensure(3 * sizeof(uint32_t), s0);
-                std::vector<int32_t> order((size_t)c->ring_n);
-                for (int64_t j = 0; j < c->ring_n; ++j) order[(size_t)j] = (int32_t)(c->ring_lo + j);
+                std::vector<int32_t> order((size_t)rn);
+                for (int64_t j = 0; j < rn; ++j) order[(size_t)j] = (int32_t)(lo + j);
                 GNNAV_HIP(hipMemcpy(c->lru_order.p, order.data(), bytes, hipMemcpyHostToDevice));
                 GNNAV_HIP(hipMemcpy(c->lru_part.p, order.data(), bytes, hipMemcpyHostToDevice));
                 GNNAV_HIP(hipMemset(c->lru_stamp.p, 0, bytes));
                 GNNAV_HIP(hipMemset(c->lru_ctl.p, 0, 3 * sizeof(uint32_t)));
-                c->lru_scan.ensure(c->ring_n, s0);
+                c->lru_scan.ensure(rn, s0);
             }
             GNNAV_HIP(hipDeviceSynchronize());
             if (!c->upd_done) GNNAV_HIP(hipEventCreateWithFlags(&c->upd_done, hipEventDisableTiming));
             c->upd_recorded = false;
         }
+        c->policy = policy;
+        c->ring_n = rn;
+        c->ring_lo = lo;
     });
 }
 

@@ -44,6 +44,7 @@
 // otherwise pay twice and that evicted the other workgroups' working sets.
 #pragma once
 
+#include <algorithm>
 #include <type_traits>
 #include <utility>
 
@@ -115,10 +116,13 @@ struct ScanState {
             launch_fill_i32(ctl.as<int32_t>(), 0, 4, s);
         }
         if (t > tiles) {
+            // a reallocation frees the old records first: until both are in
+            // place and cleared no tile count may claim them
+            tiles = 0;
             const size_t bytes = (size_t)t * kRecWords * sizeof(uint64_t);
             sums.ensure(bytes, s);
             prefix.ensure(bytes, s);
-            tiles = (int64_t)(sums.bytes / (kRecWords * sizeof(uint64_t)));
+            tiles = (int64_t)(std::min(sums.bytes, prefix.bytes) / (kRecWords * sizeof(uint64_t)));
             launch_fill_i32(sums.as<int32_t>(), 0, tiles * kRecWords * 2, s);
             launch_fill_i32(prefix.as<int32_t>(), 0, tiles * kRecWords * 2, s);
         }

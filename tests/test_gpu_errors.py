@@ -148,6 +148,55 @@ def test_lru_partition_timeout_skips_the_update(hooks):
     del ids_d
 
 
+@pytest.mark.parametrize("policy", ["fifo", "lru"])
+def test_set_policy_allocation_failure_leaves_cache_static(hooks, policy):
+    """Each device allocation of gnnav_cache_set_policy made to fail in
+    turn: the call returns E_NOMEM and the cache stays static (a gather
+    after it leaves the slot map as the degree ranking made it); the first
+    attempt that succeeds gives a cache that follows the oracle's policy."""
+    import torch
+    from test_gpu_cache_update import POLICY, check_cache
+    G = hooks
+    n, u, v = graph_case("random-8000-60000-6")
+    csr = O.build_csr(n, u, v)
+    g = G.Graph(n, u, v)
+    feats = W.features(n, 16, "f32", seed=8)
+    c = G.Cache(g, feats, "f32", 0.3)
+    ring = c.n_cached // 2
+    _, slot, _ = O.rank_cache(csr, 0.3)
+    rng = np.random.default_rng(5)
+    out = torch.zeros((3000, c.ld), device="cuda")
+    counts = torch.zeros(3, dtype=torch.int64, device="cuda")
+    code = {"fifo": 1, "lru": 2}[policy]
+    done = False
+    for k in range(12):
+        say("errors", policy, "set_policy allocation failure after", k)
+        G.debug_fail_allocations(k)
+        st = G._lib.gnnav_cache_set_policy(c._h, code, ring)
+        G.debug_fail_allocations(-1)
+        if st == 0:
+            done = True
+            break
+        assert st == E_NOMEM, (k, st)
+        ids = rng.integers(0, n, 3000).astype(np.int32)
+        ids_d = dev(ids)
+        G.gather(c, ids_d.data_ptr(), ids.size, out, counts)
+        G.sync()
+        ref_rows, ref_counts = O.gather(feats, slot, ids)
+        assert np.array_equal(host(counts), ref_counts)
+        assert np.array_equal(host(out)[:, :16], ref_rows)
+        assert np.array_equal(c.slot_map(), slot), "a failed set_policy must leave the cache static"
+    assert done and k >= 1
+    ref = POLICY[policy](csr, 0.3, ring)
+    for b in range(3):
+        ids = rng.integers(0, n, 3000).astype(np.int32)
+        ids_d = dev(ids)
+        G.gather(c, ids_d.data_ptr(), ids.size, out, counts)
+        G.sync()
+        ref.gather(feats, ids)
+        check_cache(c, ref, feats)
+
+
 def test_capacity_bound_checked_before_any_work(hooks):
     """A star with 50,000 leaves sampled with fanout -1 (every neighbour) from
     all of its vertices: the Eq. 12 bound 50,001 x 50,000 exceeds INT32_MAX,
