@@ -843,6 +843,7 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
         } else {
             // a static cache: rows partitioned by its slot map, built once per graph
             if (bc->part_graph != (const void *)g || bc->part_nnz != g->nnz) {
+                bc->part_graph = nullptr;   // a failed reallocation below has freed the old partition
                 bc->part_col.ensure(std::max<int64_t>(g->nnz, 1) * sizeof(int32_t), s);
                 bc->part_cnt.ensure(std::max<int64_t>(g->n, 1) * sizeof(int32_t), s);
                 launch_partition_rows(g->row_ptr.p, g->i64, g->col.as<int32_t>(), g->n, bc->slot_map.as<int32_t>(),
@@ -862,6 +863,7 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
     // node table: all-ones entries are older than every call's tag; after
     // 2^32 - 2 calls the tags would wrap, so the table is filled again
     if (b->map_nodes < g->n || b->map_epoch == 0xfffffffeu) {
+        b->map_nodes = 0;   // a failed reallocation below has freed the old table
         b->map.ensure(std::max<int64_t>(g->n, 1) * sizeof(uint64_t), s);
         launch_fill_i32(b->map.as<int32_t>(), -1, 2 * std::max<int64_t>(g->n, 1), s);
         b->map_nodes = g->n;

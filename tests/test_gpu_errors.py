@@ -197,6 +197,37 @@ def test_set_policy_allocation_failure_leaves_cache_static(hooks, policy):
         check_cache(c, ref, feats)
 
 
+def test_failed_node_table_growth_leaves_blocks_usable(hooks):
+    """Blocks reused across graphs: growing the node table for a larger
+    graph fails (E_NOMEM; the old table is gone), and a later sample of a
+    graph the old table would have fitted builds a new table and equals the
+    oracle's."""
+    G = hooks
+    graphs = {}
+    for n in (5000, 30000, 60000):
+        n_, u, v = graph_case(f"random-{n}-{4 * n}-7")
+        graphs[n] = (O.build_csr(n_, u, v), G.Graph(n_, u, v))
+    blk = G.Blocks()
+    fan = [5, 5]
+    for n in (5000, 30000):
+        seeds = np.random.default_rng(n).permutation(n)[:400].astype(np.int32)
+        G.sample(graphs[n][1], dev(seeds), fan, 3, blk)
+    seeds = np.random.default_rng(1).permutation(60000)[:400].astype(np.int32)
+    say("errors", "node table growth fails")
+    G.debug_fail_allocations(0)
+    assert _status(lambda: G.sample(graphs[60000][1], dev(seeds), fan, 3, blk)) == E_NOMEM
+    G.debug_fail_allocations(-1)
+    for n in (30000, 5000):
+        seeds = np.random.default_rng(n + 1).permutation(n)[:400].astype(np.int32)
+        G.sample(graphs[n][1], dev(seeds), fan, 4, blk)
+        nodes, sizes, ip, nb, ix = blk.to_host()
+        ref = O.sample_blocks(graphs[n][0], seeds, fan, 4)
+        assert sizes == ref.sizes and np.array_equal(nodes, ref.nodes)
+        for h in range(2):
+            assert np.array_equal(ix[h], ref.indices[h])
+    blk.close()
+
+
 def test_capacity_bound_checked_before_any_work(hooks):
     """A star with 50,000 leaves sampled with fanout -1 (every neighbour) from
     all of its vertices: the Eq. 12 bound 50,001 x 50,000 exceeds INT32_MAX,
