@@ -859,7 +859,11 @@ static void sample_enqueue(const gnnav_graph *g, const int32_t *seeds_dev, int64
     }
     int64_t max_list = n_seeds;
     for (int h = 1; h <= n_hops; ++h) max_list = std::max(max_list, std::max(eb[h], nb[h - 1] + 1));
-    // workspace
+    // workspace: growing it frees the previous sample's buffers, so until
+    // this sample is enqueued the blocks read as unsampled (a call that fails
+    // below, E_NOMEM, leaves nothing that points at freed memory)
+    b->L = 0;
+    b->host_sizes = false;
     // node table: all-ones entries are older than every call's tag; after
     // 2^32 - 2 calls the tags would wrap, so the table is filled again
     if (b->map_nodes < g->n || b->map_epoch == 0xfffffffeu) {

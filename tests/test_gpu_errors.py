@@ -199,9 +199,9 @@ def test_set_policy_allocation_failure_leaves_cache_static(hooks, policy):
 
 def test_failed_node_table_growth_leaves_blocks_usable(hooks):
     """Blocks reused across graphs: growing the node table for a larger
-    graph fails (E_NOMEM; the old table is gone), and a later sample of a
-    graph the old table would have fitted builds a new table and equals the
-    oracle's."""
+    graph fails (E_NOMEM; the old table is gone, and the blocks read as
+    unsampled), and a later sample of a graph the old table would have
+    fitted builds a new table and equals the oracle's."""
     G = hooks
     graphs = {}
     for n in (5000, 30000, 60000):
@@ -214,9 +214,13 @@ def test_failed_node_table_growth_leaves_blocks_usable(hooks):
         G.sample(graphs[n][1], dev(seeds), fan, 3, blk)
     seeds = np.random.default_rng(1).permutation(60000)[:400].astype(np.int32)
     say("errors", "node table growth fails")
+    assert blk.hop(1).n_dst > 0
     G.debug_fail_allocations(0)
     assert _status(lambda: G.sample(graphs[60000][1], dev(seeds), fan, 3, blk)) == E_NOMEM
     G.debug_fail_allocations(-1)
+    # the failed growth freed the previous sample's node table: the blocks
+    # read as unsampled rather than describing buffers that may be gone
+    assert _status(lambda: blk.hop(1)) == E_INVALID
     for n in (30000, 5000):
         seeds = np.random.default_rng(n + 1).permutation(n)[:400].astype(np.int32)
         G.sample(graphs[n][1], dev(seeds), fan, 4, blk)
@@ -310,6 +314,7 @@ def test_allocation_failure_leaves_handles_unwritten(hooks):
         G.sample(g, seeds_d, [5, 5], 9, blk)
     assert e.value.status == E_NOMEM
     G.debug_fail_allocations(-1)
+    assert _status(lambda: blk.hop(1)) == E_INVALID   # nothing sampled
     torch.cuda.synchronize()
     G.sample(g, seeds_d, [5, 5], 9, blk)
     nodes, sizes, _, _, ix = blk.to_host()
