@@ -242,8 +242,9 @@ void gnnav_blocks_free(gnnav_blocks *b);
  * E_CAPACITY (an Eq. 12 bound exceeds INT32_MAX; checked on the host
  * before anything is enqueued, so the blocks keep the previous sample),
  * E_RANGE (a seed outside [0, n); the blocks' contents are then unspecified
- * but reusable), E_NOMEM (the blocks' contents are then unspecified but
- * reusable), E_DEVICE (also: a device-side failure, see gnnav_sync).      */
+ * but reusable), E_NOMEM (the blocks then hold no sample: views and the
+ * forward refuse them with E_INVALID until a sample succeeds), E_DEVICE
+ * (also: a device-side failure, see gnnav_sync).                          */
 gnnav_status gnnav_sample(const gnnav_graph *g, const int32_t *seeds_dev, int64_t n_seeds,
                           const int32_t *fanouts, int32_t n_hops, uint64_t rng_seed,
                           gnnav_blocks *blocks, void *stream);
